@@ -1,0 +1,254 @@
+"""Plain, slow CPU reference ("oracle") for the Dion2 optimizer step.
+
+TEST INFRASTRUCTURE. Only the test-suite, the smoke check and the CPU-baseline
+leg of the benchmark may import this module. The product path (the HIP
+library and its Python binding) never calls it, and this module imports
+nothing from the product package.
+
+What it computes follows the paper "Dion2: A Simple Method to Shrink Matrix in
+Muon" (Ahn, Amsel, Langford):
+
+  Algorithm 1 (row-selection version; columns analogous), per weight matrix W
+  with momentum M and gradient G:
+      M <- M + G                                   (accumulate)
+      K <- Select_alpha(M)                         (alpha-fraction of lines)
+      O <- NewtonSchulz(M[K, :])                   (orthonormalise submatrix)
+      M[K, :] <- mu * M[K, :]                      (selective decay, eq. (2))
+      W[K, :] <- W[K, :] - lr*sqrt(fan_out/fan_in)*O   (sparse update, eq. (1))
+
+Precision: fp64 everywhere except where storage fixes the precision. The
+momentum is stored in fp32, so the accumulate and the decay are fp32 IEEE
+round-to-nearest-even operations (exactly what fp32 storage implies); W is
+rounded once, round-to-nearest-even, to its storage type (fp32 or bf16).
+
+Readings taken where the paper is silent (each one is listed with its reason
+in the design notes):
+  * Newton-Schulz: Muon's quintic p(x) = a x + b x^3 + c x^5 with
+    (a, b, c) = (3.4445, -4.7750, 2.0315) at every step, input divided by
+    (Frobenius norm + eps), eps = 1e-7, iterated on the orientation with the
+    smaller Gram matrix (Sec. 1 and Algorithm 1 name the iteration but give
+    neither coefficients, step count nor normalisation).
+  * Select_alpha, Default rule: the k = ceil(alpha * d) lines of largest l1
+    norm, ties to the lower index, NaN ranked as +inf, K returned ascending.
+    The l1 norm is the exact sum of |M_ij| over the line, rounded once to
+    fp64 (math.fsum), so it does not depend on a summation order.
+  * Axis AUTO selects along the shorter dimension (Sec. 4, experimental
+    details); a square matrix selects rows.
+  * sqrt(fan_out/fan_in) uses the full W's rows/cols (y = W x, so
+    fan_out = rows, fan_in = cols; Sec. 1, eq. (1)).
+"""
+from __future__ import annotations
+
+import math
+
+import numpy as np
+
+AXIS_AUTO = -1
+AXIS_ROWS = 0
+AXIS_COLS = 1
+
+# Muon's quintic Newton-Schulz coefficients (a, b, c); the paper cites Muon
+# for the iteration (Sec. 1) without printing them.
+MUON_QUINTIC = (3.4445, -4.7750, 2.0315)
+DEFAULT_EPS = 1e-7
+DEFAULT_MU = 0.95    # Algorithm 1, hyperparameter line
+DEFAULT_LR = 0.02    # Sec. 4, experimental details
+
+
+# ---------------------------------------------------------------- rounding
+
+def round_bf16(x):
+    """Round fp64 values to bfloat16, round-to-nearest-even, returned as fp64.
+
+    bfloat16 keeps 8 significant bits and fp32's exponent range. The value is
+    written as an integer multiple of its quantum 2^q (q = exponent - 8, and
+    never below the subnormal quantum 2^-133), the multiple is rounded with
+    np.rint (ties to even), and overflow beyond the largest finite bf16 goes
+    to +-inf. NaN propagates.
+    """
+    x = np.asarray(x, dtype=np.float64)
+    _, e = np.frexp(x)                        # x = m * 2^e, 0.5 <= |m| < 1
+    q = np.maximum(e - 8, -133)
+    r = np.ldexp(np.rint(np.ldexp(x, -q)), q)
+    max_bf16 = (2.0 - 2.0 ** -7) * 2.0 ** 127
+    r = np.where(np.abs(r) > max_bf16, np.copysign(np.inf, x), r)
+    return np.where(np.isnan(x), x, r)
+
+
+def round_to(x, dtype):
+    """Round fp64 values to the storage type 'f32' or 'bf16' (RNE), as fp64;
+    'f64' keeps them (used by identity checks that must not round)."""
+    if dtype == "f64":
+        return np.asarray(x, dtype=np.float64)
+    if dtype == "f32":
+        return np.asarray(x, dtype=np.float64).astype(np.float32).astype(np.float64)
+    if dtype == "bf16":
+        return round_bf16(x)
+    raise ValueError(f"unknown dtype {dtype!r}")
+
+
+# ---------------------------------------------------------------- the steps
+
+def resolve_axis(rows, cols, axis=AXIS_AUTO):
+    """Selection axis. AUTO picks the shorter dimension (Sec. 4, details);
+    a square matrix selects rows."""
+    if axis == AXIS_AUTO:
+        return AXIS_ROWS if rows <= cols else AXIS_COLS
+    if axis not in (AXIS_ROWS, AXIS_COLS):
+        raise ValueError(f"bad axis {axis}")
+    return axis
+
+
+def num_selected(alpha, d_sel):
+    """k = ceil(alpha * d_sel), clamped to [1, d_sel]: the fraction alpha of
+    lines that Algorithm 1 selects. alpha is taken as the fp32 value the
+    library receives."""
+    a = float(np.float32(alpha))
+    if not (0.0 < a <= 1.0):
+        raise ValueError(f"alpha must be in (0, 1], got {alpha}")
+    return int(min(d_sel, max(1, math.ceil(a * d_sel))))
+
+
+def momentum_accumulate(M, G):
+    """M <- M + G (Algorithm 1, first line), in fp32 arithmetic because the
+    momentum is stored in fp32. G holds values exactly representable in fp32
+    (fp32 or bf16 storage)."""
+    return np.asarray(M, dtype=np.float32) + np.asarray(G, dtype=np.float32)
+
+
+def l1_norms(M, axis):
+    """l1 norm of every line along the selection axis (Select_alpha, Default
+    rule of Algorithm 1 ranks lines by this norm). Each norm is the exact sum
+    of absolute values, rounded once to fp64."""
+    A = np.abs(np.asarray(M, dtype=np.float64))
+    lines = A if axis == AXIS_ROWS else A.T
+    return np.array([math.fsum(line.tolist()) for line in lines], dtype=np.float64)
+
+
+def sum_squares(M, axis):
+    """Squared l2 norm of every line along the selection axis, fp64."""
+    A = np.asarray(M, dtype=np.float64)
+    return np.sum(A * A, axis=1 if axis == AXIS_ROWS else 0)
+
+
+def select_top(norms, k):
+    """Select_alpha, Default rule: indices of the k largest norms, ties to the
+    lower index, NaN ranked as +inf; returned in ascending index order."""
+    key = np.where(np.isnan(norms), np.inf, norms)
+    order = np.lexsort((np.arange(key.size), -key))
+    return np.sort(order[:k]).astype(np.int64)
+
+
+def select_random(d_sel, k, rng):
+    """Select_alpha, Random rule: a uniformly random k-subset (Algorithm 1,
+    selection method 2), ascending. Not used by the default step."""
+    return np.sort(rng.choice(d_sel, size=k, replace=False)).astype(np.int64)
+
+
+def gather(M, K, axis):
+    """The submatrix M[K, :] (rows) or M[:, K] (columns), in fp64."""
+    M = np.asarray(M, dtype=np.float64)
+    return M[K, :].copy() if axis == AXIS_ROWS else M[:, K].copy()
+
+
+def newton_schulz(X, steps, coeffs=None, eps=DEFAULT_EPS):
+    """Newton-Schulz orthonormalisation (Sec. 1; Algorithm 1, third line).
+
+    X is divided by (||X||_F + eps); then each step t applies
+        A = X X^T,  B = b_t A + c_t A^2,  X <- a_t X + B X,
+    i.e. X <- p_t(X) for the odd polynomial p_t(x) = a x + b x^3 + c x^5
+    acting on the singular values. The iteration runs on the orientation with
+    the smaller Gram matrix (the result is the same spectral function either
+    way). coeffs is a list of (a, b, c) per step, or None for Muon's quintic.
+    """
+    X = np.asarray(X, dtype=np.float64)
+    if coeffs is None:
+        coeffs = [MUON_QUINTIC] * steps
+    if len(coeffs) < steps:
+        raise ValueError("need one (a, b, c) per Newton-Schulz step")
+    tall = X.shape[0] > X.shape[1]
+    if tall:
+        X = X.T
+    X = X / (np.linalg.norm(X) + eps)
+    for t in range(steps):
+        a, b, c = coeffs[t]
+        A = X @ X.T
+        B = b * A + c * (A @ A)
+        X = a * X + B @ X
+    return X.T.copy() if tall else X
+
+
+def selective_decay(M, K, mu, axis, store="fp32", decay_all=False):
+    """M[K, :] <- mu * M[K, :] (eq. (2); Algorithm 1, fourth line), in the
+    momentum's storage precision. decay_all=True is the ablation of Sec. 4.2
+    (M <- mu * M)."""
+    if store == "fp32":
+        M = np.array(M, dtype=np.float32)
+        m = np.float32(mu)
+    else:
+        M = np.array(M, dtype=np.float64)
+        m = np.float64(np.float32(mu))   # mu as the fp32 value the library receives
+    if decay_all:
+        M = m * M
+    elif axis == AXIS_ROWS:
+        M[K, :] = m * M[K, :]
+    else:
+        M[:, K] = m * M[:, K]
+    return M
+
+
+def update_scale(lr, rows, cols):
+    """lr * sqrt(fan_out / fan_in) for W in R^{fan_out x fan_in} (eq. (1)),
+    lr taken as the fp32 value the library receives."""
+    return float(np.float32(lr)) * math.sqrt(rows / cols)
+
+
+def apply_update(W, K, O, lr, axis, w_dtype):
+    """W[K, :] <- W[K, :] - lr*sqrt(fan_out/fan_in)*O (Algorithm 1, last line;
+    eq. (1)); columns analogously. Computed in fp64 and rounded once to W's
+    storage type; lines outside K are left untouched."""
+    W = np.array(W, dtype=np.float64)
+    rows, cols = W.shape
+    s = update_scale(lr, rows, cols)
+    if axis == AXIS_ROWS:
+        W[K, :] = round_to(W[K, :] - s * O, w_dtype)
+    else:
+        W[:, K] = round_to(W[:, K] - s * O, w_dtype)
+    return W
+
+
+def dion2_step(W, M, G, alpha, mu=DEFAULT_MU, lr=DEFAULT_LR, ns_steps=5,
+               axis=AXIS_AUTO, coeffs=None, eps=DEFAULT_EPS, w_dtype="f32",
+               store="fp32", decay_all=False, select="l1", rng=None):
+    """One Dion2 step on one matrix (Algorithm 1). Inputs are not modified.
+
+    W: (rows, cols) values of W's storage type w_dtype ('f32' | 'bf16').
+    M: (rows, cols) momentum (fp32 storage; store='fp64' keeps it in fp64).
+    G: (rows, cols) gradient values.
+    Returns a dict with the new W (fp64 array of w_dtype values), the new M,
+    the selected indices K (ascending), the Newton-Schulz output O in the
+    submatrix's own orientation (k x cols for rows, rows x k for columns),
+    the l1 norms, and the resolved axis.
+    """
+    W = np.asarray(W)
+    rows, cols = W.shape
+    ax = resolve_axis(rows, cols, axis)
+    d_sel = rows if ax == AXIS_ROWS else cols
+    k = num_selected(alpha, d_sel)
+    if store == "fp32":
+        M1 = momentum_accumulate(M, G)
+    else:
+        M1 = np.asarray(M, dtype=np.float64) + np.asarray(G, dtype=np.float64)
+    norms = l1_norms(M1, ax)
+    if select == "l1":
+        K = select_top(norms, k)
+    elif select == "random":
+        K = select_random(d_sel, k, rng)
+    else:
+        raise ValueError(select)
+    X = gather(M1, K, ax)
+    O = newton_schulz(X, ns_steps, coeffs, eps)
+    M2 = selective_decay(M1, K, mu, ax, store, decay_all)
+    W2 = apply_update(W, K, O, lr, ax, w_dtype)
+    return {"W": W2, "M": M2, "K": K, "O": O, "norms": norms, "axis": ax,
+            "k": k}
