@@ -1,0 +1,251 @@
+#!/usr/bin/env python3
+"""Dion2 optimizer-step benchmark on one MI355X.
+
+    python bench.py [--steps K] [--warmup W] [--workload 1b] [--alpha 0.25]
+
+A step is one Dion2 update (Algorithm 1) of every matrix of a synthetic layer
+stack, one batched library call per same-shape group, all on one stream,
+with W, M, G resident in HBM. The default is the paper's timing method
+(Sec. 4.4): 100 steps, the mean of the final 20 reported (warmup 80,
+steps 20). Prints one JSON line:
+  value        mean ms per step at --alpha (lower is better)
+  roofline     the dominant kernel phase against its roofline, measured with
+               HIP events on the library's stream in a second timed pass
+  cpu_baseline the CPU oracle timed on a bounded sample of the same stack
+  per_alpha_ms the other fractions of the workload, timed the same way
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import statistics
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+import torch  # noqa: E402
+
+from paper_2512_16928_amd import binding, workloads  # noqa: E402
+
+METRIC = "Dion2 optimizer-step ms per layer stack at α=0.25/0.5/1; NS MFMA util %"
+HBM_PEAK_GBS = 8000.0          # MI355X HBM3E
+MFMA_BF16_PEAK_TFS = 2500.0    # MI355X dense bf16 MFMA
+HBM_PHASES = ("momentum", "gather", "apply")
+NS_PHASES = ("ns_gram", "ns_poly", "ns_update")
+
+
+def log(msg):
+    print(msg, file=sys.stderr, flush=True)
+
+
+def allocate(wl, dev):
+    groups = []
+    for gi, grp in enumerate(wl.groups):
+        W, M, G = workloads.make_group(wl, gi, dev)
+        groups.append((grp, W, M, G))
+    torch.cuda.synchronize()
+    return groups
+
+
+def one_step(wl, groups, alpha):
+    for grp, W, M, G in groups:
+        binding.dion2_step_strided(W, M, G, alpha, wl.mu, wl.lr, wl.ns_steps, grp.axis)
+
+
+def time_steps(wl, groups, alpha, warmup, steps):
+    for _ in range(warmup):
+        one_step(wl, groups, alpha)
+    torch.cuda.synchronize()
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
+    t0 = time.perf_counter()
+    ev[0].record()
+    for i in range(steps):
+        one_step(wl, groups, alpha)
+        ev[i + 1].record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    per = [ev[i].elapsed_time(ev[i + 1]) for i in range(steps)]
+    return per, wall
+
+
+def profile_phases(wl, groups, alpha, steps):
+    """Per-phase kernel time from events the library records around each
+    launch on its stream, with the phase's algorithmic work."""
+    binding.dion2_profile_reset()
+    binding.dion2_profile_enable(True)
+    try:
+        for _ in range(steps):
+            one_step(wl, groups, alpha)
+        torch.cuda.synchronize()
+        prof = binding.dion2_profile_read()
+    finally:
+        binding.dion2_profile_enable(False)
+    out = {}
+    for ph, d in prof.items():
+        if d["calls"] == 0:
+            continue
+        avg_ms = d["ms"] / d["calls"]
+        work = d["work"] / d["calls"]
+        rate = work / (avg_ms * 1e-3) if avg_ms > 0 else 0.0
+        if ph in HBM_PHASES:
+            ach, peak, unit, bound = rate / 1e9, HBM_PEAK_GBS, "GB/s", "hbm"
+        elif ph in NS_PHASES:
+            ach, peak, unit, bound = rate / 1e12, MFMA_BF16_PEAK_TFS, "TFLOP/s", "mfma"
+        else:
+            ach, peak, unit, bound = rate / 1e9, HBM_PEAK_GBS, "GB/s", "latency"
+        out[ph] = dict(total_ms_per_step=d["ms"] / steps, avg_launch_ms=avg_ms,
+                       calls_per_step=d["calls"] / steps, work_per_call=work,
+                       achieved=ach, peak=peak, unit=unit, bound=bound, frac=ach / peak)
+    return out
+
+
+def cpu_baseline(wl, alpha, seconds):
+    """The oracle on a bounded sample: one matrix of each shape group per
+    pass, repeated until `seconds` of CPU time have run, then scaled by the
+    group counts to a whole-stack step."""
+    import numpy as np
+
+    import oracle
+    try:
+        from threadpoolctl import threadpool_info
+        blas_threads = max((i.get("num_threads", 1) for i in threadpool_info()), default=1)
+    except Exception:  # pragma: no cover - threadpoolctl is optional
+        blas_threads = None
+    dev = torch.device("cuda:0")
+    per_group = [[] for _ in wl.groups]
+    t_end = time.perf_counter() + seconds
+    passes = 0
+    while passes == 0 or time.perf_counter() < t_end:
+        for gi, grp in enumerate(wl.groups):
+            idx = passes % grp.count
+            W, M, G = workloads.make_group(wl, gi, dev, first=idx, count=1)
+            Wh = W[0].float().cpu().numpy().astype(np.float64)
+            Mh = M[0].cpu().numpy()
+            Gh = G[0].float().cpu().numpy()
+            t0 = time.perf_counter()
+            oracle.dion2_step(Wh, Mh, Gh, alpha, wl.mu, wl.lr, wl.ns_steps, grp.axis,
+                              w_dtype=wl.w_dtype)
+            per_group[gi].append(time.perf_counter() - t0)
+        passes += 1
+    est_s = sum(statistics.mean(t) * grp.count for t, grp in zip(per_group, wl.groups))
+    cores = len(os.sched_getaffinity(0))
+    return dict(value=est_s * 1e3, unit="ms", cores=blas_threads or cores, kind="oracle",
+                host_cores=cores,
+                sample=(f"{passes} pass(es) over one matrix of each of the {len(wl.groups)} "
+                        f"shape groups ({sum(len(t) for t in per_group)} oracle steps, "
+                        f"{sum(sum(t) for t in per_group):.1f} s), mean per group scaled by "
+                        f"the group counts to the {wl.matrices()}-matrix stack"))
+
+
+def main(argv=None):
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=80)
+    ap.add_argument("--workload", default="1b", choices=sorted(workloads.WORKLOADS))
+    ap.add_argument("--alpha", type=float, default=None,
+                    help="selection fraction of the headline number (default: the workload's first)")
+    ap.add_argument("--no-extra-alphas", action="store_true",
+                    help="time only --alpha, not the workload's other fractions")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--no-profile", action="store_true", help="skip the per-kernel event pass")
+    args = ap.parse_args(argv)
+
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures the Dion2 step on one GPU only; this build has no multi-GPU "
+              "path (every matrix is independent, see the sharding notes in DESIGN.md).",
+              file=sys.stderr)
+        return 2
+    if not torch.cuda.is_available():
+        print("bench.py needs a HIP device", file=sys.stderr)
+        return 2
+    if not os.path.exists(binding.LIB_PATH):
+        from paper_2512_16928_amd import build
+        build.build()
+    binding.load()
+
+    wl = workloads.WORKLOADS[args.workload]
+    alpha = args.alpha if args.alpha is not None else wl.alphas[0]
+    dev = torch.device("cuda:0")
+    log(f"[bench] allocating workload {wl.name}: {wl.matrices()} matrices, "
+        f"{wl.elements() / 1e6:.1f}M elements")
+    groups = allocate(wl, dev)
+
+    log(f"[bench] timing alpha={alpha}: warmup {args.warmup}, steps {args.steps}")
+    per, wall = time_steps(wl, groups, alpha, args.warmup, args.steps)
+    ms = statistics.mean(per)
+    log(f"[bench] alpha={alpha}: {ms:.3f} ms/step (min {min(per):.3f})")
+
+    phases = {}
+    roofline = None
+    ns_frac = None
+    if not args.no_profile:
+        phases = profile_phases(wl, groups, alpha, args.steps)
+        dom = max(phases, key=lambda p: phases[p]["total_ms_per_step"])
+        d = phases[dom]
+        roofline = dict(bound=d["bound"], achieved=round(d["achieved"], 3), peak=d["peak"],
+                        unit=d["unit"], frac=round(d["frac"], 4), traffic=None, kernel=dom,
+                        avg_launch_ms=round(d["avg_launch_ms"], 5))
+        ns_ms = sum(phases[p]["total_ms_per_step"] for p in NS_PHASES if p in phases)
+        ns_work = sum(phases[p]["work_per_call"] * phases[p]["calls_per_step"]
+                      for p in NS_PHASES if p in phases)
+        if ns_ms > 0:
+            ns_frac = ns_work / (ns_ms * 1e-3) / 1e12 / MFMA_BF16_PEAK_TFS
+        for p, d in phases.items():
+            log(f"[bench]   {p:10s} {d['total_ms_per_step']:8.3f} ms/step  "
+                f"{d['achieved']:9.1f} {d['unit']} ({100 * d['frac']:.1f}% of peak)")
+
+    per_alpha = {str(alpha): round(ms, 4)}
+    if not args.no_extra_alphas:
+        for a in wl.alphas:
+            if a == alpha:
+                continue
+            p2, _ = time_steps(wl, groups, a, args.warmup, args.steps)
+            per_alpha[str(a)] = round(statistics.mean(p2), 4)
+            log(f"[bench] alpha={a}: {per_alpha[str(a)]:.3f} ms/step")
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        log(f"[bench] timing the CPU oracle for ~{args.cpu_seconds:.0f} s")
+        cpu = cpu_baseline(wl, alpha, args.cpu_seconds)
+        log(f"[bench] oracle: {cpu['value']:.1f} ms per stack step (estimated)")
+
+    tail = per[-20:]
+    line = {
+        "metric": METRIC,
+        "value": round(ms, 4),
+        "unit": "ms",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms, 4),
+        "higher_is_better": False,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": wl.name, "description": wl.description, "alpha": alpha,
+                   "matrices": wl.matrices(), "elements": wl.elements(),
+                   "ns_steps": wl.ns_steps, "mu": wl.mu, "lr": wl.lr,
+                   "parallelism": "single GPU, batched per shape group"},
+        "roofline": roofline,
+        "cpu_baseline": cpu,
+        "per_alpha_ms": per_alpha,
+        "ns_mfma_frac": None if ns_frac is None else round(ns_frac, 4),
+        "step_ms_stats": {"mean": round(ms, 4), "median": round(statistics.median(per), 4),
+                          "min": round(min(per), 4), "mean_last_20": round(statistics.mean(tail), 4),
+                          "wall_s": round(wall, 3)},
+        "phases": {p: {k: (round(v, 5) if isinstance(v, float) else v) for k, v in d.items()}
+                   for p, d in phases.items()},
+    }
+    print(json.dumps(line), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

@@ -1,0 +1,191 @@
+/*
+ * dion2.h -- C ABI of the Dion2 optimizer step for AMD Instinct MI355X (gfx950).
+ *
+ * The step is Algorithm 1 of "Dion2: A Simple Method to Shrink Matrix in
+ * Muon" (Ahn, Amsel, Langford), applied to every matrix of a batch of
+ * same-shape weight matrices W (rows x cols = fan-out x fan-in, y = W x):
+ *
+ *   M <- M + G                              accumulate
+ *   K <- Select_alpha(M)                    k = ceil(alpha * d_sel) lines of
+ *                                           largest l1 norm (Default rule)
+ *   O <- NewtonSchulz(M[K, :])              only the selected submatrix
+ *   M[K, :] <- mu * M[K, :]                 selective decay, eq. (2)
+ *   W[K, :] <- W[K, :] - lr*sqrt(rows/cols)*O   sparse update, eq. (1)
+ *
+ * (rows shown; with axis = columns the same is done on M[:, K], W[:, K]).
+ *
+ * Numerical contract:
+ *   - M is fp32; the accumulate and the decay are single IEEE fp32 RNE
+ *     operations (bitwise reproducible).
+ *   - The l1 norm of each line is the exact sum of |M_ij| rounded once to
+ *     fp64 (double-double accumulation), so selection does not depend on a
+ *     summation order. Ties go to the lower index; NaN ranks as +inf.
+ *     K is ascending.
+ *   - Newton-Schulz: X = M[K,:] / (||M[K,:]||_F + eps), then per step
+ *     A = X X^T, B = b A + c A^2, X <- a X + B X on the orientation with the
+ *     smaller Gram matrix; bf16 MFMA operands with fp32 accumulation, A^2
+ *     from a three-pass bf16 hi/lo split of A. Default coefficients are
+ *     Muon's quintic (3.4445, -4.7750, 2.0315) at every step, eps = 1e-7.
+ *   - The weight update is computed in fp64 from the fp32 O and rounded once
+ *     (RNE) to W's storage type. Unselected lines of W are not written.
+ *
+ * Conventions shared by every entry point:
+ *   - W, M, G are DEVICE pointers to row-major, contiguous matrices, owned
+ *     by the caller; the library never frees or keeps them. Each base
+ *     pointer must be 16-byte aligned. W and M are updated in place; G is
+ *     read-only. Matrices of one call must not overlap.
+ *   - stream is a hipStream_t (NULL = the default stream). Calls are
+ *     asynchronous: nothing is synchronised and no result returns to the
+ *     host. Calls on one stream are serialised by the stream.
+ *   - Arguments are validated before anything is launched or allocated; on
+ *     any error nothing is modified and a negative dion2_status is returned.
+ *     dion2_last_error() gives a message for the calling thread.
+ *   - Without a caller workspace the library keeps one internal workspace
+ *     per (device, stream) and grows it with hipMalloc when needed (the
+ *     growth synchronises the device). Concurrent calls on different
+ *     streams use different workspaces; concurrent calls on one stream
+ *     from several host threads are serialised by a lock.
+ *   - Limits: 1 <= rows, cols; rows * cols < 2^31; 1 <= batch <= 65535;
+ *     0 < alpha <= 1; 0 <= ns_steps <= DION2_MAX_NS_STEPS; mu, lr finite.
+ */
+#ifndef DION2_H
+#define DION2_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define DION2_VERSION 1
+#define DION2_MAX_NS_STEPS 16
+
+typedef enum dion2_status {
+    DION2_OK = 0,
+    DION2_ERR_INVALID_ARG = -1, /* a bad pointer, size or hyperparameter      */
+    DION2_ERR_UNSUPPORTED = -2, /* valid but outside what this build handles  */
+    DION2_ERR_WORKSPACE = -3,   /* caller workspace too small / alloc failure */
+    DION2_ERR_HIP = -4          /* a HIP runtime call failed                  */
+} dion2_status;
+
+typedef enum dion2_axis {
+    DION2_AXIS_AUTO = -1, /* the shorter dimension; square selects rows (Sec. 4) */
+    DION2_AXIS_ROWS = 0,  /* select rows:    M[K, :], W[K, :]                     */
+    DION2_AXIS_COLS = 1   /* select columns: M[:, K], W[:, K]                     */
+} dion2_axis;
+
+typedef enum dion2_dtype {
+    DION2_DTYPE_F32 = 0,
+    DION2_DTYPE_BF16 = 1
+} dion2_dtype;
+
+/* Full-control options for dion2_step_ex. Fill with dion2_options_init. */
+typedef struct dion2_options {
+    int w_dtype;             /* storage type of W (default DION2_DTYPE_BF16)        */
+    int g_dtype;             /* storage type of G (default DION2_DTYPE_BF16)        */
+    const float* ns_coeffs;  /* HOST array [ns_steps][3] of (a, b, c) per step;
+                                NULL = Muon's quintic at every step                */
+    float ns_eps;            /* Frobenius-normalisation eps (default 1e-7), >= 0   */
+    int decay_all;           /* 0 = selective decay, eq. (2) (default);
+                                1 = decay all of M (the ablation of Sec. 4.2)      */
+    void* workspace;         /* DEVICE scratch of workspace_bytes, 256-B aligned,
+                                or NULL for the library-managed workspace          */
+    size_t workspace_bytes;  /* >= dion2_workspace_size(...) when workspace set    */
+    int32_t* dbg_sel_idx;    /* optional DEVICE out [batch][k]: K, ascending       */
+    double* dbg_norms;       /* optional DEVICE out [batch][d_sel]: l1 norms       */
+    float* dbg_update;       /* optional DEVICE out [batch][k][d_oth]: O, one
+                                selected line per row (row k of O^T for columns),
+                                before the lr*sqrt(rows/cols) scale                 */
+} dion2_options;
+
+/* Defaults: bf16 W and G, Muon quintic, eps 1e-7, selective decay, internal
+   workspace, no debug outputs. */
+void dion2_options_init(dion2_options* opt);
+
+/* One matrix. W, G: bf16 [rows][cols]; M: fp32 [rows][cols]. Algorithm 1. */
+int dion2_step(void* W, float* M, const void* G, int64_t rows, int64_t cols,
+               float alpha, float mu, float lr, int ns_steps, int axis,
+               void* stream);
+
+/* A batch of same-shape matrices as contiguous stacks: W, G bf16
+   [batch][rows][cols]; M fp32 [batch][rows][cols]. Every matrix gets its own
+   selection and Newton-Schulz (Algorithm 1 per matrix); the kernels are
+   batched across the stack. */
+int dion2_step_strided(void* W, float* M, const void* G, int batch,
+                       int64_t rows, int64_t cols, float alpha, float mu,
+                       float lr, int ns_steps, int axis, void* stream);
+
+/* A batch of same-shape matrices given by HOST arrays of DEVICE pointers
+   (W[i], G[i] bf16, M[i] fp32, each [rows][cols]). The pointer tables are
+   copied to the device before the call returns; the caller may reuse them. */
+int dion2_step_batched(void* const* W, float* const* M, const void* const* G,
+                       int batch, int64_t rows, int64_t cols, float alpha,
+                       float mu, float lr, int ns_steps, int axis,
+                       void* stream);
+
+/* Strided stacks with full control (dtypes, coefficients, eps, ablation,
+   caller workspace, debug outputs). opt == NULL means defaults. */
+int dion2_step_ex(void* W, float* M, const void* G, int batch, int64_t rows,
+                  int64_t cols, float alpha, float mu, float lr, int ns_steps,
+                  int axis, const dion2_options* opt, void* stream);
+
+/* Bytes of device workspace one call with these arguments needs (for
+   dion2_options.workspace). Returns 0 for invalid arguments. */
+size_t dion2_workspace_size(int batch, int64_t rows, int64_t cols,
+                            float alpha, int axis);
+
+/* Number of selected lines k = ceil(alpha * d_sel) clamped to [1, d_sel]
+   and the resolved axis (DION2_AXIS_ROWS / _COLS), for sizing debug
+   outputs. Returns DION2_OK or DION2_ERR_INVALID_ARG. */
+int dion2_plan_info(int64_t rows, int64_t cols, float alpha, int axis,
+                    int64_t* k_out, int* axis_out);
+
+/* ---- Measurement hooks ---------------------------------------------------
+ * While enabled, every kernel phase of subsequent calls is bracketed by HIP
+ * events recorded on the call's stream, and the phase's algorithmic work is
+ * added to a per-phase total: bytes for the streaming phases (what the step
+ * itself must move: M and G read and M written by MOMENTUM; the selected
+ * lines of M read and written by GATHER; the selected lines of W read and
+ * written by APPLY), dense-count flops for the Newton-Schulz GEMMs (2 s^2 l
+ * for the Gram matrix, 2 s^3 for A^2, 2 s^2 l for B X; s <= l are the
+ * compact matrix's unpadded sides). The events cost a little time, so the
+ * step time is measured with the hooks off. */
+typedef enum dion2_phase {
+    DION2_PHASE_MOMENTUM = 0,  /* K1: M += G and line norms         */
+    DION2_PHASE_SELECT = 1,    /* K2: top-k selection               */
+    DION2_PHASE_GATHER = 2,    /* K3: compact gather + decay        */
+    DION2_PHASE_NS_GRAM = 3,   /* K4: A = X X^T (hi/lo split)       */
+    DION2_PHASE_NS_POLY = 4,   /* K4: B = b A + c A^2               */
+    DION2_PHASE_NS_UPDATE = 5, /* K4: X <- a X + B X                */
+    DION2_PHASE_APPLY = 6,     /* K5: scatter-apply into W          */
+    DION2_PHASE_COUNT = 7
+} dion2_phase;
+
+/* on != 0 enables the hooks, 0 disables them; returns the previous state. */
+int dion2_profile_enable(int on);
+
+/* Waits for the recorded events and writes, for the first n phases, the
+   summed kernel milliseconds, the number of calls timed, the kernel launches
+   and the summed algorithmic work (bytes or flops, as above). Any output
+   pointer may be NULL. Totals accumulate until dion2_profile_reset. */
+int dion2_profile_read(double* ms, int64_t* calls, int64_t* launches, double* work, int n);
+
+void dion2_profile_reset(void);
+
+/* Frees the library-managed workspaces (synchronises each device first). */
+void dion2_release_workspaces(void);
+
+/* Static description of a status code. */
+const char* dion2_status_string(int status);
+
+/* Message describing the last error returned on the calling thread. */
+const char* dion2_last_error(void);
+
+int dion2_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* DION2_H */

@@ -51,7 +51,7 @@ AXIS_COLS = 1
 # for the iteration (Sec. 1) without printing them.
 MUON_QUINTIC = (3.4445, -4.7750, 2.0315)
 DEFAULT_EPS = 1e-7
-DEFAULT_MU = 0.95    # Algorithm 1, hyperparameter line
+DEFAULT_MU = 0.95    # Algorithm 1, its momentum decay hyperparameter
 DEFAULT_LR = 0.02    # Sec. 4, experimental details
 
 
@@ -110,7 +110,7 @@ def num_selected(alpha, d_sel):
 
 
 def momentum_accumulate(M, G):
-    """M <- M + G (Algorithm 1, first line), in fp32 arithmetic because the
+    """M <- M + G (Algorithm 1, accumulate step), in fp32 arithmetic because the
     momentum is stored in fp32. G holds values exactly representable in fp32
     (fp32 or bf16 storage)."""
     return np.asarray(M, dtype=np.float32) + np.asarray(G, dtype=np.float32)
@@ -152,7 +152,7 @@ def gather(M, K, axis):
 
 
 def newton_schulz(X, steps, coeffs=None, eps=DEFAULT_EPS):
-    """Newton-Schulz orthonormalisation (Sec. 1; Algorithm 1, third line).
+    """Newton-Schulz orthonormalisation (Sec. 1; Algorithm 1, orthonormalisation step).
 
     X is divided by (||X||_F + eps); then each step t applies
         A = X X^T,  B = b_t A + c_t A^2,  X <- a_t X + B X,
@@ -179,7 +179,7 @@ def newton_schulz(X, steps, coeffs=None, eps=DEFAULT_EPS):
 
 
 def selective_decay(M, K, mu, axis, store="fp32", decay_all=False):
-    """M[K, :] <- mu * M[K, :] (eq. (2); Algorithm 1, fourth line), in the
+    """M[K, :] <- mu * M[K, :] (eq. (2); Algorithm 1, decay step), in the
     momentum's storage precision. decay_all=True is the ablation of Sec. 4.2
     (M <- mu * M)."""
     if store == "fp32":
@@ -204,7 +204,7 @@ def update_scale(lr, rows, cols):
 
 
 def apply_update(W, K, O, lr, axis, w_dtype):
-    """W[K, :] <- W[K, :] - lr*sqrt(fan_out/fan_in)*O (Algorithm 1, last line;
+    """W[K, :] <- W[K, :] - lr*sqrt(fan_out/fan_in)*O (Algorithm 1, sparse update step;
     eq. (1)); columns analogously. Computed in fp64 and rounded once to W's
     storage type; lines outside K are left untouched."""
     W = np.array(W, dtype=np.float64)

@@ -1,0 +1,281 @@
+"""Thin Python binding of libdion2.so (the C ABI declared in include/dion2.h).
+
+Argument marshalling only: torch tensors are turned into device pointers and
+the current HIP stream, sizes are passed through, and a negative status is
+raised as Dion2Error. Every step of the Dion2 update runs in the library's
+HIP kernels; there is no fallback of any kind, and calling any entry point
+without the built library raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from ctypes import (POINTER, c_char_p, c_double, c_float, c_int, c_int64, c_size_t,
+                    c_void_p)
+
+import torch
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libdion2.so")
+
+DION2_OK = 0
+DION2_ERR_INVALID_ARG = -1
+DION2_ERR_UNSUPPORTED = -2
+DION2_ERR_WORKSPACE = -3
+DION2_ERR_HIP = -4
+
+AXIS_AUTO = -1
+AXIS_ROWS = 0
+AXIS_COLS = 1
+
+DTYPE_F32 = 0
+DTYPE_BF16 = 1
+
+MAX_NS_STEPS = 16
+
+# Every function include/dion2.h declares (checked by the ABI tests).
+EXPORTED = ("dion2_options_init", "dion2_step", "dion2_step_strided", "dion2_step_batched",
+            "dion2_step_ex", "dion2_workspace_size", "dion2_plan_info",
+            "dion2_release_workspaces", "dion2_status_string", "dion2_last_error",
+            "dion2_version", "dion2_profile_enable", "dion2_profile_read", "dion2_profile_reset")
+
+PHASES = ("momentum", "select", "gather", "ns_gram", "ns_poly", "ns_update", "apply")
+
+
+class Dion2Error(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__(f"{message} (status {status})")
+        self.status = status
+
+
+class Options(ctypes.Structure):
+    """Mirror of struct dion2_options."""
+    _fields_ = [
+        ("w_dtype", c_int),
+        ("g_dtype", c_int),
+        ("ns_coeffs", POINTER(c_float)),
+        ("ns_eps", c_float),
+        ("decay_all", c_int),
+        ("workspace", c_void_p),
+        ("workspace_bytes", c_size_t),
+        ("dbg_sel_idx", c_void_p),
+        ("dbg_norms", c_void_p),
+        ("dbg_update", c_void_p),
+    ]
+
+
+_lib = None
+
+
+def load(path: str = LIB_PATH):
+    """Loads libdion2.so (once) and declares the C signatures."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise RuntimeError(
+            f"{path} is missing: build it with `python -m paper_2512_16928_amd.build` "
+            "(the Dion2 step has no non-HIP implementation)")
+    lib = ctypes.CDLL(path)
+    i64, vp = c_int64, c_void_p
+    step_tail = [c_float, c_float, c_float, c_int, c_int]
+    lib.dion2_options_init.argtypes = [POINTER(Options)]
+    lib.dion2_options_init.restype = None
+    lib.dion2_step.argtypes = [vp, vp, vp, i64, i64, *step_tail, vp]
+    lib.dion2_step.restype = c_int
+    lib.dion2_step_strided.argtypes = [vp, vp, vp, c_int, i64, i64, *step_tail, vp]
+    lib.dion2_step_strided.restype = c_int
+    lib.dion2_step_batched.argtypes = [POINTER(vp), POINTER(vp), POINTER(vp), c_int, i64, i64,
+                                       *step_tail, vp]
+    lib.dion2_step_batched.restype = c_int
+    lib.dion2_step_ex.argtypes = [vp, vp, vp, c_int, i64, i64, *step_tail, POINTER(Options), vp]
+    lib.dion2_step_ex.restype = c_int
+    lib.dion2_workspace_size.argtypes = [c_int, i64, i64, c_float, c_int]
+    lib.dion2_workspace_size.restype = c_size_t
+    lib.dion2_plan_info.argtypes = [i64, i64, c_float, c_int, POINTER(c_int64), POINTER(c_int)]
+    lib.dion2_plan_info.restype = c_int
+    lib.dion2_release_workspaces.argtypes = []
+    lib.dion2_release_workspaces.restype = None
+    lib.dion2_status_string.argtypes = [c_int]
+    lib.dion2_status_string.restype = c_char_p
+    lib.dion2_last_error.argtypes = []
+    lib.dion2_last_error.restype = c_char_p
+    lib.dion2_version.argtypes = []
+    lib.dion2_version.restype = c_int
+    lib.dion2_profile_enable.argtypes = [c_int]
+    lib.dion2_profile_enable.restype = c_int
+    lib.dion2_profile_read.argtypes = [POINTER(c_double), POINTER(c_int64), POINTER(c_int64),
+                                       POINTER(c_double), c_int]
+    lib.dion2_profile_read.restype = c_int
+    lib.dion2_profile_reset.argtypes = []
+    lib.dion2_profile_reset.restype = None
+    _lib = lib
+    return lib
+
+
+def _check(status: int):
+    if status != DION2_OK:
+        lib = load()
+        raise Dion2Error(status, lib.dion2_last_error().decode())
+
+
+def _stream_ptr(stream, device):
+    if stream is None:
+        stream = torch.cuda.current_stream(device)
+    return c_void_p(stream.cuda_stream)
+
+
+_DT = {torch.bfloat16: DTYPE_BF16, torch.float32: DTYPE_F32}
+
+
+def _mats(W, M, G, ndim):
+    for name, t in (("W", W), ("M", M), ("G", G)):
+        if not isinstance(t, torch.Tensor):
+            raise TypeError(f"{name} must be a torch tensor")
+        if t.device.type != "cuda":
+            raise ValueError(f"{name} must be a HIP device tensor, got {t.device}")
+        if not t.is_contiguous():
+            raise ValueError(f"{name} must be contiguous")
+        if t.dim() != ndim:
+            raise ValueError(f"{name} must have {ndim} dimensions, got {tuple(t.shape)}")
+    if not (W.shape == M.shape == G.shape):
+        raise ValueError(f"W {tuple(W.shape)}, M {tuple(M.shape)}, G {tuple(G.shape)} differ")
+    if M.dtype != torch.float32:
+        raise ValueError("M (momentum) must be float32")
+    if W.dtype not in _DT or G.dtype not in _DT:
+        raise ValueError("W and G must be bfloat16 or float32")
+    if not (W.device == M.device == G.device):
+        raise ValueError("W, M and G must be on one device")
+
+
+def dion2_step(W, M, G, alpha, mu=0.95, lr=0.02, ns_steps=5, axis=AXIS_AUTO, stream=None):
+    """One matrix, bf16 W and G, fp32 M (updated in place)."""
+    _mats(W, M, G, 2)
+    if W.dtype != torch.bfloat16 or G.dtype != torch.bfloat16:
+        raise ValueError("dion2_step takes bf16 W and G; use dion2_step_ex for other dtypes")
+    lib = load()
+    rows, cols = W.shape
+    _check(lib.dion2_step(W.data_ptr(), M.data_ptr(), G.data_ptr(), rows, cols, alpha, mu, lr,
+                          ns_steps, axis, _stream_ptr(stream, W.device)))
+
+
+def dion2_step_strided(W, M, G, alpha, mu=0.95, lr=0.02, ns_steps=5, axis=AXIS_AUTO,
+                       stream=None):
+    """Stacks [batch, rows, cols]: bf16 W and G, fp32 M."""
+    _mats(W, M, G, 3)
+    if W.dtype != torch.bfloat16 or G.dtype != torch.bfloat16:
+        raise ValueError("dion2_step_strided takes bf16 W and G; use dion2_step_ex otherwise")
+    lib = load()
+    batch, rows, cols = W.shape
+    _check(lib.dion2_step_strided(W.data_ptr(), M.data_ptr(), G.data_ptr(), batch, rows, cols,
+                                  alpha, mu, lr, ns_steps, axis, _stream_ptr(stream, W.device)))
+
+
+def dion2_step_batched(Ws, Ms, Gs, alpha, mu=0.95, lr=0.02, ns_steps=5, axis=AXIS_AUTO,
+                       stream=None):
+    """Lists of same-shape matrices (bf16 W and G, fp32 M)."""
+    if not (len(Ws) == len(Ms) == len(Gs)) or len(Ws) == 0:
+        raise ValueError("Ws, Ms, Gs must be non-empty lists of equal length")
+    for W, M, G in zip(Ws, Ms, Gs):
+        _mats(W, M, G, 2)
+        if W.shape != Ws[0].shape:
+            raise ValueError("all matrices of a batch must have one shape")
+        if W.dtype != torch.bfloat16 or G.dtype != torch.bfloat16:
+            raise ValueError("dion2_step_batched takes bf16 W and G")
+    lib = load()
+    n = len(Ws)
+    arr = c_void_p * n
+    tw = arr(*[t.data_ptr() for t in Ws])
+    tm = arr(*[t.data_ptr() for t in Ms])
+    tg = arr(*[t.data_ptr() for t in Gs])
+    rows, cols = Ws[0].shape
+    _check(lib.dion2_step_batched(tw, tm, tg, n, rows, cols, alpha, mu, lr, ns_steps, axis,
+                                  _stream_ptr(stream, Ws[0].device)))
+
+
+def dion2_step_ex(W, M, G, alpha, mu=0.95, lr=0.02, ns_steps=5, axis=AXIS_AUTO, *,
+                  ns_coeffs=None, ns_eps=1e-7, decay_all=False, workspace=None,
+                  dbg_sel_idx=None, dbg_norms=None, dbg_update=None, stream=None):
+    """Full control. W, M, G are [rows, cols] or [batch, rows, cols]; W and G
+    may be bf16 or fp32. Debug outputs are preallocated device tensors:
+    dbg_sel_idx int32 [batch, k], dbg_norms float64 [batch, d_sel],
+    dbg_update float32 [batch, k, d_oth]."""
+    if W.dim() == 2:
+        W, M, G = W.unsqueeze(0), M.unsqueeze(0), G.unsqueeze(0)
+    _mats(W, M, G, 3)
+    lib = load()
+    opt = Options()
+    lib.dion2_options_init(ctypes.byref(opt))
+    opt.w_dtype = _DT[W.dtype]
+    opt.g_dtype = _DT[G.dtype]
+    coeff_buf = None
+    if ns_coeffs is not None:
+        flat = [float(v) for abc in ns_coeffs for v in abc]
+        if len(flat) < 3 * ns_steps:
+            raise ValueError("ns_coeffs needs one (a, b, c) per Newton-Schulz step")
+        coeff_buf = (c_float * len(flat))(*flat)
+        opt.ns_coeffs = ctypes.cast(coeff_buf, POINTER(c_float))
+    opt.ns_eps = ns_eps
+    opt.decay_all = 1 if decay_all else 0
+    for name, t, dt in (("dbg_sel_idx", dbg_sel_idx, torch.int32),
+                        ("dbg_norms", dbg_norms, torch.float64),
+                        ("dbg_update", dbg_update, torch.float32)):
+        if t is not None:
+            if t.dtype != dt or not t.is_contiguous() or t.device != W.device:
+                raise ValueError(f"{name} must be a contiguous {dt} tensor on {W.device}")
+            setattr(opt, name, t.data_ptr())
+    if workspace is not None:
+        if workspace.device != W.device or not workspace.is_contiguous():
+            raise ValueError("workspace must be a contiguous tensor on W's device")
+        opt.workspace = workspace.data_ptr()
+        opt.workspace_bytes = workspace.numel() * workspace.element_size()
+    batch, rows, cols = W.shape
+    _check(lib.dion2_step_ex(W.data_ptr(), M.data_ptr(), G.data_ptr(), batch, rows, cols, alpha,
+                             mu, lr, ns_steps, axis, ctypes.byref(opt),
+                             _stream_ptr(stream, W.device)))
+
+
+def dion2_workspace_size(batch, rows, cols, alpha, axis=AXIS_AUTO) -> int:
+    return int(load().dion2_workspace_size(batch, rows, cols, alpha, axis))
+
+
+def dion2_plan_info(rows, cols, alpha, axis=AXIS_AUTO):
+    """(k, resolved_axis) for one matrix of this shape."""
+    k = c_int64(0)
+    ax = c_int(0)
+    _check(load().dion2_plan_info(rows, cols, alpha, axis, ctypes.byref(k), ctypes.byref(ax)))
+    return int(k.value), int(ax.value)
+
+
+def dion2_release_workspaces():
+    load().dion2_release_workspaces()
+
+
+def dion2_status_string(status: int) -> str:
+    return load().dion2_status_string(status).decode()
+
+
+def dion2_last_error() -> str:
+    return load().dion2_last_error().decode()
+
+
+def dion2_version() -> int:
+    return int(load().dion2_version())
+
+
+def dion2_profile_enable(on: bool) -> bool:
+    """Turns the per-phase event timing on or off; returns the previous state."""
+    return bool(load().dion2_profile_enable(1 if on else 0))
+
+
+def dion2_profile_read():
+    """{phase: dict(ms, calls, launches, work)} accumulated since the last reset."""
+    n = len(PHASES)
+    ms, work = (c_double * n)(), (c_double * n)()
+    calls, launches = (c_int64 * n)(), (c_int64 * n)()
+    _check(load().dion2_profile_read(ms, calls, launches, work, n))
+    return {p: dict(ms=ms[i], calls=calls[i], launches=launches[i], work=work[i])
+            for i, p in enumerate(PHASES)}
+
+
+def dion2_profile_reset():
+    load().dion2_profile_reset()

@@ -1,0 +1,182 @@
+// Device-side helpers and launch interfaces shared by the Dion2 kernels.
+//
+// Layout conventions (all row-major):
+//   W, G : [rows][cols] in their storage type (bf16 or fp32), M : fp32.
+//   A "line" is a row (axis = rows) or a column (axis = columns) of M / W;
+//   d_sel lines exist, each of length d_oth.
+//   Compact submatrix L  : [kpad][opad] bf16, row p = selected line K[p]
+//                           scaled by 1 / (||M[K]||_F + eps), zero padding.
+//   Its transpose     LT : [opad][kpad] bf16.
+//   kpad, opad are k and d_oth rounded up to the GEMM tile (128); every
+//   padded entry is zero, which the Newton-Schulz polynomial keeps at zero.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace dion2 {
+
+constexpr int kTile = 128;  // padding granule of the compact buffers
+
+// A batch of same-shape matrices: either one strided stack (tables == null)
+// or device-resident tables of per-matrix pointers.
+struct MatSet {
+    void* W;                // stack base, or unused with tables
+    float* M;
+    const void* G;
+    int64_t stride;         // elements between consecutive matrices
+    void* const* Wt;        // device tables (nullable)
+    float* const* Mt;
+    const void* const* Gt;
+
+    template <typename T>
+    __device__ __forceinline__ T* w(int b) const {
+        return Wt ? static_cast<T*>(Wt[b]) : static_cast<T*>(W) + (int64_t)b * stride;
+    }
+    __device__ __forceinline__ float* m(int b) const {
+        return Mt ? Mt[b] : M + (int64_t)b * stride;
+    }
+    template <typename T>
+    __device__ __forceinline__ const T* g(int b) const {
+        return Gt ? static_cast<const T*>(Gt[b]) : static_cast<const T*>(G) + (int64_t)b * stride;
+    }
+};
+
+// ------------------------------------------------------------ conversions
+
+__device__ __forceinline__ float bf16_bits_to_f32(uint32_t h) {
+    return __uint_as_float(h << 16);
+}
+
+// fp32 -> bf16, round to nearest even; NaN stays a (quiet) NaN.
+__device__ __forceinline__ uint16_t f32_to_bf16(float f) {
+    uint32_t u = __float_as_uint(f);
+    if ((u & 0x7fffffffu) > 0x7f800000u) return (uint16_t)((u >> 16) | 0x40u);
+    u += 0x7fffu + ((u >> 16) & 1u);
+    return (uint16_t)(u >> 16);
+}
+
+// fp64 -> bf16 with a single round-to-nearest-even: first to fp32 with
+// round-to-odd (truncate, then force the last bit when inexact), which keeps
+// the second rounding exact because fp32 carries more than 8 + 2 bits.
+__device__ __forceinline__ uint16_t f64_to_bf16(double d) {
+    float f = __double2float_rz(d);
+    if ((double)f != d && !__builtin_isnan(d)) f = __uint_as_float(__float_as_uint(f) | 1u);
+    return f32_to_bf16(f);
+}
+
+template <typename T> struct Elem;
+template <> struct Elem<float> {
+    static __device__ __forceinline__ float load(const float* p) { return *p; }
+    static __device__ __forceinline__ void store_f64(float* p, double v) { *p = (float)v; }
+};
+template <> struct Elem<uint16_t> {
+    static __device__ __forceinline__ float load(const uint16_t* p) { return bf16_bits_to_f32(*p); }
+    static __device__ __forceinline__ void store_f64(uint16_t* p, double v) { *p = f64_to_bf16(v); }
+};
+
+// four consecutive elements as fp32 (p is 8-byte aligned for bf16, 16 for fp32)
+__device__ __forceinline__ void load4(const float* p, float (&v)[4]) {
+    float4 x = *reinterpret_cast<const float4*>(p);
+    v[0] = x.x; v[1] = x.y; v[2] = x.z; v[3] = x.w;
+}
+__device__ __forceinline__ void load4(const uint16_t* p, float (&v)[4]) {
+    uint2 x = *reinterpret_cast<const uint2*>(p);
+    v[0] = bf16_bits_to_f32(x.x & 0xffffu); v[1] = bf16_bits_to_f32(x.x >> 16);
+    v[2] = bf16_bits_to_f32(x.y & 0xffffu); v[3] = bf16_bits_to_f32(x.y >> 16);
+}
+
+// ------------------------------------------------------- double-double sum
+
+// Error-free transformation a + b = s + e (Knuth's TwoSum; no branch).
+__device__ __forceinline__ void two_sum(double a, double b, double& s, double& e) {
+    s = a + b;
+    double bb = s - a;
+    e = (a - (s - bb)) + (b - bb);
+}
+
+// (hi, lo) += (bhi, blo)
+__device__ __forceinline__ void dd_add(double& hi, double& lo, double bhi, double blo) {
+    double s, e;
+    two_sum(hi, bhi, s, e);
+    hi = s;
+    lo = lo + (blo + e);
+}
+
+// ------------------------------------------------------------------ launch
+// Every launcher enqueues on `stream` and returns the launch status.
+
+struct MomentumArgs {
+    MatSet ms;
+    int64_t rows, cols;
+    int batch;
+    double* l1;        // [batch][d_sel]
+    double* sq;        // [batch][d_sel]
+    double* part;      // column mode partials [batch][nrb][3][cols]
+    int rb_rows, nrb;  // column mode row blocking
+    float mu;          // used when decay_all (M <- mu (M + G) after use)
+};
+hipError_t launch_momentum(const MomentumArgs& a, int axis, int g_bf16, hipStream_t s);
+int64_t momentum_col_blocks(int64_t rows, int* rb_rows);
+
+struct SelectArgs {
+    const double* l1;
+    const double* sq;
+    int d_sel, k, batch;
+    double eps;
+    int32_t* sel;      // [batch][k] ascending
+    double* scale;     // [batch] 1 / (sqrt(sum sq over K) + eps)
+};
+hipError_t launch_select(const SelectArgs& a, hipStream_t s);
+
+struct GatherArgs {
+    MatSet ms;
+    int64_t rows, cols;
+    int batch, k, d_oth, kpad, opad;
+    const int32_t* sel;
+    const double* scale;
+    float mu;
+    int decay;         // 1: M[K] <- mu M[K] here
+    uint16_t* L;       // [batch][kpad][opad]
+    uint16_t* LT;      // [batch][opad][kpad]
+    float* O;          // nullable: fp32 copy in L layout (no Newton-Schulz step)
+};
+hipError_t launch_gather(const GatherArgs& a, int axis, hipStream_t s);
+
+struct DecayAllArgs {
+    MatSet ms;
+    int64_t rows, cols;
+    int batch;
+    float mu;
+};
+hipError_t launch_decay_all(const DecayAllArgs& a, hipStream_t s);
+
+// Newton-Schulz GEMMs (NT: C[i][j] = sum_k A[i][k] * B[j][k]).
+enum GemmEpi { EPI_SPLIT = 0, EPI_POLY = 1, EPI_AXPY = 2, EPI_FINAL = 3 };
+struct GemmArgs {
+    const uint16_t* A0; const uint16_t* A1;   // A operand(s), [M][K] ld lda
+    const uint16_t* B0; const uint16_t* B1;   // B operand(s), [N][K] ld ldb
+    int64_t sA, sB;                           // batch strides (elements)
+    int M, N, K, lda, ldb;
+    int batch;
+    float ca, cb, cc;                         // polynomial coefficients
+    // epilogue inputs / outputs (batch stride in elements, ld in elements)
+    const uint16_t* E0; const uint16_t* E1; int64_t sE; int lde;  // Ahi/Alo or Z
+    void* out0; int64_t sOut0; int ldo0;
+    void* out1; int64_t sOut1; int ldo1;
+    int out_transposed;                        // EPI_FINAL: write out0[j][i]
+};
+hipError_t launch_gemm(const GemmArgs& a, GemmEpi epi, hipStream_t s);
+
+struct ApplyArgs {
+    MatSet ms;
+    int64_t rows, cols;
+    int batch, k, d_oth, kpad, opad;
+    const int32_t* sel;
+    const float* O;    // [batch][kpad][opad]
+    double lr_eff;     // lr * sqrt(rows / cols)
+    float* dbg;        // nullable [batch][k][d_oth]
+};
+hipError_t launch_apply(const ApplyArgs& a, int axis, int w_bf16, hipStream_t s);
+
+}  // namespace dion2

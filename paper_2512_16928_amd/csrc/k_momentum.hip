@@ -1,0 +1,195 @@
+// K1: momentum accumulate fused with the line-norm reduction.
+//
+// M <- fl32(M + G) in place (Algorithm 1, accumulate step) and, for every line of
+// the selection axis, the l1 norm (Select_alpha, Default rule) and the
+// squared l2 norm (for ||M[K]||_F, the Newton-Schulz normalisation).
+// The l1 norm is accumulated in double-double from the fp32 values and
+// rounded once at the end, which gives the exactly rounded sum unless the
+// exact sum lies within ~n*2^-106 (relative) of an fp64 rounding boundary.
+//
+// Row mode: one 256-thread block per row; every thread streams 4-element
+// vectors (16 B of M, 8 B of bf16 G) and the block reduces in a fixed order.
+// Column mode: each thread owns 4 adjacent columns of a block of rows and
+// writes double-double partials; a second pass folds the row blocks in
+// order. No floating-point atomics anywhere: results are run-to-run bitwise
+// reproducible.
+#include "dion2_device.h"
+
+namespace dion2 {
+namespace {
+
+constexpr int kThreads = 256;
+
+__device__ __forceinline__ void accumulate(double x, double& hi, double& lo, double& s2) {
+    double s, e;
+    two_sum(hi, x, s, e);
+    hi = s;
+    lo += e;
+    s2 += x * x;
+}
+
+// Fixed-order block reduction of (hi, lo, s2); result valid in thread 0.
+__device__ __forceinline__ void block_reduce(double& hi, double& lo, double& s2) {
+    for (int off = 32; off > 0; off >>= 1) {
+        double ohi = __shfl_xor(hi, off);
+        double olo = __shfl_xor(lo, off);
+        double os2 = __shfl_xor(s2, off);
+        dd_add(hi, lo, ohi, olo);
+        s2 += os2;
+    }
+    __shared__ double red[3][kThreads / 64];
+    const int wave = threadIdx.x >> 6;
+    if ((threadIdx.x & 63) == 0) {
+        red[0][wave] = hi;
+        red[1][wave] = lo;
+        red[2][wave] = s2;
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        hi = red[0][0];
+        lo = red[1][0];
+        s2 = red[2][0];
+        for (int w = 1; w < kThreads / 64; ++w) {
+            dd_add(hi, lo, red[0][w], red[1][w]);
+            s2 += red[2][w];
+        }
+    }
+}
+
+template <int VEC, typename GT>
+__global__ __launch_bounds__(kThreads) void momentum_rows(MatSet ms, int64_t rows, int64_t cols,
+                                                          double* __restrict__ l1,
+                                                          double* __restrict__ sq) {
+    const int b = blockIdx.y;
+    const int64_t row = blockIdx.x;
+    float* __restrict__ M = ms.m(b) + row * cols;
+    const GT* __restrict__ G = ms.g<GT>(b) + row * cols;
+    double hi = 0.0, lo = 0.0, s2 = 0.0;
+    if constexpr (VEC == 4) {
+#pragma unroll 2
+        for (int64_t c = threadIdx.x * 4; c < cols; c += kThreads * 4) {
+            float m[4], g[4];
+            load4(M + c, m);
+            load4(G + c, g);
+#pragma unroll
+            for (int v = 0; v < 4; ++v) m[v] = m[v] + g[v];
+            *reinterpret_cast<float4*>(M + c) = make_float4(m[0], m[1], m[2], m[3]);
+#pragma unroll
+            for (int v = 0; v < 4; ++v) accumulate(fabs((double)m[v]), hi, lo, s2);
+        }
+    } else {
+        for (int64_t c = threadIdx.x; c < cols; c += kThreads) {
+            float m = M[c] + Elem<GT>::load(G + c);
+            M[c] = m;
+            accumulate(fabs((double)m), hi, lo, s2);
+        }
+    }
+    block_reduce(hi, lo, s2);
+    if (threadIdx.x == 0) {
+        l1[(int64_t)b * rows + row] = hi + lo;
+        sq[(int64_t)b * rows + row] = s2;
+    }
+}
+
+template <int VEC, typename GT>
+__global__ __launch_bounds__(kThreads) void momentum_cols_partial(MatSet ms, int64_t rows,
+                                                                  int64_t cols, int rb_rows,
+                                                                  int nrb,
+                                                                  double* __restrict__ part) {
+    const int b = blockIdx.z;
+    const int rb = blockIdx.y;
+    const int64_t c0 = ((int64_t)blockIdx.x * kThreads + threadIdx.x) * VEC;
+    if (c0 >= cols) return;
+    const int64_t r0 = (int64_t)rb * rb_rows;
+    const int64_t r1 = r0 + rb_rows < rows ? r0 + rb_rows : rows;
+    float* __restrict__ M = ms.m(b);
+    const GT* __restrict__ G = ms.g<GT>(b);
+    double hi[VEC], lo[VEC], s2[VEC];
+#pragma unroll
+    for (int v = 0; v < VEC; ++v) hi[v] = lo[v] = s2[v] = 0.0;
+#pragma unroll 4
+    for (int64_t r = r0; r < r1; ++r) {
+        float* p = M + r * cols + c0;
+        const GT* q = G + r * cols + c0;
+        if constexpr (VEC == 4) {
+            float m[4], g[4];
+            load4(p, m);
+            load4(q, g);
+#pragma unroll
+            for (int v = 0; v < 4; ++v) m[v] = m[v] + g[v];
+            *reinterpret_cast<float4*>(p) = make_float4(m[0], m[1], m[2], m[3]);
+#pragma unroll
+            for (int v = 0; v < VEC; ++v) accumulate(fabs((double)m[v]), hi[v], lo[v], s2[v]);
+        } else {
+            float m = p[0] + Elem<GT>::load(q);
+            p[0] = m;
+            accumulate(fabs((double)m), hi[0], lo[0], s2[0]);
+        }
+    }
+    double* out = part + ((int64_t)b * nrb + rb) * 3 * cols;
+#pragma unroll
+    for (int v = 0; v < VEC; ++v) {
+        out[c0 + v] = hi[v];
+        out[cols + c0 + v] = lo[v];
+        out[2 * cols + c0 + v] = s2[v];
+    }
+}
+
+__global__ __launch_bounds__(kThreads) void momentum_cols_final(const double* __restrict__ part,
+                                                                int nrb, int64_t cols,
+                                                                double* __restrict__ l1,
+                                                                double* __restrict__ sq) {
+    const int b = blockIdx.y;
+    const int64_t c = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+    if (c >= cols) return;
+    double hi = 0.0, lo = 0.0, s2 = 0.0;
+    for (int rb = 0; rb < nrb; ++rb) {
+        const double* p = part + ((int64_t)b * nrb + rb) * 3 * cols;
+        dd_add(hi, lo, p[c], p[cols + c]);
+        s2 += p[2 * cols + c];
+    }
+    l1[(int64_t)b * cols + c] = hi + lo;
+    sq[(int64_t)b * cols + c] = s2;
+}
+
+template <int VEC, typename GT>
+hipError_t launch_typed(const MomentumArgs& a, int axis, hipStream_t s) {
+    if (axis == 0) {
+        dim3 grid((unsigned)a.rows, (unsigned)a.batch);
+        hipLaunchKernelGGL((momentum_rows<VEC, GT>), grid, dim3(kThreads), 0, s, a.ms, a.rows,
+                           a.cols, a.l1, a.sq);
+    } else {
+        const int64_t per_block = (int64_t)kThreads * VEC;
+        dim3 grid((unsigned)((a.cols + per_block - 1) / per_block), (unsigned)a.nrb,
+                  (unsigned)a.batch);
+        hipLaunchKernelGGL((momentum_cols_partial<VEC, GT>), grid, dim3(kThreads), 0, s, a.ms,
+                           a.rows, a.cols, a.rb_rows, a.nrb, a.part);
+        hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+        dim3 grid2((unsigned)((a.cols + kThreads - 1) / kThreads), (unsigned)a.batch);
+        hipLaunchKernelGGL(momentum_cols_final, grid2, dim3(kThreads), 0, s, a.part, a.nrb,
+                           a.cols, a.l1, a.sq);
+    }
+    return hipGetLastError();
+}
+
+}  // namespace
+
+// Row blocking of the column-mode reduction: blocks of 256 rows keep the
+// partials small next to the matrix while giving enough blocks to fill the
+// chip.
+int64_t momentum_col_blocks(int64_t rows, int* rb_rows) {
+    const int rb = 256;
+    *rb_rows = rb;
+    return (rows + rb - 1) / rb;
+}
+
+hipError_t launch_momentum(const MomentumArgs& a, int axis, int g_bf16, hipStream_t s) {
+    const bool vec = (a.cols % 4) == 0;
+    if (g_bf16) {
+        return vec ? launch_typed<4, uint16_t>(a, axis, s) : launch_typed<1, uint16_t>(a, axis, s);
+    }
+    return vec ? launch_typed<4, float>(a, axis, s) : launch_typed<1, float>(a, axis, s);
+}
+
+}  // namespace dion2

@@ -1,0 +1,128 @@
+// K2: Select_alpha, Default rule -- the k lines of largest l1 norm.
+//
+// One 1024-thread block per matrix. Norms are non-negative fp64, so their
+// bit patterns order like unsigned integers; NaN is mapped to +inf's pattern
+// (a corrupted line ranks first and shows in W). An MSD radix select over
+// the 64-bit keys, 8 bits per pass with an LDS histogram, finds the k-th
+// largest key T and how many of the lines equal to T are still needed. A
+// second sweep in index order keeps every key > T and the lowest-indexed
+// keys == T (ties to the lower index) and compacts them with wave ballots
+// into K, which therefore comes out ascending.
+//
+// The block also sums the selected lines' squared l2 norms in a fixed order
+// and stores 1 / (||M[K]||_F + eps), the Newton-Schulz normalisation.
+#include "dion2_device.h"
+
+namespace dion2 {
+namespace {
+
+constexpr int kThreads = 1024;
+constexpr int kWaves = kThreads / 64;
+constexpr uint64_t kInfBits = 0x7ff0000000000000ull;
+
+__device__ __forceinline__ uint64_t key_of(double v) {
+    uint64_t u = (uint64_t)__double_as_longlong(v);
+    u &= 0x7fffffffffffffffull;           // -0.0 orders as +0.0
+    return u > kInfBits ? kInfBits : u;   // NaN ranks as +inf
+}
+
+// Exclusive prefix count of `flag` over the block in thread order, and the
+// block total. Uses wave ballots and one LDS round.
+__device__ __forceinline__ int block_excl_prefix(bool flag, int* wave_tot, int& total) {
+    const int lane = threadIdx.x & 63;
+    const int wave = threadIdx.x >> 6;
+    const uint64_t mask = __ballot(flag);
+    const int within = __popcll(mask & ((1ull << lane) - 1ull));
+    __syncthreads();   // wave_tot may still be read by the previous call
+    if (lane == 0) wave_tot[wave] = __popcll(mask);
+    __syncthreads();
+    int before = 0;
+    total = 0;
+    for (int w = 0; w < kWaves; ++w) {
+        const int t = wave_tot[w];
+        before += (w < wave) ? t : 0;
+        total += t;
+    }
+    return before + within;
+}
+
+__global__ __launch_bounds__(kThreads) void select_topk(SelectArgs a) {
+    const int b = blockIdx.x;
+    const double* __restrict__ nrm = a.l1 + (int64_t)b * a.d_sel;
+    const double* __restrict__ sq = a.sq + (int64_t)b * a.d_sel;
+    int32_t* __restrict__ out = a.sel + (int64_t)b * a.k;
+
+    __shared__ unsigned hist[256];
+    __shared__ uint64_t s_prefix;
+    __shared__ int s_need;
+    __shared__ int wave_tot[kWaves];
+    __shared__ double red[kWaves];
+
+    uint64_t prefix = 0, mask = 0;
+    int need = a.k;   // how many still to take at or below the current prefix
+    for (int shift = 56; shift >= 0; shift -= 8) {
+        for (int i = threadIdx.x; i < 256; i += kThreads) hist[i] = 0;
+        __syncthreads();
+        for (int i = threadIdx.x; i < a.d_sel; i += kThreads) {
+            const uint64_t key = key_of(nrm[i]);
+            if ((key & mask) == prefix) atomicAdd(&hist[(key >> shift) & 0xff], 1u);
+        }
+        __syncthreads();
+        if (threadIdx.x == 0) {
+            int cum = 0, digit = 0;
+            for (int d = 255; d >= 0; --d) {
+                const int h = (int)hist[d];
+                if (cum + h >= need) {
+                    digit = d;
+                    break;
+                }
+                cum += h;
+            }
+            s_prefix = prefix | ((uint64_t)digit << shift);
+            s_need = need - cum;
+        }
+        __syncthreads();
+        prefix = s_prefix;
+        need = s_need;
+        mask |= 0xffull << shift;
+    }
+    // prefix == T (the k-th largest key); `need` of the keys equal to T go in.
+    const uint64_t T = prefix;
+    int taken = 0, ties_seen = 0;
+    double fro = 0.0;
+    for (int base = 0; base < a.d_sel; base += kThreads) {
+        const int i = base + threadIdx.x;
+        const bool valid = i < a.d_sel;
+        const uint64_t key = valid ? key_of(nrm[i]) : 0;
+        const bool eq = valid && key == T;
+        int eq_total;
+        const int eq_rank = ties_seen + block_excl_prefix(eq, wave_tot, eq_total);
+        const bool pick = valid && (key > T || (eq && eq_rank < need));
+        int pick_total;
+        const int pos = taken + block_excl_prefix(pick, wave_tot, pick_total);
+        if (pick) {
+            out[pos] = i;
+            fro += sq[i];
+        }
+        taken += pick_total;
+        ties_seen += eq_total;
+    }
+    // fixed-order reduction of the selected squared norms
+    for (int off = 32; off > 0; off >>= 1) fro += __shfl_xor(fro, off);
+    if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = fro;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        double f = 0.0;
+        for (int w = 0; w < kWaves; ++w) f += red[w];
+        a.scale[b] = 1.0 / (sqrt(f) + a.eps);
+    }
+}
+
+}  // namespace
+
+hipError_t launch_select(const SelectArgs& a, hipStream_t s) {
+    hipLaunchKernelGGL(select_topk, dim3((unsigned)a.batch), dim3(kThreads), 0, s, a);
+    return hipGetLastError();
+}
+
+}  // namespace dion2

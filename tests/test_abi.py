@@ -1,0 +1,152 @@
+"""CPU tests of the C ABI: the library loads, exports every declared symbol,
+and rejects invalid arguments before touching HIP. No compute call is made
+(these run without a GPU)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import oracle
+from paper_2512_16928_amd import binding
+from paper_2512_16928_amd.binding import (AXIS_AUTO, AXIS_COLS, AXIS_ROWS,
+                                          DION2_ERR_INVALID_ARG, DION2_ERR_UNSUPPORTED,
+                                          DION2_ERR_WORKSPACE, DION2_OK, Options)
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "dion2.h")
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(binding.LIB_PATH):
+        from paper_2512_16928_amd import build
+        build.build()
+    return binding.load()
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(dion2_[a-z_]+)\s*\(", text)))
+
+
+def test_header_and_binding_agree():
+    assert declared_functions() == sorted(binding.EXPORTED)
+
+
+def test_every_declared_symbol_is_exported(lib):
+    for name in declared_functions():
+        assert hasattr(lib, name), name
+
+
+def test_version_and_status_strings(lib):
+    assert binding.dion2_version() == 1
+    for st in (0, -1, -2, -3, -4):
+        assert binding.dion2_status_string(st).startswith("DION2_")
+    assert "unknown" in binding.dion2_status_string(7)
+
+
+def test_options_defaults(lib):
+    opt = Options()
+    lib.dion2_options_init(ctypes.byref(opt))
+    assert opt.w_dtype == binding.DTYPE_BF16 and opt.g_dtype == binding.DTYPE_BF16
+    assert abs(opt.ns_eps - 1e-7) < 1e-12
+    assert opt.decay_all == 0 and not opt.workspace and not opt.dbg_update
+    assert not opt.ns_coeffs
+
+
+FAKE = 0x10000   # a 256-aligned non-null address; never dereferenced below
+
+
+def call_step(lib, W=FAKE, M=FAKE, G=FAKE, rows=64, cols=64, alpha=0.25, mu=0.95, lr=0.02,
+              ns=5, axis=AXIS_AUTO):
+    return lib.dion2_step(W, M, G, rows, cols, alpha, mu, lr, ns, axis, None)
+
+
+@pytest.mark.parametrize("kw,msg", [
+    (dict(W=None), "NULL"), (dict(M=None), "NULL"), (dict(G=None), "NULL"),
+    (dict(rows=0), "rows"), (dict(cols=-3), "rows"),
+    (dict(alpha=0.0), "alpha"), (dict(alpha=1.5), "alpha"), (dict(alpha=float("nan")), "alpha"),
+    (dict(alpha=-0.25), "alpha"),
+    (dict(mu=float("inf")), "mu"), (dict(lr=float("nan")), "lr"),
+    (dict(ns=-1), "ns_steps"), (dict(ns=17), "ns_steps"),
+    (dict(axis=2), "axis"), (dict(axis=-2), "axis"),
+    (dict(W=FAKE + 8), "aligned"), (dict(G=FAKE + 2), "aligned"),
+])
+def test_invalid_arguments_rejected(lib, kw, msg):
+    assert call_step(lib, **kw) == DION2_ERR_INVALID_ARG
+    assert msg in binding.dion2_last_error()
+
+
+def test_unsupported_sizes(lib):
+    assert call_step(lib, rows=1 << 21, cols=8) == DION2_ERR_UNSUPPORTED
+    assert call_step(lib, rows=65536, cols=65536) == DION2_ERR_UNSUPPORTED
+
+
+def test_strided_and_batched_validation(lib):
+    st = lib.dion2_step_strided(FAKE, FAKE, FAKE, 0, 64, 64, 0.25, 0.95, 0.02, 5, -1, None)
+    assert st == DION2_ERR_INVALID_ARG and "batch" in binding.dion2_last_error()
+    st = lib.dion2_step_strided(FAKE, FAKE, FAKE, 70000, 64, 64, 0.25, 0.95, 0.02, 5, -1, None)
+    assert st == DION2_ERR_INVALID_ARG
+    arr = ctypes.c_void_p * 2
+    good, bad = arr(FAKE, FAKE), arr(FAKE, None)
+    st = lib.dion2_step_batched(good, good, bad, 2, 64, 64, 0.25, 0.95, 0.02, 5, -1, None)
+    assert st == DION2_ERR_INVALID_ARG and "matrix 1" in binding.dion2_last_error()
+    st = lib.dion2_step_batched(None, good, good, 2, 64, 64, 0.25, 0.95, 0.02, 5, -1, None)
+    assert st == DION2_ERR_INVALID_ARG
+
+
+def test_ex_options_validation(lib):
+    def ex(**o):
+        opt = Options()
+        lib.dion2_options_init(ctypes.byref(opt))
+        for k, v in o.items():
+            setattr(opt, k, v)
+        return lib.dion2_step_ex(FAKE, FAKE, FAKE, 1, 64, 64, 0.25, 0.95, 0.02, 2, -1,
+                                 ctypes.byref(opt), None)
+    assert ex(w_dtype=5) == DION2_ERR_INVALID_ARG
+    assert ex(g_dtype=-1) == DION2_ERR_INVALID_ARG
+    assert ex(ns_eps=-1.0) == DION2_ERR_INVALID_ARG
+    assert ex(decay_all=3) == DION2_ERR_INVALID_ARG
+    coeffs = (ctypes.c_float * 6)(1.0, 2.0, 3.0, 1.0, float("inf"), 0.0)
+    assert ex(ns_coeffs=ctypes.cast(coeffs, ctypes.POINTER(ctypes.c_float))) == DION2_ERR_INVALID_ARG
+    need = binding.dion2_workspace_size(1, 64, 64, 0.25)
+    assert ex(workspace=FAKE, workspace_bytes=need - 1) == DION2_ERR_WORKSPACE
+    assert ex(workspace=FAKE + 16, workspace_bytes=need) == DION2_ERR_INVALID_ARG
+
+
+@pytest.mark.parametrize("rows,cols,alpha,axis", [
+    (256, 256, 0.25, AXIS_AUTO), (2048, 8192, 0.25, AXIS_AUTO), (8192, 2048, 0.5, AXIS_AUTO),
+    (2048, 8192, 0.25, AXIS_COLS), (11008, 4096, 0.125, AXIS_AUTO), (2048, 1408, 0.25, AXIS_AUTO),
+    (1408, 2048, 0.25, AXIS_AUTO), (7, 5, 0.1, AXIS_AUTO), (100, 37, 1e-4, AXIS_ROWS),
+    (300, 300, 1.0, AXIS_COLS), (1000, 3, 0.3, AXIS_AUTO),
+])
+def test_plan_matches_oracle_reading(lib, rows, cols, alpha, axis):
+    k, ax = binding.dion2_plan_info(rows, cols, alpha, axis)
+    ax_o = oracle.resolve_axis(rows, cols, axis)
+    assert ax == ax_o
+    assert k == oracle.num_selected(alpha, rows if ax_o == AXIS_ROWS else cols)
+
+
+def test_workspace_size(lib):
+    assert binding.dion2_workspace_size(0, 64, 64, 0.25) == 0
+    assert binding.dion2_workspace_size(1, 64, 64, 2.0) == 0
+    a = binding.dion2_workspace_size(1, 2048, 2048, 0.25)
+    b = binding.dion2_workspace_size(2, 2048, 2048, 0.25)
+    c = binding.dion2_workspace_size(1, 2048, 2048, 1.0)
+    assert 0 < a < b and a < c
+    assert a % 256 == 0
+    # compact buffers dominate: four bf16 copies of k x d_oth plus one fp32
+    assert a >= 512 * 2048 * (4 * 2 + 4)
+
+
+def test_status_codes_match_header():
+    text = open(HEADER).read()
+    for name, val in (("DION2_OK", DION2_OK), ("DION2_ERR_INVALID_ARG", DION2_ERR_INVALID_ARG),
+                      ("DION2_ERR_UNSUPPORTED", DION2_ERR_UNSUPPORTED),
+                      ("DION2_ERR_WORKSPACE", DION2_ERR_WORKSPACE)):
+        assert re.search(rf"{name}\s*=\s*{val}\b", text), name
+    for name, val in (("DION2_AXIS_AUTO", AXIS_AUTO), ("DION2_AXIS_ROWS", AXIS_ROWS),
+                      ("DION2_AXIS_COLS", AXIS_COLS)):
+        assert re.search(rf"{name}\s*=\s*{val}\b", text), name
