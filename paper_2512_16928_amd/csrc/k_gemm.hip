@@ -60,48 +60,57 @@ __global__ __launch_bounds__(kThreads, 2) void gemm_nt(GemmArgs a) {
     const int lane = tid & 63, wave = tid >> 6;
     const int wm = wave >> 1, wn = wave & 1;
 
-    // operand sources for this block: tiles 0..NTILE-1 are
-    // NPASS==1: {A0 rows, B0 rows};  NPASS==3: {A0, A1, B0, B1}
-    const uint16_t* src[C::NTILE];
-    int ld[C::NTILE];
+    // Operand tiles of this block: NPASS==1 {A0, B0}; NPASS==3 {A0, A1, B0, B1}.
+    // Every thread stages eight 16-byte chunks per K-slice (NTILE * PER_T == 8),
+    // held in eight named registers so none of them can live in scratch.
+    static_assert(C::NTILE * C::PER_T == 8, "eight staged chunks per thread");
+    const uint16_t* tsrc[4];
+    int tld[4];
+    tsrc[0] = a.A0 + (int64_t)b * a.sA + (int64_t)row0 * a.lda;
+    tld[0] = a.lda;
     if constexpr (NPASS == 1) {
-        src[0] = a.A0 + (int64_t)b * a.sA + (int64_t)row0 * a.lda;
-        src[1] = a.B0 + (int64_t)b * a.sB + (int64_t)col0 * a.ldb;
-        ld[0] = a.lda;
-        ld[1] = a.ldb;
+        tsrc[1] = a.B0 + (int64_t)b * a.sB + (int64_t)col0 * a.ldb;
+        tld[1] = a.ldb;
+        tsrc[2] = tsrc[3] = nullptr;
+        tld[2] = tld[3] = 0;
     } else {
-        src[0] = a.A0 + (int64_t)b * a.sA + (int64_t)row0 * a.lda;
-        src[1] = a.A1 + (int64_t)b * a.sA + (int64_t)row0 * a.lda;
-        src[2] = a.B0 + (int64_t)b * a.sB + (int64_t)col0 * a.ldb;
-        src[3] = a.B1 + (int64_t)b * a.sB + (int64_t)col0 * a.ldb;
-        ld[0] = ld[1] = a.lda;
-        ld[2] = ld[3] = a.ldb;
+        tsrc[1] = a.A1 + (int64_t)b * a.sA + (int64_t)row0 * a.lda;
+        tsrc[2] = a.B0 + (int64_t)b * a.sB + (int64_t)col0 * a.ldb;
+        tsrc[3] = a.B1 + (int64_t)b * a.sB + (int64_t)col0 * a.ldb;
+        tld[1] = a.lda;
+        tld[2] = tld[3] = a.ldb;
     }
-
-    uint4 regs[C::NTILE][C::PER_T];
-    auto gload = [&](int k0) {
-#pragma unroll
-        for (int t = 0; t < C::NTILE; ++t) {
-#pragma unroll
-            for (int i = 0; i < C::PER_T; ++i) {
-                const int c = tid + i * kThreads;
-                const int r = c / C::CPR, kc = c % C::CPR;
-                regs[t][i] = *reinterpret_cast<const uint4*>(src[t] + (int64_t)r * ld[t] + k0 + kc * 8);
-            }
-        }
-    };
-    auto sstore = [&](int buf) {
-#pragma unroll
-        for (int t = 0; t < C::NTILE; ++t) {
-#pragma unroll
-            for (int i = 0; i < C::PER_T; ++i) {
-                const int c = tid + i * kThreads;
-                const int r = c / C::CPR, kc = c % C::CPR;
-                *reinterpret_cast<uint4*>(smem + buf * C::STAGE + t * C::TILE + r * C::LDK + kc * 8) =
-                    regs[t][i];
-            }
-        }
-    };
+#define DION2_CHUNK_PTR(I)                                                              \
+    const uint16_t* gp##I;                                                              \
+    int so##I;                                                                          \
+    {                                                                                   \
+        constexpr int t = (I) / C::PER_T, i = (I) % C::PER_T;                           \
+        const int c = tid + i * kThreads;                                               \
+        gp##I = tsrc[t] + (int64_t)(c / C::CPR) * tld[t] + (c % C::CPR) * 8;            \
+        so##I = t * C::TILE + (c / C::CPR) * C::LDK + (c % C::CPR) * 8;                 \
+    }
+    DION2_CHUNK_PTR(0) DION2_CHUNK_PTR(1) DION2_CHUNK_PTR(2) DION2_CHUNK_PTR(3)
+    DION2_CHUNK_PTR(4) DION2_CHUNK_PTR(5) DION2_CHUNK_PTR(6) DION2_CHUNK_PTR(7)
+#undef DION2_CHUNK_PTR
+    uint4 r0, r1, r2, r3, r4, r5, r6, r7;
+#define DION2_GLOAD(K0)                                                                 \
+    r0 = *reinterpret_cast<const uint4*>(gp0 + (K0));                                   \
+    r1 = *reinterpret_cast<const uint4*>(gp1 + (K0));                                   \
+    r2 = *reinterpret_cast<const uint4*>(gp2 + (K0));                                   \
+    r3 = *reinterpret_cast<const uint4*>(gp3 + (K0));                                   \
+    r4 = *reinterpret_cast<const uint4*>(gp4 + (K0));                                   \
+    r5 = *reinterpret_cast<const uint4*>(gp5 + (K0));                                   \
+    r6 = *reinterpret_cast<const uint4*>(gp6 + (K0));                                   \
+    r7 = *reinterpret_cast<const uint4*>(gp7 + (K0));
+#define DION2_SSTORE(BASE)                                                              \
+    *reinterpret_cast<uint4*>((BASE) + so0) = r0;                                       \
+    *reinterpret_cast<uint4*>((BASE) + so1) = r1;                                       \
+    *reinterpret_cast<uint4*>((BASE) + so2) = r2;                                       \
+    *reinterpret_cast<uint4*>((BASE) + so3) = r3;                                       \
+    *reinterpret_cast<uint4*>((BASE) + so4) = r4;                                       \
+    *reinterpret_cast<uint4*>((BASE) + so5) = r5;                                       \
+    *reinterpret_cast<uint4*>((BASE) + so6) = r6;                                       \
+    *reinterpret_cast<uint4*>((BASE) + so7) = r7;
 
     f32x16 acc[2][2];
 #pragma unroll
@@ -112,14 +121,19 @@ __global__ __launch_bounds__(kThreads, 2) void gemm_nt(GemmArgs a) {
             for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
     const int nk = a.K / C::BK;
-    gload(0);
-    sstore(0);
+    DION2_GLOAD(0)
+    DION2_SSTORE(smem)
     __syncthreads();
     const int arow = wm * 64 + (lane & 31);
     const int brow = wn * 64 + (lane & 31);
     const int kl = 8 * (lane >> 5);
     for (int kt = 0; kt < nk; ++kt) {
-        if (kt + 1 < nk) gload((kt + 1) * C::BK);
+        // next K-slice (the last iteration re-reads the current one, which is
+        // in bounds, and stages it into the idle buffer)
+        const int k0 = (kt + 1 < nk ? kt + 1 : kt) * C::BK;
+        DION2_GLOAD(k0)
+        // keep the prefetch ahead of the MFMAs so its latency overlaps them
+        __builtin_amdgcn_sched_barrier(0);
         const uint16_t* st = smem + (kt & 1) * C::STAGE;
 #pragma unroll
         for (int kk = 0; kk < C::BK / 16; ++kk) {
@@ -159,9 +173,15 @@ __global__ __launch_bounds__(kThreads, 2) void gemm_nt(GemmArgs a) {
                     }
             }
         }
-        if (kt + 1 < nk) sstore((kt + 1) & 1);
+        __builtin_amdgcn_sched_barrier(0);
+        {
+            uint16_t* dst = smem + ((kt + 1) & 1) * C::STAGE;
+            DION2_SSTORE(dst)
+        }
         __syncthreads();
     }
+#undef DION2_GLOAD
+#undef DION2_SSTORE
 
     // ---- epilogue: stage the fp32 tile in LDS
     float* Cs = reinterpret_cast<float*>(smem_raw);
