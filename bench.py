@@ -154,12 +154,15 @@ def main(argv=None):
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-profile", action="store_true", help="skip the per-kernel event pass")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="also run plain 1 GiB device copies, the reference dispatches that "
+                         "scale HBM byte counters (FETCH_SIZE / WRITE_SIZE) in a profiler run")
     args = ap.parse_args(argv)
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py measures the Dion2 step on one GPU only; this build has no multi-GPU "
-              "path (every matrix is independent, see the sharding notes in DESIGN.md).",
-              file=sys.stderr)
+        print("bench.py measures the Dion2 step on one GPU only: there is no multi-GPU path "
+              "(every matrix's step is independent, so several GPUs would each own whole "
+              "shape groups); run it without --gpus or with --gpus 1.", file=sys.stderr)
         return 2
     if not torch.cuda.is_available():
         print("bench.py needs a HIP device", file=sys.stderr)
@@ -168,6 +171,15 @@ def main(argv=None):
         from paper_2512_16928_amd import build
         build.build()
     binding.load()
+
+    if args.copy_calibration:
+        src = torch.empty(1 << 28, dtype=torch.float32, device="cuda:0").fill_(1.0)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
+        log("[bench] ran 3 plain copies of 1 GiB (counter calibration)")
 
     wl = workloads.WORKLOADS[args.workload]
     alpha = args.alpha if args.alpha is not None else wl.alphas[0]

@@ -59,7 +59,7 @@ struct Plan {
     int batch;
     int nrb, rb_rows;         // column-mode reduction blocking
     // workspace offsets
-    size_t o_l1, o_sq, o_part, o_sel, o_scale, o_L[2], o_LT[2], o_Ahi, o_Alo, o_B, o_O,
+    size_t o_l1, o_sq, o_part, o_sel, o_scale, o_L, o_LT, o_Z1, o_Ahi, o_Alo, o_B, o_O,
         o_tables, total;
 };
 
@@ -105,10 +105,9 @@ int make_plan(int batch, int64_t rows, int64_t cols, float alpha, int axis, Plan
     P.o_sel = take(B * P.k * 4);
     P.o_scale = take(B * 8);
     const size_t comp = B * (size_t)P.kpad * (size_t)P.opad * 2;
-    P.o_L[0] = take(comp);
-    P.o_L[1] = take(comp);
-    P.o_LT[0] = take(comp);
-    P.o_LT[1] = take(comp);
+    P.o_L = take(comp);
+    P.o_LT = take(comp);
+    P.o_Z1 = take(comp);
     const size_t gram = B * (size_t)P.s_pad * (size_t)P.s_pad * 2;
     P.o_Ahi = take(gram);
     P.o_Alo = take(gram);
@@ -321,8 +320,9 @@ int run_step(const Plan& P, void* W, float* M, const void* G, const Tables* tabs
     double* sq = reinterpret_cast<double*>(ws + P.o_sq);
     int32_t* sel = reinterpret_cast<int32_t*>(ws + P.o_sel);
     double* scale = reinterpret_cast<double*>(ws + P.o_scale);
-    uint16_t* L[2] = {reinterpret_cast<uint16_t*>(ws + P.o_L[0]), reinterpret_cast<uint16_t*>(ws + P.o_L[1])};
-    uint16_t* LT[2] = {reinterpret_cast<uint16_t*>(ws + P.o_LT[0]), reinterpret_cast<uint16_t*>(ws + P.o_LT[1])};
+    uint16_t* L = reinterpret_cast<uint16_t*>(ws + P.o_L);
+    uint16_t* LT = reinterpret_cast<uint16_t*>(ws + P.o_LT);
+    uint16_t* Z1 = reinterpret_cast<uint16_t*>(ws + P.o_Z1);
     uint16_t* Ahi = reinterpret_cast<uint16_t*>(ws + P.o_Ahi);
     uint16_t* Alo = reinterpret_cast<uint16_t*>(ws + P.o_Alo);
     uint16_t* Bm = reinterpret_cast<uint16_t*>(ws + P.o_B);
@@ -376,8 +376,8 @@ int run_step(const Plan& P, void* W, float* M, const void* G, const Tables* tabs
     ga.scale = scale;
     ga.mu = mu;
     ga.decay = opt.decay_all ? 0 : 1;
-    ga.L = L[0];
-    ga.LT = LT[0];
+    ga.L = L;
+    ga.LT = LT;
     ga.O = ns_steps == 0 ? O : nullptr;
     e = timed(DION2_PHASE_GATHER, sel_el * 8.0, 1, stream,
               [&] { return launch_gather(ga, P.axis, stream); });
@@ -393,17 +393,18 @@ int run_step(const Plan& P, void* W, float* M, const void* G, const Tables* tabs
     const double l_r = (double)(P.k < P.d_oth ? P.d_oth : P.k);
     const int64_t sZ = P.s_pad * P.l_pad;
     const int64_t sA = P.s_pad * P.s_pad;
+    // Z is the wide orientation of the compact matrix; the iteration
+    // ping-pongs it between its gather buffer and Z1.
+    uint16_t* zbuf[2] = {P.z_is_L ? L : LT, Z1};
     int cur = 0;
     for (int t = 0; t < ns_steps; ++t) {
         const float* cf = opt.ns_coeffs ? opt.ns_coeffs + 3 * t : kMuonQuintic;
-        uint16_t* Z = P.z_is_L ? L[cur] : LT[cur];
-        uint16_t* ZT = P.z_is_L ? LT[cur] : L[cur];
-        uint16_t* Zn = P.z_is_L ? L[1 - cur] : LT[1 - cur];
-        uint16_t* ZTn = P.z_is_L ? LT[1 - cur] : L[1 - cur];
+        uint16_t* Z = zbuf[cur];
+        uint16_t* Zn = zbuf[1 - cur];
 
+        // A = Z Z^T, split into bf16 hi + lo
         GemmArgs g{};
         g.batch = P.batch;
-        // A = Z Z^T, split into bf16 hi + lo
         g.A0 = Z;
         g.B0 = Z;
         g.sA = g.sB = sZ;
@@ -441,18 +442,18 @@ int run_step(const Plan& P, void* W, float* M, const void* G, const Tables* tabs
                   [&] { return launch_gemm(q, EPI_POLY, stream); });
         if (e != hipSuccess) return hip_fail(e, "launch K4 polynomial");
 
-        // Z' = a Z + B Z  (B operand = rows of Z^T)
+        // Z' = a Z + B Z (B operand: Z itself, [K = s][N = l]; a Z in the epilogue)
         GemmArgs x{};
         x.batch = P.batch;
         x.A0 = Bm;
-        x.B0 = ZT;
+        x.B0 = Z;
         x.sA = sA;
         x.sB = sZ;
         x.M = (int)P.s_pad;
         x.N = (int)P.l_pad;
         x.K = (int)P.s_pad;
         x.lda = (int)P.s_pad;
-        x.ldb = (int)P.s_pad;
+        x.ldb = (int)P.l_pad;
         x.ca = cf[0];
         x.E0 = Z;
         x.sE = sZ;
@@ -461,11 +462,8 @@ int run_step(const Plan& P, void* W, float* M, const void* G, const Tables* tabs
             x.out0 = Zn;
             x.sOut0 = sZ;
             x.ldo0 = (int)P.l_pad;
-            x.out1 = ZTn;
-            x.sOut1 = sZ;
-            x.ldo1 = (int)P.s_pad;
             e = timed(DION2_PHASE_NS_UPDATE, 2.0 * s_r * s_r * l_r * P.batch, 1, stream,
-                      [&] { return launch_gemm(x, EPI_AXPY, stream); });
+                      [&] { return launch_gemm(x, EPI_UPDATE, stream); });
         } else {
             // O in the L layout [kpad][opad]
             x.out0 = O;

@@ -6,7 +6,8 @@
 //   d_sel lines exist, each of length d_oth.
 //   Compact submatrix L  : [kpad][opad] bf16, row p = selected line K[p]
 //                           scaled by 1 / (||M[K]||_F + eps), zero padding.
-//   Its transpose     LT : [opad][kpad] bf16.
+//   Its transpose     LT : [opad][kpad] bf16. Newton-Schulz iterates on the
+//                           wide one of the two (L when k <= d_oth).
 //   kpad, opad are k and d_oth rounded up to the GEMM tile (128); every
 //   padded entry is zero, which the Newton-Schulz polynomial keeps at zero.
 #pragma once
@@ -151,17 +152,21 @@ struct DecayAllArgs {
 };
 hipError_t launch_decay_all(const DecayAllArgs& a, hipStream_t s);
 
-// Newton-Schulz GEMMs (NT: C[i][j] = sum_k A[i][k] * B[j][k]).
-enum GemmEpi { EPI_SPLIT = 0, EPI_POLY = 1, EPI_AXPY = 2, EPI_FINAL = 3 };
+// Newton-Schulz GEMMs, C = A B with A given as rows [M][K]:
+//   EPI_SPLIT  (B as rows [N][K]): out0 = bf16(C), out1 = bf16(C - out0)
+//   EPI_POLY   (B as rows [N][K], three passes hi/lo): out0 = bf16(cb (E0 + E1) + cc C)
+//   EPI_UPDATE (B as [K][N]): out0 = bf16(ca E0 + C)
+//   EPI_FINAL  (B as [K][N]): out0 = ca E0 + C in fp32, or its transpose when out_transposed
+enum GemmEpi { EPI_SPLIT = 0, EPI_POLY = 1, EPI_UPDATE = 2, EPI_FINAL = 3 };
 struct GemmArgs {
     const uint16_t* A0; const uint16_t* A1;   // A operand(s), [M][K] ld lda
-    const uint16_t* B0; const uint16_t* B1;   // B operand(s), [N][K] ld ldb
+    const uint16_t* B0; const uint16_t* B1;   // B operand(s), [N][K] or [K][N], ld ldb
     int64_t sA, sB;                           // batch strides (elements)
     int M, N, K, lda, ldb;
     int batch;
     float ca, cb, cc;                         // polynomial coefficients
     // epilogue inputs / outputs (batch stride in elements, ld in elements)
-    const uint16_t* E0; const uint16_t* E1; int64_t sE; int lde;  // Ahi/Alo or Z
+    const uint16_t* E0; const uint16_t* E1; int64_t sE; int lde;  // A hi / lo, or Z
     void* out0; int64_t sOut0; int ldo0;
     void* out1; int64_t sOut1; int ldo1;
     int out_transposed;                        // EPI_FINAL: write out0[j][i]
