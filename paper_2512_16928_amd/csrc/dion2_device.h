@@ -49,12 +49,10 @@ __device__ __forceinline__ float bf16_bits_to_f32(uint32_t h) {
     return __uint_as_float(h << 16);
 }
 
-// fp32 -> bf16, round to nearest even; NaN stays a (quiet) NaN.
+// fp32 -> bf16, round to nearest even (gfx950's v_cvt_pk_bf16_f32); NaN
+// stays a quiet NaN.
 __device__ __forceinline__ uint16_t f32_to_bf16(float f) {
-    uint32_t u = __float_as_uint(f);
-    if ((u & 0x7fffffffu) > 0x7f800000u) return (uint16_t)((u >> 16) | 0x40u);
-    u += 0x7fffu + ((u >> 16) & 1u);
-    return (uint16_t)(u >> 16);
+    return __builtin_bit_cast(uint16_t, (__bf16)f);
 }
 
 // fp64 -> bf16 with a single round-to-nearest-even: first to fp32 with

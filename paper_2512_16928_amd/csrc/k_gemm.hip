@@ -1,10 +1,10 @@
 // K4: the Newton-Schulz GEMMs on MFMA (bf16 operands, fp32 accumulation).
 //
 // One Newton-Schulz step on the wide compact matrix Z (s x l, s <= l) is
-//   A  = Z Z^T                     gemm<1, BT=0, EPI_SPLIT>   A kept as bf16 hi + lo
-//   B  = b A + c A^2               gemm<3, BT=0, EPI_POLY>    A^2 = A A^T from three
-//                                                             passes hi*hi+hi*lo+lo*hi
-//   Z' = a Z + B Z                 gemm<1, BT=1, EPI_UPDATE | EPI_FINAL>
+//   A  = Z Z^T                     gemm<1, EPI_SPLIT>, B as rows  A kept as bf16 hi + lo
+//   B  = b A + c A^2               gemm<3, EPI_POLY>, B as rows   A^2 = A A^T from three
+//                                                                 passes hi*hi+hi*lo+lo*hi
+//   Z' = a Z + B Z                 gemm<1, EPI_UPDATE | EPI_FINAL>, B operand = Z as [K][N]
 // The a Z term is added in fp32 in the epilogue rather than folded into the
 // diagonal of B: with it separate, lines of Z that are exactly equal stay
 // exactly equal through every step (their rows of A, B and Z' come from
@@ -15,19 +15,26 @@
 // with K contiguous. The B operand is given either as rows with K
 // contiguous (BT = 0: Z Z^T reads Z twice, A^2 reads A, which is symmetric)
 // or as a row-major [K][N] matrix (BT = 1: the update reads Z itself). For
-// BT = 1 the K-slice of Z is staged in LDS as is and the MFMA fragments are
-// read with gfx950's transposing LDS read (ds_read_b64_tr_b16): a lane of
-// a 16-lane group receives element (i mod 4) of the 8 bytes addressed by
-// source lane 4e + i/4 for e = 0..3, so pointing source lane s at row s/4,
-// column 4 (s mod 4) hands lane i four consecutive K values of column i.
+// BT = 1 the MFMA fragments are read with gfx950's transposing LDS read
+// (ds_read_b64_tr_b16): a lane of a 16-lane group receives element (i mod 4)
+// of the 8 bytes addressed by source lane 4e + i/4 for e = 0..3, so pointing
+// source lane s at row s/4, column 4 (s mod 4) hands lane i four
+// consecutive K values of column i.
 //
 // Tiling for gfx950: a BM x BN output tile per block of WM x WN wave64s,
 // each wave a (BM/WM) x (BN/WN) tile of v_mfma_f32_32x32x16_bf16 blocks.
-// Operand K-slices (BK deep) are staged through LDS, double-buffered; the
-// next slice is fetched into named registers before the current slice's
-// MFMAs so its latency overlaps them. Tiles are numbered XCD-aware. The
-// epilogue goes through a per-wave 32 x 32 LDS tile so row-major and
-// transposed outputs are both written as 16-byte chunks.
+// K-slices (BK deep) go from global memory straight into an S-stage LDS
+// ring with global_load_lds_dwordx4 (each lane's 16 bytes land at the
+// wave's LDS base + 16 * lane), S - 1 slices ahead of the MFMAs, so no
+// registers stage the operands and a slice's load latency is covered by
+// S - 2 slices of compute. Tiles are stored unpadded with an XOR swizzle of
+// their 16-byte chunks, chosen so both the fragment reads (ds_read_b128)
+// and the transposing reads hit distinct LDS banks; each lane fetches the
+// global chunk that belongs in its LDS slot. Tiles are numbered XCD-aware;
+// the symmetric products (A and B) compute only the tiles on and above the
+// diagonal and write each one twice. The epilogue goes through a per-wave
+// 32 x 32 LDS tile so row-major and transposed outputs are both written as
+// 16-byte chunks.
 //
 // All dimensions are multiples of the tile (compact buffers are zero padded
 // to 128, and the padding stays zero through every step).
@@ -41,102 +48,169 @@ constexpr int kXcds = 8;   // accelerator complex dies on MI355X
 typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8;
 typedef __attribute__((ext_vector_type(4))) short i16x4;
 typedef __attribute__((ext_vector_type(16))) float f32x16;
+typedef __attribute__((address_space(3))) void lds_void;
 
+// two fp32 -> packed bf16 pair (RNE), one v_cvt_pk_bf16_f32
 __device__ __forceinline__ uint32_t pack2(float x, float y) {
-    return (uint32_t)f32_to_bf16(x) | ((uint32_t)f32_to_bf16(y) << 16);
+    typedef __attribute__((ext_vector_type(2))) __bf16 bf16x2;
+    const bf16x2 v = {(__bf16)x, (__bf16)y};
+    return __builtin_bit_cast(uint32_t, v);
 }
 
-template <int NPASS, int BT_, int BM_, int BN_, int BK_, int WM_, int WN_>
+template <int NPASS, int BT_, int BM_, int BN_, int BK_, int WM_, int WN_, int S_>
 struct Tile {
-    static constexpr int BT = BT_;
+    static constexpr int BT = BT_, S = S_;
     static constexpr int BM = BM_, BN = BN_, BK = BK_, WM = WM_, WN = WN_;
-    static constexpr int THREADS = 64 * WM * WN;
+    static constexpr int WAVES = WM * WN;
+    static constexpr int THREADS = 64 * WAVES;
     static constexpr int TM = BM / WM, TN = BN / WN;     // wave tile
     static constexpr int FM = TM / 32, FN = TN / 32;     // MFMA blocks per wave
     static constexpr int NA = NPASS == 1 ? 1 : 2;        // A operand tiles (hi[, lo])
     static constexpr int NB = NPASS == 1 ? 1 : 2;        // B operand tiles
-    static constexpr int LDK = BK + 8;                   // padded K-major LDS row (bf16)
-    static constexpr int LDN = BN + 16;                  // padded N-major LDS row (BT = 1)
-    static constexpr int CPR = BK / 8;                   // 16-byte chunks per K-major row
-    static constexpr int A_CH = BM * CPR, B_CH = BN * CPR;
-    static constexpr int NCH = (NA * A_CH + NB * B_CH) / THREADS;  // chunks per thread
-    static constexpr int A_TILE = BM * LDK;
-    static constexpr int B_TILE = BT ? BK * LDN : BN * LDK;
-    static constexpr int STAGE = NA * A_TILE + NB * B_TILE;        // elements
+    // K-major tiles: rows of BK bf16 (pitch PK bytes), CPR chunks of 16 B
+    static constexpr int PK = BK * 2;
+    static constexpr int CPR = BK / 8;
+    static constexpr int GK = 256 / PK;                  // rows sharing one bank sweep
+    // N-major tile (BT = 1): rows of BN bf16 (pitch PN bytes)
+    static constexpr int PN = BN * 2;
+    static constexpr int A_BYTES = BM * PK;
+    static constexpr int B_BYTES = BN * PK;              // same size either layout
+    static constexpr int STAGE_BYTES = NA * A_BYTES + NB * B_BYTES;
+    static constexpr int STAGE_INSTS = STAGE_BYTES / 1024;   // 1 KB per wave instruction
+    static constexpr int IPW = STAGE_INSTS / WAVES;      // load instructions per wave per slice
     static constexpr int EPI_LD = 33;                    // fp32 staging row (32 + 1)
-    static constexpr int EPI_BYTES = WM * WN * 32 * EPI_LD * 4;
-    static constexpr int SMEM = (2 * STAGE * 2 > EPI_BYTES) ? 2 * STAGE * 2 : EPI_BYTES;
+    static constexpr int EPI_BYTES = WAVES * 32 * EPI_LD * 4;
+    static constexpr int SMEM = (S * STAGE_BYTES > EPI_BYTES) ? S * STAGE_BYTES : EPI_BYTES;
     static_assert(TM % 32 == 0 && TN % 32 == 0, "wave tile is whole 32x32 blocks");
-    static_assert(A_CH % THREADS == 0 && B_CH % THREADS == 0, "chunks split evenly");
-    static_assert(NCH >= 1 && NCH <= 16, "at most 16 staged chunks per thread");
-    static_assert(BK % 16 == 0, "BK is a multiple of the MFMA K");
-    static_assert(!BT || NPASS == 1, "the transposed B operand is single-pass");
+    static_assert(BK % 16 == 0 && (BK == 32 || BK == 64), "BK of 32 or 64");
+    static_assert(A_BYTES % 1024 == 0 && B_BYTES % 1024 == 0, "tiles are whole 1 KB blocks");
+    static_assert(STAGE_INSTS % WAVES == 0, "load instructions split evenly over waves");
+    static_assert(!BT || (NPASS == 1 && BN == 128), "the [K][N] B operand is single-pass, BN 128");
+    static_assert(S >= 2 && S <= 4, "two to four stages");
 };
 
-// Tile and in-tile position of a thread's I-th staged chunk. Chunks run over
-// the A tiles, then the B tiles; every chunk index I maps all threads of the
-// block into one tile (the tiles are whole multiples of the block size).
-template <typename T, int I>
-struct Chunk {
-    static constexpr int flat0 = I * T::THREADS;
-    static constexpr bool is_a = flat0 < T::NA * T::A_CH;
-    static constexpr int tile = is_a ? flat0 / T::A_CH : (flat0 - T::NA * T::A_CH) / T::B_CH;
-    static constexpr int within0 = is_a ? flat0 % T::A_CH : (flat0 - T::NA * T::A_CH) % T::B_CH;
-    static constexpr int lds_base = is_a ? tile * T::A_TILE : T::NA * T::A_TILE + tile * T::B_TILE;
-};
-
-// B fragment (8 consecutive K of one column) through two transposing reads.
-// `col` is the fragment's first column in the staged [BK][LDN] tile.
+// Byte offset, inside a K-major tile, of logical 16-byte chunk c of row r.
 template <typename T>
-__device__ __forceinline__ bf16x8 b_frag_tr(const uint16_t* sb, int krow, int col, int lane) {
+__device__ __forceinline__ int kmajor_off(int r, int c) {
+    return r * T::PK + 16 * (c ^ ((r / T::GK) % T::CPR));
+}
+// Byte offset, inside the [BK][BN] tile, of logical 16-byte chunk c of row r.
+__device__ __forceinline__ int nmajor_off(int r, int c) {
+    return r * 256 + 16 * (c ^ ((r & 3) << 2));
+}
+
+// Issue the direct-to-LDS loads of K-slice `kt` into the stage at `dst`.
+// Wave w owns the stage's 1 KB blocks w, w + WAVES, ...; lane i of a block
+// fills the block's 16-byte slot i with the global chunk that belongs there.
+template <int NPASS, typename T>
+__device__ __forceinline__ void load_slice(const GemmArgs& a, unsigned char* dst, int kt,
+                                           const uint16_t* const (&abase)[2],
+                                           const uint16_t* const (&bbase)[2], int wave, int lane) {
+#pragma unroll
+    for (int q = 0; q < T::IPW; ++q) {
+        const int blk = wave + q * T::WAVES;   // 1 KB block of the stage (wave-uniform)
+        const uint16_t* src;
+        if (blk * 1024 < T::NA * T::A_BYTES) {
+            // K-major A tile: the block holds 1024 / PK whole rows
+            const int t = (blk * 1024) / T::A_BYTES;
+            const int lb = (blk * 1024) % T::A_BYTES + lane * 16;
+            const int r = lb / T::PK, slot = (lb % T::PK) / 16;
+            const int c = slot ^ ((r / T::GK) % T::CPR);
+            src = (t ? abase[1] : abase[0]) + (int64_t)r * a.lda + (int64_t)kt * T::BK + c * 8;
+        } else {
+            const int bb = blk * 1024 - T::NA * T::A_BYTES;
+            const int t = bb / T::B_BYTES;
+            const int lb = bb % T::B_BYTES + lane * 16;
+            if constexpr (T::BT) {
+                const int r = lb / 256, slot = (lb % 256) / 16;
+                const int c = slot ^ ((r & 3) << 2);
+                src = bbase[0] + ((int64_t)kt * T::BK + r) * a.ldb + c * 8;
+            } else {
+                const int r = lb / T::PK, slot = (lb % T::PK) / 16;
+                const int c = slot ^ ((r / T::GK) % T::CPR);
+                src = (t ? bbase[1] : bbase[0]) + (int64_t)r * a.ldb + (int64_t)kt * T::BK + c * 8;
+            }
+        }
+        __builtin_amdgcn_global_load_lds(src, (lds_void*)(dst + blk * 1024), 16, 0, 0);
+    }
+}
+
+// Wait until at most N vector-memory loads of this wave are outstanding
+// (vmcnt only; lgkmcnt and expcnt left at their maxima).
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+    static_assert(N >= 0 && N < 64, "vmcnt range");
+    __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+
+// B fragment (8 consecutive K of one column) from the [BK][BN] tile through
+// two transposing reads; `col` is the fragment's first column.
+template <typename T>
+__device__ __forceinline__ bf16x8 b_frag_tr(const unsigned char* sb, int krow, int col, int lane) {
     const int g = lane >> 4, s = lane & 15;
     const int row = krow + 8 * (g >> 1) + (s >> 2);
     const int c = col + 16 * (g & 1) + 4 * (s & 3);
     typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
-    const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(sb + row * T::LDN + c));
-    const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(sb + (row + 4) * T::LDN + c));
+    const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+        (lds_i16x4*)(sb + nmajor_off(row, c >> 3) + 2 * (c & 7)));
+    const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+        (lds_i16x4*)(sb + nmajor_off(row + 4, c >> 3) + 2 * (c & 7)));
     typedef __attribute__((ext_vector_type(8))) short i16x8;
     const i16x8 v = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
     return __builtin_bit_cast(bf16x8, v);
 }
 
+// Transposed read of a wave's 32 x 32 staging tile: the lane's 16 values v
+// (row er, columns ec..ec+15) are stored back, and t receives row er of the
+// transpose (entries (ec + q, er) of the block).
+template <typename T>
+__device__ __forceinline__ void mirror16(float* stage, const float (&v)[16], float (&t)[16],
+                                         int er, int ec) {
+    __builtin_amdgcn_wave_barrier();
+#pragma unroll
+    for (int q = 0; q < 16; ++q) stage[er * T::EPI_LD + ec + q] = v[q];
+    __builtin_amdgcn_wave_barrier();
+#pragma unroll
+    for (int q = 0; q < 16; ++q) t[q] = stage[(ec + q) * T::EPI_LD + er];
+}
+
 // MFMAs of one BK-deep K-slice staged at `st`, fragments software-pipelined
 // (k-step kk+1 is read from LDS while the MFMAs of kk run).
 template <int NPASS, typename T>
-__device__ __forceinline__ void mma_slice(f32x16 (&acc)[T::FM][T::FN], const uint16_t* st,
+__device__ __forceinline__ void mma_slice(f32x16 (&acc)[T::FM][T::FN], const unsigned char* st,
                                           int wm, int wn, int lane) {
-    const uint16_t* sa0 = st;
-    const uint16_t* sa1 = st + T::A_TILE;
-    const uint16_t* sb0 = st + T::NA * T::A_TILE;
-    const uint16_t* sb1 = sb0 + T::B_TILE;
+    const unsigned char* sa0 = st;
+    const unsigned char* sa1 = st + T::A_BYTES;
+    const unsigned char* sb0 = st + T::NA * T::A_BYTES;
+    const unsigned char* sb1 = sb0 + T::B_BYTES;
     const int arow = wm * T::TM + (lane & 31);
     const int brow = wn * T::TN + (lane & 31);
-    const int kl = 8 * (lane >> 5);
+    const int half = lane >> 5;
     constexpr int KK = T::BK / 16;
     bf16x8 fa0[2][T::FM], fb0[2][T::FN], fa1[2][T::FM], fb1[2][T::FN];
 #pragma unroll
     for (int kk = 0; kk <= KK; ++kk) {
         if (kk < KK) {
-            const int ko = kk * 16 + kl;
+            const int c = 2 * kk + half;   // logical 16-byte chunk of the K-major rows
             const int slot = kk & 1;
 #pragma unroll
             for (int i = 0; i < T::FM; ++i)
-                fa0[slot][i] = *reinterpret_cast<const bf16x8*>(sa0 + (arow + i * 32) * T::LDK + ko);
+                fa0[slot][i] = *reinterpret_cast<const bf16x8*>(sa0 + kmajor_off<T>(arow + i * 32, c));
 #pragma unroll
             for (int j = 0; j < T::FN; ++j) {
                 if constexpr (T::BT) {
                     fb0[slot][j] = b_frag_tr<T>(sb0, kk * 16, wn * T::TN + j * 32, lane);
                 } else {
-                    fb0[slot][j] = *reinterpret_cast<const bf16x8*>(sb0 + (brow + j * 32) * T::LDK + ko);
+                    fb0[slot][j] = *reinterpret_cast<const bf16x8*>(sb0 + kmajor_off<T>(brow + j * 32, c));
                 }
             }
             if constexpr (NPASS == 3) {
 #pragma unroll
                 for (int i = 0; i < T::FM; ++i)
-                    fa1[slot][i] = *reinterpret_cast<const bf16x8*>(sa1 + (arow + i * 32) * T::LDK + ko);
+                    fa1[slot][i] = *reinterpret_cast<const bf16x8*>(sa1 + kmajor_off<T>(arow + i * 32, c));
 #pragma unroll
                 for (int j = 0; j < T::FN; ++j)
-                    fb1[slot][j] = *reinterpret_cast<const bf16x8*>(sb1 + (brow + j * 32) * T::LDK + ko);
+                    fb1[slot][j] = *reinterpret_cast<const bf16x8*>(sb1 + kmajor_off<T>(brow + j * 32, c));
             }
         }
         if (kk > 0) {
@@ -155,10 +229,9 @@ __device__ __forceinline__ void mma_slice(f32x16 (&acc)[T::FM][T::FN], const uin
     }
 }
 
-template <int NPASS, int EPI, typename T>
+template <int NPASS, int EPI, typename T, bool SYM>
 __global__ __launch_bounds__(T::THREADS) void gemm(GemmArgs a) {
-    __shared__ __attribute__((aligned(16))) unsigned char smem_raw[T::SMEM];
-    uint16_t* smem = reinterpret_cast<uint16_t*>(smem_raw);
+    __shared__ __attribute__((aligned(1024))) unsigned char smem_raw[T::SMEM];
 
     // XCD-aware tile order. Workgroups are dispatched round-robin over the
     // eight XCDs, each with its own L2; renumbering puts consecutive tiles --
@@ -169,10 +242,23 @@ __global__ __launch_bounds__(T::THREADS) void gemm(GemmArgs a) {
     const int hw = blockIdx.x + nx * (blockIdx.y + ny * blockIdx.z);
     const int logical = (total % kXcds == 0) ? (hw % kXcds) * (total / kXcds) + hw / kXcds : hw;
     const int b = logical / (nx * ny);
-    const int row0 = ((logical / nx) % ny) * T::BM;   // output rows (M)
-    const int col0 = (logical % nx) * T::BN;          // output cols (N)
+    int row0 = ((logical / nx) % ny) * T::BM;   // output rows (M)
+    int col0 = (logical % nx) * T::BN;          // output cols (N)
+    if constexpr (SYM) {
+        // symmetric output: x enumerates the upper-triangle tiles I <= J
+        // row by row; each is written at (I, J) and mirrored to (J, I)
+        const int tiles = a.M / T::BM;
+        int rem = logical % nx, I = 0;
+        while (rem >= tiles - I) {
+            rem -= tiles - I;
+            ++I;
+        }
+        row0 = I * T::BM;
+        col0 = (I + rem) * T::BN;
+    }
     const int tid = threadIdx.x;
-    const int lane = tid & 63, wave = tid >> 6;
+    const int lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // uniform per wave
     const int wm = wave / T::WN, wn = wave % T::WN;
 
     const uint16_t* abase[2];
@@ -185,46 +271,30 @@ __global__ __launch_bounds__(T::THREADS) void gemm(GemmArgs a) {
         bbase[0] = a.B0 + (int64_t)b * a.sB + (int64_t)col0 * a.ldb;
         bbase[1] = NPASS == 3 ? a.B1 + (int64_t)b * a.sB + (int64_t)col0 * a.ldb : bbase[0];
     }
-    // elements between consecutive K-slices of one staged chunk
-    const int64_t astep = T::BK;
-    const int64_t bstep = T::BT ? (int64_t)T::BK * a.ldb : T::BK;
 
-    // staged chunk I: global pointer of slice 0, per-slice stride, LDS offset
-#define DION2_CH_DECL(I) const uint16_t* gp##I = nullptr; int64_t gs##I = 0; int so##I = 0; uint4 r##I;
-#define DION2_CH_INIT(I)                                                                \
-    if constexpr ((I) < T::NCH) {                                                       \
-        using CI = Chunk<T, I>;                                                         \
-        const int w = CI::within0 + tid;                                                \
-        if constexpr (CI::is_a) {                                                       \
-            const int rr = w / T::CPR, kc = w % T::CPR;                                 \
-            gp##I = abase[CI::tile] + (int64_t)rr * a.lda + kc * 8;                     \
-            gs##I = astep;                                                              \
-            so##I = CI::lds_base + rr * T::LDK + kc * 8;                                \
-        } else if constexpr (T::BT) {                                                   \
-            const int kr = w / (T::BN / 8), c8 = w % (T::BN / 8);                       \
-            gp##I = bbase[CI::tile] + (int64_t)kr * a.ldb + c8 * 8;                     \
-            gs##I = bstep;                                                              \
-            so##I = CI::lds_base + kr * T::LDN + c8 * 8;                                \
-        } else {                                                                        \
-            const int rr = w / T::CPR, kc = w % T::CPR;                                 \
-            gp##I = bbase[CI::tile] + (int64_t)rr * a.ldb + kc * 8;                     \
-            gs##I = bstep;                                                              \
-            so##I = CI::lds_base + rr * T::LDK + kc * 8;                                \
-        }                                                                               \
+    // Epilogue operands (Z for a Z, or A's hi / lo for the polynomial) are
+    // fetched first so their latency hides behind the main loop.
+    const int er = lane >> 1;          // epilogue: row (or transposed row) of this lane
+    const int ec = (lane & 1) * 16;    // epilogue: 16 consecutive columns
+    constexpr bool kPreE0 = EPI == EPI_POLY || EPI == EPI_UPDATE || EPI == EPI_FINAL;
+    constexpr bool kPreE1 = EPI == EPI_POLY;
+    const bool pre = kPreE0 && !(EPI == EPI_FINAL && a.out_transposed);
+    uint4 e0[T::FM][T::FN][2], e1[T::FM][T::FN][2];
+    if (pre) {
+#pragma unroll
+        for (int i = 0; i < T::FM; ++i)
+#pragma unroll
+            for (int j = 0; j < T::FN; ++j) {
+                const int64_t eo = (int64_t)b * a.sE + (int64_t)(row0 + wm * T::TM + i * 32 + er) * a.lde +
+                                   col0 + wn * T::TN + j * 32 + ec;
+                e0[i][j][0] = reinterpret_cast<const uint4*>(a.E0 + eo)[0];
+                e0[i][j][1] = reinterpret_cast<const uint4*>(a.E0 + eo)[1];
+                if constexpr (kPreE1) {
+                    e1[i][j][0] = reinterpret_cast<const uint4*>(a.E1 + eo)[0];
+                    e1[i][j][1] = reinterpret_cast<const uint4*>(a.E1 + eo)[1];
+                }
+            }
     }
-#define DION2_CH_LOAD(I, KT)                                                            \
-    if constexpr ((I) < T::NCH) r##I = *reinterpret_cast<const uint4*>(gp##I + (KT) * gs##I);
-#define DION2_CH_STORE(I, BASE)                                                         \
-    if constexpr ((I) < T::NCH) *reinterpret_cast<uint4*>((BASE) + so##I) = r##I;
-#define DION2_CH_ALL(M, ...)                                                            \
-    M(0, __VA_ARGS__) M(1, __VA_ARGS__) M(2, __VA_ARGS__) M(3, __VA_ARGS__)             \
-    M(4, __VA_ARGS__) M(5, __VA_ARGS__) M(6, __VA_ARGS__) M(7, __VA_ARGS__)             \
-    M(8, __VA_ARGS__) M(9, __VA_ARGS__) M(10, __VA_ARGS__) M(11, __VA_ARGS__)           \
-    M(12, __VA_ARGS__) M(13, __VA_ARGS__) M(14, __VA_ARGS__) M(15, __VA_ARGS__)
-#define DION2_CH_DECL_(I, ...) DION2_CH_DECL(I)
-#define DION2_CH_INIT_(I, ...) DION2_CH_INIT(I)
-    DION2_CH_ALL(DION2_CH_DECL_, 0)
-    DION2_CH_ALL(DION2_CH_INIT_, 0)
 
     f32x16 acc[T::FM][T::FN];
 #pragma unroll
@@ -234,35 +304,33 @@ __global__ __launch_bounds__(T::THREADS) void gemm(GemmArgs a) {
 #pragma unroll
             for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
+    // S-stage ring: slices 0..S-2 in flight before the first MFMA; at
+    // iteration kt slice kt+S-1 is requested into the stage freed by kt-1.
+    // Requests past the last slice re-read it (in bounds) so every iteration
+    // issues the same number of loads and the vmcnt wait stays exact.
     const int nk = a.K / T::BK;
-    DION2_CH_ALL(DION2_CH_LOAD, 0)
-    DION2_CH_ALL(DION2_CH_STORE, smem)
-    __syncthreads();
+#pragma unroll
+    for (int p = 0; p < T::S - 1; ++p)
+        load_slice<NPASS, T>(a, smem_raw + p * T::STAGE_BYTES, p < nk ? p : nk - 1, abase, bbase, wave, lane);
     for (int kt = 0; kt < nk; ++kt) {
-        // next K-slice (the last iteration re-reads the current one, which is
-        // in bounds, and stages it into the idle buffer)
-        const int kn = kt + 1 < nk ? kt + 1 : kt;
-        DION2_CH_ALL(DION2_CH_LOAD, kn)
-        __builtin_amdgcn_sched_barrier(0);
-        mma_slice<NPASS, T>(acc, smem + (kt & 1) * T::STAGE, wm, wn, lane);
-        __builtin_amdgcn_sched_barrier(0);
-        DION2_CH_ALL(DION2_CH_STORE, smem + ((kt + 1) & 1) * T::STAGE)
-        __syncthreads();
+        // This wave's part of slice kt has landed; the bare barrier then makes
+        // every wave's part visible and frees stage kt-1 (its fragments were
+        // consumed by MFMAs issued before the barrier). A full __syncthreads
+        // would also drain the loads of the slices in flight behind kt.
+        wait_vmcnt<(T::S - 2) * T::IPW>();
+        __builtin_amdgcn_s_barrier();
+        const int kn = kt + T::S - 1;
+        load_slice<NPASS, T>(a, smem_raw + (kn % T::S) * T::STAGE_BYTES, kn < nk ? kn : nk - 1,
+                             abase, bbase, wave, lane);
+        mma_slice<NPASS, T>(acc, smem_raw + (kt % T::S) * T::STAGE_BYTES, wm, wn, lane);
     }
-#undef DION2_CH_DECL
-#undef DION2_CH_INIT
-#undef DION2_CH_LOAD
-#undef DION2_CH_STORE
-#undef DION2_CH_ALL
-#undef DION2_CH_DECL_
-#undef DION2_CH_INIT_
+    wait_vmcnt<0>();   // no load may land in the ring once the epilogue reuses it
+    __syncthreads();
 
     // ---- epilogue, one 32 x 32 block at a time through a per-wave LDS tile.
     // The tile belongs to its wave alone and LDS accesses of one wave complete
     // in issue order, so wave barriers order the staging.
     float* stage = reinterpret_cast<float*>(smem_raw) + wave * 32 * T::EPI_LD;
-    const int er = lane >> 1;          // row (or transposed row) handled by this lane
-    const int ec = (lane & 1) * 16;    // 16 consecutive columns
 #pragma unroll
     for (int i = 0; i < T::FM; ++i) {
 #pragma unroll
@@ -292,9 +360,8 @@ __global__ __launch_bounds__(T::THREADS) void gemm(GemmArgs a) {
                 const int64_t zr = transposed ? R + ec : R + er;
                 const int64_t zc = transposed ? Cc + er : Cc + ec;
                 if (!transposed) {
-                    const uint16_t* zp = a.E0 + (int64_t)b * a.sE + zr * a.lde + zc;
-                    const uint4 z0 = reinterpret_cast<const uint4*>(zp)[0];
-                    const uint4 z1 = reinterpret_cast<const uint4*>(zp)[1];
+                    const uint4 z0 = e0[i][j][0];
+                    const uint4 z1 = e0[i][j][1];
                     const uint32_t zw[8] = {z0.x, z0.y, z0.z, z0.w, z1.x, z1.y, z1.z, z1.w};
 #pragma unroll
                     for (int q = 0; q < 8; ++q) {
@@ -322,13 +389,30 @@ __global__ __launch_bounds__(T::THREADS) void gemm(GemmArgs a) {
                 reinterpret_cast<uint4*>(hp)[1] = make_uint4(h[4], h[5], h[6], h[7]);
                 reinterpret_cast<uint4*>(lp)[0] = make_uint4(l[0], l[1], l[2], l[3]);
                 reinterpret_cast<uint4*>(lp)[1] = make_uint4(l[4], l[5], l[6], l[7]);
+                if (SYM && row0 != col0) {
+                    float t[16];
+                    mirror16<T>(stage, v, t, er, ec);
+                    uint32_t th[8], tl[8];
+#pragma unroll
+                    for (int q = 0; q < 8; ++q) {
+                        const uint16_t h0 = f32_to_bf16(t[2 * q]), h1 = f32_to_bf16(t[2 * q + 1]);
+                        th[q] = (uint32_t)h0 | ((uint32_t)h1 << 16);
+                        tl[q] = pack2(t[2 * q] - bf16_bits_to_f32(h0), t[2 * q + 1] - bf16_bits_to_f32(h1));
+                    }
+                    const int64_t mrow = Cc + er, mcol = R + ec;
+                    uint16_t* mh = static_cast<uint16_t*>(a.out0) + (int64_t)b * a.sOut0 + mrow * a.ldo0 + mcol;
+                    uint16_t* ml = static_cast<uint16_t*>(a.out1) + (int64_t)b * a.sOut1 + mrow * a.ldo1 + mcol;
+                    reinterpret_cast<uint4*>(mh)[0] = make_uint4(th[0], th[1], th[2], th[3]);
+                    reinterpret_cast<uint4*>(mh)[1] = make_uint4(th[4], th[5], th[6], th[7]);
+                    reinterpret_cast<uint4*>(ml)[0] = make_uint4(tl[0], tl[1], tl[2], tl[3]);
+                    reinterpret_cast<uint4*>(ml)[1] = make_uint4(tl[4], tl[5], tl[6], tl[7]);
+                }
             } else if constexpr (EPI == EPI_POLY) {
                 // B = b (A_hi + A_lo) + c A^2
-                const int64_t eo = (int64_t)b * a.sE + orow * a.lde + ocol;
-                const uint4 h0 = reinterpret_cast<const uint4*>(a.E0 + eo)[0];
-                const uint4 h1 = reinterpret_cast<const uint4*>(a.E0 + eo)[1];
-                const uint4 l0 = reinterpret_cast<const uint4*>(a.E1 + eo)[0];
-                const uint4 l1 = reinterpret_cast<const uint4*>(a.E1 + eo)[1];
+                const uint4 h0 = e0[i][j][0];
+                const uint4 h1 = e0[i][j][1];
+                const uint4 l0 = e1[i][j][0];
+                const uint4 l1 = e1[i][j][1];
                 const uint32_t hw[8] = {h0.x, h0.y, h0.z, h0.w, h1.x, h1.y, h1.z, h1.w};
                 const uint32_t lw[8] = {l0.x, l0.y, l0.z, l0.w, l1.x, l1.y, l1.z, l1.w};
                 uint32_t o[8];
@@ -336,11 +420,23 @@ __global__ __launch_bounds__(T::THREADS) void gemm(GemmArgs a) {
                 for (int q = 0; q < 8; ++q) {
                     const float a0 = bf16_bits_to_f32(hw[q] & 0xffffu) + bf16_bits_to_f32(lw[q] & 0xffffu);
                     const float a1 = bf16_bits_to_f32(hw[q] >> 16) + bf16_bits_to_f32(lw[q] >> 16);
-                    o[q] = pack2(a.cb * a0 + a.cc * v[2 * q], a.cb * a1 + a.cc * v[2 * q + 1]);
+                    v[2 * q] = a.cb * a0 + a.cc * v[2 * q];
+                    v[2 * q + 1] = a.cb * a1 + a.cc * v[2 * q + 1];
+                    o[q] = pack2(v[2 * q], v[2 * q + 1]);
                 }
                 uint16_t* op = static_cast<uint16_t*>(a.out0) + (int64_t)b * a.sOut0 + orow * a.ldo0 + ocol;
                 reinterpret_cast<uint4*>(op)[0] = make_uint4(o[0], o[1], o[2], o[3]);
                 reinterpret_cast<uint4*>(op)[1] = make_uint4(o[4], o[5], o[6], o[7]);
+                if (SYM && row0 != col0) {
+                    float t[16];
+                    mirror16<T>(stage, v, t, er, ec);
+                    const int64_t mrow = Cc + er, mcol = R + ec;
+                    uint16_t* mp = static_cast<uint16_t*>(a.out0) + (int64_t)b * a.sOut0 + mrow * a.ldo0 + mcol;
+                    reinterpret_cast<uint4*>(mp)[0] = make_uint4(pack2(t[0], t[1]), pack2(t[2], t[3]),
+                                                                 pack2(t[4], t[5]), pack2(t[6], t[7]));
+                    reinterpret_cast<uint4*>(mp)[1] = make_uint4(pack2(t[8], t[9]), pack2(t[10], t[11]),
+                                                                 pack2(t[12], t[13]), pack2(t[14], t[15]));
+                }
             } else if constexpr (EPI == EPI_UPDATE) {
                 uint16_t* op = static_cast<uint16_t*>(a.out0) + (int64_t)b * a.sOut0 + orow * a.ldo0 + ocol;
                 reinterpret_cast<uint4*>(op)[0] = make_uint4(pack2(v[0], v[1]), pack2(v[2], v[3]),
@@ -358,23 +454,34 @@ __global__ __launch_bounds__(T::THREADS) void gemm(GemmArgs a) {
     }
 }
 
-template <int NPASS, int EPI, typename T>
+template <int NPASS, int EPI, typename T, bool SYM = false>
 hipError_t launch_tile(const GemmArgs& a, hipStream_t s) {
     if (a.M % T::BM || a.N % T::BN || a.K % T::BK) return hipErrorInvalidValue;
     dim3 grid((unsigned)(a.N / T::BN), (unsigned)(a.M / T::BM), (unsigned)a.batch);
-    hipLaunchKernelGGL((gemm<NPASS, EPI, T>), grid, dim3(T::THREADS), 0, s, a);
+    if (SYM) {
+        if (a.M != a.N || T::BM != T::BN) return hipErrorInvalidValue;
+        const unsigned tiles = (unsigned)(a.M / T::BM);
+        grid = dim3(tiles * (tiles + 1) / 2, 1, (unsigned)a.batch);
+    }
+    hipLaunchKernelGGL((gemm<NPASS, EPI, T, SYM>), grid, dim3(T::THREADS), 0, s, a);
     return hipGetLastError();
 }
 
 }  // namespace
 
 hipError_t launch_gemm(const GemmArgs& a, GemmEpi epi, hipStream_t s) {
-    using TG = Tile<1, 0, 128, 128, 64, 2, 2>;   // Gram
-    using TP = Tile<3, 0, 128, 128, 32, 2, 2>;   // polynomial (three passes)
-    using TU = Tile<1, 1, 128, 128, 64, 2, 2>;   // update (B operand [K][N])
+    // Tile choices measured on MI355X at the Newton-Schulz shapes: 128 x 128
+    // tiles keep enough blocks in flight for s = 512; from s = 1024 the
+    // symmetric Gram product runs faster on 256 x 256 tiles of 8 waves.
+    using TG = Tile<1, 0, 128, 128, 32, 2, 2, 4>;    // Gram
+    using TGL = Tile<1, 0, 256, 256, 32, 4, 2, 3>;   // Gram, large s
+    using TP = Tile<3, 0, 128, 128, 32, 4, 2, 2>;    // polynomial (three passes)
+    using TU = Tile<1, 1, 128, 128, 32, 2, 2, 3>;    // update (B operand [K][N])
     switch (epi) {
-        case EPI_SPLIT: return launch_tile<1, EPI_SPLIT, TG>(a, s);
-        case EPI_POLY: return launch_tile<3, EPI_POLY, TP>(a, s);
+        case EPI_SPLIT:
+            if (a.M >= 1024 && a.M % 256 == 0) return launch_tile<1, EPI_SPLIT, TGL, true>(a, s);
+            return launch_tile<1, EPI_SPLIT, TG, true>(a, s);
+        case EPI_POLY: return launch_tile<3, EPI_POLY, TP, true>(a, s);
         case EPI_UPDATE: return launch_tile<1, EPI_UPDATE, TU>(a, s);
         case EPI_FINAL: return launch_tile<1, EPI_FINAL, TU>(a, s);
     }
