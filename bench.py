@@ -17,6 +17,7 @@ steps 20). Prints one JSON line:
 from __future__ import annotations
 
 import argparse
+import glob
 import json
 import os
 import statistics
@@ -29,7 +30,7 @@ if ROOT not in sys.path:
 
 import torch  # noqa: E402
 
-from paper_2512_16928_amd import binding, workloads  # noqa: E402
+from paper_2512_16928_amd import binding, profsum, workloads  # noqa: E402
 
 METRIC = "Dion2 optimizer-step ms per layer stack at α=0.25/0.5/1; NS MFMA util %"
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E
@@ -51,9 +52,17 @@ def allocate(wl, dev):
     return groups
 
 
+NS_FORMS = {"auto": binding.NS_AUTO, "direct": binding.NS_DIRECT, "gram": binding.NS_GRAM}
+NS_FORM = binding.NS_AUTO
+
+
 def one_step(wl, groups, alpha):
     for grp, W, M, G in groups:
-        binding.dion2_step_strided(W, M, G, alpha, wl.mu, wl.lr, wl.ns_steps, grp.axis)
+        if NS_FORM == binding.NS_AUTO:
+            binding.dion2_step_strided(W, M, G, alpha, wl.mu, wl.lr, wl.ns_steps, grp.axis)
+        else:
+            binding.dion2_step_ex(W, M, G, alpha, wl.mu, wl.lr, wl.ns_steps, grp.axis,
+                                  ns_form=NS_FORM)
 
 
 def time_steps(wl, groups, alpha, warmup, steps):
@@ -154,10 +163,14 @@ def main(argv=None):
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-profile", action="store_true", help="skip the per-kernel event pass")
+    ap.add_argument("--ns-form", default="auto", choices=sorted(NS_FORMS),
+                    help="Newton-Schulz evaluation order (default: chosen by shape)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run plain 1 GiB device copies, the reference dispatches that "
                          "scale HBM byte counters (FETCH_SIZE / WRITE_SIZE) in a profiler run")
     args = ap.parse_args(argv)
+    global NS_FORM
+    NS_FORM = NS_FORMS[args.ns_form]
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures the Dion2 step on one GPU only: there is no multi-GPU path "
@@ -173,13 +186,15 @@ def main(argv=None):
     binding.load()
 
     if args.copy_calibration:
+        # one elementwise kernel per copy (a device-to-device copy_ splits
+        # into many smaller dispatches): 1 GiB read, 1 GiB written
         src = torch.empty(1 << 28, dtype=torch.float32, device="cuda:0").fill_(1.0)
         dst = torch.empty_like(src)
         for _ in range(3):
-            dst.copy_(src)
+            torch.neg(src, out=dst)
         torch.cuda.synchronize()
         del src, dst
-        log("[bench] ran 3 plain copies of 1 GiB (counter calibration)")
+        log("[bench] ran 3 plain 1 GiB copies (torch.neg) for counter calibration")
 
     wl = workloads.WORKLOADS[args.workload]
     alpha = args.alpha if args.alpha is not None else wl.alphas[0]
@@ -200,9 +215,16 @@ def main(argv=None):
         phases = profile_phases(wl, groups, alpha, args.steps)
         dom = max(phases, key=lambda p: phases[p]["total_ms_per_step"])
         d = phases[dom]
+        traffic = None
+        for path in sorted(glob.glob(os.path.join(ROOT, "profiles", "*traffic*.txt"))):
+            traffic = traffic or profsum.lookup_traffic(path, dom, wl.name, alpha)
         roofline = dict(bound=d["bound"], achieved=round(d["achieved"], 3), peak=d["peak"],
-                        unit=d["unit"], frac=round(d["frac"], 4), traffic=None, kernel=dom,
-                        avg_launch_ms=round(d["avg_launch_ms"], 5))
+                        unit=d["unit"], frac=round(d["frac"], 4),
+                        traffic=None if traffic is None else round(traffic),
+                        traffic_unit="bytes per launch", kernel=dom,
+                        avg_launch_ms=round(d["avg_launch_ms"], 5),
+                        algorithmic_per_launch=round(d["work_per_call"]),
+                        algorithmic_unit="bytes" if d["unit"] == "GB/s" else "flops")
         ns_ms = sum(phases[p]["total_ms_per_step"] for p in NS_PHASES if p in phases)
         ns_work = sum(phases[p]["work_per_call"] * phases[p]["calls_per_step"]
                       for p in NS_PHASES if p in phases)
@@ -243,7 +265,7 @@ def main(argv=None):
         "data": "synthetic",
         "config": {"workload": wl.name, "description": wl.description, "alpha": alpha,
                    "matrices": wl.matrices(), "elements": wl.elements(),
-                   "ns_steps": wl.ns_steps, "mu": wl.mu, "lr": wl.lr,
+                   "ns_steps": wl.ns_steps, "mu": wl.mu, "lr": wl.lr, "ns_form": args.ns_form,
                    "parallelism": "single GPU, batched per shape group"},
         "roofline": roofline,
         "cpu_baseline": cpu,

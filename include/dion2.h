@@ -23,9 +23,19 @@
  *     K is ascending.
  *   - Newton-Schulz: X = M[K,:] / (||M[K,:]||_F + eps), then per step
  *     A = X X^T, B = b A + c A^2, X <- a X + B X on the orientation with the
- *     smaller Gram matrix; bf16 MFMA operands with fp32 accumulation, A^2
- *     from a three-pass bf16 hi/lo split of A. Default coefficients are
- *     Muon's quintic (3.4445, -4.7750, 2.0315) at every step, eps = 1e-7.
+ *     smaller Gram matrix (s x s, X is s x l, s <= l); X is rounded once to
+ *     bf16 and every product runs on bf16 MFMA operands with fp32
+ *     accumulation. Two evaluation orders give the same result in exact
+ *     arithmetic (dion2_options.ns_form):
+ *       DIRECT  the steps as written, X kept in bf16 between steps, A^2 from
+ *               a three-pass bf16 hi/lo split of A;
+ *       GRAM    the iteration carried on s x s matrices: with
+ *               Q_t = a I + b A_t + c A_t^2 one has X_{t+1} = Q_t X_t and
+ *               A_{t+1} = Q_t A_t Q_t, so X_T = (Q_{T-1} ... Q_0) X_0; every
+ *               s x s product uses hi/lo pairs (three passes) and the final
+ *               product two, so X is read only twice.
+ *     Default coefficients are Muon's quintic (3.4445, -4.7750, 2.0315) at
+ *     every step, eps = 1e-7.
  *   - The weight update is computed in fp64 from the fp32 O and rounded once
  *     (RNE) to W's storage type. Unselected lines of W are not written.
  *
@@ -80,6 +90,12 @@ typedef enum dion2_dtype {
     DION2_DTYPE_BF16 = 1
 } dion2_dtype;
 
+typedef enum dion2_ns_form {
+    DION2_NS_AUTO = 0,   /* GRAM when l >= 3 s (padded sides), else DIRECT     */
+    DION2_NS_DIRECT = 1, /* iterate on X (s x l)                               */
+    DION2_NS_GRAM = 2    /* iterate on s x s matrices, X read twice            */
+} dion2_ns_form;
+
 /* Full-control options for dion2_step_ex. Fill with dion2_options_init. */
 typedef struct dion2_options {
     int w_dtype;             /* storage type of W (default DION2_DTYPE_BF16)        */
@@ -97,10 +113,11 @@ typedef struct dion2_options {
     float* dbg_update;       /* optional DEVICE out [batch][k][d_oth]: O, one
                                 selected line per row (row k of O^T for columns),
                                 before the lr*sqrt(rows/cols) scale                 */
+    int ns_form;             /* dion2_ns_form (default DION2_NS_AUTO)               */
 } dion2_options;
 
 /* Defaults: bf16 W and G, Muon quintic, eps 1e-7, selective decay, internal
-   workspace, no debug outputs. */
+   workspace, no debug outputs, Newton-Schulz form chosen by shape. */
 void dion2_options_init(dion2_options* opt);
 
 /* One matrix. W, G: bf16 [rows][cols]; M: fp32 [rows][cols]. Algorithm 1. */
@@ -131,7 +148,9 @@ int dion2_step_ex(void* W, float* M, const void* G, int batch, int64_t rows,
                   int axis, const dion2_options* opt, void* stream);
 
 /* Bytes of device workspace one call with these arguments needs (for
-   dion2_options.workspace). Returns 0 for invalid arguments. */
+   dion2_options.workspace) with ns_form = DION2_NS_AUTO; a forced form may
+   need more (dion2_step_ex then fails with DION2_ERR_WORKSPACE). Returns 0
+   for invalid arguments. */
 size_t dion2_workspace_size(int batch, int64_t rows, int64_t cols,
                             float alpha, int axis);
 
@@ -147,17 +166,20 @@ int dion2_plan_info(int64_t rows, int64_t cols, float alpha, int axis,
  * added to a per-phase total: bytes for the streaming phases (what the step
  * itself must move: M and G read and M written by MOMENTUM; the selected
  * lines of M read and written by GATHER; the selected lines of W read and
- * written by APPLY), dense-count flops for the Newton-Schulz GEMMs (2 s^2 l
- * for the Gram matrix, 2 s^3 for A^2, 2 s^2 l for B X; s <= l are the
- * compact matrix's unpadded sides). The events cost a little time, so the
- * step time is measured with the hooks off. */
+ * written by APPLY), and MFMA flops for the Newton-Schulz GEMMs, counting
+ * every bf16 hi/lo pass and counting a product with a symmetric result at
+ * s (s + 1) per inner index (the half it computes) instead of 2 s^2: the
+ * Gram matrix s (s + 1) l, a three-pass s x s product 3 s (s + 1) s, the
+ * update B X 2 s^2 l and the two-pass final product of the GRAM form
+ * 4 s^2 l (s <= l are the compact matrix's unpadded sides). The events cost
+ * a little time, so the step time is measured with the hooks off. */
 typedef enum dion2_phase {
     DION2_PHASE_MOMENTUM = 0,  /* K1: M += G and line norms         */
     DION2_PHASE_SELECT = 1,    /* K2: top-k selection               */
     DION2_PHASE_GATHER = 2,    /* K3: compact gather + decay        */
     DION2_PHASE_NS_GRAM = 3,   /* K4: A = X X^T (hi/lo split)       */
-    DION2_PHASE_NS_POLY = 4,   /* K4: B = b A + c A^2               */
-    DION2_PHASE_NS_UPDATE = 5, /* K4: X <- a X + B X                */
+    DION2_PHASE_NS_POLY = 4,   /* K4: the s x s products            */
+    DION2_PHASE_NS_UPDATE = 5, /* K4: X <- a X + B X, or O = P X_0  */
     DION2_PHASE_APPLY = 6,     /* K5: scatter-apply into W          */
     DION2_PHASE_COUNT = 7
 } dion2_phase;

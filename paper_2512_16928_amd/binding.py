@@ -29,6 +29,7 @@ AXIS_COLS = 1
 
 DTYPE_F32 = 0
 DTYPE_BF16 = 1
+NS_AUTO, NS_DIRECT, NS_GRAM = 0, 1, 2
 
 MAX_NS_STEPS = 16
 
@@ -60,6 +61,7 @@ class Options(ctypes.Structure):
         ("dbg_sel_idx", c_void_p),
         ("dbg_norms", c_void_p),
         ("dbg_update", c_void_p),
+        ("ns_form", c_int),
     ]
 
 
@@ -194,11 +196,13 @@ def dion2_step_batched(Ws, Ms, Gs, alpha, mu=0.95, lr=0.02, ns_steps=5, axis=AXI
 
 def dion2_step_ex(W, M, G, alpha, mu=0.95, lr=0.02, ns_steps=5, axis=AXIS_AUTO, *,
                   ns_coeffs=None, ns_eps=1e-7, decay_all=False, workspace=None,
-                  dbg_sel_idx=None, dbg_norms=None, dbg_update=None, stream=None):
+                  dbg_sel_idx=None, dbg_norms=None, dbg_update=None, ns_form=NS_AUTO,
+                  stream=None):
     """Full control. W, M, G are [rows, cols] or [batch, rows, cols]; W and G
     may be bf16 or fp32. Debug outputs are preallocated device tensors:
     dbg_sel_idx int32 [batch, k], dbg_norms float64 [batch, d_sel],
-    dbg_update float32 [batch, k, d_oth]."""
+    dbg_update float32 [batch, k, d_oth]. ns_form is NS_AUTO, NS_DIRECT or
+    NS_GRAM (the Newton-Schulz evaluation order)."""
     if W.dim() == 2:
         W, M, G = W.unsqueeze(0), M.unsqueeze(0), G.unsqueeze(0)
     _mats(W, M, G, 3)
@@ -216,6 +220,7 @@ def dion2_step_ex(W, M, G, alpha, mu=0.95, lr=0.02, ns_steps=5, axis=AXIS_AUTO, 
         opt.ns_coeffs = ctypes.cast(coeff_buf, POINTER(c_float))
     opt.ns_eps = ns_eps
     opt.decay_all = 1 if decay_all else 0
+    opt.ns_form = ns_form
     for name, t, dt in (("dbg_sel_idx", dbg_sel_idx, torch.int32),
                         ("dbg_norms", dbg_norms, torch.float64),
                         ("dbg_update", dbg_update, torch.float32)):

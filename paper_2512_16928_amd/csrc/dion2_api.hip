@@ -2,7 +2,8 @@
 // management and the launch sequence of one step (Algorithm 1):
 //
 //   K1 momentum + line norms -> K2 top-k select -> K3 gather + decay
-//   -> ns_steps x (K4 Gram split -> K4 A^2 combine -> K4 a Z + B Z)
+//   -> K4 Newton-Schulz, DIRECT: ns_steps x (Gram split -> A^2 combine -> a Z + B Z)
+//                        GRAM:   Gram split -> ns_steps x (s x s products) -> P Z
 //   -> K5 scatter-apply
 //
 // Nothing here computes part of the step on the host; the host only decides
@@ -58,12 +59,16 @@ struct Plan {
     int64_t s_pad, l_pad;
     int batch;
     int nrb, rb_rows;         // column-mode reduction blocking
+    bool gram;                // Newton-Schulz on s x s matrices (DION2_NS_GRAM)
     // workspace offsets
-    size_t o_l1, o_sq, o_part, o_sel, o_scale, o_L, o_LT, o_Z1, o_Ahi, o_Alo, o_B, o_O,
-        o_tables, total;
+    size_t o_l1, o_sq, o_part, o_sel, o_scale, o_Z, o_Z1, o_S, S_bytes, o_O, o_tables, total;
 };
 
-int make_plan(int batch, int64_t rows, int64_t cols, float alpha, int axis, Plan* p) {
+// s x s buffers of the two Newton-Schulz forms (bf16 [batch][s_pad][s_pad])
+enum { SQ_AHI, SQ_ALO, SQ_B, SQ_DIRECT_COUNT = 3 };
+enum { SQ_QHI = 2, SQ_QLO, SQ_THI, SQ_TLO, SQ_P0HI, SQ_P0LO, SQ_P1HI, SQ_P1LO, SQ_GRAM_COUNT };
+
+int make_plan(int batch, int64_t rows, int64_t cols, float alpha, int axis, int ns_form, Plan* p) {
     if (batch < 1 || batch > 65535) return fail(DION2_ERR_INVALID_ARG, "batch %d not in [1, 65535]", batch);
     if (rows < 1 || cols < 1)
         return fail(DION2_ERR_INVALID_ARG, "rows (%lld) and cols (%lld) must be >= 1",
@@ -75,6 +80,8 @@ int make_plan(int batch, int64_t rows, int64_t cols, float alpha, int axis, Plan
         return fail(DION2_ERR_INVALID_ARG, "alpha %g not in (0, 1]", (double)alpha);
     if (axis != DION2_AXIS_AUTO && axis != DION2_AXIS_ROWS && axis != DION2_AXIS_COLS)
         return fail(DION2_ERR_INVALID_ARG, "axis %d is not AUTO, ROWS or COLS", axis);
+    if (ns_form != DION2_NS_AUTO && ns_form != DION2_NS_DIRECT && ns_form != DION2_NS_GRAM)
+        return fail(DION2_ERR_INVALID_ARG, "ns_form %d is not AUTO, DIRECT or GRAM", ns_form);
     Plan& P = *p;
     P.axis = axis == DION2_AXIS_AUTO ? (rows <= cols ? 0 : 1) : axis;
     P.rows = rows;
@@ -88,6 +95,9 @@ int make_plan(int batch, int64_t rows, int64_t cols, float alpha, int axis, Plan
     P.z_is_L = P.k <= P.d_oth;
     P.s_pad = P.z_is_L ? P.kpad : P.opad;
     P.l_pad = P.z_is_L ? P.opad : P.kpad;
+    // The GRAM form trades 2 (s x l) GEMMs and the X traffic of every step
+    // for about four three-pass s x s products; it pays once X is wide.
+    P.gram = ns_form == DION2_NS_GRAM || (ns_form == DION2_NS_AUTO && P.l_pad >= 3 * P.s_pad);
     P.batch = batch;
     P.nrb = P.axis == 1 ? (int)momentum_col_blocks(rows, &P.rb_rows) : 0;
     if (P.axis == 0) P.rb_rows = 0;
@@ -105,13 +115,10 @@ int make_plan(int batch, int64_t rows, int64_t cols, float alpha, int axis, Plan
     P.o_sel = take(B * P.k * 4);
     P.o_scale = take(B * 8);
     const size_t comp = B * (size_t)P.kpad * (size_t)P.opad * 2;
-    P.o_L = take(comp);
-    P.o_LT = take(comp);
-    P.o_Z1 = take(comp);
-    const size_t gram = B * (size_t)P.s_pad * (size_t)P.s_pad * 2;
-    P.o_Ahi = take(gram);
-    P.o_Alo = take(gram);
-    P.o_B = take(gram);
+    P.o_Z = take(comp);
+    P.o_Z1 = take(P.gram ? 0 : comp);
+    P.S_bytes = align256(B * (size_t)P.s_pad * (size_t)P.s_pad * 2);
+    P.o_S = take(P.S_bytes * (P.gram ? SQ_GRAM_COUNT : SQ_DIRECT_COUNT));
     P.o_O = take(B * (size_t)P.kpad * (size_t)P.opad * 4);
     P.o_tables = take(3 * B * sizeof(void*));
     P.total = off;
@@ -232,6 +239,177 @@ hipError_t timed(int phase, double work, int launches, hipStream_t s, F&& fn) {
     return e;
 }
 
+// ------------------------------------------------------ Newton-Schulz
+
+// Z is the wide orientation [s_pad][l_pad] of the compact matrix; O receives
+// the result in the L layout [kpad][opad] (the transpose when Z is L^T).
+
+double sym_flops(double s, double inner) { return s * (s + 1.0) * inner; }
+
+GemmArgs gram_args(const Plan& P, const uint16_t* Z, uint16_t* hi, uint16_t* lo) {
+    GemmArgs g{};
+    g.batch = P.batch;
+    g.A0 = g.B0 = Z;
+    g.sA = g.sB = P.s_pad * P.l_pad;
+    g.M = g.N = (int)P.s_pad;
+    g.K = (int)P.l_pad;
+    g.lda = g.ldb = (int)P.l_pad;
+    g.out0 = hi;
+    g.out1 = lo;
+    g.sOut0 = g.sOut1 = P.s_pad * P.s_pad;
+    g.ldo0 = g.ldo1 = (int)P.s_pad;
+    return g;
+}
+
+// Three-pass symmetric s x s product C = X Y (Y symmetric, given by rows),
+// both operands as hi / lo pairs.
+GemmArgs sym3_args(const Plan& P, const uint16_t* xh, const uint16_t* xl, const uint16_t* yh,
+                   const uint16_t* yl, void* oh, void* ol) {
+    GemmArgs q{};
+    q.batch = P.batch;
+    q.A0 = xh;
+    q.A1 = xl;
+    q.B0 = yh;
+    q.B1 = yl;
+    q.sA = q.sB = P.s_pad * P.s_pad;
+    q.M = q.N = q.K = (int)P.s_pad;
+    q.lda = q.ldb = (int)P.s_pad;
+    q.out0 = oh;
+    q.out1 = ol;
+    q.sOut0 = q.sOut1 = P.s_pad * P.s_pad;
+    q.ldo0 = q.ldo1 = (int)P.s_pad;
+    return q;
+}
+
+// C = X Z with X [s][s] by rows and Z [s][l] as the B operand ([K][N]).
+GemmArgs right_args(const Plan& P, const uint16_t* xh, const uint16_t* xl, const uint16_t* Z) {
+    GemmArgs x{};
+    x.batch = P.batch;
+    x.A0 = xh;
+    x.A1 = xl;
+    x.B0 = Z;
+    x.sA = P.s_pad * P.s_pad;
+    x.sB = P.s_pad * P.l_pad;
+    x.M = (int)P.s_pad;
+    x.N = (int)P.l_pad;
+    x.K = (int)P.s_pad;
+    x.lda = (int)P.s_pad;
+    x.ldb = (int)P.l_pad;
+    return x;
+}
+
+void final_output(const Plan& P, GemmArgs& x, float* O) {
+    x.out0 = O;
+    x.sOut0 = P.kpad * P.opad;
+    x.ldo0 = (int)P.opad;
+    x.out_transposed = P.z_is_L ? 0 : 1;
+}
+
+// DIRECT: per step A = Z Z^T (hi / lo), B = b A + c A^2, Z <- a Z + B Z.
+hipError_t ns_direct(const Plan& P, uint16_t* Z0, uint16_t* Z1, uint16_t* const* sq, float* O,
+                     int ns_steps, const dion2_options& opt, hipStream_t stream) {
+    const double s_r = (double)(P.k < P.d_oth ? P.k : P.d_oth);   // unpadded sides
+    const double l_r = (double)(P.k < P.d_oth ? P.d_oth : P.k);
+    const double nb = (double)P.batch;
+    uint16_t* zbuf[2] = {Z0, Z1};
+    int cur = 0;
+    for (int t = 0; t < ns_steps; ++t) {
+        const float* cf = opt.ns_coeffs ? opt.ns_coeffs + 3 * t : kMuonQuintic;
+        uint16_t* Z = zbuf[cur];
+        GemmArgs g = gram_args(P, Z, sq[SQ_AHI], sq[SQ_ALO]);
+        hipError_t e = timed(DION2_PHASE_NS_GRAM, sym_flops(s_r, l_r) * nb, 1, stream,
+                             [&] { return launch_gemm(g, EPI_SPLIT, 1, stream); });
+        if (e != hipSuccess) return e;
+
+        GemmArgs q = sym3_args(P, sq[SQ_AHI], sq[SQ_ALO], sq[SQ_AHI], sq[SQ_ALO], sq[SQ_B], nullptr);
+        q.cb = cf[1];
+        q.cc = cf[2];
+        q.E0 = sq[SQ_AHI];
+        q.E1 = sq[SQ_ALO];
+        q.sE = P.s_pad * P.s_pad;
+        q.lde = (int)P.s_pad;
+        e = timed(DION2_PHASE_NS_POLY, 3.0 * sym_flops(s_r, s_r) * nb, 1, stream,
+                  [&] { return launch_gemm(q, EPI_POLY, 3, stream); });
+        if (e != hipSuccess) return e;
+
+        // Z' = a Z + B Z (a Z added in the epilogue)
+        GemmArgs x = right_args(P, sq[SQ_B], nullptr, Z);
+        x.ca = cf[0];
+        x.E0 = Z;
+        x.sE = P.s_pad * P.l_pad;
+        x.lde = (int)P.l_pad;
+        const bool last = t + 1 == ns_steps;
+        if (!last) {
+            x.out0 = zbuf[1 - cur];
+            x.sOut0 = P.s_pad * P.l_pad;
+            x.ldo0 = (int)P.l_pad;
+        } else {
+            final_output(P, x, O);
+        }
+        e = timed(DION2_PHASE_NS_UPDATE, 2.0 * s_r * s_r * l_r * nb, 1, stream,
+                  [&] { return launch_gemm(x, last ? EPI_FINAL : EPI_UPDATE, 1, stream); });
+        if (e != hipSuccess) return e;
+        cur = 1 - cur;
+    }
+    return hipSuccess;
+}
+
+// GRAM: A_0 = Z Z^T; per step Q_t = a I + b A_t + c A_t^2, P <- Q_t P and
+// A_{t+1} = Q_t (Q_t A_t); finally O = P Z. Every s x s matrix is a
+// polynomial in A_0, hence symmetric, and all of them commute.
+hipError_t ns_gram(const Plan& P, const uint16_t* Z, uint16_t* const* sq, float* O, int ns_steps,
+                   const dion2_options& opt, hipStream_t stream) {
+    const double s_r = (double)(P.k < P.d_oth ? P.k : P.d_oth);
+    const double l_r = (double)(P.k < P.d_oth ? P.d_oth : P.k);
+    const double nb = (double)P.batch;
+    const double f3 = 3.0 * sym_flops(s_r, s_r) * nb;
+    uint16_t* Ah = sq[SQ_AHI];
+    uint16_t* Al = sq[SQ_ALO];
+    uint16_t* Ph[2] = {sq[SQ_P0HI], sq[SQ_P1HI]};
+    uint16_t* Pl[2] = {sq[SQ_P0LO], sq[SQ_P1LO]};
+    int cur = 0;
+
+    GemmArgs g = gram_args(P, Z, Ah, Al);
+    hipError_t e = timed(DION2_PHASE_NS_GRAM, sym_flops(s_r, l_r) * nb, 1, stream,
+                         [&] { return launch_gemm(g, EPI_SPLIT, 1, stream); });
+    if (e != hipSuccess) return e;
+    for (int t = 0; t < ns_steps; ++t) {
+        const float* cf = opt.ns_coeffs ? opt.ns_coeffs + 3 * t : kMuonQuintic;
+        // Q_t; the first one is P itself
+        uint16_t* qh = t == 0 ? Ph[0] : sq[SQ_QHI];
+        uint16_t* ql = t == 0 ? Pl[0] : sq[SQ_QLO];
+        GemmArgs q = sym3_args(P, Ah, Al, Ah, Al, qh, ql);
+        q.ca = cf[0];
+        q.cb = cf[1];
+        q.cc = cf[2];
+        q.E0 = Ah;
+        q.E1 = Al;
+        q.sE = P.s_pad * P.s_pad;
+        q.lde = (int)P.s_pad;
+        e = timed(DION2_PHASE_NS_POLY, f3, 1, stream, [&] { return launch_gemm(q, EPI_QPOLY, 3, stream); });
+        if (e != hipSuccess) return e;
+        if (t > 0) {
+            GemmArgs p = sym3_args(P, qh, ql, Ph[cur], Pl[cur], Ph[1 - cur], Pl[1 - cur]);
+            e = timed(DION2_PHASE_NS_POLY, f3, 1, stream, [&] { return launch_gemm(p, EPI_SPLIT, 3, stream); });
+            if (e != hipSuccess) return e;
+            cur = 1 - cur;
+        }
+        if (t + 1 < ns_steps) {
+            GemmArgs u = sym3_args(P, qh, ql, Ah, Al, sq[SQ_THI], sq[SQ_TLO]);
+            e = timed(DION2_PHASE_NS_POLY, f3, 1, stream, [&] { return launch_gemm(u, EPI_SPLIT, 3, stream); });
+            if (e != hipSuccess) return e;
+            GemmArgs v = sym3_args(P, qh, ql, sq[SQ_THI], sq[SQ_TLO], Ah, Al);
+            e = timed(DION2_PHASE_NS_POLY, f3, 1, stream, [&] { return launch_gemm(v, EPI_SPLIT, 3, stream); });
+            if (e != hipSuccess) return e;
+        }
+    }
+    // O = (P_hi + P_lo) Z
+    GemmArgs x = right_args(P, Ph[cur], Pl[cur], Z);
+    final_output(P, x, O);
+    return timed(DION2_PHASE_NS_UPDATE, 4.0 * s_r * s_r * l_r * nb, 1, stream,
+                 [&] { return launch_gemm(x, EPI_FINAL, 2, stream); });
+}
+
 // ------------------------------------------------------------------ step
 
 struct Tables {
@@ -320,12 +498,12 @@ int run_step(const Plan& P, void* W, float* M, const void* G, const Tables* tabs
     double* sq = reinterpret_cast<double*>(ws + P.o_sq);
     int32_t* sel = reinterpret_cast<int32_t*>(ws + P.o_sel);
     double* scale = reinterpret_cast<double*>(ws + P.o_scale);
-    uint16_t* L = reinterpret_cast<uint16_t*>(ws + P.o_L);
-    uint16_t* LT = reinterpret_cast<uint16_t*>(ws + P.o_LT);
+    // compact matrix in its wide orientation: L [kpad][opad] or L^T [opad][kpad]
+    uint16_t* Z0 = reinterpret_cast<uint16_t*>(ws + P.o_Z);
     uint16_t* Z1 = reinterpret_cast<uint16_t*>(ws + P.o_Z1);
-    uint16_t* Ahi = reinterpret_cast<uint16_t*>(ws + P.o_Ahi);
-    uint16_t* Alo = reinterpret_cast<uint16_t*>(ws + P.o_Alo);
-    uint16_t* Bm = reinterpret_cast<uint16_t*>(ws + P.o_B);
+    uint16_t* sbuf[SQ_GRAM_COUNT];
+    for (int i = 0; i < SQ_GRAM_COUNT; ++i)
+        sbuf[i] = reinterpret_cast<uint16_t*>(ws + P.o_S + (size_t)i * P.S_bytes);
     float* O = reinterpret_cast<float*>(ws + P.o_O);
 
     // K1
@@ -376,8 +554,8 @@ int run_step(const Plan& P, void* W, float* M, const void* G, const Tables* tabs
     ga.scale = scale;
     ga.mu = mu;
     ga.decay = opt.decay_all ? 0 : 1;
-    ga.L = L;
-    ga.LT = LT;
+    ga.L = P.z_is_L ? Z0 : nullptr;
+    ga.LT = P.z_is_L ? nullptr : Z0;
     ga.O = ns_steps == 0 ? O : nullptr;
     e = timed(DION2_PHASE_GATHER, sel_el * 8.0, 1, stream,
               [&] { return launch_gather(ga, P.axis, stream); });
@@ -389,93 +567,11 @@ int run_step(const Plan& P, void* W, float* M, const void* G, const Tables* tabs
     }
 
     // K4: Newton-Schulz
-    const double s_r = (double)(P.k < P.d_oth ? P.k : P.d_oth);   // unpadded sides
-    const double l_r = (double)(P.k < P.d_oth ? P.d_oth : P.k);
-    const int64_t sZ = P.s_pad * P.l_pad;
-    const int64_t sA = P.s_pad * P.s_pad;
-    // Z is the wide orientation of the compact matrix; the iteration
-    // ping-pongs it between its gather buffer and Z1.
-    uint16_t* zbuf[2] = {P.z_is_L ? L : LT, Z1};
-    int cur = 0;
-    for (int t = 0; t < ns_steps; ++t) {
-        const float* cf = opt.ns_coeffs ? opt.ns_coeffs + 3 * t : kMuonQuintic;
-        uint16_t* Z = zbuf[cur];
-        uint16_t* Zn = zbuf[1 - cur];
-
-        // A = Z Z^T, split into bf16 hi + lo
-        GemmArgs g{};
-        g.batch = P.batch;
-        g.A0 = Z;
-        g.B0 = Z;
-        g.sA = g.sB = sZ;
-        g.M = g.N = (int)P.s_pad;
-        g.K = (int)P.l_pad;
-        g.lda = g.ldb = (int)P.l_pad;
-        g.out0 = Ahi;
-        g.out1 = Alo;
-        g.sOut0 = g.sOut1 = sA;
-        g.ldo0 = g.ldo1 = (int)P.s_pad;
-        e = timed(DION2_PHASE_NS_GRAM, 2.0 * s_r * s_r * l_r * P.batch, 1, stream,
-                  [&] { return launch_gemm(g, EPI_SPLIT, stream); });
-        if (e != hipSuccess) return hip_fail(e, "launch K4 Gram");
-
-        // B = b A + c A^2 (A^2 = A A^T in three bf16 passes)
-        GemmArgs q{};
-        q.batch = P.batch;
-        q.A0 = Ahi;
-        q.A1 = Alo;
-        q.B0 = Ahi;
-        q.B1 = Alo;
-        q.sA = q.sB = sA;
-        q.M = q.N = q.K = (int)P.s_pad;
-        q.lda = q.ldb = (int)P.s_pad;
-        q.cb = cf[1];
-        q.cc = cf[2];
-        q.E0 = Ahi;
-        q.E1 = Alo;
-        q.sE = sA;
-        q.lde = (int)P.s_pad;
-        q.out0 = Bm;
-        q.sOut0 = sA;
-        q.ldo0 = (int)P.s_pad;
-        e = timed(DION2_PHASE_NS_POLY, 2.0 * s_r * s_r * s_r * P.batch, 1, stream,
-                  [&] { return launch_gemm(q, EPI_POLY, stream); });
-        if (e != hipSuccess) return hip_fail(e, "launch K4 polynomial");
-
-        // Z' = a Z + B Z (B operand: Z itself, [K = s][N = l]; a Z in the epilogue)
-        GemmArgs x{};
-        x.batch = P.batch;
-        x.A0 = Bm;
-        x.B0 = Z;
-        x.sA = sA;
-        x.sB = sZ;
-        x.M = (int)P.s_pad;
-        x.N = (int)P.l_pad;
-        x.K = (int)P.s_pad;
-        x.lda = (int)P.s_pad;
-        x.ldb = (int)P.l_pad;
-        x.ca = cf[0];
-        x.E0 = Z;
-        x.sE = sZ;
-        x.lde = (int)P.l_pad;
-        if (t + 1 < ns_steps) {
-            x.out0 = Zn;
-            x.sOut0 = sZ;
-            x.ldo0 = (int)P.l_pad;
-            e = timed(DION2_PHASE_NS_UPDATE, 2.0 * s_r * s_r * l_r * P.batch, 1, stream,
-                      [&] { return launch_gemm(x, EPI_UPDATE, stream); });
-        } else {
-            // O in the L layout [kpad][opad]
-            x.out0 = O;
-            x.sOut0 = P.kpad * P.opad;
-            x.ldo0 = (int)P.opad;
-            x.out_transposed = P.z_is_L ? 0 : 1;
-            e = timed(DION2_PHASE_NS_UPDATE, 2.0 * s_r * s_r * l_r * P.batch, 1, stream,
-                      [&] { return launch_gemm(x, EPI_FINAL, stream); });
-        }
-        if (e != hipSuccess) return hip_fail(e, "launch K4 update");
-        cur = 1 - cur;
+    if (ns_steps > 0) {   // with no step the gather has written O
+        e = P.gram ? ns_gram(P, Z0, sbuf, O, ns_steps, opt, stream)
+                   : ns_direct(P, Z0, Z1, sbuf, O, ns_steps, opt, stream);
     }
+    if (e != hipSuccess) return hip_fail(e, "launch K4 Newton-Schulz");
 
     // K5
     ApplyArgs aa{};
@@ -536,7 +632,7 @@ int step_impl(void* W, float* M, const void* G, const Tables* tabs, int batch, i
     if (opt_in) opt = *opt_in;
     else dion2_options_init(&opt);
     Plan P;
-    int st = make_plan(batch, rows, cols, alpha, axis, &P);
+    int st = make_plan(batch, rows, cols, alpha, axis, opt.ns_form, &P);
     if (st != DION2_OK) return st;
     st = validate_common(mu, lr, ns_steps, opt);
     if (st != DION2_OK) return st;
@@ -576,6 +672,7 @@ void dion2_options_init(dion2_options* opt) {
     opt->ns_coeffs = nullptr;
     opt->ns_eps = 1e-7f;
     opt->decay_all = 0;
+    opt->ns_form = DION2_NS_AUTO;
 }
 
 int dion2_step(void* W, float* M, const void* G, int64_t rows, int64_t cols, float alpha,
@@ -607,14 +704,14 @@ int dion2_step_ex(void* W, float* M, const void* G, int batch, int64_t rows, int
 
 size_t dion2_workspace_size(int batch, int64_t rows, int64_t cols, float alpha, int axis) {
     Plan P;
-    if (make_plan(batch, rows, cols, alpha, axis, &P) != DION2_OK) return 0;
+    if (make_plan(batch, rows, cols, alpha, axis, DION2_NS_AUTO, &P) != DION2_OK) return 0;
     return P.total;
 }
 
 int dion2_plan_info(int64_t rows, int64_t cols, float alpha, int axis, int64_t* k_out,
                     int* axis_out) {
     Plan P;
-    int st = make_plan(1, rows, cols, alpha, axis, &P);
+    int st = make_plan(1, rows, cols, alpha, axis, DION2_NS_AUTO, &P);
     if (st != DION2_OK) return st;
     if (k_out) *k_out = P.k;
     if (axis_out) *axis_out = P.axis;

@@ -136,8 +136,8 @@ struct GatherArgs {
     const double* scale;
     float mu;
     int decay;         // 1: M[K] <- mu M[K] here
-    uint16_t* L;       // [batch][kpad][opad]
-    uint16_t* LT;      // [batch][opad][kpad]
+    uint16_t* L;       // nullable [batch][kpad][opad]
+    uint16_t* LT;      // nullable [batch][opad][kpad] (one of L, LT is written)
     float* O;          // nullable: fp32 copy in L layout (no Newton-Schulz step)
 };
 hipError_t launch_gather(const GatherArgs& a, int axis, hipStream_t s);
@@ -150,12 +150,20 @@ struct DecayAllArgs {
 };
 hipError_t launch_decay_all(const DecayAllArgs& a, hipStream_t s);
 
-// Newton-Schulz GEMMs, C = A B with A given as rows [M][K]:
-//   EPI_SPLIT  (B as rows [N][K]): out0 = bf16(C), out1 = bf16(C - out0)
-//   EPI_POLY   (B as rows [N][K], three passes hi/lo): out0 = bf16(cb (E0 + E1) + cc C)
-//   EPI_UPDATE (B as [K][N]): out0 = bf16(ca E0 + C)
-//   EPI_FINAL  (B as [K][N]): out0 = ca E0 + C in fp32, or its transpose when out_transposed
-enum GemmEpi { EPI_SPLIT = 0, EPI_POLY = 1, EPI_UPDATE = 2, EPI_FINAL = 3 };
+// Newton-Schulz GEMMs, C = A B with A given as rows [M][K]. With npass = 3
+// both operands come as bf16 hi + lo pairs (A0/A1, B0/B1) and
+// C = A0 B0 + A0 B1 + A1 B0; with npass = 2 only A does (C = A0 B0 + A1 B0).
+//   EPI_SPLIT  (B as rows [N][K], symmetric C; npass 1 or 3):
+//              out0 = bf16(C), out1 = bf16(C - out0)
+//   EPI_POLY   (B as rows [N][K], npass 3): out0 = bf16(cb (E0 + E1) + cc C)
+//   EPI_QPOLY  (B as rows [N][K], npass 3): Q = ca I + cb (E0 + E1) + cc C,
+//              out0 = bf16(Q), out1 = bf16(Q - out0)
+//   EPI_UPDATE (B as [K][N], npass 1): out0 = bf16(ca E0 + C)
+//   EPI_FINAL  (B as [K][N], npass 1 or 2): out0 = ca E0 + C in fp32 (no
+//              E0 term when E0 is null), or its transpose when out_transposed
+// The symmetric products (EPI_SPLIT, EPI_POLY, EPI_QPOLY) compute the tiles
+// on and above the diagonal and mirror them.
+enum GemmEpi { EPI_SPLIT = 0, EPI_POLY = 1, EPI_UPDATE = 2, EPI_FINAL = 3, EPI_QPOLY = 4 };
 struct GemmArgs {
     const uint16_t* A0; const uint16_t* A1;   // A operand(s), [M][K] ld lda
     const uint16_t* B0; const uint16_t* B1;   // B operand(s), [N][K] or [K][N], ld ldb
@@ -169,7 +177,7 @@ struct GemmArgs {
     void* out1; int64_t sOut1; int ldo1;
     int out_transposed;                        // EPI_FINAL: write out0[j][i]
 };
-hipError_t launch_gemm(const GemmArgs& a, GemmEpi epi, hipStream_t s);
+hipError_t launch_gemm(const GemmArgs& a, GemmEpi epi, int npass, hipStream_t s);
 
 struct ApplyArgs {
     MatSet ms;

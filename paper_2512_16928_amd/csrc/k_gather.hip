@@ -5,11 +5,11 @@
 //   LT[j][p] = L[p][j]                                       [opad][kpad]
 //   M_line(K[p]) <- fl32(mu * M_line(K[p]))                   (Algorithm 1, decay step)
 //
-// Both layouts are written so every Newton-Schulz GEMM reads K-contiguous
-// operands. One 256-thread block handles a 64 x 64 tile of (line p, other
-// index j): the side that is contiguous in M is read and written directly,
-// the other side goes through an LDS tile. Tiles cover the padded extents,
-// and padding (p >= k or j >= d_oth) is written as zero.
+// Only the orientation Newton-Schulz iterates on is written (the wide one;
+// the other pointer is null). One 256-thread block handles a 64 x 64 tile of
+// (line p, other index j): the side that is contiguous in M is read and
+// written directly, the other side goes through an LDS tile. Tiles cover the
+// padded extents, and padding (p >= k or j >= d_oth) is written as zero.
 #include "dion2_device.h"
 
 namespace dion2 {
@@ -28,8 +28,8 @@ __global__ __launch_bounds__(kThreads) void gather_rows(GatherArgs a) {
     float* __restrict__ M = a.ms.m(b);
     const int32_t* __restrict__ K = a.sel + (int64_t)b * a.k;
     const float sc = (float)a.scale[b];
-    uint16_t* __restrict__ L = a.L + (int64_t)b * a.kpad * a.opad;
-    uint16_t* __restrict__ LT = a.LT + (int64_t)b * a.opad * a.kpad;
+    uint16_t* __restrict__ L = a.L ? a.L + (int64_t)b * a.kpad * a.opad : nullptr;
+    uint16_t* __restrict__ LT = a.LT ? a.LT + (int64_t)b * a.opad * a.kpad : nullptr;
     float* __restrict__ O = a.O ? a.O + (int64_t)b * a.kpad * a.opad : nullptr;
     const int j = j0 + 4 * tx;
 #pragma unroll
@@ -59,14 +59,17 @@ __global__ __launch_bounds__(kThreads) void gather_rows(GatherArgs a) {
                 }
             }
         }
-        uint2 packed;
-        packed.x = (uint32_t)f32_to_bf16(x[0]) | ((uint32_t)f32_to_bf16(x[1]) << 16);
-        packed.y = (uint32_t)f32_to_bf16(x[2]) | ((uint32_t)f32_to_bf16(x[3]) << 16);
-        *reinterpret_cast<uint2*>(L + (int64_t)p * a.opad + j) = packed;
+        if (L) {
+            uint2 packed;
+            packed.x = (uint32_t)f32_to_bf16(x[0]) | ((uint32_t)f32_to_bf16(x[1]) << 16);
+            packed.y = (uint32_t)f32_to_bf16(x[2]) | ((uint32_t)f32_to_bf16(x[3]) << 16);
+            *reinterpret_cast<uint2*>(L + (int64_t)p * a.opad + j) = packed;
+        }
         if (O) *reinterpret_cast<float4*>(O + (int64_t)p * a.opad + j) = make_float4(x[0], x[1], x[2], x[3]);
 #pragma unroll
         for (int v = 0; v < 4; ++v) tile[pl][4 * tx + v] = x[v];
     }
+    if (!LT) return;   // uniform over the block
     __syncthreads();
     // transposed: LT[j][p], p contiguous
     const int p = p0 + 4 * tx;
@@ -92,8 +95,8 @@ __global__ __launch_bounds__(kThreads) void gather_cols(GatherArgs a) {
     float* __restrict__ M = a.ms.m(b);
     const int32_t* __restrict__ K = a.sel + (int64_t)b * a.k;
     const float sc = (float)a.scale[b];
-    uint16_t* __restrict__ L = a.L + (int64_t)b * a.kpad * a.opad;
-    uint16_t* __restrict__ LT = a.LT + (int64_t)b * a.opad * a.kpad;
+    uint16_t* __restrict__ L = a.L ? a.L + (int64_t)b * a.kpad * a.opad : nullptr;
+    uint16_t* __restrict__ LT = a.LT ? a.LT + (int64_t)b * a.opad * a.kpad : nullptr;
     float* __restrict__ O = a.O ? a.O + (int64_t)b * a.kpad * a.opad : nullptr;
     const int p = p0 + 4 * tx;
     int col[4];
@@ -115,13 +118,16 @@ __global__ __launch_bounds__(kThreads) void gather_cols(GatherArgs a) {
                 }
             }
         }
-        uint2 packed;
-        packed.x = (uint32_t)f32_to_bf16(x[0]) | ((uint32_t)f32_to_bf16(x[1]) << 16);
-        packed.y = (uint32_t)f32_to_bf16(x[2]) | ((uint32_t)f32_to_bf16(x[3]) << 16);
-        *reinterpret_cast<uint2*>(LT + (int64_t)r * a.kpad + p) = packed;
+        if (LT) {
+            uint2 packed;
+            packed.x = (uint32_t)f32_to_bf16(x[0]) | ((uint32_t)f32_to_bf16(x[1]) << 16);
+            packed.y = (uint32_t)f32_to_bf16(x[2]) | ((uint32_t)f32_to_bf16(x[3]) << 16);
+            *reinterpret_cast<uint2*>(LT + (int64_t)r * a.kpad + p) = packed;
+        }
 #pragma unroll
         for (int v = 0; v < 4; ++v) tile[4 * tx + v][rl] = x[v];
     }
+    if (!L && !O) return;   // uniform over the block
     __syncthreads();
     // L[p][r], r contiguous
     const int r = r0 + 4 * tx;
@@ -131,10 +137,12 @@ __global__ __launch_bounds__(kThreads) void gather_cols(GatherArgs a) {
         float x[4];
 #pragma unroll
         for (int v = 0; v < 4; ++v) x[v] = tile[pl][4 * tx + v];
-        uint2 packed;
-        packed.x = (uint32_t)f32_to_bf16(x[0]) | ((uint32_t)f32_to_bf16(x[1]) << 16);
-        packed.y = (uint32_t)f32_to_bf16(x[2]) | ((uint32_t)f32_to_bf16(x[3]) << 16);
-        *reinterpret_cast<uint2*>(L + (int64_t)(p0 + pl) * a.opad + r) = packed;
+        if (L) {
+            uint2 packed;
+            packed.x = (uint32_t)f32_to_bf16(x[0]) | ((uint32_t)f32_to_bf16(x[1]) << 16);
+            packed.y = (uint32_t)f32_to_bf16(x[2]) | ((uint32_t)f32_to_bf16(x[3]) << 16);
+            *reinterpret_cast<uint2*>(L + (int64_t)(p0 + pl) * a.opad + r) = packed;
+        }
         if (O) *reinterpret_cast<float4*>(O + (int64_t)(p0 + pl) * a.opad + r) = make_float4(x[0], x[1], x[2], x[3]);
     }
 }

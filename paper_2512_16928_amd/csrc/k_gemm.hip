@@ -66,7 +66,7 @@ struct Tile {
     static constexpr int TM = BM / WM, TN = BN / WN;     // wave tile
     static constexpr int FM = TM / 32, FN = TN / 32;     // MFMA blocks per wave
     static constexpr int NA = NPASS == 1 ? 1 : 2;        // A operand tiles (hi[, lo])
-    static constexpr int NB = NPASS == 1 ? 1 : 2;        // B operand tiles
+    static constexpr int NB = NPASS == 3 ? 2 : 1;        // B operand tiles
     // K-major tiles: rows of BK bf16 (pitch PK bytes), CPR chunks of 16 B
     static constexpr int PK = BK * 2;
     static constexpr int CPR = BK / 8;
@@ -85,7 +85,8 @@ struct Tile {
     static_assert(BK % 16 == 0 && (BK == 32 || BK == 64), "BK of 32 or 64");
     static_assert(A_BYTES % 1024 == 0 && B_BYTES % 1024 == 0, "tiles are whole 1 KB blocks");
     static_assert(STAGE_INSTS % WAVES == 0, "load instructions split evenly over waves");
-    static_assert(!BT || (NPASS == 1 && BN == 128), "the [K][N] B operand is single-pass, BN 128");
+    static_assert(NPASS >= 1 && NPASS <= 3, "one to three passes");
+    static_assert(!BT || (NPASS <= 2 && BN == 128), "the [K][N] B operand: one or two passes, BN 128");
     static_assert(S >= 2 && S <= 4, "two to four stages");
 };
 
@@ -204,10 +205,12 @@ __device__ __forceinline__ void mma_slice(f32x16 (&acc)[T::FM][T::FN], const uns
                     fb0[slot][j] = *reinterpret_cast<const bf16x8*>(sb0 + kmajor_off<T>(brow + j * 32, c));
                 }
             }
-            if constexpr (NPASS == 3) {
+            if constexpr (NPASS >= 2) {
 #pragma unroll
                 for (int i = 0; i < T::FM; ++i)
                     fa1[slot][i] = *reinterpret_cast<const bf16x8*>(sa1 + kmajor_off<T>(arow + i * 32, c));
+            }
+            if constexpr (NPASS == 3) {
 #pragma unroll
                 for (int j = 0; j < T::FN; ++j)
                     fb1[slot][j] = *reinterpret_cast<const bf16x8*>(sb1 + kmajor_off<T>(brow + j * 32, c));
@@ -219,13 +222,47 @@ __device__ __forceinline__ void mma_slice(f32x16 (&acc)[T::FM][T::FN], const uns
             for (int i = 0; i < T::FM; ++i)
 #pragma unroll
                 for (int j = 0; j < T::FN; ++j) {
-                    if constexpr (NPASS == 3) {
+                    if constexpr (NPASS == 3)
                         acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa0[slot][i], fb1[slot][j], acc[i][j], 0, 0, 0);
+                    if constexpr (NPASS >= 2)
                         acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa1[slot][i], fb0[slot][j], acc[i][j], 0, 0, 0);
-                    }
                     acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa0[slot][i], fb0[slot][j], acc[i][j], 0, 0, 0);
                 }
         }
+    }
+}
+
+// Store 16 consecutive outputs of row `orow` from column `ocol` in the
+// epilogue's output form: bf16 hi + lo (EPI_SPLIT, EPI_QPOLY), bf16
+// (EPI_POLY, EPI_UPDATE) or fp32 (EPI_FINAL); 16-byte stores.
+template <int EPI>
+__device__ __forceinline__ void store16(const GemmArgs& a, int b, int64_t orow, int64_t ocol,
+                                        const float (&v)[16]) {
+    if constexpr (EPI == EPI_SPLIT || EPI == EPI_QPOLY) {
+        uint32_t h[8], l[8];
+#pragma unroll
+        for (int q = 0; q < 8; ++q) {
+            const uint16_t h0 = f32_to_bf16(v[2 * q]), h1 = f32_to_bf16(v[2 * q + 1]);
+            h[q] = (uint32_t)h0 | ((uint32_t)h1 << 16);
+            l[q] = pack2(v[2 * q] - bf16_bits_to_f32(h0), v[2 * q + 1] - bf16_bits_to_f32(h1));
+        }
+        uint16_t* hp = static_cast<uint16_t*>(a.out0) + (int64_t)b * a.sOut0 + orow * a.ldo0 + ocol;
+        uint16_t* lp = static_cast<uint16_t*>(a.out1) + (int64_t)b * a.sOut1 + orow * a.ldo1 + ocol;
+        reinterpret_cast<uint4*>(hp)[0] = make_uint4(h[0], h[1], h[2], h[3]);
+        reinterpret_cast<uint4*>(hp)[1] = make_uint4(h[4], h[5], h[6], h[7]);
+        reinterpret_cast<uint4*>(lp)[0] = make_uint4(l[0], l[1], l[2], l[3]);
+        reinterpret_cast<uint4*>(lp)[1] = make_uint4(l[4], l[5], l[6], l[7]);
+    } else if constexpr (EPI == EPI_POLY || EPI == EPI_UPDATE) {
+        uint16_t* op = static_cast<uint16_t*>(a.out0) + (int64_t)b * a.sOut0 + orow * a.ldo0 + ocol;
+        reinterpret_cast<uint4*>(op)[0] = make_uint4(pack2(v[0], v[1]), pack2(v[2], v[3]),
+                                                     pack2(v[4], v[5]), pack2(v[6], v[7]));
+        reinterpret_cast<uint4*>(op)[1] = make_uint4(pack2(v[8], v[9]), pack2(v[10], v[11]),
+                                                     pack2(v[12], v[13]), pack2(v[14], v[15]));
+    } else {
+        float* op = static_cast<float*>(a.out0) + (int64_t)b * a.sOut0 + orow * a.ldo0 + ocol;
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+            reinterpret_cast<float4*>(op)[q] = make_float4(v[4 * q], v[4 * q + 1], v[4 * q + 2], v[4 * q + 3]);
     }
 }
 
@@ -264,7 +301,7 @@ __global__ __launch_bounds__(T::THREADS) void gemm(GemmArgs a) {
     const uint16_t* abase[2];
     const uint16_t* bbase[2];
     abase[0] = a.A0 + (int64_t)b * a.sA + (int64_t)row0 * a.lda;
-    abase[1] = NPASS == 3 ? a.A1 + (int64_t)b * a.sA + (int64_t)row0 * a.lda : abase[0];
+    abase[1] = NPASS >= 2 ? a.A1 + (int64_t)b * a.sA + (int64_t)row0 * a.lda : abase[0];
     if constexpr (T::BT) {
         bbase[0] = bbase[1] = a.B0 + (int64_t)b * a.sB + col0;
     } else {
@@ -276,9 +313,9 @@ __global__ __launch_bounds__(T::THREADS) void gemm(GemmArgs a) {
     // fetched first so their latency hides behind the main loop.
     const int er = lane >> 1;          // epilogue: row (or transposed row) of this lane
     const int ec = (lane & 1) * 16;    // epilogue: 16 consecutive columns
-    constexpr bool kPreE0 = EPI == EPI_POLY || EPI == EPI_UPDATE || EPI == EPI_FINAL;
-    constexpr bool kPreE1 = EPI == EPI_POLY;
-    const bool pre = kPreE0 && !(EPI == EPI_FINAL && a.out_transposed);
+    constexpr bool kPreE0 = EPI == EPI_POLY || EPI == EPI_QPOLY || EPI == EPI_UPDATE || EPI == EPI_FINAL;
+    constexpr bool kPreE1 = EPI == EPI_POLY || EPI == EPI_QPOLY;
+    const bool pre = kPreE0 && a.E0 != nullptr && !(EPI == EPI_FINAL && a.out_transposed);
     uint4 e0[T::FM][T::FN][2], e1[T::FM][T::FN][2];
     if (pre) {
 #pragma unroll
@@ -356,10 +393,8 @@ __global__ __launch_bounds__(T::THREADS) void gemm(GemmArgs a) {
             const int64_t orow = transposed ? Cc + er : R + er;
             const int64_t ocol = transposed ? R + ec : Cc + ec;
             if constexpr (EPI == EPI_UPDATE || EPI == EPI_FINAL) {
-                // a Z at this lane's 16 block entries (row zr, columns zc..zc+15)
-                const int64_t zr = transposed ? R + ec : R + er;
-                const int64_t zc = transposed ? Cc + er : Cc + ec;
-                if (!transposed) {
+                // + a Z at this lane's 16 entries (none when E0 is null)
+                if (pre) {
                     const uint4 z0 = e0[i][j][0];
                     const uint4 z1 = e0[i][j][1];
                     const uint32_t zw[8] = {z0.x, z0.y, z0.z, z0.w, z1.x, z1.y, z1.z, z1.w};
@@ -368,86 +403,41 @@ __global__ __launch_bounds__(T::THREADS) void gemm(GemmArgs a) {
                         v[2 * q] += a.ca * bf16_bits_to_f32(zw[q] & 0xffffu);
                         v[2 * q + 1] += a.ca * bf16_bits_to_f32(zw[q] >> 16);
                     }
-                } else {
+                } else if (transposed && a.E0) {
                     // transposed output: entry q is Z[R + ec + q][Cc + er]
-                    const uint16_t* zp = a.E0 + (int64_t)b * a.sE + zr * a.lde + zc;
+                    const uint16_t* zp = a.E0 + (int64_t)b * a.sE + (int64_t)(R + ec) * a.lde + Cc + er;
 #pragma unroll
                     for (int q = 0; q < 16; ++q) v[q] += a.ca * bf16_bits_to_f32(zp[(int64_t)q * a.lde]);
                 }
-            }
-            if constexpr (EPI == EPI_SPLIT) {
-                uint32_t h[8], l[8];
-#pragma unroll
-                for (int q = 0; q < 8; ++q) {
-                    const uint16_t h0 = f32_to_bf16(v[2 * q]), h1 = f32_to_bf16(v[2 * q + 1]);
-                    h[q] = (uint32_t)h0 | ((uint32_t)h1 << 16);
-                    l[q] = pack2(v[2 * q] - bf16_bits_to_f32(h0), v[2 * q + 1] - bf16_bits_to_f32(h1));
-                }
-                uint16_t* hp = static_cast<uint16_t*>(a.out0) + (int64_t)b * a.sOut0 + orow * a.ldo0 + ocol;
-                uint16_t* lp = static_cast<uint16_t*>(a.out1) + (int64_t)b * a.sOut1 + orow * a.ldo1 + ocol;
-                reinterpret_cast<uint4*>(hp)[0] = make_uint4(h[0], h[1], h[2], h[3]);
-                reinterpret_cast<uint4*>(hp)[1] = make_uint4(h[4], h[5], h[6], h[7]);
-                reinterpret_cast<uint4*>(lp)[0] = make_uint4(l[0], l[1], l[2], l[3]);
-                reinterpret_cast<uint4*>(lp)[1] = make_uint4(l[4], l[5], l[6], l[7]);
-                if (SYM && row0 != col0) {
-                    float t[16];
-                    mirror16<T>(stage, v, t, er, ec);
-                    uint32_t th[8], tl[8];
-#pragma unroll
-                    for (int q = 0; q < 8; ++q) {
-                        const uint16_t h0 = f32_to_bf16(t[2 * q]), h1 = f32_to_bf16(t[2 * q + 1]);
-                        th[q] = (uint32_t)h0 | ((uint32_t)h1 << 16);
-                        tl[q] = pack2(t[2 * q] - bf16_bits_to_f32(h0), t[2 * q + 1] - bf16_bits_to_f32(h1));
-                    }
-                    const int64_t mrow = Cc + er, mcol = R + ec;
-                    uint16_t* mh = static_cast<uint16_t*>(a.out0) + (int64_t)b * a.sOut0 + mrow * a.ldo0 + mcol;
-                    uint16_t* ml = static_cast<uint16_t*>(a.out1) + (int64_t)b * a.sOut1 + mrow * a.ldo1 + mcol;
-                    reinterpret_cast<uint4*>(mh)[0] = make_uint4(th[0], th[1], th[2], th[3]);
-                    reinterpret_cast<uint4*>(mh)[1] = make_uint4(th[4], th[5], th[6], th[7]);
-                    reinterpret_cast<uint4*>(ml)[0] = make_uint4(tl[0], tl[1], tl[2], tl[3]);
-                    reinterpret_cast<uint4*>(ml)[1] = make_uint4(tl[4], tl[5], tl[6], tl[7]);
-                }
-            } else if constexpr (EPI == EPI_POLY) {
-                // B = b (A_hi + A_lo) + c A^2
+            } else if constexpr (EPI == EPI_POLY || EPI == EPI_QPOLY) {
+                // b (A_hi + A_lo) + c A^2 [+ a I]
                 const uint4 h0 = e0[i][j][0];
                 const uint4 h1 = e0[i][j][1];
                 const uint4 l0 = e1[i][j][0];
                 const uint4 l1 = e1[i][j][1];
                 const uint32_t hw[8] = {h0.x, h0.y, h0.z, h0.w, h1.x, h1.y, h1.z, h1.w};
                 const uint32_t lw[8] = {l0.x, l0.y, l0.z, l0.w, l1.x, l1.y, l1.z, l1.w};
-                uint32_t o[8];
 #pragma unroll
                 for (int q = 0; q < 8; ++q) {
                     const float a0 = bf16_bits_to_f32(hw[q] & 0xffffu) + bf16_bits_to_f32(lw[q] & 0xffffu);
                     const float a1 = bf16_bits_to_f32(hw[q] >> 16) + bf16_bits_to_f32(lw[q] >> 16);
                     v[2 * q] = a.cb * a0 + a.cc * v[2 * q];
                     v[2 * q + 1] = a.cb * a1 + a.cc * v[2 * q + 1];
-                    o[q] = pack2(v[2 * q], v[2 * q + 1]);
                 }
-                uint16_t* op = static_cast<uint16_t*>(a.out0) + (int64_t)b * a.sOut0 + orow * a.ldo0 + ocol;
-                reinterpret_cast<uint4*>(op)[0] = make_uint4(o[0], o[1], o[2], o[3]);
-                reinterpret_cast<uint4*>(op)[1] = make_uint4(o[4], o[5], o[6], o[7]);
-                if (SYM && row0 != col0) {
-                    float t[16];
-                    mirror16<T>(stage, v, t, er, ec);
-                    const int64_t mrow = Cc + er, mcol = R + ec;
-                    uint16_t* mp = static_cast<uint16_t*>(a.out0) + (int64_t)b * a.sOut0 + mrow * a.ldo0 + mcol;
-                    reinterpret_cast<uint4*>(mp)[0] = make_uint4(pack2(t[0], t[1]), pack2(t[2], t[3]),
-                                                                 pack2(t[4], t[5]), pack2(t[6], t[7]));
-                    reinterpret_cast<uint4*>(mp)[1] = make_uint4(pack2(t[8], t[9]), pack2(t[10], t[11]),
-                                                                 pack2(t[12], t[13]), pack2(t[14], t[15]));
-                }
-            } else if constexpr (EPI == EPI_UPDATE) {
-                uint16_t* op = static_cast<uint16_t*>(a.out0) + (int64_t)b * a.sOut0 + orow * a.ldo0 + ocol;
-                reinterpret_cast<uint4*>(op)[0] = make_uint4(pack2(v[0], v[1]), pack2(v[2], v[3]),
-                                                             pack2(v[4], v[5]), pack2(v[6], v[7]));
-                reinterpret_cast<uint4*>(op)[1] = make_uint4(pack2(v[8], v[9]), pack2(v[10], v[11]),
-                                                             pack2(v[12], v[13]), pack2(v[14], v[15]));
-            } else {
-                float* op = static_cast<float*>(a.out0) + (int64_t)b * a.sOut0 + orow * a.ldo0 + ocol;
+                if constexpr (EPI == EPI_QPOLY) {
+                    // entry (R + er, Cc + ec + q) is on the diagonal iff er == ec + q
+                    if (R == Cc) {
 #pragma unroll
-                for (int q = 0; q < 4; ++q)
-                    reinterpret_cast<float4*>(op)[q] = make_float4(v[4 * q], v[4 * q + 1], v[4 * q + 2], v[4 * q + 3]);
+                        for (int q = 0; q < 16; ++q)
+                            if (er == ec + q) v[q] += a.ca;
+                    }
+                }
+            }
+            store16<EPI>(a, b, orow, ocol, v);
+            if (SYM && row0 != col0) {
+                float t[16];
+                mirror16<T>(stage, v, t, er, ec);
+                store16<EPI>(a, b, (int64_t)Cc + er, (int64_t)R + ec, t);
             }
             __builtin_amdgcn_wave_barrier();   // the stage tile is rewritten next
         }
@@ -469,21 +459,34 @@ hipError_t launch_tile(const GemmArgs& a, hipStream_t s) {
 
 }  // namespace
 
-hipError_t launch_gemm(const GemmArgs& a, GemmEpi epi, hipStream_t s) {
+hipError_t launch_gemm(const GemmArgs& a, GemmEpi epi, int npass, hipStream_t s) {
     // Tile choices measured on MI355X at the Newton-Schulz shapes: 128 x 128
     // tiles keep enough blocks in flight for s = 512; from s = 1024 the
     // symmetric Gram product runs faster on 256 x 256 tiles of 8 waves.
     using TG = Tile<1, 0, 128, 128, 32, 2, 2, 4>;    // Gram
     using TGL = Tile<1, 0, 256, 256, 32, 4, 2, 3>;   // Gram, large s
-    using TP = Tile<3, 0, 128, 128, 32, 4, 2, 2>;    // polynomial (three passes)
+    using TP = Tile<3, 0, 128, 128, 32, 4, 2, 2>;    // three-pass symmetric products
     using TU = Tile<1, 1, 128, 128, 32, 2, 2, 3>;    // update (B operand [K][N])
+    using TU2 = Tile<2, 1, 128, 128, 32, 2, 2, 3>;   // two-pass final product
     switch (epi) {
         case EPI_SPLIT:
+            if (npass == 3) return launch_tile<3, EPI_SPLIT, TP, true>(a, s);
+            if (npass != 1) break;
             if (a.M >= 1024 && a.M % 256 == 0) return launch_tile<1, EPI_SPLIT, TGL, true>(a, s);
             return launch_tile<1, EPI_SPLIT, TG, true>(a, s);
-        case EPI_POLY: return launch_tile<3, EPI_POLY, TP, true>(a, s);
-        case EPI_UPDATE: return launch_tile<1, EPI_UPDATE, TU>(a, s);
-        case EPI_FINAL: return launch_tile<1, EPI_FINAL, TU>(a, s);
+        case EPI_POLY:
+            if (npass == 3) return launch_tile<3, EPI_POLY, TP, true>(a, s);
+            break;
+        case EPI_QPOLY:
+            if (npass == 3) return launch_tile<3, EPI_QPOLY, TP, true>(a, s);
+            break;
+        case EPI_UPDATE:
+            if (npass == 1) return launch_tile<1, EPI_UPDATE, TU>(a, s);
+            break;
+        case EPI_FINAL:
+            if (npass == 1) return launch_tile<1, EPI_FINAL, TU>(a, s);
+            if (npass == 2) return launch_tile<2, EPI_FINAL, TU2>(a, s);
+            break;
     }
     return hipErrorInvalidValue;
 }

@@ -1,0 +1,213 @@
+"""Summaries of rocprofv3 CSV output for the Dion2 kernels.
+
+    python -m paper_2512_16928_amd.profsum stats DIR
+        per-kernel and per-phase launch statistics from a
+        `rocprofv3 --kernel-trace --stats -f csv -d DIR` run
+    python -m paper_2512_16928_amd.profsum traffic FETCH_DIR WRITE_DIR --workload W --alpha A
+        HBM bytes per launch of every phase from two `--pmc FETCH_SIZE` and
+        `--pmc WRITE_SIZE` runs, scaled by what the same counters read for
+        the calibration copy (a single elementwise kernel, `torch.neg` of
+        2^28 fp32 values: 1 GiB read, 1 GiB written)
+
+The traffic summary ends with one `traffic ...` line per phase, tagged with
+a hash of the kernel sources it was taken on; bench.py reports a phase's
+traffic only while those sources are unchanged.
+"""
+from __future__ import annotations
+
+import argparse
+import csv
+import glob
+import hashlib
+import os
+import re
+import statistics
+import sys
+
+PKG = os.path.dirname(os.path.abspath(__file__))
+CSRC = os.path.join(PKG, "csrc")
+
+# phase -> kernel source files whose text decides the phase's kernels
+PHASE_SOURCES = {
+    "momentum": ("k_momentum.hip",),
+    "select": ("k_select.hip",),
+    "gather": ("k_gather.hip",),
+    "ns_gram": ("k_gemm.hip",),
+    "ns_poly": ("k_gemm.hip",),
+    "ns_update": ("k_gemm.hip",),
+    "apply": ("k_apply.hip",),
+}
+CALIB_BYTES = float(1 << 30)   # the calibration copy reads and writes this much
+CALIB_PATTERN = "neg_kernel"
+
+
+def source_hash(phase: str) -> str:
+    h = hashlib.sha256()
+    for f in PHASE_SOURCES[phase] + ("dion2_device.h", "dion2_api.hip"):
+        with open(os.path.join(CSRC, f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def _local(kernel: str) -> str:
+    """Demangled name without return type, namespaces and arguments."""
+    k = kernel.replace("(anonymous namespace)::", "")
+    k = k[5:] if k.startswith("void ") else k
+    return k.split("dion2::", 1)[1] if k.startswith("dion2::") else k
+
+
+def phase_of(kernel: str):
+    """Library phase of a demangled kernel name, or None for other kernels."""
+    if "dion2::" not in kernel:
+        return None
+    k = _local(kernel)
+    if k.startswith("momentum"):
+        return "momentum"
+    if k.startswith("select"):
+        return "select"
+    if k.startswith("gather") or k.startswith("decay_all"):
+        return "gather"
+    if k.startswith("apply"):
+        return "apply"
+    m = re.match(r"gemm<(\d+), (?:\(dion2::GemmEpi\))?(\d)", k)
+    if m:
+        return {"0": "ns_gram", "1": "ns_poly", "2": "ns_update", "3": "ns_update"}[m.group(2)]
+    return None
+
+
+def short_name(kernel: str, width: int = 72) -> str:
+    k = _local(kernel).replace("dion2::", "")
+    k = k.split("(dion2", 1)[0] if "dion2::" in kernel else k
+    return k if len(k) <= width else k[: width - 3] + "..."
+
+
+def find_csv(d: str, suffix: str) -> str:
+    hits = sorted(glob.glob(os.path.join(d, "**", f"*{suffix}"), recursive=True))
+    if not hits:
+        sys.exit(f"no *{suffix} under {d}")
+    return hits[-1]
+
+
+def cmd_stats(args):
+    path = find_csv(args.dir, "kernel_stats.csv")
+    rows = list(csv.DictReader(open(path)))
+    total = sum(float(r["TotalDurationNs"]) for r in rows)
+    phases = {}
+    print(f"{'kernel':72s} {'calls':>7s} {'avg us':>9s} {'total ms':>9s} {'%':>6s}")
+    for r in sorted(rows, key=lambda r: -float(r["TotalDurationNs"])):
+        name, calls, tot = r["Name"], int(r["Calls"]), float(r["TotalDurationNs"])
+        ph = phase_of(name)
+        if ph:
+            p = phases.setdefault(ph, [0, 0.0])
+            p[0] += calls
+            p[1] += tot
+        if tot / total < 0.001 and not ph:
+            continue
+        print(f"{short_name(name):72s} {calls:7d} {tot / calls / 1e3:9.2f} {tot / 1e6:9.3f} "
+              f"{100 * tot / total:6.2f}")
+    print()
+    print(f"{'phase':12s} {'launches':>9s} {'avg us/launch':>14s} {'total ms':>9s}")
+    for ph in PHASE_SOURCES:
+        if ph in phases:
+            n, t = phases[ph]
+            print(f"{ph:12s} {n:9d} {t / n / 1e3:14.2f} {t / 1e6:9.3f}")
+
+
+def read_counter(d: str, counter: str):
+    """{dispatch id: (kernel name, grid size, value in bytes)} for one counter."""
+    path = find_csv(d, "counter_collection.csv")
+    out = {}
+    for r in csv.DictReader(open(path)):
+        if r["Counter_Name"] != counter:
+            continue
+        did = int(r["Dispatch_Id"])
+        name, grid, val = r["Kernel_Name"], int(r["Grid_Size"]), float(r["Counter_Value"])
+        prev = out.get(did)
+        out[did] = (name, grid, val * 1024.0 + (prev[2] if prev else 0.0))
+    return out
+
+
+def cmd_traffic(args):
+    fetch = read_counter(args.fetch_dir, "FETCH_SIZE")
+    write = read_counter(args.write_dir, "WRITE_SIZE")
+
+    def calib(data):
+        v = [b for n, _, b in data.values() if CALIB_PATTERN in n]
+        if not v:
+            sys.exit(f"no calibration dispatch ({CALIB_PATTERN}) in the counter output")
+        return statistics.median(v), len(v)
+
+    cf, nf = calib(fetch)
+    cw, nw = calib(write)
+    f_fetch, f_write = CALIB_BYTES / cf, CALIB_BYTES / cw
+    print(f"calibration copy (torch.neg, 2^28 fp32): FETCH_SIZE {cf / 2**30:.3f} GiB "
+          f"({nf} dispatches), WRITE_SIZE {cw / 2**30:.3f} GiB ({nw} dispatches)")
+    print(f"scale factors: fetch x{f_fetch:.3f}, write x{f_write:.3f}")
+    print()
+
+    def per_phase(data, factor):
+        acc = {}
+        for name, _, b in data.values():
+            ph = phase_of(name)
+            if ph:
+                a = acc.setdefault(ph, {}).setdefault(short_name(name), [0, 0.0])
+                a[0] += 1
+                a[1] += b * factor
+        return acc
+
+    pf, pw = per_phase(fetch, f_fetch), per_phase(write, f_write)
+    print(f"{'kernel':72s} {'n':>5s} {'read MiB':>10s} {'write MiB':>10s}  (scaled, per dispatch)")
+    lines = []
+    for ph in PHASE_SOURCES:
+        if ph not in pf or ph not in pw:
+            continue
+        nf_tot = sum(n for n, _ in pf[ph].values())
+        nw_tot = sum(n for n, _ in pw[ph].values())
+        for k in pf[ph]:
+            n, b = pf[ph][k]
+            wn, wb = pw[ph].get(k, (1, 0.0))
+            print(f"{k:72s} {n:5d} {b / n / 2**20:10.2f} {wb / max(wn, 1) / 2**20:10.2f}")
+        rd = sum(b for _, b in pf[ph].values()) / nf_tot
+        wr = sum(b for _, b in pw[ph].values()) / nw_tot
+        lines.append(f"traffic phase={ph} workload={args.workload} alpha={args.alpha} "
+                     f"sources={source_hash(ph)} read_bytes_per_launch={rd:.0f} "
+                     f"write_bytes_per_launch={wr:.0f} bytes_per_launch={rd + wr:.0f} "
+                     f"launches={nf_tot}")
+    print()
+    for ln in lines:
+        print(ln)
+
+
+def lookup_traffic(path: str, phase: str, workload: str, alpha: float):
+    """Scaled HBM bytes per launch of `phase` from a committed traffic summary,
+    or None when absent or taken on other kernel sources."""
+    if not os.path.exists(path):
+        return None
+    want = source_hash(phase)
+    for ln in open(path):
+        if not ln.startswith("traffic "):
+            continue
+        kv = dict(x.split("=", 1) for x in ln.split()[1:])
+        if (kv.get("phase") == phase and kv.get("workload") == workload
+                and float(kv.get("alpha", "nan")) == alpha and kv.get("sources") == want):
+            return float(kv["bytes_per_launch"])
+    return None
+
+
+def main(argv=None):
+    ap = argparse.ArgumentParser(description=__doc__,
+                                 formatter_class=argparse.RawDescriptionHelpFormatter)
+    sub = ap.add_subparsers(dest="cmd", required=True)
+    s = sub.add_parser("stats")
+    s.add_argument("dir")
+    t = sub.add_parser("traffic")
+    t.add_argument("fetch_dir")
+    t.add_argument("write_dir")
+    t.add_argument("--workload", required=True)
+    t.add_argument("--alpha", type=float, required=True)
+    args = ap.parse_args(argv)
+    {"stats": cmd_stats, "traffic": cmd_traffic}[args.cmd](args)
+
+
+if __name__ == "__main__":
+    main()

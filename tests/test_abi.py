@@ -109,6 +109,8 @@ def test_ex_options_validation(lib):
     assert ex(g_dtype=-1) == DION2_ERR_INVALID_ARG
     assert ex(ns_eps=-1.0) == DION2_ERR_INVALID_ARG
     assert ex(decay_all=3) == DION2_ERR_INVALID_ARG
+    assert ex(ns_form=3) == DION2_ERR_INVALID_ARG and "ns_form" in binding.dion2_last_error()
+    assert ex(ns_form=-1) == DION2_ERR_INVALID_ARG
     coeffs = (ctypes.c_float * 6)(1.0, 2.0, 3.0, 1.0, float("inf"), 0.0)
     assert ex(ns_coeffs=ctypes.cast(coeffs, ctypes.POINTER(ctypes.c_float))) == DION2_ERR_INVALID_ARG
     need = binding.dion2_workspace_size(1, 64, 64, 0.25)
@@ -137,8 +139,11 @@ def test_workspace_size(lib):
     c = binding.dion2_workspace_size(1, 2048, 2048, 1.0)
     assert 0 < a < b and a < c
     assert a % 256 == 0
-    # compact buffers dominate: three bf16 copies of k x d_oth plus one fp32
-    assert a >= 512 * 2048 * (3 * 2 + 4)
+    # k = 512 of 2048 with l = 4 s: the GRAM form, one bf16 compact matrix,
+    # the fp32 result and ten bf16 s x s buffers
+    assert a >= 512 * 2048 * (2 + 4) + 10 * 512 * 512 * 2
+    # alpha = 1 (s = l): the DIRECT form, two bf16 compact buffers, three s x s
+    assert c >= 2048 * 2048 * (2 * 2 + 4) + 3 * 2048 * 2048 * 2
 
 
 def test_status_codes_match_header():

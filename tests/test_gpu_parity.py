@@ -17,7 +17,7 @@ import torch
 
 import oracle
 from paper_2512_16928_amd import binding, workloads
-from paper_2512_16928_amd.binding import AXIS_AUTO, AXIS_COLS, AXIS_ROWS
+from paper_2512_16928_amd.binding import AXIS_AUTO, AXIS_COLS, AXIS_ROWS, NS_DIRECT, NS_GRAM
 
 pytestmark = pytest.mark.gpu
 
@@ -28,8 +28,11 @@ def rel_fro(a, b):
     return float(np.linalg.norm(a - b) / max(np.linalg.norm(b), 1e-300))
 
 
+FORMS = pytest.mark.parametrize("form", [NS_DIRECT, NS_GRAM], ids=["direct", "gram"])
+
+
 def run_gpu(W, M, G, alpha, ns_steps=5, axis=AXIS_AUTO, mu=0.95, lr=0.02, coeffs=None,
-            decay_all=False):
+            decay_all=False, form=binding.NS_AUTO):
     """One library call on stacks [B, rows, cols]; returns host copies and the
     debug outputs."""
     B, rows, cols = W.shape
@@ -41,7 +44,8 @@ def run_gpu(W, M, G, alpha, ns_steps=5, axis=AXIS_AUTO, mu=0.95, lr=0.02, coeffs
     upd = torch.full((B, k, d_oth), float("nan"), dtype=torch.float32, device=dev)
     W0, M0 = W.cpu(), M.cpu()
     binding.dion2_step_ex(W, M, G, alpha, mu, lr, ns_steps, axis, ns_coeffs=coeffs,
-                          decay_all=decay_all, dbg_sel_idx=sel, dbg_norms=nrm, dbg_update=upd)
+                          decay_all=decay_all, dbg_sel_idx=sel, dbg_norms=nrm, dbg_update=upd,
+                          ns_form=form)
     torch.cuda.synchronize()
     return dict(W=W.cpu(), M=M.cpu(), K=sel.cpu(), norms=nrm.cpu(), O=upd.cpu(), W0=W0, M0=M0,
                 G=G.cpu(), axis=ax, k=k)
@@ -96,10 +100,11 @@ def test_single_256_fp32_full(hip_device):
     (1, 40, 1.0, AXIS_AUTO, "bf16"),         # a single row
     (384, 640, 0.1, AXIS_AUTO, "bf16"),      # alpha not a power of two
 ])
-def test_ragged_shapes(hip_device, rows, cols, alpha, axis, wdt):
+@FORMS
+def test_ragged_shapes(hip_device, rows, cols, alpha, axis, wdt, form):
     wl = one_group_workload(rows, cols, axis=axis, w_dtype=wdt, name=f"r{rows}c{cols}")
     W, M, G = workloads.make_group(wl, 0, hip_device)
-    res = run_gpu(W, M, G, alpha, axis=axis)
+    res = run_gpu(W, M, G, alpha, axis=axis, form=form)
     check_matrix(res, 0, alpha, axis=axis)
 
 
@@ -137,10 +142,11 @@ def test_plain_entry_point_equals_ex(hip_device):
     (0, None), (1, None), (3, [(1.5, -0.5, 0.0)] * 3),
     (4, [(3.0, -3.2, 1.2), (2.0, -1.5, 0.5), (1.5, -0.5, 0.0), (1.5, -0.5, 0.0)]),
 ])
-def test_ns_schedules(hip_device, ns_steps, coeffs):
+@FORMS
+def test_ns_schedules(hip_device, ns_steps, coeffs, form):
     wl = one_group_workload(160, 512, name=f"sched{ns_steps}")
     W, M, G = workloads.make_group(wl, 0, hip_device)
-    res = run_gpu(W, M, G, 0.5, ns_steps=ns_steps, coeffs=coeffs)
+    res = run_gpu(W, M, G, 0.5, ns_steps=ns_steps, coeffs=coeffs, form=form)
     check_matrix(res, 0, 0.5, ns_steps=ns_steps, coeffs=coeffs)
 
 
@@ -163,13 +169,14 @@ def test_zero_state_selects_first_lines(hip_device):
         assert not torch.any(res["O"][b])
 
 
-def test_exact_ties_go_to_lower_index(hip_device):
+@FORMS
+def test_exact_ties_go_to_lower_index(hip_device, form):
     wl = one_group_workload(128, 192, name="ties")
     W, M, G = workloads.make_group(wl, 0, hip_device)
     # rows 2j and 2j+1 identical: every norm appears twice
     M[0, 1::2] = M[0, 0::2]
     G[0, 1::2] = G[0, 0::2]
-    res = run_gpu(W, M, G, 0.25)
+    res = run_gpu(W, M, G, 0.25, form=form)
     check_matrix(res, 0, 0.25)
     K = res["K"][0].tolist()
     assert all((i % 2 == 0) or (i - 1 in K) for i in K)
@@ -196,13 +203,34 @@ def test_run_twice_bitwise(hip_device):
     assert torch.equal(W, W2) and torch.equal(M, M2)
 
 
-def test_two_steps_in_a_row(hip_device):
+@FORMS
+def test_two_steps_in_a_row(hip_device, form):
     wl = one_group_workload(256, 384, name="twostep")
     W, M, G = workloads.make_group(wl, 0, hip_device)
-    res1 = run_gpu(W, M, G, 0.25)
+    res1 = run_gpu(W, M, G, 0.25, form=form)
     check_matrix(res1, 0, 0.25)
-    res2 = run_gpu(W, M, G, 0.25)   # continues from the updated state
+    res2 = run_gpu(W, M, G, 0.25, form=form)   # continues from the updated state
     check_matrix(res2, 0, 0.25)
+
+
+def test_gram_form_tracks_duplicate_lines(hip_device):
+    """Duplicate selected lines make the Gram matrix singular; the GRAM form's
+    accumulated polynomial is large on that null space, yet O stays within
+    tolerance and duplicate lines of O stay equal to rounding."""
+    wl = one_group_workload(256, 1024, name="dupgram")
+    W, M, G = workloads.make_group(wl, 0, hip_device)
+    for j in range(0, 256, 8):
+        M[0, j + 1:j + 4] = M[0, j]
+        G[0, j + 1:j + 4] = G[0, j]
+    res = run_gpu(W, M, G, 0.5, form=NS_GRAM)
+    check_matrix(res, 0, 0.5)
+    K = res["K"][0].tolist()
+    O = res["O"][0]
+    pos = {r: i for i, r in enumerate(K)}
+    for j in range(0, 256, 8):
+        rows = [pos[r] for r in range(j, j + 4) if r in pos]
+        for r in rows[1:]:
+            assert torch.allclose(O[r], O[rows[0]], rtol=0, atol=1e-3 * float(O[rows[0]].abs().max()))
 
 
 @pytest.mark.parametrize("gi,alpha,samples", [(0, 0.25, (0, 63)), (1, 0.25, (7,)), (2, 0.25, (15,)),
