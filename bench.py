@@ -95,10 +95,10 @@ def profile_phases(wl, groups, alpha, steps):
         binding.dion2_profile_enable(False)
     out = {}
     for ph, d in prof.items():
-        if d["calls"] == 0:
+        if d["launches"] == 0:
             continue
-        avg_ms = d["ms"] / d["calls"]
-        work = d["work"] / d["calls"]
+        avg_ms = d["ms"] / d["launches"]       # per kernel launch
+        work = d["work"] / d["launches"]
         rate = work / (avg_ms * 1e-3) if avg_ms > 0 else 0.0
         if ph in HBM_PHASES:
             ach, peak, unit, bound = rate / 1e9, HBM_PEAK_GBS, "GB/s", "hbm"
@@ -107,7 +107,7 @@ def profile_phases(wl, groups, alpha, steps):
         else:
             ach, peak, unit, bound = rate / 1e9, HBM_PEAK_GBS, "GB/s", "latency"
         out[ph] = dict(total_ms_per_step=d["ms"] / steps, avg_launch_ms=avg_ms,
-                       calls_per_step=d["calls"] / steps, work_per_call=work,
+                       launches_per_step=d["launches"] / steps, work_per_launch=work,
                        achieved=ach, peak=peak, unit=unit, bound=bound, frac=ach / peak)
     return out
 
@@ -223,10 +223,10 @@ def main(argv=None):
                         traffic=None if traffic is None else round(traffic),
                         traffic_unit="bytes per launch", kernel=dom,
                         avg_launch_ms=round(d["avg_launch_ms"], 5),
-                        algorithmic_per_launch=round(d["work_per_call"]),
+                        algorithmic_per_launch=round(d["work_per_launch"]),
                         algorithmic_unit="bytes" if d["unit"] == "GB/s" else "flops")
         ns_ms = sum(phases[p]["total_ms_per_step"] for p in NS_PHASES if p in phases)
-        ns_work = sum(phases[p]["work_per_call"] * phases[p]["calls_per_step"]
+        ns_work = sum(phases[p]["work_per_launch"] * phases[p]["launches_per_step"]
                       for p in NS_PHASES if p in phases)
         if ns_ms > 0:
             ns_frac = ns_work / (ns_ms * 1e-3) / 1e12 / MFMA_BF16_PEAK_TFS

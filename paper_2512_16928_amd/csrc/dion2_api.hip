@@ -61,7 +61,7 @@ struct Plan {
     int nrb, rb_rows;         // column-mode reduction blocking
     bool gram;                // Newton-Schulz on s x s matrices (DION2_NS_GRAM)
     // workspace offsets
-    size_t o_l1, o_sq, o_part, o_sel, o_scale, o_Z, o_Z1, o_S, S_bytes, o_O, o_tables, total;
+    size_t o_l1, o_sq, o_part, o_sel, o_rank, o_scale, o_Z, o_Z1, o_S, S_bytes, o_O, o_tables, total;
 };
 
 // s x s buffers of the two Newton-Schulz forms (bf16 [batch][s_pad][s_pad])
@@ -113,6 +113,7 @@ int make_plan(int batch, int64_t rows, int64_t cols, float alpha, int axis, int 
     P.o_sq = take(B * P.d_sel * 8);
     P.o_part = take(P.axis == 1 ? B * P.nrb * 3 * (size_t)cols * 8 : 0);
     P.o_sel = take(B * P.k * 4);
+    P.o_rank = take(P.axis == 1 ? B * (size_t)(P.d_sel + 1) * 4 : 0);
     P.o_scale = take(B * 8);
     const size_t comp = B * (size_t)P.kpad * (size_t)P.opad * 2;
     P.o_Z = take(comp);
@@ -298,11 +299,14 @@ GemmArgs right_args(const Plan& P, const uint16_t* xh, const uint16_t* xl, const
     return x;
 }
 
+// O goes to the layout the apply pass reads along W's rows: L [kpad][opad]
+// for row selection, L^T [opad][kpad] for column selection.
 void final_output(const Plan& P, GemmArgs& x, float* O) {
+    const bool want_lt = P.axis == 1;
     x.out0 = O;
     x.sOut0 = P.kpad * P.opad;
-    x.ldo0 = (int)P.opad;
-    x.out_transposed = P.z_is_L ? 0 : 1;
+    x.ldo0 = (int)(want_lt ? P.kpad : P.opad);
+    x.out_transposed = P.z_is_L == want_lt ? 1 : 0;   // Z's natural layout is L iff z_is_L
 }
 
 // DIRECT: per step A = Z Z^T (hi / lo), B = b A + c A^2, Z <- a Z + B Z.
@@ -373,36 +377,42 @@ hipError_t ns_gram(const Plan& P, const uint16_t* Z, uint16_t* const* sq, float*
     hipError_t e = timed(DION2_PHASE_NS_GRAM, sym_flops(s_r, l_r) * nb, 1, stream,
                          [&] { return launch_gemm(g, EPI_SPLIT, 1, stream); });
     if (e != hipSuccess) return e;
-    for (int t = 0; t < ns_steps; ++t) {
-        const float* cf = opt.ns_coeffs ? opt.ns_coeffs + 3 * t : kMuonQuintic;
-        // Q_t; the first one is P itself
-        uint16_t* qh = t == 0 ? Ph[0] : sq[SQ_QHI];
-        uint16_t* ql = t == 0 ? Pl[0] : sq[SQ_QLO];
-        GemmArgs q = sym3_args(P, Ah, Al, Ah, Al, qh, ql);
-        q.ca = cf[0];
-        q.cb = cf[1];
-        q.cc = cf[2];
-        q.E0 = Ah;
-        q.E1 = Al;
-        q.sE = P.s_pad * P.s_pad;
-        q.lde = (int)P.s_pad;
-        e = timed(DION2_PHASE_NS_POLY, f3, 1, stream, [&] { return launch_gemm(q, EPI_QPOLY, 3, stream); });
-        if (e != hipSuccess) return e;
-        if (t > 0) {
-            GemmArgs p = sym3_args(P, qh, ql, Ph[cur], Pl[cur], Ph[1 - cur], Pl[1 - cur]);
-            e = timed(DION2_PHASE_NS_POLY, f3, 1, stream, [&] { return launch_gemm(p, EPI_SPLIT, 3, stream); });
-            if (e != hipSuccess) return e;
-            cur = 1 - cur;
+    // the s x s products run back to back and are timed as one span
+    const int nprod = ns_steps + 3 * (ns_steps - 1);
+    e = timed(DION2_PHASE_NS_POLY, f3 * nprod, nprod, stream, [&]() -> hipError_t {
+        for (int t = 0; t < ns_steps; ++t) {
+            const float* cf = opt.ns_coeffs ? opt.ns_coeffs + 3 * t : kMuonQuintic;
+            // Q_t; the first one is P itself
+            uint16_t* qh = t == 0 ? Ph[0] : sq[SQ_QHI];
+            uint16_t* ql = t == 0 ? Pl[0] : sq[SQ_QLO];
+            GemmArgs q = sym3_args(P, Ah, Al, Ah, Al, qh, ql);
+            q.ca = cf[0];
+            q.cb = cf[1];
+            q.cc = cf[2];
+            q.E0 = Ah;
+            q.E1 = Al;
+            q.sE = P.s_pad * P.s_pad;
+            q.lde = (int)P.s_pad;
+            hipError_t r = launch_gemm(q, EPI_QPOLY, 3, stream);
+            if (r != hipSuccess) return r;
+            if (t > 0) {   // P <- Q_t P
+                GemmArgs p = sym3_args(P, qh, ql, Ph[cur], Pl[cur], Ph[1 - cur], Pl[1 - cur]);
+                r = launch_gemm(p, EPI_SPLIT, 3, stream);
+                if (r != hipSuccess) return r;
+                cur = 1 - cur;
+            }
+            if (t + 1 < ns_steps) {   // A <- Q_t (Q_t A)
+                GemmArgs u = sym3_args(P, qh, ql, Ah, Al, sq[SQ_THI], sq[SQ_TLO]);
+                r = launch_gemm(u, EPI_SPLIT, 3, stream);
+                if (r != hipSuccess) return r;
+                GemmArgs v = sym3_args(P, qh, ql, sq[SQ_THI], sq[SQ_TLO], Ah, Al);
+                r = launch_gemm(v, EPI_SPLIT, 3, stream);
+                if (r != hipSuccess) return r;
+            }
         }
-        if (t + 1 < ns_steps) {
-            GemmArgs u = sym3_args(P, qh, ql, Ah, Al, sq[SQ_THI], sq[SQ_TLO]);
-            e = timed(DION2_PHASE_NS_POLY, f3, 1, stream, [&] { return launch_gemm(u, EPI_SPLIT, 3, stream); });
-            if (e != hipSuccess) return e;
-            GemmArgs v = sym3_args(P, qh, ql, sq[SQ_THI], sq[SQ_TLO], Ah, Al);
-            e = timed(DION2_PHASE_NS_POLY, f3, 1, stream, [&] { return launch_gemm(v, EPI_SPLIT, 3, stream); });
-            if (e != hipSuccess) return e;
-        }
-    }
+        return hipSuccess;
+    });
+    if (e != hipSuccess) return e;
     // O = (P_hi + P_lo) Z
     GemmArgs x = right_args(P, Ph[cur], Pl[cur], Z);
     final_output(P, x, O);
@@ -497,6 +507,7 @@ int run_step(const Plan& P, void* W, float* M, const void* G, const Tables* tabs
     double* l1 = reinterpret_cast<double*>(ws + P.o_l1);
     double* sq = reinterpret_cast<double*>(ws + P.o_sq);
     int32_t* sel = reinterpret_cast<int32_t*>(ws + P.o_sel);
+    int32_t* rank = P.axis == 1 ? reinterpret_cast<int32_t*>(ws + P.o_rank) : nullptr;
     double* scale = reinterpret_cast<double*>(ws + P.o_scale);
     // compact matrix in its wide orientation: L [kpad][opad] or L^T [opad][kpad]
     uint16_t* Z0 = reinterpret_cast<uint16_t*>(ws + P.o_Z);
@@ -522,7 +533,17 @@ int run_step(const Plan& P, void* W, float* M, const void* G, const Tables* tabs
     const double g_bytes = opt.g_dtype == DION2_DTYPE_BF16 ? 2.0 : 4.0;
     const double w_bytes = opt.w_dtype == DION2_DTYPE_BF16 ? 2.0 : 4.0;
     const double sel_el = (double)P.batch * (double)P.k * (double)P.d_oth;
-    e = timed(DION2_PHASE_MOMENTUM, n_el * (8.0 + g_bytes), P.axis == 0 ? 1 : 2, stream,
+    // Bytes each phase must move as designed. Rows: K1 reads M, G and writes
+    // M; K3 reads and writes the selected rows of M and writes the compact
+    // bf16 copy; K5 reads O and reads and writes the selected rows of W.
+    // Columns (selected columns touch every cache line of a row): K1 only
+    // reads M and G; K3 reads M, G and writes M whole, plus the compact copy;
+    // K5 reads O and reads and writes W whole.
+    const bool cm = P.axis == 1;
+    const double k1_bytes = n_el * ((cm ? 4.0 : 8.0) + g_bytes);
+    const double k3_bytes = (cm ? n_el * (8.0 + g_bytes) : sel_el * 8.0) + sel_el * 2.0;
+    const double k5_bytes = (cm ? n_el : sel_el) * 2.0 * w_bytes + sel_el * 4.0;
+    e = timed(DION2_PHASE_MOMENTUM, k1_bytes, P.axis == 0 ? 1 : 2, stream,
               [&] { return launch_momentum(ma, P.axis, opt.g_dtype == DION2_DTYPE_BF16, stream); });
     if (e != hipSuccess) return hip_fail(e, "launch K1 momentum");
 
@@ -536,6 +557,7 @@ int run_step(const Plan& P, void* W, float* M, const void* G, const Tables* tabs
     sa.eps = (double)opt.ns_eps;
     sa.sel = sel;
     sa.scale = scale;
+    sa.rank = rank;
     e = timed(DION2_PHASE_SELECT, (double)P.batch * (double)P.d_sel * 16.0, 1, stream,
               [&] { return launch_select(sa, stream); });
     if (e != hipSuccess) return hip_fail(e, "launch K2 select");
@@ -551,16 +573,18 @@ int run_step(const Plan& P, void* W, float* M, const void* G, const Tables* tabs
     ga.kpad = (int)P.kpad;
     ga.opad = (int)P.opad;
     ga.sel = sel;
+    ga.rank = rank;
     ga.scale = scale;
     ga.mu = mu;
-    ga.decay = opt.decay_all ? 0 : 1;
+    // rows: selective decay here, decay-all by its own pass; columns: both here
+    ga.decay = cm ? (opt.decay_all ? 2 : 1) : (opt.decay_all ? 0 : 1);
     ga.L = P.z_is_L ? Z0 : nullptr;
     ga.LT = P.z_is_L ? nullptr : Z0;
     ga.O = ns_steps == 0 ? O : nullptr;
-    e = timed(DION2_PHASE_GATHER, sel_el * 8.0, 1, stream,
-              [&] { return launch_gather(ga, P.axis, stream); });
+    e = timed(DION2_PHASE_GATHER, k3_bytes, 1, stream,
+              [&] { return launch_gather(ga, P.axis, opt.g_dtype == DION2_DTYPE_BF16, stream); });
     if (e != hipSuccess) return hip_fail(e, "launch K3 gather");
-    if (opt.decay_all) {
+    if (opt.decay_all && !cm) {
         DecayAllArgs da{ms, P.rows, P.cols, P.batch, mu};
         e = launch_decay_all(da, stream);
         if (e != hipSuccess) return hip_fail(e, "launch decay-all");
@@ -584,10 +608,11 @@ int run_step(const Plan& P, void* W, float* M, const void* G, const Tables* tabs
     aa.kpad = (int)P.kpad;
     aa.opad = (int)P.opad;
     aa.sel = sel;
+    aa.rank = rank;
     aa.O = O;
     aa.lr_eff = (double)lr * std::sqrt((double)P.rows / (double)P.cols);
     aa.dbg = opt.dbg_update;
-    e = timed(DION2_PHASE_APPLY, sel_el * 2.0 * w_bytes, 1, stream,
+    e = timed(DION2_PHASE_APPLY, k5_bytes, 1, stream,
               [&] { return launch_apply(aa, P.axis, opt.w_dtype == DION2_DTYPE_BF16, stream); });
     if (e != hipSuccess) return hip_fail(e, "launch K5 apply");
 

@@ -43,6 +43,32 @@ struct MatSet {
     }
 };
 
+// ------------------------------------------------------- global accesses
+// Pointers reached through MatSet (possibly from a device pointer table) are
+// generic; these helpers access them as global memory, so the compiler emits
+// global (not flat) loads and stores and waits on vmcnt alone.
+#define DION2_GLOBAL __attribute__((address_space(1)))
+template <int N> struct RawBits;
+template <> struct RawBits<2> { typedef unsigned short T; };
+template <> struct RawBits<4> { typedef unsigned int T; };
+template <> struct RawBits<8> { typedef unsigned int T __attribute__((ext_vector_type(2))); };
+template <> struct RawBits<16> { typedef unsigned int T __attribute__((ext_vector_type(4))); };
+template <typename V>
+__device__ __forceinline__ V ldg(const void* p) {
+    typedef typename RawBits<sizeof(V)>::T R;
+    const R r = *(const DION2_GLOBAL R*)p;
+    V v;
+    __builtin_memcpy(&v, &r, sizeof(V));
+    return v;
+}
+template <typename V>
+__device__ __forceinline__ void stg(void* p, const V& v) {
+    typedef typename RawBits<sizeof(V)>::T R;
+    R r;
+    __builtin_memcpy(&r, &v, sizeof(V));
+    *(DION2_GLOBAL R*)p = r;
+}
+
 // ------------------------------------------------------------ conversions
 
 __device__ __forceinline__ float bf16_bits_to_f32(uint32_t h) {
@@ -66,21 +92,30 @@ __device__ __forceinline__ uint16_t f64_to_bf16(double d) {
 
 template <typename T> struct Elem;
 template <> struct Elem<float> {
-    static __device__ __forceinline__ float load(const float* p) { return *p; }
-    static __device__ __forceinline__ void store_f64(float* p, double v) { *p = (float)v; }
+    static __device__ __forceinline__ float load(const float* p) { return ldg<float>(p); }
+    static __device__ __forceinline__ void store_f64(float* p, double v) { stg<float>(p, (float)v); }
 };
 template <> struct Elem<uint16_t> {
-    static __device__ __forceinline__ float load(const uint16_t* p) { return bf16_bits_to_f32(*p); }
-    static __device__ __forceinline__ void store_f64(uint16_t* p, double v) { *p = f64_to_bf16(v); }
+    static __device__ __forceinline__ float load(const uint16_t* p) { return bf16_bits_to_f32(ldg<uint16_t>(p)); }
+    static __device__ __forceinline__ void store_f64(uint16_t* p, double v) { stg<uint16_t>(p, f64_to_bf16(v)); }
 };
 
 // four consecutive elements as fp32 (p is 8-byte aligned for bf16, 16 for fp32)
 __device__ __forceinline__ void load4(const float* p, float (&v)[4]) {
-    float4 x = *reinterpret_cast<const float4*>(p);
+    const float4 x = ldg<float4>(p);
     v[0] = x.x; v[1] = x.y; v[2] = x.z; v[3] = x.w;
 }
 __device__ __forceinline__ void load4(const uint16_t* p, float (&v)[4]) {
-    uint2 x = *reinterpret_cast<const uint2*>(p);
+    const uint2 x = ldg<uint2>(p);
+    v[0] = bf16_bits_to_f32(x.x & 0xffffu); v[1] = bf16_bits_to_f32(x.x >> 16);
+    v[2] = bf16_bits_to_f32(x.y & 0xffffu); v[3] = bf16_bits_to_f32(x.y >> 16);
+}
+
+// the same four values from a vector already in registers
+__device__ __forceinline__ void unpack4(const float4& x, float (&v)[4]) {
+    v[0] = x.x; v[1] = x.y; v[2] = x.z; v[3] = x.w;
+}
+__device__ __forceinline__ void unpack4(const uint2& x, float (&v)[4]) {
     v[0] = bf16_bits_to_f32(x.x & 0xffffu); v[1] = bf16_bits_to_f32(x.x >> 16);
     v[2] = bf16_bits_to_f32(x.y & 0xffffu); v[3] = bf16_bits_to_f32(x.y >> 16);
 }
@@ -125,6 +160,7 @@ struct SelectArgs {
     double eps;
     int32_t* sel;      // [batch][k] ascending
     double* scale;     // [batch] 1 / (sqrt(sum sq over K) + eps)
+    int32_t* rank;     // nullable [batch][d_sel + 1]: selected lines below i
 };
 hipError_t launch_select(const SelectArgs& a, hipStream_t s);
 
@@ -133,14 +169,16 @@ struct GatherArgs {
     int64_t rows, cols;
     int batch, k, d_oth, kpad, opad;
     const int32_t* sel;
+    const int32_t* rank;   // column mode: [batch][cols + 1], see SelectArgs
     const double* scale;
     float mu;
-    int decay;         // 1: M[K] <- mu M[K] here
+    int decay;         // 0: none, 1: M[K] <- mu M[K] here, 2: M <- mu M (column mode)
     uint16_t* L;       // nullable [batch][kpad][opad]
     uint16_t* LT;      // nullable [batch][opad][kpad] (one of L, LT is written)
-    float* O;          // nullable: fp32 copy in L layout (no Newton-Schulz step)
+    float* O;          // nullable: fp32 copy (no Newton-Schulz step), L layout for
+                       // rows, L^T layout [opad][kpad] for columns
 };
-hipError_t launch_gather(const GatherArgs& a, int axis, hipStream_t s);
+hipError_t launch_gather(const GatherArgs& a, int axis, int g_bf16, hipStream_t s);
 
 struct DecayAllArgs {
     MatSet ms;
@@ -184,7 +222,8 @@ struct ApplyArgs {
     int64_t rows, cols;
     int batch, k, d_oth, kpad, opad;
     const int32_t* sel;
-    const float* O;    // [batch][kpad][opad]
+    const int32_t* rank;   // column mode: [batch][cols + 1], see SelectArgs
+    const float* O;    // [batch][kpad][opad] (rows) or [batch][opad][kpad] (columns)
     double lr_eff;     // lr * sqrt(rows / cols)
     float* dbg;        // nullable [batch][k][d_oth]
 };

@@ -8,14 +8,14 @@
 // copied out unpadded for inspection.
 //
 // Row mode reads O rows and W rows along j (both contiguous). Column mode
-// stages a 64 x 64 tile of O in LDS so that W is walked along its rows,
-// touching the selected columns K[p] of each row in ascending order.
+// streams W by rows and reads O transposed.
+#include <type_traits>
+
 #include "dion2_device.h"
 
 namespace dion2 {
 namespace {
 
-constexpr int kT = 64;
 constexpr int kThreads = 256;
 
 template <typename WT>
@@ -25,65 +25,161 @@ __device__ __forceinline__ void update(WT* w, float o, double lr_eff) {
     Elem<WT>::store_f64(w, r);
 }
 
-template <typename WT>
+// four consecutive elements of W: load as fp32, store rounded from fp64
+__device__ __forceinline__ void load4w(const float* p, float (&v)[4]) { load4(p, v); }
+__device__ __forceinline__ void load4w(const uint16_t* p, float (&v)[4]) { load4(p, v); }
+__device__ __forceinline__ void store4w(float* p, const double (&r)[4]) {
+    stg(p, make_float4((float)r[0], (float)r[1], (float)r[2], (float)r[3]));
+}
+__device__ __forceinline__ void store4w(uint16_t* p, const double (&r)[4]) {
+    uint2 u;
+    u.x = (uint32_t)f64_to_bf16(r[0]) | ((uint32_t)f64_to_bf16(r[1]) << 16);
+    u.y = (uint32_t)f64_to_bf16(r[2]) | ((uint32_t)f64_to_bf16(r[3]) << 16);
+    stg(p, u);
+}
+
+// Row mode: one wave per selected line p, four elements per lane.
+template <int VEC, typename WT>
 __global__ __launch_bounds__(kThreads) void apply_rows(ApplyArgs a) {
-    const int b = blockIdx.z;
-    const int p0 = blockIdx.y * kT, j0 = blockIdx.x * kT;
-    const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
-    WT* __restrict__ W = a.ms.w<WT>(b);
-    const int32_t* __restrict__ K = a.sel + (int64_t)b * a.k;
-    const float* __restrict__ O = a.O + (int64_t)b * a.kpad * a.opad;
-    const int j = j0 + tx;
-    if (j >= a.d_oth) return;
-    for (int pl = ty; pl < kT; pl += 4) {
-        const int p = p0 + pl;
-        if (p >= a.k) break;
-        const float o = O[(int64_t)p * a.opad + j];
-        update(W + (int64_t)K[p] * a.cols + j, o, a.lr_eff);
-        if (a.dbg) a.dbg[((int64_t)b * a.k + p) * a.d_oth + j] = o;
+    const int b = blockIdx.y;
+    const int lane = threadIdx.x & 63;
+    const int p = blockIdx.x * (kThreads / 64) + (threadIdx.x >> 6);
+    if (p >= a.k) return;   // whole wave
+    WT* __restrict__ w = a.ms.w<WT>(b) + (int64_t)a.sel[(int64_t)b * a.k + p] * a.cols;
+    const float* __restrict__ o = a.O + (int64_t)b * a.kpad * a.opad + (int64_t)p * a.opad;
+    float* dbg = a.dbg ? a.dbg + ((int64_t)b * a.k + p) * a.d_oth : nullptr;
+    if constexpr (VEC == 4) {
+        for (int j = 4 * lane; j < a.d_oth; j += 256) {
+            float x[4], u[4];
+            load4w(w + j, x);
+            load4(o + j, u);
+            double r[4];
+#pragma unroll
+            for (int v = 0; v < 4; ++v) r[v] = __dsub_rn((double)x[v], __dmul_rn(a.lr_eff, (double)u[v]));
+            store4w(w + j, r);
+            if (dbg) *reinterpret_cast<float4*>(dbg + j) = make_float4(u[0], u[1], u[2], u[3]);
+        }
+    } else {
+        for (int j = lane; j < a.d_oth; j += 64) {
+            update(w + j, o[j], a.lr_eff);
+            if (dbg) dbg[j] = o[j];
+        }
     }
 }
 
-template <typename WT>
+// Column mode: the selected columns are spread through every row of W, so
+// W is streamed row by row. O comes in the L^T layout [opad][kpad], so the
+// values a row needs, O^T[r][rank[c]] for its selected columns c, sit
+// together in one row of O^T. A block covers kCW columns x kRB rows; each
+// lane owns four columns of kRB / 4 rows and issues all its loads before
+// any store. Every four-column group is written back, unselected entries
+// with their own bits, so each cache line of W is rewritten whole.
+constexpr int kCW = 256;
+constexpr int kRB = 64;
+
+template <int VEC, typename WT>
 __global__ __launch_bounds__(kThreads) void apply_cols(ApplyArgs a) {
-    __shared__ float tile[kT][kT + 1];   // [p local][r local]
     const int b = blockIdx.z;
-    const int p0 = blockIdx.y * kT, r0 = blockIdx.x * kT;
-    const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
+    const int64_t c0 = (int64_t)blockIdx.x * kCW;
+    const int r0 = blockIdx.y * kRB;
+    const int32_t* __restrict__ rank = a.rank + (int64_t)b * (a.cols + 1);
     WT* __restrict__ W = a.ms.w<WT>(b);
-    const int32_t* __restrict__ K = a.sel + (int64_t)b * a.k;
-    const float* __restrict__ O = a.O + (int64_t)b * a.kpad * a.opad;
-    // load O[p][r] along r (contiguous); padding of O is in bounds
-    for (int pl = ty; pl < kT; pl += 4) {
-        const int p = p0 + pl;
-        const float o = O[(int64_t)p * a.opad + r0 + tx];
-        tile[pl][tx] = o;
-        if (a.dbg && p < a.k && r0 + tx < a.d_oth)
-            a.dbg[((int64_t)b * a.k + p) * a.d_oth + r0 + tx] = o;
+    const float* __restrict__ OT = a.O + (int64_t)b * a.opad * a.kpad;
+    const int cq = threadIdx.x & 63, rg = threadIdx.x >> 6;
+    const int64_t c = c0 + 4 * cq;
+    int p[4];   // line of each column, -1 if unselected
+    {
+        int rk[5];   // rank[c .. c + 4], clamped to the array (branch-free loads)
+#pragma unroll
+        for (int v = 0; v < 5; ++v) rk[v] = ldg<int32_t>(rank + (c + v < a.cols ? c + v : a.cols));
+#pragma unroll
+        for (int v = 0; v < 4; ++v) p[v] = (c + v < a.cols && rk[v + 1] > rk[v]) ? rk[v] : -1;
     }
-    __syncthreads();
-    const int p = p0 + tx;
-    if (p >= a.k) return;
-    const int col = K[p];
-    for (int rl = ty; rl < kT; rl += 4) {
-        const int r = r0 + rl;
-        if (r >= a.d_oth) break;
-        update(W + (int64_t)r * a.cols + col, tile[tx][rl], a.lr_eff);
+    constexpr int kR = kRB / 4;   // rows per thread
+    if (VEC == 4 && c + 3 < a.cols) {
+        typedef typename std::conditional<sizeof(WT) == 2, uint2, float4>::type Raw;
+        Raw raw[kR];
+        float o[kR][4];
+        // branch-free loads (an unselected column reads line 0, unused; rows
+        // past the matrix read its last row) so all of them are in flight
+        // together
+        int pc[4];
+#pragma unroll
+        for (int v = 0; v < 4; ++v) pc[v] = p[v] >= 0 ? p[v] : 0;
+#pragma unroll
+        for (int i = 0; i < kR; ++i) {
+            int64_t r = r0 + rg + 4 * i;
+            r = r < a.rows ? r : a.rows - 1;
+            raw[i] = ldg<Raw>(W + r * a.cols + c);
+#pragma unroll
+            for (int v = 0; v < 4; ++v) o[i][v] = OT[r * a.kpad + pc[v]];
+        }
+#pragma unroll
+        for (int i = 0; i < kR; ++i) {
+            const int64_t r = r0 + rg + 4 * i;
+            if (r >= a.rows) continue;
+            // unselected entries are written back with their own bits
+            if constexpr (sizeof(WT) == 2) {
+                const uint2 x = reinterpret_cast<const uint2&>(raw[i]);
+                uint32_t h[4] = {x.x & 0xffffu, x.x >> 16, x.y & 0xffffu, x.y >> 16};
+#pragma unroll
+                for (int v = 0; v < 4; ++v)
+                    if (p[v] >= 0)
+                        h[v] = f64_to_bf16(__dsub_rn((double)bf16_bits_to_f32(h[v]),
+                                                     __dmul_rn(a.lr_eff, (double)o[i][v])));
+                stg(W + r * a.cols + c, make_uint2(h[0] | (h[1] << 16), h[2] | (h[3] << 16)));
+            } else {
+                float4 x = reinterpret_cast<const float4&>(raw[i]);
+                float f[4] = {x.x, x.y, x.z, x.w};
+#pragma unroll
+                for (int v = 0; v < 4; ++v)
+                    if (p[v] >= 0) f[v] = (float)__dsub_rn((double)f[v], __dmul_rn(a.lr_eff, (double)o[i][v]));
+                stg(W + r * a.cols + c, make_float4(f[0], f[1], f[2], f[3]));
+            }
+        }
+    } else {
+        for (int rl = rg; rl < kRB; rl += 4) {
+            const int64_t r = r0 + rl;
+            if (r >= a.rows) break;
+#pragma unroll
+            for (int v = 0; v < 4; ++v)
+                if (p[v] >= 0) update(W + r * a.cols + c + v, OT[r * a.kpad + p[v]], a.lr_eff);
+        }
+    }
+    if (a.dbg) {   // O in the [k][d_oth] layout (inspection only)
+        for (int rl = rg; rl < kRB; rl += 4) {
+            const int64_t r = r0 + rl;
+            if (r >= a.rows) break;
+#pragma unroll
+            for (int v = 0; v < 4; ++v)
+                if (p[v] >= 0) a.dbg[((int64_t)b * a.k + p[v]) * a.d_oth + r] = OT[r * a.kpad + p[v]];
+        }
     }
 }
 
 }  // namespace
 
 hipError_t launch_apply(const ApplyArgs& a, int axis, int w_bf16, hipStream_t s) {
-    const unsigned gj = (unsigned)((a.d_oth + kT - 1) / kT);
-    const unsigned gp = (unsigned)((a.k + kT - 1) / kT);
-    dim3 grid(gj, gp, (unsigned)a.batch);
+    const bool vec = a.cols % 4 == 0;
     if (axis == 0) {
-        if (w_bf16) hipLaunchKernelGGL((apply_rows<uint16_t>), grid, dim3(kThreads), 0, s, a);
-        else hipLaunchKernelGGL((apply_rows<float>), grid, dim3(kThreads), 0, s, a);
+        dim3 grid((unsigned)((a.k + 3) / 4), (unsigned)a.batch);
+        if (w_bf16) {
+            if (vec) hipLaunchKernelGGL((apply_rows<4, uint16_t>), grid, dim3(kThreads), 0, s, a);
+            else hipLaunchKernelGGL((apply_rows<1, uint16_t>), grid, dim3(kThreads), 0, s, a);
+        } else {
+            if (vec) hipLaunchKernelGGL((apply_rows<4, float>), grid, dim3(kThreads), 0, s, a);
+            else hipLaunchKernelGGL((apply_rows<1, float>), grid, dim3(kThreads), 0, s, a);
+        }
     } else {
-        if (w_bf16) hipLaunchKernelGGL((apply_cols<uint16_t>), grid, dim3(kThreads), 0, s, a);
-        else hipLaunchKernelGGL((apply_cols<float>), grid, dim3(kThreads), 0, s, a);
+        dim3 grid((unsigned)((a.cols + kCW - 1) / kCW), (unsigned)((a.rows + kRB - 1) / kRB),
+                  (unsigned)a.batch);
+        if (w_bf16) {
+            if (vec) hipLaunchKernelGGL((apply_cols<4, uint16_t>), grid, dim3(kThreads), 0, s, a);
+            else hipLaunchKernelGGL((apply_cols<1, uint16_t>), grid, dim3(kThreads), 0, s, a);
+        } else {
+            if (vec) hipLaunchKernelGGL((apply_cols<4, float>), grid, dim3(kThreads), 0, s, a);
+            else hipLaunchKernelGGL((apply_cols<1, float>), grid, dim3(kThreads), 0, s, a);
+        }
     }
     return hipGetLastError();
 }

@@ -1,5 +1,6 @@
 // K3: gather the selected lines into the compact bf16 submatrix, scaled for
-// Newton-Schulz, fused with the selective decay of eq. (2).
+// Newton-Schulz, fused with the selective decay of eq. (2) (and, in column
+// mode, with the store of the accumulated momentum).
 //
 //   L[p][j]  = bf16(M_line(K[p])[j] / (||M[K]||_F + eps))   [kpad][opad]
 //   LT[j][p] = L[p][j]                                       [opad][kpad]
@@ -10,6 +11,8 @@
 // (line p, other index j): the side that is contiguous in M is read and
 // written directly, the other side goes through an LDS tile. Tiles cover the
 // padded extents, and padding (p >= k or j >= d_oth) is written as zero.
+#include <type_traits>
+
 #include "dion2_device.h"
 
 namespace dion2 {
@@ -44,17 +47,14 @@ __global__ __launch_bounds__(kThreads) void gather_rows(GatherArgs a) {
                 load4(row + j, m);
 #pragma unroll
                 for (int v = 0; v < 4; ++v) x[v] = m[v] * sc;
-                if (a.decay) {
-                    *reinterpret_cast<float4*>(row + j) =
-                        make_float4(a.mu * m[0], a.mu * m[1], a.mu * m[2], a.mu * m[3]);
-                }
+                if (a.decay) stg(row + j, make_float4(a.mu * m[0], a.mu * m[1], a.mu * m[2], a.mu * m[3]));
             } else {
 #pragma unroll
                 for (int v = 0; v < 4; ++v) {
                     if (j + v < a.d_oth) {
-                        const float m = row[j + v];
+                        const float m = ldg<float>(row + j + v);
                         x[v] = m * sc;
-                        if (a.decay) row[j + v] = a.mu * m;
+                        if (a.decay) stg(row + j + v, a.mu * m);
                     }
                 }
             }
@@ -86,64 +86,144 @@ __global__ __launch_bounds__(kThreads) void gather_rows(GatherArgs a) {
 }
 
 // Column mode: line p is column K[p] of M; the other index r is the row.
-// Reading along a row picks K[p], K[p+1], ... (ascending, nearby columns).
-__global__ __launch_bounds__(kThreads) void gather_cols(GatherArgs a) {
-    __shared__ float tile[kT][kT + 1];   // [p local][r local]
+// Selected columns are scattered through every row, so decaying them in
+// place would dirty every cache line of M anyway; instead this pass streams
+// whole rows once: M <- fl32(M + G) (the momentum pass only read M to get
+// the column norms), times mu on the selected columns (every column with
+// decay == 2), and the selected columns, scaled, go through an LDS tile
+// into the compact matrix. A block covers kCW columns x kRB rows; rank[c]
+// (selected columns below c) gives each selected column its line p, and
+// the block's lines are p0 = rank[c0] .. p1 = rank[c0 + kCW].
+constexpr int kCW = 256;
+constexpr int kRB = 64;
+
+template <int VEC, typename GT>
+__global__ __launch_bounds__(kThreads) void update_cols(GatherArgs a) {
+    __shared__ float tile[kCW][kRB + 1];   // [p - p0][r - r0]
     const int b = blockIdx.z;
-    const int p0 = blockIdx.y * kT, r0 = blockIdx.x * kT;
-    const int tx = threadIdx.x & 15, ty = threadIdx.x >> 4;
+    const int64_t c0 = (int64_t)blockIdx.x * kCW;
+    const int r0 = blockIdx.y * kRB;
+    const int64_t cend = c0 + kCW < a.cols ? c0 + kCW : a.cols;
+    const int32_t* __restrict__ rank = a.rank + (int64_t)b * (a.cols + 1);
+    const int p0 = rank[c0], p1 = rank[cend];
     float* __restrict__ M = a.ms.m(b);
-    const int32_t* __restrict__ K = a.sel + (int64_t)b * a.k;
+    const GT* __restrict__ G = a.ms.g<GT>(b);
     const float sc = (float)a.scale[b];
-    uint16_t* __restrict__ L = a.L ? a.L + (int64_t)b * a.kpad * a.opad : nullptr;
-    uint16_t* __restrict__ LT = a.LT ? a.LT + (int64_t)b * a.opad * a.kpad : nullptr;
-    float* __restrict__ O = a.O ? a.O + (int64_t)b * a.kpad * a.opad : nullptr;
-    const int p = p0 + 4 * tx;
-    int col[4];
+    const int cq = threadIdx.x & 63, rg = threadIdx.x >> 6;
+    const int64_t c = c0 + 4 * cq;
+    int pl[4];        // tile row of each of the four columns, -1 if unselected
+    bool in[4];
+    {
+        int rk[5];   // rank[c .. c + 4], clamped to the array (branch-free loads)
 #pragma unroll
-    for (int v = 0; v < 4; ++v) col[v] = (p + v < a.k) ? K[p + v] : -1;
+        for (int v = 0; v < 5; ++v) rk[v] = ldg<int32_t>(rank + (c + v < a.cols ? c + v : a.cols));
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-        const int rl = ty + 16 * i;
-        const int r = r0 + rl;
-        float x[4] = {0.f, 0.f, 0.f, 0.f};
-        if (r < a.d_oth) {
-            float* row = M + (int64_t)r * a.cols;
+        for (int v = 0; v < 4; ++v) {
+            in[v] = c + v < a.cols;
+            pl[v] = (in[v] && rk[v + 1] > rk[v]) ? rk[v] - p0 : -1;
+        }
+    }
+    constexpr int kR = kRB / 4;   // rows per thread
+    if (VEC == 4 && in[3]) {
+        // every row's M and G are loaded before the first store
+        typedef typename std::conditional<sizeof(GT) == 2, uint2, float4>::type GRaw;
+        float4 mr[kR];
+        GRaw gr[kR];
 #pragma unroll
-            for (int v = 0; v < 4; ++v) {
-                if (col[v] >= 0) {
-                    const float m = row[col[v]];
-                    x[v] = m * sc;
-                    if (a.decay) row[col[v]] = a.mu * m;
-                }
+        for (int i = 0; i < kR; ++i) {
+            const int64_t r = r0 + rg + 4 * i;
+            if (r < a.rows) {
+                mr[i] = ldg<float4>(M + r * a.cols + c);
+                gr[i] = ldg<GRaw>(G + r * a.cols + c);
             }
         }
-        if (LT) {
-            uint2 packed;
-            packed.x = (uint32_t)f32_to_bf16(x[0]) | ((uint32_t)f32_to_bf16(x[1]) << 16);
-            packed.y = (uint32_t)f32_to_bf16(x[2]) | ((uint32_t)f32_to_bf16(x[3]) << 16);
-            *reinterpret_cast<uint2*>(LT + (int64_t)r * a.kpad + p) = packed;
-        }
 #pragma unroll
-        for (int v = 0; v < 4; ++v) tile[4 * tx + v][rl] = x[v];
+        for (int i = 0; i < kR; ++i) {
+            const int rl = rg + 4 * i;
+            const int64_t r = r0 + rl;
+            float m[4] = {0.f, 0.f, 0.f, 0.f};
+            if (r < a.rows) {
+                float g[4];
+                unpack4(gr[i], g);
+                m[0] = mr[i].x + g[0];
+                m[1] = mr[i].y + g[1];
+                m[2] = mr[i].z + g[2];
+                m[3] = mr[i].w + g[3];
+                float o[4];
+#pragma unroll
+                for (int v = 0; v < 4; ++v)
+                    o[v] = (a.decay == 2 || (a.decay == 1 && pl[v] >= 0)) ? a.mu * m[v] : m[v];
+                stg(M + r * a.cols + c, make_float4(o[0], o[1], o[2], o[3]));
+            }
+#pragma unroll
+            for (int v = 0; v < 4; ++v)
+                if (pl[v] >= 0) tile[pl[v]][rl] = m[v] * sc;   // rows past d_oth give zeros
+        }
+    } else {
+        for (int i = 0; i < kR; ++i) {
+            const int rl = rg + 4 * i;
+            const int64_t r = r0 + rl;
+            float m[4] = {0.f, 0.f, 0.f, 0.f};
+            if (r < a.rows) {
+#pragma unroll
+                for (int v = 0; v < 4; ++v) {
+                    if (in[v]) {
+                        m[v] = ldg<float>(M + r * a.cols + c + v) + Elem<GT>::load(G + r * a.cols + c + v);
+                        stg(M + r * a.cols + c + v,
+                            (a.decay == 2 || (a.decay == 1 && pl[v] >= 0)) ? a.mu * m[v] : m[v]);
+                    }
+                }
+            }
+#pragma unroll
+            for (int v = 0; v < 4; ++v)
+                if (pl[v] >= 0) tile[pl[v]][rl] = m[v] * sc;
+        }
     }
-    if (!L && !O) return;   // uniform over the block
     __syncthreads();
-    // L[p][r], r contiguous
-    const int r = r0 + 4 * tx;
+    const int np = p1 - p0;
+    const bool last = cend == a.cols;   // this chunk also zeroes the padded lines k..kpad
+    if (a.L) {
+        // L[p][r0 .. r0 + 64), four rows per thread
+        const int q = threadIdx.x & 15;
+        for (int pi = threadIdx.x >> 4; pi < np; pi += kThreads / 16) {
+            float x[4];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-        const int pl = ty + 16 * i;
-        float x[4];
-#pragma unroll
-        for (int v = 0; v < 4; ++v) x[v] = tile[pl][4 * tx + v];
-        if (L) {
+            for (int v = 0; v < 4; ++v) x[v] = tile[pi][4 * q + v];
+            const int64_t off = (int64_t)b * a.kpad * a.opad + (int64_t)(p0 + pi) * a.opad + r0 + 4 * q;
             uint2 packed;
             packed.x = (uint32_t)f32_to_bf16(x[0]) | ((uint32_t)f32_to_bf16(x[1]) << 16);
             packed.y = (uint32_t)f32_to_bf16(x[2]) | ((uint32_t)f32_to_bf16(x[3]) << 16);
-            *reinterpret_cast<uint2*>(L + (int64_t)(p0 + pl) * a.opad + r) = packed;
+            *reinterpret_cast<uint2*>(a.L + off) = packed;
         }
-        if (O) *reinterpret_cast<float4*>(O + (int64_t)(p0 + pl) * a.opad + r) = make_float4(x[0], x[1], x[2], x[3]);
+        if (last) {
+            for (int pi = a.k + (threadIdx.x >> 4); pi < a.kpad; pi += kThreads / 16) {
+                const int64_t off = (int64_t)b * a.kpad * a.opad + (int64_t)pi * a.opad + r0 + 4 * q;
+                *reinterpret_cast<uint2*>(a.L + off) = make_uint2(0u, 0u);
+            }
+        }
+    }
+    if (a.O) {
+        // fp32 O^T[r][p0 .. p1), p contiguous (the layout the apply pass reads)
+        float* O = a.O + (int64_t)b * a.opad * a.kpad;
+        for (int idx = threadIdx.x; idx < kRB * np; idx += kThreads) {
+            const int rl = idx / np, pi = idx % np;
+            O[(int64_t)(r0 + rl) * a.kpad + p0 + pi] = tile[pi][rl];
+        }
+    }
+    if (a.LT) {
+        // L^T[r][p0 .. p1), p contiguous
+        uint16_t* LT = a.LT + (int64_t)b * a.opad * a.kpad;
+        for (int idx = threadIdx.x; idx < kRB * np; idx += kThreads) {
+            const int rl = idx / np, pi = idx % np;
+            LT[(int64_t)(r0 + rl) * a.kpad + p0 + pi] = f32_to_bf16(tile[pi][rl]);
+        }
+        if (last) {
+            const int npad = a.kpad - a.k;
+            for (int idx = threadIdx.x; idx < kRB * npad; idx += kThreads) {
+                const int rl = idx / npad, pi = idx % npad;
+                LT[(int64_t)(r0 + rl) * a.kpad + a.k + pi] = 0;
+            }
+        }
     }
 }
 
@@ -153,22 +233,30 @@ __global__ __launch_bounds__(kThreads) void decay_all(DecayAllArgs a) {
     const int64_t n = a.rows * a.cols;
     for (int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x; i < n;
          i += (int64_t)gridDim.x * kThreads) {
-        M[i] = a.mu * M[i];
+        stg(M + i, a.mu * ldg<float>(M + i));
     }
 }
 
 }  // namespace
 
-hipError_t launch_gather(const GatherArgs& a, int axis, hipStream_t s) {
-    dim3 grid((unsigned)(a.opad / kT), (unsigned)(a.kpad / kT), (unsigned)a.batch);
+hipError_t launch_gather(const GatherArgs& a, int axis, int g_bf16, hipStream_t s) {
     if (axis == 0) {
+        dim3 grid((unsigned)(a.opad / kT), (unsigned)(a.kpad / kT), (unsigned)a.batch);
         if (a.cols % 4 == 0) {
             hipLaunchKernelGGL((gather_rows<4>), grid, dim3(kThreads), 0, s, a);
         } else {
             hipLaunchKernelGGL((gather_rows<1>), grid, dim3(kThreads), 0, s, a);
         }
     } else {
-        hipLaunchKernelGGL(gather_cols, grid, dim3(kThreads), 0, s, a);
+        dim3 grid((unsigned)((a.cols + kCW - 1) / kCW), (unsigned)(a.opad / kRB), (unsigned)a.batch);
+        const bool vec = a.cols % 4 == 0;
+        if (g_bf16) {
+            if (vec) hipLaunchKernelGGL((update_cols<4, uint16_t>), grid, dim3(kThreads), 0, s, a);
+            else hipLaunchKernelGGL((update_cols<1, uint16_t>), grid, dim3(kThreads), 0, s, a);
+        } else {
+            if (vec) hipLaunchKernelGGL((update_cols<4, float>), grid, dim3(kThreads), 0, s, a);
+            else hipLaunchKernelGGL((update_cols<1, float>), grid, dim3(kThreads), 0, s, a);
+        }
     }
     return hipGetLastError();
 }

@@ -7,11 +7,14 @@
 // rounded once at the end, which gives the exactly rounded sum unless the
 // exact sum lies within ~n*2^-106 (relative) of an fp64 rounding boundary.
 //
-// Row mode: one 256-thread block per row; every thread streams 4-element
-// vectors (16 B of M, 8 B of bf16 G) and the block reduces in a fixed order.
-// Column mode: each thread owns 4 adjacent columns of a block of rows and
-// writes double-double partials; a second pass folds the row blocks in
-// order. No floating-point atomics anywhere: results are run-to-run bitwise
+// Row mode: one wave per row (four rows per 256-thread block); every lane
+// streams 4-element vectors (16 B of M, 8 B of bf16 G), eight vectors in
+// flight, and the wave reduces in a fixed shuffle order.
+// Column mode: M is only read here (the gather pass rewrites whole rows of
+// M once the selection is known, so the sum is stored once); each thread
+// owns 4 adjacent columns of a block of rows and writes double-double
+// partials, and a second pass folds the row blocks in order. No
+// floating-point atomics anywhere: results are run-to-run bitwise
 // reproducible.
 #include "dion2_device.h"
 
@@ -28,8 +31,8 @@ __device__ __forceinline__ void accumulate(double x, double& hi, double& lo, dou
     s2 += x * x;
 }
 
-// Fixed-order block reduction of (hi, lo, s2); result valid in thread 0.
-__device__ __forceinline__ void block_reduce(double& hi, double& lo, double& s2) {
+// Fixed-order wave reduction of (hi, lo, s2); result valid in every lane.
+__device__ __forceinline__ void wave_reduce(double& hi, double& lo, double& s2) {
     for (int off = 32; off > 0; off >>= 1) {
         double ohi = __shfl_xor(hi, off);
         double olo = __shfl_xor(lo, off);
@@ -37,55 +40,68 @@ __device__ __forceinline__ void block_reduce(double& hi, double& lo, double& s2)
         dd_add(hi, lo, ohi, olo);
         s2 += os2;
     }
-    __shared__ double red[3][kThreads / 64];
-    const int wave = threadIdx.x >> 6;
-    if ((threadIdx.x & 63) == 0) {
-        red[0][wave] = hi;
-        red[1][wave] = lo;
-        red[2][wave] = s2;
-    }
-    __syncthreads();
-    if (threadIdx.x == 0) {
-        hi = red[0][0];
-        lo = red[1][0];
-        s2 = red[2][0];
-        for (int w = 1; w < kThreads / 64; ++w) {
-            dd_add(hi, lo, red[0][w], red[1][w]);
-            s2 += red[2][w];
-        }
-    }
 }
+
+constexpr int kRowsPerBlock = kThreads / 64;
+constexpr int kRowVecs = 8;   // 4-element vectors per lane in flight
 
 template <int VEC, typename GT>
 __global__ __launch_bounds__(kThreads) void momentum_rows(MatSet ms, int64_t rows, int64_t cols,
                                                           double* __restrict__ l1,
                                                           double* __restrict__ sq) {
     const int b = blockIdx.y;
-    const int64_t row = blockIdx.x;
+    const int lane = threadIdx.x & 63;
+    const int64_t row = (int64_t)blockIdx.x * kRowsPerBlock + (threadIdx.x >> 6);
+    if (row >= rows) return;   // whole wave
     float* __restrict__ M = ms.m(b) + row * cols;
     const GT* __restrict__ G = ms.g<GT>(b) + row * cols;
-    double hi = 0.0, lo = 0.0, s2 = 0.0;
+    // four independent accumulators (element v of each vector goes to set v)
+    // keep the fp64 dependency chains short; they are folded in a fixed order
+    double h4[4] = {0.0, 0.0, 0.0, 0.0}, l4[4] = {0.0, 0.0, 0.0, 0.0}, q4[4] = {0.0, 0.0, 0.0, 0.0};
     if constexpr (VEC == 4) {
-#pragma unroll 2
-        for (int64_t c = threadIdx.x * 4; c < cols; c += kThreads * 4) {
+        constexpr int kStep = 64 * 4 * kRowVecs;
+        int64_t c = 0;
+        for (; c + kStep <= cols; c += kStep) {
+            float m[kRowVecs][4], g[kRowVecs][4];
+#pragma unroll
+            for (int u = 0; u < kRowVecs; ++u) {
+                load4(M + c + (u * 64 + lane) * 4, m[u]);
+                load4(G + c + (u * 64 + lane) * 4, g[u]);
+            }
+#pragma unroll
+            for (int u = 0; u < kRowVecs; ++u) {
+#pragma unroll
+                for (int v = 0; v < 4; ++v) m[u][v] = m[u][v] + g[u][v];
+                stg(M + c + (u * 64 + lane) * 4, make_float4(m[u][0], m[u][1], m[u][2], m[u][3]));
+#pragma unroll
+                for (int v = 0; v < 4; ++v) accumulate(fabs((double)m[u][v]), h4[v], l4[v], q4[v]);
+            }
+        }
+        for (int64_t cc = c + lane * 4; cc < cols; cc += 64 * 4) {
             float m[4], g[4];
-            load4(M + c, m);
-            load4(G + c, g);
+            load4(M + cc, m);
+            load4(G + cc, g);
 #pragma unroll
             for (int v = 0; v < 4; ++v) m[v] = m[v] + g[v];
-            *reinterpret_cast<float4*>(M + c) = make_float4(m[0], m[1], m[2], m[3]);
+            stg(M + cc, make_float4(m[0], m[1], m[2], m[3]));
 #pragma unroll
-            for (int v = 0; v < 4; ++v) accumulate(fabs((double)m[v]), hi, lo, s2);
+            for (int v = 0; v < 4; ++v) accumulate(fabs((double)m[v]), h4[v], l4[v], q4[v]);
         }
     } else {
-        for (int64_t c = threadIdx.x; c < cols; c += kThreads) {
-            float m = M[c] + Elem<GT>::load(G + c);
-            M[c] = m;
-            accumulate(fabs((double)m), hi, lo, s2);
+        for (int64_t c = lane; c < cols; c += 64) {
+            const float m = ldg<float>(M + c) + Elem<GT>::load(G + c);
+            stg(M + c, m);
+            accumulate(fabs((double)m), h4[0], l4[0], q4[0]);
         }
     }
-    block_reduce(hi, lo, s2);
-    if (threadIdx.x == 0) {
+    double hi = h4[0], lo = l4[0], s2 = q4[0];
+#pragma unroll
+    for (int v = 1; v < 4; ++v) {
+        dd_add(hi, lo, h4[v], l4[v]);
+        s2 += q4[v];
+    }
+    wave_reduce(hi, lo, s2);
+    if (lane == 0) {
         l1[(int64_t)b * rows + row] = hi + lo;
         sq[(int64_t)b * rows + row] = s2;
     }
@@ -102,14 +118,14 @@ __global__ __launch_bounds__(kThreads) void momentum_cols_partial(MatSet ms, int
     if (c0 >= cols) return;
     const int64_t r0 = (int64_t)rb * rb_rows;
     const int64_t r1 = r0 + rb_rows < rows ? r0 + rb_rows : rows;
-    float* __restrict__ M = ms.m(b);
+    const float* __restrict__ M = ms.m(b);
     const GT* __restrict__ G = ms.g<GT>(b);
     double hi[VEC], lo[VEC], s2[VEC];
 #pragma unroll
     for (int v = 0; v < VEC; ++v) hi[v] = lo[v] = s2[v] = 0.0;
 #pragma unroll 4
     for (int64_t r = r0; r < r1; ++r) {
-        float* p = M + r * cols + c0;
+        const float* p = M + r * cols + c0;
         const GT* q = G + r * cols + c0;
         if constexpr (VEC == 4) {
             float m[4], g[4];
@@ -117,12 +133,10 @@ __global__ __launch_bounds__(kThreads) void momentum_cols_partial(MatSet ms, int
             load4(q, g);
 #pragma unroll
             for (int v = 0; v < 4; ++v) m[v] = m[v] + g[v];
-            *reinterpret_cast<float4*>(p) = make_float4(m[0], m[1], m[2], m[3]);
 #pragma unroll
             for (int v = 0; v < VEC; ++v) accumulate(fabs((double)m[v]), hi[v], lo[v], s2[v]);
         } else {
-            float m = p[0] + Elem<GT>::load(q);
-            p[0] = m;
+            const float m = ldg<float>(p) + Elem<GT>::load(q);
             accumulate(fabs((double)m), hi[0], lo[0], s2[0]);
         }
     }
@@ -155,7 +169,7 @@ __global__ __launch_bounds__(kThreads) void momentum_cols_final(const double* __
 template <int VEC, typename GT>
 hipError_t launch_typed(const MomentumArgs& a, int axis, hipStream_t s) {
     if (axis == 0) {
-        dim3 grid((unsigned)a.rows, (unsigned)a.batch);
+        dim3 grid((unsigned)((a.rows + kRowsPerBlock - 1) / kRowsPerBlock), (unsigned)a.batch);
         hipLaunchKernelGGL((momentum_rows<VEC, GT>), grid, dim3(kThreads), 0, s, a.ms, a.rows,
                            a.cols, a.l1, a.sq);
     } else {

@@ -4,13 +4,17 @@
 // bit patterns order like unsigned integers; NaN is mapped to +inf's pattern
 // (a corrupted line ranks first and shows in W). An MSD radix select over
 // the 64-bit keys, 8 bits per pass with an LDS histogram, finds the k-th
-// largest key T and how many of the lines equal to T are still needed. A
+// largest key T and how many of the lines equal to T are still needed; the
+// digit of each pass comes from a suffix scan of the histogram by one wave.
+// Keys are cached in LDS when the matrix has at most kCache lines. A
 // second sweep in index order keeps every key > T and the lowest-indexed
 // keys == T (ties to the lower index) and compacts them with wave ballots
 // into K, which therefore comes out ascending.
 //
 // The block also sums the selected lines' squared l2 norms in a fixed order
-// and stores 1 / (||M[K]||_F + eps), the Newton-Schulz normalisation.
+// and stores 1 / (||M[K]||_F + eps), the Newton-Schulz normalisation, and
+// optionally rank[i] = the number of selected lines below i (i <= d_sel),
+// which the column-mode gather uses to place line i at rank[i].
 #include "dion2_device.h"
 
 namespace dion2 {
@@ -19,6 +23,7 @@ namespace {
 constexpr int kThreads = 1024;
 constexpr int kWaves = kThreads / 64;
 constexpr uint64_t kInfBits = 0x7ff0000000000000ull;
+constexpr int kCache = 8192;   // lines whose keys are kept in LDS (64 KB)
 
 __device__ __forceinline__ uint64_t key_of(double v) {
     uint64_t u = (uint64_t)__double_as_longlong(v);
@@ -51,35 +56,65 @@ __global__ __launch_bounds__(kThreads) void select_topk(SelectArgs a) {
     const double* __restrict__ nrm = a.l1 + (int64_t)b * a.d_sel;
     const double* __restrict__ sq = a.sq + (int64_t)b * a.d_sel;
     int32_t* __restrict__ out = a.sel + (int64_t)b * a.k;
+    int32_t* __restrict__ rank = a.rank ? a.rank + (int64_t)b * (a.d_sel + 1) : nullptr;
 
+    __shared__ uint64_t cache[kCache];
     __shared__ unsigned hist[256];
     __shared__ uint64_t s_prefix;
     __shared__ int s_need;
     __shared__ int wave_tot[kWaves];
     __shared__ double red[kWaves];
 
+    const bool cached = a.d_sel <= kCache;   // uniform
+    if (cached)
+        for (int i = threadIdx.x; i < a.d_sel; i += kThreads) cache[i] = key_of(nrm[i]);
+    auto key_at = [&](int i) { return cached ? cache[i] : key_of(nrm[i]); };
+    const int lane = threadIdx.x & 63;
+
     uint64_t prefix = 0, mask = 0;
     int need = a.k;   // how many still to take at or below the current prefix
     for (int shift = 56; shift >= 0; shift -= 8) {
-        for (int i = threadIdx.x; i < 256; i += kThreads) hist[i] = 0;
+        if (threadIdx.x < 256) hist[threadIdx.x] = 0;
         __syncthreads();
-        for (int i = threadIdx.x; i < a.d_sel; i += kThreads) {
-            const uint64_t key = key_of(nrm[i]);
-            if ((key & mask) == prefix) atomicAdd(&hist[(key >> shift) & 0xff], 1u);
+        for (int base = 0; base < a.d_sel; base += kThreads) {
+            const int i = base + threadIdx.x;
+            const uint64_t key = i < a.d_sel ? key_at(i) : 0;
+            const bool in = i < a.d_sel && (key & mask) == prefix;
+            const unsigned digit = (unsigned)(key >> shift) & 0xffu;
+            // one atomic per wave when every candidate lane has the same digit
+            const uint64_t cand = __ballot(in);
+            if (cand == 0) continue;
+            const int first = __builtin_ctzll(cand);
+            const unsigned d0 = __shfl(digit, first);
+            if (__ballot(in && digit != d0) == 0) {
+                if (lane == first) atomicAdd(&hist[d0], (unsigned)__popcll(cand));
+            } else if (in) {
+                atomicAdd(&hist[digit], 1u);
+            }
         }
         __syncthreads();
-        if (threadIdx.x == 0) {
-            int cum = 0, digit = 0;
-            for (int d = 255; d >= 0; --d) {
-                const int h = (int)hist[d];
-                if (cum + h >= need) {
-                    digit = d;
-                    break;
-                }
-                cum += h;
+        if (threadIdx.x < 64) {
+            // lane l owns bins 4l .. 4l+3; above[l] = count in bins > 4l+3
+            unsigned c[4];
+#pragma unroll
+            for (int q = 0; q < 4; ++q) c[q] = hist[4 * lane + q];
+            const unsigned own = c[0] + c[1] + c[2] + c[3];
+            unsigned incl = own;   // inclusive suffix sum over lanes >= l
+#pragma unroll
+            for (int off = 1; off < 64; off <<= 1) {
+                const unsigned v = __shfl_down(incl, off);
+                if (lane + off < 64) incl += v;
             }
-            s_prefix = prefix | ((uint64_t)digit << shift);
-            s_need = need - cum;
+            unsigned above = incl - own;
+            // the digit is the largest d whose suffix count reaches `need`
+#pragma unroll
+            for (int q = 3; q >= 0; --q) {
+                if (above < (unsigned)need && above + c[q] >= (unsigned)need) {
+                    s_prefix = prefix | ((uint64_t)(4 * lane + q) << shift);
+                    s_need = need - (int)above;
+                }
+                above += c[q];
+            }
         }
         __syncthreads();
         prefix = s_prefix;
@@ -93,7 +128,7 @@ __global__ __launch_bounds__(kThreads) void select_topk(SelectArgs a) {
     for (int base = 0; base < a.d_sel; base += kThreads) {
         const int i = base + threadIdx.x;
         const bool valid = i < a.d_sel;
-        const uint64_t key = valid ? key_of(nrm[i]) : 0;
+        const uint64_t key = valid ? key_at(i) : 0;
         const bool eq = valid && key == T;
         int eq_total;
         const int eq_rank = ties_seen + block_excl_prefix(eq, wave_tot, eq_total);
@@ -104,6 +139,7 @@ __global__ __launch_bounds__(kThreads) void select_topk(SelectArgs a) {
             out[pos] = i;
             fro += sq[i];
         }
+        if (rank && valid) rank[i] = pos;   // selected lines before i
         taken += pick_total;
         ties_seen += eq_total;
     }
@@ -115,6 +151,7 @@ __global__ __launch_bounds__(kThreads) void select_topk(SelectArgs a) {
         double f = 0.0;
         for (int w = 0; w < kWaves; ++w) f += red[w];
         a.scale[b] = 1.0 / (sqrt(f) + a.eps);
+        if (rank) rank[a.d_sel] = a.k;
     }
 }
 

@@ -65,13 +65,18 @@ def phase_of(kernel: str):
         return "momentum"
     if k.startswith("select"):
         return "select"
-    if k.startswith("gather") or k.startswith("decay_all"):
+    if k.startswith("gather") or k.startswith("update_cols") or k.startswith("decay_all"):
         return "gather"
     if k.startswith("apply"):
         return "apply"
     m = re.match(r"gemm<(\d+), (?:\(dion2::GemmEpi\))?(\d)", k)
     if m:
-        return {"0": "ns_gram", "1": "ns_poly", "2": "ns_update", "3": "ns_update"}[m.group(2)]
+        npass, epi = int(m.group(1)), int(m.group(2))
+        if epi in (2, 3):            # update / final product with X
+            return "ns_update"
+        if epi == 0 and npass == 1:  # X X^T
+            return "ns_gram"
+        return "ns_poly"             # the s x s products
     return None
 
 

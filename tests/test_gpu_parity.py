@@ -142,9 +142,10 @@ def test_plain_entry_point_equals_ex(hip_device):
     (0, None), (1, None), (3, [(1.5, -0.5, 0.0)] * 3),
     (4, [(3.0, -3.2, 1.2), (2.0, -1.5, 0.5), (1.5, -0.5, 0.0), (1.5, -0.5, 0.0)]),
 ])
+@pytest.mark.parametrize("rows,cols", [(160, 512), (512, 160)], ids=["rowsel", "colsel"])
 @FORMS
-def test_ns_schedules(hip_device, ns_steps, coeffs, form):
-    wl = one_group_workload(160, 512, name=f"sched{ns_steps}")
+def test_ns_schedules(hip_device, ns_steps, coeffs, form, rows, cols):
+    wl = one_group_workload(rows, cols, name=f"sched{ns_steps}")
     W, M, G = workloads.make_group(wl, 0, hip_device)
     res = run_gpu(W, M, G, 0.5, ns_steps=ns_steps, coeffs=coeffs, form=form)
     check_matrix(res, 0, 0.5, ns_steps=ns_steps, coeffs=coeffs)
