@@ -299,19 +299,41 @@ GemmArgs right_args(const Plan& P, const uint16_t* xh, const uint16_t* xl, const
     return x;
 }
 
-// O goes to the layout the apply pass reads along W's rows: L [kpad][opad]
-// for row selection, L^T [opad][kpad] for column selection.
-void final_output(const Plan& P, GemmArgs& x, float* O) {
+// The final Newton-Schulz product either stores O for the apply pass, in the
+// layout that pass reads along W's rows (L [kpad][opad] for row selection,
+// L^T [opad][kpad] for columns), or, for row selection with O in the L
+// layout and bf16 W, applies the update step itself (EPI_APPLY).
+struct FinalSpec {
+    bool fuse;          // EPI_APPLY instead of EPI_FINAL + K5
+    MatSet ms;
+    const int32_t* sel;
+    double lr_eff;
+    float* dbg;
+};
+
+GemmEpi final_output(const Plan& P, GemmArgs& x, float* O, const FinalSpec& f) {
     const bool want_lt = P.axis == 1;
+    x.out_transposed = P.z_is_L == want_lt ? 1 : 0;   // Z's natural layout is L iff z_is_L
+    if (f.fuse) {
+        x.out_transposed = 0;
+        x.ms = f.ms;
+        x.sel = f.sel;
+        x.k = (int)P.k;
+        x.d_oth = (int)P.d_oth;
+        x.cols = P.cols;
+        x.lr_eff = f.lr_eff;
+        x.dbg = f.dbg;
+        return EPI_APPLY;
+    }
     x.out0 = O;
     x.sOut0 = P.kpad * P.opad;
     x.ldo0 = (int)(want_lt ? P.kpad : P.opad);
-    x.out_transposed = P.z_is_L == want_lt ? 1 : 0;   // Z's natural layout is L iff z_is_L
+    return EPI_FINAL;
 }
 
 // DIRECT: per step A = Z Z^T (hi / lo), B = b A + c A^2, Z <- a Z + B Z.
 hipError_t ns_direct(const Plan& P, uint16_t* Z0, uint16_t* Z1, uint16_t* const* sq, float* O,
-                     int ns_steps, const dion2_options& opt, hipStream_t stream) {
+                     int ns_steps, const dion2_options& opt, const FinalSpec& fin, hipStream_t stream) {
     const double s_r = (double)(P.k < P.d_oth ? P.k : P.d_oth);   // unpadded sides
     const double l_r = (double)(P.k < P.d_oth ? P.d_oth : P.k);
     const double nb = (double)P.batch;
@@ -343,15 +365,16 @@ hipError_t ns_direct(const Plan& P, uint16_t* Z0, uint16_t* Z1, uint16_t* const*
         x.sE = P.s_pad * P.l_pad;
         x.lde = (int)P.l_pad;
         const bool last = t + 1 == ns_steps;
+        GemmEpi epi = EPI_UPDATE;
         if (!last) {
             x.out0 = zbuf[1 - cur];
             x.sOut0 = P.s_pad * P.l_pad;
             x.ldo0 = (int)P.l_pad;
         } else {
-            final_output(P, x, O);
+            epi = final_output(P, x, O, fin);
         }
         e = timed(DION2_PHASE_NS_UPDATE, 2.0 * s_r * s_r * l_r * nb, 1, stream,
-                  [&] { return launch_gemm(x, last ? EPI_FINAL : EPI_UPDATE, 1, stream); });
+                  [&] { return launch_gemm(x, epi, 1, stream); });
         if (e != hipSuccess) return e;
         cur = 1 - cur;
     }
@@ -362,7 +385,7 @@ hipError_t ns_direct(const Plan& P, uint16_t* Z0, uint16_t* Z1, uint16_t* const*
 // A_{t+1} = Q_t (Q_t A_t); finally O = P Z. Every s x s matrix is a
 // polynomial in A_0, hence symmetric, and all of them commute.
 hipError_t ns_gram(const Plan& P, const uint16_t* Z, uint16_t* const* sq, float* O, int ns_steps,
-                   const dion2_options& opt, hipStream_t stream) {
+                   const dion2_options& opt, const FinalSpec& fin, hipStream_t stream) {
     const double s_r = (double)(P.k < P.d_oth ? P.k : P.d_oth);
     const double l_r = (double)(P.k < P.d_oth ? P.d_oth : P.k);
     const double nb = (double)P.batch;
@@ -415,9 +438,9 @@ hipError_t ns_gram(const Plan& P, const uint16_t* Z, uint16_t* const* sq, float*
     if (e != hipSuccess) return e;
     // O = (P_hi + P_lo) Z
     GemmArgs x = right_args(P, Ph[cur], Pl[cur], Z);
-    final_output(P, x, O);
+    const GemmEpi epi = final_output(P, x, O, fin);
     return timed(DION2_PHASE_NS_UPDATE, 4.0 * s_r * s_r * l_r * nb, 1, stream,
-                 [&] { return launch_gemm(x, EPI_FINAL, 2, stream); });
+                 [&] { return launch_gemm(x, epi, 2, stream); });
 }
 
 // ------------------------------------------------------------------ step
@@ -591,9 +614,16 @@ int run_step(const Plan& P, void* W, float* M, const void* G, const Tables* tabs
     }
 
     // K4: Newton-Schulz
+    FinalSpec fin{};
+    fin.lr_eff = (double)lr * std::sqrt((double)P.rows / (double)P.cols);
+    fin.fuse = ns_steps > 0 && P.axis == 0 && P.z_is_L && opt.w_dtype == DION2_DTYPE_BF16 &&
+               P.cols % 8 == 0 && P.cols >= 16;
+    fin.ms = ms;
+    fin.sel = sel;
+    fin.dbg = opt.dbg_update;
     if (ns_steps > 0) {   // with no step the gather has written O
-        e = P.gram ? ns_gram(P, Z0, sbuf, O, ns_steps, opt, stream)
-                   : ns_direct(P, Z0, Z1, sbuf, O, ns_steps, opt, stream);
+        e = P.gram ? ns_gram(P, Z0, sbuf, O, ns_steps, opt, fin, stream)
+                   : ns_direct(P, Z0, Z1, sbuf, O, ns_steps, opt, fin, stream);
     }
     if (e != hipSuccess) return hip_fail(e, "launch K4 Newton-Schulz");
 
@@ -610,11 +640,13 @@ int run_step(const Plan& P, void* W, float* M, const void* G, const Tables* tabs
     aa.sel = sel;
     aa.rank = rank;
     aa.O = O;
-    aa.lr_eff = (double)lr * std::sqrt((double)P.rows / (double)P.cols);
+    aa.lr_eff = fin.lr_eff;
     aa.dbg = opt.dbg_update;
-    e = timed(DION2_PHASE_APPLY, k5_bytes, 1, stream,
-              [&] { return launch_apply(aa, P.axis, opt.w_dtype == DION2_DTYPE_BF16, stream); });
-    if (e != hipSuccess) return hip_fail(e, "launch K5 apply");
+    if (!fin.fuse) {   // otherwise the final Newton-Schulz product has applied it
+        e = timed(DION2_PHASE_APPLY, k5_bytes, 1, stream,
+                  [&] { return launch_apply(aa, P.axis, opt.w_dtype == DION2_DTYPE_BF16, stream); });
+        if (e != hipSuccess) return hip_fail(e, "launch K5 apply");
+    }
 
     if (opt.dbg_sel_idx) {
         e = hipMemcpyAsync(opt.dbg_sel_idx, sel, (size_t)P.batch * P.k * 4, hipMemcpyDeviceToDevice, stream);

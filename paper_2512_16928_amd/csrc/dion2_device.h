@@ -199,9 +199,14 @@ hipError_t launch_decay_all(const DecayAllArgs& a, hipStream_t s);
 //   EPI_UPDATE (B as [K][N], npass 1): out0 = bf16(ca E0 + C)
 //   EPI_FINAL  (B as [K][N], npass 1 or 2): out0 = ca E0 + C in fp32 (no
 //              E0 term when E0 is null), or its transpose when out_transposed
+//   EPI_APPLY  (B as [K][N], npass 1 or 2): O = ca E0 + C (row selection, O in
+//              the L layout) is not stored; the update step is applied
+//              directly: W[K[p]][j] <- bf16(W[K[p]][j] - lr_eff O[p][j]) for
+//              p < k, j < d_oth (bf16 W, cols % 8 == 0); dbg gets O if set
 // The symmetric products (EPI_SPLIT, EPI_POLY, EPI_QPOLY) compute the tiles
 // on and above the diagonal and mirror them.
-enum GemmEpi { EPI_SPLIT = 0, EPI_POLY = 1, EPI_UPDATE = 2, EPI_FINAL = 3, EPI_QPOLY = 4 };
+enum GemmEpi { EPI_SPLIT = 0, EPI_POLY = 1, EPI_UPDATE = 2, EPI_FINAL = 3, EPI_QPOLY = 4,
+               EPI_APPLY = 5 };
 struct GemmArgs {
     const uint16_t* A0; const uint16_t* A1;   // A operand(s), [M][K] ld lda
     const uint16_t* B0; const uint16_t* B1;   // B operand(s), [N][K] or [K][N], ld ldb
@@ -214,6 +219,13 @@ struct GemmArgs {
     void* out0; int64_t sOut0; int ldo0;
     void* out1; int64_t sOut1; int ldo1;
     int out_transposed;                        // EPI_FINAL: write out0[j][i]
+    // EPI_APPLY only
+    MatSet ms;                                 // W
+    const int32_t* sel;                        // [batch][k]
+    int k, d_oth;
+    int64_t cols;
+    double lr_eff;
+    float* dbg;                                // nullable [batch][k][d_oth]
 };
 hipError_t launch_gemm(const GemmArgs& a, GemmEpi epi, int npass, hipStream_t s);
 

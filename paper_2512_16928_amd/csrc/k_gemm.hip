@@ -313,7 +313,8 @@ __global__ __launch_bounds__(T::THREADS) void gemm(GemmArgs a) {
     // fetched first so their latency hides behind the main loop.
     const int er = lane >> 1;          // epilogue: row (or transposed row) of this lane
     const int ec = (lane & 1) * 16;    // epilogue: 16 consecutive columns
-    constexpr bool kPreE0 = EPI == EPI_POLY || EPI == EPI_QPOLY || EPI == EPI_UPDATE || EPI == EPI_FINAL;
+    constexpr bool kPreE0 = EPI == EPI_POLY || EPI == EPI_QPOLY || EPI == EPI_UPDATE || EPI == EPI_FINAL ||
+                            EPI == EPI_APPLY;
     constexpr bool kPreE1 = EPI == EPI_POLY || EPI == EPI_QPOLY;
     const bool pre = kPreE0 && a.E0 != nullptr && !(EPI == EPI_FINAL && a.out_transposed);
     uint4 e0[T::FM][T::FN][2], e1[T::FM][T::FN][2];
@@ -331,6 +332,29 @@ __global__ __launch_bounds__(T::THREADS) void gemm(GemmArgs a) {
                     e1[i][j][1] = reinterpret_cast<const uint4*>(a.E1 + eo)[1];
                 }
             }
+    }
+
+    // EPI_APPLY: the W entries this lane updates (16 consecutive bf16 per
+    // block, row K[p] of W) are fetched before the main loop as well.
+    // Addresses are clamped into W so the loads are unconditional; the
+    // epilogue uses them only where they are the right entries.
+    int32_t wrow[T::FM];
+    uint4 wv[T::FM][T::FN][2];
+    if constexpr (EPI == EPI_APPLY) {
+        const uint16_t* W = a.ms.w<uint16_t>(b);
+#pragma unroll
+        for (int i = 0; i < T::FM; ++i) {
+            const int p = row0 + wm * T::TM + i * 32 + er;
+            wrow[i] = ldg<int32_t>(a.sel + (int64_t)b * a.k + (p < a.k ? p : a.k - 1));
+#pragma unroll
+            for (int j = 0; j < T::FN; ++j) {
+                int64_t jc = col0 + wn * T::TN + j * 32 + ec;
+                jc = jc + 16 <= a.cols ? jc : a.cols - 16;
+                const uint16_t* src = W + (int64_t)wrow[i] * a.cols + jc;
+                wv[i][j][0] = ldg<uint4>(src);
+                wv[i][j][1] = ldg<uint4>(src + 8);
+            }
+        }
     }
 
     f32x16 acc[T::FM][T::FN];
@@ -392,7 +416,7 @@ __global__ __launch_bounds__(T::THREADS) void gemm(GemmArgs a) {
             }
             const int64_t orow = transposed ? Cc + er : R + er;
             const int64_t ocol = transposed ? R + ec : Cc + ec;
-            if constexpr (EPI == EPI_UPDATE || EPI == EPI_FINAL) {
+            if constexpr (EPI == EPI_UPDATE || EPI == EPI_FINAL || EPI == EPI_APPLY) {
                 // + a Z at this lane's 16 entries (none when E0 is null)
                 if (pre) {
                     const uint4 z0 = e0[i][j][0];
@@ -433,7 +457,41 @@ __global__ __launch_bounds__(T::THREADS) void gemm(GemmArgs a) {
                     }
                 }
             }
-            store16<EPI>(a, b, orow, ocol, v);
+            if constexpr (EPI == EPI_APPLY) {
+                // W[K[p]][j] <- bf16(W[K[p]][j] - lr_eff O[p][j]) (update step, eq. (1))
+                if (orow < a.k) {
+                    uint16_t* w = a.ms.w<uint16_t>(b) + (int64_t)wrow[i] * a.cols + ocol;
+                    if (ocol + 16 <= a.d_oth) {
+                        const uint32_t ww[8] = {wv[i][j][0].x, wv[i][j][0].y, wv[i][j][0].z, wv[i][j][0].w,
+                                                wv[i][j][1].x, wv[i][j][1].y, wv[i][j][1].z, wv[i][j][1].w};
+                        uint32_t o[8];
+#pragma unroll
+                        for (int q = 0; q < 8; ++q) {
+                            const double w0 = (double)bf16_bits_to_f32(ww[q] & 0xffffu);
+                            const double w1 = (double)bf16_bits_to_f32(ww[q] >> 16);
+                            o[q] = (uint32_t)f64_to_bf16(__dsub_rn(w0, __dmul_rn(a.lr_eff, (double)v[2 * q]))) |
+                                   ((uint32_t)f64_to_bf16(__dsub_rn(w1, __dmul_rn(a.lr_eff, (double)v[2 * q + 1]))) << 16);
+                        }
+                        stg(w, make_uint4(o[0], o[1], o[2], o[3]));
+                        stg(w + 8, make_uint4(o[4], o[5], o[6], o[7]));
+                    } else {
+#pragma unroll
+                        for (int q = 0; q < 16; ++q) {
+                            if (ocol + q < a.d_oth) {
+                                const double x = (double)bf16_bits_to_f32(ldg<uint16_t>(w + q));
+                                stg(w + q, f64_to_bf16(__dsub_rn(x, __dmul_rn(a.lr_eff, (double)v[q]))));
+                            }
+                        }
+                    }
+                    if (a.dbg) {
+#pragma unroll
+                        for (int q = 0; q < 16; ++q)
+                            if (ocol + q < a.d_oth) a.dbg[((int64_t)b * a.k + orow) * a.d_oth + ocol + q] = v[q];
+                    }
+                }
+            } else {
+                store16<EPI>(a, b, orow, ocol, v);
+            }
             if (SYM && row0 != col0) {
                 float t[16];
                 mirror16<T>(stage, v, t, er, ec);
@@ -486,6 +544,11 @@ hipError_t launch_gemm(const GemmArgs& a, GemmEpi epi, int npass, hipStream_t s)
         case EPI_FINAL:
             if (npass == 1) return launch_tile<1, EPI_FINAL, TU>(a, s);
             if (npass == 2) return launch_tile<2, EPI_FINAL, TU2>(a, s);
+            break;
+        case EPI_APPLY:
+            if (a.cols % 8 || a.cols < 16 || a.out_transposed) break;
+            if (npass == 1) return launch_tile<1, EPI_APPLY, TU>(a, s);
+            if (npass == 2) return launch_tile<2, EPI_APPLY, TU2>(a, s);
             break;
     }
     return hipErrorInvalidValue;

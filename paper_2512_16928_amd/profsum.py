@@ -72,7 +72,7 @@ def phase_of(kernel: str):
     m = re.match(r"gemm<(\d+), (?:\(dion2::GemmEpi\))?(\d)", k)
     if m:
         npass, epi = int(m.group(1)), int(m.group(2))
-        if epi in (2, 3):            # update / final product with X
+        if epi in (2, 3, 5):         # update / final product with X (5: with the update step)
             return "ns_update"
         if epi == 0 and npass == 1:  # X X^T
             return "ns_gram"
