@@ -139,10 +139,55 @@ def select_top(norms, k):
     return np.sort(order[:k]).astype(np.int64)
 
 
-def select_random(d_sel, k, rng):
-    """Select_alpha, Random rule: a uniformly random k-subset (Algorithm 1,
-    selection method 2), ascending. Not used by the default step."""
-    return np.sort(rng.choice(d_sel, size=k, replace=False)).astype(np.int64)
+# Philox-4x32-10 (Salmon, Moraes, Dror and Shaw, "Parallel random numbers:
+# as easy as 1, 2, 3", SC 2011): a keyed bijection on 128-bit counters made
+# of ten rounds; each round multiplies two of the four words by fixed odd
+# constants, swaps the halves and mixes in the round key, and the key is
+# bumped by the Weyl constants between rounds.
+PHILOX_M = (0xD2511F53, 0xCD9E8D57)     # round multipliers
+PHILOX_W = (0x9E3779B9, 0xBB67AE85)     # key increments (golden ratio, sqrt(3) - 1)
+_U32 = np.uint64(0xFFFFFFFF)
+
+
+def philox4x32_10(counter, key):
+    """Philox-4x32-10 of uint32 arrays counter [..., 4] and key [..., 2]
+    (broadcasting); returns uint32 [..., 4]."""
+    counter = np.asarray(counter, dtype=np.uint64)
+    key = np.asarray(key, dtype=np.uint64)
+    c0, c1, c2, c3 = (counter[..., i] & _U32 for i in range(4))
+    k0, k1 = key[..., 0] & _U32, key[..., 1] & _U32
+    m0, m1 = np.uint64(PHILOX_M[0]), np.uint64(PHILOX_M[1])
+    for r in range(10):
+        if r:
+            k0 = (k0 + np.uint64(PHILOX_W[0])) & _U32
+            k1 = (k1 + np.uint64(PHILOX_W[1])) & _U32
+        p0 = c0 * m0                       # 32 x 32 -> 64 bits, exact in uint64
+        p1 = c2 * m1
+        c0, c1, c2, c3 = ((p1 >> np.uint64(32)) ^ c1 ^ k0, p1 & _U32,
+                          (p0 >> np.uint64(32)) ^ c3 ^ k1, p0 & _U32)
+    return np.stack([c0, c1, c2, c3], axis=-1).astype(np.uint32)
+
+
+def random_line_keys(d_sel, seed, step, matrix):
+    """64-bit key of every line for the Random rule: Philox-4x32-10 of the
+    counter (line, matrix, step low word, step high word) under the key
+    (seed low word, seed high word); the first two output words, high first."""
+    i = np.arange(d_sel, dtype=np.uint64)
+    seed, step, matrix = int(seed), int(step), int(matrix)
+    ctr = np.stack([i, np.full_like(i, matrix & 0xFFFFFFFF), np.full_like(i, step & 0xFFFFFFFF),
+                    np.full_like(i, step >> 32)], axis=-1)
+    out = philox4x32_10(ctr, [seed & 0xFFFFFFFF, seed >> 32]).astype(np.uint64)
+    return (out[..., 0] << np.uint64(32)) | out[..., 1]
+
+
+def select_random(d_sel, k, seed, step, matrix):
+    """Select_alpha, Random rule (Algorithm 1, selection step: lines chosen
+    uniformly at random; Sec. 3.1): the k lines with the smallest keys
+    (i.i.d. uniform, so every k-subset is equally likely), ties to the lower
+    index, returned ascending."""
+    keys = random_line_keys(d_sel, seed, step, matrix)
+    order = np.lexsort((np.arange(d_sel), keys))
+    return np.sort(order[:k]).astype(np.int64)
 
 
 def gather(M, K, axis):
@@ -219,7 +264,7 @@ def apply_update(W, K, O, lr, axis, w_dtype):
 
 def dion2_step(W, M, G, alpha, mu=DEFAULT_MU, lr=DEFAULT_LR, ns_steps=5,
                axis=AXIS_AUTO, coeffs=None, eps=DEFAULT_EPS, w_dtype="f32",
-               store="fp32", decay_all=False, select="l1", rng=None):
+               store="fp32", decay_all=False, select="l1", seed=0, step=0, matrix=0):
     """One Dion2 step on one matrix (Algorithm 1). Inputs are not modified.
 
     W: (rows, cols) values of W's storage type w_dtype ('f32' | 'bf16').
@@ -228,7 +273,8 @@ def dion2_step(W, M, G, alpha, mu=DEFAULT_MU, lr=DEFAULT_LR, ns_steps=5,
     Returns a dict with the new W (fp64 array of w_dtype values), the new M,
     the selected indices K (ascending), the Newton-Schulz output O in the
     submatrix's own orientation (k x cols for rows, rows x k for columns),
-    the l1 norms, and the resolved axis.
+    the l1 norms, and the resolved axis. select='random' takes the Random
+    rule keyed by (seed, step, matrix).
     """
     W = np.asarray(W)
     rows, cols = W.shape
@@ -243,7 +289,7 @@ def dion2_step(W, M, G, alpha, mu=DEFAULT_MU, lr=DEFAULT_LR, ns_steps=5,
     if select == "l1":
         K = select_top(norms, k)
     elif select == "random":
-        K = select_random(d_sel, k, rng)
+        K = select_random(d_sel, k, seed, step, matrix)
     else:
         raise ValueError(select)
     X = gather(M1, K, ax)

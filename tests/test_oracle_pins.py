@@ -375,3 +375,68 @@ def test_paper_constants_are_the_defaults():
     for a in pc["alphas_swept"]["value"]:
         for d in (1024, 2048):
             assert oracle.num_selected(a, d) == a * d
+
+
+# ---- Random rule (Algorithm 1, selection step; Sec. 3.1) --------------------
+
+# Published known-answer values of Philox-4x32-10 (Salmon et al., SC 2011):
+# (counter words, key words) -> output words.
+PHILOX_KAT = [
+    ((0, 0, 0, 0), (0, 0), (0x6627E8D5, 0xE169C58D, 0xBC57AC4C, 0x9B00DBD8)),
+    ((0xFFFFFFFF,) * 4, (0xFFFFFFFF, 0xFFFFFFFF), (0x408F276D, 0x41C83B0E, 0xA20BC7C6, 0x6D5451FD)),
+    ((0x243F6A88, 0x85A308D3, 0x13198A2E, 0x03707344), (0xA4093822, 0x299F31D0),
+     (0xD16CFE09, 0x94FDCCEB, 0x5001E420, 0x24126EA1)),
+]
+
+
+@pytest.mark.parametrize("ctr,key,want", PHILOX_KAT)
+def test_philox_known_answers(ctr, key, want):
+    got = tuple(int(x) for x in oracle.philox4x32_10(ctr, key))
+    assert got == want
+
+
+def test_philox_broadcasts_like_scalar_calls():
+    ctr = np.array([[i, 7, 9, 11] for i in range(5)], dtype=np.uint32)
+    batch = oracle.philox4x32_10(ctr, (3, 4))
+    for i in range(5):
+        assert tuple(batch[i]) == tuple(oracle.philox4x32_10(ctr[i], (3, 4)))
+
+
+def test_random_selection_is_the_k_smallest_keys():
+    """Brute force: sort (key, index) pairs with Python's sort."""
+    for d, k, seed, step, m in [(37, 5, 1, 0, 0), (300, 75, 2**40 + 3, 2**33 + 1, 17), (8, 8, 5, 6, 7)]:
+        keys = oracle.random_line_keys(d, seed, step, m)
+        want = sorted(i for _, i in sorted((int(kk), i) for i, kk in enumerate(keys))[:k])
+        assert oracle.select_random(d, k, seed, step, m).tolist() == want
+
+
+def test_random_selection_valid_and_keyed():
+    K = oracle.select_random(1000, 250, 42, 3, 5)
+    assert len(K) == 250 and len(set(K.tolist())) == 250
+    assert np.all(np.diff(K) > 0) and K[0] >= 0 and K[-1] < 1000
+    assert np.array_equal(K, oracle.select_random(1000, 250, 42, 3, 5))       # deterministic
+    for other in [(43, 3, 5), (42, 4, 5), (42, 3, 6)]:                          # seed, step, matrix
+        assert not np.array_equal(K, oracle.select_random(1000, 250, *other))
+
+
+def test_random_selection_is_uniform():
+    """Each line's inclusion count over 3000 draws is Binomial(3000, k/d):
+    within 5 standard deviations of its mean."""
+    d, k, n = 40, 10, 3000
+    counts = np.zeros(d)
+    for step in range(n):
+        counts[oracle.select_random(d, k, 99, step, 0)] += 1
+    mean, sd = n * k / d, np.sqrt(n * (k / d) * (1 - k / d))
+    assert np.all(np.abs(counts - mean) < 5 * sd)
+
+
+def test_step_with_random_selection():
+    rng = np.random.default_rng(23)
+    W, M, G = make_case(rng, 32, 48)     # rows are selected: d_sel = 32, k = 8
+    out = oracle.dion2_step(W, M, G, alpha=0.25, select="random", seed=7, step=2, matrix=1)
+    K = out["K"]
+    assert K.tolist() == oracle.select_random(32, 8, 7, 2, 1).tolist()
+    keep = [i for i in range(32) if i not in set(K.tolist())]
+    np.testing.assert_array_equal(out["W"][keep], W[keep])
+    acc = oracle.momentum_accumulate(M, G)
+    np.testing.assert_array_equal(out["M"][keep], acc[keep])
