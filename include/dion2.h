@@ -20,7 +20,7 @@
  *   - The l1 norm of each line is the exact sum of |M_ij| rounded once to
  *     fp64 (double-double accumulation), so selection does not depend on a
  *     summation order. Ties go to the lower index; NaN ranks as +inf.
- *     K is ascending.
+ *     K is ascending. (dion2_options.select_rule selects the Random rule.)
  *   - Newton-Schulz: X = M[K,:] / (||M[K,:]||_F + eps), then per step
  *     A = X X^T, B = b A + c A^2, X <- a X + B X on the orientation with the
  *     smaller Gram matrix (s x s, X is s x l, s <= l); X is rounded once to
@@ -90,6 +90,12 @@ typedef enum dion2_dtype {
     DION2_DTYPE_BF16 = 1
 } dion2_dtype;
 
+typedef enum dion2_select_rule {
+    DION2_SELECT_L1 = 0,     /* the k lines of largest l1 norm (default)         */
+    DION2_SELECT_RANDOM = 1  /* k lines uniformly at random: the k smallest of
+                                Philox-4x32-10 keys, see dion2_options          */
+} dion2_select_rule;
+
 typedef enum dion2_ns_form {
     DION2_NS_AUTO = 0,   /* GRAM when l >= 3 s (padded sides), else DIRECT     */
     DION2_NS_DIRECT = 1, /* iterate on X (s x l)                               */
@@ -114,10 +120,22 @@ typedef struct dion2_options {
                                 selected line per row (row k of O^T for columns),
                                 before the lr*sqrt(rows/cols) scale                 */
     int ns_form;             /* dion2_ns_form (default DION2_NS_AUTO)               */
+    int select_rule;         /* dion2_select_rule (default DION2_SELECT_L1).
+                                RANDOM (Algorithm 1, selection step; Sec. 3.1):
+                                line i of matrix b gets the 64-bit key made of the
+                                first two output words (high first) of
+                                Philox-4x32-10 with counter (i, rand_matrix0 + b,
+                                rand_step low, rand_step high) and key (rand_seed
+                                low, rand_seed high); the k smallest keys are
+                                selected, ties to the lower index             */
+    uint64_t rand_seed;      /* RANDOM: generator key (default 0)                   */
+    uint64_t rand_step;      /* RANDOM: optimizer step, so each step draws anew     */
+    int64_t rand_matrix0;    /* RANDOM: index of the batch's first matrix; >= 0 and
+                                rand_matrix0 + batch <= 2^32                       */
 } dion2_options;
 
 /* Defaults: bf16 W and G, Muon quintic, eps 1e-7, selective decay, internal
-   workspace, no debug outputs, Newton-Schulz form chosen by shape. */
+   workspace, no debug outputs, Newton-Schulz form chosen by shape, l1 rule. */
 void dion2_options_init(dion2_options* opt);
 
 /* One matrix. W, G: bf16 [rows][cols]; M: fp32 [rows][cols]. Algorithm 1. */

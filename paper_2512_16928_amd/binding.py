@@ -30,6 +30,7 @@ AXIS_COLS = 1
 DTYPE_F32 = 0
 DTYPE_BF16 = 1
 NS_AUTO, NS_DIRECT, NS_GRAM = 0, 1, 2
+SELECT_L1, SELECT_RANDOM = 0, 1
 
 MAX_NS_STEPS = 16
 
@@ -62,6 +63,10 @@ class Options(ctypes.Structure):
         ("dbg_norms", c_void_p),
         ("dbg_update", c_void_p),
         ("ns_form", c_int),
+        ("select_rule", c_int),
+        ("rand_seed", ctypes.c_uint64),
+        ("rand_step", ctypes.c_uint64),
+        ("rand_matrix0", ctypes.c_int64),
     ]
 
 
@@ -197,12 +202,13 @@ def dion2_step_batched(Ws, Ms, Gs, alpha, mu=0.95, lr=0.02, ns_steps=5, axis=AXI
 def dion2_step_ex(W, M, G, alpha, mu=0.95, lr=0.02, ns_steps=5, axis=AXIS_AUTO, *,
                   ns_coeffs=None, ns_eps=1e-7, decay_all=False, workspace=None,
                   dbg_sel_idx=None, dbg_norms=None, dbg_update=None, ns_form=NS_AUTO,
-                  stream=None):
+                  select_rule=SELECT_L1, rand_seed=0, rand_step=0, rand_matrix0=0, stream=None):
     """Full control. W, M, G are [rows, cols] or [batch, rows, cols]; W and G
     may be bf16 or fp32. Debug outputs are preallocated device tensors:
     dbg_sel_idx int32 [batch, k], dbg_norms float64 [batch, d_sel],
     dbg_update float32 [batch, k, d_oth]. ns_form is NS_AUTO, NS_DIRECT or
-    NS_GRAM (the Newton-Schulz evaluation order)."""
+    NS_GRAM (the Newton-Schulz evaluation order). select_rule SELECT_RANDOM
+    draws the lines from Philox keys of (rand_seed, rand_step, rand_matrix0 + b)."""
     if W.dim() == 2:
         W, M, G = W.unsqueeze(0), M.unsqueeze(0), G.unsqueeze(0)
     _mats(W, M, G, 3)
@@ -221,6 +227,10 @@ def dion2_step_ex(W, M, G, alpha, mu=0.95, lr=0.02, ns_steps=5, axis=AXIS_AUTO, 
     opt.ns_eps = ns_eps
     opt.decay_all = 1 if decay_all else 0
     opt.ns_form = ns_form
+    opt.select_rule = select_rule
+    opt.rand_seed = rand_seed
+    opt.rand_step = rand_step
+    opt.rand_matrix0 = rand_matrix0
     for name, t, dt in (("dbg_sel_idx", dbg_sel_idx, torch.int32),
                         ("dbg_norms", dbg_norms, torch.float64),
                         ("dbg_update", dbg_update, torch.float32)):

@@ -581,6 +581,10 @@ int run_step(const Plan& P, void* W, float* M, const void* G, const Tables* tabs
     sa.sel = sel;
     sa.scale = scale;
     sa.rank = rank;
+    sa.rule = opt.select_rule;
+    sa.seed = opt.rand_seed;
+    sa.step = opt.rand_step;
+    sa.matrix0 = opt.rand_matrix0;
     e = timed(DION2_PHASE_SELECT, (double)P.batch * (double)P.d_sel * 16.0, 1, stream,
               [&] { return launch_select(sa, stream); });
     if (e != hipSuccess) return hip_fail(e, "launch K2 select");
@@ -674,6 +678,8 @@ int validate_common(float mu, float lr, int ns_steps, const dion2_options& opt) 
         return fail(DION2_ERR_INVALID_ARG, "ns_eps must be finite and >= 0");
     if (opt.decay_all != 0 && opt.decay_all != 1)
         return fail(DION2_ERR_INVALID_ARG, "decay_all must be 0 or 1");
+    if (opt.select_rule != DION2_SELECT_L1 && opt.select_rule != DION2_SELECT_RANDOM)
+        return fail(DION2_ERR_INVALID_ARG, "select_rule %d is not L1 or RANDOM", opt.select_rule);
     if (opt.ns_coeffs) {
         for (int i = 0; i < 3 * ns_steps; ++i)
             if (!std::isfinite(opt.ns_coeffs[i]))
@@ -693,6 +699,10 @@ int step_impl(void* W, float* M, const void* G, const Tables* tabs, int batch, i
     if (st != DION2_OK) return st;
     st = validate_common(mu, lr, ns_steps, opt);
     if (st != DION2_OK) return st;
+    if (opt.select_rule == DION2_SELECT_RANDOM &&
+        (opt.rand_matrix0 < 0 || opt.rand_matrix0 + batch > (int64_t(1) << 32)))
+        return fail(DION2_ERR_INVALID_ARG, "rand_matrix0 %lld with batch %d leaves [0, 2^32)",
+                    (long long)opt.rand_matrix0, batch);
     if (tabs) {
         if (!tabs->W || !tabs->M || !tabs->G)
             return fail(DION2_ERR_INVALID_ARG, "pointer tables must not be NULL");
@@ -730,6 +740,10 @@ void dion2_options_init(dion2_options* opt) {
     opt->ns_eps = 1e-7f;
     opt->decay_all = 0;
     opt->ns_form = DION2_NS_AUTO;
+    opt->select_rule = DION2_SELECT_L1;
+    opt->rand_seed = 0;
+    opt->rand_step = 0;
+    opt->rand_matrix0 = 0;
 }
 
 int dion2_step(void* W, float* M, const void* G, int64_t rows, int64_t cols, float alpha,

@@ -161,6 +161,9 @@ struct SelectArgs {
     int32_t* sel;      // [batch][k] ascending
     double* scale;     // [batch] 1 / (sqrt(sum sq over K) + eps)
     int32_t* rank;     // nullable [batch][d_sel + 1]: selected lines below i
+    int rule;          // 0: largest l1 norms, 1: smallest Philox keys (Random rule)
+    uint64_t seed, step;
+    int64_t matrix0;   // Random rule: counter word of the batch's first matrix
 };
 hipError_t launch_select(const SelectArgs& a, hipStream_t s);
 

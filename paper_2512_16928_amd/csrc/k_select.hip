@@ -1,4 +1,5 @@
-// K2: Select_alpha, Default rule -- the k lines of largest l1 norm.
+// K2: Select_alpha -- the k lines of largest l1 norm (Default rule), or k
+// lines uniformly at random (Random rule) from counter-based Philox keys.
 //
 // One 1024-thread block per matrix. Norms are non-negative fp64, so their
 // bit patterns order like unsigned integers; NaN is mapped to +inf's pattern
@@ -24,6 +25,31 @@ constexpr int kThreads = 1024;
 constexpr int kWaves = kThreads / 64;
 constexpr uint64_t kInfBits = 0x7ff0000000000000ull;
 constexpr int kCache = 8192;   // lines whose keys are kept in LDS (64 KB)
+
+// Random rule: Philox-4x32-10 (Salmon, Moraes, Dror and Shaw, SC 2011), ten
+// rounds of two 32 x 32 -> 64-bit products with the halves swapped and the
+// round key mixed in, the key bumped by the Weyl constants between rounds.
+// The line's key is the first two output words, high first.
+__device__ __forceinline__ uint64_t philox_line_key(uint32_t line, uint32_t matrix, uint64_t step,
+                                                    uint64_t seed) {
+    uint32_t c0 = line, c1 = matrix, c2 = (uint32_t)step, c3 = (uint32_t)(step >> 32);
+    uint32_t k0 = (uint32_t)seed, k1 = (uint32_t)(seed >> 32);
+#pragma unroll
+    for (int r = 0; r < 10; ++r) {
+        if (r) {
+            k0 += 0x9E3779B9u;
+            k1 += 0xBB67AE85u;
+        }
+        const uint32_t lo0 = 0xD2511F53u * c0, hi0 = __umulhi(0xD2511F53u, c0);
+        const uint32_t lo1 = 0xCD9E8D57u * c2, hi1 = __umulhi(0xCD9E8D57u, c2);
+        const uint32_t n0 = hi1 ^ c1 ^ k0, n2 = hi0 ^ c3 ^ k1;
+        c0 = n0;
+        c1 = lo1;
+        c2 = n2;
+        c3 = lo0;
+    }
+    return ((uint64_t)c0 << 32) | c1;
+}
 
 __device__ __forceinline__ uint64_t key_of(double v) {
     uint64_t u = (uint64_t)__double_as_longlong(v);
@@ -65,10 +91,17 @@ __global__ __launch_bounds__(kThreads) void select_topk(SelectArgs a) {
     __shared__ int wave_tot[kWaves];
     __shared__ double red[kWaves];
 
+    // Keys ordered so that the k largest are taken: l1 norms as they are,
+    // Philox keys complemented (the k smallest keys win; equal keys stay
+    // equal, so ties still go to the lower index).
+    const uint32_t mtx = (uint32_t)(a.matrix0 + b);
+    auto make_key = [&](int i) {
+        return a.rule ? ~philox_line_key((uint32_t)i, mtx, a.step, a.seed) : key_of(nrm[i]);
+    };
     const bool cached = a.d_sel <= kCache;   // uniform
     if (cached)
-        for (int i = threadIdx.x; i < a.d_sel; i += kThreads) cache[i] = key_of(nrm[i]);
-    auto key_at = [&](int i) { return cached ? cache[i] : key_of(nrm[i]); };
+        for (int i = threadIdx.x; i < a.d_sel; i += kThreads) cache[i] = make_key(i);
+    auto key_at = [&](int i) { return cached ? cache[i] : make_key(i); };
     const int lane = threadIdx.x & 63;
 
     uint64_t prefix = 0, mask = 0;

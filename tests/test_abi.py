@@ -54,6 +54,8 @@ def test_options_defaults(lib):
     assert abs(opt.ns_eps - 1e-7) < 1e-12
     assert opt.decay_all == 0 and not opt.workspace and not opt.dbg_update
     assert not opt.ns_coeffs
+    assert opt.ns_form == binding.NS_AUTO and opt.select_rule == binding.SELECT_L1
+    assert opt.rand_seed == 0 and opt.rand_step == 0 and opt.rand_matrix0 == 0
 
 
 FAKE = 0x10000   # a 256-aligned non-null address; never dereferenced below
@@ -111,6 +113,10 @@ def test_ex_options_validation(lib):
     assert ex(decay_all=3) == DION2_ERR_INVALID_ARG
     assert ex(ns_form=3) == DION2_ERR_INVALID_ARG and "ns_form" in binding.dion2_last_error()
     assert ex(ns_form=-1) == DION2_ERR_INVALID_ARG
+    assert ex(select_rule=2) == DION2_ERR_INVALID_ARG and "select_rule" in binding.dion2_last_error()
+    assert ex(select_rule=1, rand_matrix0=-1) == DION2_ERR_INVALID_ARG
+    assert ex(select_rule=1, rand_matrix0=1 << 32) == DION2_ERR_INVALID_ARG   # batch of 1
+    assert "2^32" in binding.dion2_last_error()
     coeffs = (ctypes.c_float * 6)(1.0, 2.0, 3.0, 1.0, float("inf"), 0.0)
     assert ex(ns_coeffs=ctypes.cast(coeffs, ctypes.POINTER(ctypes.c_float))) == DION2_ERR_INVALID_ARG
     need = binding.dion2_workspace_size(1, 64, 64, 0.25)

@@ -32,7 +32,7 @@ FORMS = pytest.mark.parametrize("form", [NS_DIRECT, NS_GRAM], ids=["direct", "gr
 
 
 def run_gpu(W, M, G, alpha, ns_steps=5, axis=AXIS_AUTO, mu=0.95, lr=0.02, coeffs=None,
-            decay_all=False, form=binding.NS_AUTO):
+            decay_all=False, form=binding.NS_AUTO, rand=None):
     """One library call on stacks [B, rows, cols]; returns host copies and the
     debug outputs."""
     B, rows, cols = W.shape
@@ -43,22 +43,29 @@ def run_gpu(W, M, G, alpha, ns_steps=5, axis=AXIS_AUTO, mu=0.95, lr=0.02, coeffs
     nrm = torch.full((B, d_sel), -1.0, dtype=torch.float64, device=dev)
     upd = torch.full((B, k, d_oth), float("nan"), dtype=torch.float32, device=dev)
     W0, M0 = W.cpu(), M.cpu()
+    extra = {}
+    if rand is not None:   # (seed, step, first matrix index): the Random rule
+        extra = dict(select_rule=binding.SELECT_RANDOM, rand_seed=rand[0], rand_step=rand[1],
+                     rand_matrix0=rand[2])
     binding.dion2_step_ex(W, M, G, alpha, mu, lr, ns_steps, axis, ns_coeffs=coeffs,
                           decay_all=decay_all, dbg_sel_idx=sel, dbg_norms=nrm, dbg_update=upd,
-                          ns_form=form)
+                          ns_form=form, **extra)
     torch.cuda.synchronize()
     return dict(W=W.cpu(), M=M.cpu(), K=sel.cpu(), norms=nrm.cpu(), O=upd.cpu(), W0=W0, M0=M0,
                 G=G.cpu(), axis=ax, k=k)
 
 
 def check_matrix(res, b, alpha, ns_steps=5, axis=AXIS_AUTO, mu=0.95, lr=0.02, coeffs=None,
-                 decay_all=False, ns_tol=NS_TOL):
+                 decay_all=False, ns_tol=NS_TOL, rand=None):
     wdt = "bf16" if res["W0"].dtype == torch.bfloat16 else "f32"
     W0 = res["W0"][b].float().numpy().astype(np.float64)
     M0 = res["M0"][b].numpy()
     G = res["G"][b].float().numpy()
+    sel_kw = {}
+    if rand is not None:
+        sel_kw = dict(select="random", seed=rand[0], step=rand[1], matrix=rand[2] + b)
     out = oracle.dion2_step(W0, M0, G, alpha, mu, lr, ns_steps, axis, coeffs, w_dtype=wdt,
-                            decay_all=decay_all)
+                            decay_all=decay_all, **sel_kw)
     assert out["axis"] == res["axis"] and out["k"] == res["k"]
     K = res["K"][b].numpy().astype(np.int64)
     np.testing.assert_array_equal(K, out["K"], err_msg="selected indices")
@@ -271,3 +278,79 @@ def test_colsel_spikes_selected(hip_device):
     spiked = torch.nonzero(gabs > 5 * gabs.median()).flatten().tolist()
     assert len(spiked) == int(0.05 * 8192)
     assert set(spiked) <= set(res["K"][1].tolist())
+
+
+@pytest.mark.parametrize("gi", [0, 1, 2], ids=["4096x4096", "11008x4096", "4096x11008"])
+@pytest.mark.parametrize("alpha", [0.125, 0.25])
+def test_7b_shapes_sampled(hip_device, gi, alpha):
+    """7B-style shapes (the 11008x4096 group selects columns): two matrices of
+    each group in one batched call, both checked in full."""
+    wl = workloads.WORKLOADS["7b"]
+    W, M, G = workloads.make_group(wl, gi, hip_device, first=5, count=2)
+    res = run_gpu(W, M, G, alpha)
+    for b in range(2):
+        check_matrix(res, b, alpha)
+
+
+def test_7b_square_muon(hip_device):
+    """alpha = 1 (every line selected: Muon) on a 4096x4096 matrix."""
+    wl = workloads.WORKLOADS["7b"]
+    W, M, G = workloads.make_group(wl, 0, hip_device, first=9, count=1)
+    res = run_gpu(W, M, G, 1.0)
+    assert res["k"] == 4096
+    check_matrix(res, 0, 1.0)
+
+
+@pytest.mark.parametrize("gi", [0, 1], ids=["2048x1408", "1408x2048"])
+@pytest.mark.parametrize("m0_zero", [True, False], ids=["m0-zero", "m0-drawn"])
+def test_moe_experts_with_zero_gradients(hip_device, gi, m0_zero):
+    """MoE expert shapes with 30% zero-gradient experts. With zero momentum a
+    zero expert is all ties: K = first k lines, O = 0, W unchanged."""
+    wl = workloads.WORKLOADS["moe"]
+    zero = set(workloads.zero_gradient_matrices(wl, gi))
+    # a window of 8 experts holding both kinds
+    first = next(f for f in range(0, 57) if 0 < len(zero & set(range(f, f + 8))) < 8)
+    W, M, G = workloads.make_group(wl, gi, hip_device, m0_zero=m0_zero, first=first, count=8)
+    res = run_gpu(W, M, G, 0.25)
+    for b in range(8):
+        check_matrix(res, b, 0.25)
+        if first + b in zero:
+            assert not torch.any(res["G"][b])
+            if m0_zero:
+                assert res["K"][b].tolist() == list(range(res["k"]))
+                assert torch.equal(res["W"][b], res["W0"][b])
+                assert not torch.any(res["O"][b])
+
+
+@pytest.mark.parametrize("rows,cols,axis", [(384, 640, AXIS_AUTO), (640, 384, AXIS_AUTO),
+                                            (300, 200, AXIS_ROWS)], ids=["rowsel", "colsel", "k>d_oth"])
+@FORMS
+def test_random_selection(hip_device, rows, cols, axis, form):
+    """Random rule: the GPU draws the same Philox keys as the oracle, so K is
+    identical; matrix b of the batch uses counter word rand_matrix0 + b."""
+    wl = one_group_workload(rows, cols, count=3, axis=axis, name=f"rand{rows}")
+    W, M, G = workloads.make_group(wl, 0, hip_device)
+    rand = (0x1234_5678_9ABC_DEF0, 2**33 + 7, 41)
+    res = run_gpu(W, M, G, 0.25, axis=axis, form=form, rand=rand)
+    for b in range(3):
+        check_matrix(res, b, 0.25, axis=axis, rand=rand)
+    assert not torch.equal(res["K"][0], res["K"][1])   # each matrix draws its own subset
+
+
+def test_random_selection_full_1b_group(hip_device):
+    """The Random rule on the whole 2048x2048 group of the 1B-style stack."""
+    wl = workloads.WORKLOADS["1b"]
+    W, M, G = workloads.make_group(wl, 0, hip_device)
+    k, ax = binding.dion2_plan_info(2048, 2048, 0.25, AXIS_AUTO)
+    sel = torch.empty((64, k), dtype=torch.int32, device=hip_device)
+    snap = {b: (W[b].cpu(), M[b].cpu(), G[b].cpu()) for b in (0, 63)}
+    upd = torch.empty((64, k, 2048), dtype=torch.float32, device=hip_device)
+    nrm = torch.empty((64, 2048), dtype=torch.float64, device=hip_device)
+    binding.dion2_step_ex(W, M, G, 0.25, dbg_sel_idx=sel, dbg_norms=nrm, dbg_update=upd,
+                          select_rule=binding.SELECT_RANDOM, rand_seed=5, rand_step=100)
+    torch.cuda.synchronize()
+    for b in (0, 63):
+        res = dict(W0=snap[b][0][None], M0=snap[b][1][None], G=snap[b][2][None],
+                   W=W[b].cpu()[None], M=M[b].cpu()[None], K=sel[b].cpu()[None],
+                   norms=nrm[b].cpu()[None], O=upd[b].cpu()[None], axis=ax, k=k)
+        check_matrix(res, 0, 0.25, rand=(5, 100, b))
