@@ -13,6 +13,7 @@ steps 20). Prints one JSON line:
                HIP events on the library's stream in a second timed pass
   cpu_baseline the CPU oracle timed on a bounded sample of the same stack
   per_alpha_ms the other fractions of the workload, timed the same way
+  per_rule_ms  the l1 (Default) and Random selection rules at --alpha
 """
 from __future__ import annotations
 
@@ -53,27 +54,33 @@ def allocate(wl, dev):
 
 
 NS_FORMS = {"auto": binding.NS_AUTO, "direct": binding.NS_DIRECT, "gram": binding.NS_GRAM}
+SELECT_RULES = {"l1": binding.SELECT_L1, "random": binding.SELECT_RANDOM}
 NS_FORM = binding.NS_AUTO
+STEP = [0]   # optimizer step counter (the Random rule draws anew every step)
 
 
-def one_step(wl, groups, alpha):
+def one_step(wl, groups, alpha, rule=binding.SELECT_L1):
+    STEP[0] += 1
+    first = 0
     for grp, W, M, G in groups:
-        if NS_FORM == binding.NS_AUTO:
+        if NS_FORM == binding.NS_AUTO and rule == binding.SELECT_L1:
             binding.dion2_step_strided(W, M, G, alpha, wl.mu, wl.lr, wl.ns_steps, grp.axis)
         else:
             binding.dion2_step_ex(W, M, G, alpha, wl.mu, wl.lr, wl.ns_steps, grp.axis,
-                                  ns_form=NS_FORM)
+                                  ns_form=NS_FORM, select_rule=rule, rand_seed=1234,
+                                  rand_step=STEP[0], rand_matrix0=first)
+        first += grp.count
 
 
-def time_steps(wl, groups, alpha, warmup, steps):
+def time_steps(wl, groups, alpha, warmup, steps, rule=binding.SELECT_L1):
     for _ in range(warmup):
-        one_step(wl, groups, alpha)
+        one_step(wl, groups, alpha, rule)
     torch.cuda.synchronize()
     ev = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
     t0 = time.perf_counter()
     ev[0].record()
     for i in range(steps):
-        one_step(wl, groups, alpha)
+        one_step(wl, groups, alpha, rule)
         ev[i + 1].record()
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
@@ -165,6 +172,8 @@ def main(argv=None):
     ap.add_argument("--no-profile", action="store_true", help="skip the per-kernel event pass")
     ap.add_argument("--ns-form", default="auto", choices=sorted(NS_FORMS),
                     help="Newton-Schulz evaluation order (default: chosen by shape)")
+    ap.add_argument("--no-random-rule", action="store_true",
+                    help="skip timing the Random selection rule at --alpha")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run plain 1 GiB device copies, the reference dispatches that "
                          "scale HBM byte counters (FETCH_SIZE / WRITE_SIZE) in a profiler run")
@@ -243,6 +252,12 @@ def main(argv=None):
             per_alpha[str(a)] = round(statistics.mean(p2), 4)
             log(f"[bench] alpha={a}: {per_alpha[str(a)]:.3f} ms/step")
 
+    per_rule = {"l1": round(ms, 4)}
+    if not args.no_random_rule:
+        p3, _ = time_steps(wl, groups, alpha, args.warmup, args.steps, binding.SELECT_RANDOM)
+        per_rule["random"] = round(statistics.mean(p3), 4)
+        log(f"[bench] alpha={alpha}, Random rule: {per_rule['random']:.3f} ms/step")
+
     cpu = None
     if not args.no_cpu_baseline:
         log(f"[bench] timing the CPU oracle for ~{args.cpu_seconds:.0f} s")
@@ -270,6 +285,7 @@ def main(argv=None):
         "roofline": roofline,
         "cpu_baseline": cpu,
         "per_alpha_ms": per_alpha,
+        "per_rule_ms": per_rule,
         "ns_mfma_frac": None if ns_frac is None else round(ns_frac, 4),
         "step_ms_stats": {"mean": round(ms, 4), "median": round(statistics.median(per), 4),
                           "min": round(min(per), 4), "mean_last_20": round(statistics.mean(tail), 4),
