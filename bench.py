@@ -4,8 +4,10 @@
     python bench.py [--steps K] [--warmup W] [--workload 1b] [--alpha 0.25]
 
 A step is one Dion2 update (Algorithm 1) of every matrix of a synthetic layer
-stack, one batched library call per same-shape group, all on one stream,
-with W, M, G resident in HBM. The default is the paper's timing method
+stack, one batched library call per same-shape group, with W, M, G resident
+in HBM. The groups are independent, so by default each runs on its own
+stream (forked from and joined into the timing stream); --streams 0 runs
+them back to back on one stream. The default is the paper's timing method
 (Sec. 4.4): 100 steps, the mean of the final 20 reported (warmup 80,
 steps 20). Prints one JSON line:
   value        mean ms per step at --alpha (lower is better)
@@ -56,20 +58,36 @@ def allocate(wl, dev):
 NS_FORMS = {"auto": binding.NS_AUTO, "direct": binding.NS_DIRECT, "gram": binding.NS_GRAM}
 SELECT_RULES = {"l1": binding.SELECT_L1, "random": binding.SELECT_RANDOM}
 NS_FORM = binding.NS_AUTO
-STEP = [0]   # optimizer step counter (the Random rule draws anew every step)
+STEP = [0]      # optimizer step counter (the Random rule draws anew every step)
+STREAMS = []    # one stream per shape group when the groups run concurrently
 
 
 def one_step(wl, groups, alpha, rule=binding.SELECT_L1):
+    """One optimizer step over the whole stack: one library call per shape
+    group. The groups are independent, so with STREAMS set each runs on its
+    own stream (forked from and joined back into the current stream)."""
     STEP[0] += 1
     first = 0
-    for grp, W, M, G in groups:
-        if NS_FORM == binding.NS_AUTO and rule == binding.SELECT_L1:
-            binding.dion2_step_strided(W, M, G, alpha, wl.mu, wl.lr, wl.ns_steps, grp.axis)
-        else:
-            binding.dion2_step_ex(W, M, G, alpha, wl.mu, wl.lr, wl.ns_steps, grp.axis,
-                                  ns_form=NS_FORM, select_rule=rule, rand_seed=1234,
-                                  rand_step=STEP[0], rand_matrix0=first)
+    main = torch.cuda.current_stream()
+    if STREAMS:
+        fork = torch.cuda.Event()
+        fork.record(main)
+    for gi, (grp, W, M, G) in enumerate(groups):
+        s = STREAMS[gi % len(STREAMS)] if STREAMS else main
+        if STREAMS:
+            s.wait_event(fork)
+        with torch.cuda.stream(s):
+            if NS_FORM == binding.NS_AUTO and rule == binding.SELECT_L1:
+                binding.dion2_step_strided(W, M, G, alpha, wl.mu, wl.lr, wl.ns_steps, grp.axis)
+            else:
+                binding.dion2_step_ex(W, M, G, alpha, wl.mu, wl.lr, wl.ns_steps, grp.axis,
+                                      ns_form=NS_FORM, select_rule=rule, rand_seed=1234,
+                                      rand_step=STEP[0], rand_matrix0=first)
         first += grp.count
+    for s in STREAMS:
+        join = torch.cuda.Event()
+        join.record(s)
+        main.wait_event(join)
 
 
 def time_steps(wl, groups, alpha, warmup, steps, rule=binding.SELECT_L1):
@@ -172,6 +190,9 @@ def main(argv=None):
     ap.add_argument("--no-profile", action="store_true", help="skip the per-kernel event pass")
     ap.add_argument("--ns-form", default="auto", choices=sorted(NS_FORMS),
                     help="Newton-Schulz evaluation order (default: chosen by shape)")
+    ap.add_argument("--streams", type=int, default=-1,
+                    help="run the shape groups on this many streams (0: all on the current "
+                         "stream; default: one stream per group, the groups being independent)")
     ap.add_argument("--no-random-rule", action="store_true",
                     help="skip timing the Random selection rule at --alpha")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -207,6 +228,9 @@ def main(argv=None):
 
     wl = workloads.WORKLOADS[args.workload]
     alpha = args.alpha if args.alpha is not None else wl.alphas[0]
+    if args.streams < 0:
+        args.streams = len(wl.groups)
+    STREAMS.extend(torch.cuda.Stream() for _ in range(args.streams))   # default priority
     dev = torch.device("cuda:0")
     log(f"[bench] allocating workload {wl.name}: {wl.matrices()} matrices, "
         f"{wl.elements() / 1e6:.1f}M elements")
@@ -281,7 +305,8 @@ def main(argv=None):
         "config": {"workload": wl.name, "description": wl.description, "alpha": alpha,
                    "matrices": wl.matrices(), "elements": wl.elements(),
                    "ns_steps": wl.ns_steps, "mu": wl.mu, "lr": wl.lr, "ns_form": args.ns_form,
-                   "parallelism": "single GPU, batched per shape group"},
+                   "parallelism": "single GPU, batched per shape group",
+                   "streams": args.streams},
         "roofline": roofline,
         "cpu_baseline": cpu,
         "per_alpha_ms": per_alpha,
