@@ -108,7 +108,10 @@ def time_steps(wl, groups, alpha, warmup, steps, rule=binding.SELECT_L1):
 
 def profile_phases(wl, groups, alpha, steps):
     """Per-phase kernel time from events the library records around each
-    launch on its stream, with the phase's algorithmic work."""
+    launch on its stream, with the phase's algorithmic work. The groups run
+    back to back here, so each phase is timed without other work beside it."""
+    saved = STREAMS[:]
+    STREAMS.clear()
     binding.dion2_profile_reset()
     binding.dion2_profile_enable(True)
     try:
@@ -118,6 +121,7 @@ def profile_phases(wl, groups, alpha, steps):
         prof = binding.dion2_profile_read()
     finally:
         binding.dion2_profile_enable(False)
+        STREAMS.extend(saved)
     out = {}
     for ph, d in prof.items():
         if d["launches"] == 0:
