@@ -38,7 +38,7 @@ from paper_2512_16928_amd import binding, profsum, workloads  # noqa: E402
 METRIC = "Dion2 optimizer-step ms per layer stack at α=0.25/0.5/1; NS MFMA util %"
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E
 MFMA_BF16_PEAK_TFS = 2500.0    # MI355X dense bf16 MFMA
-HBM_PHASES = ("momentum", "gather", "apply")
+RIDGE_FLOP_PER_BYTE = MFMA_BF16_PEAK_TFS * 1e12 / (HBM_PEAK_GBS * 1e9)
 NS_PHASES = ("ns_gram", "ns_poly", "ns_update")
 
 
@@ -127,17 +127,21 @@ def profile_phases(wl, groups, alpha, steps):
         if d["launches"] == 0:
             continue
         avg_ms = d["ms"] / d["launches"]       # per kernel launch
-        work = d["work"] / d["launches"]
-        rate = work / (avg_ms * 1e-3) if avg_ms > 0 else 0.0
-        if ph in HBM_PHASES:
-            ach, peak, unit, bound = rate / 1e9, HBM_PEAK_GBS, "GB/s", "hbm"
-        elif ph in NS_PHASES:
-            ach, peak, unit, bound = rate / 1e12, MFMA_BF16_PEAK_TFS, "TFLOP/s", "mfma"
+        flops, nbytes = d["flops"] / d["launches"], d["bytes"] / d["launches"]
+        sec = avg_ms * 1e-3
+        # the bound is the roofline's: MFMA where the phase's arithmetic
+        # intensity reaches the ridge point, HBM below it
+        if ph == "select":
+            bound, ach, peak, unit = "latency", nbytes / sec / 1e9, HBM_PEAK_GBS, "GB/s"
+        elif flops > 0 and flops / nbytes >= RIDGE_FLOP_PER_BYTE:
+            bound, ach, peak, unit = "mfma", flops / sec / 1e12, MFMA_BF16_PEAK_TFS, "TFLOP/s"
         else:
-            ach, peak, unit, bound = rate / 1e9, HBM_PEAK_GBS, "GB/s", "latency"
+            bound, ach, peak, unit = "hbm", nbytes / sec / 1e9, HBM_PEAK_GBS, "GB/s"
         out[ph] = dict(total_ms_per_step=d["ms"] / steps, avg_launch_ms=avg_ms,
-                       launches_per_step=d["launches"] / steps, work_per_launch=work,
-                       achieved=ach, peak=peak, unit=unit, bound=bound, frac=ach / peak)
+                       launches_per_step=d["launches"] / steps, flops_per_launch=flops,
+                       bytes_per_launch=nbytes, achieved=ach, peak=peak, unit=unit, bound=bound,
+                       frac=ach / peak,
+                       mfma_tflops=flops / sec / 1e12, hbm_gbs=nbytes / sec / 1e9)
     return out
 
 
@@ -260,16 +264,20 @@ def main(argv=None):
                         traffic=None if traffic is None else round(traffic),
                         traffic_unit="bytes per launch", kernel=dom,
                         avg_launch_ms=round(d["avg_launch_ms"], 5),
-                        algorithmic_per_launch=round(d["work_per_launch"]),
-                        algorithmic_unit="bytes" if d["unit"] == "GB/s" else "flops")
+                        algorithmic_per_launch=round(d["bytes_per_launch"] if d["unit"] == "GB/s"
+                                                     else d["flops_per_launch"]),
+                        algorithmic_unit="bytes" if d["unit"] == "GB/s" else "flops",
+                        flops_per_launch=round(d["flops_per_launch"]),
+                        bytes_per_launch=round(d["bytes_per_launch"]))
         ns_ms = sum(phases[p]["total_ms_per_step"] for p in NS_PHASES if p in phases)
-        ns_work = sum(phases[p]["work_per_launch"] * phases[p]["launches_per_step"]
+        ns_work = sum(phases[p]["flops_per_launch"] * phases[p]["launches_per_step"]
                       for p in NS_PHASES if p in phases)
         if ns_ms > 0:
             ns_frac = ns_work / (ns_ms * 1e-3) / 1e12 / MFMA_BF16_PEAK_TFS
         for p, d in phases.items():
-            log(f"[bench]   {p:10s} {d['total_ms_per_step']:8.3f} ms/step  "
-                f"{d['achieved']:9.1f} {d['unit']} ({100 * d['frac']:.1f}% of peak)")
+            log(f"[bench]   {p:10s} {d['total_ms_per_step']:8.3f} ms/step  {d['bound']:7s} "
+                f"{d['achieved']:9.1f} {d['unit']} ({100 * d['frac']:.1f}% of peak)"
+                f"   [{d['hbm_gbs']:7.0f} GB/s, {d['mfma_tflops']:6.1f} TFLOP/s]")
 
     per_alpha = {str(alpha): round(ms, 4)}
     if not args.no_extra_alphas:

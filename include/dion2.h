@@ -180,17 +180,26 @@ int dion2_plan_info(int64_t rows, int64_t cols, float alpha, int axis,
 
 /* ---- Measurement hooks ---------------------------------------------------
  * While enabled, every kernel phase of subsequent calls is bracketed by HIP
- * events recorded on the call's stream, and the phase's algorithmic work is
- * added to a per-phase total: bytes for the streaming phases (what the step
- * itself must move: M and G read and M written by MOMENTUM; the selected
- * lines of M read and written by GATHER; the selected lines of W read and
- * written by APPLY), and MFMA flops for the Newton-Schulz GEMMs, counting
- * every bf16 hi/lo pass and counting a product with a symmetric result at
- * s (s + 1) per inner index (the half it computes) instead of 2 s^2: the
- * Gram matrix s (s + 1) l, a three-pass s x s product 3 s (s + 1) s, the
- * update B X 2 s^2 l and the two-pass final product of the GRAM form
- * 4 s^2 l (s <= l are the compact matrix's unpadded sides). The events cost
- * a little time, so the step time is measured with the hooks off. */
+ * events recorded on the call's stream (the Newton-Schulz s x s products of
+ * the GRAM form, which run back to back, as one span), and the phase's
+ * algorithmic work is added to per-phase totals, as flops and as bytes:
+ *   bytes: what the phase must move as designed. MOMENTUM: M and G read, M
+ *     written (rows) or M and G read (columns). GATHER: the selected lines of
+ *     M read and written and the compact bf16 copy written (rows), or M and
+ *     G read and M written whole plus the compact copy (columns). APPLY: O
+ *     read and the selected lines of W read and written (rows), or W read
+ *     and written whole (columns). Newton-Schulz: each product's distinct
+ *     operands read and its result written (the Gram matrix: X in, A hi/lo
+ *     out; an s x s product: two hi/lo operands in, one out; the final
+ *     product: X in, O (or W's selected lines, read and written) out).
+ *   flops: MFMA flops of the Newton-Schulz GEMMs, every bf16 hi/lo pass
+ *     included, a product with a symmetric result counted at s (s + 1) per
+ *     inner index (the half it computes) instead of 2 s^2: the Gram matrix
+ *     s (s + 1) l, a three-pass s x s product 3 s (s + 1) s, the update B X
+ *     2 s^2 l and the two-pass final product of the GRAM form 4 s^2 l (s <= l
+ *     are the compact matrix's unpadded sides); 0 for the other phases.
+ * The events cost a little time, so the step time is measured with the
+ * hooks off. */
 typedef enum dion2_phase {
     DION2_PHASE_MOMENTUM = 0,  /* K1: M += G and line norms         */
     DION2_PHASE_SELECT = 1,    /* K2: top-k selection               */
@@ -206,10 +215,11 @@ typedef enum dion2_phase {
 int dion2_profile_enable(int on);
 
 /* Waits for the recorded events and writes, for the first n phases, the
-   summed kernel milliseconds, the number of calls timed, the kernel launches
-   and the summed algorithmic work (bytes or flops, as above). Any output
-   pointer may be NULL. Totals accumulate until dion2_profile_reset. */
-int dion2_profile_read(double* ms, int64_t* calls, int64_t* launches, double* work, int n);
+   summed kernel milliseconds, the number of spans timed, the kernel launches
+   and the summed algorithmic flops and bytes (as above). Any output pointer
+   may be NULL. Totals accumulate until dion2_profile_reset. */
+int dion2_profile_read(double* ms, int64_t* calls, int64_t* launches, double* flops,
+                       double* bytes, int n);
 
 void dion2_profile_reset(void);
 

@@ -111,7 +111,7 @@ def load(path: str = LIB_PATH):
     lib.dion2_profile_enable.argtypes = [c_int]
     lib.dion2_profile_enable.restype = c_int
     lib.dion2_profile_read.argtypes = [POINTER(c_double), POINTER(c_int64), POINTER(c_int64),
-                                       POINTER(c_double), c_int]
+                                       POINTER(c_double), POINTER(c_double), c_int]
     lib.dion2_profile_read.restype = c_int
     lib.dion2_profile_reset.argtypes = []
     lib.dion2_profile_reset.restype = None
@@ -283,13 +283,14 @@ def dion2_profile_enable(on: bool) -> bool:
 
 
 def dion2_profile_read():
-    """{phase: dict(ms, calls, launches, work)} accumulated since the last reset."""
+    """{phase: dict(ms, calls, launches, flops, bytes)} accumulated since the
+    last reset."""
     n = len(PHASES)
-    ms, work = (c_double * n)(), (c_double * n)()
+    ms, flops, nbytes = (c_double * n)(), (c_double * n)(), (c_double * n)()
     calls, launches = (c_int64 * n)(), (c_int64 * n)()
-    _check(load().dion2_profile_read(ms, calls, launches, work, n))
-    return {p: dict(ms=ms[i], calls=calls[i], launches=launches[i], work=work[i])
-            for i, p in enumerate(PHASES)}
+    _check(load().dion2_profile_read(ms, calls, launches, flops, nbytes, n))
+    return {p: dict(ms=ms[i], calls=calls[i], launches=launches[i], flops=flops[i],
+                    bytes=nbytes[i]) for i, p in enumerate(PHASES)}
 
 
 def dion2_profile_reset():

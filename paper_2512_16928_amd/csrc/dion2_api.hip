@@ -173,7 +173,7 @@ int ensure_device(Workspace* w, size_t bytes) {
 struct ProfRecord {
     int phase;
     hipEvent_t start, stop;
-    double work;
+    double flops, bytes;
     int launches;
 };
 
@@ -185,7 +185,8 @@ struct Profiler {
     double ms[DION2_PHASE_COUNT] = {};
     int64_t calls[DION2_PHASE_COUNT] = {};
     int64_t launches[DION2_PHASE_COUNT] = {};
-    double work[DION2_PHASE_COUNT] = {};
+    double flops[DION2_PHASE_COUNT] = {};
+    double bytes[DION2_PHASE_COUNT] = {};
 
     hipEvent_t get() {
         if (!pool.empty()) {
@@ -204,11 +205,12 @@ Profiler g_prof;
 // Brackets one kernel phase with events when the hooks are on.
 class PhaseTimer {
   public:
-    PhaseTimer(int phase, double work, int launches, hipStream_t s) : s_(s) {
+    PhaseTimer(int phase, double flops, double bytes, int launches, hipStream_t s) : s_(s) {
         std::lock_guard<std::mutex> lk(g_prof.mu);
         if (!g_prof.on) return;
         rec_.phase = phase;
-        rec_.work = work;
+        rec_.flops = flops;
+        rec_.bytes = bytes;
         rec_.launches = launches;
         rec_.start = g_prof.get();
         rec_.stop = g_prof.get();
@@ -233,8 +235,8 @@ class PhaseTimer {
 };
 
 template <typename F>
-hipError_t timed(int phase, double work, int launches, hipStream_t s, F&& fn) {
-    PhaseTimer t(phase, work, launches, s);
+hipError_t timed(int phase, double flops, double bytes, int launches, hipStream_t s, F&& fn) {
+    PhaseTimer t(phase, flops, bytes, launches, s);
     hipError_t e = fn();
     t.finish(e == hipSuccess);
     return e;
@@ -337,13 +339,14 @@ hipError_t ns_direct(const Plan& P, uint16_t* Z0, uint16_t* Z1, uint16_t* const*
     const double s_r = (double)(P.k < P.d_oth ? P.k : P.d_oth);   // unpadded sides
     const double l_r = (double)(P.k < P.d_oth ? P.d_oth : P.k);
     const double nb = (double)P.batch;
+    const double gram_bytes = (2.0 * s_r * l_r + 4.0 * s_r * s_r) * nb;   // Z in, A hi + lo out
     uint16_t* zbuf[2] = {Z0, Z1};
     int cur = 0;
     for (int t = 0; t < ns_steps; ++t) {
         const float* cf = opt.ns_coeffs ? opt.ns_coeffs + 3 * t : kMuonQuintic;
         uint16_t* Z = zbuf[cur];
         GemmArgs g = gram_args(P, Z, sq[SQ_AHI], sq[SQ_ALO]);
-        hipError_t e = timed(DION2_PHASE_NS_GRAM, sym_flops(s_r, l_r) * nb, 1, stream,
+        hipError_t e = timed(DION2_PHASE_NS_GRAM, sym_flops(s_r, l_r) * nb, gram_bytes, 1, stream,
                              [&] { return launch_gemm(g, EPI_SPLIT, 1, stream); });
         if (e != hipSuccess) return e;
 
@@ -354,7 +357,7 @@ hipError_t ns_direct(const Plan& P, uint16_t* Z0, uint16_t* Z1, uint16_t* const*
         q.E1 = sq[SQ_ALO];
         q.sE = P.s_pad * P.s_pad;
         q.lde = (int)P.s_pad;
-        e = timed(DION2_PHASE_NS_POLY, 3.0 * sym_flops(s_r, s_r) * nb, 1, stream,
+        e = timed(DION2_PHASE_NS_POLY, 3.0 * sym_flops(s_r, s_r) * nb, 6.0 * s_r * s_r * nb, 1, stream,
                   [&] { return launch_gemm(q, EPI_POLY, 3, stream); });
         if (e != hipSuccess) return e;
 
@@ -373,7 +376,8 @@ hipError_t ns_direct(const Plan& P, uint16_t* Z0, uint16_t* Z1, uint16_t* const*
         } else {
             epi = final_output(P, x, O, fin);
         }
-        e = timed(DION2_PHASE_NS_UPDATE, 2.0 * s_r * s_r * l_r * nb, 1, stream,
+        const double ubytes = (2.0 * s_r * s_r + (last ? 6.0 : 4.0) * s_r * l_r) * nb;
+        e = timed(DION2_PHASE_NS_UPDATE, 2.0 * s_r * s_r * l_r * nb, ubytes, 1, stream,
                   [&] { return launch_gemm(x, epi, 1, stream); });
         if (e != hipSuccess) return e;
         cur = 1 - cur;
@@ -390,6 +394,7 @@ hipError_t ns_gram(const Plan& P, const uint16_t* Z, uint16_t* const* sq, float*
     const double l_r = (double)(P.k < P.d_oth ? P.d_oth : P.k);
     const double nb = (double)P.batch;
     const double f3 = 3.0 * sym_flops(s_r, s_r) * nb;
+    const double gram_bytes = (2.0 * s_r * l_r + 4.0 * s_r * s_r) * nb;
     uint16_t* Ah = sq[SQ_AHI];
     uint16_t* Al = sq[SQ_ALO];
     uint16_t* Ph[2] = {sq[SQ_P0HI], sq[SQ_P1HI]};
@@ -397,12 +402,15 @@ hipError_t ns_gram(const Plan& P, const uint16_t* Z, uint16_t* const* sq, float*
     int cur = 0;
 
     GemmArgs g = gram_args(P, Z, Ah, Al);
-    hipError_t e = timed(DION2_PHASE_NS_GRAM, sym_flops(s_r, l_r) * nb, 1, stream,
+    hipError_t e = timed(DION2_PHASE_NS_GRAM, sym_flops(s_r, l_r) * nb, gram_bytes, 1, stream,
                          [&] { return launch_gemm(g, EPI_SPLIT, 1, stream); });
     if (e != hipSuccess) return e;
     // the s x s products run back to back and are timed as one span
+    // bytes: Q_t from A (hi + lo in and out, 8 s^2), the other products two
+    // hi/lo operands in and one out (12 s^2)
     const int nprod = ns_steps + 3 * (ns_steps - 1);
-    e = timed(DION2_PHASE_NS_POLY, f3 * nprod, nprod, stream, [&]() -> hipError_t {
+    const double sq_bytes = (8.0 * ns_steps + 12.0 * (nprod - ns_steps)) * s_r * s_r * nb;
+    e = timed(DION2_PHASE_NS_POLY, f3 * nprod, sq_bytes, nprod, stream, [&]() -> hipError_t {
         for (int t = 0; t < ns_steps; ++t) {
             const float* cf = opt.ns_coeffs ? opt.ns_coeffs + 3 * t : kMuonQuintic;
             // Q_t; the first one is P itself
@@ -439,7 +447,9 @@ hipError_t ns_gram(const Plan& P, const uint16_t* Z, uint16_t* const* sq, float*
     // O = (P_hi + P_lo) Z
     GemmArgs x = right_args(P, Ph[cur], Pl[cur], Z);
     const GemmEpi epi = final_output(P, x, O, fin);
-    return timed(DION2_PHASE_NS_UPDATE, 4.0 * s_r * s_r * l_r * nb, 1, stream,
+    // P hi + lo and Z in, O (or W's selected lines, read and written) out
+    const double fbytes = (4.0 * s_r * s_r + 6.0 * s_r * l_r) * nb;
+    return timed(DION2_PHASE_NS_UPDATE, 4.0 * s_r * s_r * l_r * nb, fbytes, 1, stream,
                  [&] { return launch_gemm(x, epi, 2, stream); });
 }
 
@@ -566,7 +576,7 @@ int run_step(const Plan& P, void* W, float* M, const void* G, const Tables* tabs
     const double k1_bytes = n_el * ((cm ? 4.0 : 8.0) + g_bytes);
     const double k3_bytes = (cm ? n_el * (8.0 + g_bytes) : sel_el * 8.0) + sel_el * 2.0;
     const double k5_bytes = (cm ? n_el : sel_el) * 2.0 * w_bytes + sel_el * 4.0;
-    e = timed(DION2_PHASE_MOMENTUM, k1_bytes, P.axis == 0 ? 1 : 2, stream,
+    e = timed(DION2_PHASE_MOMENTUM, 0.0, k1_bytes, P.axis == 0 ? 1 : 2, stream,
               [&] { return launch_momentum(ma, P.axis, opt.g_dtype == DION2_DTYPE_BF16, stream); });
     if (e != hipSuccess) return hip_fail(e, "launch K1 momentum");
 
@@ -585,7 +595,7 @@ int run_step(const Plan& P, void* W, float* M, const void* G, const Tables* tabs
     sa.seed = opt.rand_seed;
     sa.step = opt.rand_step;
     sa.matrix0 = opt.rand_matrix0;
-    e = timed(DION2_PHASE_SELECT, (double)P.batch * (double)P.d_sel * 16.0, 1, stream,
+    e = timed(DION2_PHASE_SELECT, 0.0, (double)P.batch * (double)P.d_sel * 16.0, 1, stream,
               [&] { return launch_select(sa, stream); });
     if (e != hipSuccess) return hip_fail(e, "launch K2 select");
 
@@ -608,7 +618,7 @@ int run_step(const Plan& P, void* W, float* M, const void* G, const Tables* tabs
     ga.L = P.z_is_L ? Z0 : nullptr;
     ga.LT = P.z_is_L ? nullptr : Z0;
     ga.O = ns_steps == 0 ? O : nullptr;
-    e = timed(DION2_PHASE_GATHER, k3_bytes, 1, stream,
+    e = timed(DION2_PHASE_GATHER, 0.0, k3_bytes, 1, stream,
               [&] { return launch_gather(ga, P.axis, opt.g_dtype == DION2_DTYPE_BF16, stream); });
     if (e != hipSuccess) return hip_fail(e, "launch K3 gather");
     if (opt.decay_all && !cm) {
@@ -647,7 +657,7 @@ int run_step(const Plan& P, void* W, float* M, const void* G, const Tables* tabs
     aa.lr_eff = fin.lr_eff;
     aa.dbg = opt.dbg_update;
     if (!fin.fuse) {   // otherwise the final Newton-Schulz product has applied it
-        e = timed(DION2_PHASE_APPLY, k5_bytes, 1, stream,
+        e = timed(DION2_PHASE_APPLY, 0.0, k5_bytes, 1, stream,
                   [&] { return launch_apply(aa, P.axis, opt.w_dtype == DION2_DTYPE_BF16, stream); });
         if (e != hipSuccess) return hip_fail(e, "launch K5 apply");
     }
@@ -817,7 +827,8 @@ int dion2_profile_enable(int on) {
     return prev;
 }
 
-int dion2_profile_read(double* ms, int64_t* calls, int64_t* launches, double* work, int n) {
+int dion2_profile_read(double* ms, int64_t* calls, int64_t* launches, double* flops,
+                       double* bytes, int n) {
     std::lock_guard<std::mutex> lk(g_prof.mu);
     for (const ProfRecord& r : g_prof.pending) {
         hipError_t e = hipEventSynchronize(r.stop);
@@ -830,7 +841,8 @@ int dion2_profile_read(double* ms, int64_t* calls, int64_t* launches, double* wo
         g_prof.ms[r.phase] += t;
         g_prof.calls[r.phase] += 1;
         g_prof.launches[r.phase] += r.launches;
-        g_prof.work[r.phase] += r.work;
+        g_prof.flops[r.phase] += r.flops;
+        g_prof.bytes[r.phase] += r.bytes;
         g_prof.pool.push_back(r.start);
         g_prof.pool.push_back(r.stop);
     }
@@ -841,7 +853,8 @@ int dion2_profile_read(double* ms, int64_t* calls, int64_t* launches, double* wo
         if (ms) ms[i] = g_prof.ms[i];
         if (calls) calls[i] = g_prof.calls[i];
         if (launches) launches[i] = g_prof.launches[i];
-        if (work) work[i] = g_prof.work[i];
+        if (flops) flops[i] = g_prof.flops[i];
+        if (bytes) bytes[i] = g_prof.bytes[i];
     }
     return DION2_OK;
 }
@@ -858,7 +871,8 @@ void dion2_profile_reset(void) {
         g_prof.ms[i] = 0.0;
         g_prof.calls[i] = 0;
         g_prof.launches[i] = 0;
-        g_prof.work[i] = 0.0;
+        g_prof.flops[i] = 0.0;
+        g_prof.bytes[i] = 0.0;
     }
 }
 
