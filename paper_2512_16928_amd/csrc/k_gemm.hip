@@ -518,14 +518,17 @@ hipError_t launch_tile(const GemmArgs& a, hipStream_t s) {
 }  // namespace
 
 hipError_t launch_gemm(const GemmArgs& a, GemmEpi epi, int npass, hipStream_t s) {
-    // Tile choices measured on MI355X at the Newton-Schulz shapes: 128 x 128
-    // tiles keep enough blocks in flight for s = 512; from s = 1024 the
-    // symmetric Gram product runs faster on 256 x 256 tiles of 8 waves.
+    // Tile choices measured on MI355X at the Newton-Schulz shapes. At s = 512
+    // the kernels are bound by load latency, so blocks resident per CU count
+    // for more than ring depth: 128 x 128 tiles keep enough blocks in flight;
+    // from s = 1024 the Gram matrix runs faster on
+    // 256 x 256 tiles of 8 waves; the X-side products use a two-stage ring,
+    // which leaves room for three blocks per CU.
     using TG = Tile<1, 0, 128, 128, 32, 2, 2, 4>;    // Gram
     using TGL = Tile<1, 0, 256, 256, 32, 4, 2, 3>;   // Gram, large s
     using TP = Tile<3, 0, 128, 128, 32, 4, 2, 2>;    // three-pass symmetric products
-    using TU = Tile<1, 1, 128, 128, 32, 2, 2, 3>;    // update (B operand [K][N])
-    using TU2 = Tile<2, 1, 128, 128, 32, 2, 2, 3>;   // two-pass final product
+    using TU = Tile<1, 1, 128, 128, 32, 2, 2, 2>;    // update (B operand [K][N])
+    using TU2 = Tile<2, 1, 128, 128, 32, 2, 2, 2>;   // two-pass final product
     switch (epi) {
         case EPI_SPLIT:
             if (npass == 3) return launch_tile<3, EPI_SPLIT, TP, true>(a, s);
