@@ -405,12 +405,17 @@ hipError_t ns_gram(const Plan& P, const uint16_t* Z, uint16_t* const* sq, float*
     hipError_t e = timed(DION2_PHASE_NS_GRAM, sym_flops(s_r, l_r) * nb, gram_bytes, 1, stream,
                          [&] { return launch_gemm(g, EPI_SPLIT, 1, stream); });
     if (e != hipSuccess) return e;
-    // the s x s products run back to back and are timed as one span
-    // bytes: Q_t from A (hi + lo in and out, 8 s^2), the other products two
-    // hi/lo operands in and one out (12 s^2)
+    // The s x s products run back to back and are timed as one span. Per
+    // step: Q_t (from A: hi + lo in and out, 8 s^2 bytes), P <- Q_t P and
+    // T = Q_t A (one dual launch when both are due; each product two hi/lo
+    // operands in and one out, 12 s^2, less the shared Q_t's 4 s^2 when
+    // fused), A <- Q_t T (12 s^2).
     const int nprod = ns_steps + 3 * (ns_steps - 1);
-    const double sq_bytes = (8.0 * ns_steps + 12.0 * (nprod - ns_steps)) * s_r * s_r * nb;
-    e = timed(DION2_PHASE_NS_POLY, f3 * nprod, sq_bytes, nprod, stream, [&]() -> hipError_t {
+    const int ndual = ns_steps >= 3 ? ns_steps - 2 : 0;
+    const int nlaunch = ns_steps == 1 ? 1 : 3 * ns_steps - 1;
+    const double sq_bytes =
+        (8.0 * ns_steps + 12.0 * (nprod - ns_steps) - 4.0 * ndual) * s_r * s_r * nb;
+    e = timed(DION2_PHASE_NS_POLY, f3 * nprod, sq_bytes, nlaunch, stream, [&]() -> hipError_t {
         for (int t = 0; t < ns_steps; ++t) {
             const float* cf = opt.ns_coeffs ? opt.ns_coeffs + 3 * t : kMuonQuintic;
             // Q_t; the first one is P itself
@@ -426,16 +431,24 @@ hipError_t ns_gram(const Plan& P, const uint16_t* Z, uint16_t* const* sq, float*
             q.lde = (int)P.s_pad;
             hipError_t r = launch_gemm(q, EPI_QPOLY, 3, stream);
             if (r != hipSuccess) return r;
-            if (t > 0) {   // P <- Q_t P
-                GemmArgs p = sym3_args(P, qh, ql, Ph[cur], Pl[cur], Ph[1 - cur], Pl[1 - cur]);
-                r = launch_gemm(p, EPI_SPLIT, 3, stream);
-                if (r != hipSuccess) return r;
-                cur = 1 - cur;
-            }
-            if (t + 1 < ns_steps) {   // A <- Q_t (Q_t A)
-                GemmArgs u = sym3_args(P, qh, ql, Ah, Al, sq[SQ_THI], sq[SQ_TLO]);
+            // P <- Q_t P (t > 0) and T = Q_t A (t < T - 1) share Q_t: one
+            // launch when both are due
+            const bool do_p = t > 0, do_t = t + 1 < ns_steps;
+            if (do_p || do_t) {
+                GemmArgs u = do_p ? sym3_args(P, qh, ql, Ph[cur], Pl[cur], Ph[1 - cur], Pl[1 - cur])
+                                  : sym3_args(P, qh, ql, Ah, Al, sq[SQ_THI], sq[SQ_TLO]);
+                if (do_p && do_t) {
+                    u.dual = 1;
+                    u.B0x = Ah;
+                    u.B1x = Al;
+                    u.out0x = sq[SQ_THI];
+                    u.out1x = sq[SQ_TLO];
+                }
                 r = launch_gemm(u, EPI_SPLIT, 3, stream);
                 if (r != hipSuccess) return r;
+                if (do_p) cur = 1 - cur;
+            }
+            if (do_t) {   // A <- Q_t T
                 GemmArgs v = sym3_args(P, qh, ql, sq[SQ_THI], sq[SQ_TLO], Ah, Al);
                 r = launch_gemm(v, EPI_SPLIT, 3, stream);
                 if (r != hipSuccess) return r;

@@ -222,6 +222,11 @@ struct GemmArgs {
     void* out0; int64_t sOut0; int ldo0;
     void* out1; int64_t sOut1; int ldo1;
     int out_transposed;                        // EPI_FINAL: write out0[j][i]
+    // dual launch (EPI_SPLIT, npass 3): a second product with the same A
+    // operand, B = B0x/B1x into out0x/out1x, computed in the same grid
+    int dual;
+    const uint16_t* B0x; const uint16_t* B1x;
+    void* out0x; void* out1x;
     // EPI_APPLY only
     MatSet ms;                                 // W
     const int32_t* sel;                        // [batch][k]

@@ -278,7 +278,18 @@ __global__ __launch_bounds__(T::THREADS) void gemm(GemmArgs a) {
     const int total = nx * ny * gridDim.z;
     const int hw = blockIdx.x + nx * (blockIdx.y + ny * blockIdx.z);
     const int logical = (total % kXcds == 0) ? (hw % kXcds) * (total / kXcds) + hw / kXcds : hw;
-    const int b = logical / (nx * ny);
+    int b = logical / (nx * ny);
+    if (a.dual) {
+        // matrix b's two products are neighbours in the tile order, so the
+        // shared A operand is fetched into one L2 for both
+        if (b & 1) {
+            a.B0 = a.B0x;
+            a.B1 = a.B1x;
+            a.out0 = a.out0x;
+            a.out1 = a.out1x;
+        }
+        b >>= 1;
+    }
     int row0 = ((logical / nx) % ny) * T::BM;   // output rows (M)
     int col0 = (logical % nx) * T::BN;          // output cols (N)
     if constexpr (SYM) {
@@ -505,11 +516,12 @@ __global__ __launch_bounds__(T::THREADS) void gemm(GemmArgs a) {
 template <int NPASS, int EPI, typename T, bool SYM = false>
 hipError_t launch_tile(const GemmArgs& a, hipStream_t s) {
     if (a.M % T::BM || a.N % T::BN || a.K % T::BK) return hipErrorInvalidValue;
-    dim3 grid((unsigned)(a.N / T::BN), (unsigned)(a.M / T::BM), (unsigned)a.batch);
+    const unsigned zb = (unsigned)a.batch * (a.dual ? 2u : 1u);
+    dim3 grid((unsigned)(a.N / T::BN), (unsigned)(a.M / T::BM), zb);
     if (SYM) {
         if (a.M != a.N || T::BM != T::BN) return hipErrorInvalidValue;
         const unsigned tiles = (unsigned)(a.M / T::BM);
-        grid = dim3(tiles * (tiles + 1) / 2, 1, (unsigned)a.batch);
+        grid = dim3(tiles * (tiles + 1) / 2, 1, zb);
     }
     hipLaunchKernelGGL((gemm<NPASS, EPI, T, SYM>), grid, dim3(T::THREADS), 0, s, a);
     return hipGetLastError();
@@ -529,6 +541,7 @@ hipError_t launch_gemm(const GemmArgs& a, GemmEpi epi, int npass, hipStream_t s)
     using TP = Tile<3, 0, 128, 128, 32, 4, 2, 2>;    // three-pass symmetric products
     using TU = Tile<1, 1, 128, 128, 32, 2, 2, 2>;    // update (B operand [K][N])
     using TU2 = Tile<2, 1, 128, 128, 32, 2, 2, 2>;   // two-pass final product
+    if (a.dual && !(epi == EPI_SPLIT && npass == 3)) return hipErrorInvalidValue;
     switch (epi) {
         case EPI_SPLIT:
             if (npass == 3) return launch_tile<3, EPI_SPLIT, TP, true>(a, s);
