@@ -69,6 +69,24 @@ __device__ __forceinline__ void stg(void* p, const V& v) {
     *(DION2_GLOBAL R*)p = r;
 }
 
+// Non-temporal variants for data touched once per step (streamed past the
+// caches rather than kept).
+template <typename V>
+__device__ __forceinline__ V ldg_nt(const void* p) {
+    typedef typename RawBits<sizeof(V)>::T R;
+    const R r = __builtin_nontemporal_load((const DION2_GLOBAL R*)p);
+    V v;
+    __builtin_memcpy(&v, &r, sizeof(V));
+    return v;
+}
+template <typename V>
+__device__ __forceinline__ void stg_nt(void* p, const V& v) {
+    typedef typename RawBits<sizeof(V)>::T R;
+    R r;
+    __builtin_memcpy(&r, &v, sizeof(V));
+    __builtin_nontemporal_store(r, (DION2_GLOBAL R*)p);
+}
+
 // ------------------------------------------------------------ conversions
 
 __device__ __forceinline__ float bf16_bits_to_f32(uint32_t h) {

@@ -100,17 +100,19 @@ __global__ __launch_bounds__(kThreads) void apply_cols(ApplyArgs a) {
         typedef typename std::conditional<sizeof(WT) == 2, uint2, float4>::type Raw;
         Raw raw[kR];
         float o[kR][4];
-        // branch-free loads (an unselected column reads line 0, unused; rows
-        // past the matrix read its last row) so all of them are in flight
-        // together
+        // branch-free loads so all of them are in flight together: an
+        // unselected column reads the block's first line (a word of the same
+        // row segment, so no extra cache line; unused), rows past the matrix
+        // read its last row
+        const int pfirst = ldg<int32_t>(rank + c0);
         int pc[4];
 #pragma unroll
-        for (int v = 0; v < 4; ++v) pc[v] = p[v] >= 0 ? p[v] : 0;
+        for (int v = 0; v < 4; ++v) pc[v] = p[v] >= 0 ? p[v] : pfirst;
 #pragma unroll
         for (int i = 0; i < kR; ++i) {
             int64_t r = r0 + rg + 4 * i;
             r = r < a.rows ? r : a.rows - 1;
-            raw[i] = ldg<Raw>(W + r * a.cols + c);
+            raw[i] = ldg_nt<Raw>(W + r * a.cols + c);
 #pragma unroll
             for (int v = 0; v < 4; ++v) o[i][v] = OT[r * a.kpad + pc[v]];
         }
@@ -127,14 +129,14 @@ __global__ __launch_bounds__(kThreads) void apply_cols(ApplyArgs a) {
                     if (p[v] >= 0)
                         h[v] = f64_to_bf16(__dsub_rn((double)bf16_bits_to_f32(h[v]),
                                                      __dmul_rn(a.lr_eff, (double)o[i][v])));
-                stg(W + r * a.cols + c, make_uint2(h[0] | (h[1] << 16), h[2] | (h[3] << 16)));
+                stg_nt(W + r * a.cols + c, make_uint2(h[0] | (h[1] << 16), h[2] | (h[3] << 16)));
             } else {
                 float4 x = reinterpret_cast<const float4&>(raw[i]);
                 float f[4] = {x.x, x.y, x.z, x.w};
 #pragma unroll
                 for (int v = 0; v < 4; ++v)
                     if (p[v] >= 0) f[v] = (float)__dsub_rn((double)f[v], __dmul_rn(a.lr_eff, (double)o[i][v]));
-                stg(W + r * a.cols + c, make_float4(f[0], f[1], f[2], f[3]));
+                stg_nt(W + r * a.cols + c, make_float4(f[0], f[1], f[2], f[3]));
             }
         }
     } else {

@@ -44,10 +44,10 @@ __global__ __launch_bounds__(kThreads) void gather_rows(GatherArgs a) {
             float* row = M + (int64_t)K[p] * a.cols;
             if (VEC == 4 && j + 3 < a.d_oth) {
                 float m[4];
-                load4(row + j, m);
+                unpack4(ldg_nt<float4>(row + j), m);
 #pragma unroll
                 for (int v = 0; v < 4; ++v) x[v] = m[v] * sc;
-                if (a.decay) stg(row + j, make_float4(a.mu * m[0], a.mu * m[1], a.mu * m[2], a.mu * m[3]));
+                if (a.decay) stg_nt(row + j, make_float4(a.mu * m[0], a.mu * m[1], a.mu * m[2], a.mu * m[3]));
             } else {
 #pragma unroll
                 for (int v = 0; v < 4; ++v) {
@@ -133,8 +133,8 @@ __global__ __launch_bounds__(kThreads) void update_cols(GatherArgs a) {
         for (int i = 0; i < kR; ++i) {
             const int64_t r = r0 + rg + 4 * i;
             if (r < a.rows) {
-                mr[i] = ldg<float4>(M + r * a.cols + c);
-                gr[i] = ldg<GRaw>(G + r * a.cols + c);
+                mr[i] = ldg_nt<float4>(M + r * a.cols + c);
+                gr[i] = ldg_nt<GRaw>(G + r * a.cols + c);
             }
         }
 #pragma unroll
@@ -153,7 +153,7 @@ __global__ __launch_bounds__(kThreads) void update_cols(GatherArgs a) {
 #pragma unroll
                 for (int v = 0; v < 4; ++v)
                     o[v] = (a.decay == 2 || (a.decay == 1 && pl[v] >= 0)) ? a.mu * m[v] : m[v];
-                stg(M + r * a.cols + c, make_float4(o[0], o[1], o[2], o[3]));
+                stg_nt(M + r * a.cols + c, make_float4(o[0], o[1], o[2], o[3]));
             }
 #pragma unroll
             for (int v = 0; v < 4; ++v)

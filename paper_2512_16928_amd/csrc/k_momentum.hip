@@ -9,13 +9,16 @@
 //
 // Row mode: one wave per row (four rows per 256-thread block); every lane
 // streams 4-element vectors (16 B of M, 8 B of bf16 G), eight vectors in
-// flight, and the wave reduces in a fixed shuffle order.
+// flight, and the wave reduces in a fixed shuffle order. M and G are
+// streamed with non-temporal loads and stores (each is touched once).
 // Column mode: M is only read here (the gather pass rewrites whole rows of
 // M once the selection is known, so the sum is stored once); each thread
 // owns 4 adjacent columns of a block of rows and writes double-double
 // partials, and a second pass folds the row blocks in order. No
 // floating-point atomics anywhere: results are run-to-run bitwise
 // reproducible.
+#include <type_traits>
+
 #include "dion2_device.h"
 
 namespace dion2 {
@@ -65,14 +68,15 @@ __global__ __launch_bounds__(kThreads) void momentum_rows(MatSet ms, int64_t row
             float m[kRowVecs][4], g[kRowVecs][4];
 #pragma unroll
             for (int u = 0; u < kRowVecs; ++u) {
-                load4(M + c + (u * 64 + lane) * 4, m[u]);
-                load4(G + c + (u * 64 + lane) * 4, g[u]);
+                unpack4(ldg_nt<float4>(M + c + (u * 64 + lane) * 4), m[u]);
+                unpack4(ldg_nt<typename std::conditional<sizeof(GT) == 2, uint2, float4>::type>(
+                            G + c + (u * 64 + lane) * 4), g[u]);
             }
 #pragma unroll
             for (int u = 0; u < kRowVecs; ++u) {
 #pragma unroll
                 for (int v = 0; v < 4; ++v) m[u][v] = m[u][v] + g[u][v];
-                stg(M + c + (u * 64 + lane) * 4, make_float4(m[u][0], m[u][1], m[u][2], m[u][3]));
+                stg_nt(M + c + (u * 64 + lane) * 4, make_float4(m[u][0], m[u][1], m[u][2], m[u][3]));
 #pragma unroll
                 for (int v = 0; v < 4; ++v) accumulate(fabs((double)m[u][v]), h4[v], l4[v], q4[v]);
             }
@@ -129,8 +133,8 @@ __global__ __launch_bounds__(kThreads) void momentum_cols_partial(MatSet ms, int
         const GT* q = G + r * cols + c0;
         if constexpr (VEC == 4) {
             float m[4], g[4];
-            load4(p, m);
-            load4(q, g);
+            unpack4(ldg_nt<float4>(p), m);
+            unpack4(ldg_nt<typename std::conditional<sizeof(GT) == 2, uint2, float4>::type>(q), g);
 #pragma unroll
             for (int v = 0; v < 4; ++v) m[v] = m[v] + g[v];
 #pragma unroll
