@@ -46,11 +46,16 @@ def log(msg):
     print(msg, file=sys.stderr, flush=True)
 
 
-def allocate(wl, dev):
+def allocate(wl, dev, split=1):
+    """The stack's tensors, one entry per library call: each shape group, or
+    each of `split` equal sub-batches of it (views of the same storage)."""
     groups = []
     for gi, grp in enumerate(wl.groups):
         W, M, G = workloads.make_group(wl, gi, dev)
-        groups.append((grp, W, M, G))
+        n = max(1, min(split, grp.count))
+        bounds = [grp.count * i // n for i in range(n + 1)]
+        for lo, hi in zip(bounds[:-1], bounds[1:]):
+            groups.append((grp, W[lo:hi], M[lo:hi], G[lo:hi]))
     torch.cuda.synchronize()
     return groups
 
@@ -83,7 +88,7 @@ def one_step(wl, groups, alpha, rule=binding.SELECT_L1):
                 binding.dion2_step_ex(W, M, G, alpha, wl.mu, wl.lr, wl.ns_steps, grp.axis,
                                       ns_form=NS_FORM, select_rule=rule, rand_seed=1234,
                                       rand_step=STEP[0], rand_matrix0=first)
-        first += grp.count
+        first += W.shape[0]
     for s in STREAMS:
         join = torch.cuda.Event()
         join.record(s)
@@ -198,6 +203,8 @@ def main(argv=None):
     ap.add_argument("--no-profile", action="store_true", help="skip the per-kernel event pass")
     ap.add_argument("--ns-form", default="auto", choices=sorted(NS_FORMS),
                     help="Newton-Schulz evaluation order (default: chosen by shape)")
+    ap.add_argument("--split", type=int, default=1,
+                    help="issue each shape group as this many sub-batch calls")
     ap.add_argument("--streams", type=int, default=-1,
                     help="run the shape groups on this many streams (0: all on the current "
                          "stream; default: one stream per group, the groups being independent)")
@@ -237,12 +244,12 @@ def main(argv=None):
     wl = workloads.WORKLOADS[args.workload]
     alpha = args.alpha if args.alpha is not None else wl.alphas[0]
     if args.streams < 0:
-        args.streams = len(wl.groups)
+        args.streams = len(wl.groups) * max(1, args.split)
     STREAMS.extend(torch.cuda.Stream() for _ in range(args.streams))   # default priority
     dev = torch.device("cuda:0")
     log(f"[bench] allocating workload {wl.name}: {wl.matrices()} matrices, "
         f"{wl.elements() / 1e6:.1f}M elements")
-    groups = allocate(wl, dev)
+    groups = allocate(wl, dev, args.split)
 
     log(f"[bench] timing alpha={alpha}: warmup {args.warmup}, steps {args.steps}")
     per, wall = time_steps(wl, groups, alpha, args.warmup, args.steps)
@@ -318,7 +325,7 @@ def main(argv=None):
                    "matrices": wl.matrices(), "elements": wl.elements(),
                    "ns_steps": wl.ns_steps, "mu": wl.mu, "lr": wl.lr, "ns_form": args.ns_form,
                    "parallelism": "single GPU, batched per shape group",
-                   "streams": args.streams},
+                   "streams": args.streams, "split": args.split},
         "roofline": roofline,
         "cpu_baseline": cpu,
         "per_alpha_ms": per_alpha,
