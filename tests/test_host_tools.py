@@ -1,0 +1,49 @@
+"""CPU tests of the host-side tools: the profile summariser's kernel-to-phase
+mapping and the benchmark's single-GPU guard."""
+import os
+import subprocess
+import sys
+
+from paper_2512_16928_amd import profsum
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def test_phase_of_kernel_names():
+    cases = {
+        "void dion2::(anonymous namespace)::momentum_rows<4, unsigned short>(dion2::MatSet, long)": "momentum",
+        "dion2::(anonymous namespace)::momentum_cols_final(double const*, int, long)": "momentum",
+        "dion2::(anonymous namespace)::select_topk(dion2::SelectArgs)": "select",
+        "void dion2::(anonymous namespace)::gather_rows<4>(dion2::GatherArgs)": "gather",
+        "void dion2::(anonymous namespace)::update_cols<4, unsigned short>(dion2::GatherArgs)": "gather",
+        "void dion2::(anonymous namespace)::apply_cols<4, unsigned short>(dion2::ApplyArgs)": "apply",
+        "void dion2::(anonymous namespace)::gemm<1, 0, dion2::(anonymous namespace)::Tile<1, 0, 128, 128, 32, 2, 2, 4>, true>(dion2::GemmArgs)": "ns_gram",
+        "void dion2::(anonymous namespace)::gemm<3, 0, dion2::(anonymous namespace)::Tile<3, 0, 128, 128, 32, 4, 2, 2>, true>(dion2::GemmArgs)": "ns_poly",
+        "void dion2::(anonymous namespace)::gemm<3, 4, dion2::(anonymous namespace)::Tile<3, 0, 128, 128, 32, 4, 2, 2>, true>(dion2::GemmArgs)": "ns_poly",
+        "void dion2::(anonymous namespace)::gemm<3, 1, dion2::(anonymous namespace)::Tile<3, 0, 128, 128, 32, 4, 2, 2>, true>(dion2::GemmArgs)": "ns_poly",
+        "void dion2::(anonymous namespace)::gemm<1, 2, dion2::(anonymous namespace)::Tile<1, 1, 128, 128, 32, 2, 2, 2>, false>(dion2::GemmArgs)": "ns_update",
+        "void dion2::(anonymous namespace)::gemm<2, 3, dion2::(anonymous namespace)::Tile<2, 1, 128, 128, 32, 2, 2, 2>, false>(dion2::GemmArgs)": "ns_update",
+        "void dion2::(anonymous namespace)::gemm<2, 5, dion2::(anonymous namespace)::Tile<2, 1, 128, 128, 32, 2, 2, 2>, false>(dion2::GemmArgs)": "ns_update",
+        "void at::native::vectorized_elementwise_kernel<4, at::native::neg_kernel_cuda>": None,
+    }
+    for name, phase in cases.items():
+        assert profsum.phase_of(name) == phase, name
+
+
+def test_traffic_lookup_requires_matching_sources(tmp_path):
+    good = profsum.source_hash("ns_poly")
+    f = tmp_path / "t_traffic.txt"
+    f.write_text(f"traffic phase=ns_poly workload=1b alpha=0.25 sources={good} "
+                 "read_bytes_per_launch=1 write_bytes_per_launch=2 bytes_per_launch=3 launches=1\n"
+                 "traffic phase=apply workload=1b alpha=0.25 sources=0000000000000000 "
+                 "read_bytes_per_launch=1 write_bytes_per_launch=2 bytes_per_launch=3 launches=1\n")
+    assert profsum.lookup_traffic(str(f), "ns_poly", "1b", 0.25) == 3.0
+    assert profsum.lookup_traffic(str(f), "ns_poly", "1b", 0.5) is None     # other workload point
+    assert profsum.lookup_traffic(str(f), "apply", "1b", 0.25) is None      # stale sources
+
+
+def test_bench_refuses_more_than_one_gpu():
+    r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", "2"],
+                       capture_output=True, text=True, timeout=300)
+    assert r.returncode == 2
+    assert "one GPU" in r.stderr
