@@ -112,10 +112,15 @@ template <typename T> struct Elem;
 template <> struct Elem<float> {
     static __device__ __forceinline__ float load(const float* p) { return ldg<float>(p); }
     static __device__ __forceinline__ void store_f64(float* p, double v) { stg<float>(p, (float)v); }
+    // the same on an LDS copy
+    static __device__ __forceinline__ float lds_load(const float* p) { return *p; }
+    static __device__ __forceinline__ void lds_store_f64(float* p, double v) { *p = (float)v; }
 };
 template <> struct Elem<uint16_t> {
     static __device__ __forceinline__ float load(const uint16_t* p) { return bf16_bits_to_f32(ldg<uint16_t>(p)); }
     static __device__ __forceinline__ void store_f64(uint16_t* p, double v) { stg<uint16_t>(p, f64_to_bf16(v)); }
+    static __device__ __forceinline__ float lds_load(const uint16_t* p) { return bf16_bits_to_f32(*p); }
+    static __device__ __forceinline__ void lds_store_f64(uint16_t* p, double v) { *p = f64_to_bf16(v); }
 };
 
 // four consecutive elements as fp32 (p is 8-byte aligned for bf16, 16 for fp32)

@@ -8,7 +8,11 @@
 // copied out unpadded for inspection.
 //
 // Row mode reads O rows and W rows along j (both contiguous). Column mode
-// streams W by rows and reads O transposed.
+// streams W by rows and reads O transposed: when the column count is a
+// multiple of 8 a block takes a strip of 512 columns (8 per lane, one
+// 16-byte bf16 chunk) over 16 rows, stages the strip's slice of O^T in LDS
+// and rewrites only the chunks that hold a selected column; other column
+// counts take a generic four-column (or one-column) path.
 #include <type_traits>
 
 #include "dion2_device.h"
@@ -159,6 +163,248 @@ __global__ __launch_bounds__(kThreads) void apply_cols(ApplyArgs a) {
     }
 }
 
+// Column mode, cols % 8 == 0. A block covers a strip of kStrip columns x
+// kStripRows rows; lane l owns columns c .. c + 7 (c = strip + 8 l) of the
+// four rows of its wave. The selected columns of a strip have consecutive
+// ranks [rank[s0], rank[s1]), so the values the strip needs sit in one
+// contiguous slice of each O^T row; every wave copies the slices of its own
+// rows into LDS with aligned 16-byte loads (the slice start rounded down to
+// a multiple of 4) and then reads O^T[r][rank[c]] from there. A chunk with
+// no selected column is neither read nor written; in the others the
+// unselected entries keep their bits.
+constexpr int kLaneCols = 8;
+constexpr int kStrip = 64 * kLaneCols;
+constexpr int kStripRows = 16;
+constexpr int kRowsPerWave = kStripRows / 4;
+constexpr int kOtPitch = kStrip + 4;   // floats: a slice spans at most kStrip + 3
+
+template <typename WT>
+struct Chunk8;   // eight consecutive W entries
+template <>
+struct Chunk8<uint16_t> {
+    uint4 u;
+    __device__ __forceinline__ void load(const uint16_t* p) { u = ldg_nt<uint4>(p); }
+    __device__ __forceinline__ void store(uint16_t* p) const { stg_nt(p, u); }
+    __device__ __forceinline__ void put(uint16_t* lds) const { *reinterpret_cast<uint4*>(lds) = u; }
+    __device__ __forceinline__ void get_lds(const uint16_t* lds) { u = *reinterpret_cast<const uint4*>(lds); }
+    __device__ __forceinline__ float get(int v) const {
+        const uint32_t w = v < 2 ? u.x : v < 4 ? u.y : v < 6 ? u.z : u.w;
+        return bf16_bits_to_f32((v & 1) ? (w >> 16) : (w & 0xffffu));
+    }
+    __device__ __forceinline__ void set(int v, double r) {
+        const uint32_t h = f64_to_bf16(r);
+        uint32_t& w = v < 2 ? u.x : v < 4 ? u.y : v < 6 ? u.z : u.w;
+        w = (v & 1) ? ((w & 0xffffu) | (h << 16)) : ((w & 0xffff0000u) | h);
+    }
+};
+template <>
+struct Chunk8<float> {
+    float f[8];
+    __device__ __forceinline__ void load(const float* p) {
+        unpack4(ldg_nt<float4>(p), *reinterpret_cast<float(*)[4]>(&f[0]));
+        unpack4(ldg_nt<float4>(p + 4), *reinterpret_cast<float(*)[4]>(&f[4]));
+    }
+    __device__ __forceinline__ void store(float* p) const {
+        stg_nt(p, make_float4(f[0], f[1], f[2], f[3]));
+        stg_nt(p + 4, make_float4(f[4], f[5], f[6], f[7]));
+    }
+    __device__ __forceinline__ void put(float* lds) const {
+        reinterpret_cast<float4*>(lds)[0] = make_float4(f[0], f[1], f[2], f[3]);
+        reinterpret_cast<float4*>(lds)[1] = make_float4(f[4], f[5], f[6], f[7]);
+    }
+    __device__ __forceinline__ void get_lds(const float* lds) {
+        unpack4(reinterpret_cast<const float4*>(lds)[0], *reinterpret_cast<float(*)[4]>(&f[0]));
+        unpack4(reinterpret_cast<const float4*>(lds)[1], *reinterpret_cast<float(*)[4]>(&f[4]));
+    }
+    __device__ __forceinline__ float get(int v) const { return f[v]; }
+    __device__ __forceinline__ void set(int v, double r) { f[v] = (float)r; }
+};
+
+template <typename WT>
+__global__ __launch_bounds__(kThreads) void apply_cols_strip(ApplyArgs a) {
+    __shared__ __attribute__((aligned(16))) float ot[kStripRows][kOtPitch];
+    const int b = blockIdx.z;
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int64_t s0 = (int64_t)blockIdx.x * kStrip;
+    const int64_t s1 = s0 + kStrip < a.cols ? s0 + kStrip : a.cols;
+    const int64_t r0 = (int64_t)blockIdx.y * kStripRows;
+    const int32_t* __restrict__ rank = a.rank + (int64_t)b * (a.cols + 1);
+    WT* __restrict__ W = a.ms.w<WT>(b);
+    const float* __restrict__ OT = a.O + (int64_t)b * a.opad * a.kpad;
+
+    // ranks of this lane's columns (clamped past the strip: no column)
+    const int64_t c = s0 + kLaneCols * lane;
+    int rk[kLaneCols + 1];
+#pragma unroll
+    for (int v = 0; v <= kLaneCols; ++v) rk[v] = ldg<int32_t>(rank + (c < s1 ? c + v : s1));
+    unsigned m = 0;
+#pragma unroll
+    for (int v = 0; v < kLaneCols; ++v) m |= (rk[v + 1] > rk[v] ? 1u : 0u) << v;
+
+    // this wave's rows (past the matrix: its last row, never stored)
+    int64_t rr[kRowsPerWave];
+#pragma unroll
+    for (int i = 0; i < kRowsPerWave; ++i) {
+        const int64_t r = r0 + wave + 4 * i;
+        rr[i] = r < a.rows ? r : a.rows - 1;
+    }
+    Chunk8<WT> w[kRowsPerWave];
+    if (m) {
+#pragma unroll
+        for (int i = 0; i < kRowsPerWave; ++i) w[i].load(W + rr[i] * a.cols + c);
+    }
+
+    // the strip's O^T slices of this wave's rows into LDS
+    const int R0 = ldg<int32_t>(rank + s0) & ~3;
+    const int R1 = ldg<int32_t>(rank + s1);
+    const int nq = (R1 - R0 + 3) >> 2;   // 16-byte pieces per row; R0 + 4 nq <= kpad
+#pragma unroll
+    for (int i = 0; i < kRowsPerWave; ++i) {
+        const float* src = OT + rr[i] * a.kpad + R0;
+        float* dst = &ot[wave + 4 * i][0];
+        for (int q = lane; q < nq; q += 64) {
+            const float4 x = ldg<float4>(src + 4 * q);
+            *reinterpret_cast<float4*>(dst + 4 * q) = x;
+        }
+    }
+    // LDS accesses of one wave complete in issue order: no block barrier
+    __builtin_amdgcn_wave_barrier();
+    if (!m) return;
+
+#pragma unroll
+    for (int i = 0; i < kRowsPerWave; ++i) {
+        const int64_t r = r0 + wave + 4 * i;
+        if (r >= a.rows) break;
+        const float* o = &ot[wave + 4 * i][0];
+#pragma unroll
+        for (int v = 0; v < kLaneCols; ++v) {
+            if (m & (1u << v)) {
+                const float ov = o[rk[v] - R0];
+                w[i].set(v, __dsub_rn((double)w[i].get(v), __dmul_rn(a.lr_eff, (double)ov)));
+                if (a.dbg) a.dbg[((int64_t)b * a.k + rk[v]) * a.d_oth + r] = ov;
+            }
+        }
+        w[i].store(W + r * a.cols + c);
+    }
+}
+
+// Column mode, cols % 8 == 0, k <= 1024 and a row of W within 8 KB: whole
+// rows per wave, the arithmetic spread over the selected entries rather
+// than over the columns. A wave copies its row of W into LDS (16-byte
+// chunks), lane l updates there the entries of ranks p = l + 64 t (column
+// K[p], value O^T[r][p], read coalesced), and the row goes back to W whole.
+// Every lane does the same number of updates, so nothing diverges; K is
+// staged in LDS once per block.
+constexpr int kSelRows = 32;                 // rows per block (8 per wave)
+constexpr int kSelRowBytes = 8192;           // LDS row buffer per wave
+constexpr int kSelMaxK = 1024;
+
+template <typename WT, int NCH, int KT>
+__global__ __launch_bounds__(kThreads) void apply_cols_sel(ApplyArgs a) {
+    __shared__ __attribute__((aligned(16))) WT row_s[4][kSelRowBytes / sizeof(WT)];
+    __shared__ int32_t sel_s[kSelMaxK];
+    const int b = blockIdx.y;
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    {
+        constexpr int kN = kSelMaxK / kThreads;
+        const int32_t* sel = a.sel + (int64_t)b * a.k;
+        int32_t t[kN];   // all loads in flight before the first LDS write
+#pragma unroll
+        for (int q = 0; q < kN; ++q) {
+            const int i = threadIdx.x + q * kThreads;
+            t[q] = ldg<int32_t>(sel + (i < a.k ? i : a.k - 1));
+        }
+#pragma unroll
+        for (int q = 0; q < kN; ++q) sel_s[threadIdx.x + q * kThreads] = t[q];
+    }
+    __syncthreads();
+
+    WT* __restrict__ W = a.ms.w<WT>(b);
+    const float* __restrict__ OT = a.O + (int64_t)b * a.opad * a.kpad;
+    WT* rs = row_s[wave];
+    int coff[NCH];   // this lane's chunks; past the row end: clamped, unused
+    bool cval[NCH];
+#pragma unroll
+    for (int j = 0; j < NCH; ++j) {
+        const int c = kLaneCols * (lane + 64 * j);
+        cval[j] = c < a.cols;
+        coff[j] = cval[j] ? c : (int)a.cols - kLaneCols;
+    }
+    // Software pipelined over the wave's rows: the loads of the next row are
+    // issued before the stores of this one. Vector memory counters retire in
+    // issue order, so a wait for loads issued after a row's stores would also
+    // wait for those stores to be acknowledged; issued before them, it does
+    // not. The last row's "next" loads re-read that row, unused.
+    auto load_row = [&](int64_t r, Chunk8<WT> (&w)[NCH], float (&o)[KT]) {
+#pragma unroll
+        for (int j = 0; j < NCH; ++j) w[j].load(W + r * a.cols + coff[j]);
+        const float* src = OT + r * a.kpad;
+#pragma unroll
+        for (int t = 0; t < KT; ++t) {
+            const int p = lane + 64 * t;
+            o[t] = ldg<float>(src + (p < a.k ? p : a.k - 1));
+        }
+    };
+    const int64_t r_end = (int64_t)(blockIdx.x + 1) * kSelRows < a.rows ? (int64_t)(blockIdx.x + 1) * kSelRows
+                                                                         : a.rows;
+    int64_t r = (int64_t)blockIdx.x * kSelRows + wave;
+    if (r >= r_end) return;   // whole wave; no block barrier follows
+    Chunk8<WT> w[NCH], wn[NCH];
+    float o[KT], on[KT];
+    load_row(r, w, o);
+    for (; r < r_end; r += 4) {
+        load_row(r + 4 < r_end ? r + 4 : r, wn, on);
+#pragma unroll
+        for (int j = 0; j < NCH; ++j)
+            if (cval[j]) w[j].put(rs + coff[j]);
+        // LDS accesses of one wave complete in issue order
+        __builtin_amdgcn_wave_barrier();
+#pragma unroll
+        for (int t = 0; t < KT; ++t) {
+            const int p = lane + 64 * t;
+            if (p < a.k) {
+                WT* e = rs + sel_s[p];
+                Elem<WT>::lds_store_f64(e, __dsub_rn((double)Elem<WT>::lds_load(e), __dmul_rn(a.lr_eff, (double)o[t])));
+                if (a.dbg) a.dbg[((int64_t)b * a.k + p) * a.d_oth + r] = o[t];
+            }
+        }
+        __builtin_amdgcn_wave_barrier();
+#pragma unroll
+        for (int j = 0; j < NCH; ++j) {
+            if (cval[j]) {
+                w[j].get_lds(rs + coff[j]);
+                w[j].store(W + r * a.cols + coff[j]);
+            }
+        }
+        __builtin_amdgcn_wave_barrier();   // the row buffer is rewritten next
+#pragma unroll
+        for (int j = 0; j < NCH; ++j) w[j] = wn[j];
+#pragma unroll
+        for (int t = 0; t < KT; ++t) o[t] = on[t];
+    }
+}
+
+template <typename WT, int NCH>
+void launch_cols_sel_k(const ApplyArgs& a, hipStream_t s) {
+    dim3 grid((unsigned)((a.rows + kSelRows - 1) / kSelRows), (unsigned)a.batch);
+    if (a.k <= 256) hipLaunchKernelGGL((apply_cols_sel<WT, NCH, 4>), grid, dim3(kThreads), 0, s, a);
+    else if (a.k <= 512) hipLaunchKernelGGL((apply_cols_sel<WT, NCH, 8>), grid, dim3(kThreads), 0, s, a);
+    else hipLaunchKernelGGL((apply_cols_sel<WT, NCH, 16>), grid, dim3(kThreads), 0, s, a);
+}
+
+template <typename WT>
+bool launch_cols_sel(const ApplyArgs& a, hipStream_t s) {
+    constexpr int64_t kMaxCols = kSelRowBytes / sizeof(WT);
+    if (a.cols % kLaneCols || a.cols > kMaxCols || a.k > kSelMaxK) return false;
+    const int64_t nch = (a.cols + kStrip - 1) / kStrip;
+    if (nch <= 1) launch_cols_sel_k<WT, 1>(a, s);
+    else if (nch <= 2) launch_cols_sel_k<WT, 2>(a, s);
+    else if (nch <= 4) launch_cols_sel_k<WT, 4>(a, s);
+    else if constexpr (kMaxCols > 2048) launch_cols_sel_k<WT, 8>(a, s);
+    else return false;
+    return true;
+}
+
 }  // namespace
 
 hipError_t launch_apply(const ApplyArgs& a, int axis, int w_bf16, hipStream_t s) {
@@ -172,6 +418,13 @@ hipError_t launch_apply(const ApplyArgs& a, int axis, int w_bf16, hipStream_t s)
             if (vec) hipLaunchKernelGGL((apply_rows<4, float>), grid, dim3(kThreads), 0, s, a);
             else hipLaunchKernelGGL((apply_rows<1, float>), grid, dim3(kThreads), 0, s, a);
         }
+    } else if (w_bf16 ? launch_cols_sel<uint16_t>(a, s) : launch_cols_sel<float>(a, s)) {
+        // whole rows per wave, one update per selected entry
+    } else if (a.cols % kLaneCols == 0) {
+        dim3 grid((unsigned)((a.cols + kStrip - 1) / kStrip),
+                  (unsigned)((a.rows + kStripRows - 1) / kStripRows), (unsigned)a.batch);
+        if (w_bf16) hipLaunchKernelGGL((apply_cols_strip<uint16_t>), grid, dim3(kThreads), 0, s, a);
+        else hipLaunchKernelGGL((apply_cols_strip<float>), grid, dim3(kThreads), 0, s, a);
     } else {
         dim3 grid((unsigned)((a.cols + kCW - 1) / kCW), (unsigned)((a.rows + kRB - 1) / kRB),
                   (unsigned)a.batch);

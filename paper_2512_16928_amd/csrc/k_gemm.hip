@@ -290,8 +290,12 @@ __global__ __launch_bounds__(T::THREADS) void gemm(GemmArgs a) {
         }
         b >>= 1;
     }
-    int row0 = ((logical / nx) % ny) * T::BM;   // output rows (M)
-    int col0 = (logical % nx) * T::BN;          // output cols (N)
+    // Within a matrix the tiles run down each column strip first: the ny
+    // tiles that read one strip of the B operand are dispatched together, so
+    // the strip is fetched into L2 once, while the A operand (the s x s
+    // factor, the smaller one) stays resident across strips.
+    int row0 = (logical % ny) * T::BM;          // output rows (M)
+    int col0 = ((logical / ny) % nx) * T::BN;   // output cols (N)
     if constexpr (SYM) {
         // symmetric output: x enumerates the upper-triangle tiles I <= J
         // row by row; each is written at (I, J) and mirrored to (J, I)

@@ -106,6 +106,10 @@ def test_single_256_fp32_full(hip_device):
     (300, 200, 0.75, AXIS_ROWS, "f32"),      # k = 225 > d_oth = 200, rows
     (1, 40, 1.0, AXIS_AUTO, "bf16"),         # a single row
     (384, 640, 0.1, AXIS_AUTO, "bf16"),      # alpha not a power of two
+    (200, 96, 0.5, AXIS_AUTO, "f32"),        # columns, fp32 W, one row per wave
+    (40, 4616, 0.5, AXIS_COLS, "bf16"),      # columns beyond 4096: 512-column strips
+    (24, 4104, 0.25, AXIS_COLS, "f32"),      # the same with fp32 W, ragged last strip
+    (64, 2048, 0.75, AXIS_COLS, "bf16"),     # k = 1536 > 1024: strips as well
 ])
 @FORMS
 def test_ragged_shapes(hip_device, rows, cols, alpha, axis, wdt, form):
