@@ -100,12 +100,20 @@ __device__ __forceinline__ uint16_t f32_to_bf16(float f) {
 }
 
 // fp64 -> bf16 with a single round-to-nearest-even: first to fp32 with
-// round-to-odd (truncate, then force the last bit when inexact), which keeps
-// the second rounding exact because fp32 carries more than 8 + 2 bits.
+// round-to-odd (toward zero, then the last bit forced when inexact), which
+// keeps the second rounding exact because fp32 carries more than 8 + 2 bits.
+// Round-to-odd is built from the hardware's nearest-even conversion: where
+// that rounded away from zero the magnitude steps back one unit (the bit
+// pattern minus one, also from inf to the largest finite value). A NaN
+// stays a NaN. About eight vector instructions, where a directed-rounding
+// conversion is emulated with some twenty.
 __device__ __forceinline__ uint16_t f64_to_bf16(double d) {
-    float f = __double2float_rz(d);
-    if ((double)f != d && !__builtin_isnan(d)) f = __uint_as_float(__float_as_uint(f) | 1u);
-    return f32_to_bf16(f);
+    const float f = (float)d;
+    const double back = (double)f;
+    uint32_t u = __float_as_uint(f);
+    u -= __builtin_fabs(back) > __builtin_fabs(d) ? 1u : 0u;
+    u |= back != d ? 1u : 0u;
+    return f32_to_bf16(__uint_as_float(u));
 }
 
 template <typename T> struct Elem;
