@@ -4,10 +4,11 @@
     python bench.py [--steps K] [--warmup W] [--workload 1b] [--alpha 0.25]
 
 A step is one Dion2 update (Algorithm 1) of every matrix of a synthetic layer
-stack, one batched library call per same-shape group, with W, M, G resident
-in HBM. The groups are independent, so by default each runs on its own
-stream (forked from and joined into the timing stream); --streams 0 runs
-them back to back on one stream. The default is the paper's timing method
+stack with W, M, G resident in HBM: by default one dion2_step_groups call
+for the whole stack (groups of one padded Newton-Schulz size share their
+chain of s x s products). With --calls per-group it is one batched call per
+same-shape group, each on its own stream (forked from and joined into the
+timing stream), or back to back on one stream with --streams 0. The default is the paper's timing method
 (Sec. 4.4): 100 steps, the mean of the final 20 reported (warmup 80,
 steps 20). Prints one JSON line:
   value        mean ms per step at --alpha (lower is better)
@@ -65,6 +66,8 @@ SELECT_RULES = {"l1": binding.SELECT_L1, "random": binding.SELECT_RANDOM}
 NS_FORM = binding.NS_AUTO
 STEP = [0]      # optimizer step counter (the Random rule draws anew every step)
 STREAMS = []    # one stream per shape group when the groups run concurrently
+GROUPED = [False]   # one dion2_step_groups call for the whole stack
+GROUP_STREAMS = [0]  # streams the grouped call may spread its groups over (0: library's choice)
 
 
 def one_step(wl, groups, alpha, rule=binding.SELECT_L1):
@@ -72,6 +75,12 @@ def one_step(wl, groups, alpha, rule=binding.SELECT_L1):
     group. The groups are independent, so with STREAMS set each runs on its
     own stream (forked from and joined back into the current stream)."""
     STEP[0] += 1
+    if GROUPED[0]:
+        binding.dion2_step_groups([(W, M, G, grp.axis) for grp, W, M, G in groups], alpha, wl.mu,
+                                  wl.lr, wl.ns_steps, ns_form=NS_FORM, select_rule=rule,
+                                  rand_seed=1234, rand_step=STEP[0], rand_matrix0=0,
+                                  group_streams=GROUP_STREAMS[0])
+        return
     first = 0
     main = torch.cuda.current_stream()
     if STREAMS:
@@ -114,9 +123,11 @@ def time_steps(wl, groups, alpha, warmup, steps, rule=binding.SELECT_L1):
 def profile_phases(wl, groups, alpha, steps):
     """Per-phase kernel time from events the library records around each
     launch on its stream, with the phase's algorithmic work. The groups run
-    back to back here, so each phase is timed without other work beside it."""
-    saved = STREAMS[:]
+    back to back here (one stream), so each phase is timed without other work
+    beside it."""
+    saved, saved_gs = STREAMS[:], GROUP_STREAMS[0]
     STREAMS.clear()
+    GROUP_STREAMS[0] = 1
     binding.dion2_profile_reset()
     binding.dion2_profile_enable(True)
     try:
@@ -127,6 +138,7 @@ def profile_phases(wl, groups, alpha, steps):
     finally:
         binding.dion2_profile_enable(False)
         STREAMS.extend(saved)
+        GROUP_STREAMS[0] = saved_gs
     out = {}
     for ph, d in prof.items():
         if d["launches"] == 0:
@@ -208,6 +220,13 @@ def main(argv=None):
     ap.add_argument("--streams", type=int, default=-1,
                     help="run the shape groups on this many streams (0: all on the current "
                          "stream; default: one stream per group, the groups being independent)")
+    ap.add_argument("--calls", default="grouped", choices=("grouped", "per-group"),
+                    help="one dion2_step_groups call for the whole stack (groups of one padded "
+                         "Newton-Schulz size share their s x s chain), or one call per shape "
+                         "group on its own stream")
+    ap.add_argument("--group-streams", type=int, default=0,
+                    help="with --calls grouped: streams the library may spread the groups over "
+                         "(0: its choice, 1: all on one stream)")
     ap.add_argument("--no-random-rule", action="store_true",
                     help="skip timing the Random selection rule at --alpha")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -243,6 +262,10 @@ def main(argv=None):
 
     wl = workloads.WORKLOADS[args.workload]
     alpha = args.alpha if args.alpha is not None else wl.alphas[0]
+    GROUPED[0] = args.calls == "grouped"
+    GROUP_STREAMS[0] = args.group_streams
+    if GROUPED[0]:
+        args.streams = 0
     if args.streams < 0:
         args.streams = len(wl.groups) * max(1, args.split)
     STREAMS.extend(torch.cuda.Stream() for _ in range(args.streams))   # default priority
@@ -325,6 +348,7 @@ def main(argv=None):
                    "matrices": wl.matrices(), "elements": wl.elements(),
                    "ns_steps": wl.ns_steps, "mu": wl.mu, "lr": wl.lr, "ns_form": args.ns_form,
                    "parallelism": "single GPU, batched per shape group",
+                   "calls": args.calls, "group_streams": args.group_streams,
                    "streams": args.streams, "split": args.split},
         "roofline": roofline,
         "cpu_baseline": cpu,

@@ -132,6 +132,9 @@ typedef struct dion2_options {
     uint64_t rand_step;      /* RANDOM: optimizer step, so each step draws anew     */
     int64_t rand_matrix0;    /* RANDOM: index of the batch's first matrix; >= 0 and
                                 rand_matrix0 + batch <= 2^32                       */
+    int group_streams;       /* dion2_step_groups: how many streams the groups may
+                                run on at once (0 = the library's choice, 1 = all
+                                on the call's stream, at most 8)                   */
 } dion2_options;
 
 /* Defaults: bf16 W and G, Muon quintic, eps 1e-7, selective decay, internal
@@ -164,6 +167,42 @@ int dion2_step_batched(void* const* W, float* const* M, const void* const* G,
 int dion2_step_ex(void* W, float* M, const void* G, int batch, int64_t rows,
                   int64_t cols, float alpha, float mu, float lr, int ns_steps,
                   int axis, const dion2_options* opt, void* stream);
+
+/* One same-shape group for dion2_step_groups: contiguous DEVICE stacks W
+   and G [batch][rows][cols] in the storage types of the options, M fp32
+   [batch][rows][cols], each 16-byte aligned, and the group's selection axis
+   (DION2_AXIS_*). */
+typedef struct dion2_group {
+    void* W;
+    float* M;
+    const void* G;
+    int batch;
+    int64_t rows, cols;
+    int axis;
+} dion2_group;
+
+/* The step of Algorithm 1 for several same-shape groups in one call on one
+   stream, with shared hyper-parameters and options (a model's whole layer
+   stack, say). The result is bitwise that of dion2_step_ex called for each
+   group in order; for the RANDOM rule group g's matrix indices start at
+   rand_matrix0 plus the batches of groups 0 .. g-1. Groups whose
+   Newton-Schulz runs in the GRAM form with the same padded s x s size share
+   one batched chain of s x s products, launched once for all of them.
+   groups is a HOST array of ngroups entries, read before the call returns.
+   The groups are independent until their chains, so they may run
+   concurrently on internal streams of default priority (opt->group_streams);
+   those fork from `stream` and are joined back into it before the call
+   returns: work queued on `stream` before the call is done before any of
+   it starts, and work queued after waits for all of it.
+   The workspace is the library's (opt->workspace must be NULL) and the debug
+   outputs must be NULL. Errors: DION2_ERR_INVALID_ARG for ngroups outside
+   [1, 64], a NULL array or stack pointer, an unaligned stack, a set
+   workspace or debug output, group_streams outside [0, 8], or an argument
+   dion2_step_ex would reject for some group (nothing is modified then);
+   DION2_ERR_HIP if an internal stream or event cannot be created. */
+int dion2_step_groups(const dion2_group* groups, int ngroups, float alpha,
+                      float mu, float lr, int ns_steps,
+                      const dion2_options* opt, void* stream);
 
 /* Bytes of device workspace one call with these arguments needs (for
    dion2_options.workspace) with ns_form = DION2_NS_AUTO; a forced form may

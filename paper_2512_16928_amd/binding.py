@@ -36,7 +36,7 @@ MAX_NS_STEPS = 16
 
 # Every function include/dion2.h declares (checked by the ABI tests).
 EXPORTED = ("dion2_options_init", "dion2_step", "dion2_step_strided", "dion2_step_batched",
-            "dion2_step_ex", "dion2_workspace_size", "dion2_plan_info",
+            "dion2_step_ex", "dion2_step_groups", "dion2_workspace_size", "dion2_plan_info",
             "dion2_release_workspaces", "dion2_status_string", "dion2_last_error",
             "dion2_version", "dion2_profile_enable", "dion2_profile_read", "dion2_profile_reset")
 
@@ -67,10 +67,24 @@ class Options(ctypes.Structure):
         ("rand_seed", ctypes.c_uint64),
         ("rand_step", ctypes.c_uint64),
         ("rand_matrix0", ctypes.c_int64),
+        ("group_streams", c_int),
     ]
 
 
 _lib = None
+
+
+class Group(ctypes.Structure):
+    """dion2_group: one same-shape stack of a grouped call."""
+    _fields_ = [
+        ("W", c_void_p),
+        ("M", c_void_p),
+        ("G", c_void_p),
+        ("batch", c_int),
+        ("rows", c_int64),
+        ("cols", c_int64),
+        ("axis", c_int),
+    ]
 
 
 def load(path: str = LIB_PATH):
@@ -96,6 +110,9 @@ def load(path: str = LIB_PATH):
     lib.dion2_step_batched.restype = c_int
     lib.dion2_step_ex.argtypes = [vp, vp, vp, c_int, i64, i64, *step_tail, POINTER(Options), vp]
     lib.dion2_step_ex.restype = c_int
+    lib.dion2_step_groups.argtypes = [POINTER(Group), c_int, c_float, c_float, c_float, c_int,
+                                      POINTER(Options), vp]
+    lib.dion2_step_groups.restype = c_int
     lib.dion2_workspace_size.argtypes = [c_int, i64, i64, c_float, c_int]
     lib.dion2_workspace_size.restype = c_size_t
     lib.dion2_plan_info.argtypes = [i64, i64, c_float, c_int, POINTER(c_int64), POINTER(c_int)]
@@ -247,6 +264,67 @@ def dion2_step_ex(W, M, G, alpha, mu=0.95, lr=0.02, ns_steps=5, axis=AXIS_AUTO, 
     _check(lib.dion2_step_ex(W.data_ptr(), M.data_ptr(), G.data_ptr(), batch, rows, cols, alpha,
                              mu, lr, ns_steps, axis, ctypes.byref(opt),
                              _stream_ptr(stream, W.device)))
+
+
+def _options(W, G, ns_steps, ns_coeffs, ns_eps, decay_all, ns_form, select_rule, rand_seed,
+             rand_step, rand_matrix0):
+    """Options struct (and the coefficient buffer it points to, kept alive by the caller)."""
+    lib = load()
+    opt = Options()
+    lib.dion2_options_init(ctypes.byref(opt))
+    opt.w_dtype = _DT[W.dtype]
+    opt.g_dtype = _DT[G.dtype]
+    coeff_buf = None
+    if ns_coeffs is not None:
+        flat = [float(v) for abc in ns_coeffs for v in abc]
+        if len(flat) < 3 * ns_steps:
+            raise ValueError("ns_coeffs needs one (a, b, c) per Newton-Schulz step")
+        coeff_buf = (c_float * len(flat))(*flat)
+        opt.ns_coeffs = ctypes.cast(coeff_buf, POINTER(c_float))
+    opt.ns_eps = ns_eps
+    opt.decay_all = 1 if decay_all else 0
+    opt.ns_form = ns_form
+    opt.select_rule = select_rule
+    opt.rand_seed = rand_seed
+    opt.rand_step = rand_step
+    opt.rand_matrix0 = rand_matrix0
+    return opt, coeff_buf
+
+
+def dion2_step_groups(groups, alpha, mu=0.95, lr=0.02, ns_steps=5, *, ns_coeffs=None,
+                      ns_eps=1e-7, decay_all=False, ns_form=NS_AUTO, select_rule=SELECT_L1,
+                      rand_seed=0, rand_step=0, rand_matrix0=0, group_streams=0, stream=None):
+    """Several same-shape stacks in one call: groups is a list of (W, M, G, axis)
+    with W, M, G [batch, rows, cols] on one device, W and G of one dtype pair
+    across groups. Bitwise the result of dion2_step_ex per group; groups of one
+    padded Newton-Schulz size share their chain of s x s products."""
+    if not groups:
+        raise ValueError("groups must be a non-empty list")
+    arr = (Group * len(groups))()
+    for i, (W, M, G, axis) in enumerate(groups):
+        _mats(W, M, G, 3)
+        if W.dtype != groups[0][0].dtype or G.dtype != groups[0][2].dtype:
+            raise ValueError("every group must have the same W and G dtypes")
+        if W.device != groups[0][0].device:
+            raise ValueError("every group must be on one device")
+        arr[i] = Group(W.data_ptr(), M.data_ptr(), G.data_ptr(), W.shape[0], W.shape[1],
+                       W.shape[2], axis)
+    W0, _, G0, _ = groups[0]
+    opt, keep = _options(W0, G0, ns_steps, ns_coeffs, ns_eps, decay_all, ns_form, select_rule,
+                         rand_seed, rand_step, rand_matrix0)
+    opt.group_streams = group_streams
+    lib = load()
+    _check(lib.dion2_step_groups(arr, len(groups), alpha, mu, lr, ns_steps, ctypes.byref(opt),
+                                 _stream_ptr(stream, W0.device)))
+    del keep
+
+
+def dion2_step_groups_raw(group_array, ngroups, alpha, mu, lr, ns_steps, opt, stream):
+    """The C call as is (for argument-validation tests): a ctypes Group array or
+    None, an Options or None, a stream pointer."""
+    lib = load()
+    return lib.dion2_step_groups(group_array, ngroups, alpha, mu, lr, ns_steps,
+                                 ctypes.byref(opt) if opt is not None else None, stream)
 
 
 def dion2_workspace_size(batch, rows, cols, alpha, axis=AXIS_AUTO) -> int:

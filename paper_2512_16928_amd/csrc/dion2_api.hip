@@ -68,7 +68,10 @@ struct Plan {
 enum { SQ_AHI, SQ_ALO, SQ_B, SQ_DIRECT_COUNT = 3 };
 enum { SQ_QHI = 2, SQ_QLO, SQ_THI, SQ_TLO, SQ_P0HI, SQ_P0LO, SQ_P1HI, SQ_P1LO, SQ_GRAM_COUNT };
 
-int make_plan(int batch, int64_t rows, int64_t cols, float alpha, int axis, int ns_form, Plan* p) {
+// own_sq = false leaves out the s x s buffers (a grouped call carves them
+// once for every group of a shared Newton-Schulz chain).
+int make_plan(int batch, int64_t rows, int64_t cols, float alpha, int axis, int ns_form, Plan* p,
+              bool own_sq = true) {
     if (batch < 1 || batch > 65535) return fail(DION2_ERR_INVALID_ARG, "batch %d not in [1, 65535]", batch);
     if (rows < 1 || cols < 1)
         return fail(DION2_ERR_INVALID_ARG, "rows (%lld) and cols (%lld) must be >= 1",
@@ -119,7 +122,7 @@ int make_plan(int batch, int64_t rows, int64_t cols, float alpha, int axis, int 
     P.o_Z = take(comp);
     P.o_Z1 = take(P.gram ? 0 : comp);
     P.S_bytes = align256(B * (size_t)P.s_pad * (size_t)P.s_pad * 2);
-    P.o_S = take(P.S_bytes * (P.gram ? SQ_GRAM_COUNT : SQ_DIRECT_COUNT));
+    P.o_S = take(own_sq ? P.S_bytes * (P.gram ? SQ_GRAM_COUNT : SQ_DIRECT_COUNT) : 0);
     P.o_O = take(B * (size_t)P.kpad * (size_t)P.opad * 4);
     P.o_tables = take(3 * B * sizeof(void*));
     P.total = off;
@@ -135,8 +138,27 @@ struct Workspace {
     size_t pinned_count = 0;
     hipEvent_t tables_done = nullptr;
     bool tables_pending = false;
+    std::vector<hipStream_t> aux;  // grouped calls: streams the groups run on
+    std::vector<hipEvent_t> ev;    // grouped calls: fork / dependency / join events
     std::mutex use;                // serialises host threads sharing a stream
 };
+
+// At least n auxiliary streams (default priority) and m events.
+int ensure_aux(Workspace* w, int n, int m) {
+    while ((int)w->aux.size() < n) {
+        hipStream_t s = nullptr;
+        hipError_t e = hipStreamCreateWithFlags(&s, hipStreamNonBlocking);
+        if (e != hipSuccess) return hip_fail(e, "hipStreamCreateWithFlags");
+        w->aux.push_back(s);
+    }
+    while ((int)w->ev.size() < m) {
+        hipEvent_t ev = nullptr;
+        hipError_t e = hipEventCreateWithFlags(&ev, hipEventDisableTiming);
+        if (e != hipSuccess) return hip_fail(e, "hipEventCreateWithFlags");
+        w->ev.push_back(ev);
+    }
+    return DION2_OK;
+}
 
 std::mutex g_ws_mutex;
 std::map<std::pair<int, hipStream_t>, Workspace*> g_ws;
@@ -387,56 +409,79 @@ hipError_t ns_direct(const Plan& P, uint16_t* Z0, uint16_t* Z1, uint16_t* const*
 
 // GRAM: A_0 = Z Z^T; per step Q_t = a I + b A_t + c A_t^2, P <- Q_t P and
 // A_{t+1} = Q_t (Q_t A_t); finally O = P Z. Every s x s matrix is a
-// polynomial in A_0, hence symmetric, and all of them commute.
-hipError_t ns_gram(const Plan& P, const uint16_t* Z, uint16_t* const* sq, float* O, int ns_steps,
-                   const dion2_options& opt, const FinalSpec& fin, hipStream_t stream) {
+// polynomial in A_0, hence symmetric, and all of them commute. The three
+// parts are separate so that a grouped call can run the chain of s x s
+// products once for several groups of the same padded size.
+
+// A_0 = Z Z^T as a hi / lo pair
+hipError_t gram_a0(const Plan& P, const uint16_t* Z, uint16_t* Ah, uint16_t* Al, hipStream_t stream) {
     const double s_r = (double)(P.k < P.d_oth ? P.k : P.d_oth);
     const double l_r = (double)(P.k < P.d_oth ? P.d_oth : P.k);
     const double nb = (double)P.batch;
-    const double f3 = 3.0 * sym_flops(s_r, s_r) * nb;
-    const double gram_bytes = (2.0 * s_r * l_r + 4.0 * s_r * s_r) * nb;
+    const double gram_bytes = (2.0 * s_r * l_r + 4.0 * s_r * s_r) * nb;   // Z in, A hi + lo out
+    GemmArgs g = gram_args(P, Z, Ah, Al);
+    return timed(DION2_PHASE_NS_GRAM, sym_flops(s_r, l_r) * nb, gram_bytes, 1, stream,
+                 [&] { return launch_gemm(g, EPI_SPLIT, 1, stream); });
+}
+
+// Work of one group's s x s products, for the profiler. Per step: Q_t (from
+// A: hi + lo in and out, 8 s^2 bytes), P <- Q_t P and T = Q_t A (one dual
+// launch when both are due; each product two hi/lo operands in and one out,
+// 12 s^2, less the shared Q_t's 4 s^2 when fused), A <- Q_t T (12 s^2).
+struct ChainCost {
+    double flops = 0.0, bytes = 0.0;
+};
+int chain_products(int ns_steps) { return ns_steps + 3 * (ns_steps - 1); }
+int chain_launches(int ns_steps) { return ns_steps == 1 ? 1 : 3 * ns_steps - 1; }
+ChainCost chain_cost(const Plan& P, int ns_steps) {
+    const double s_r = (double)(P.k < P.d_oth ? P.k : P.d_oth);
+    const double nb = (double)P.batch;
+    const int nprod = chain_products(ns_steps);
+    const int ndual = ns_steps >= 3 ? ns_steps - 2 : 0;
+    ChainCost c;
+    c.flops = 3.0 * sym_flops(s_r, s_r) * nb * nprod;
+    c.bytes = (8.0 * ns_steps + 12.0 * (nprod - ns_steps) - 4.0 * ndual) * s_r * s_r * nb;
+    return c;
+}
+
+// The s x s products of `batch` matrices of padded side s_pad (buffers sq,
+// each [batch][s_pad][s_pad], A_0 in sq[SQ_AHI / SQ_ALO]). *cur_out tells
+// which P pair holds the product of the Q_t: SQ_P0* (0) or SQ_P1* (1).
+hipError_t gram_chain(int batch, int64_t s_pad, uint16_t* const* sq, int ns_steps,
+                      const dion2_options& opt, const ChainCost& cost, hipStream_t stream,
+                      int* cur_out) {
+    Plan C{};
+    C.batch = batch;
+    C.s_pad = s_pad;
     uint16_t* Ah = sq[SQ_AHI];
     uint16_t* Al = sq[SQ_ALO];
     uint16_t* Ph[2] = {sq[SQ_P0HI], sq[SQ_P1HI]};
     uint16_t* Pl[2] = {sq[SQ_P0LO], sq[SQ_P1LO]};
     int cur = 0;
-
-    GemmArgs g = gram_args(P, Z, Ah, Al);
-    hipError_t e = timed(DION2_PHASE_NS_GRAM, sym_flops(s_r, l_r) * nb, gram_bytes, 1, stream,
-                         [&] { return launch_gemm(g, EPI_SPLIT, 1, stream); });
-    if (e != hipSuccess) return e;
-    // The s x s products run back to back and are timed as one span. Per
-    // step: Q_t (from A: hi + lo in and out, 8 s^2 bytes), P <- Q_t P and
-    // T = Q_t A (one dual launch when both are due; each product two hi/lo
-    // operands in and one out, 12 s^2, less the shared Q_t's 4 s^2 when
-    // fused), A <- Q_t T (12 s^2).
-    const int nprod = ns_steps + 3 * (ns_steps - 1);
-    const int ndual = ns_steps >= 3 ? ns_steps - 2 : 0;
-    const int nlaunch = ns_steps == 1 ? 1 : 3 * ns_steps - 1;
-    const double sq_bytes =
-        (8.0 * ns_steps + 12.0 * (nprod - ns_steps) - 4.0 * ndual) * s_r * s_r * nb;
-    e = timed(DION2_PHASE_NS_POLY, f3 * nprod, sq_bytes, nlaunch, stream, [&]() -> hipError_t {
+    // the products run back to back and are timed as one span
+    hipError_t e = timed(DION2_PHASE_NS_POLY, cost.flops, cost.bytes, chain_launches(ns_steps), stream,
+                         [&]() -> hipError_t {
         for (int t = 0; t < ns_steps; ++t) {
             const float* cf = opt.ns_coeffs ? opt.ns_coeffs + 3 * t : kMuonQuintic;
             // Q_t; the first one is P itself
             uint16_t* qh = t == 0 ? Ph[0] : sq[SQ_QHI];
             uint16_t* ql = t == 0 ? Pl[0] : sq[SQ_QLO];
-            GemmArgs q = sym3_args(P, Ah, Al, Ah, Al, qh, ql);
+            GemmArgs q = sym3_args(C, Ah, Al, Ah, Al, qh, ql);
             q.ca = cf[0];
             q.cb = cf[1];
             q.cc = cf[2];
             q.E0 = Ah;
             q.E1 = Al;
-            q.sE = P.s_pad * P.s_pad;
-            q.lde = (int)P.s_pad;
+            q.sE = C.s_pad * C.s_pad;
+            q.lde = (int)C.s_pad;
             hipError_t r = launch_gemm(q, EPI_QPOLY, 3, stream);
             if (r != hipSuccess) return r;
             // P <- Q_t P (t > 0) and T = Q_t A (t < T - 1) share Q_t: one
             // launch when both are due
             const bool do_p = t > 0, do_t = t + 1 < ns_steps;
             if (do_p || do_t) {
-                GemmArgs u = do_p ? sym3_args(P, qh, ql, Ph[cur], Pl[cur], Ph[1 - cur], Pl[1 - cur])
-                                  : sym3_args(P, qh, ql, Ah, Al, sq[SQ_THI], sq[SQ_TLO]);
+                GemmArgs u = do_p ? sym3_args(C, qh, ql, Ph[cur], Pl[cur], Ph[1 - cur], Pl[1 - cur])
+                                  : sym3_args(C, qh, ql, Ah, Al, sq[SQ_THI], sq[SQ_TLO]);
                 if (do_p && do_t) {
                     u.dual = 1;
                     u.B0x = Ah;
@@ -449,16 +494,24 @@ hipError_t ns_gram(const Plan& P, const uint16_t* Z, uint16_t* const* sq, float*
                 if (do_p) cur = 1 - cur;
             }
             if (do_t) {   // A <- Q_t T
-                GemmArgs v = sym3_args(P, qh, ql, sq[SQ_THI], sq[SQ_TLO], Ah, Al);
+                GemmArgs v = sym3_args(C, qh, ql, sq[SQ_THI], sq[SQ_TLO], Ah, Al);
                 r = launch_gemm(v, EPI_SPLIT, 3, stream);
                 if (r != hipSuccess) return r;
             }
         }
         return hipSuccess;
     });
-    if (e != hipSuccess) return e;
-    // O = (P_hi + P_lo) Z
-    GemmArgs x = right_args(P, Ph[cur], Pl[cur], Z);
+    *cur_out = cur;
+    return e;
+}
+
+// O = (P_hi + P_lo) Z, or the update step applied in the epilogue
+hipError_t gram_final(const Plan& P, const uint16_t* Ph, const uint16_t* Pl, const uint16_t* Z,
+                      float* O, const FinalSpec& fin, hipStream_t stream) {
+    const double s_r = (double)(P.k < P.d_oth ? P.k : P.d_oth);
+    const double l_r = (double)(P.k < P.d_oth ? P.d_oth : P.k);
+    const double nb = (double)P.batch;
+    GemmArgs x = right_args(P, Ph, Pl, Z);
     const GemmEpi epi = final_output(P, x, O, fin);
     // P hi + lo and Z in, O (or W's selected lines, read and written) out
     const double fbytes = (4.0 * s_r * s_r + 6.0 * s_r * l_r) * nb;
@@ -466,7 +519,185 @@ hipError_t ns_gram(const Plan& P, const uint16_t* Z, uint16_t* const* sq, float*
                  [&] { return launch_gemm(x, epi, 2, stream); });
 }
 
+hipError_t ns_gram(const Plan& P, const uint16_t* Z, uint16_t* const* sq, float* O, int ns_steps,
+                   const dion2_options& opt, const FinalSpec& fin, hipStream_t stream) {
+    hipError_t e = gram_a0(P, Z, sq[SQ_AHI], sq[SQ_ALO], stream);
+    if (e != hipSuccess) return e;
+    int cur = 0;
+    e = gram_chain(P.batch, P.s_pad, sq, ns_steps, opt, chain_cost(P, ns_steps), stream, &cur);
+    if (e != hipSuccess) return e;
+    return gram_final(P, cur ? sq[SQ_P1HI] : sq[SQ_P0HI], cur ? sq[SQ_P1LO] : sq[SQ_P0LO], Z, O, fin,
+                      stream);
+}
+
 // ------------------------------------------------------------------ step
+
+// Device buffers of one group's step, carved from its workspace region.
+struct Bufs {
+    double* l1;
+    double* sq;
+    int32_t* sel;
+    int32_t* rank;
+    double* scale;
+    uint16_t* Z0;   // compact matrix in its wide orientation: L [kpad][opad] or L^T [opad][kpad]
+    uint16_t* Z1;
+    uint16_t* sbuf[SQ_GRAM_COUNT];   // s x s buffers (null when a shared chain owns them)
+    float* O;
+    double* part;
+};
+
+Bufs carve(const Plan& P, char* ws) {
+    Bufs b{};
+    b.l1 = reinterpret_cast<double*>(ws + P.o_l1);
+    b.sq = reinterpret_cast<double*>(ws + P.o_sq);
+    b.sel = reinterpret_cast<int32_t*>(ws + P.o_sel);
+    b.rank = P.axis == 1 ? reinterpret_cast<int32_t*>(ws + P.o_rank) : nullptr;
+    b.scale = reinterpret_cast<double*>(ws + P.o_scale);
+    b.Z0 = reinterpret_cast<uint16_t*>(ws + P.o_Z);
+    b.Z1 = reinterpret_cast<uint16_t*>(ws + P.o_Z1);
+    for (int i = 0; i < SQ_GRAM_COUNT; ++i)
+        b.sbuf[i] = reinterpret_cast<uint16_t*>(ws + P.o_S + (size_t)i * P.S_bytes);
+    b.O = reinterpret_cast<float*>(ws + P.o_O);
+    b.part = reinterpret_cast<double*>(ws + P.o_part);
+    return b;
+}
+
+// Bytes each phase must move as designed. Rows: K1 reads M, G and writes M;
+// K3 reads and writes the selected rows of M and writes the compact bf16
+// copy; K5 reads O and reads and writes the selected rows of W. Columns
+// (selected columns touch every cache line of a row): K1 only reads M and
+// G; K3 reads M, G and writes M whole, plus the compact copy; K5 reads O and
+// reads and writes W whole.
+struct PhaseBytes {
+    double k1, k3, k5;
+};
+PhaseBytes phase_bytes(const Plan& P, const dion2_options& opt) {
+    const double n_el = (double)P.batch * (double)P.rows * (double)P.cols;
+    const double g_bytes = opt.g_dtype == DION2_DTYPE_BF16 ? 2.0 : 4.0;
+    const double w_bytes = opt.w_dtype == DION2_DTYPE_BF16 ? 2.0 : 4.0;
+    const double sel_el = (double)P.batch * (double)P.k * (double)P.d_oth;
+    const bool cm = P.axis == 1;
+    PhaseBytes pb;
+    pb.k1 = n_el * ((cm ? 4.0 : 8.0) + g_bytes);
+    pb.k3 = (cm ? n_el * (8.0 + g_bytes) : sel_el * 8.0) + sel_el * 2.0;
+    pb.k5 = (cm ? n_el : sel_el) * 2.0 * w_bytes + sel_el * 4.0;
+    return pb;
+}
+
+// K1 momentum and line norms, K2 selection, K3 gather and decay.
+int front(const Plan& P, const MatSet& ms, const Bufs& b, float mu, int ns_steps,
+          const dion2_options& opt, hipStream_t stream) {
+    const PhaseBytes pb = phase_bytes(P, opt);
+    const bool cm = P.axis == 1;
+    MomentumArgs ma{};
+    ma.ms = ms;
+    ma.rows = P.rows;
+    ma.cols = P.cols;
+    ma.batch = P.batch;
+    ma.l1 = b.l1;
+    ma.sq = b.sq;
+    ma.part = b.part;
+    ma.rb_rows = P.rb_rows;
+    ma.nrb = P.nrb;
+    ma.mu = mu;
+    hipError_t e = timed(DION2_PHASE_MOMENTUM, 0.0, pb.k1, P.axis == 0 ? 1 : 2, stream,
+                         [&] { return launch_momentum(ma, P.axis, opt.g_dtype == DION2_DTYPE_BF16, stream); });
+    if (e != hipSuccess) return hip_fail(e, "launch K1 momentum");
+
+    SelectArgs sa{};
+    sa.l1 = b.l1;
+    sa.sq = b.sq;
+    sa.d_sel = (int)P.d_sel;
+    sa.k = (int)P.k;
+    sa.batch = P.batch;
+    sa.eps = (double)opt.ns_eps;
+    sa.sel = b.sel;
+    sa.scale = b.scale;
+    sa.rank = b.rank;
+    sa.rule = opt.select_rule;
+    sa.seed = opt.rand_seed;
+    sa.step = opt.rand_step;
+    sa.matrix0 = opt.rand_matrix0;
+    e = timed(DION2_PHASE_SELECT, 0.0, (double)P.batch * (double)P.d_sel * 16.0, 1, stream,
+              [&] { return launch_select(sa, stream); });
+    if (e != hipSuccess) return hip_fail(e, "launch K2 select");
+
+    GatherArgs ga{};
+    ga.ms = ms;
+    ga.rows = P.rows;
+    ga.cols = P.cols;
+    ga.batch = P.batch;
+    ga.k = (int)P.k;
+    ga.d_oth = (int)P.d_oth;
+    ga.kpad = (int)P.kpad;
+    ga.opad = (int)P.opad;
+    ga.sel = b.sel;
+    ga.rank = b.rank;
+    ga.scale = b.scale;
+    ga.mu = mu;
+    // rows: selective decay here, decay-all by its own pass; columns: both here
+    ga.decay = cm ? (opt.decay_all ? 2 : 1) : (opt.decay_all ? 0 : 1);
+    ga.L = P.z_is_L ? b.Z0 : nullptr;
+    ga.LT = P.z_is_L ? nullptr : b.Z0;
+    ga.O = ns_steps == 0 ? b.O : nullptr;
+    e = timed(DION2_PHASE_GATHER, 0.0, pb.k3, 1, stream,
+              [&] { return launch_gather(ga, P.axis, opt.g_dtype == DION2_DTYPE_BF16, stream); });
+    if (e != hipSuccess) return hip_fail(e, "launch K3 gather");
+    if (opt.decay_all && !cm) {
+        DecayAllArgs da{ms, P.rows, P.cols, P.batch, mu};
+        e = launch_decay_all(da, stream);
+        if (e != hipSuccess) return hip_fail(e, "launch decay-all");
+    }
+    return DION2_OK;
+}
+
+// Whether the final Newton-Schulz product applies the update itself (row
+// selection with O in the L layout and bf16 W), and its operands.
+FinalSpec make_final(const Plan& P, const MatSet& ms, const Bufs& b, float lr, int ns_steps,
+                     const dion2_options& opt) {
+    FinalSpec fin{};
+    fin.lr_eff = (double)lr * std::sqrt((double)P.rows / (double)P.cols);
+    fin.fuse = ns_steps > 0 && P.axis == 0 && P.z_is_L && opt.w_dtype == DION2_DTYPE_BF16 &&
+               P.cols % 8 == 0 && P.cols >= 16;
+    fin.ms = ms;
+    fin.sel = b.sel;
+    fin.dbg = opt.dbg_update;
+    return fin;
+}
+
+// K5 (unless fused into the final product) and the debug copies.
+int back(const Plan& P, const MatSet& ms, const Bufs& b, const FinalSpec& fin,
+         const dion2_options& opt, hipStream_t stream) {
+    hipError_t e;
+    if (!fin.fuse) {
+        ApplyArgs aa{};
+        aa.ms = ms;
+        aa.rows = P.rows;
+        aa.cols = P.cols;
+        aa.batch = P.batch;
+        aa.k = (int)P.k;
+        aa.d_oth = (int)P.d_oth;
+        aa.kpad = (int)P.kpad;
+        aa.opad = (int)P.opad;
+        aa.sel = b.sel;
+        aa.rank = b.rank;
+        aa.O = b.O;
+        aa.lr_eff = fin.lr_eff;
+        aa.dbg = opt.dbg_update;
+        e = timed(DION2_PHASE_APPLY, 0.0, phase_bytes(P, opt).k5, 1, stream,
+                  [&] { return launch_apply(aa, P.axis, opt.w_dtype == DION2_DTYPE_BF16, stream); });
+        if (e != hipSuccess) return hip_fail(e, "launch K5 apply");
+    }
+    if (opt.dbg_sel_idx) {
+        e = hipMemcpyAsync(opt.dbg_sel_idx, b.sel, (size_t)P.batch * P.k * 4, hipMemcpyDeviceToDevice, stream);
+        if (e != hipSuccess) return hip_fail(e, "copy dbg_sel_idx");
+    }
+    if (opt.dbg_norms) {
+        e = hipMemcpyAsync(opt.dbg_norms, b.l1, (size_t)P.batch * P.d_sel * 8, hipMemcpyDeviceToDevice, stream);
+        if (e != hipSuccess) return hip_fail(e, "copy dbg_norms");
+    }
+    return DION2_OK;
+}
 
 struct Tables {
     void* const* W;
@@ -550,140 +781,16 @@ int run_step(const Plan& P, void* W, float* M, const void* G, const Tables* tabs
         ms.G = G;
     }
 
-    double* l1 = reinterpret_cast<double*>(ws + P.o_l1);
-    double* sq = reinterpret_cast<double*>(ws + P.o_sq);
-    int32_t* sel = reinterpret_cast<int32_t*>(ws + P.o_sel);
-    int32_t* rank = P.axis == 1 ? reinterpret_cast<int32_t*>(ws + P.o_rank) : nullptr;
-    double* scale = reinterpret_cast<double*>(ws + P.o_scale);
-    // compact matrix in its wide orientation: L [kpad][opad] or L^T [opad][kpad]
-    uint16_t* Z0 = reinterpret_cast<uint16_t*>(ws + P.o_Z);
-    uint16_t* Z1 = reinterpret_cast<uint16_t*>(ws + P.o_Z1);
-    uint16_t* sbuf[SQ_GRAM_COUNT];
-    for (int i = 0; i < SQ_GRAM_COUNT; ++i)
-        sbuf[i] = reinterpret_cast<uint16_t*>(ws + P.o_S + (size_t)i * P.S_bytes);
-    float* O = reinterpret_cast<float*>(ws + P.o_O);
-
-    // K1
-    MomentumArgs ma{};
-    ma.ms = ms;
-    ma.rows = P.rows;
-    ma.cols = P.cols;
-    ma.batch = P.batch;
-    ma.l1 = l1;
-    ma.sq = sq;
-    ma.part = reinterpret_cast<double*>(ws + P.o_part);
-    ma.rb_rows = P.rb_rows;
-    ma.nrb = P.nrb;
-    ma.mu = mu;
-    const double n_el = (double)P.batch * (double)P.rows * (double)P.cols;
-    const double g_bytes = opt.g_dtype == DION2_DTYPE_BF16 ? 2.0 : 4.0;
-    const double w_bytes = opt.w_dtype == DION2_DTYPE_BF16 ? 2.0 : 4.0;
-    const double sel_el = (double)P.batch * (double)P.k * (double)P.d_oth;
-    // Bytes each phase must move as designed. Rows: K1 reads M, G and writes
-    // M; K3 reads and writes the selected rows of M and writes the compact
-    // bf16 copy; K5 reads O and reads and writes the selected rows of W.
-    // Columns (selected columns touch every cache line of a row): K1 only
-    // reads M and G; K3 reads M, G and writes M whole, plus the compact copy;
-    // K5 reads O and reads and writes W whole.
-    const bool cm = P.axis == 1;
-    const double k1_bytes = n_el * ((cm ? 4.0 : 8.0) + g_bytes);
-    const double k3_bytes = (cm ? n_el * (8.0 + g_bytes) : sel_el * 8.0) + sel_el * 2.0;
-    const double k5_bytes = (cm ? n_el : sel_el) * 2.0 * w_bytes + sel_el * 4.0;
-    e = timed(DION2_PHASE_MOMENTUM, 0.0, k1_bytes, P.axis == 0 ? 1 : 2, stream,
-              [&] { return launch_momentum(ma, P.axis, opt.g_dtype == DION2_DTYPE_BF16, stream); });
-    if (e != hipSuccess) return hip_fail(e, "launch K1 momentum");
-
-    // K2
-    SelectArgs sa{};
-    sa.l1 = l1;
-    sa.sq = sq;
-    sa.d_sel = (int)P.d_sel;
-    sa.k = (int)P.k;
-    sa.batch = P.batch;
-    sa.eps = (double)opt.ns_eps;
-    sa.sel = sel;
-    sa.scale = scale;
-    sa.rank = rank;
-    sa.rule = opt.select_rule;
-    sa.seed = opt.rand_seed;
-    sa.step = opt.rand_step;
-    sa.matrix0 = opt.rand_matrix0;
-    e = timed(DION2_PHASE_SELECT, 0.0, (double)P.batch * (double)P.d_sel * 16.0, 1, stream,
-              [&] { return launch_select(sa, stream); });
-    if (e != hipSuccess) return hip_fail(e, "launch K2 select");
-
-    // K3
-    GatherArgs ga{};
-    ga.ms = ms;
-    ga.rows = P.rows;
-    ga.cols = P.cols;
-    ga.batch = P.batch;
-    ga.k = (int)P.k;
-    ga.d_oth = (int)P.d_oth;
-    ga.kpad = (int)P.kpad;
-    ga.opad = (int)P.opad;
-    ga.sel = sel;
-    ga.rank = rank;
-    ga.scale = scale;
-    ga.mu = mu;
-    // rows: selective decay here, decay-all by its own pass; columns: both here
-    ga.decay = cm ? (opt.decay_all ? 2 : 1) : (opt.decay_all ? 0 : 1);
-    ga.L = P.z_is_L ? Z0 : nullptr;
-    ga.LT = P.z_is_L ? nullptr : Z0;
-    ga.O = ns_steps == 0 ? O : nullptr;
-    e = timed(DION2_PHASE_GATHER, 0.0, k3_bytes, 1, stream,
-              [&] { return launch_gather(ga, P.axis, opt.g_dtype == DION2_DTYPE_BF16, stream); });
-    if (e != hipSuccess) return hip_fail(e, "launch K3 gather");
-    if (opt.decay_all && !cm) {
-        DecayAllArgs da{ms, P.rows, P.cols, P.batch, mu};
-        e = launch_decay_all(da, stream);
-        if (e != hipSuccess) return hip_fail(e, "launch decay-all");
-    }
-
-    // K4: Newton-Schulz
-    FinalSpec fin{};
-    fin.lr_eff = (double)lr * std::sqrt((double)P.rows / (double)P.cols);
-    fin.fuse = ns_steps > 0 && P.axis == 0 && P.z_is_L && opt.w_dtype == DION2_DTYPE_BF16 &&
-               P.cols % 8 == 0 && P.cols >= 16;
-    fin.ms = ms;
-    fin.sel = sel;
-    fin.dbg = opt.dbg_update;
+    Bufs b = carve(P, ws);
+    int st = front(P, ms, b, mu, ns_steps, opt, stream);
+    if (st != DION2_OK) return st;
+    const FinalSpec fin = make_final(P, ms, b, lr, ns_steps, opt);
     if (ns_steps > 0) {   // with no step the gather has written O
-        e = P.gram ? ns_gram(P, Z0, sbuf, O, ns_steps, opt, fin, stream)
-                   : ns_direct(P, Z0, Z1, sbuf, O, ns_steps, opt, fin, stream);
+        e = P.gram ? ns_gram(P, b.Z0, b.sbuf, b.O, ns_steps, opt, fin, stream)
+                   : ns_direct(P, b.Z0, b.Z1, b.sbuf, b.O, ns_steps, opt, fin, stream);
+        if (e != hipSuccess) return hip_fail(e, "launch K4 Newton-Schulz");
     }
-    if (e != hipSuccess) return hip_fail(e, "launch K4 Newton-Schulz");
-
-    // K5
-    ApplyArgs aa{};
-    aa.ms = ms;
-    aa.rows = P.rows;
-    aa.cols = P.cols;
-    aa.batch = P.batch;
-    aa.k = (int)P.k;
-    aa.d_oth = (int)P.d_oth;
-    aa.kpad = (int)P.kpad;
-    aa.opad = (int)P.opad;
-    aa.sel = sel;
-    aa.rank = rank;
-    aa.O = O;
-    aa.lr_eff = fin.lr_eff;
-    aa.dbg = opt.dbg_update;
-    if (!fin.fuse) {   // otherwise the final Newton-Schulz product has applied it
-        e = timed(DION2_PHASE_APPLY, 0.0, k5_bytes, 1, stream,
-                  [&] { return launch_apply(aa, P.axis, opt.w_dtype == DION2_DTYPE_BF16, stream); });
-        if (e != hipSuccess) return hip_fail(e, "launch K5 apply");
-    }
-
-    if (opt.dbg_sel_idx) {
-        e = hipMemcpyAsync(opt.dbg_sel_idx, sel, (size_t)P.batch * P.k * 4, hipMemcpyDeviceToDevice, stream);
-        if (e != hipSuccess) return hip_fail(e, "copy dbg_sel_idx");
-    }
-    if (opt.dbg_norms) {
-        e = hipMemcpyAsync(opt.dbg_norms, l1, (size_t)P.batch * P.d_sel * 8, hipMemcpyDeviceToDevice, stream);
-        if (e != hipSuccess) return hip_fail(e, "copy dbg_norms");
-    }
-    return DION2_OK;
+    return back(P, ms, b, fin, opt, stream);
 }
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
@@ -750,6 +857,233 @@ int step_impl(void* W, float* M, const void* G, const Tables* tabs, int batch, i
     return run_step(P, W, M, G, tabs, mu, lr, ns_steps, opt, static_cast<hipStream_t>(stream));
 }
 
+// Several same-shape groups in one call. Each group runs K1-K3 in its own
+// workspace region; the groups in the GRAM form are gathered into chains by
+// padded s (one chain per size) whose s x s buffers hold all their matrices
+// back to back, so every product of the chain is one launch for all of
+// them; then each group's final product and K5 run. DIRECT groups run
+// whole in the first pass. Per matrix the arithmetic is that of a call per
+// group (every kernel treats the matrices of a batch independently).
+constexpr int kMaxGroups = 64;
+constexpr int kMaxGroupStreams = 8;
+constexpr int kDefaultGroupStreams = 4;
+// Groups share a chain only while one product of theirs has fewer
+// output tiles than this (two per compute unit).
+constexpr int64_t kChainShareTiles = 512;
+
+int groups_impl(const dion2_group* groups, int ngroups, float alpha, float mu, float lr,
+                int ns_steps, const dion2_options* opt_in, hipStream_t stream) {
+    dion2_options opt;
+    if (opt_in) opt = *opt_in;
+    else dion2_options_init(&opt);
+    if (!groups) return fail(DION2_ERR_INVALID_ARG, "groups must not be NULL");
+    if (ngroups < 1 || ngroups > kMaxGroups)
+        return fail(DION2_ERR_INVALID_ARG, "ngroups %d not in [1, %d]", ngroups, kMaxGroups);
+    if (opt.workspace)
+        return fail(DION2_ERR_INVALID_ARG, "grouped calls use the library workspace (workspace must be NULL)");
+    if (opt.dbg_sel_idx || opt.dbg_norms || opt.dbg_update)
+        return fail(DION2_ERR_INVALID_ARG, "grouped calls take no debug outputs");
+    if (opt.group_streams < 0 || opt.group_streams > kMaxGroupStreams)
+        return fail(DION2_ERR_INVALID_ARG, "group_streams %d not in [0, %d]", opt.group_streams,
+                    kMaxGroupStreams);
+    int st = validate_common(mu, lr, ns_steps, opt);
+    if (st != DION2_OK) return st;
+
+    struct Chain {
+        int64_t s_pad;
+        int batch = 0;
+        size_t off = 0, S_bytes = 0;
+    };
+    std::vector<Plan> plans(ngroups);
+    std::vector<int> chain_of(ngroups, -1);
+    std::vector<int> chain_pos(ngroups, 0);   // first matrix of the group in its chain
+    std::vector<Chain> chains;
+    int64_t total_batch = 0;
+    for (int g = 0; g < ngroups; ++g) {
+        const dion2_group& G = groups[g];
+        Plan P;
+        st = make_plan(G.batch, G.rows, G.cols, alpha, G.axis, opt.ns_form, &P);
+        if (st != DION2_OK) return fail(st, "group %d: %s", g, g_last_error.c_str());
+        if (!G.W || !G.M || !G.G) return fail(DION2_ERR_INVALID_ARG, "group %d: W, M and G must not be NULL", g);
+        if (!aligned16(G.W) || !aligned16(G.M) || !aligned16(G.G))
+            return fail(DION2_ERR_INVALID_ARG, "group %d: W, M and G must be 16-byte aligned", g);
+        // A group whose s x s products alone fill the chip keeps its own
+        // chain (and can overlap the other groups); smaller ones share.
+        const int64_t st_tiles = P.s_pad / kTile;
+        const bool small = (int64_t)P.batch * st_tiles * (st_tiles + 1) / 2 < kChainShareTiles;
+        if (P.gram && ns_steps > 0 && small) {
+            int c = 0;
+            while (c < (int)chains.size() && chains[c].s_pad != P.s_pad) ++c;
+            if (c == (int)chains.size()) {
+                chains.push_back(Chain{});
+                chains[c].s_pad = P.s_pad;
+            }
+            chain_of[g] = c;
+            chain_pos[g] = chains[c].batch;
+            chains[c].batch += P.batch;
+            make_plan(G.batch, G.rows, G.cols, alpha, G.axis, opt.ns_form, &P, false);
+        }
+        plans[g] = P;
+        total_batch += G.batch;
+    }
+    if (opt.select_rule == DION2_SELECT_RANDOM &&
+        (opt.rand_matrix0 < 0 || opt.rand_matrix0 + total_batch > (int64_t(1) << 32)))
+        return fail(DION2_ERR_INVALID_ARG, "rand_matrix0 %lld with %lld matrices leaves [0, 2^32)",
+                    (long long)opt.rand_matrix0, (long long)total_batch);
+    for (const Chain& c : chains)
+        if (c.batch > 65535) return fail(DION2_ERR_INVALID_ARG, "more than 65535 matrices share one chain");
+
+    // one workspace: the groups' regions, then the chains' s x s buffers
+    std::vector<size_t> goff(ngroups);
+    size_t total = 0;
+    for (int g = 0; g < ngroups; ++g) {
+        goff[g] = total;
+        total += align256(plans[g].total);
+    }
+    for (Chain& c : chains) {
+        c.S_bytes = align256((size_t)c.batch * (size_t)c.s_pad * (size_t)c.s_pad * 2);
+        c.off = total;
+        total += c.S_bytes * SQ_GRAM_COUNT;
+    }
+
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+    Workspace* w = workspace_for(dev, stream);
+    std::unique_lock<std::mutex> use_lock(w->use);
+    st = ensure_device(w, total);
+    if (st != DION2_OK) return st;
+    char* ws = static_cast<char*>(w->dev);
+
+    auto chain_buf = [&](int c, int i) {
+        return reinterpret_cast<uint16_t*>(ws + chains[c].off + (size_t)i * chains[c].S_bytes);
+    };
+    // Streams: with one, everything goes on `stream` in order. Otherwise the
+    // groups (and chains) are dealt round-robin to auxiliary streams forked
+    // from `stream`; a chain waits for its groups' A_0, a group's final
+    // product for its chain, and `stream` for every auxiliary stream.
+    const int want = opt.group_streams == 0 ? kDefaultGroupStreams : opt.group_streams;
+    const int nS = want < ngroups ? want : ngroups;
+    const int nchain = (int)chains.size();
+    std::vector<hipStream_t> strm(nS, stream);
+    hipEvent_t fork = nullptr;
+    std::vector<hipEvent_t> ev_a0(ngroups, nullptr), ev_chain(nchain, nullptr), ev_join(nS, nullptr);
+    if (nS > 1) {
+        st = ensure_aux(w, nS, 1 + ngroups + nchain + nS);
+        if (st != DION2_OK) return st;
+        int ei = 0;
+        fork = w->ev[ei++];
+        for (int g = 0; g < ngroups; ++g) ev_a0[g] = w->ev[ei++];
+        for (int c = 0; c < nchain; ++c) ev_chain[c] = w->ev[ei++];
+        for (int i = 0; i < nS; ++i) ev_join[i] = w->ev[ei++];
+        e = hipEventRecord(fork, stream);
+        if (e != hipSuccess) return hip_fail(e, "hipEventRecord(fork)");
+        for (int i = 0; i < nS; ++i) {
+            strm[i] = w->aux[i];
+            e = hipStreamWaitEvent(strm[i], fork, 0);
+            if (e != hipSuccess) return hip_fail(e, "hipStreamWaitEvent(fork)");
+        }
+    }
+    auto stream_of = [&](int i) { return strm[i % nS]; };
+
+    std::vector<Bufs> bufs(ngroups);
+    std::vector<MatSet> sets(ngroups);
+    std::vector<dion2_options> gopt(ngroups, opt);
+    std::vector<FinalSpec> fins(ngroups);
+    int64_t matrix0 = opt.rand_matrix0;
+    // pass 1: K1-K3 of every group; DIRECT groups complete, GRAM groups put
+    // A_0 into their chain
+    for (int g = 0; g < ngroups; ++g) {
+        const Plan& P = plans[g];
+        const hipStream_t s = stream_of(g);
+        MatSet ms{};
+        ms.stride = P.rows * P.cols;
+        ms.W = groups[g].W;
+        ms.M = groups[g].M;
+        ms.G = groups[g].G;
+        sets[g] = ms;
+        gopt[g].rand_matrix0 = matrix0;
+        matrix0 += P.batch;
+        Bufs b = carve(P, ws + goff[g]);
+        const int c = chain_of[g];
+        if (c >= 0) {
+            const size_t m0 = (size_t)chain_pos[g] * (size_t)P.s_pad * (size_t)P.s_pad;
+            for (int i = 0; i < SQ_GRAM_COUNT; ++i) b.sbuf[i] = chain_buf(c, i) + m0;
+        }
+        bufs[g] = b;
+        st = front(P, ms, b, mu, ns_steps, gopt[g], s);
+        if (st != DION2_OK) return st;
+        fins[g] = make_final(P, ms, b, lr, ns_steps, gopt[g]);
+        if (c >= 0) {
+            e = gram_a0(P, b.Z0, b.sbuf[SQ_AHI], b.sbuf[SQ_ALO], s);
+            if (e != hipSuccess) return hip_fail(e, "launch K4 Gram");
+            if (nS > 1) {
+                e = hipEventRecord(ev_a0[g], s);
+                if (e != hipSuccess) return hip_fail(e, "hipEventRecord(A_0)");
+            }
+            continue;
+        }
+        if (ns_steps > 0) {
+            e = P.gram ? ns_gram(P, b.Z0, b.sbuf, b.O, ns_steps, gopt[g], fins[g], s)
+                       : ns_direct(P, b.Z0, b.Z1, b.sbuf, b.O, ns_steps, gopt[g], fins[g], s);
+            if (e != hipSuccess) return hip_fail(e, "launch K4 Newton-Schulz");
+        }
+        st = back(P, ms, b, fins[g], gopt[g], s);
+        if (st != DION2_OK) return st;
+    }
+    // pass 2: each chain's s x s products, all its matrices per launch
+    std::vector<int> chain_cur(nchain, 0);
+    for (int c = 0; c < nchain; ++c) {
+        int first = 0;   // the chain runs on the stream of its first group
+        while (chain_of[first] != c) ++first;
+        const hipStream_t s = stream_of(first);
+        ChainCost cost;
+        for (int g = 0; g < ngroups; ++g) {
+            if (chain_of[g] != c) continue;
+            const ChainCost cg = chain_cost(plans[g], ns_steps);
+            cost.flops += cg.flops;
+            cost.bytes += cg.bytes;
+            if (nS > 1) {
+                e = hipStreamWaitEvent(s, ev_a0[g], 0);
+                if (e != hipSuccess) return hip_fail(e, "hipStreamWaitEvent(A_0)");
+            }
+        }
+        uint16_t* sq[SQ_GRAM_COUNT];
+        for (int i = 0; i < SQ_GRAM_COUNT; ++i) sq[i] = chain_buf(c, i);
+        e = gram_chain(chains[c].batch, chains[c].s_pad, sq, ns_steps, opt, cost, s, &chain_cur[c]);
+        if (e != hipSuccess) return hip_fail(e, "launch K4 s x s products");
+        if (nS > 1) {
+            e = hipEventRecord(ev_chain[c], s);
+            if (e != hipSuccess) return hip_fail(e, "hipEventRecord(chain)");
+        }
+    }
+    // pass 3: final products and K5 of the chained groups
+    for (int g = 0; g < ngroups; ++g) {
+        const int c = chain_of[g];
+        if (c < 0) continue;
+        const hipStream_t s = stream_of(g);
+        if (nS > 1) {
+            e = hipStreamWaitEvent(s, ev_chain[c], 0);
+            if (e != hipSuccess) return hip_fail(e, "hipStreamWaitEvent(chain)");
+        }
+        const Plan& P = plans[g];
+        const Bufs& b = bufs[g];
+        const int cur = chain_cur[c];
+        e = gram_final(P, cur ? b.sbuf[SQ_P1HI] : b.sbuf[SQ_P0HI], cur ? b.sbuf[SQ_P1LO] : b.sbuf[SQ_P0LO],
+                       b.Z0, b.O, fins[g], s);
+        if (e != hipSuccess) return hip_fail(e, "launch K4 final product");
+        st = back(P, sets[g], b, fins[g], gopt[g], s);
+        if (st != DION2_OK) return st;
+    }
+    for (int i = 0; nS > 1 && i < nS; ++i) {
+        e = hipEventRecord(ev_join[i], strm[i]);
+        if (e != hipSuccess) return hip_fail(e, "hipEventRecord(join)");
+        e = hipStreamWaitEvent(stream, ev_join[i], 0);
+        if (e != hipSuccess) return hip_fail(e, "hipStreamWaitEvent(join)");
+    }
+    return DION2_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -767,6 +1101,7 @@ void dion2_options_init(dion2_options* opt) {
     opt->rand_seed = 0;
     opt->rand_step = 0;
     opt->rand_matrix0 = 0;
+    opt->group_streams = 0;
 }
 
 int dion2_step(void* W, float* M, const void* G, int64_t rows, int64_t cols, float alpha,
@@ -796,6 +1131,11 @@ int dion2_step_ex(void* W, float* M, const void* G, int batch, int64_t rows, int
                      stream);
 }
 
+int dion2_step_groups(const dion2_group* groups, int ngroups, float alpha, float mu, float lr,
+                      int ns_steps, const dion2_options* opt, void* stream) {
+    return groups_impl(groups, ngroups, alpha, mu, lr, ns_steps, opt, static_cast<hipStream_t>(stream));
+}
+
 size_t dion2_workspace_size(int batch, int64_t rows, int64_t cols, float alpha, int axis) {
     Plan P;
     if (make_plan(batch, rows, cols, alpha, axis, DION2_NS_AUTO, &P) != DION2_OK) return 0;
@@ -823,6 +1163,10 @@ void dion2_release_workspaces(void) {
         if (w->dev) hipFree(w->dev);
         if (w->pinned) hipHostFree(w->pinned);
         if (w->tables_done) hipEventDestroy(w->tables_done);
+        for (hipStream_t a : w->aux) hipStreamDestroy(a);
+        for (hipEvent_t ev : w->ev) hipEventDestroy(ev);
+        w->aux.clear();
+        w->ev.clear();
         w->dev = nullptr;
         w->bytes = 0;
         w->pinned = nullptr;

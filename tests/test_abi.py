@@ -161,3 +161,51 @@ def test_status_codes_match_header():
     for name, val in (("DION2_AXIS_AUTO", AXIS_AUTO), ("DION2_AXIS_ROWS", AXIS_ROWS),
                       ("DION2_AXIS_COLS", AXIS_COLS)):
         assert re.search(rf"{name}\s*=\s*{val}\b", text), name
+
+
+def groups_array(specs):
+    arr = (binding.Group * max(len(specs), 1))()
+    for i, kw in enumerate(specs):
+        g = dict(W=FAKE, M=FAKE, G=FAKE, batch=2, rows=64, cols=64, axis=AXIS_AUTO)
+        g.update(kw)
+        arr[i] = binding.Group(g["W"], g["M"], g["G"], g["batch"], g["rows"], g["cols"], g["axis"])
+    return arr
+
+
+@pytest.mark.parametrize("specs,n,opt_kw,msg", [
+    ([{}], 0, {}, "ngroups"),
+    ([{}], 65, {}, "ngroups"),
+    ([{}, {"W": None}], 2, {}, "NULL"),
+    ([{}, {"G": FAKE + 4}], 2, {}, "aligned"),
+    ([{"rows": 0}], 1, {}, "rows"),
+    ([{}, {"axis": 5}], 2, {}, "axis"),
+    ([{"batch": 0}], 1, {}, "batch"),
+    ([{}], 1, {"workspace": FAKE, "workspace_bytes": 1 << 30}, "workspace"),
+    ([{}], 1, {"dbg_norms": FAKE}, "debug"),
+    ([{}], 1, {"select_rule": 7}, "select_rule"),
+    ([{"batch": 3}, {"batch": 3}], 2, {"select_rule": 1, "rand_matrix0": (1 << 32) - 5}, "rand_matrix0"),
+])
+def test_groups_validation(lib, specs, n, opt_kw, msg):
+    arr = groups_array(specs)
+    opt = Options()
+    lib.dion2_options_init(ctypes.byref(opt))
+    for k, v in opt_kw.items():
+        setattr(opt, k, v)
+    st = binding.dion2_step_groups_raw(arr, n, 0.25, 0.95, 0.02, 5, opt, None)
+    assert st == DION2_ERR_INVALID_ARG
+    assert msg in binding.dion2_last_error()
+
+
+def test_groups_null_array(lib):
+    assert binding.dion2_step_groups_raw(None, 1, 0.25, 0.95, 0.02, 5, None, None) == DION2_ERR_INVALID_ARG
+
+
+def test_groups_stream_count_validated(lib):
+    arr = groups_array([{}])
+    opt = Options()
+    lib.dion2_options_init(ctypes.byref(opt))
+    assert opt.group_streams == 0
+    for bad in (-1, 9):
+        opt.group_streams = bad
+        assert binding.dion2_step_groups_raw(arr, 1, 0.25, 0.95, 0.02, 5, opt, None) == DION2_ERR_INVALID_ARG
+        assert "group_streams" in binding.dion2_last_error()

@@ -358,3 +358,61 @@ def test_random_selection_full_1b_group(hip_device):
                    W=W[b].cpu()[None], M=M[b].cpu()[None], K=sel[b].cpu()[None],
                    norms=nrm[b].cpu()[None], O=upd[b].cpu()[None], axis=ax, k=k)
         check_matrix(res, 0, 0.25, rand=(5, 100, b))
+
+
+# Several shape groups in one grouped call: five in the GRAM form (four of
+# padded s = 128, one of 256: two shared chains) and one in the DIRECT form.
+GROUPED = workloads.Workload(
+    "grouped", "test", (workloads.Group("a", 256, 640, 2), workloads.Group("b", 640, 256, 3),
+                        workloads.Group("c", 384, 384, 2), workloads.Group("d", 300, 200, 1),
+                        workloads.Group("e", 128, 160, 2), workloads.Group("f", 1024, 2048, 1)),
+    (0.25,))
+
+
+@pytest.mark.parametrize("gs", [1, 0, 3], ids=["one-stream", "default-streams", "three-streams"])
+@pytest.mark.parametrize("rand", [None, (11, 3, 5)], ids=["l1", "random"])
+def test_groups_equal_per_group_calls(hip_device, rand, gs):
+    """dion2_step_groups is bitwise the per-group dion2_step_ex calls on one
+    stream or spread over several, its chains really are shared (s x s
+    launches counted), and one group is tied to the oracle through the
+    per-group call's debug outputs."""
+    alpha = 0.25
+    stacks = [workloads.make_group(GROUPED, gi, hip_device) for gi in range(len(GROUPED.groups))]
+    solo = [tuple(t.clone() for t in s) for s in stacks]
+    kw = {}
+    if rand is not None:
+        kw = dict(select_rule=binding.SELECT_RANDOM, rand_seed=rand[0], rand_step=rand[1])
+    # per group, in order, with the Random rule's matrix indices continuing
+    m0 = rand[2] if rand else 0
+    for W, M, G in solo:
+        binding.dion2_step_ex(W, M, G, alpha, rand_matrix0=m0, **kw)
+        m0 += W.shape[0]
+    binding.dion2_profile_reset()
+    binding.dion2_profile_enable(True)
+    binding.dion2_step_groups([(W, M, G, AXIS_AUTO) for W, M, G in stacks], alpha,
+                              rand_matrix0=rand[2] if rand else 0, group_streams=gs, **kw)
+    torch.cuda.synchronize()
+    prof = binding.dion2_profile_read()
+    binding.dion2_profile_enable(False)
+    for gi, ((W, M, _), (Ws, Ms, _)) in enumerate(zip(stacks, solo)):
+        assert torch.equal(M, Ms), f"group {gi}: momentum"
+        assert torch.equal(W.view(torch.int16), Ws.view(torch.int16)), f"group {gi}: weights"
+    # two chains of 14 launches (5 Newton-Schulz steps) instead of one per
+    # GRAM group, plus the DIRECT group's 5 polynomial products
+    assert prof["ns_poly"]["launches"] == 2 * 14 + 5
+    # the first group against the oracle (its own call, with debug outputs)
+    W, M, G = workloads.make_group(GROUPED, 0, hip_device)
+    res = run_gpu(W, M, G, alpha, rand=(rand[0], rand[1], rand[2]) if rand else None)
+    assert torch.equal(res["W"].view(torch.int16), solo[0][0].cpu().view(torch.int16))
+    check_matrix(res, 1, alpha, rand=rand)
+
+
+def test_groups_single_group_equals_strided(hip_device):
+    """One group through the grouped entry point equals dion2_step_strided."""
+    wl = one_group_workload(2048, 2048, count=4, name="g1")
+    W, M, G = workloads.make_group(wl, 0, hip_device)
+    W2, M2, G2 = W.clone(), M.clone(), G.clone()
+    binding.dion2_step_strided(W, M, G, 0.25)
+    binding.dion2_step_groups([(W2, M2, G2, AXIS_AUTO)], 0.25)
+    torch.cuda.synchronize()
+    assert torch.equal(M, M2) and torch.equal(W.view(torch.int16), W2.view(torch.int16))
