@@ -4,11 +4,10 @@
     python bench.py [--steps K] [--warmup W] [--workload 1b] [--alpha 0.25]
 
 A step is one Dion2 update (Algorithm 1) of every matrix of a synthetic layer
-stack with W, M, G resident in HBM: by default one dion2_step_groups call
-for the whole stack (groups of one padded Newton-Schulz size share their
-chain of s x s products). With --calls per-group it is one batched call per
-same-shape group, each on its own stream (forked from and joined into the
-timing stream), or back to back on one stream with --streams 0. The default is the paper's timing method
+stack with W, M, G resident in HBM: one batched call per same-shape group,
+each on its own stream (forked from and joined into the timing stream), or
+back to back on one stream with --streams 0. --calls grouped makes it one
+dion2_step_groups call for the whole stack instead. The default is the paper's timing method
 (Sec. 4.4): 100 steps, the mean of the final 20 reported (warmup 80,
 steps 20). Prints one JSON line:
   value        mean ms per step at --alpha (lower is better)
@@ -220,7 +219,7 @@ def main(argv=None):
     ap.add_argument("--streams", type=int, default=-1,
                     help="run the shape groups on this many streams (0: all on the current "
                          "stream; default: one stream per group, the groups being independent)")
-    ap.add_argument("--calls", default="grouped", choices=("grouped", "per-group"),
+    ap.add_argument("--calls", default="per-group", choices=("grouped", "per-group"),
                     help="one dion2_step_groups call for the whole stack (groups of one padded "
                          "Newton-Schulz size share their s x s chain), or one call per shape "
                          "group on its own stream")

@@ -867,9 +867,13 @@ int step_impl(void* W, float* M, const void* G, const Tables* tabs, int batch, i
 constexpr int kMaxGroups = 64;
 constexpr int kMaxGroupStreams = 8;
 constexpr int kDefaultGroupStreams = 4;
-// Groups share a chain only while one product of theirs has fewer
-// output tiles than this (two per compute unit).
-constexpr int64_t kChainShareTiles = 512;
+// Groups share a chain only while one product of theirs has fewer output
+// tiles than this (half the compute units). Sharing makes the chain wait for
+// every member's first half, so groups big enough to keep half the chip
+// busy do better on their own stream, overlapping the others: the three
+// groups of the 1B stack at alpha = 0.25 (160 to 640 tiles) measured 40 us
+// per step slower with the two small ones sharing.
+constexpr int64_t kChainShareTiles = 128;
 
 int groups_impl(const dion2_group* groups, int ngroups, float alpha, float mu, float lr,
                 int ns_steps, const dion2_options* opt_in, hipStream_t stream) {
