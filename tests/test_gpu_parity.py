@@ -416,3 +416,36 @@ def test_groups_single_group_equals_strided(hip_device):
     binding.dion2_step_groups([(W2, M2, G2, AXIS_AUTO)], 0.25)
     torch.cuda.synchronize()
     assert torch.equal(M, M2) and torch.equal(W.view(torch.int16), W2.view(torch.int16))
+
+
+@pytest.mark.parametrize("case", ["f32-decay-all-schedule", "forced-direct", "forced-gram", "no-steps"])
+def test_groups_options_equal_per_group_calls(hip_device, case):
+    """Options reach every group of a grouped call as they reach dion2_step_ex:
+    fp32 W and G, the decay-all ablation, a per-step coefficient schedule, a
+    forced Newton-Schulz form, and zero steps (O = the scaled compact matrix)."""
+    wdt = "f32" if case.startswith("f32") else "bf16"
+    wl = workloads.Workload("grouped-opt", "test",
+                            (workloads.Group("a", 256, 640, 2), workloads.Group("b", 640, 256, 2),
+                             workloads.Group("c", 128, 160, 1)), (0.25,), w_dtype=wdt)
+    kw = {}
+    ns_steps = 5
+    if case == "f32-decay-all-schedule":
+        kw = dict(decay_all=True,
+                  ns_coeffs=[(3.4445, -4.7750, 2.0315)] * 3 + [(1.5, -0.5, 0.0)] * 2)
+    elif case == "forced-direct":
+        kw = dict(ns_form=NS_DIRECT)
+    elif case == "forced-gram":
+        kw = dict(ns_form=NS_GRAM)
+    else:
+        ns_steps = 0
+    stacks = [workloads.make_group(wl, gi, hip_device) for gi in range(len(wl.groups))]
+    solo = [tuple(t.clone() for t in s) for s in stacks]
+    for W, M, G in solo:
+        binding.dion2_step_ex(W, M, G, 0.25, 0.95, 0.02, ns_steps, **kw)
+    binding.dion2_step_groups([(W, M, G, AXIS_AUTO) for W, M, G in stacks], 0.25, 0.95, 0.02,
+                              ns_steps, **kw)
+    torch.cuda.synchronize()
+    iview = torch.int32 if wdt == "f32" else torch.int16
+    for gi, ((W, M, _), (Ws, Ms, _)) in enumerate(zip(stacks, solo)):
+        assert torch.equal(M, Ms), f"group {gi}: momentum"
+        assert torch.equal(W.view(iview), Ws.view(iview)), f"group {gi}: weights"
