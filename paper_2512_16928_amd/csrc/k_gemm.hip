@@ -33,8 +33,9 @@
 // global chunk that belongs in its LDS slot. Tiles are numbered XCD-aware;
 // the symmetric products (A and B) compute only the tiles on and above the
 // diagonal and write each one twice. The epilogue goes through a per-wave
-// 32 x 32 LDS tile so row-major and transposed outputs are both written as
-// 16-byte chunks.
+// 32 x 32 LDS tile: each lane finishes 16 entries of a row there, and the
+// block then leaves in whole row segments (64 bytes of bf16 or 128 bytes of
+// fp32 per row), row-major or transposed for the mirrored copy.
 //
 // All dimensions are multiples of the tile (compact buffers are zero padded
 // to 128, and the padding stays zero through every step).
@@ -161,20 +162,6 @@ __device__ __forceinline__ bf16x8 b_frag_tr(const unsigned char* sb, int krow, i
     return __builtin_bit_cast(bf16x8, v);
 }
 
-// Transposed read of a wave's 32 x 32 staging tile: the lane's 16 values v
-// (row er, columns ec..ec+15) are stored back, and t receives row er of the
-// transpose (entries (ec + q, er) of the block).
-template <typename T>
-__device__ __forceinline__ void mirror16(float* stage, const float (&v)[16], float (&t)[16],
-                                         int er, int ec) {
-    __builtin_amdgcn_wave_barrier();
-#pragma unroll
-    for (int q = 0; q < 16; ++q) stage[er * T::EPI_LD + ec + q] = v[q];
-    __builtin_amdgcn_wave_barrier();
-#pragma unroll
-    for (int q = 0; q < 16; ++q) t[q] = stage[(ec + q) * T::EPI_LD + er];
-}
-
 // MFMAs of one BK-deep K-slice staged at `st`, fragments software-pipelined
 // (k-step kk+1 is read from LDS while the MFMAs of kk run).
 template <int NPASS, typename T>
@@ -232,37 +219,51 @@ __device__ __forceinline__ void mma_slice(f32x16 (&acc)[T::FM][T::FN], const uns
     }
 }
 
-// Store 16 consecutive outputs of row `orow` from column `ocol` in the
-// epilogue's output form: bf16 hi + lo (EPI_SPLIT, EPI_QPOLY), bf16
-// (EPI_POLY, EPI_UPDATE) or fp32 (EPI_FINAL); 16-byte stores.
-template <int EPI>
-__device__ __forceinline__ void store16(const GemmArgs& a, int b, int64_t orow, int64_t ocol,
-                                        const float (&v)[16]) {
-    if constexpr (EPI == EPI_SPLIT || EPI == EPI_QPOLY) {
-        uint32_t h[8], l[8];
+// Store a wave's finished 32 x 32 block from its LDS tile (fp32, row pitch
+// EPI_LD) to output rows orow0 .. orow0 + 31, columns ocol0 .. ocol0 + 31, in
+// the epilogue's output form. Lanes take whole row segments: for bf16
+// outputs four lanes cover a row's 64 bytes (16 rows per instruction), for
+// fp32 eight lanes its 128 bytes, so every store instruction writes
+// contiguous segments of few cache lines. With TR the tile is read
+// transposed (output row q = tile column q), for the mirrored block.
+template <int EPI, typename T, bool TR>
+__device__ __forceinline__ void store_block(const GemmArgs& a, int b, const float* stage, int64_t orow0,
+                                            int64_t ocol0, int lane) {
+    auto at = [&](int r, int c) { return TR ? stage[c * T::EPI_LD + r] : stage[r * T::EPI_LD + c]; };
+    if constexpr (EPI == EPI_FINAL) {
+        const int c4 = 4 * (lane & 7);
 #pragma unroll
-        for (int q = 0; q < 8; ++q) {
-            const uint16_t h0 = f32_to_bf16(v[2 * q]), h1 = f32_to_bf16(v[2 * q + 1]);
-            h[q] = (uint32_t)h0 | ((uint32_t)h1 << 16);
-            l[q] = pack2(v[2 * q] - bf16_bits_to_f32(h0), v[2 * q + 1] - bf16_bits_to_f32(h1));
+        for (int q = 0; q < 4; ++q) {
+            const int r = 8 * q + (lane >> 3);
+            float* op = static_cast<float*>(a.out0) + (int64_t)b * a.sOut0 + (orow0 + r) * a.ldo0 + ocol0 + c4;
+            *reinterpret_cast<float4*>(op) = make_float4(at(r, c4), at(r, c4 + 1), at(r, c4 + 2), at(r, c4 + 3));
         }
-        uint16_t* hp = static_cast<uint16_t*>(a.out0) + (int64_t)b * a.sOut0 + orow * a.ldo0 + ocol;
-        uint16_t* lp = static_cast<uint16_t*>(a.out1) + (int64_t)b * a.sOut1 + orow * a.ldo1 + ocol;
-        reinterpret_cast<uint4*>(hp)[0] = make_uint4(h[0], h[1], h[2], h[3]);
-        reinterpret_cast<uint4*>(hp)[1] = make_uint4(h[4], h[5], h[6], h[7]);
-        reinterpret_cast<uint4*>(lp)[0] = make_uint4(l[0], l[1], l[2], l[3]);
-        reinterpret_cast<uint4*>(lp)[1] = make_uint4(l[4], l[5], l[6], l[7]);
-    } else if constexpr (EPI == EPI_POLY || EPI == EPI_UPDATE) {
-        uint16_t* op = static_cast<uint16_t*>(a.out0) + (int64_t)b * a.sOut0 + orow * a.ldo0 + ocol;
-        reinterpret_cast<uint4*>(op)[0] = make_uint4(pack2(v[0], v[1]), pack2(v[2], v[3]),
-                                                     pack2(v[4], v[5]), pack2(v[6], v[7]));
-        reinterpret_cast<uint4*>(op)[1] = make_uint4(pack2(v[8], v[9]), pack2(v[10], v[11]),
-                                                     pack2(v[12], v[13]), pack2(v[14], v[15]));
     } else {
-        float* op = static_cast<float*>(a.out0) + (int64_t)b * a.sOut0 + orow * a.ldo0 + ocol;
+        const int c8 = 8 * (lane & 3);
 #pragma unroll
-        for (int q = 0; q < 4; ++q)
-            reinterpret_cast<float4*>(op)[q] = make_float4(v[4 * q], v[4 * q + 1], v[4 * q + 2], v[4 * q + 3]);
+        for (int q = 0; q < 2; ++q) {
+            const int r = 16 * q + (lane >> 2);
+            float v[8];
+#pragma unroll
+            for (int t = 0; t < 8; ++t) v[t] = at(r, c8 + t);
+            if constexpr (EPI == EPI_SPLIT || EPI == EPI_QPOLY) {
+                uint32_t h[4], l[4];
+#pragma unroll
+                for (int t = 0; t < 4; ++t) {
+                    const uint16_t h0 = f32_to_bf16(v[2 * t]), h1 = f32_to_bf16(v[2 * t + 1]);
+                    h[t] = (uint32_t)h0 | ((uint32_t)h1 << 16);
+                    l[t] = pack2(v[2 * t] - bf16_bits_to_f32(h0), v[2 * t + 1] - bf16_bits_to_f32(h1));
+                }
+                uint16_t* hp = static_cast<uint16_t*>(a.out0) + (int64_t)b * a.sOut0 + (orow0 + r) * a.ldo0 + ocol0 + c8;
+                uint16_t* lp = static_cast<uint16_t*>(a.out1) + (int64_t)b * a.sOut1 + (orow0 + r) * a.ldo1 + ocol0 + c8;
+                *reinterpret_cast<uint4*>(hp) = make_uint4(h[0], h[1], h[2], h[3]);
+                *reinterpret_cast<uint4*>(lp) = make_uint4(l[0], l[1], l[2], l[3]);
+            } else {   // EPI_POLY, EPI_UPDATE: bf16
+                uint16_t* op = static_cast<uint16_t*>(a.out0) + (int64_t)b * a.sOut0 + (orow0 + r) * a.ldo0 + ocol0 + c8;
+                *reinterpret_cast<uint4*>(op) = make_uint4(pack2(v[0], v[1]), pack2(v[2], v[3]),
+                                                           pack2(v[4], v[5]), pack2(v[6], v[7]));
+            }
+        }
     }
 }
 
@@ -505,12 +506,14 @@ __global__ __launch_bounds__(T::THREADS) void gemm(GemmArgs a) {
                     }
                 }
             } else {
-                store16<EPI>(a, b, orow, ocol, v);
-            }
-            if (SYM && row0 != col0) {
-                float t[16];
-                mirror16<T>(stage, v, t, er, ec);
-                store16<EPI>(a, b, (int64_t)Cc + er, (int64_t)R + ec, t);
+                // the finished values go back to the tile (this lane's own
+                // entries) and leave it in whole row segments
+                __builtin_amdgcn_wave_barrier();
+#pragma unroll
+                for (int q = 0; q < 16; ++q) stage[er * T::EPI_LD + ec + q] = v[q];
+                __builtin_amdgcn_wave_barrier();
+                store_block<EPI, T, false>(a, b, stage, orow - er, ocol - ec, lane);
+                if (SYM && row0 != col0) store_block<EPI, T, true>(a, b, stage, (int64_t)Cc, (int64_t)R, lane);
             }
             __builtin_amdgcn_wave_barrier();   // the stage tile is rewritten next
         }
