@@ -35,16 +35,31 @@ __global__ __launch_bounds__(kThreads) void gather_rows(GatherArgs a) {
     uint16_t* __restrict__ LT = a.LT ? a.LT + (int64_t)b * a.opad * a.kpad : nullptr;
     float* __restrict__ O = a.O ? a.O + (int64_t)b * a.kpad * a.opad : nullptr;
     const int j = j0 + 4 * tx;
+    // the four rows' indices and values are all requested before the first
+    // store: memory counters retire in issue order, so a load issued after a
+    // store would also wait for the store's acknowledgement
+    int64_t roff[4];
+    float4 mv[4];
+    const bool vec = VEC == 4 && j + 3 < a.d_oth;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const int p = p0 + ty + 16 * i;
+        roff[i] = (int64_t)ldg<int32_t>(K + (p < a.k ? p : a.k - 1)) * a.cols;
+    }
+    if (vec) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) mv[i] = ldg_nt<float4>(M + roff[i] + j);
+    }
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
         const int pl = ty + 16 * i;
         const int p = p0 + pl;
         float x[4] = {0.f, 0.f, 0.f, 0.f};
         if (p < a.k) {
-            float* row = M + (int64_t)K[p] * a.cols;
-            if (VEC == 4 && j + 3 < a.d_oth) {
+            float* row = M + roff[i];
+            if (vec) {
                 float m[4];
-                unpack4(ldg_nt<float4>(row + j), m);
+                unpack4(mv[i], m);
 #pragma unroll
                 for (int v = 0; v < 4; ++v) x[v] = m[v] * sc;
                 if (a.decay) stg_nt(row + j, make_float4(a.mu * m[0], a.mu * m[1], a.mu * m[2], a.mu * m[3]));
