@@ -288,34 +288,39 @@ __global__ __launch_bounds__(kThreads) void apply_cols_strip(ApplyArgs a) {
     }
 }
 
-// Column mode, cols % 8 == 0, k <= 1024 and a row of W within 8 KB: whole
+// Column mode, cols % 8 == 0 and a row of W within 8 KB: whole
 // rows per wave, the arithmetic spread over the selected entries rather
 // than over the columns. A wave copies its row of W into LDS (16-byte
 // chunks), lane l updates there the entries of ranks p = l + 64 t (column
 // K[p], value O^T[r][p], read coalesced), and the row goes back to W whole.
 // Every lane does the same number of updates, so nothing diverges; K is
-// staged in LDS once per block.
+// staged in LDS once per block. The first 64 KT ranks of a row are fetched
+// with the row (one row ahead); larger k take further passes of 64 KT.
 constexpr int kSelRows = 32;                 // rows per block (8 per wave)
 constexpr int kSelRowBytes = 8192;           // LDS row buffer per wave
-constexpr int kSelMaxK = 1024;
+constexpr int kSelMaxK = 4096;               // (a row buffer holds at most 4096 columns)
 
 template <typename WT, int NCH, int KT>
 __global__ __launch_bounds__(kThreads) void apply_cols_sel(ApplyArgs a) {
     __shared__ __attribute__((aligned(16))) WT row_s[4][kSelRowBytes / sizeof(WT)];
-    __shared__ int32_t sel_s[kSelMaxK];
+    extern __shared__ int32_t sel_s[];   // k entries (dynamic: k * 4 bytes)
     const int b = blockIdx.y;
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     {
-        constexpr int kN = kSelMaxK / kThreads;
         const int32_t* sel = a.sel + (int64_t)b * a.k;
-        int32_t t[kN];   // all loads in flight before the first LDS write
+        for (int i0 = 0; i0 < a.k; i0 += 4 * kThreads) {
+            int32_t t[4];   // four loads in flight before the LDS writes
 #pragma unroll
-        for (int q = 0; q < kN; ++q) {
-            const int i = threadIdx.x + q * kThreads;
-            t[q] = ldg<int32_t>(sel + (i < a.k ? i : a.k - 1));
+            for (int q = 0; q < 4; ++q) {
+                const int i = i0 + threadIdx.x + q * kThreads;
+                t[q] = ldg<int32_t>(sel + (i < a.k ? i : a.k - 1));
+            }
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                const int i = i0 + threadIdx.x + q * kThreads;
+                if (i < a.k) sel_s[i] = t[q];
+            }
         }
-#pragma unroll
-        for (int q = 0; q < kN; ++q) sel_s[threadIdx.x + q * kThreads] = t[q];
     }
     __syncthreads();
 
@@ -359,14 +364,25 @@ __global__ __launch_bounds__(kThreads) void apply_cols_sel(ApplyArgs a) {
             if (cval[j]) w[j].put(rs + coff[j]);
         // LDS accesses of one wave complete in issue order
         __builtin_amdgcn_wave_barrier();
-#pragma unroll
-        for (int t = 0; t < KT; ++t) {
-            const int p = lane + 64 * t;
+        auto update = [&](int p, float ov) {
             if (p < a.k) {
                 WT* e = rs + sel_s[p];
-                Elem<WT>::lds_store_f64(e, __dsub_rn((double)Elem<WT>::lds_load(e), __dmul_rn(a.lr_eff, (double)o[t])));
-                if (a.dbg) a.dbg[((int64_t)b * a.k + p) * a.d_oth + r] = o[t];
+                Elem<WT>::lds_store_f64(e, __dsub_rn((double)Elem<WT>::lds_load(e), __dmul_rn(a.lr_eff, (double)ov)));
+                if (a.dbg) a.dbg[((int64_t)b * a.k + p) * a.d_oth + r] = ov;
             }
+        };
+#pragma unroll
+        for (int t = 0; t < KT; ++t) update(lane + 64 * t, o[t]);
+        for (int p0 = 64 * KT; p0 < a.k; p0 += 64 * 8) {   // k > 64 KT only
+            const float* src = OT + r * a.kpad;
+            float ox[8];
+#pragma unroll
+            for (int t = 0; t < 8; ++t) {
+                const int p = p0 + lane + 64 * t;
+                ox[t] = ldg<float>(src + (p < a.k ? p : a.k - 1));
+            }
+#pragma unroll
+            for (int t = 0; t < 8; ++t) update(p0 + lane + 64 * t, ox[t]);
         }
         __builtin_amdgcn_wave_barrier();
 #pragma unroll
@@ -387,9 +403,10 @@ __global__ __launch_bounds__(kThreads) void apply_cols_sel(ApplyArgs a) {
 template <typename WT, int NCH>
 void launch_cols_sel_k(const ApplyArgs& a, hipStream_t s) {
     dim3 grid((unsigned)((a.rows + kSelRows - 1) / kSelRows), (unsigned)a.batch);
-    if (a.k <= 256) hipLaunchKernelGGL((apply_cols_sel<WT, NCH, 4>), grid, dim3(kThreads), 0, s, a);
-    else if (a.k <= 512) hipLaunchKernelGGL((apply_cols_sel<WT, NCH, 8>), grid, dim3(kThreads), 0, s, a);
-    else hipLaunchKernelGGL((apply_cols_sel<WT, NCH, 16>), grid, dim3(kThreads), 0, s, a);
+    const size_t lds = (size_t)a.k * sizeof(int32_t);   // K's copy; the row buffers are static
+    if (a.k <= 256) hipLaunchKernelGGL((apply_cols_sel<WT, NCH, 4>), grid, dim3(kThreads), lds, s, a);
+    else if (a.k <= 512) hipLaunchKernelGGL((apply_cols_sel<WT, NCH, 8>), grid, dim3(kThreads), lds, s, a);
+    else hipLaunchKernelGGL((apply_cols_sel<WT, NCH, 16>), grid, dim3(kThreads), lds, s, a);
 }
 
 template <typename WT>

@@ -109,7 +109,9 @@ def test_single_256_fp32_full(hip_device):
     (200, 96, 0.5, AXIS_AUTO, "f32"),        # columns, fp32 W, one row per wave
     (40, 4616, 0.5, AXIS_COLS, "bf16"),      # columns beyond 4096: 512-column strips
     (24, 4104, 0.25, AXIS_COLS, "f32"),      # the same with fp32 W, ragged last strip
-    (64, 2048, 0.75, AXIS_COLS, "bf16"),     # k = 1536 > 1024: strips as well
+    (64, 2048, 0.75, AXIS_COLS, "bf16"),     # k = 1536: one row per wave, two passes of ranks
+    (48, 4096, 1.0, AXIS_COLS, "bf16"),      # k = 4096, the widest row of the LDS buffer
+    (40, 2048, 0.6, AXIS_COLS, "f32"),       # fp32 W, k = 1229 (ragged last pass)
 ])
 @FORMS
 def test_ragged_shapes(hip_device, rows, cols, alpha, axis, wdt, form):
