@@ -972,6 +972,26 @@ int groups_impl(const dion2_group* groups, int ngroups, float alpha, float mu, f
     std::vector<hipStream_t> strm(nS, stream);
     hipEvent_t fork = nullptr;
     std::vector<hipEvent_t> ev_a0(ngroups, nullptr), ev_chain(nchain, nullptr), ev_join(nS, nullptr);
+    // Once forked, `stream` waits for every auxiliary stream on every way out
+    // (an error return included), so later work on it never overlaps this
+    // call's kernels.
+    struct Join {
+        int n;
+        const std::vector<hipStream_t>& from;
+        const std::vector<hipEvent_t>& ev;
+        hipStream_t to;
+        hipError_t run() {
+            hipError_t first = hipSuccess;
+            for (int i = 0; i < n; ++i) {
+                hipError_t e = hipEventRecord(ev[i], from[i]);
+                if (e == hipSuccess) e = hipStreamWaitEvent(to, ev[i], 0);
+                if (e != hipSuccess && first == hipSuccess) first = e;
+            }
+            n = 0;
+            return first;
+        }
+        ~Join() { run(); }
+    } join{0, strm, ev_join, stream};
     if (nS > 1) {
         st = ensure_aux(w, nS, 1 + ngroups + nchain + nS);
         if (st != DION2_OK) return st;
@@ -980,10 +1000,11 @@ int groups_impl(const dion2_group* groups, int ngroups, float alpha, float mu, f
         for (int g = 0; g < ngroups; ++g) ev_a0[g] = w->ev[ei++];
         for (int c = 0; c < nchain; ++c) ev_chain[c] = w->ev[ei++];
         for (int i = 0; i < nS; ++i) ev_join[i] = w->ev[ei++];
+        for (int i = 0; i < nS; ++i) strm[i] = w->aux[i];
+        join.n = nS;   // from here on every exit joins
         e = hipEventRecord(fork, stream);
         if (e != hipSuccess) return hip_fail(e, "hipEventRecord(fork)");
         for (int i = 0; i < nS; ++i) {
-            strm[i] = w->aux[i];
             e = hipStreamWaitEvent(strm[i], fork, 0);
             if (e != hipSuccess) return hip_fail(e, "hipStreamWaitEvent(fork)");
         }
@@ -1079,12 +1100,8 @@ int groups_impl(const dion2_group* groups, int ngroups, float alpha, float mu, f
         st = back(P, sets[g], b, fins[g], gopt[g], s);
         if (st != DION2_OK) return st;
     }
-    for (int i = 0; nS > 1 && i < nS; ++i) {
-        e = hipEventRecord(ev_join[i], strm[i]);
-        if (e != hipSuccess) return hip_fail(e, "hipEventRecord(join)");
-        e = hipStreamWaitEvent(stream, ev_join[i], 0);
-        if (e != hipSuccess) return hip_fail(e, "hipStreamWaitEvent(join)");
-    }
+    e = join.run();
+    if (e != hipSuccess) return hip_fail(e, "joining the group streams");
     return DION2_OK;
 }
 
