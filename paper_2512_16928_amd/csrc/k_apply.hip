@@ -8,11 +8,14 @@
 // copied out unpadded for inspection.
 //
 // Row mode reads O rows and W rows along j (both contiguous). Column mode
-// streams W by rows and reads O transposed: when the column count is a
-// multiple of 8 a block takes a strip of 512 columns (8 per lane, one
-// 16-byte bf16 chunk) over 16 rows, stages the strip's slice of O^T in LDS
-// and rewrites only the chunks that hold a selected column; other column
-// counts take a generic four-column (or one-column) path.
+// streams W by rows and reads O transposed, in one of three kernels:
+//   apply_cols_sel    column count a multiple of 8 and a row of W within
+//                     8 KB (the common case): one row per wave, copied into
+//                     LDS, one fp64 update per selected entry per lane;
+//   apply_cols_strip  wider rows: 512-column strips, the strip's slice of
+//                     O^T staged in LDS, only chunks with a selected column
+//                     rewritten;
+//   apply_cols        other column counts: four (or one) columns per lane.
 #include <type_traits>
 
 #include "dion2_device.h"
@@ -298,7 +301,7 @@ __global__ __launch_bounds__(kThreads) void apply_cols_strip(ApplyArgs a) {
 // with the row (one row ahead); larger k take further passes of 64 KT.
 constexpr int kSelRows = 32;                 // rows per block (8 per wave)
 constexpr int kSelRowBytes = 8192;           // LDS row buffer per wave
-constexpr int kSelMaxK = 4096;               // (a row buffer holds at most 4096 columns)
+constexpr int kSelMaxK = 4096;               // k <= cols <= 4096 (bf16) or 2048 (fp32)
 
 template <typename WT, int NCH, int KT>
 __global__ __launch_bounds__(kThreads) void apply_cols_sel(ApplyArgs a) {
