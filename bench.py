@@ -16,6 +16,8 @@ steps 20). Prints one JSON line:
   cpu_baseline the CPU oracle timed on a bounded sample of the same stack
   per_alpha_ms the other fractions of the workload, timed the same way
   per_rule_ms  the l1 (Default) and Random selection rules at --alpha
+  per_chain_ms the GRAM chain's storage: bf16 hi/lo pairs (the default) and
+               the opt-in scaled fp16 (ns_chain), at every fraction
 """
 from __future__ import annotations
 
@@ -63,6 +65,8 @@ def allocate(wl, dev, split=1):
 NS_FORMS = {"auto": binding.NS_AUTO, "direct": binding.NS_DIRECT, "gram": binding.NS_GRAM}
 SELECT_RULES = {"l1": binding.SELECT_L1, "random": binding.SELECT_RANDOM}
 NS_FORM = binding.NS_AUTO
+NS_CHAINS = {"hilo": binding.CHAIN_HILO, "f16": binding.CHAIN_F16}
+NS_CHAIN = binding.CHAIN_HILO
 STEP = [0]      # optimizer step counter (the Random rule draws anew every step)
 STREAMS = []    # one stream per shape group when the groups run concurrently
 GROUPED = [False]   # one dion2_step_groups call for the whole stack
@@ -78,7 +82,7 @@ def one_step(wl, groups, alpha, rule=binding.SELECT_L1):
         binding.dion2_step_groups([(W, M, G, grp.axis) for grp, W, M, G in groups], alpha, wl.mu,
                                   wl.lr, wl.ns_steps, ns_form=NS_FORM, select_rule=rule,
                                   rand_seed=1234, rand_step=STEP[0], rand_matrix0=0,
-                                  group_streams=GROUP_STREAMS[0])
+                                  group_streams=GROUP_STREAMS[0], ns_chain=NS_CHAIN)
         return
     first = 0
     main = torch.cuda.current_stream()
@@ -90,12 +94,12 @@ def one_step(wl, groups, alpha, rule=binding.SELECT_L1):
         if STREAMS:
             s.wait_event(fork)
         with torch.cuda.stream(s):
-            if NS_FORM == binding.NS_AUTO and rule == binding.SELECT_L1:
+            if NS_FORM == binding.NS_AUTO and NS_CHAIN == binding.CHAIN_HILO and rule == binding.SELECT_L1:
                 binding.dion2_step_strided(W, M, G, alpha, wl.mu, wl.lr, wl.ns_steps, grp.axis)
             else:
                 binding.dion2_step_ex(W, M, G, alpha, wl.mu, wl.lr, wl.ns_steps, grp.axis,
                                       ns_form=NS_FORM, select_rule=rule, rand_seed=1234,
-                                      rand_step=STEP[0], rand_matrix0=first)
+                                      rand_step=STEP[0], rand_matrix0=first, ns_chain=NS_CHAIN)
         first += W.shape[0]
     for s in STREAMS:
         join = torch.cuda.Event()
@@ -214,6 +218,10 @@ def main(argv=None):
     ap.add_argument("--no-profile", action="store_true", help="skip the per-kernel event pass")
     ap.add_argument("--ns-form", default="auto", choices=sorted(NS_FORMS),
                     help="Newton-Schulz evaluation order (default: chosen by shape)")
+    ap.add_argument("--ns-chain", default="hilo", choices=sorted(NS_CHAINS),
+                    help="storage of the GRAM form's s x s matrices: bf16 hi/lo pairs "
+                         "(default) or scaled fp16 (one MFMA pass per product, less "
+                         "accurate on ill-conditioned inputs)")
     ap.add_argument("--split", type=int, default=1,
                     help="issue each shape group as this many sub-batch calls")
     ap.add_argument("--streams", type=int, default=-1,
@@ -226,14 +234,17 @@ def main(argv=None):
     ap.add_argument("--group-streams", type=int, default=0,
                     help="with --calls grouped: streams the library may spread the groups over "
                          "(0: its choice, 1: all on one stream)")
+    ap.add_argument("--no-chain-compare", action="store_true",
+                    help="skip timing the other GRAM chain storage (--ns-chain) at each fraction")
     ap.add_argument("--no-random-rule", action="store_true",
                     help="skip timing the Random selection rule at --alpha")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run plain 1 GiB device copies, the reference dispatches that "
                          "scale HBM byte counters (FETCH_SIZE / WRITE_SIZE) in a profiler run")
     args = ap.parse_args(argv)
-    global NS_FORM
+    global NS_FORM, NS_CHAIN
     NS_FORM = NS_FORMS[args.ns_form]
+    NS_CHAIN = NS_CHAINS[args.ns_chain]
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures the Dion2 step on one GPU only: there is no multi-GPU path "
@@ -317,6 +328,22 @@ def main(argv=None):
             per_alpha[str(a)] = round(statistics.mean(p2), 4)
             log(f"[bench] alpha={a}: {per_alpha[str(a)]:.3f} ms/step")
 
+    per_chain = {}
+    if not args.no_chain_compare:
+        own = NS_CHAIN
+        other = binding.CHAIN_F16 if own == binding.CHAIN_HILO else binding.CHAIN_HILO
+        names = {v: k for k, v in NS_CHAINS.items()}
+        per_chain[names[own]] = dict(per_alpha)
+        per_chain[names[other]] = {}
+        NS_CHAIN = other
+        try:
+            for a in ([alpha] if args.no_extra_alphas else list(dict.fromkeys([alpha, *wl.alphas]))):
+                p4, _ = time_steps(wl, groups, a, args.warmup, args.steps)
+                per_chain[names[other]][str(a)] = round(statistics.mean(p4), 4)
+                log(f"[bench] alpha={a}, chain {names[other]}: {per_chain[names[other]][str(a)]:.3f} ms/step")
+        finally:
+            NS_CHAIN = own
+
     per_rule = {"l1": round(ms, 4)}
     if not args.no_random_rule:
         p3, _ = time_steps(wl, groups, alpha, args.warmup, args.steps, binding.SELECT_RANDOM)
@@ -346,6 +373,7 @@ def main(argv=None):
         "config": {"workload": wl.name, "description": wl.description, "alpha": alpha,
                    "matrices": wl.matrices(), "elements": wl.elements(),
                    "ns_steps": wl.ns_steps, "mu": wl.mu, "lr": wl.lr, "ns_form": args.ns_form,
+                   "ns_chain": args.ns_chain,
                    "parallelism": "single GPU, batched per shape group",
                    "calls": args.calls, "group_streams": args.group_streams,
                    "streams": args.streams, "split": args.split},
@@ -353,6 +381,7 @@ def main(argv=None):
         "cpu_baseline": cpu,
         "per_alpha_ms": per_alpha,
         "per_rule_ms": per_rule,
+        "per_chain_ms": per_chain,
         "ns_mfma_frac": None if ns_frac is None else round(ns_frac, 4),
         "step_ms_stats": {"mean": round(ms, 4), "median": round(statistics.median(per), 4),
                           "min": round(min(per), 4), "mean_last_20": round(statistics.mean(tail), 4),

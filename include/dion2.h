@@ -31,9 +31,15 @@
  *               a three-pass bf16 hi/lo split of A;
  *       GRAM    the iteration carried on s x s matrices: with
  *               Q_t = a I + b A_t + c A_t^2 one has X_{t+1} = Q_t X_t and
- *               A_{t+1} = Q_t A_t Q_t, so X_T = (Q_{T-1} ... Q_0) X_0; every
- *               s x s product uses hi/lo pairs (three passes) and the final
- *               product two, so X is read only twice.
+ *               A_{t+1} = Q_t A_t Q_t, so X_T = (Q_{T-1} ... Q_0) X_0, and X
+ *               is read only twice. The s x s matrices are kept either as
+ *               bf16 hi/lo pairs (three MFMA passes per product) or in fp16
+ *               with a power-of-two scale per kind of matrix, derived from
+ *               the coefficients so that no value overflows or falls into
+ *               fp16's subnormal range (one pass, less accurate on
+ *               ill-conditioned inputs; dion2_options.ns_chain).
+ *               The final product takes P_T as a bf16 hi/lo pair (two
+ *               passes).
  *     Default coefficients are Muon's quintic (3.4445, -4.7750, 2.0315) at
  *     every step, eps = 1e-7.
  *   - The weight update is computed in fp64 from the fp32 O and rounded once
@@ -102,6 +108,20 @@ typedef enum dion2_ns_form {
     DION2_NS_GRAM = 2    /* iterate on s x s matrices, X read twice            */
 } dion2_ns_form;
 
+typedef enum dion2_ns_chain {
+    DION2_CHAIN_HILO = 0, /* GRAM s x s matrices as bf16 hi/lo pairs (default)  */
+    DION2_CHAIN_F16 = 1   /* GRAM s x s matrices in scaled fp16: one MFMA pass
+                             per product instead of three. The Gram matrix
+                             squares Z's condition number, and fp16 keeps 11
+                             significant bits, so accuracy drops for inputs
+                             whose spectrum is dominated by a few directions
+                             (kappa(Z)^2 beyond about 2^11); balanced wide
+                             inputs stay within 2x of HILO. With ns_coeffs
+                             that take the chain's values beyond 2^40 the call
+                             fails with DION2_ERR_UNSUPPORTED; a chain of one
+                             step (ns_steps = 1) uses HILO.                   */
+} dion2_ns_chain;
+
 /* Full-control options for dion2_step_ex. Fill with dion2_options_init. */
 typedef struct dion2_options {
     int w_dtype;             /* storage type of W (default DION2_DTYPE_BF16)        */
@@ -135,6 +155,7 @@ typedef struct dion2_options {
     int group_streams;       /* dion2_step_groups: how many streams the groups may
                                 run on at once (0 = the library's choice, 1 = all
                                 on the call's stream, at most 8)                   */
+    int ns_chain;            /* dion2_ns_chain (default DION2_CHAIN_HILO)           */
 } dion2_options;
 
 /* Defaults: bf16 W and G, Muon quintic, eps 1e-7, selective decay, internal

@@ -30,6 +30,7 @@ AXIS_COLS = 1
 DTYPE_F32 = 0
 DTYPE_BF16 = 1
 NS_AUTO, NS_DIRECT, NS_GRAM = 0, 1, 2
+CHAIN_HILO, CHAIN_F16 = 0, 1
 SELECT_L1, SELECT_RANDOM = 0, 1
 
 MAX_NS_STEPS = 16
@@ -68,6 +69,7 @@ class Options(ctypes.Structure):
         ("rand_step", ctypes.c_uint64),
         ("rand_matrix0", ctypes.c_int64),
         ("group_streams", c_int),
+        ("ns_chain", c_int),
     ]
 
 
@@ -219,35 +221,22 @@ def dion2_step_batched(Ws, Ms, Gs, alpha, mu=0.95, lr=0.02, ns_steps=5, axis=AXI
 def dion2_step_ex(W, M, G, alpha, mu=0.95, lr=0.02, ns_steps=5, axis=AXIS_AUTO, *,
                   ns_coeffs=None, ns_eps=1e-7, decay_all=False, workspace=None,
                   dbg_sel_idx=None, dbg_norms=None, dbg_update=None, ns_form=NS_AUTO,
-                  select_rule=SELECT_L1, rand_seed=0, rand_step=0, rand_matrix0=0, stream=None):
+                  select_rule=SELECT_L1, rand_seed=0, rand_step=0, rand_matrix0=0,
+                  ns_chain=CHAIN_HILO, stream=None):
     """Full control. W, M, G are [rows, cols] or [batch, rows, cols]; W and G
     may be bf16 or fp32. Debug outputs are preallocated device tensors:
     dbg_sel_idx int32 [batch, k], dbg_norms float64 [batch, d_sel],
     dbg_update float32 [batch, k, d_oth]. ns_form is NS_AUTO, NS_DIRECT or
-    NS_GRAM (the Newton-Schulz evaluation order). select_rule SELECT_RANDOM
-    draws the lines from Philox keys of (rand_seed, rand_step, rand_matrix0 + b)."""
+    NS_GRAM (the Newton-Schulz evaluation order); ns_chain CHAIN_HILO or
+    CHAIN_F16 (storage of the GRAM form's s x s matrices).
+    select_rule SELECT_RANDOM draws the lines from Philox keys of
+    (rand_seed, rand_step, rand_matrix0 + b)."""
     if W.dim() == 2:
         W, M, G = W.unsqueeze(0), M.unsqueeze(0), G.unsqueeze(0)
     _mats(W, M, G, 3)
     lib = load()
-    opt = Options()
-    lib.dion2_options_init(ctypes.byref(opt))
-    opt.w_dtype = _DT[W.dtype]
-    opt.g_dtype = _DT[G.dtype]
-    coeff_buf = None
-    if ns_coeffs is not None:
-        flat = [float(v) for abc in ns_coeffs for v in abc]
-        if len(flat) < 3 * ns_steps:
-            raise ValueError("ns_coeffs needs one (a, b, c) per Newton-Schulz step")
-        coeff_buf = (c_float * len(flat))(*flat)
-        opt.ns_coeffs = ctypes.cast(coeff_buf, POINTER(c_float))
-    opt.ns_eps = ns_eps
-    opt.decay_all = 1 if decay_all else 0
-    opt.ns_form = ns_form
-    opt.select_rule = select_rule
-    opt.rand_seed = rand_seed
-    opt.rand_step = rand_step
-    opt.rand_matrix0 = rand_matrix0
+    opt, coeff_buf = _options(W, G, ns_steps, ns_coeffs, ns_eps, decay_all, ns_form, select_rule,
+                              rand_seed, rand_step, rand_matrix0, ns_chain)
     for name, t, dt in (("dbg_sel_idx", dbg_sel_idx, torch.int32),
                         ("dbg_norms", dbg_norms, torch.float64),
                         ("dbg_update", dbg_update, torch.float32)):
@@ -264,10 +253,11 @@ def dion2_step_ex(W, M, G, alpha, mu=0.95, lr=0.02, ns_steps=5, axis=AXIS_AUTO, 
     _check(lib.dion2_step_ex(W.data_ptr(), M.data_ptr(), G.data_ptr(), batch, rows, cols, alpha,
                              mu, lr, ns_steps, axis, ctypes.byref(opt),
                              _stream_ptr(stream, W.device)))
+    del coeff_buf
 
 
 def _options(W, G, ns_steps, ns_coeffs, ns_eps, decay_all, ns_form, select_rule, rand_seed,
-             rand_step, rand_matrix0):
+             rand_step, rand_matrix0, ns_chain=CHAIN_HILO):
     """Options struct (and the coefficient buffer it points to, kept alive by the caller)."""
     lib = load()
     opt = Options()
@@ -288,12 +278,14 @@ def _options(W, G, ns_steps, ns_coeffs, ns_eps, decay_all, ns_form, select_rule,
     opt.rand_seed = rand_seed
     opt.rand_step = rand_step
     opt.rand_matrix0 = rand_matrix0
+    opt.ns_chain = ns_chain
     return opt, coeff_buf
 
 
 def dion2_step_groups(groups, alpha, mu=0.95, lr=0.02, ns_steps=5, *, ns_coeffs=None,
                       ns_eps=1e-7, decay_all=False, ns_form=NS_AUTO, select_rule=SELECT_L1,
-                      rand_seed=0, rand_step=0, rand_matrix0=0, group_streams=0, stream=None):
+                      rand_seed=0, rand_step=0, rand_matrix0=0, group_streams=0,
+                      ns_chain=CHAIN_HILO, stream=None):
     """Several same-shape stacks in one call: groups is a list of (W, M, G, axis)
     with W, M, G [batch, rows, cols] on one device, W and G of one dtype pair
     across groups. Bitwise the result of dion2_step_ex per group; groups of one
@@ -311,7 +303,7 @@ def dion2_step_groups(groups, alpha, mu=0.95, lr=0.02, ns_steps=5, *, ns_coeffs=
                        W.shape[2], axis)
     W0, _, G0, _ = groups[0]
     opt, keep = _options(W0, G0, ns_steps, ns_coeffs, ns_eps, decay_all, ns_form, select_rule,
-                         rand_seed, rand_step, rand_matrix0)
+                         rand_seed, rand_step, rand_matrix0, ns_chain)
     opt.group_streams = group_streams
     lib = load()
     _check(lib.dion2_step_groups(arr, len(groups), alpha, mu, lr, ns_steps, ctypes.byref(opt),

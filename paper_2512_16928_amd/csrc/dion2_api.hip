@@ -266,6 +266,72 @@ hipError_t timed(int phase, double flops, double bytes, int launches, hipStream_
 
 // ------------------------------------------------------ Newton-Schulz
 
+// Storage of the GRAM form's s x s matrices. Every one of them is a
+// polynomial in A_0 = Z Z^T, so its eigenvalues follow the scalar iteration
+// x_{t+1} = x_t q_t(x_t)^2, q_t(x) = a + b x + c x^2, from A_0's
+// eigenvalues, which lie in [0, ||Z||_F^2] = [0, 1] up to rounding; an entry
+// of a symmetric matrix is at most its spectral norm. Scanning x_0 over
+// [0, 1.0625] bounds A_t, Q_t = q_t(A_t), T_t = Q_t A_t and the partial
+// products P_t = Q_{t-1} ... Q_0. In the fp16 form each kind is stored as
+// fp16(2^e X), e chosen so that its bound lands at 2^14 or below: four times
+// under fp16's largest finite value, and entries down to 2^-28 of the bound
+// stay clear of fp16's subnormal range.
+struct ChainFmt {
+    bool f16 = false;
+    int eA = 0, eQ = 0, eT = 0, eP = 0;
+};
+
+bool chain_bounds(const float* coeffs, int ns_steps, ChainFmt* f) {
+    double mA = 1.0625, mQ = 0.0, mT = 0.0, mP = 0.0;
+    constexpr int kGrid = 2048;
+    for (int i = 0; i <= kGrid; ++i) {
+        double x = 1.0625 * i / kGrid, p = 1.0;
+        for (int t = 0; t < ns_steps; ++t) {
+            const float* cf = coeffs ? coeffs + 3 * t : kMuonQuintic;
+            const double q = (double)cf[0] + (double)cf[1] * x + (double)cf[2] * x * x;
+            mQ = std::fmax(mQ, std::fabs(q));
+            mT = std::fmax(mT, std::fabs(q * x));
+            p *= q;
+            x *= q * q;
+            if (t + 1 < ns_steps) {   // the last P is written as a hi / lo pair
+                mP = std::fmax(mP, std::fabs(p));
+                mA = std::fmax(mA, std::fabs(x));
+            }
+        }
+    }
+    auto expo = [](double m, int* e) {
+        if (!std::isfinite(m) || m > 0x1p40) return false;
+        *e = m < 0x1p-26 ? 40 : (int)std::floor(std::log2(16384.0 / m));
+        return true;
+    };
+    return expo(mA, &f->eA) && expo(mQ, &f->eQ) && expo(mT, &f->eT) && expo(mP, &f->eP);
+}
+
+// dion2_options.ns_chain resolved for a call: fp16 for chains of two or more
+// steps when asked for.
+int chain_format(const dion2_options& opt, int ns_steps, ChainFmt* f) {
+    *f = ChainFmt{};
+    if (opt.ns_chain != DION2_CHAIN_HILO && opt.ns_chain != DION2_CHAIN_F16)
+        return fail(DION2_ERR_INVALID_ARG, "ns_chain %d is not HILO or F16", opt.ns_chain);
+    if (opt.ns_chain != DION2_CHAIN_F16 || ns_steps < 2) return DION2_OK;
+    ChainFmt g;
+    if (opt.ns_coeffs) {
+        if (!chain_bounds(opt.ns_coeffs, ns_steps, &g))
+            return fail(DION2_ERR_UNSUPPORTED,
+                        "ns_chain F16: these coefficients take the chain's values beyond fp16's range");
+    } else {
+        static const std::vector<ChainFmt> tab = [] {
+            std::vector<ChainFmt> v(DION2_MAX_NS_STEPS + 1);
+            for (int n = 0; n <= DION2_MAX_NS_STEPS; ++n) chain_bounds(nullptr, n, &v[n]);
+            return v;
+        }();
+        g = tab[ns_steps];
+    }
+    g.f16 = true;
+    *f = g;
+    return DION2_OK;
+}
+
 // Z is the wide orientation [s_pad][l_pad] of the compact matrix; O receives
 // the result in the L layout [kpad][opad] (the transpose when Z is L^T).
 
@@ -413,46 +479,120 @@ hipError_t ns_direct(const Plan& P, uint16_t* Z0, uint16_t* Z1, uint16_t* const*
 // parts are separate so that a grouped call can run the chain of s x s
 // products once for several groups of the same padded size.
 
-// A_0 = Z Z^T as a hi / lo pair
-hipError_t gram_a0(const Plan& P, const uint16_t* Z, uint16_t* Ah, uint16_t* Al, hipStream_t stream) {
+// A_0 = Z Z^T as a hi / lo pair, or in fp16 (scaled) for the fp16 chain
+hipError_t gram_a0(const Plan& P, const uint16_t* Z, uint16_t* Ah, uint16_t* Al, const ChainFmt& fmt,
+                   hipStream_t stream) {
     const double s_r = (double)(P.k < P.d_oth ? P.k : P.d_oth);
     const double l_r = (double)(P.k < P.d_oth ? P.d_oth : P.k);
     const double nb = (double)P.batch;
-    const double gram_bytes = (2.0 * s_r * l_r + 4.0 * s_r * s_r) * nb;   // Z in, A hi + lo out
-    GemmArgs g = gram_args(P, Z, Ah, Al);
+    // Z in, A out (hi + lo, or fp16)
+    const double gram_bytes = (2.0 * s_r * l_r + (fmt.f16 ? 2.0 : 4.0) * s_r * s_r) * nb;
+    GemmArgs g = gram_args(P, Z, Ah, fmt.f16 ? nullptr : Al);
+    if (fmt.f16) g.oexp = fmt.eA;
     return timed(DION2_PHASE_NS_GRAM, sym_flops(s_r, l_r) * nb, gram_bytes, 1, stream,
-                 [&] { return launch_gemm(g, EPI_SPLIT, 1, stream); });
+                 [&] { return launch_gemm(g, fmt.f16 ? EPI_H16 : EPI_SPLIT, 1, stream); });
 }
 
 // Work of one group's s x s products, for the profiler. Per step: Q_t (from
 // A: hi + lo in and out, 8 s^2 bytes), P <- Q_t P and T = Q_t A (one dual
 // launch when both are due; each product two hi/lo operands in and one out,
-// 12 s^2, less the shared Q_t's 4 s^2 when fused), A <- Q_t T (12 s^2).
+// 12 s^2, less the shared Q_t's 4 s^2 when fused), A <- Q_t T (12 s^2). The
+// fp16 chain runs one pass per product on 2-byte entries, and its last
+// P product writes the 4-byte hi / lo pair.
 struct ChainCost {
     double flops = 0.0, bytes = 0.0;
 };
 int chain_products(int ns_steps) { return ns_steps + 3 * (ns_steps - 1); }
 int chain_launches(int ns_steps) { return ns_steps == 1 ? 1 : 3 * ns_steps - 1; }
-ChainCost chain_cost(const Plan& P, int ns_steps) {
+ChainCost chain_cost(const Plan& P, int ns_steps, const ChainFmt& fmt) {
     const double s_r = (double)(P.k < P.d_oth ? P.k : P.d_oth);
     const double nb = (double)P.batch;
     const int nprod = chain_products(ns_steps);
     const int ndual = ns_steps >= 3 ? ns_steps - 2 : 0;
+    const double per = (8.0 * ns_steps + 12.0 * (nprod - ns_steps) - 4.0 * ndual);
     ChainCost c;
-    c.flops = 3.0 * sym_flops(s_r, s_r) * nb * nprod;
-    c.bytes = (8.0 * ns_steps + 12.0 * (nprod - ns_steps) - 4.0 * ndual) * s_r * s_r * nb;
+    c.flops = (fmt.f16 ? 1.0 : 3.0) * sym_flops(s_r, s_r) * nb * nprod;
+    c.bytes = (fmt.f16 ? per / 2.0 + 2.0 : per) * s_r * s_r * nb;
     return c;
 }
 
 // The s x s products of `batch` matrices of padded side s_pad (buffers sq,
 // each [batch][s_pad][s_pad], A_0 in sq[SQ_AHI / SQ_ALO]). *cur_out tells
 // which P pair holds the product of the Q_t: SQ_P0* (0) or SQ_P1* (1).
+// The chain in fp16: the same products, one pass each, every matrix kept as
+// fp16(2^e X) with the exponents of ChainFmt (the host tracks which one each
+// buffer carries); the last P product writes the hi / lo pair the final
+// product reads.
+hipError_t chain_f16(const Plan& C, uint16_t* const* sq, int ns_steps, const dion2_options& opt,
+                     const ChainFmt& f, hipStream_t stream, int* cur_out) {
+    const int64_t s2 = C.s_pad * C.s_pad;
+    uint16_t* A = sq[SQ_AHI];
+    uint16_t* T = sq[SQ_THI];
+    uint16_t* Ph[2] = {sq[SQ_P0HI], sq[SQ_P1HI]};
+    uint16_t* Pl[2] = {sq[SQ_P0LO], sq[SQ_P1LO]};
+    auto prod = [&](const uint16_t* x, const uint16_t* y, void* out, int oexp) {
+        GemmArgs g = sym3_args(C, x, nullptr, y, nullptr, out, nullptr);
+        g.f16 = 1;
+        g.oexp = oexp;
+        return g;
+    };
+    int cur = 0, pexp = 0;
+    for (int t = 0; t < ns_steps; ++t) {
+        const float* cf = opt.ns_coeffs ? opt.ns_coeffs + 3 * t : kMuonQuintic;
+        // Q_t; the first one is P itself
+        uint16_t* q = t == 0 ? Ph[0] : sq[SQ_QHI];
+        GemmArgs g = prod(A, A, q, -2 * f.eA);
+        g.ca = cf[0];
+        g.cb = cf[1];
+        g.cc = cf[2];
+        g.E0 = A;
+        g.sE = s2;
+        g.lde = (int)C.s_pad;
+        g.eexp = -f.eA;
+        g.sexp = f.eQ;
+        hipError_t r = launch_gemm(g, EPI_QPOLY_H16, 1, stream);
+        if (r != hipSuccess) return r;
+        if (t == 0) pexp = f.eQ;
+        const bool do_p = t > 0, do_t = t + 1 < ns_steps;
+        if (!do_t) {   // the last step: P_T = Q_t P as the hi / lo pair
+            GemmArgs u = prod(q, Ph[cur], Ph[1 - cur], -f.eQ - pexp);
+            u.out1 = Pl[1 - cur];
+            r = launch_gemm(u, EPI_SPLIT, 1, stream);
+            if (r != hipSuccess) return r;
+            cur = 1 - cur;
+            break;
+        }
+        // P <- Q_t P (t > 0) and T = Q_t A in one dual launch, then A <- Q_t T
+        GemmArgs u = do_p ? prod(q, Ph[cur], Ph[1 - cur], f.eP - f.eQ - pexp)
+                          : prod(q, A, T, f.eT - f.eQ - f.eA);
+        if (do_p) {
+            u.dual = 1;
+            u.B0x = A;
+            u.out0x = T;
+            u.oexpx = f.eT - f.eQ - f.eA;
+        }
+        r = launch_gemm(u, EPI_H16, 1, stream);
+        if (r != hipSuccess) return r;
+        if (do_p) {
+            cur = 1 - cur;
+            pexp = f.eP;
+        }
+        r = launch_gemm(prod(q, T, A, f.eA - f.eQ - f.eT), EPI_H16, 1, stream);
+        if (r != hipSuccess) return r;
+    }
+    *cur_out = cur;
+    return hipSuccess;
+}
+
 hipError_t gram_chain(int batch, int64_t s_pad, uint16_t* const* sq, int ns_steps,
-                      const dion2_options& opt, const ChainCost& cost, hipStream_t stream,
-                      int* cur_out) {
+                      const dion2_options& opt, const ChainFmt& fmt, const ChainCost& cost,
+                      hipStream_t stream, int* cur_out) {
     Plan C{};
     C.batch = batch;
     C.s_pad = s_pad;
+    if (fmt.f16)
+        return timed(DION2_PHASE_NS_POLY, cost.flops, cost.bytes, chain_launches(ns_steps), stream,
+                     [&] { return chain_f16(C, sq, ns_steps, opt, fmt, stream, cur_out); });
     uint16_t* Ah = sq[SQ_AHI];
     uint16_t* Al = sq[SQ_ALO];
     uint16_t* Ph[2] = {sq[SQ_P0HI], sq[SQ_P1HI]};
@@ -520,11 +660,12 @@ hipError_t gram_final(const Plan& P, const uint16_t* Ph, const uint16_t* Pl, con
 }
 
 hipError_t ns_gram(const Plan& P, const uint16_t* Z, uint16_t* const* sq, float* O, int ns_steps,
-                   const dion2_options& opt, const FinalSpec& fin, hipStream_t stream) {
-    hipError_t e = gram_a0(P, Z, sq[SQ_AHI], sq[SQ_ALO], stream);
+                   const dion2_options& opt, const ChainFmt& fmt, const FinalSpec& fin,
+                   hipStream_t stream) {
+    hipError_t e = gram_a0(P, Z, sq[SQ_AHI], sq[SQ_ALO], fmt, stream);
     if (e != hipSuccess) return e;
     int cur = 0;
-    e = gram_chain(P.batch, P.s_pad, sq, ns_steps, opt, chain_cost(P, ns_steps), stream, &cur);
+    e = gram_chain(P.batch, P.s_pad, sq, ns_steps, opt, fmt, chain_cost(P, ns_steps, fmt), stream, &cur);
     if (e != hipSuccess) return e;
     return gram_final(P, cur ? sq[SQ_P1HI] : sq[SQ_P0HI], cur ? sq[SQ_P1LO] : sq[SQ_P0LO], Z, O, fin,
                       stream);
@@ -706,7 +847,8 @@ struct Tables {
 };
 
 int run_step(const Plan& P, void* W, float* M, const void* G, const Tables* tabs,
-             float mu, float lr, int ns_steps, const dion2_options& opt, hipStream_t stream) {
+             float mu, float lr, int ns_steps, const dion2_options& opt, const ChainFmt& fmt,
+             hipStream_t stream) {
     int dev = 0;
     hipError_t e = hipGetDevice(&dev);
     if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
@@ -786,7 +928,7 @@ int run_step(const Plan& P, void* W, float* M, const void* G, const Tables* tabs
     if (st != DION2_OK) return st;
     const FinalSpec fin = make_final(P, ms, b, lr, ns_steps, opt);
     if (ns_steps > 0) {   // with no step the gather has written O
-        e = P.gram ? ns_gram(P, b.Z0, b.sbuf, b.O, ns_steps, opt, fin, stream)
+        e = P.gram ? ns_gram(P, b.Z0, b.sbuf, b.O, ns_steps, opt, fmt, fin, stream)
                    : ns_direct(P, b.Z0, b.Z1, b.sbuf, b.O, ns_steps, opt, fin, stream);
         if (e != hipSuccess) return hip_fail(e, "launch K4 Newton-Schulz");
     }
@@ -829,6 +971,9 @@ int step_impl(void* W, float* M, const void* G, const Tables* tabs, int batch, i
     if (st != DION2_OK) return st;
     st = validate_common(mu, lr, ns_steps, opt);
     if (st != DION2_OK) return st;
+    ChainFmt fmt;
+    st = chain_format(opt, ns_steps, &fmt);
+    if (st != DION2_OK) return st;
     if (opt.select_rule == DION2_SELECT_RANDOM &&
         (opt.rand_matrix0 < 0 || opt.rand_matrix0 + batch > (int64_t(1) << 32)))
         return fail(DION2_ERR_INVALID_ARG, "rand_matrix0 %lld with batch %d leaves [0, 2^32)",
@@ -854,7 +999,7 @@ int step_impl(void* W, float* M, const void* G, const Tables* tabs, int batch, i
             return fail(DION2_ERR_WORKSPACE, "workspace of %zu bytes is below the %zu needed",
                         opt.workspace_bytes, P.total);
     }
-    return run_step(P, W, M, G, tabs, mu, lr, ns_steps, opt, static_cast<hipStream_t>(stream));
+    return run_step(P, W, M, G, tabs, mu, lr, ns_steps, opt, fmt, static_cast<hipStream_t>(stream));
 }
 
 // Several same-shape groups in one call. Each group runs K1-K3 in its own
@@ -891,6 +1036,9 @@ int groups_impl(const dion2_group* groups, int ngroups, float alpha, float mu, f
         return fail(DION2_ERR_INVALID_ARG, "group_streams %d not in [0, %d]", opt.group_streams,
                     kMaxGroupStreams);
     int st = validate_common(mu, lr, ns_steps, opt);
+    if (st != DION2_OK) return st;
+    ChainFmt fmt;
+    st = chain_format(opt, ns_steps, &fmt);
     if (st != DION2_OK) return st;
 
     struct Chain {
@@ -1040,7 +1188,7 @@ int groups_impl(const dion2_group* groups, int ngroups, float alpha, float mu, f
         if (st != DION2_OK) return st;
         fins[g] = make_final(P, ms, b, lr, ns_steps, gopt[g]);
         if (c >= 0) {
-            e = gram_a0(P, b.Z0, b.sbuf[SQ_AHI], b.sbuf[SQ_ALO], s);
+            e = gram_a0(P, b.Z0, b.sbuf[SQ_AHI], b.sbuf[SQ_ALO], fmt, s);
             if (e != hipSuccess) return hip_fail(e, "launch K4 Gram");
             if (nS > 1) {
                 e = hipEventRecord(ev_a0[g], s);
@@ -1049,7 +1197,7 @@ int groups_impl(const dion2_group* groups, int ngroups, float alpha, float mu, f
             continue;
         }
         if (ns_steps > 0) {
-            e = P.gram ? ns_gram(P, b.Z0, b.sbuf, b.O, ns_steps, gopt[g], fins[g], s)
+            e = P.gram ? ns_gram(P, b.Z0, b.sbuf, b.O, ns_steps, gopt[g], fmt, fins[g], s)
                        : ns_direct(P, b.Z0, b.Z1, b.sbuf, b.O, ns_steps, gopt[g], fins[g], s);
             if (e != hipSuccess) return hip_fail(e, "launch K4 Newton-Schulz");
         }
@@ -1065,7 +1213,7 @@ int groups_impl(const dion2_group* groups, int ngroups, float alpha, float mu, f
         ChainCost cost;
         for (int g = 0; g < ngroups; ++g) {
             if (chain_of[g] != c) continue;
-            const ChainCost cg = chain_cost(plans[g], ns_steps);
+            const ChainCost cg = chain_cost(plans[g], ns_steps, fmt);
             cost.flops += cg.flops;
             cost.bytes += cg.bytes;
             if (nS > 1) {
@@ -1075,7 +1223,7 @@ int groups_impl(const dion2_group* groups, int ngroups, float alpha, float mu, f
         }
         uint16_t* sq[SQ_GRAM_COUNT];
         for (int i = 0; i < SQ_GRAM_COUNT; ++i) sq[i] = chain_buf(c, i);
-        e = gram_chain(chains[c].batch, chains[c].s_pad, sq, ns_steps, opt, cost, s, &chain_cur[c]);
+        e = gram_chain(chains[c].batch, chains[c].s_pad, sq, ns_steps, opt, fmt, cost, s, &chain_cur[c]);
         if (e != hipSuccess) return hip_fail(e, "launch K4 s x s products");
         if (nS > 1) {
             e = hipEventRecord(ev_chain[c], s);
@@ -1123,6 +1271,7 @@ void dion2_options_init(dion2_options* opt) {
     opt->rand_step = 0;
     opt->rand_matrix0 = 0;
     opt->group_streams = 0;
+    opt->ns_chain = DION2_CHAIN_HILO;
 }
 
 int dion2_step(void* W, float* M, const void* G, int64_t rows, int64_t cols, float alpha,

@@ -237,10 +237,16 @@ hipError_t launch_decay_all(const DecayAllArgs& a, hipStream_t s);
 //              the L layout) is not stored; the update step is applied
 //              directly: W[K[p]][j] <- bf16(W[K[p]][j] - lr_eff O[p][j]) for
 //              p < k, j < d_oth (bf16 W, cols % 8 == 0); dbg gets O if set
-// The symmetric products (EPI_SPLIT, EPI_POLY, EPI_QPOLY) compute the tiles
-// on and above the diagonal and mirror them.
+//   EPI_H16    (B as rows [N][K], symmetric C; npass 1): out0 = fp16(2^oexp C)
+//   EPI_QPOLY_H16 (B as rows [N][K], npass 1, fp16 operands and E0):
+//              Q = ca I + cb 2^eexp E0 + cc 2^oexp C, out0 = fp16(2^sexp Q)
+// With f16 set the operands are fp16 (one pass); EPI_SPLIT then stores
+// 2^oexp C as the hi / lo pair. The power-of-two exponents keep the fp16
+// values of the Gram-form chain clear of fp16's overflow and subnormal range.
+// The symmetric products (EPI_SPLIT, EPI_POLY, EPI_QPOLY, EPI_H16,
+// EPI_QPOLY_H16) compute the tiles on and above the diagonal and mirror them.
 enum GemmEpi { EPI_SPLIT = 0, EPI_POLY = 1, EPI_UPDATE = 2, EPI_FINAL = 3, EPI_QPOLY = 4,
-               EPI_APPLY = 5 };
+               EPI_APPLY = 5, EPI_H16 = 6, EPI_QPOLY_H16 = 7 };
 struct GemmArgs {
     const uint16_t* A0; const uint16_t* A1;   // A operand(s), [M][K] ld lda
     const uint16_t* B0; const uint16_t* B1;   // B operand(s), [N][K] or [K][N], ld ldb
@@ -253,11 +259,15 @@ struct GemmArgs {
     void* out0; int64_t sOut0; int ldo0;
     void* out1; int64_t sOut1; int ldo1;
     int out_transposed;                        // EPI_FINAL: write out0[j][i]
-    // dual launch (EPI_SPLIT, npass 3): a second product with the same A
-    // operand, B = B0x/B1x into out0x/out1x, computed in the same grid
+    // dual launch (EPI_SPLIT npass 3, or EPI_H16): a second product with the
+    // same A operand, B = B0x/B1x into out0x/out1x (scale 2^oexpx), computed
+    // in the same grid
     int dual;
     const uint16_t* B0x; const uint16_t* B1x;
     void* out0x; void* out1x;
+    // fp16 Gram-form chain: fp16 operands, and the scale exponents above
+    int f16;
+    int oexp, oexpx, eexp, sexp;
     // EPI_APPLY only
     MatSet ms;                                 // W
     const int32_t* sel;                        // [batch][k]

@@ -21,6 +21,10 @@
 // source lane s at row s/4, column 4 (s mod 4) hands lane i four
 // consecutive K values of column i.
 //
+// The GRAM form's chain of s x s products runs the same way on bf16 hi / lo
+// pairs (three passes), or, as an option, on scaled fp16 matrices with
+// v_mfma_f32_32x32x16_f16 (one pass; EPI_H16 and EPI_QPOLY_H16 store fp16).
+//
 // Tiling for gfx950: a BM x BN output tile per block of WM x WN wave64s,
 // each wave a (BM/WM) x (BN/WN) tile of v_mfma_f32_32x32x16_bf16 blocks.
 // K-slices (BK deep) go from global memory straight into an S-stage LDS
@@ -32,13 +36,16 @@
 // and the transposing reads hit distinct LDS banks; each lane fetches the
 // global chunk that belongs in its LDS slot. Tiles are numbered XCD-aware;
 // the symmetric products (A and B) compute only the tiles on and above the
-// diagonal and write each one twice. The epilogue goes through a per-wave
+// diagonal and write each one twice, so that the stored matrix is exactly
+// symmetric. The epilogue goes through a per-wave
 // 32 x 32 LDS tile: each lane finishes 16 entries of a row there, and the
 // block then leaves in whole row segments (64 bytes of bf16 or 128 bytes of
 // fp32 per row), row-major or transposed for the mirrored copy.
 //
 // All dimensions are multiples of the tile (compact buffers are zero padded
 // to 128, and the padding stays zero through every step).
+#include <type_traits>
+
 #include "dion2_device.h"
 
 namespace dion2 {
@@ -47,6 +54,7 @@ namespace {
 constexpr int kXcds = 8;   // accelerator complex dies on MI355X
 
 typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8;
+typedef __attribute__((ext_vector_type(8))) _Float16 f16x8;
 typedef __attribute__((ext_vector_type(4))) short i16x4;
 typedef __attribute__((ext_vector_type(16))) float f32x16;
 typedef __attribute__((address_space(3))) void lds_void;
@@ -58,9 +66,30 @@ __device__ __forceinline__ uint32_t pack2(float x, float y) {
     return __builtin_bit_cast(uint32_t, v);
 }
 
-template <int NPASS, int BT_, int BM_, int BN_, int BK_, int WM_, int WN_, int S_>
+// two fp32 -> packed fp16 pair (RNE)
+__device__ __forceinline__ uint32_t pack2h(float x, float y) {
+    typedef __attribute__((ext_vector_type(2))) _Float16 f16x2;
+    const f16x2 v = {(_Float16)x, (_Float16)y};
+    return __builtin_bit_cast(uint32_t, v);
+}
+
+__device__ __forceinline__ float f16_bits_to_f32(uint32_t h) {
+    return (float)__builtin_bit_cast(_Float16, (uint16_t)h);
+}
+
+// One 32 x 32 x 16 MFMA block on bf16 or fp16 fragments.
+__device__ __forceinline__ f32x16 mfma32(bf16x8 a, bf16x8 b, f32x16 c) {
+    return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+}
+__device__ __forceinline__ f32x16 mfma32(f16x8 a, f16x8 b, f32x16 c) {
+    return __builtin_amdgcn_mfma_f32_32x32x16_f16(a, b, c, 0, 0, 0);
+}
+
+template <int NPASS, int BT_, int BM_, int BN_, int BK_, int WM_, int WN_, int S_, bool F16_ = false>
 struct Tile {
     static constexpr int BT = BT_, S = S_;
+    static constexpr bool F16 = F16_;                    // fp16 operands (else bf16)
+    using Frag = typename std::conditional<F16_, f16x8, bf16x8>::type;
     static constexpr int BM = BM_, BN = BN_, BK = BK_, WM = WM_, WN = WN_;
     static constexpr int WAVES = WM * WN;
     static constexpr int THREADS = 64 * WAVES;
@@ -89,6 +118,7 @@ struct Tile {
     static_assert(NPASS >= 1 && NPASS <= 3, "one to three passes");
     static_assert(!BT || (NPASS <= 2 && BN == 128), "the [K][N] B operand: one or two passes, BN 128");
     static_assert(S >= 2 && S <= 4, "two to four stages");
+    static_assert(!F16 || (NPASS == 1 && !BT), "fp16 operands: one pass, B as rows");
 };
 
 // Byte offset, inside a K-major tile, of logical 16-byte chunk c of row r.
@@ -175,7 +205,8 @@ __device__ __forceinline__ void mma_slice(f32x16 (&acc)[T::FM][T::FN], const uns
     const int brow = wn * T::TN + (lane & 31);
     const int half = lane >> 5;
     constexpr int KK = T::BK / 16;
-    bf16x8 fa0[2][T::FM], fb0[2][T::FN], fa1[2][T::FM], fb1[2][T::FN];
+    using Frag = typename T::Frag;
+    Frag fa0[2][T::FM], fb0[2][T::FN], fa1[2][T::FM], fb1[2][T::FN];
 #pragma unroll
     for (int kk = 0; kk <= KK; ++kk) {
         if (kk < KK) {
@@ -183,24 +214,24 @@ __device__ __forceinline__ void mma_slice(f32x16 (&acc)[T::FM][T::FN], const uns
             const int slot = kk & 1;
 #pragma unroll
             for (int i = 0; i < T::FM; ++i)
-                fa0[slot][i] = *reinterpret_cast<const bf16x8*>(sa0 + kmajor_off<T>(arow + i * 32, c));
+                fa0[slot][i] = *reinterpret_cast<const Frag*>(sa0 + kmajor_off<T>(arow + i * 32, c));
 #pragma unroll
             for (int j = 0; j < T::FN; ++j) {
                 if constexpr (T::BT) {
                     fb0[slot][j] = b_frag_tr<T>(sb0, kk * 16, wn * T::TN + j * 32, lane);
                 } else {
-                    fb0[slot][j] = *reinterpret_cast<const bf16x8*>(sb0 + kmajor_off<T>(brow + j * 32, c));
+                    fb0[slot][j] = *reinterpret_cast<const Frag*>(sb0 + kmajor_off<T>(brow + j * 32, c));
                 }
             }
             if constexpr (NPASS >= 2) {
 #pragma unroll
                 for (int i = 0; i < T::FM; ++i)
-                    fa1[slot][i] = *reinterpret_cast<const bf16x8*>(sa1 + kmajor_off<T>(arow + i * 32, c));
+                    fa1[slot][i] = *reinterpret_cast<const Frag*>(sa1 + kmajor_off<T>(arow + i * 32, c));
             }
             if constexpr (NPASS == 3) {
 #pragma unroll
                 for (int j = 0; j < T::FN; ++j)
-                    fb1[slot][j] = *reinterpret_cast<const bf16x8*>(sb1 + kmajor_off<T>(brow + j * 32, c));
+                    fb1[slot][j] = *reinterpret_cast<const Frag*>(sb1 + kmajor_off<T>(brow + j * 32, c));
             }
         }
         if (kk > 0) {
@@ -209,11 +240,9 @@ __device__ __forceinline__ void mma_slice(f32x16 (&acc)[T::FM][T::FN], const uns
             for (int i = 0; i < T::FM; ++i)
 #pragma unroll
                 for (int j = 0; j < T::FN; ++j) {
-                    if constexpr (NPASS == 3)
-                        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa0[slot][i], fb1[slot][j], acc[i][j], 0, 0, 0);
-                    if constexpr (NPASS >= 2)
-                        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa1[slot][i], fb0[slot][j], acc[i][j], 0, 0, 0);
-                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa0[slot][i], fb0[slot][j], acc[i][j], 0, 0, 0);
+                    if constexpr (NPASS == 3) acc[i][j] = mfma32(fa0[slot][i], fb1[slot][j], acc[i][j]);
+                    if constexpr (NPASS >= 2) acc[i][j] = mfma32(fa1[slot][i], fb0[slot][j], acc[i][j]);
+                    acc[i][j] = mfma32(fa0[slot][i], fb0[slot][j], acc[i][j]);
                 }
         }
     }
@@ -225,11 +254,20 @@ __device__ __forceinline__ void mma_slice(f32x16 (&acc)[T::FM][T::FN], const uns
 // outputs four lanes cover a row's 64 bytes (16 rows per instruction), for
 // fp32 eight lanes its 128 bytes, so every store instruction writes
 // contiguous segments of few cache lines. With TR the tile is read
-// transposed (output row q = tile column q), for the mirrored block.
+// transposed (output row q = tile column q), for the mirrored block; with
+// diag (a block on the diagonal of a symmetric product) the entries below
+// the diagonal are taken from their mirror images above it.
 template <int EPI, typename T, bool TR>
 __device__ __forceinline__ void store_block(const GemmArgs& a, int b, const float* stage, int64_t orow0,
-                                            int64_t ocol0, int lane) {
-    auto at = [&](int r, int c) { return TR ? stage[c * T::EPI_LD + r] : stage[r * T::EPI_LD + c]; };
+                                            int64_t ocol0, int lane, bool diag = false) {
+    auto at = [&](int r, int c) {
+        if (diag && c < r) {
+            const int t = r;
+            r = c;
+            c = t;
+        }
+        return TR ? stage[c * T::EPI_LD + r] : stage[r * T::EPI_LD + c];
+    };
     if constexpr (EPI == EPI_FINAL) {
         const int c4 = 4 * (lane & 7);
 #pragma unroll
@@ -258,6 +296,10 @@ __device__ __forceinline__ void store_block(const GemmArgs& a, int b, const floa
                 uint16_t* lp = static_cast<uint16_t*>(a.out1) + (int64_t)b * a.sOut1 + (orow0 + r) * a.ldo1 + ocol0 + c8;
                 *reinterpret_cast<uint4*>(hp) = make_uint4(h[0], h[1], h[2], h[3]);
                 *reinterpret_cast<uint4*>(lp) = make_uint4(l[0], l[1], l[2], l[3]);
+            } else if constexpr (EPI == EPI_H16 || EPI == EPI_QPOLY_H16) {
+                uint16_t* op = static_cast<uint16_t*>(a.out0) + (int64_t)b * a.sOut0 + (orow0 + r) * a.ldo0 + ocol0 + c8;
+                *reinterpret_cast<uint4*>(op) = make_uint4(pack2h(v[0], v[1]), pack2h(v[2], v[3]),
+                                                           pack2h(v[4], v[5]), pack2h(v[6], v[7]));
             } else {   // EPI_POLY, EPI_UPDATE: bf16
                 uint16_t* op = static_cast<uint16_t*>(a.out0) + (int64_t)b * a.sOut0 + (orow0 + r) * a.ldo0 + ocol0 + c8;
                 *reinterpret_cast<uint4*>(op) = make_uint4(pack2(v[0], v[1]), pack2(v[2], v[3]),
@@ -288,6 +330,7 @@ __global__ __launch_bounds__(T::THREADS) void gemm(GemmArgs a) {
             a.B1 = a.B1x;
             a.out0 = a.out0x;
             a.out1 = a.out1x;
+            a.oexp = a.oexpx;
         }
         b >>= 1;
     }
@@ -330,7 +373,7 @@ __global__ __launch_bounds__(T::THREADS) void gemm(GemmArgs a) {
     const int er = lane >> 1;          // epilogue: row (or transposed row) of this lane
     const int ec = (lane & 1) * 16;    // epilogue: 16 consecutive columns
     constexpr bool kPreE0 = EPI == EPI_POLY || EPI == EPI_QPOLY || EPI == EPI_UPDATE || EPI == EPI_FINAL ||
-                            EPI == EPI_APPLY;
+                            EPI == EPI_APPLY || EPI == EPI_QPOLY_H16;
     constexpr bool kPreE1 = EPI == EPI_POLY || EPI == EPI_QPOLY;
     const bool pre = kPreE0 && a.E0 != nullptr && !(EPI == EPI_FINAL && a.out_transposed);
     uint4 e0[T::FM][T::FN][2], e1[T::FM][T::FN][2];
@@ -408,16 +451,26 @@ __global__ __launch_bounds__(T::THREADS) void gemm(GemmArgs a) {
     // The tile belongs to its wave alone and LDS accesses of one wave complete
     // in issue order, so wave barriers order the staging.
     float* stage = reinterpret_cast<float*>(smem_raw) + wave * 32 * T::EPI_LD;
+    // the fp16 chain's products carry power-of-two scales (exact)
+    constexpr bool kScaled = T::F16 || EPI == EPI_H16;
+    const float osc = kScaled ? __builtin_amdgcn_ldexpf(1.0f, a.oexp) : 1.0f;
 #pragma unroll
     for (int i = 0; i < T::FM; ++i) {
 #pragma unroll
         for (int j = 0; j < T::FN; ++j) {
             const int R = row0 + wm * T::TM + i * 32;   // block origin in the output
             const int Cc = col0 + wn * T::TN + j * 32;
+            // A symmetric product is stored exactly symmetric: blocks above
+            // the diagonal are written twice, blocks on it from their upper
+            // triangle, and blocks below it (in diagonal tiles) not at all.
+            // Rounding leaves the computed product slightly asymmetric;
+            // carried along, that asymmetry feeds the Gram chain's unstable
+            // directions.
+            if (SYM && R > Cc) continue;
 #pragma unroll
             for (int r = 0; r < 16; ++r) {
                 const int m = (r >> 2) * 8 + (lane >> 5) * 4 + (r & 3);
-                stage[m * T::EPI_LD + (lane & 31)] = acc[i][j][r];
+                stage[m * T::EPI_LD + (lane & 31)] = kScaled ? acc[i][j][r] * osc : acc[i][j][r];
             }
             __builtin_amdgcn_wave_barrier();
             float v[16];
@@ -472,6 +525,26 @@ __global__ __launch_bounds__(T::THREADS) void gemm(GemmArgs a) {
                             if (er == ec + q) v[q] += a.ca;
                     }
                 }
+            } else if constexpr (EPI == EPI_QPOLY_H16) {
+                // Q = a I + b A + c A^2 from the fp16 A (scale 2^-eexp back
+                // to A), stored as fp16(2^sexp Q)
+                const float esc = __builtin_amdgcn_ldexpf(1.0f, a.eexp);
+                const float ssc = __builtin_amdgcn_ldexpf(1.0f, a.sexp);
+                const uint4 h0 = e0[i][j][0];
+                const uint4 h1 = e0[i][j][1];
+                const uint32_t hw[8] = {h0.x, h0.y, h0.z, h0.w, h1.x, h1.y, h1.z, h1.w};
+#pragma unroll
+                for (int q = 0; q < 8; ++q) {
+                    v[2 * q] = a.cb * (esc * f16_bits_to_f32(hw[q] & 0xffffu)) + a.cc * v[2 * q];
+                    v[2 * q + 1] = a.cb * (esc * f16_bits_to_f32(hw[q] >> 16)) + a.cc * v[2 * q + 1];
+                }
+                if (R == Cc) {
+#pragma unroll
+                    for (int q = 0; q < 16; ++q)
+                        if (er == ec + q) v[q] += a.ca;
+                }
+#pragma unroll
+                for (int q = 0; q < 16; ++q) v[q] *= ssc;
             }
             if constexpr (EPI == EPI_APPLY) {
                 // W[K[p]][j] <- bf16(W[K[p]][j] - lr_eff O[p][j]) (update step, eq. (1))
@@ -512,8 +585,8 @@ __global__ __launch_bounds__(T::THREADS) void gemm(GemmArgs a) {
 #pragma unroll
                 for (int q = 0; q < 16; ++q) stage[er * T::EPI_LD + ec + q] = v[q];
                 __builtin_amdgcn_wave_barrier();
-                store_block<EPI, T, false>(a, b, stage, orow - er, ocol - ec, lane);
-                if (SYM && row0 != col0) store_block<EPI, T, true>(a, b, stage, (int64_t)Cc, (int64_t)R, lane);
+                store_block<EPI, T, false>(a, b, stage, orow - er, ocol - ec, lane, SYM && R == Cc);
+                if (SYM && R != Cc) store_block<EPI, T, true>(a, b, stage, (int64_t)Cc, (int64_t)R, lane);
             }
             __builtin_amdgcn_wave_barrier();   // the stage tile is rewritten next
         }
@@ -548,6 +621,21 @@ hipError_t launch_gemm(const GemmArgs& a, GemmEpi epi, int npass, hipStream_t s)
     using TP = Tile<3, 0, 128, 128, 32, 4, 2, 2>;    // three-pass symmetric products
     using TU = Tile<1, 1, 128, 128, 32, 2, 2, 2>;    // update (B operand [K][N])
     using TU2 = Tile<2, 1, 128, 128, 32, 2, 2, 2>;   // two-pass final product
+    using TH = Tile<1, 0, 128, 128, 32, 2, 2, 4, true>;   // fp16 s x s products
+    if (a.f16) {
+        if (npass != 1) return hipErrorInvalidValue;
+        switch (epi) {
+            case EPI_SPLIT:
+                if (a.dual) break;
+                return launch_tile<1, EPI_SPLIT, TH, true>(a, s);
+            case EPI_H16: return launch_tile<1, EPI_H16, TH, true>(a, s);
+            case EPI_QPOLY_H16:
+                if (a.dual) break;
+                return launch_tile<1, EPI_QPOLY_H16, TH, true>(a, s);
+            default: break;
+        }
+        return hipErrorInvalidValue;
+    }
     if (a.dual && !(epi == EPI_SPLIT && npass == 3)) return hipErrorInvalidValue;
     switch (epi) {
         case EPI_SPLIT:
@@ -555,6 +643,10 @@ hipError_t launch_gemm(const GemmArgs& a, GemmEpi epi, int npass, hipStream_t s)
             if (npass != 1) break;
             if (a.M >= 1024 && a.M % 256 == 0) return launch_tile<1, EPI_SPLIT, TGL, true>(a, s);
             return launch_tile<1, EPI_SPLIT, TG, true>(a, s);
+        case EPI_H16:   // the Gram matrix of bf16 Z into the fp16 chain
+            if (npass != 1) break;
+            if (a.M >= 1024 && a.M % 256 == 0) return launch_tile<1, EPI_H16, TGL, true>(a, s);
+            return launch_tile<1, EPI_H16, TG, true>(a, s);
         case EPI_POLY:
             if (npass == 3) return launch_tile<3, EPI_POLY, TP, true>(a, s);
             break;

@@ -117,6 +117,12 @@ def test_ex_options_validation(lib):
     assert ex(select_rule=1, rand_matrix0=-1) == DION2_ERR_INVALID_ARG
     assert ex(select_rule=1, rand_matrix0=1 << 32) == DION2_ERR_INVALID_ARG   # batch of 1
     assert "2^32" in binding.dion2_last_error()
+    assert ex(ns_chain=2) == DION2_ERR_INVALID_ARG and "ns_chain" in binding.dion2_last_error()
+    assert ex(ns_chain=-1) == DION2_ERR_INVALID_ARG
+    big = (ctypes.c_float * 6)(1e5, 0.0, 0.0, 1e5, 0.0, 0.0)   # A_1 = 1e10 A_0, T_1 = 1e15 A_0
+    big_p = ctypes.cast(big, ctypes.POINTER(ctypes.c_float))
+    assert ex(ns_chain=binding.CHAIN_F16, ns_coeffs=big_p) == DION2_ERR_UNSUPPORTED
+    assert "fp16" in binding.dion2_last_error()
     coeffs = (ctypes.c_float * 6)(1.0, 2.0, 3.0, 1.0, float("inf"), 0.0)
     assert ex(ns_coeffs=ctypes.cast(coeffs, ctypes.POINTER(ctypes.c_float))) == DION2_ERR_INVALID_ARG
     need = binding.dion2_workspace_size(1, 64, 64, 0.25)

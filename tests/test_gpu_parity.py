@@ -5,7 +5,8 @@ Acceptance (per matrix):
   * the l1 line norms equal the oracle's exactly rounded sums bitwise;
   * the momentum M equals the oracle's fp32 result bitwise;
   * the Newton-Schulz output O (debug output, before the lr scale) is within
-    relative Frobenius error 2e-2 of the oracle's fp64 result (bf16 MFMA);
+    relative Frobenius error 2e-2 of the oracle's fp64 result (bf16 and fp16
+    MFMA);
   * W equals the oracle's update rule applied to the GPU's O bitwise, so
     unselected lines are untouched and the selected ones are rounded once.
 """
@@ -29,10 +30,11 @@ def rel_fro(a, b):
 
 
 FORMS = pytest.mark.parametrize("form", [NS_DIRECT, NS_GRAM], ids=["direct", "gram"])
+CHAINS = pytest.mark.parametrize("chain", [binding.CHAIN_HILO, binding.CHAIN_F16], ids=["hilo", "f16"])
 
 
 def run_gpu(W, M, G, alpha, ns_steps=5, axis=AXIS_AUTO, mu=0.95, lr=0.02, coeffs=None,
-            decay_all=False, form=binding.NS_AUTO, rand=None):
+            decay_all=False, form=binding.NS_AUTO, rand=None, chain=binding.CHAIN_HILO):
     """One library call on stacks [B, rows, cols]; returns host copies and the
     debug outputs."""
     B, rows, cols = W.shape
@@ -49,7 +51,7 @@ def run_gpu(W, M, G, alpha, ns_steps=5, axis=AXIS_AUTO, mu=0.95, lr=0.02, coeffs
                      rand_matrix0=rand[2])
     binding.dion2_step_ex(W, M, G, alpha, mu, lr, ns_steps, axis, ns_coeffs=coeffs,
                           decay_all=decay_all, dbg_sel_idx=sel, dbg_norms=nrm, dbg_update=upd,
-                          ns_form=form, **extra)
+                          ns_form=form, ns_chain=chain, **extra)
     torch.cuda.synchronize()
     return dict(W=W.cpu(), M=M.cpu(), K=sel.cpu(), norms=nrm.cpu(), O=upd.cpu(), W0=W0, M0=M0,
                 G=G.cpu(), axis=ax, k=k)
@@ -162,6 +164,69 @@ def test_ns_schedules(hip_device, ns_steps, coeffs, form, rows, cols):
     W, M, G = workloads.make_group(wl, 0, hip_device)
     res = run_gpu(W, M, G, 0.5, ns_steps=ns_steps, coeffs=coeffs, form=form)
     check_matrix(res, 0, 0.5, ns_steps=ns_steps, coeffs=coeffs)
+
+
+@pytest.mark.parametrize("ns_steps,coeffs", [
+    (2, None), (3, [(1.5, -0.5, 0.0)] * 3),
+    (4, [(3.0, -3.2, 1.2), (2.0, -1.5, 0.5), (1.5, -0.5, 0.0), (1.5, -0.5, 0.0)]),
+    (8, [(3.4445, -4.7750, 2.0315)] * 6 + [(1.875, -1.25, 0.375)] * 2),
+])
+def test_f16_chain_schedules(hip_device, ns_steps, coeffs):
+    """The fp16 chain takes its scales from the coefficients: forced on a
+    per-step schedule it stays within tolerance of the oracle."""
+    wl = one_group_workload(160, 640, name=f"f16sched{ns_steps}")
+    W, M, G = workloads.make_group(wl, 0, hip_device)
+    res = run_gpu(W, M, G, 0.5, ns_steps=ns_steps, coeffs=coeffs, form=NS_GRAM,
+                  chain=binding.CHAIN_F16)
+    check_matrix(res, 0, 0.5, ns_steps=ns_steps, coeffs=coeffs)
+
+
+def test_f16_chain_of_one_step_is_hilo(hip_device):
+    """A chain of one step has no product to gain from fp16: it runs in hi/lo."""
+    wl = one_group_workload(128, 512, count=2, name="f16one")
+    W, M, G = workloads.make_group(wl, 0, hip_device)
+    W2, M2 = W.clone(), M.clone()
+    binding.dion2_step_ex(W, M, G, 0.5, 0.95, 0.02, 1, ns_form=NS_GRAM, ns_chain=binding.CHAIN_F16)
+    binding.dion2_step_ex(W2, M2, G, 0.5, 0.95, 0.02, 1, ns_form=NS_GRAM, ns_chain=binding.CHAIN_HILO)
+    torch.cuda.synchronize()
+    assert torch.equal(W.view(torch.int16), W2.view(torch.int16)) and torch.equal(M, M2)
+
+
+@pytest.mark.parametrize("wl_name,gi,first,alpha", [
+    ("1b", 0, 9, 0.25),          # 2048x2048: s = 512, l = 2048
+    ("1b", 1, 4, 0.25),          # 8192x2048, columns: s = 512, l = 8192
+    ("1b-colsel", 2, 3, 0.25),   # 5% of the columns with x20 gradients
+    ("moe", 0, 70, 0.25),        # 2048x1408 expert: s = 352 padded to 384
+])
+def test_gram_chain_storage(hip_device, wl_name, gi, first, alpha):
+    """Both storages of the GRAM chain against the oracle on one matrix of a
+    benchmark shape. The fp16 chain keeps 11 significant bits where the hi/lo
+    pairs keep about 16; on these wide, balanced matrices Z's own bf16
+    rounding dominates both, and fp16 stays within twice the hi/lo error."""
+    wl = workloads.WORKLOADS[wl_name]
+    grp = wl.groups[gi]
+    W, M, G = workloads.make_group(wl, gi, hip_device, first=first, count=1)
+    errs = {}
+    for chain in (binding.CHAIN_HILO, binding.CHAIN_F16):
+        res = run_gpu(W.clone(), M.clone(), G, alpha, axis=grp.axis, form=NS_GRAM, chain=chain)
+        errs[chain] = check_matrix(res, 0, alpha, axis=grp.axis)
+    assert errs[binding.CHAIN_F16] <= 2.0 * errs[binding.CHAIN_HILO] + 1e-3, errs
+
+
+@pytest.mark.parametrize("rows,cols,alpha,axis", [
+    (200, 328, 0.25, AXIS_AUTO),    # rows, s = 50, l = 328
+    (328, 200, 0.25, AXIS_AUTO),    # columns, s = 50
+    (130, 75, 0.5, AXIS_AUTO),      # columns, s = 38, l = 130
+    (384, 640, 0.1, AXIS_AUTO),     # rows, s = 39
+    (256, 1024, 0.5, AXIS_ROWS),    # s = 128: one whole tile
+    (640, 1664, 0.3, AXIS_ROWS),    # s = 192 padded to 256: mirrored off-diagonal tiles
+])
+def test_f16_chain_ragged(hip_device, rows, cols, alpha, axis):
+    """The fp16 chain on ragged wide shapes (padding inside the s x s tiles)."""
+    wl = one_group_workload(rows, cols, axis=axis, name=f"f16r{rows}c{cols}")
+    W, M, G = workloads.make_group(wl, 0, hip_device)
+    res = run_gpu(W, M, G, alpha, axis=axis, form=NS_GRAM, chain=binding.CHAIN_F16)
+    check_matrix(res, 0, alpha, axis=axis)
 
 
 def test_decay_all_ablation(hip_device):
@@ -420,7 +485,8 @@ def test_groups_single_group_equals_strided(hip_device):
     assert torch.equal(M, M2) and torch.equal(W.view(torch.int16), W2.view(torch.int16))
 
 
-@pytest.mark.parametrize("case", ["f32-decay-all-schedule", "forced-direct", "forced-gram", "no-steps"])
+@pytest.mark.parametrize("case", ["f32-decay-all-schedule", "forced-direct", "forced-gram", "no-steps",
+                                  "f16-chain", "f16-chain-schedule"])
 def test_groups_options_equal_per_group_calls(hip_device, case):
     """Options reach every group of a grouped call as they reach dion2_step_ex:
     fp32 W and G, the decay-all ablation, a per-step coefficient schedule, a
@@ -438,6 +504,11 @@ def test_groups_options_equal_per_group_calls(hip_device, case):
         kw = dict(ns_form=NS_DIRECT)
     elif case == "forced-gram":
         kw = dict(ns_form=NS_GRAM)
+    elif case == "f16-chain":
+        kw = dict(ns_form=NS_GRAM, ns_chain=binding.CHAIN_F16)
+    elif case == "f16-chain-schedule":
+        kw = dict(ns_form=NS_GRAM, ns_chain=binding.CHAIN_F16,
+                  ns_coeffs=[(3.4445, -4.7750, 2.0315)] * 4 + [(1.5, -0.5, 0.0)])
     else:
         ns_steps = 0
     stacks = [workloads.make_group(wl, gi, hip_device) for gi in range(len(wl.groups))]
