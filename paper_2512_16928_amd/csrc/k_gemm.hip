@@ -255,17 +255,13 @@ __device__ __forceinline__ void mma_slice(f32x16 (&acc)[T::FM][T::FN], const uns
 // fp32 eight lanes its 128 bytes, so every store instruction writes
 // contiguous segments of few cache lines. With TR the tile is read
 // transposed (output row q = tile column q), for the mirrored block; with
-// diag (a block on the diagonal of a symmetric product) the entries below
+// DIAG (a block on the diagonal of a symmetric product) the entries below
 // the diagonal are taken from their mirror images above it.
-template <int EPI, typename T, bool TR>
+template <int EPI, typename T, bool TR, bool DIAG = false>
 __device__ __forceinline__ void store_block(const GemmArgs& a, int b, const float* stage, int64_t orow0,
-                                            int64_t ocol0, int lane, bool diag = false) {
+                                            int64_t ocol0, int lane) {
     auto at = [&](int r, int c) {
-        if (diag && c < r) {
-            const int t = r;
-            r = c;
-            c = t;
-        }
+        if (DIAG && c < r) return stage[c * T::EPI_LD + r];
         return TR ? stage[c * T::EPI_LD + r] : stage[r * T::EPI_LD + c];
     };
     if constexpr (EPI == EPI_FINAL) {
@@ -585,8 +581,12 @@ __global__ __launch_bounds__(T::THREADS) void gemm(GemmArgs a) {
 #pragma unroll
                 for (int q = 0; q < 16; ++q) stage[er * T::EPI_LD + ec + q] = v[q];
                 __builtin_amdgcn_wave_barrier();
-                store_block<EPI, T, false>(a, b, stage, orow - er, ocol - ec, lane, SYM && R == Cc);
-                if (SYM && R != Cc) store_block<EPI, T, true>(a, b, stage, (int64_t)Cc, (int64_t)R, lane);
+                if (SYM && R == Cc) {
+                    store_block<EPI, T, false, true>(a, b, stage, orow - er, ocol - ec, lane);
+                } else {
+                    store_block<EPI, T, false>(a, b, stage, orow - er, ocol - ec, lane);
+                    if (SYM) store_block<EPI, T, true>(a, b, stage, (int64_t)Cc, (int64_t)R, lane);
+                }
             }
             __builtin_amdgcn_wave_barrier();   // the stage tile is rewritten next
         }
