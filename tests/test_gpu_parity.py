@@ -336,6 +336,30 @@ def test_1b_stack_full_size_sampled(hip_device, gi, alpha, samples):
         check_matrix(res, 0, alpha)
 
 
+@pytest.mark.parametrize("gi,sample", [(0, 40), (1, 11), (2, 2)])
+def test_1b_stack_full_size_f16_chain(hip_device, gi, sample):
+    """The opt-in fp16 chain over a whole 1B-stack group in one batched call
+    (the configuration the benchmark's per_chain_ms times), one sampled
+    matrix checked in full."""
+    wl = workloads.WORKLOADS["1b"]
+    W, M, G = workloads.make_group(wl, gi, hip_device)
+    grp = wl.groups[gi]
+    k, ax = binding.dion2_plan_info(grp.rows, grp.cols, 0.25, grp.axis)
+    d_sel, d_oth = (grp.rows, grp.cols) if ax == AXIS_ROWS else (grp.cols, grp.rows)
+    sel = torch.empty((grp.count, k), dtype=torch.int32, device=hip_device)
+    nrm = torch.empty((grp.count, d_sel), dtype=torch.float64, device=hip_device)
+    upd = torch.empty((grp.count, k, d_oth), dtype=torch.float32, device=hip_device)
+    snap = (W[sample].cpu(), M[sample].cpu(), G[sample].cpu())
+    binding.dion2_step_ex(W, M, G, 0.25, dbg_sel_idx=sel, dbg_norms=nrm, dbg_update=upd,
+                          ns_chain=binding.CHAIN_F16)
+    torch.cuda.synchronize()
+    res = dict(W0=snap[0][None], M0=snap[1][None], G=snap[2][None], W=W[sample].cpu()[None],
+               M=M[sample].cpu()[None], K=sel[sample].cpu()[None], norms=nrm[sample].cpu()[None],
+               O=upd[sample].cpu()[None], axis=ax, k=k)
+    err = check_matrix(res, 0, 0.25)
+    assert err <= 5e-3, f"fp16 chain at a 1B shape: {err:.3e}"
+
+
 def test_colsel_spikes_selected(hip_device):
     """Column selection on 2048x8192 with 5% of columns spiked x20: every
     spiked column is selected, and the sampled matrix matches the oracle."""
