@@ -22,6 +22,7 @@ steps 20). Prints one JSON line:
 from __future__ import annotations
 
 import argparse
+import dataclasses
 import glob
 import json
 import os
@@ -222,6 +223,8 @@ def main(argv=None):
                     help="storage of the GRAM form's s x s matrices: bf16 hi/lo pairs "
                          "(default) or scaled fp16 (one MFMA pass per product, less "
                          "accurate on ill-conditioned inputs)")
+    ap.add_argument("--ns-steps", type=int, default=None,
+                    help="Newton-Schulz steps (default: the workload's, 5)")
     ap.add_argument("--split", type=int, default=1,
                     help="issue each shape group as this many sub-batch calls")
     ap.add_argument("--streams", type=int, default=-1,
@@ -271,6 +274,8 @@ def main(argv=None):
         log("[bench] ran 3 plain 1 GiB copies (torch.neg) for counter calibration")
 
     wl = workloads.WORKLOADS[args.workload]
+    if args.ns_steps is not None:
+        wl = dataclasses.replace(wl, ns_steps=args.ns_steps)
     alpha = args.alpha if args.alpha is not None else wl.alphas[0]
     GROUPED[0] = args.calls == "grouped"
     GROUP_STREAMS[0] = args.group_streams
