@@ -18,6 +18,8 @@ steps 20). Prints one JSON line:
   per_rule_ms  the l1 (Default) and Random selection rules at --alpha
   per_chain_ms the GRAM chain's storage: bf16 hi/lo pairs (the default) and
                the opt-in scaled fp16 (ns_chain), at every fraction
+  per_master_ms X rounded once to bf16 (the default) against the opt-in fp32
+               master (ns_master), at every fraction
 """
 from __future__ import annotations
 
@@ -68,6 +70,8 @@ SELECT_RULES = {"l1": binding.SELECT_L1, "random": binding.SELECT_RANDOM}
 NS_FORM = binding.NS_AUTO
 NS_CHAINS = {"hilo": binding.CHAIN_HILO, "f16": binding.CHAIN_F16}
 NS_CHAIN = binding.CHAIN_HILO
+NS_MASTERS = {"bf16": binding.MASTER_BF16, "fp32": binding.MASTER_FP32}
+NS_MASTER = binding.MASTER_BF16
 STEP = [0]      # optimizer step counter (the Random rule draws anew every step)
 STREAMS = []    # one stream per shape group when the groups run concurrently
 GROUPED = [False]   # one dion2_step_groups call for the whole stack
@@ -83,7 +87,8 @@ def one_step(wl, groups, alpha, rule=binding.SELECT_L1):
         binding.dion2_step_groups([(W, M, G, grp.axis) for grp, W, M, G in groups], alpha, wl.mu,
                                   wl.lr, wl.ns_steps, ns_form=NS_FORM, select_rule=rule,
                                   rand_seed=1234, rand_step=STEP[0], rand_matrix0=0,
-                                  group_streams=GROUP_STREAMS[0], ns_chain=NS_CHAIN)
+                                  group_streams=GROUP_STREAMS[0], ns_chain=NS_CHAIN,
+                                  ns_master=NS_MASTER)
         return
     first = 0
     main = torch.cuda.current_stream()
@@ -95,12 +100,14 @@ def one_step(wl, groups, alpha, rule=binding.SELECT_L1):
         if STREAMS:
             s.wait_event(fork)
         with torch.cuda.stream(s):
-            if NS_FORM == binding.NS_AUTO and NS_CHAIN == binding.CHAIN_HILO and rule == binding.SELECT_L1:
+            if (NS_FORM == binding.NS_AUTO and NS_CHAIN == binding.CHAIN_HILO
+                    and NS_MASTER == binding.MASTER_BF16 and rule == binding.SELECT_L1):
                 binding.dion2_step_strided(W, M, G, alpha, wl.mu, wl.lr, wl.ns_steps, grp.axis)
             else:
                 binding.dion2_step_ex(W, M, G, alpha, wl.mu, wl.lr, wl.ns_steps, grp.axis,
                                       ns_form=NS_FORM, select_rule=rule, rand_seed=1234,
-                                      rand_step=STEP[0], rand_matrix0=first, ns_chain=NS_CHAIN)
+                                      rand_step=STEP[0], rand_matrix0=first, ns_chain=NS_CHAIN,
+                                      ns_master=NS_MASTER)
         first += W.shape[0]
     for s in STREAMS:
         join = torch.cuda.Event()
@@ -223,6 +230,9 @@ def main(argv=None):
                     help="storage of the GRAM form's s x s matrices: bf16 hi/lo pairs "
                          "(default) or scaled fp16 (one MFMA pass per product, less "
                          "accurate on ill-conditioned inputs)")
+    ap.add_argument("--ns-master", default="bf16", choices=sorted(NS_MASTERS),
+                    help="X rounded once to bf16 (default), or kept as a bf16 hi/lo pair through "
+                         "every product (fp32; runs in the GRAM order)")
     ap.add_argument("--ns-steps", type=int, default=None,
                     help="Newton-Schulz steps (default: the workload's, 5)")
     ap.add_argument("--split", type=int, default=1,
@@ -245,9 +255,10 @@ def main(argv=None):
                     help="also run plain 1 GiB device copies, the reference dispatches that "
                          "scale HBM byte counters (FETCH_SIZE / WRITE_SIZE) in a profiler run")
     args = ap.parse_args(argv)
-    global NS_FORM, NS_CHAIN
+    global NS_FORM, NS_CHAIN, NS_MASTER
     NS_FORM = NS_FORMS[args.ns_form]
     NS_CHAIN = NS_CHAINS[args.ns_chain]
+    NS_MASTER = NS_MASTERS[args.ns_master]
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures the Dion2 step on one GPU only: there is no multi-GPU path "
@@ -333,21 +344,31 @@ def main(argv=None):
             per_alpha[str(a)] = round(statistics.mean(p2), 4)
             log(f"[bench] alpha={a}: {per_alpha[str(a)]:.3f} ms/step")
 
-    per_chain = {}
-    if not args.no_chain_compare:
+    alphas = [alpha] if args.no_extra_alphas else list(dict.fromkeys([alpha, *wl.alphas]))
+    per_chain, per_master = {}, {}
+    if not args.no_chain_compare and NS_MASTER == binding.MASTER_BF16 and NS_FORM != binding.NS_DIRECT:
+        # the other storage of the GRAM chain, and the fp32 master, at every fraction
         own = NS_CHAIN
         other = binding.CHAIN_F16 if own == binding.CHAIN_HILO else binding.CHAIN_HILO
         names = {v: k for k, v in NS_CHAINS.items()}
         per_chain[names[own]] = dict(per_alpha)
         per_chain[names[other]] = {}
-        NS_CHAIN = other
+        per_master = {"bf16": dict(per_alpha), "fp32": {}}
         try:
-            for a in ([alpha] if args.no_extra_alphas else list(dict.fromkeys([alpha, *wl.alphas]))):
+            for a in alphas:
+                NS_CHAIN = other
                 p4, _ = time_steps(wl, groups, a, args.warmup, args.steps)
                 per_chain[names[other]][str(a)] = round(statistics.mean(p4), 4)
                 log(f"[bench] alpha={a}, chain {names[other]}: {per_chain[names[other]][str(a)]:.3f} ms/step")
+                NS_CHAIN = binding.CHAIN_HILO
+                NS_MASTER = binding.MASTER_FP32
+                p5, _ = time_steps(wl, groups, a, args.warmup, args.steps)
+                per_master["fp32"][str(a)] = round(statistics.mean(p5), 4)
+                log(f"[bench] alpha={a}, fp32 master: {per_master['fp32'][str(a)]:.3f} ms/step")
+                NS_MASTER = binding.MASTER_BF16
         finally:
             NS_CHAIN = own
+            NS_MASTER = binding.MASTER_BF16
 
     per_rule = {"l1": round(ms, 4)}
     if not args.no_random_rule:
@@ -378,7 +399,7 @@ def main(argv=None):
         "config": {"workload": wl.name, "description": wl.description, "alpha": alpha,
                    "matrices": wl.matrices(), "elements": wl.elements(),
                    "ns_steps": wl.ns_steps, "mu": wl.mu, "lr": wl.lr, "ns_form": args.ns_form,
-                   "ns_chain": args.ns_chain,
+                   "ns_chain": args.ns_chain, "ns_master": args.ns_master,
                    "parallelism": "single GPU, batched per shape group",
                    "calls": args.calls, "group_streams": args.group_streams,
                    "streams": args.streams, "split": args.split},
@@ -387,6 +408,7 @@ def main(argv=None):
         "per_alpha_ms": per_alpha,
         "per_rule_ms": per_rule,
         "per_chain_ms": per_chain,
+        "per_master_ms": per_master,
         "ns_mfma_frac": None if ns_frac is None else round(ns_frac, 4),
         "step_ms_stats": {"mean": round(ms, 4), "median": round(statistics.median(per), 4),
                           "min": round(min(per), 4), "mean_last_20": round(statistics.mean(tail), 4),

@@ -40,6 +40,10 @@
  *               ill-conditioned inputs; dion2_options.ns_chain).
  *               The final product takes P_T as a bf16 hi/lo pair (two
  *               passes).
+ *     With dion2_options.ns_master = DION2_MASTER_FP32, X itself is kept as
+ *     a bf16 hi/lo pair (about 16 significant bits) instead of being rounded
+ *     once to bf16: the Gram matrix and the final product take three passes,
+ *     and the iteration runs in the GRAM order.
  *     Default coefficients are Muon's quintic (3.4445, -4.7750, 2.0315) at
  *     every step, eps = 1e-7.
  *   - The weight update is computed in fp64 from the fp32 O and rounded once
@@ -122,6 +126,18 @@ typedef enum dion2_ns_chain {
                              step (ns_steps = 1) uses HILO.                   */
 } dion2_ns_chain;
 
+typedef enum dion2_ns_master {
+    DION2_MASTER_BF16 = 0, /* X rounded once to bf16 (default)                 */
+    DION2_MASTER_FP32 = 1  /* X as a bf16 hi/lo pair through every product: the
+                              GRAM order with hi/lo s x s matrices, three-pass
+                              Gram and final products. Needs ns_form AUTO or
+                              GRAM (DIRECT: DION2_ERR_UNSUPPORTED) and ns_chain
+                              HILO (F16: DION2_ERR_INVALID_ARG). Costs three
+                              times the Gram products and 1.5 times the final
+                              one; the result is 10 to 70 times closer to the
+                              exact iteration                                */
+} dion2_ns_master;
+
 /* Full-control options for dion2_step_ex. Fill with dion2_options_init. */
 typedef struct dion2_options {
     int w_dtype;             /* storage type of W (default DION2_DTYPE_BF16)        */
@@ -156,6 +172,7 @@ typedef struct dion2_options {
                                 run on at once (0 = the library's choice, 1 = all
                                 on the call's stream, at most 8)                   */
     int ns_chain;            /* dion2_ns_chain (default DION2_CHAIN_HILO)           */
+    int ns_master;           /* dion2_ns_master (default DION2_MASTER_BF16)         */
 } dion2_options;
 
 /* Defaults: bf16 W and G, Muon quintic, eps 1e-7, selective decay, internal
@@ -226,8 +243,9 @@ int dion2_step_groups(const dion2_group* groups, int ngroups, float alpha,
                       const dion2_options* opt, void* stream);
 
 /* Bytes of device workspace one call with these arguments needs (for
-   dion2_options.workspace) with ns_form = DION2_NS_AUTO; a forced form may
-   need more (dion2_step_ex then fails with DION2_ERR_WORKSPACE). Returns 0
+   dion2_options.workspace) with ns_form = DION2_NS_AUTO and ns_master =
+   DION2_MASTER_BF16; a forced form or the fp32 master may need more
+   (dion2_step_ex then fails with DION2_ERR_WORKSPACE). Returns 0
    for invalid arguments. */
 size_t dion2_workspace_size(int batch, int64_t rows, int64_t cols,
                             float alpha, int axis);

@@ -31,6 +31,7 @@ DTYPE_F32 = 0
 DTYPE_BF16 = 1
 NS_AUTO, NS_DIRECT, NS_GRAM = 0, 1, 2
 CHAIN_HILO, CHAIN_F16 = 0, 1
+MASTER_BF16, MASTER_FP32 = 0, 1
 SELECT_L1, SELECT_RANDOM = 0, 1
 
 MAX_NS_STEPS = 16
@@ -70,6 +71,7 @@ class Options(ctypes.Structure):
         ("rand_matrix0", ctypes.c_int64),
         ("group_streams", c_int),
         ("ns_chain", c_int),
+        ("ns_master", c_int),
     ]
 
 
@@ -222,13 +224,15 @@ def dion2_step_ex(W, M, G, alpha, mu=0.95, lr=0.02, ns_steps=5, axis=AXIS_AUTO, 
                   ns_coeffs=None, ns_eps=1e-7, decay_all=False, workspace=None,
                   dbg_sel_idx=None, dbg_norms=None, dbg_update=None, ns_form=NS_AUTO,
                   select_rule=SELECT_L1, rand_seed=0, rand_step=0, rand_matrix0=0,
-                  ns_chain=CHAIN_HILO, stream=None):
+                  ns_chain=CHAIN_HILO, ns_master=MASTER_BF16, stream=None):
     """Full control. W, M, G are [rows, cols] or [batch, rows, cols]; W and G
     may be bf16 or fp32. Debug outputs are preallocated device tensors:
     dbg_sel_idx int32 [batch, k], dbg_norms float64 [batch, d_sel],
     dbg_update float32 [batch, k, d_oth]. ns_form is NS_AUTO, NS_DIRECT or
     NS_GRAM (the Newton-Schulz evaluation order); ns_chain CHAIN_HILO or
-    CHAIN_F16 (storage of the GRAM form's s x s matrices).
+    CHAIN_F16 (storage of the GRAM form's s x s matrices); ns_master
+    MASTER_BF16 or MASTER_FP32 (X rounded once to bf16, or kept as a hi/lo
+    pair through every product).
     select_rule SELECT_RANDOM draws the lines from Philox keys of
     (rand_seed, rand_step, rand_matrix0 + b)."""
     if W.dim() == 2:
@@ -236,7 +240,7 @@ def dion2_step_ex(W, M, G, alpha, mu=0.95, lr=0.02, ns_steps=5, axis=AXIS_AUTO, 
     _mats(W, M, G, 3)
     lib = load()
     opt, coeff_buf = _options(W, G, ns_steps, ns_coeffs, ns_eps, decay_all, ns_form, select_rule,
-                              rand_seed, rand_step, rand_matrix0, ns_chain)
+                              rand_seed, rand_step, rand_matrix0, ns_chain, ns_master)
     for name, t, dt in (("dbg_sel_idx", dbg_sel_idx, torch.int32),
                         ("dbg_norms", dbg_norms, torch.float64),
                         ("dbg_update", dbg_update, torch.float32)):
@@ -257,7 +261,7 @@ def dion2_step_ex(W, M, G, alpha, mu=0.95, lr=0.02, ns_steps=5, axis=AXIS_AUTO, 
 
 
 def _options(W, G, ns_steps, ns_coeffs, ns_eps, decay_all, ns_form, select_rule, rand_seed,
-             rand_step, rand_matrix0, ns_chain=CHAIN_HILO):
+             rand_step, rand_matrix0, ns_chain=CHAIN_HILO, ns_master=MASTER_BF16):
     """Options struct (and the coefficient buffer it points to, kept alive by the caller)."""
     lib = load()
     opt = Options()
@@ -279,13 +283,14 @@ def _options(W, G, ns_steps, ns_coeffs, ns_eps, decay_all, ns_form, select_rule,
     opt.rand_step = rand_step
     opt.rand_matrix0 = rand_matrix0
     opt.ns_chain = ns_chain
+    opt.ns_master = ns_master
     return opt, coeff_buf
 
 
 def dion2_step_groups(groups, alpha, mu=0.95, lr=0.02, ns_steps=5, *, ns_coeffs=None,
                       ns_eps=1e-7, decay_all=False, ns_form=NS_AUTO, select_rule=SELECT_L1,
                       rand_seed=0, rand_step=0, rand_matrix0=0, group_streams=0,
-                      ns_chain=CHAIN_HILO, stream=None):
+                      ns_chain=CHAIN_HILO, ns_master=MASTER_BF16, stream=None):
     """Several same-shape stacks in one call: groups is a list of (W, M, G, axis)
     with W, M, G [batch, rows, cols] on one device, W and G of one dtype pair
     across groups. Bitwise the result of dion2_step_ex per group; groups of one
@@ -303,7 +308,7 @@ def dion2_step_groups(groups, alpha, mu=0.95, lr=0.02, ns_steps=5, *, ns_coeffs=
                        W.shape[2], axis)
     W0, _, G0, _ = groups[0]
     opt, keep = _options(W0, G0, ns_steps, ns_coeffs, ns_eps, decay_all, ns_form, select_rule,
-                         rand_seed, rand_step, rand_matrix0, ns_chain)
+                         rand_seed, rand_step, rand_matrix0, ns_chain, ns_master)
     opt.group_streams = group_streams
     lib = load()
     _check(lib.dion2_step_groups(arr, len(groups), alpha, mu, lr, ns_steps, ctypes.byref(opt),

@@ -60,6 +60,7 @@ struct Plan {
     int batch;
     int nrb, rb_rows;         // column-mode reduction blocking
     bool gram;                // Newton-Schulz on s x s matrices (DION2_NS_GRAM)
+    bool master;              // X kept as a hi / lo pair (DION2_MASTER_FP32; implies gram)
     // workspace offsets
     size_t o_l1, o_sq, o_part, o_sel, o_rank, o_scale, o_Z, o_Z1, o_S, S_bytes, o_O, o_tables, total;
 };
@@ -71,7 +72,7 @@ enum { SQ_QHI = 2, SQ_QLO, SQ_THI, SQ_TLO, SQ_P0HI, SQ_P0LO, SQ_P1HI, SQ_P1LO, S
 // own_sq = false leaves out the s x s buffers (a grouped call carves them
 // once for every group of a shared Newton-Schulz chain).
 int make_plan(int batch, int64_t rows, int64_t cols, float alpha, int axis, int ns_form, Plan* p,
-              bool own_sq = true) {
+              bool own_sq = true, bool master = false) {
     if (batch < 1 || batch > 65535) return fail(DION2_ERR_INVALID_ARG, "batch %d not in [1, 65535]", batch);
     if (rows < 1 || cols < 1)
         return fail(DION2_ERR_INVALID_ARG, "rows (%lld) and cols (%lld) must be >= 1",
@@ -101,6 +102,9 @@ int make_plan(int batch, int64_t rows, int64_t cols, float alpha, int axis, int 
     // The GRAM form trades 2 (s x l) GEMMs and the X traffic of every step
     // for about four three-pass s x s products; it pays once X is wide.
     P.gram = ns_form == DION2_NS_GRAM || (ns_form == DION2_NS_AUTO && P.l_pad >= 3 * P.s_pad);
+    // the fp32 master runs in the GRAM order (its caller rejects a forced DIRECT)
+    P.master = master;
+    if (master) P.gram = true;
     P.batch = batch;
     P.nrb = P.axis == 1 ? (int)momentum_col_blocks(rows, &P.rb_rows) : 0;
     if (P.axis == 0) P.rb_rows = 0;
@@ -120,7 +124,7 @@ int make_plan(int batch, int64_t rows, int64_t cols, float alpha, int axis, int 
     P.o_scale = take(B * 8);
     const size_t comp = B * (size_t)P.kpad * (size_t)P.opad * 2;
     P.o_Z = take(comp);
-    P.o_Z1 = take(P.gram ? 0 : comp);
+    P.o_Z1 = take(P.gram && !P.master ? 0 : comp);   // DIRECT's ping-pong copy, or the lo half of X
     P.S_bytes = align256(B * (size_t)P.s_pad * (size_t)P.s_pad * 2);
     P.o_S = take(own_sq ? P.S_bytes * (P.gram ? SQ_GRAM_COUNT : SQ_DIRECT_COUNT) : 0);
     P.o_O = take(B * (size_t)P.kpad * (size_t)P.opad * 4);
@@ -479,18 +483,21 @@ hipError_t ns_direct(const Plan& P, uint16_t* Z0, uint16_t* Z1, uint16_t* const*
 // parts are separate so that a grouped call can run the chain of s x s
 // products once for several groups of the same padded size.
 
-// A_0 = Z Z^T as a hi / lo pair, or in fp16 (scaled) for the fp16 chain
-hipError_t gram_a0(const Plan& P, const uint16_t* Z, uint16_t* Ah, uint16_t* Al, const ChainFmt& fmt,
-                   hipStream_t stream) {
+// A_0 = Z Z^T as a hi / lo pair, or in fp16 (scaled) for the fp16 chain.
+// With Zlo (the fp32 master) Z is the pair Z + Zlo: three passes.
+hipError_t gram_a0(const Plan& P, const uint16_t* Z, const uint16_t* Zlo, uint16_t* Ah, uint16_t* Al,
+                   const ChainFmt& fmt, hipStream_t stream) {
     const double s_r = (double)(P.k < P.d_oth ? P.k : P.d_oth);
     const double l_r = (double)(P.k < P.d_oth ? P.d_oth : P.k);
     const double nb = (double)P.batch;
-    // Z in, A out (hi + lo, or fp16)
-    const double gram_bytes = (2.0 * s_r * l_r + (fmt.f16 ? 2.0 : 4.0) * s_r * s_r) * nb;
+    const int npass = Zlo ? 3 : 1;
+    // Z in (hi, and lo), A out (hi + lo, or fp16)
+    const double gram_bytes = ((Zlo ? 4.0 : 2.0) * s_r * l_r + (fmt.f16 ? 2.0 : 4.0) * s_r * s_r) * nb;
     GemmArgs g = gram_args(P, Z, Ah, fmt.f16 ? nullptr : Al);
     if (fmt.f16) g.oexp = fmt.eA;
-    return timed(DION2_PHASE_NS_GRAM, sym_flops(s_r, l_r) * nb, gram_bytes, 1, stream,
-                 [&] { return launch_gemm(g, fmt.f16 ? EPI_H16 : EPI_SPLIT, 1, stream); });
+    if (Zlo) g.A1 = g.B1 = Zlo;
+    return timed(DION2_PHASE_NS_GRAM, npass * sym_flops(s_r, l_r) * nb, gram_bytes, 1, stream,
+                 [&] { return launch_gemm(g, fmt.f16 ? EPI_H16 : EPI_SPLIT, npass, stream); });
 }
 
 // Work of one group's s x s products, for the profiler. Per step: Q_t (from
@@ -645,30 +652,33 @@ hipError_t gram_chain(int batch, int64_t s_pad, uint16_t* const* sq, int ns_step
     return e;
 }
 
-// O = (P_hi + P_lo) Z, or the update step applied in the epilogue
+// O = (P_hi + P_lo) Z, or the update step applied in the epilogue; with Zlo
+// (the fp32 master) Z is the pair Z + Zlo and the product takes three passes.
 hipError_t gram_final(const Plan& P, const uint16_t* Ph, const uint16_t* Pl, const uint16_t* Z,
-                      float* O, const FinalSpec& fin, hipStream_t stream) {
+                      const uint16_t* Zlo, float* O, const FinalSpec& fin, hipStream_t stream) {
     const double s_r = (double)(P.k < P.d_oth ? P.k : P.d_oth);
     const double l_r = (double)(P.k < P.d_oth ? P.d_oth : P.k);
     const double nb = (double)P.batch;
     GemmArgs x = right_args(P, Ph, Pl, Z);
+    if (Zlo) x.B1 = Zlo;
     const GemmEpi epi = final_output(P, x, O, fin);
-    // P hi + lo and Z in, O (or W's selected lines, read and written) out
-    const double fbytes = (4.0 * s_r * s_r + 6.0 * s_r * l_r) * nb;
-    return timed(DION2_PHASE_NS_UPDATE, 4.0 * s_r * s_r * l_r * nb, fbytes, 1, stream,
-                 [&] { return launch_gemm(x, epi, 2, stream); });
+    const int npass = Zlo ? 3 : 2;
+    // P hi + lo and Z (hi, and lo) in, O (or W's selected lines, read and written) out
+    const double fbytes = (4.0 * s_r * s_r + (Zlo ? 8.0 : 6.0) * s_r * l_r) * nb;
+    return timed(DION2_PHASE_NS_UPDATE, 2.0 * npass * s_r * s_r * l_r * nb, fbytes, 1, stream,
+                 [&] { return launch_gemm(x, epi, npass, stream); });
 }
 
-hipError_t ns_gram(const Plan& P, const uint16_t* Z, uint16_t* const* sq, float* O, int ns_steps,
-                   const dion2_options& opt, const ChainFmt& fmt, const FinalSpec& fin,
+hipError_t ns_gram(const Plan& P, const uint16_t* Z, const uint16_t* Zlo, uint16_t* const* sq, float* O,
+                   int ns_steps, const dion2_options& opt, const ChainFmt& fmt, const FinalSpec& fin,
                    hipStream_t stream) {
-    hipError_t e = gram_a0(P, Z, sq[SQ_AHI], sq[SQ_ALO], fmt, stream);
+    hipError_t e = gram_a0(P, Z, Zlo, sq[SQ_AHI], sq[SQ_ALO], fmt, stream);
     if (e != hipSuccess) return e;
     int cur = 0;
     e = gram_chain(P.batch, P.s_pad, sq, ns_steps, opt, fmt, chain_cost(P, ns_steps, fmt), stream, &cur);
     if (e != hipSuccess) return e;
-    return gram_final(P, cur ? sq[SQ_P1HI] : sq[SQ_P0HI], cur ? sq[SQ_P1LO] : sq[SQ_P0LO], Z, O, fin,
-                      stream);
+    return gram_final(P, cur ? sq[SQ_P1HI] : sq[SQ_P0HI], cur ? sq[SQ_P1LO] : sq[SQ_P0LO], Z, Zlo, O,
+                      fin, stream);
 }
 
 // ------------------------------------------------------------------ step
@@ -780,6 +790,10 @@ int front(const Plan& P, const MatSet& ms, const Bufs& b, float mu, int ns_steps
     ga.decay = cm ? (opt.decay_all ? 2 : 1) : (opt.decay_all ? 0 : 1);
     ga.L = P.z_is_L ? b.Z0 : nullptr;
     ga.LT = P.z_is_L ? nullptr : b.Z0;
+    if (P.master && ns_steps > 0) {   // the lo half of X beside it
+        ga.Llo = P.z_is_L ? b.Z1 : nullptr;
+        ga.LTlo = P.z_is_L ? nullptr : b.Z1;
+    }
     ga.O = ns_steps == 0 ? b.O : nullptr;
     e = timed(DION2_PHASE_GATHER, 0.0, pb.k3, 1, stream,
               [&] { return launch_gather(ga, P.axis, opt.g_dtype == DION2_DTYPE_BF16, stream); });
@@ -928,7 +942,7 @@ int run_step(const Plan& P, void* W, float* M, const void* G, const Tables* tabs
     if (st != DION2_OK) return st;
     const FinalSpec fin = make_final(P, ms, b, lr, ns_steps, opt);
     if (ns_steps > 0) {   // with no step the gather has written O
-        e = P.gram ? ns_gram(P, b.Z0, b.sbuf, b.O, ns_steps, opt, fmt, fin, stream)
+        e = P.gram ? ns_gram(P, b.Z0, P.master ? b.Z1 : nullptr, b.sbuf, b.O, ns_steps, opt, fmt, fin, stream)
                    : ns_direct(P, b.Z0, b.Z1, b.sbuf, b.O, ns_steps, opt, fin, stream);
         if (e != hipSuccess) return hip_fail(e, "launch K4 Newton-Schulz");
     }
@@ -952,6 +966,12 @@ int validate_common(float mu, float lr, int ns_steps, const dion2_options& opt) 
         return fail(DION2_ERR_INVALID_ARG, "decay_all must be 0 or 1");
     if (opt.select_rule != DION2_SELECT_L1 && opt.select_rule != DION2_SELECT_RANDOM)
         return fail(DION2_ERR_INVALID_ARG, "select_rule %d is not L1 or RANDOM", opt.select_rule);
+    if (opt.ns_master != DION2_MASTER_BF16 && opt.ns_master != DION2_MASTER_FP32)
+        return fail(DION2_ERR_INVALID_ARG, "ns_master %d is not BF16 or FP32", opt.ns_master);
+    if (opt.ns_master == DION2_MASTER_FP32 && opt.ns_chain == DION2_CHAIN_F16)
+        return fail(DION2_ERR_INVALID_ARG, "ns_master FP32 keeps the s x s chain in hi / lo pairs (ns_chain F16 given)");
+    if (opt.ns_master == DION2_MASTER_FP32 && opt.ns_form == DION2_NS_DIRECT)
+        return fail(DION2_ERR_UNSUPPORTED, "ns_master FP32 runs in the GRAM order (ns_form DIRECT given)");
     if (opt.ns_coeffs) {
         for (int i = 0; i < 3 * ns_steps; ++i)
             if (!std::isfinite(opt.ns_coeffs[i]))
@@ -967,7 +987,8 @@ int step_impl(void* W, float* M, const void* G, const Tables* tabs, int batch, i
     if (opt_in) opt = *opt_in;
     else dion2_options_init(&opt);
     Plan P;
-    int st = make_plan(batch, rows, cols, alpha, axis, opt.ns_form, &P);
+    int st = make_plan(batch, rows, cols, alpha, axis, opt.ns_form, &P, true,
+                       opt.ns_master == DION2_MASTER_FP32);
     if (st != DION2_OK) return st;
     st = validate_common(mu, lr, ns_steps, opt);
     if (st != DION2_OK) return st;
@@ -1054,7 +1075,8 @@ int groups_impl(const dion2_group* groups, int ngroups, float alpha, float mu, f
     for (int g = 0; g < ngroups; ++g) {
         const dion2_group& G = groups[g];
         Plan P;
-        st = make_plan(G.batch, G.rows, G.cols, alpha, G.axis, opt.ns_form, &P);
+        const bool master = opt.ns_master == DION2_MASTER_FP32;
+        st = make_plan(G.batch, G.rows, G.cols, alpha, G.axis, opt.ns_form, &P, true, master);
         if (st != DION2_OK) return fail(st, "group %d: %s", g, g_last_error.c_str());
         if (!G.W || !G.M || !G.G) return fail(DION2_ERR_INVALID_ARG, "group %d: W, M and G must not be NULL", g);
         if (!aligned16(G.W) || !aligned16(G.M) || !aligned16(G.G))
@@ -1073,7 +1095,7 @@ int groups_impl(const dion2_group* groups, int ngroups, float alpha, float mu, f
             chain_of[g] = c;
             chain_pos[g] = chains[c].batch;
             chains[c].batch += P.batch;
-            make_plan(G.batch, G.rows, G.cols, alpha, G.axis, opt.ns_form, &P, false);
+            make_plan(G.batch, G.rows, G.cols, alpha, G.axis, opt.ns_form, &P, false, master);
         }
         plans[g] = P;
         total_batch += G.batch;
@@ -1188,7 +1210,7 @@ int groups_impl(const dion2_group* groups, int ngroups, float alpha, float mu, f
         if (st != DION2_OK) return st;
         fins[g] = make_final(P, ms, b, lr, ns_steps, gopt[g]);
         if (c >= 0) {
-            e = gram_a0(P, b.Z0, b.sbuf[SQ_AHI], b.sbuf[SQ_ALO], fmt, s);
+            e = gram_a0(P, b.Z0, P.master ? b.Z1 : nullptr, b.sbuf[SQ_AHI], b.sbuf[SQ_ALO], fmt, s);
             if (e != hipSuccess) return hip_fail(e, "launch K4 Gram");
             if (nS > 1) {
                 e = hipEventRecord(ev_a0[g], s);
@@ -1197,7 +1219,7 @@ int groups_impl(const dion2_group* groups, int ngroups, float alpha, float mu, f
             continue;
         }
         if (ns_steps > 0) {
-            e = P.gram ? ns_gram(P, b.Z0, b.sbuf, b.O, ns_steps, gopt[g], fmt, fins[g], s)
+            e = P.gram ? ns_gram(P, b.Z0, P.master ? b.Z1 : nullptr, b.sbuf, b.O, ns_steps, gopt[g], fmt, fins[g], s)
                        : ns_direct(P, b.Z0, b.Z1, b.sbuf, b.O, ns_steps, gopt[g], fins[g], s);
             if (e != hipSuccess) return hip_fail(e, "launch K4 Newton-Schulz");
         }
@@ -1243,7 +1265,7 @@ int groups_impl(const dion2_group* groups, int ngroups, float alpha, float mu, f
         const Bufs& b = bufs[g];
         const int cur = chain_cur[c];
         e = gram_final(P, cur ? b.sbuf[SQ_P1HI] : b.sbuf[SQ_P0HI], cur ? b.sbuf[SQ_P1LO] : b.sbuf[SQ_P0LO],
-                       b.Z0, b.O, fins[g], s);
+                       b.Z0, P.master ? b.Z1 : nullptr, b.O, fins[g], s);
         if (e != hipSuccess) return hip_fail(e, "launch K4 final product");
         st = back(P, sets[g], b, fins[g], gopt[g], s);
         if (st != DION2_OK) return st;
@@ -1272,6 +1294,7 @@ void dion2_options_init(dion2_options* opt) {
     opt->rand_matrix0 = 0;
     opt->group_streams = 0;
     opt->ns_chain = DION2_CHAIN_HILO;
+    opt->ns_master = DION2_MASTER_BF16;
 }
 
 int dion2_step(void* W, float* M, const void* G, int64_t rows, int64_t cols, float alpha,

@@ -209,6 +209,8 @@ struct GatherArgs {
     int decay;         // 0: none, 1: M[K] <- mu M[K] here, 2: M <- mu M (column mode)
     uint16_t* L;       // nullable [batch][kpad][opad]
     uint16_t* LT;      // nullable [batch][opad][kpad] (one of L, LT is written)
+    uint16_t* Llo;     // nullable: with L (LT), the lo halves bf16(x - L) of the
+    uint16_t* LTlo;    // same entries, for the fp32-master Newton-Schulz
     float* O;          // nullable: fp32 copy (no Newton-Schulz step), L layout for
                        // rows, L^T layout [opad][kpad] for columns
 };
@@ -231,9 +233,9 @@ hipError_t launch_decay_all(const DecayAllArgs& a, hipStream_t s);
 //   EPI_QPOLY  (B as rows [N][K], npass 3): Q = ca I + cb (E0 + E1) + cc C,
 //              out0 = bf16(Q), out1 = bf16(Q - out0)
 //   EPI_UPDATE (B as [K][N], npass 1): out0 = bf16(ca E0 + C)
-//   EPI_FINAL  (B as [K][N], npass 1 or 2): out0 = ca E0 + C in fp32 (no
+//   EPI_FINAL  (B as [K][N], npass 1 to 3): out0 = ca E0 + C in fp32 (no
 //              E0 term when E0 is null), or its transpose when out_transposed
-//   EPI_APPLY  (B as [K][N], npass 1 or 2): O = ca E0 + C (row selection, O in
+//   EPI_APPLY  (B as [K][N], npass 1 to 3): O = ca E0 + C (row selection, O in
 //              the L layout) is not stored; the update step is applied
 //              directly: W[K[p]][j] <- bf16(W[K[p]][j] - lr_eff O[p][j]) for
 //              p < k, j < d_oth (bf16 W, cols % 8 == 0); dbg gets O if set

@@ -7,7 +7,8 @@
 //   M_line(K[p]) <- fl32(mu * M_line(K[p]))                   (Algorithm 1, decay step)
 //
 // Only the orientation Newton-Schulz iterates on is written (the wide one;
-// the other pointer is null). One 256-thread block handles a 64 x 64 tile of
+// the other pointer is null). For the fp32-master Newton-Schulz the lo
+// halves bf16(x - bf16(x)) go out beside it (Llo / LTlo). One 256-thread block handles a 64 x 64 tile of
 // (line p, other index j): the side that is contiguous in M is read and
 // written directly, the other side goes through an LDS tile. Tiles cover the
 // padded extents, and padding (p >= k or j >= d_oth) is written as zero.
@@ -20,6 +21,20 @@ namespace {
 
 constexpr int kT = 64;   // tile edge
 constexpr int kThreads = 256;
+
+// Four values as packed bf16 his, and their lo halves bf16(x - hi).
+__device__ __forceinline__ void pack_hilo4(const float (&x)[4], uint2* hi, uint2* lo) {
+    uint16_t h[4], l[4];
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+        h[v] = f32_to_bf16(x[v]);
+        l[v] = f32_to_bf16(x[v] - bf16_bits_to_f32(h[v]));
+    }
+    hi->x = (uint32_t)h[0] | ((uint32_t)h[1] << 16);
+    hi->y = (uint32_t)h[2] | ((uint32_t)h[3] << 16);
+    lo->x = (uint32_t)l[0] | ((uint32_t)l[1] << 16);
+    lo->y = (uint32_t)l[2] | ((uint32_t)l[3] << 16);
+}
 
 // Row mode: line p is row K[p] of M; j runs along the row (contiguous).
 template <int VEC>
@@ -75,10 +90,10 @@ __global__ __launch_bounds__(kThreads) void gather_rows(GatherArgs a) {
             }
         }
         if (L) {
-            uint2 packed;
-            packed.x = (uint32_t)f32_to_bf16(x[0]) | ((uint32_t)f32_to_bf16(x[1]) << 16);
-            packed.y = (uint32_t)f32_to_bf16(x[2]) | ((uint32_t)f32_to_bf16(x[3]) << 16);
-            *reinterpret_cast<uint2*>(L + (int64_t)p * a.opad + j) = packed;
+            uint2 hi, lo;
+            pack_hilo4(x, &hi, &lo);
+            *reinterpret_cast<uint2*>(L + (int64_t)p * a.opad + j) = hi;
+            if (a.Llo) *reinterpret_cast<uint2*>(a.Llo + (int64_t)b * a.kpad * a.opad + (int64_t)p * a.opad + j) = lo;
         }
         if (O) *reinterpret_cast<float4*>(O + (int64_t)p * a.opad + j) = make_float4(x[0], x[1], x[2], x[3]);
 #pragma unroll
@@ -91,12 +106,13 @@ __global__ __launch_bounds__(kThreads) void gather_rows(GatherArgs a) {
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
         const int jl = ty + 16 * i;
-        uint2 packed;
-        packed.x = (uint32_t)f32_to_bf16(tile[4 * tx + 0][jl]) |
-                   ((uint32_t)f32_to_bf16(tile[4 * tx + 1][jl]) << 16);
-        packed.y = (uint32_t)f32_to_bf16(tile[4 * tx + 2][jl]) |
-                   ((uint32_t)f32_to_bf16(tile[4 * tx + 3][jl]) << 16);
-        *reinterpret_cast<uint2*>(LT + (int64_t)(j0 + jl) * a.kpad + p) = packed;
+        const float x[4] = {tile[4 * tx + 0][jl], tile[4 * tx + 1][jl], tile[4 * tx + 2][jl],
+                            tile[4 * tx + 3][jl]};
+        uint2 hi, lo;
+        pack_hilo4(x, &hi, &lo);
+        *reinterpret_cast<uint2*>(LT + (int64_t)(j0 + jl) * a.kpad + p) = hi;
+        if (a.LTlo)
+            *reinterpret_cast<uint2*>(a.LTlo + (int64_t)b * a.opad * a.kpad + (int64_t)(j0 + jl) * a.kpad + p) = lo;
     }
 }
 
@@ -205,15 +221,16 @@ __global__ __launch_bounds__(kThreads) void update_cols(GatherArgs a) {
 #pragma unroll
             for (int v = 0; v < 4; ++v) x[v] = tile[pi][4 * q + v];
             const int64_t off = (int64_t)b * a.kpad * a.opad + (int64_t)(p0 + pi) * a.opad + r0 + 4 * q;
-            uint2 packed;
-            packed.x = (uint32_t)f32_to_bf16(x[0]) | ((uint32_t)f32_to_bf16(x[1]) << 16);
-            packed.y = (uint32_t)f32_to_bf16(x[2]) | ((uint32_t)f32_to_bf16(x[3]) << 16);
-            *reinterpret_cast<uint2*>(a.L + off) = packed;
+            uint2 hi, lo;
+            pack_hilo4(x, &hi, &lo);
+            *reinterpret_cast<uint2*>(a.L + off) = hi;
+            if (a.Llo) *reinterpret_cast<uint2*>(a.Llo + off) = lo;
         }
         if (last) {
             for (int pi = a.k + (threadIdx.x >> 4); pi < a.kpad; pi += kThreads / 16) {
                 const int64_t off = (int64_t)b * a.kpad * a.opad + (int64_t)pi * a.opad + r0 + 4 * q;
                 *reinterpret_cast<uint2*>(a.L + off) = make_uint2(0u, 0u);
+                if (a.Llo) *reinterpret_cast<uint2*>(a.Llo + off) = make_uint2(0u, 0u);
             }
         }
     }
@@ -228,15 +245,20 @@ __global__ __launch_bounds__(kThreads) void update_cols(GatherArgs a) {
     if (a.LT) {
         // L^T[r][p0 .. p1), p contiguous
         uint16_t* LT = a.LT + (int64_t)b * a.opad * a.kpad;
+        uint16_t* LTlo = a.LTlo ? a.LTlo + (int64_t)b * a.opad * a.kpad : nullptr;
         for (int idx = threadIdx.x; idx < kRB * np; idx += kThreads) {
             const int rl = idx / np, pi = idx % np;
-            LT[(int64_t)(r0 + rl) * a.kpad + p0 + pi] = f32_to_bf16(tile[pi][rl]);
+            const float x = tile[pi][rl];
+            const uint16_t h = f32_to_bf16(x);
+            LT[(int64_t)(r0 + rl) * a.kpad + p0 + pi] = h;
+            if (LTlo) LTlo[(int64_t)(r0 + rl) * a.kpad + p0 + pi] = f32_to_bf16(x - bf16_bits_to_f32(h));
         }
         if (last) {
             const int npad = a.kpad - a.k;
             for (int idx = threadIdx.x; idx < kRB * npad; idx += kThreads) {
                 const int rl = idx / npad, pi = idx % npad;
                 LT[(int64_t)(r0 + rl) * a.kpad + a.k + pi] = 0;
+                if (LTlo) LTlo[(int64_t)(r0 + rl) * a.kpad + a.k + pi] = 0;
             }
         }
     }

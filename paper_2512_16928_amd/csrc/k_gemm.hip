@@ -116,7 +116,7 @@ struct Tile {
     static_assert(A_BYTES % 1024 == 0 && B_BYTES % 1024 == 0, "tiles are whole 1 KB blocks");
     static_assert(STAGE_INSTS % WAVES == 0, "load instructions split evenly over waves");
     static_assert(NPASS >= 1 && NPASS <= 3, "one to three passes");
-    static_assert(!BT || (NPASS <= 2 && BN == 128), "the [K][N] B operand: one or two passes, BN 128");
+    static_assert(!BT || BN == 128, "the [K][N] B operand: BN 128");
     static_assert(S >= 2 && S <= 4, "two to four stages");
     static_assert(!F16 || (NPASS == 1 && !BT), "fp16 operands: one pass, B as rows");
 };
@@ -156,7 +156,7 @@ __device__ __forceinline__ void load_slice(const GemmArgs& a, unsigned char* dst
             if constexpr (T::BT) {
                 const int r = lb / 256, slot = (lb % 256) / 16;
                 const int c = slot ^ ((r & 3) << 2);
-                src = bbase[0] + ((int64_t)kt * T::BK + r) * a.ldb + c * 8;
+                src = (t ? bbase[1] : bbase[0]) + ((int64_t)kt * T::BK + r) * a.ldb + c * 8;
             } else {
                 const int r = lb / T::PK, slot = (lb % T::PK) / 16;
                 const int c = slot ^ ((r / T::GK) % T::CPR);
@@ -230,8 +230,13 @@ __device__ __forceinline__ void mma_slice(f32x16 (&acc)[T::FM][T::FN], const uns
             }
             if constexpr (NPASS == 3) {
 #pragma unroll
-                for (int j = 0; j < T::FN; ++j)
-                    fb1[slot][j] = *reinterpret_cast<const Frag*>(sb1 + kmajor_off<T>(brow + j * 32, c));
+                for (int j = 0; j < T::FN; ++j) {
+                    if constexpr (T::BT) {
+                        fb1[slot][j] = b_frag_tr<T>(sb1, kk * 16, wn * T::TN + j * 32, lane);
+                    } else {
+                        fb1[slot][j] = *reinterpret_cast<const Frag*>(sb1 + kmajor_off<T>(brow + j * 32, c));
+                    }
+                }
             }
         }
         if (kk > 0) {
@@ -358,7 +363,8 @@ __global__ __launch_bounds__(T::THREADS) void gemm(GemmArgs a) {
     abase[0] = a.A0 + (int64_t)b * a.sA + (int64_t)row0 * a.lda;
     abase[1] = NPASS >= 2 ? a.A1 + (int64_t)b * a.sA + (int64_t)row0 * a.lda : abase[0];
     if constexpr (T::BT) {
-        bbase[0] = bbase[1] = a.B0 + (int64_t)b * a.sB + col0;
+        bbase[0] = a.B0 + (int64_t)b * a.sB + col0;
+        bbase[1] = NPASS == 3 ? a.B1 + (int64_t)b * a.sB + col0 : bbase[0];
     } else {
         bbase[0] = a.B0 + (int64_t)b * a.sB + (int64_t)col0 * a.ldb;
         bbase[1] = NPASS == 3 ? a.B1 + (int64_t)b * a.sB + (int64_t)col0 * a.ldb : bbase[0];
@@ -621,6 +627,7 @@ hipError_t launch_gemm(const GemmArgs& a, GemmEpi epi, int npass, hipStream_t s)
     using TP = Tile<3, 0, 128, 128, 32, 4, 2, 2>;    // three-pass symmetric products
     using TU = Tile<1, 1, 128, 128, 32, 2, 2, 2>;    // update (B operand [K][N])
     using TU2 = Tile<2, 1, 128, 128, 32, 2, 2, 2>;   // two-pass final product
+    using TU3 = Tile<3, 1, 128, 128, 32, 2, 2, 2>;   // three-pass final product (fp32 master)
     using TH = Tile<1, 0, 128, 128, 32, 2, 2, 4, true>;   // fp16 s x s products
     if (a.f16) {
         if (npass != 1) return hipErrorInvalidValue;
@@ -659,11 +666,13 @@ hipError_t launch_gemm(const GemmArgs& a, GemmEpi epi, int npass, hipStream_t s)
         case EPI_FINAL:
             if (npass == 1) return launch_tile<1, EPI_FINAL, TU>(a, s);
             if (npass == 2) return launch_tile<2, EPI_FINAL, TU2>(a, s);
+            if (npass == 3) return launch_tile<3, EPI_FINAL, TU3>(a, s);
             break;
         case EPI_APPLY:
             if (a.cols % 8 || a.cols < 16 || a.out_transposed) break;
             if (npass == 1) return launch_tile<1, EPI_APPLY, TU>(a, s);
             if (npass == 2) return launch_tile<2, EPI_APPLY, TU2>(a, s);
+            if (npass == 3) return launch_tile<3, EPI_APPLY, TU3>(a, s);
             break;
     }
     return hipErrorInvalidValue;

@@ -123,6 +123,12 @@ def test_ex_options_validation(lib):
     big_p = ctypes.cast(big, ctypes.POINTER(ctypes.c_float))
     assert ex(ns_chain=binding.CHAIN_F16, ns_coeffs=big_p) == DION2_ERR_UNSUPPORTED
     assert "fp16" in binding.dion2_last_error()
+    assert ex(ns_master=2) == DION2_ERR_INVALID_ARG and "ns_master" in binding.dion2_last_error()
+    assert ex(ns_master=1, ns_chain=binding.CHAIN_F16) == DION2_ERR_INVALID_ARG
+    assert ex(ns_master=1, ns_form=binding.NS_DIRECT) == DION2_ERR_UNSUPPORTED
+    # the fp32 master runs in the GRAM order: more workspace than the AUTO plan's DIRECT form here
+    need_auto = binding.dion2_workspace_size(1, 64, 64, 0.25)
+    assert ex(ns_master=1, workspace=FAKE, workspace_bytes=need_auto) == DION2_ERR_WORKSPACE
     coeffs = (ctypes.c_float * 6)(1.0, 2.0, 3.0, 1.0, float("inf"), 0.0)
     assert ex(ns_coeffs=ctypes.cast(coeffs, ctypes.POINTER(ctypes.c_float))) == DION2_ERR_INVALID_ARG
     need = binding.dion2_workspace_size(1, 64, 64, 0.25)

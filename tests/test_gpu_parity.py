@@ -34,7 +34,8 @@ CHAINS = pytest.mark.parametrize("chain", [binding.CHAIN_HILO, binding.CHAIN_F16
 
 
 def run_gpu(W, M, G, alpha, ns_steps=5, axis=AXIS_AUTO, mu=0.95, lr=0.02, coeffs=None,
-            decay_all=False, form=binding.NS_AUTO, rand=None, chain=binding.CHAIN_HILO):
+            decay_all=False, form=binding.NS_AUTO, rand=None, chain=binding.CHAIN_HILO,
+            master=binding.MASTER_BF16):
     """One library call on stacks [B, rows, cols]; returns host copies and the
     debug outputs."""
     B, rows, cols = W.shape
@@ -51,7 +52,7 @@ def run_gpu(W, M, G, alpha, ns_steps=5, axis=AXIS_AUTO, mu=0.95, lr=0.02, coeffs
                      rand_matrix0=rand[2])
     binding.dion2_step_ex(W, M, G, alpha, mu, lr, ns_steps, axis, ns_coeffs=coeffs,
                           decay_all=decay_all, dbg_sel_idx=sel, dbg_norms=nrm, dbg_update=upd,
-                          ns_form=form, ns_chain=chain, **extra)
+                          ns_form=form, ns_chain=chain, ns_master=master, **extra)
     torch.cuda.synchronize()
     return dict(W=W.cpu(), M=M.cpu(), K=sel.cpu(), norms=nrm.cpu(), O=upd.cpu(), W0=W0, M0=M0,
                 G=G.cpu(), axis=ax, k=k)
@@ -227,6 +228,52 @@ def test_f16_chain_ragged(hip_device, rows, cols, alpha, axis):
     W, M, G = workloads.make_group(wl, 0, hip_device)
     res = run_gpu(W, M, G, alpha, axis=axis, form=NS_GRAM, chain=binding.CHAIN_F16)
     check_matrix(res, 0, alpha, axis=axis)
+
+
+MASTER_TOL = 2e-3   # fp32 master: X as a hi/lo pair, about 16 significant bits throughout
+
+
+@pytest.mark.parametrize("rows,cols,alpha,axis,wdt", [
+    (200, 328, 0.25, AXIS_AUTO, "bf16"),     # rows, s = 50, Z = L
+    (328, 200, 0.25, AXIS_AUTO, "bf16"),     # columns, Z = L
+    (96, 1000, 0.5, AXIS_AUTO, "f32"),       # rows, fp32 W
+    (300, 200, 0.75, AXIS_ROWS, "f32"),      # k = 225 > d_oth = 200: Z = L^T
+    (64, 256, 0.5, AXIS_COLS, "bf16"),       # columns, k = 128 > d_oth = 64: Z = L^T
+    (257, 129, 1.0, AXIS_AUTO, "bf16"),      # alpha = 1, square-ish
+    (130, 75, 0.5, AXIS_AUTO, "bf16"),       # cols % 4 != 0
+    (640, 1664, 0.3, AXIS_ROWS, "bf16"),     # s = 193: several tiles, ragged
+])
+def test_fp32_master_ragged(hip_device, rows, cols, alpha, axis, wdt):
+    """X kept as a bf16 hi/lo pair through every product: the tolerance is a
+    tenth of the bf16 one."""
+    wl = one_group_workload(rows, cols, axis=axis, w_dtype=wdt, name=f"m{rows}c{cols}")
+    W, M, G = workloads.make_group(wl, 0, hip_device)
+    res = run_gpu(W, M, G, alpha, axis=axis, master=binding.MASTER_FP32)
+    check_matrix(res, 0, alpha, axis=axis, ns_tol=MASTER_TOL)
+
+
+@pytest.mark.parametrize("gi,sample", [(0, 21), (1, 5), (2, 12)])
+def test_1b_stack_full_size_fp32_master(hip_device, gi, sample):
+    """The fp32 master over a whole 1B-stack group in one batched call, one
+    sampled matrix against the oracle: at least five times closer than the
+    default's bound, and within 2e-4."""
+    wl = workloads.WORKLOADS["1b"]
+    W, M, G = workloads.make_group(wl, gi, hip_device)
+    grp = wl.groups[gi]
+    k, ax = binding.dion2_plan_info(grp.rows, grp.cols, 0.25, grp.axis)
+    d_sel, d_oth = (grp.rows, grp.cols) if ax == AXIS_ROWS else (grp.cols, grp.rows)
+    sel = torch.empty((grp.count, k), dtype=torch.int32, device=hip_device)
+    nrm = torch.empty((grp.count, d_sel), dtype=torch.float64, device=hip_device)
+    upd = torch.empty((grp.count, k, d_oth), dtype=torch.float32, device=hip_device)
+    snap = (W[sample].cpu(), M[sample].cpu(), G[sample].cpu())
+    binding.dion2_step_ex(W, M, G, 0.25, dbg_sel_idx=sel, dbg_norms=nrm, dbg_update=upd,
+                          ns_master=binding.MASTER_FP32)
+    torch.cuda.synchronize()
+    res = dict(W0=snap[0][None], M0=snap[1][None], G=snap[2][None], W=W[sample].cpu()[None],
+               M=M[sample].cpu()[None], K=sel[sample].cpu()[None], norms=nrm[sample].cpu()[None],
+               O=upd[sample].cpu()[None], axis=ax, k=k)
+    err = check_matrix(res, 0, 0.25, ns_tol=MASTER_TOL)
+    assert err <= 2e-4, f"fp32 master at a 1B shape: {err:.3e}"
 
 
 def test_decay_all_ablation(hip_device):
@@ -510,7 +557,7 @@ def test_groups_single_group_equals_strided(hip_device):
 
 
 @pytest.mark.parametrize("case", ["f32-decay-all-schedule", "forced-direct", "forced-gram", "no-steps",
-                                  "f16-chain", "f16-chain-schedule"])
+                                  "f16-chain", "f16-chain-schedule", "fp32-master"])
 def test_groups_options_equal_per_group_calls(hip_device, case):
     """Options reach every group of a grouped call as they reach dion2_step_ex:
     fp32 W and G, the decay-all ablation, a per-step coefficient schedule, a
@@ -530,6 +577,8 @@ def test_groups_options_equal_per_group_calls(hip_device, case):
         kw = dict(ns_form=NS_GRAM)
     elif case == "f16-chain":
         kw = dict(ns_form=NS_GRAM, ns_chain=binding.CHAIN_F16)
+    elif case == "fp32-master":
+        kw = dict(ns_master=binding.MASTER_FP32)
     elif case == "f16-chain-schedule":
         kw = dict(ns_form=NS_GRAM, ns_chain=binding.CHAIN_F16,
                   ns_coeffs=[(3.4445, -4.7750, 2.0315)] * 4 + [(1.5, -0.5, 0.0)])
