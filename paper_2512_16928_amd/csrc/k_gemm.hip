@@ -24,6 +24,9 @@
 // The GRAM form's chain of s x s products runs the same way on bf16 hi / lo
 // pairs (three passes), or, as an option, on scaled fp16 matrices with
 // v_mfma_f32_32x32x16_f16 (one pass; EPI_H16 and EPI_QPOLY_H16 store fp16).
+// With the fp32 master Z itself is a hi / lo pair: the Gram matrix takes
+// three passes, and so does the final product, whose [K][N] operand then
+// has a lo tile read through the same transposing LDS reads.
 //
 // Tiling for gfx950: a BM x BN output tile per block of WM x WN wave64s,
 // each wave a (BM/WM) x (BN/WN) tile of v_mfma_f32_32x32x16_bf16 blocks.
@@ -37,8 +40,8 @@
 // global chunk that belongs in its LDS slot. Tiles are numbered XCD-aware;
 // the symmetric products (A and B) compute only the tiles on and above the
 // diagonal and write each one twice, so that the stored matrix is exactly
-// symmetric. The epilogue goes through a per-wave
-// 32 x 32 LDS tile: each lane finishes 16 entries of a row there, and the
+// symmetric. The epilogue goes through a per-wave 32 x 32 LDS tile: each
+// lane finishes 16 entries of a row there, and the
 // block then leaves in whole row segments (64 bytes of bf16 or 128 bytes of
 // fp32 per row), row-major or transposed for the mirrored copy.
 //

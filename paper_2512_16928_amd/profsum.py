@@ -41,11 +41,21 @@ CALIB_BYTES = float(1 << 30)   # the calibration copy reads and writes this much
 CALIB_PATTERN = "neg_kernel"
 
 
+_TOKENS = re.compile(r'"(?:\\.|[^"\\])*"|\'(?:\\.|[^\'\\])*\'|//[^\n]*|/\*.*?\*/', re.S)
+
+
+def code_text(src: str) -> str:
+    """Source text without comments and with whitespace collapsed: what the
+    compiler sees, so that editing a comment does not count as a change."""
+    out = _TOKENS.sub(lambda m: " " if m.group(0)[0] == "/" else m.group(0), src)
+    return " ".join(out.split())
+
+
 def source_hash(phase: str) -> str:
     h = hashlib.sha256()
     for f in PHASE_SOURCES[phase] + ("dion2_device.h", "dion2_api.hip"):
-        with open(os.path.join(CSRC, f), "rb") as fh:
-            h.update(fh.read())
+        with open(os.path.join(CSRC, f), encoding="utf-8") as fh:
+            h.update(code_text(fh.read()).encode())
     return h.hexdigest()[:16]
 
 

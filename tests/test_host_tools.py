@@ -47,3 +47,14 @@ def test_bench_refuses_more_than_one_gpu():
                        capture_output=True, text=True, timeout=300)
     assert r.returncode == 2
     assert "one GPU" in r.stderr
+
+
+def test_source_hash_ignores_comments_only():
+    """The traffic lines stay valid across comment edits, not code edits."""
+    base = 'int f(int x) { return x + 1; } // add one\nconst char* s = "// kept";\n'
+    same = '/* header */ int f(int x)  {  return x + 1; }\n// another note\nconst char* s = "// kept";'
+    other = base.replace("x + 1", "x + 2")
+    strings = base.replace('"// kept"', '"// changed"')
+    assert profsum.code_text(base) == profsum.code_text(same)
+    assert profsum.code_text(base) != profsum.code_text(other)
+    assert profsum.code_text(base) != profsum.code_text(strings)
