@@ -176,7 +176,8 @@ typedef struct dion2_options {
 } dion2_options;
 
 /* Defaults: bf16 W and G, Muon quintic, eps 1e-7, selective decay, internal
-   workspace, no debug outputs, Newton-Schulz form chosen by shape, l1 rule. */
+   workspace, no debug outputs, Newton-Schulz form chosen by shape with a
+   hi/lo s x s chain and X rounded once to bf16, l1 rule. */
 void dion2_options_init(dion2_options* opt);
 
 /* One matrix. W, G: bf16 [rows][cols]; M: fp32 [rows][cols]. Algorithm 1. */
@@ -201,7 +202,8 @@ int dion2_step_batched(void* const* W, float* const* M, const void* const* G,
                        void* stream);
 
 /* Strided stacks with full control (dtypes, coefficients, eps, ablation,
-   caller workspace, debug outputs). opt == NULL means defaults. */
+   Newton-Schulz form and precision, selection rule, caller workspace, debug
+   outputs). opt == NULL means defaults. */
 int dion2_step_ex(void* W, float* M, const void* G, int batch, int64_t rows,
                   int64_t cols, float alpha, float mu, float lr, int ns_steps,
                   int axis, const dion2_options* opt, void* stream);
@@ -235,9 +237,10 @@ typedef struct dion2_group {
    The workspace is the library's (opt->workspace must be NULL) and the debug
    outputs must be NULL. Errors: DION2_ERR_INVALID_ARG for ngroups outside
    [1, 64], a NULL array or stack pointer, an unaligned stack, a set
-   workspace or debug output, group_streams outside [0, 8], or an argument
-   dion2_step_ex would reject for some group (nothing is modified then);
-   DION2_ERR_HIP if an internal stream or event cannot be created. */
+   workspace or debug output, group_streams outside [0, 8]; the status
+   dion2_step_ex would return for an argument it rejects for some group
+   (nothing is modified in either case); DION2_ERR_HIP if an internal stream
+   or event cannot be created. */
 int dion2_step_groups(const dion2_group* groups, int ngroups, float alpha,
                       float mu, float lr, int ns_steps,
                       const dion2_options* opt, void* stream);
