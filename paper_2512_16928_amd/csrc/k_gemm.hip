@@ -478,6 +478,17 @@ __global__ __launch_bounds__(T::THREADS) void gemm(GemmArgs a) {
                 stage[m * T::EPI_LD + (lane & 31)] = kScaled ? acc[i][j][r] * osc : acc[i][j][r];
             }
             __builtin_amdgcn_wave_barrier();
+            if constexpr (EPI == EPI_SPLIT || EPI == EPI_H16) {
+                // no arithmetic after the accumulators: they leave the tile as staged
+                if (SYM && R == Cc) {
+                    store_block<EPI, T, false, true>(a, b, stage, (int64_t)R, (int64_t)Cc, lane);
+                } else {
+                    store_block<EPI, T, false>(a, b, stage, (int64_t)R, (int64_t)Cc, lane);
+                    if (SYM) store_block<EPI, T, true>(a, b, stage, (int64_t)Cc, (int64_t)R, lane);
+                }
+                __builtin_amdgcn_wave_barrier();   // the stage tile is rewritten next
+                continue;
+            }
             float v[16];
             const bool transposed = EPI == EPI_FINAL && a.out_transposed;
             if (!transposed) {
