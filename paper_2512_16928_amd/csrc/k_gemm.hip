@@ -613,10 +613,42 @@ __global__ __launch_bounds__(T::THREADS) void gemm(GemmArgs a) {
     }
 }
 
+constexpr unsigned kMaxGridZ = 65535;   // the grid's z extent holds the batch
+
 template <int NPASS, int EPI, typename T, bool SYM = false>
 hipError_t launch_tile(const GemmArgs& a, hipStream_t s) {
     if (a.M % T::BM || a.N % T::BN || a.K % T::BK) return hipErrorInvalidValue;
-    const unsigned zb = (unsigned)a.batch * (a.dual ? 2u : 1u);
+    const unsigned per = a.dual ? 2u : 1u;
+    if (SYM && (unsigned)a.batch * per > kMaxGridZ) {
+        // A dual launch of more than 32767 matrices: consecutive launches
+        // over slices of the batch (the symmetric products' operands and
+        // outputs are all bf16 / fp16 stacks with a batch stride).
+        const int chunk = (int)(kMaxGridZ / per);
+        auto at = [](const void* p, int64_t elems) {
+            return p ? static_cast<const uint16_t*>(p) + elems : nullptr;
+        };
+        for (int b0 = 0; b0 < a.batch; b0 += chunk) {
+            GemmArgs c = a;
+            c.batch = a.batch - b0 < chunk ? a.batch - b0 : chunk;
+            c.A0 = at(a.A0, b0 * a.sA);
+            c.A1 = at(a.A1, b0 * a.sA);
+            c.B0 = at(a.B0, b0 * a.sB);
+            c.B1 = at(a.B1, b0 * a.sB);
+            c.B0x = at(a.B0x, b0 * a.sB);
+            c.B1x = at(a.B1x, b0 * a.sB);
+            c.E0 = at(a.E0, b0 * a.sE);
+            c.E1 = at(a.E1, b0 * a.sE);
+            c.out0 = const_cast<uint16_t*>(at(a.out0, b0 * a.sOut0));
+            c.out1 = const_cast<uint16_t*>(at(a.out1, b0 * a.sOut1));
+            c.out0x = const_cast<uint16_t*>(at(a.out0x, b0 * a.sOut0));
+            c.out1x = const_cast<uint16_t*>(at(a.out1x, b0 * a.sOut1));
+            const hipError_t e = launch_tile<NPASS, EPI, T, SYM>(c, s);
+            if (e != hipSuccess) return e;
+        }
+        return hipSuccess;
+    }
+    const unsigned zb = (unsigned)a.batch * per;
+    if (zb > kMaxGridZ) return hipErrorInvalidValue;
     dim3 grid((unsigned)(a.N / T::BN), (unsigned)(a.M / T::BM), zb);
     if (SYM) {
         if (a.M != a.N || T::BM != T::BN) return hipErrorInvalidValue;

@@ -276,6 +276,34 @@ def test_1b_stack_full_size_fp32_master(hip_device, gi, sample):
     assert err <= 2e-4, f"fp32 master at a 1B shape: {err:.3e}"
 
 
+@pytest.mark.parametrize("chain", [binding.CHAIN_HILO, binding.CHAIN_F16], ids=["hilo", "f16"])
+def test_batch_beyond_grid_z(hip_device, chain):
+    """40000 matrices in one GRAM call: the dual s x s launches would need a
+    grid z extent of 80000, beyond the hardware's 65535, and go out as
+    consecutive launches over slices of the batch. Matrices on either side of
+    the slice boundary are checked against the oracle and against calls over
+    a few matrices."""
+    n = 40000
+    wl = one_group_workload(8, 64, count=n, name="bigbatch")
+    W, M, G = workloads.make_group(wl, 0, hip_device)
+    picks = [0, 32766, 32767, 32768, n - 1]
+    solo = {b: (W[b:b + 1].clone(), M[b:b + 1].clone(), G[b:b + 1].clone()) for b in picks}
+    snap = {b: (W[b].cpu(), M[b].cpu(), G[b].cpu()) for b in picks}
+    binding.dion2_step_ex(W, M, G, 0.5, ns_form=NS_GRAM, ns_chain=chain)
+    for b in picks:
+        Ws, Ms, Gs = solo[b]
+        binding.dion2_step_ex(Ws, Ms, Gs, 0.5, ns_form=NS_GRAM, ns_chain=chain)
+    torch.cuda.synchronize()
+    for b in picks:
+        assert torch.equal(W[b].view(torch.int16), solo[b][0][0].view(torch.int16)), f"matrix {b}: weights"
+        assert torch.equal(M[b], solo[b][1][0]), f"matrix {b}: momentum"
+        out = oracle.dion2_step(snap[b][0].float().numpy().astype(np.float64), snap[b][1].numpy(),
+                                snap[b][2].float().numpy(), 0.5, 0.95, 0.02, 5, AXIS_AUTO, w_dtype="bf16")
+        np.testing.assert_array_equal(M[b].cpu().numpy(), out["M"], err_msg=f"matrix {b}: momentum")
+    del W, M, G
+    binding.dion2_release_workspaces()
+
+
 def test_decay_all_ablation(hip_device):
     wl = one_group_workload(128, 256, name="decayall")
     W, M, G = workloads.make_group(wl, 0, hip_device)
