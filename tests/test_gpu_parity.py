@@ -584,6 +584,40 @@ def test_groups_single_group_equals_strided(hip_device):
     assert torch.equal(M, M2) and torch.equal(W.view(torch.int16), W2.view(torch.int16))
 
 
+def test_groups_at_the_group_limit(hip_device):
+    """64 groups (the most one call takes), of varied small shapes and axes, on
+    the most streams a call may use: bitwise the per-group calls."""
+    shapes = [(64 + 16 * (g % 7), 96 + 32 * (g % 5), (AXIS_AUTO, AXIS_ROWS, AXIS_COLS)[g % 3]) for g in range(64)]
+    wl = workloads.Workload("limit", "test", tuple(workloads.Group(f"g{g}", r, c, 1 + g % 2, ax)
+                                                   for g, (r, c, ax) in enumerate(shapes)), (0.25,))
+    stacks = [workloads.make_group(wl, gi, hip_device) for gi in range(64)]
+    solo = [tuple(t.clone() for t in st) for st in stacks]
+    for gi, (W, M, G) in enumerate(solo):
+        binding.dion2_step_ex(W, M, G, 0.3, 0.95, 0.02, 5, wl.groups[gi].axis)
+    binding.dion2_step_groups([(W, M, G, wl.groups[gi].axis) for gi, (W, M, G) in enumerate(stacks)],
+                              0.3, 0.95, 0.02, 5, group_streams=8)
+    torch.cuda.synchronize()
+    for gi, ((W, M, _), (Ws, Ms, _)) in enumerate(zip(stacks, solo)):
+        assert torch.equal(M, Ms), f"group {gi}: momentum"
+        assert torch.equal(W.view(torch.int16), Ws.view(torch.int16)), f"group {gi}: weights"
+
+
+def test_sixteen_newton_schulz_steps(hip_device):
+    """The most steps a call takes. DIRECT rounds X to bf16 after every step,
+    so its distance from the fp64 iteration grows with the step count
+    (about 1e-2 at 5 steps); the GRAM form and the fp32 master carry the
+    iteration in hi/lo pairs and stay at their 5-step error."""
+    wl = one_group_workload(160, 640, name="ns16")
+    W, M, G = workloads.make_group(wl, 0, hip_device)
+    errs = {}
+    for name, kw, tol in (("direct", dict(form=NS_DIRECT), 8e-2), ("gram", dict(form=NS_GRAM), NS_TOL),
+                          ("master", dict(master=binding.MASTER_FP32), MASTER_TOL)):
+        res = run_gpu(W.clone(), M.clone(), G, 0.5, ns_steps=16, **kw)
+        errs[name] = check_matrix(res, 0, 0.5, ns_steps=16, ns_tol=tol)
+    assert errs["gram"] < errs["direct"] and errs["master"] < errs["gram"], errs
+    print("16-step errors", errs)
+
+
 @pytest.mark.parametrize("case", ["f32-decay-all-schedule", "forced-direct", "forced-gram", "no-steps",
                                   "f16-chain", "f16-chain-schedule", "fp32-master"])
 def test_groups_options_equal_per_group_calls(hip_device, case):
