@@ -304,6 +304,35 @@ def test_batch_beyond_grid_z(hip_device, chain):
     binding.dion2_release_workspaces()
 
 
+@pytest.mark.parametrize("rows,cols,alpha", [(256, 1024, 0.25), (1024, 256, 0.5), (384, 384, 0.5)],
+                         ids=["rows-gram", "cols-gram", "square-direct"])
+def test_caller_workspace(hip_device, rows, cols, alpha):
+    """A caller-provided workspace of dion2_workspace_size bytes gives bitwise
+    the result of the library's own; one byte short, or a plan that needs more
+    (the fp32 master on a DIRECT shape), is refused before anything runs."""
+    wl = one_group_workload(rows, cols, count=2, name=f"ws{rows}x{cols}")
+    W, M, G = workloads.make_group(wl, 0, hip_device)
+    W2, M2 = W.clone(), M.clone()
+    need = binding.dion2_workspace_size(2, rows, cols, alpha)
+    assert need > 0
+    ws = torch.empty(need, dtype=torch.uint8, device=hip_device)
+    binding.dion2_step_ex(W, M, G, alpha, workspace=ws)
+    binding.dion2_step_ex(W2, M2, G, alpha)
+    torch.cuda.synchronize()
+    assert torch.equal(W.view(torch.int16), W2.view(torch.int16)) and torch.equal(M, M2)
+    W3, M3 = W.clone(), M.clone()
+    with pytest.raises(binding.Dion2Error) as ei:
+        binding.dion2_step_ex(W3, M3, G, alpha, workspace=ws[:need - 256])
+    assert ei.value.status == binding.DION2_ERR_WORKSPACE
+    k, _ = binding.dion2_plan_info(rows, cols, alpha, AXIS_AUTO)
+    if rows == cols:   # AUTO is DIRECT here; the fp32 master's GRAM plan needs more
+        with pytest.raises(binding.Dion2Error) as ei:
+            binding.dion2_step_ex(W3, M3, G, alpha, workspace=ws, ns_master=binding.MASTER_FP32)
+        assert ei.value.status == binding.DION2_ERR_WORKSPACE
+    torch.cuda.synchronize()
+    assert torch.equal(W3.view(torch.int16), W.view(torch.int16)) and torch.equal(M3, M), "refused calls modified state"
+
+
 def test_decay_all_ablation(hip_device):
     wl = one_group_workload(128, 256, name="decayall")
     W, M, G = workloads.make_group(wl, 0, hip_device)
