@@ -35,7 +35,7 @@ CHAINS = pytest.mark.parametrize("chain", [binding.CHAIN_HILO, binding.CHAIN_F16
 
 def run_gpu(W, M, G, alpha, ns_steps=5, axis=AXIS_AUTO, mu=0.95, lr=0.02, coeffs=None,
             decay_all=False, form=binding.NS_AUTO, rand=None, chain=binding.CHAIN_HILO,
-            master=binding.MASTER_BF16):
+            master=binding.MASTER_BF16, eps=1e-7):
     """One library call on stacks [B, rows, cols]; returns host copies and the
     debug outputs."""
     B, rows, cols = W.shape
@@ -50,7 +50,7 @@ def run_gpu(W, M, G, alpha, ns_steps=5, axis=AXIS_AUTO, mu=0.95, lr=0.02, coeffs
     if rand is not None:   # (seed, step, first matrix index): the Random rule
         extra = dict(select_rule=binding.SELECT_RANDOM, rand_seed=rand[0], rand_step=rand[1],
                      rand_matrix0=rand[2])
-    binding.dion2_step_ex(W, M, G, alpha, mu, lr, ns_steps, axis, ns_coeffs=coeffs,
+    binding.dion2_step_ex(W, M, G, alpha, mu, lr, ns_steps, axis, ns_coeffs=coeffs, ns_eps=eps,
                           decay_all=decay_all, dbg_sel_idx=sel, dbg_norms=nrm, dbg_update=upd,
                           ns_form=form, ns_chain=chain, ns_master=master, **extra)
     torch.cuda.synchronize()
@@ -59,7 +59,7 @@ def run_gpu(W, M, G, alpha, ns_steps=5, axis=AXIS_AUTO, mu=0.95, lr=0.02, coeffs
 
 
 def check_matrix(res, b, alpha, ns_steps=5, axis=AXIS_AUTO, mu=0.95, lr=0.02, coeffs=None,
-                 decay_all=False, ns_tol=NS_TOL, rand=None):
+                 decay_all=False, ns_tol=NS_TOL, rand=None, eps=1e-7):
     wdt = "bf16" if res["W0"].dtype == torch.bfloat16 else "f32"
     W0 = res["W0"][b].float().numpy().astype(np.float64)
     M0 = res["M0"][b].numpy()
@@ -67,8 +67,8 @@ def check_matrix(res, b, alpha, ns_steps=5, axis=AXIS_AUTO, mu=0.95, lr=0.02, co
     sel_kw = {}
     if rand is not None:
         sel_kw = dict(select="random", seed=rand[0], step=rand[1], matrix=rand[2] + b)
-    out = oracle.dion2_step(W0, M0, G, alpha, mu, lr, ns_steps, axis, coeffs, w_dtype=wdt,
-                            decay_all=decay_all, **sel_kw)
+    out = oracle.dion2_step(W0, M0, G, alpha, mu, lr, ns_steps, axis, coeffs, eps=float(np.float32(eps)),
+                            w_dtype=wdt, decay_all=decay_all, **sel_kw)
     assert out["axis"] == res["axis"] and out["k"] == res["k"]
     K = res["K"][b].numpy().astype(np.int64)
     np.testing.assert_array_equal(K, out["K"], err_msg="selected indices")
@@ -331,6 +331,18 @@ def test_caller_workspace(hip_device, rows, cols, alpha):
         assert ei.value.status == binding.DION2_ERR_WORKSPACE
     torch.cuda.synchronize()
     assert torch.equal(W3.view(torch.int16), W.view(torch.int16)) and torch.equal(M3, M), "refused calls modified state"
+
+
+@pytest.mark.parametrize("eps", [0.0, 1.0], ids=["eps0", "eps-large"])
+@FORMS
+def test_normalisation_eps(hip_device, eps, form):
+    """dion2_options.ns_eps reaches the normalisation X / (||X||_F + eps):
+    with ||X||_F about 1.4 here, eps = 1 shrinks X by 40%, which moves O
+    many times the tolerance away unless both sides use it."""
+    wl = one_group_workload(128, 512, name="eps")
+    W, M, G = workloads.make_group(wl, 0, hip_device)
+    res = run_gpu(W, M, G, 0.25, form=form, eps=eps)
+    check_matrix(res, 0, 0.25, eps=eps)
 
 
 def test_decay_all_ablation(hip_device):
