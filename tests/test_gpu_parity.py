@@ -345,6 +345,19 @@ def test_normalisation_eps(hip_device, eps, form):
     check_matrix(res, 0, 0.25, eps=eps)
 
 
+@pytest.mark.parametrize("wdt,gdt", [("bf16", "f32"), ("f32", "bf16")])
+@pytest.mark.parametrize("axis", [AXIS_ROWS, AXIS_COLS])
+def test_mixed_w_and_g_dtypes(hip_device, wdt, gdt, axis):
+    """W and G in different storage types (dion2_options.w_dtype / g_dtype)."""
+    wl = one_group_workload(192, 320, axis=axis, w_dtype="f32", name=f"mix{axis}")
+    W, M, G = workloads.make_group(wl, 0, hip_device)   # fp32 W and G
+    to = {"bf16": torch.bfloat16, "f32": torch.float32}
+    W = W.to(to[wdt]).contiguous()
+    G = G.to(to[gdt]).contiguous()
+    res = run_gpu(W, M, G, 0.25, axis=axis)
+    check_matrix(res, 0, 0.25, axis=axis)
+
+
 def test_decay_all_ablation(hip_device):
     wl = one_group_workload(128, 256, name="decayall")
     W, M, G = workloads.make_group(wl, 0, hip_device)
