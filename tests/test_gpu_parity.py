@@ -115,6 +115,9 @@ def test_single_256_fp32_full(hip_device):
     (64, 2048, 0.75, AXIS_COLS, "bf16"),     # k = 1536: one row per wave, two passes of ranks
     (48, 4096, 1.0, AXIS_COLS, "bf16"),      # k = 4096, the widest row of the LDS buffer
     (40, 2048, 0.6, AXIS_COLS, "f32"),       # fp32 W, k = 1229 (ragged last pass)
+    (100, 250, 0.3, AXIS_ROWS, "bf16"),      # rows, cols % 4 != 0: scalar row apply
+    (64, 100, 0.5, AXIS_ROWS, "bf16"),       # rows, cols % 8 = 4: vector row apply, no fused update
+    (90, 154, 0.4, AXIS_ROWS, "f32"),        # rows, fp32 W, cols % 4 != 0
 ])
 @FORMS
 def test_ragged_shapes(hip_device, rows, cols, alpha, axis, wdt, form):
