@@ -173,6 +173,17 @@ typedef struct dion2_options {
                                 on the call's stream, at most 8)                   */
     int ns_chain;            /* dion2_ns_chain (default DION2_CHAIN_HILO)           */
     int ns_master;           /* dion2_ns_master (default DION2_MASTER_BF16)         */
+    uint16_t* dbg_compact;   /* optional DEVICE out [batch][k][d_oth] bf16 bits: X,
+                                the normalised submatrix Newton-Schulz starts from
+                                (Algorithm 1, orthonormalisation step), selected
+                                line p in row p; each entry is
+                                bf16(fl32(M[K] * fl32(1 / (||M[K]||_F + eps))))
+                                from the accumulated momentum, the hi half with
+                                DION2_MASTER_FP32. Written with ns_steps 0 too  */
+    uint16_t* dbg_compact_lo;/* optional DEVICE out, same layout: the lo halves
+                                bf16(x - hi) of X's fp32 values; only with
+                                DION2_MASTER_FP32 and ns_steps >= 1, else the
+                                call returns DION2_ERR_INVALID_ARG              */
 } dion2_options;
 
 /* Defaults: bf16 W and G, Muon quintic, eps 1e-7, selective decay, internal

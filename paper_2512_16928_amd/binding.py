@@ -72,6 +72,8 @@ class Options(ctypes.Structure):
         ("group_streams", c_int),
         ("ns_chain", c_int),
         ("ns_master", c_int),
+        ("dbg_compact", c_void_p),
+        ("dbg_compact_lo", c_void_p),
     ]
 
 
@@ -222,13 +224,16 @@ def dion2_step_batched(Ws, Ms, Gs, alpha, mu=0.95, lr=0.02, ns_steps=5, axis=AXI
 
 def dion2_step_ex(W, M, G, alpha, mu=0.95, lr=0.02, ns_steps=5, axis=AXIS_AUTO, *,
                   ns_coeffs=None, ns_eps=1e-7, decay_all=False, workspace=None,
-                  dbg_sel_idx=None, dbg_norms=None, dbg_update=None, ns_form=NS_AUTO,
-                  select_rule=SELECT_L1, rand_seed=0, rand_step=0, rand_matrix0=0,
-                  ns_chain=CHAIN_HILO, ns_master=MASTER_BF16, stream=None):
+                  dbg_sel_idx=None, dbg_norms=None, dbg_update=None, dbg_compact=None,
+                  dbg_compact_lo=None, ns_form=NS_AUTO, select_rule=SELECT_L1, rand_seed=0,
+                  rand_step=0, rand_matrix0=0, ns_chain=CHAIN_HILO, ns_master=MASTER_BF16,
+                  stream=None):
     """Full control. W, M, G are [rows, cols] or [batch, rows, cols]; W and G
     may be bf16 or fp32. Debug outputs are preallocated device tensors:
     dbg_sel_idx int32 [batch, k], dbg_norms float64 [batch, d_sel],
-    dbg_update float32 [batch, k, d_oth]. ns_form is NS_AUTO, NS_DIRECT or
+    dbg_update float32 [batch, k, d_oth], dbg_compact and dbg_compact_lo
+    bfloat16 [batch, k, d_oth] (X before Newton-Schulz, and with MASTER_FP32
+    its lo halves). ns_form is NS_AUTO, NS_DIRECT or
     NS_GRAM (the Newton-Schulz evaluation order); ns_chain CHAIN_HILO or
     CHAIN_F16 (storage of the GRAM form's s x s matrices); ns_master
     MASTER_BF16 or MASTER_FP32 (X rounded once to bf16, or kept as a hi/lo
@@ -243,7 +248,9 @@ def dion2_step_ex(W, M, G, alpha, mu=0.95, lr=0.02, ns_steps=5, axis=AXIS_AUTO, 
                               rand_seed, rand_step, rand_matrix0, ns_chain, ns_master)
     for name, t, dt in (("dbg_sel_idx", dbg_sel_idx, torch.int32),
                         ("dbg_norms", dbg_norms, torch.float64),
-                        ("dbg_update", dbg_update, torch.float32)):
+                        ("dbg_update", dbg_update, torch.float32),
+                        ("dbg_compact", dbg_compact, torch.bfloat16),
+                        ("dbg_compact_lo", dbg_compact_lo, torch.bfloat16)):
         if t is not None:
             if t.dtype != dt or not t.is_contiguous() or t.device != W.device:
                 raise ValueError(f"{name} must be a contiguous {dt} tensor on {W.device}")

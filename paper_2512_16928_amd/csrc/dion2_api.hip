@@ -798,6 +798,15 @@ int front(const Plan& P, const MatSet& ms, const Bufs& b, float mu, int ns_steps
     e = timed(DION2_PHASE_GATHER, 0.0, pb.k3, 1, stream,
               [&] { return launch_gather(ga, P.axis, opt.g_dtype == DION2_DTYPE_BF16, stream); });
     if (e != hipSuccess) return hip_fail(e, "launch K3 gather");
+    // the debug copies of X, before Newton-Schulz overwrites the DIRECT form's buffer
+    for (int h = 0; h < 2; ++h) {
+        uint16_t* dst = h == 0 ? opt.dbg_compact : opt.dbg_compact_lo;
+        if (!dst) continue;
+        CompactCopyArgs ca{h == 0 ? b.Z0 : b.Z1, dst, P.batch, (int)P.k, (int)P.d_oth,
+                           (int)P.kpad, (int)P.opad, P.z_is_L ? 0 : 1};
+        e = launch_copy_compact(ca, stream);
+        if (e != hipSuccess) return hip_fail(e, "launch debug copy of X");
+    }
     if (opt.decay_all && !cm) {
         DecayAllArgs da{ms, P.rows, P.cols, P.batch, mu};
         e = launch_decay_all(da, stream);
@@ -972,6 +981,8 @@ int validate_common(float mu, float lr, int ns_steps, const dion2_options& opt) 
         return fail(DION2_ERR_INVALID_ARG, "ns_master FP32 keeps the s x s chain in hi / lo pairs (ns_chain F16 given)");
     if (opt.ns_master == DION2_MASTER_FP32 && opt.ns_form == DION2_NS_DIRECT)
         return fail(DION2_ERR_UNSUPPORTED, "ns_master FP32 runs in the GRAM order (ns_form DIRECT given)");
+    if (opt.dbg_compact_lo && (opt.ns_master != DION2_MASTER_FP32 || ns_steps < 1))
+        return fail(DION2_ERR_INVALID_ARG, "dbg_compact_lo needs ns_master FP32 and ns_steps >= 1");
     if (opt.ns_coeffs) {
         for (int i = 0; i < 3 * ns_steps; ++i)
             if (!std::isfinite(opt.ns_coeffs[i]))
@@ -1051,7 +1062,7 @@ int groups_impl(const dion2_group* groups, int ngroups, float alpha, float mu, f
         return fail(DION2_ERR_INVALID_ARG, "ngroups %d not in [1, %d]", ngroups, kMaxGroups);
     if (opt.workspace)
         return fail(DION2_ERR_INVALID_ARG, "grouped calls use the library workspace (workspace must be NULL)");
-    if (opt.dbg_sel_idx || opt.dbg_norms || opt.dbg_update)
+    if (opt.dbg_sel_idx || opt.dbg_norms || opt.dbg_update || opt.dbg_compact || opt.dbg_compact_lo)
         return fail(DION2_ERR_INVALID_ARG, "grouped calls take no debug outputs");
     if (opt.group_streams < 0 || opt.group_streams > kMaxGroupStreams)
         return fail(DION2_ERR_INVALID_ARG, "group_streams %d not in [0, %d]", opt.group_streams,

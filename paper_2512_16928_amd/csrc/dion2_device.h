@@ -224,6 +224,16 @@ struct DecayAllArgs {
 };
 hipError_t launch_decay_all(const DecayAllArgs& a, hipStream_t s);
 
+// Copy of the compact matrix (hi or lo half) as the gather left it, unpadded,
+// line p in row p: out[b][p][j] for p < k, j < d_oth.
+struct CompactCopyArgs {
+    const uint16_t* Z;   // [batch][kpad][opad], or [batch][opad][kpad] when transposed
+    uint16_t* out;       // [batch][k][d_oth]
+    int batch, k, d_oth, kpad, opad;
+    int transposed;
+};
+hipError_t launch_copy_compact(const CompactCopyArgs& a, hipStream_t s);
+
 // Newton-Schulz GEMMs, C = A B with A given as rows [M][K]. With npass = 3
 // both operands come as bf16 hi + lo pairs (A0/A1, B0/B1) and
 // C = A0 B0 + A0 B1 + A1 B0; with npass = 2 only A does (C = A0 B0 + A1 B0).

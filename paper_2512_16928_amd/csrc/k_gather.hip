@@ -274,7 +274,27 @@ __global__ __launch_bounds__(kThreads) void decay_all(DecayAllArgs a) {
     }
 }
 
+__global__ __launch_bounds__(kThreads) void copy_compact(CompactCopyArgs a) {
+    const int b = blockIdx.y;
+    const int64_t n = (int64_t)a.k * a.d_oth;
+    const uint16_t* __restrict__ Z = a.Z + (int64_t)b * a.kpad * a.opad;
+    uint16_t* __restrict__ out = a.out + (int64_t)b * n;
+    for (int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x; i < n;
+         i += (int64_t)gridDim.x * kThreads) {
+        const int64_t p = i / a.d_oth, j = i % a.d_oth;
+        out[i] = a.transposed ? Z[j * a.kpad + p] : Z[p * a.opad + j];
+    }
+}
+
 }  // namespace
+
+hipError_t launch_copy_compact(const CompactCopyArgs& a, hipStream_t s) {
+    const int64_t n = (int64_t)a.k * a.d_oth;
+    int64_t blocks = (n + kThreads - 1) / kThreads;
+    if (blocks > 1024) blocks = 1024;
+    hipLaunchKernelGGL(copy_compact, dim3((unsigned)blocks, (unsigned)a.batch), dim3(kThreads), 0, s, a);
+    return hipGetLastError();
+}
 
 hipError_t launch_gather(const GatherArgs& a, int axis, int g_bf16, hipStream_t s) {
     if (axis == 0) {

@@ -56,6 +56,8 @@ def test_options_defaults(lib):
     assert not opt.ns_coeffs
     assert opt.ns_form == binding.NS_AUTO and opt.select_rule == binding.SELECT_L1
     assert opt.rand_seed == 0 and opt.rand_step == 0 and opt.rand_matrix0 == 0
+    assert opt.ns_chain == binding.CHAIN_HILO and opt.ns_master == binding.MASTER_BF16
+    assert not opt.dbg_compact and not opt.dbg_compact_lo
 
 
 FAKE = 0x10000   # a 256-aligned non-null address; never dereferenced below
@@ -129,6 +131,14 @@ def test_ex_options_validation(lib):
     # the fp32 master runs in the GRAM order: more workspace than the AUTO plan's DIRECT form here
     need_auto = binding.dion2_workspace_size(1, 64, 64, 0.25)
     assert ex(ns_master=1, workspace=FAKE, workspace_bytes=need_auto) == DION2_ERR_WORKSPACE
+    # the lo halves of X exist only with the fp32 master and a Newton-Schulz step
+    assert ex(dbg_compact_lo=FAKE) == DION2_ERR_INVALID_ARG
+    assert "dbg_compact_lo" in binding.dion2_last_error()
+    opt = Options()
+    lib.dion2_options_init(ctypes.byref(opt))
+    opt.ns_master, opt.dbg_compact_lo = 1, FAKE
+    st = lib.dion2_step_ex(FAKE, FAKE, FAKE, 1, 64, 64, 0.25, 0.95, 0.02, 0, -1, ctypes.byref(opt), None)
+    assert st == DION2_ERR_INVALID_ARG and "ns_steps" in binding.dion2_last_error()
     coeffs = (ctypes.c_float * 6)(1.0, 2.0, 3.0, 1.0, float("inf"), 0.0)
     assert ex(ns_coeffs=ctypes.cast(coeffs, ctypes.POINTER(ctypes.c_float))) == DION2_ERR_INVALID_ARG
     need = binding.dion2_workspace_size(1, 64, 64, 0.25)
@@ -194,6 +204,8 @@ def groups_array(specs):
     ([{"batch": 0}], 1, {}, "batch"),
     ([{}], 1, {"workspace": FAKE, "workspace_bytes": 1 << 30}, "workspace"),
     ([{}], 1, {"dbg_norms": FAKE}, "debug"),
+    ([{}], 1, {"dbg_compact": FAKE}, "debug"),
+    ([{}], 1, {"dbg_compact_lo": FAKE, "ns_master": 1}, "debug"),
     ([{}], 1, {"select_rule": 7}, "select_rule"),
     ([{"batch": 3}, {"batch": 3}], 2, {"select_rule": 1, "rand_matrix0": (1 << 32) - 5}, "rand_matrix0"),
 ])

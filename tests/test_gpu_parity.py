@@ -35,7 +35,7 @@ CHAINS = pytest.mark.parametrize("chain", [binding.CHAIN_HILO, binding.CHAIN_F16
 
 def run_gpu(W, M, G, alpha, ns_steps=5, axis=AXIS_AUTO, mu=0.95, lr=0.02, coeffs=None,
             decay_all=False, form=binding.NS_AUTO, rand=None, chain=binding.CHAIN_HILO,
-            master=binding.MASTER_BF16, eps=1e-7):
+            master=binding.MASTER_BF16, eps=1e-7, dbg_compact=None, dbg_compact_lo=None):
     """One library call on stacks [B, rows, cols]; returns host copies and the
     debug outputs."""
     B, rows, cols = W.shape
@@ -52,7 +52,8 @@ def run_gpu(W, M, G, alpha, ns_steps=5, axis=AXIS_AUTO, mu=0.95, lr=0.02, coeffs
                      rand_matrix0=rand[2])
     binding.dion2_step_ex(W, M, G, alpha, mu, lr, ns_steps, axis, ns_coeffs=coeffs, ns_eps=eps,
                           decay_all=decay_all, dbg_sel_idx=sel, dbg_norms=nrm, dbg_update=upd,
-                          ns_form=form, ns_chain=chain, ns_master=master, **extra)
+                          ns_form=form, ns_chain=chain, ns_master=master, dbg_compact=dbg_compact,
+                          dbg_compact_lo=dbg_compact_lo, **extra)
     torch.cuda.synchronize()
     return dict(W=W.cpu(), M=M.cpu(), K=sel.cpu(), norms=nrm.cpu(), O=upd.cpu(), W0=W0, M0=M0,
                 G=G.cpu(), axis=ax, k=k)
@@ -359,6 +360,86 @@ def test_mixed_w_and_g_dtypes(hip_device, wdt, gdt, axis):
     G = G.to(to[gdt]).contiguous()
     res = run_gpu(W, M, G, 0.25, axis=axis)
     check_matrix(res, 0, 0.25, axis=axis)
+
+
+def compact_x_want(M0, G, K, axis, eps):
+    """X as K3 writes it, from the oracle's accumulated momentum and its
+    Frobenius norm, with the rounding decisions taken in the kernel's
+    precision: x = fl32(m * fl32(1 / (||M[K]||_F + eps))), hi = bf16(x),
+    lo = bf16(x - hi). Also the fp64 quotient the definition rounds."""
+    Macc = oracle.momentum_accumulate(M0, G)
+    X = oracle.gather(Macc, K, axis)
+    if axis == AXIS_COLS:
+        X = X.T                                       # line p in row p
+    q = X / (np.linalg.norm(X) + eps)                 # the oracle's normalisation
+    sc = np.float32(1.0 / (np.linalg.norm(X) + eps))
+    x32 = X.astype(np.float32) * sc
+    hi = oracle.round_bf16(x32.astype(np.float64))
+    lo = oracle.round_bf16((x32 - hi.astype(np.float32)).astype(np.float64))
+    return hi, lo, q
+
+
+@pytest.mark.parametrize("rows,cols,alpha,axis,gdt,form,steps", [
+    (96, 256, 0.25, AXIS_ROWS, "bf16", binding.NS_AUTO, 5),     # L layout, DIRECT overwrites it
+    (200, 64, 0.5, AXIS_ROWS, "f32", binding.NS_AUTO, 5),       # k > d_oth: L^T layout
+    (256, 96, 0.25, AXIS_COLS, "bf16", NS_GRAM, 5),             # column gather (update_cols)
+    (64, 200, 0.5, AXIS_COLS, "f32", binding.NS_AUTO, 5),       # columns, L^T layout
+    (130, 70, 1.0, AXIS_AUTO, "bf16", binding.NS_AUTO, 0),      # ragged, no Newton-Schulz step
+])
+def test_compact_x_bitwise(hip_device, rows, cols, alpha, axis, gdt, form, steps):
+    """K3: the compact matrix equals the oracle's normalised selected lines,
+    rounded to bf16 in the kernel's precision, bit for bit, for every layout
+    and both gathers; the decayed M and the rest of the step as usual."""
+    wl = one_group_workload(rows, cols, count=3, axis=axis, w_dtype="f32", name=f"cx{rows}")
+    W, M, G = workloads.make_group(wl, 0, hip_device)
+    W = W.to(torch.bfloat16).contiguous()
+    G = G.to(torch.bfloat16 if gdt == "bf16" else torch.float32).contiguous()
+    B = W.shape[0]
+    k, ax = binding.dion2_plan_info(rows, cols, alpha, axis)
+    d_oth = cols if ax == AXIS_ROWS else rows
+    cx = torch.zeros((B, k, d_oth), dtype=torch.bfloat16, device=hip_device)
+    M0, G0 = M.cpu().numpy(), G.float().cpu().numpy()
+    res = run_gpu(W, M, G, alpha, ns_steps=steps, axis=axis, form=form, dbg_compact=cx)
+    got = cx.float().cpu().numpy().astype(np.float64)
+    eps = float(np.float32(1e-7))
+    for b in range(B):
+        check_matrix(res, b, alpha, ns_steps=steps, axis=axis)
+        hi, _, q = compact_x_want(M0[b], G0[b], res["K"][b].numpy().astype(np.int64), ax, eps)
+        np.testing.assert_array_equal(got[b], hi, err_msg=f"compact X, matrix {b}")
+        # against the fp64 definition only rounding-boundary cases may differ, by one unit
+        off = got[b] != oracle.round_bf16(q)
+        assert off.mean() < 1e-3
+        assert np.all(np.abs(got[b][off] - q[off]) <= 2.0 ** -7 * np.abs(q[off]))
+
+
+@pytest.mark.parametrize("rows,cols,alpha,axis", [
+    (160, 384, 0.25, AXIS_AUTO),     # rows, L layout
+    (200, 64, 0.5, AXIS_ROWS),       # rows, L^T layout
+    (64, 200, 0.5, AXIS_COLS),       # columns, L^T layout
+])
+def test_compact_x_lo_halves_fp32_master(hip_device, rows, cols, alpha, axis):
+    """With the fp32 master K3 also writes the lo halves bf16(x - bf16(x)):
+    both halves bitwise, and hi + lo within 2^-15 of the exact quotient
+    (2^-16 from rounding lo, 2^-23 from the fp32 quotient)."""
+    wl = one_group_workload(rows, cols, count=2, axis=axis, name=f"cxlo{rows}")
+    W, M, G = workloads.make_group(wl, 0, hip_device)
+    B = W.shape[0]
+    k, ax = binding.dion2_plan_info(rows, cols, alpha, axis)
+    d_oth = cols if ax == AXIS_ROWS else rows
+    hi_t = torch.zeros((B, k, d_oth), dtype=torch.bfloat16, device=hip_device)
+    lo_t = torch.zeros_like(hi_t)
+    M0, G0 = M.cpu().numpy(), G.float().cpu().numpy()
+    res = run_gpu(W, M, G, alpha, axis=axis, master=binding.MASTER_FP32, dbg_compact=hi_t,
+                  dbg_compact_lo=lo_t)
+    eps = float(np.float32(1e-7))
+    for b in range(B):
+        check_matrix(res, b, alpha, axis=axis, ns_tol=MASTER_TOL)
+        hi, lo, q = compact_x_want(M0[b], G0[b], res["K"][b].numpy().astype(np.int64), ax, eps)
+        gh = hi_t[b].float().cpu().numpy().astype(np.float64)
+        gl = lo_t[b].float().cpu().numpy().astype(np.float64)
+        np.testing.assert_array_equal(gh, hi, err_msg="hi halves")
+        np.testing.assert_array_equal(gl, lo, err_msg="lo halves")
+        assert np.all(np.abs(gh + gl - q) <= 2.0 ** -15 * np.abs(q))
 
 
 def test_decay_all_ablation(hip_device):
