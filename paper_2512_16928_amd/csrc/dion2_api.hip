@@ -903,7 +903,7 @@ int run_step(const Plan& P, void* W, float* M, const void* G, const Tables* tabs
                 w->tables_pending = false;
             }
             if (w->pinned_count < n) {
-                if (w->pinned) hipHostFree(w->pinned);
+                if (w->pinned) (void)hipHostFree(w->pinned);   // a failed free only leaks
                 w->pinned = nullptr;
                 w->pinned_count = 0;
                 e = hipHostMalloc(reinterpret_cast<void**>(&w->pinned), n * sizeof(void*));
@@ -1171,7 +1171,7 @@ int groups_impl(const dion2_group* groups, int ngroups, float alpha, float mu, f
             n = 0;
             return first;
         }
-        ~Join() { run(); }
+        ~Join() { (void)run(); }   // error paths: the status is already set
     } join{0, strm, ev_join, stream};
     if (nS > 1) {
         st = ensure_aux(w, nS, 1 + ngroups + nchain + nS);
@@ -1363,12 +1363,13 @@ void dion2_release_workspaces(void) {
     for (auto& kv : g_ws) {
         Workspace* w = kv.second;
         std::lock_guard<std::mutex> use(w->use);
-        if (hipSetDevice(kv.first.first) == hipSuccess) hipDeviceSynchronize();
-        if (w->dev) hipFree(w->dev);
-        if (w->pinned) hipHostFree(w->pinned);
-        if (w->tables_done) hipEventDestroy(w->tables_done);
-        for (hipStream_t a : w->aux) hipStreamDestroy(a);
-        for (hipEvent_t ev : w->ev) hipEventDestroy(ev);
+        // best effort: a failure here leaves memory to the process's end
+        if (hipSetDevice(kv.first.first) == hipSuccess) (void)hipDeviceSynchronize();
+        if (w->dev) (void)hipFree(w->dev);
+        if (w->pinned) (void)hipHostFree(w->pinned);
+        if (w->tables_done) (void)hipEventDestroy(w->tables_done);
+        for (hipStream_t a : w->aux) (void)hipStreamDestroy(a);
+        for (hipEvent_t ev : w->ev) (void)hipEventDestroy(ev);
         w->aux.clear();
         w->ev.clear();
         w->dev = nullptr;
@@ -1378,7 +1379,7 @@ void dion2_release_workspaces(void) {
         w->tables_done = nullptr;
         w->tables_pending = false;
     }
-    if (prev >= 0) hipSetDevice(prev);
+    if (prev >= 0) (void)hipSetDevice(prev);
 }
 
 int dion2_profile_enable(int on) {
@@ -1423,7 +1424,7 @@ int dion2_profile_read(double* ms, int64_t* calls, int64_t* launches, double* fl
 void dion2_profile_reset(void) {
     std::lock_guard<std::mutex> lk(g_prof.mu);
     for (const ProfRecord& r : g_prof.pending) {
-        hipEventSynchronize(r.stop);
+        (void)hipEventSynchronize(r.stop);   // the events are reused; their times are dropped
         g_prof.pool.push_back(r.start);
         g_prof.pool.push_back(r.stop);
     }

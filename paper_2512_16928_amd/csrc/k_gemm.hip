@@ -667,12 +667,14 @@ hipError_t launch_gemm(const GemmArgs& a, GemmEpi epi, int npass, hipStream_t s)
     // for more than ring depth: 128 x 128 tiles keep enough blocks in flight;
     // from s = 1024 the Gram matrix runs faster on
     // 256 x 256 tiles of 8 waves; the X-side products use a two-stage ring,
-    // which leaves room for three blocks per CU.
+    // which leaves room for three blocks per CU; with the update applied in
+    // the epilogue eight waves per block hide more of the W traffic.
     using TG = Tile<1, 0, 128, 128, 32, 2, 2, 4>;    // Gram
     using TGL = Tile<1, 0, 256, 256, 32, 4, 2, 3>;   // Gram, large s
     using TP = Tile<3, 0, 128, 128, 32, 4, 2, 2>;    // three-pass symmetric products
     using TU = Tile<1, 1, 128, 128, 32, 2, 2, 2>;    // update (B operand [K][N])
     using TU2 = Tile<2, 1, 128, 128, 32, 2, 2, 2>;   // two-pass final product
+    using TU2A = Tile<2, 1, 128, 128, 32, 4, 2, 2>;  // two-pass final product applying the update
     using TU3 = Tile<3, 1, 128, 128, 32, 2, 2, 2>;   // three-pass final product (fp32 master)
     using TH = Tile<1, 0, 128, 128, 32, 2, 2, 4, true>;   // fp16 s x s products
     if (a.f16) {
@@ -717,8 +719,10 @@ hipError_t launch_gemm(const GemmArgs& a, GemmEpi epi, int npass, hipStream_t s)
         case EPI_APPLY:
             if (a.cols % 8 || a.cols < 16 || a.out_transposed) break;
             if (npass == 1) return launch_tile<1, EPI_APPLY, TU>(a, s);
-            if (npass == 2) return launch_tile<2, EPI_APPLY, TU2>(a, s);
+            if (npass == 2) return launch_tile<2, EPI_APPLY, TU2A>(a, s);
             if (npass == 3) return launch_tile<3, EPI_APPLY, TU3>(a, s);
+            break;
+        default:   // the fp16 epilogues run only with fp16 operands (above)
             break;
     }
     return hipErrorInvalidValue;
