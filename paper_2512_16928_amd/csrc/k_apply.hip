@@ -228,9 +228,12 @@ __global__ __launch_bounds__(kThreads) void apply_cols_strip(ApplyArgs a) {
     __shared__ __attribute__((aligned(16))) float ot[kStripRows][kOtPitch];
     const int b = blockIdx.z;
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    const int64_t s0 = (int64_t)blockIdx.x * kStrip;
+    // blocks run along the strips of one row block, then the next row block
+    // (one grid dimension: a million rows make 65536 row blocks)
+    const int64_t nstrips = (a.cols + kStrip - 1) / kStrip;
+    const int64_t s0 = ((int64_t)blockIdx.x % nstrips) * kStrip;
     const int64_t s1 = s0 + kStrip < a.cols ? s0 + kStrip : a.cols;
-    const int64_t r0 = (int64_t)blockIdx.y * kStripRows;
+    const int64_t r0 = ((int64_t)blockIdx.x / nstrips) * kStripRows;
     const int32_t* __restrict__ rank = a.rank + (int64_t)b * (a.cols + 1);
     WT* __restrict__ W = a.ms.w<WT>(b);
     const float* __restrict__ OT = a.O + (int64_t)b * a.opad * a.kpad;
@@ -441,8 +444,8 @@ hipError_t launch_apply(const ApplyArgs& a, int axis, int w_bf16, hipStream_t s)
     } else if (w_bf16 ? launch_cols_sel<uint16_t>(a, s) : launch_cols_sel<float>(a, s)) {
         // whole rows per wave, one update per selected entry
     } else if (a.cols % kLaneCols == 0) {
-        dim3 grid((unsigned)((a.cols + kStrip - 1) / kStrip),
-                  (unsigned)((a.rows + kStripRows - 1) / kStripRows), (unsigned)a.batch);
+        const int64_t blocks = (a.cols + kStrip - 1) / kStrip * ((a.rows + kStripRows - 1) / kStripRows);
+        dim3 grid((unsigned)blocks, 1, (unsigned)a.batch);
         if (w_bf16) hipLaunchKernelGGL((apply_cols_strip<uint16_t>), grid, dim3(kThreads), 0, s, a);
         else hipLaunchKernelGGL((apply_cols_strip<float>), grid, dim3(kThreads), 0, s, a);
     } else {

@@ -442,6 +442,74 @@ def test_compact_x_lo_halves_fp32_master(hip_device, rows, cols, alpha, axis):
         assert np.all(np.abs(gh + gl - q) <= 2.0 ** -15 * np.abs(q))
 
 
+@pytest.mark.parametrize("rows,cols,axis", [
+    (1 << 20, 64, AXIS_AUTO),     # columns of a million entries: Gram over K = 2^20
+    (1 << 20, 16, AXIS_ROWS),     # 2^20 lines to select from (keys beyond the LDS cache), L^T
+    (16, 1 << 20, AXIS_AUTO),     # rows of a million entries: 8192 column tiles, fused update
+])
+def test_maximum_dimension(hip_device, rows, cols, axis):
+    """A side of 2^20, the longest the library takes, against the whole
+    oracle step (the oracle's exact l1 sums take about 15 s here)."""
+    wl = one_group_workload(rows, cols, axis=axis, name=f"max{rows}x{cols}")
+    W, M, G = workloads.make_group(wl, 0, hip_device)
+    k, ax = binding.dion2_plan_info(rows, cols, 0.25, axis)
+    d_oth = cols if ax == AXIS_ROWS else rows
+    cx = torch.zeros((1, k, d_oth), dtype=torch.bfloat16, device=hip_device)
+    M0, G0 = M.cpu().numpy(), G.float().cpu().numpy()
+    res = run_gpu(W, M, G, 0.25, axis=axis, dbg_compact=cx)
+    check_matrix(res, 0, 0.25, axis=axis)
+    hi, _, _ = compact_x_want(M0[0], G0[0], res["K"][0].numpy().astype(np.int64), ax,
+                              float(np.float32(1e-7)))
+    np.testing.assert_array_equal(cx[0].float().cpu().numpy().astype(np.float64), hi)
+
+
+def test_maximum_rows_column_strips(hip_device):
+    """2^20 rows x 1032 columns at alpha = 1: every column selected, k > 1024,
+    so the update runs on the 512-column strip kernel over 65536 row blocks,
+    and the Gram product sums over K = 2^20. The oracle's whole step is out of
+    reach at this size (about 2e13 fp64 flops), so the test checks what holds
+    at any size: K, the l1 norms of sampled columns (exact sums), M and W
+    bitwise on sampled rows (W given the GPU's O), X bitwise on sampled rows,
+    and every singular value of O inside the band the five quintic steps
+    reach from a well-conditioned start, [0.68, 1.2] (Sec. 1)."""
+    rows, cols, lr, mu = 1 << 20, 1032, 0.02, 0.95
+    wl = one_group_workload(rows, cols, axis=AXIS_COLS, name="maxstrip")
+    W, M, G = workloads.make_group(wl, 0, hip_device)
+    k, ax = binding.dion2_plan_info(rows, cols, 1.0, AXIS_COLS)
+    assert (k, ax) == (cols, AXIS_COLS)
+    rng = np.random.default_rng(7)
+    rs = np.unique(np.concatenate([[0, 1, rows - 1], rng.integers(0, rows, 61)]))
+    cs = np.array([0, 1, 517, cols - 1])
+    rs_t = torch.from_numpy(rs).to(hip_device)
+    W0 = W[0, rs_t].float().cpu().numpy().astype(np.float64)
+    M0, G0 = M[0].cpu().numpy(), G[0].float().cpu().numpy()
+    sel = torch.full((1, k), -1, dtype=torch.int32, device=hip_device)
+    nrm = torch.full((1, cols), -1.0, dtype=torch.float64, device=hip_device)
+    upd = torch.full((1, k, rows), float("nan"), dtype=torch.float32, device=hip_device)
+    cx = torch.zeros((1, k, rows), dtype=torch.bfloat16, device=hip_device)
+    binding.dion2_step_ex(W, M, G, 1.0, mu, lr, 5, AXIS_COLS, dbg_sel_idx=sel, dbg_norms=nrm,
+                          dbg_update=upd, dbg_compact=cx)
+    torch.cuda.synchronize()
+    K = np.arange(cols)
+    np.testing.assert_array_equal(sel[0].cpu().numpy(), K)
+    Macc = oracle.momentum_accumulate(M0, G0)
+    np.testing.assert_array_equal(nrm[0].cpu().numpy()[cs], oracle.l1_norms(Macc[:, cs], AXIS_COLS))
+    M_want = oracle.selective_decay(Macc[rs], K, mu, AXIS_COLS)
+    np.testing.assert_array_equal(M[0, rs_t].cpu().numpy(), M_want, err_msg="momentum rows")
+    O_rows = upd[0][:, rs_t].cpu().numpy().astype(np.float64).T      # O[r, p], paper orientation
+    W_want = oracle.round_to(W0 - oracle.update_scale(lr, rows, cols) * O_rows, "bf16")
+    np.testing.assert_array_equal(W[0, rs_t].float().cpu().numpy().astype(np.float64), W_want,
+                                  err_msg="weight rows")
+    fro = math.sqrt(sum(float(np.sum(np.square(Macc[i:i + 65536].astype(np.float64))))
+                        for i in range(0, rows, 65536)))
+    sc = np.float32(1.0 / (fro + float(np.float32(1e-7))))
+    x_want = oracle.round_bf16((Macc[rs].astype(np.float32) * sc).astype(np.float64))
+    np.testing.assert_array_equal(cx[0][:, rs_t].float().cpu().numpy().astype(np.float64).T, x_want)
+    O = upd[0].cpu().numpy()                                          # [k, rows] fp32
+    ev = np.linalg.eigvalsh(O @ O.T)
+    assert 0.68 ** 2 - 1e-2 <= ev.min() and ev.max() <= 1.2 ** 2 + 1e-2, (ev.min(), ev.max())
+
+
 def test_decay_all_ablation(hip_device):
     wl = one_group_workload(128, 256, name="decayall")
     W, M, G = workloads.make_group(wl, 0, hip_device)
