@@ -308,13 +308,23 @@ def main(argv=None):
     phases = {}
     roofline = None
     ns_frac = None
+    mfma_counters = {}
     if not args.no_profile:
         phases = profile_phases(wl, groups, alpha, args.steps)
         dom = max(phases, key=lambda p: phases[p]["total_ms_per_step"])
         d = phases[dom]
+        # the committed counter summaries were taken with the default
+        # Newton-Schulz settings; other settings run other kernels
+        profiled = (args.ns_chain == "hilo" and args.ns_master == "bf16" and args.ns_form == "auto"
+                    and wl.ns_steps == workloads.WORKLOADS[args.workload].ns_steps)
         traffic = None
         for path in sorted(glob.glob(os.path.join(ROOT, "profiles", "*traffic*.txt"))):
-            traffic = traffic or profsum.lookup_traffic(path, dom, wl.name, alpha)
+            traffic = traffic or (profsum.lookup_traffic(path, dom, wl.name, alpha) if profiled else None)
+        for p in NS_PHASES:
+            for path in sorted(glob.glob(os.path.join(ROOT, "profiles", "*mfma*.txt"))):
+                hit = profsum.lookup_mfma(path, p, wl.name, alpha) if profiled else None
+                if hit and p not in mfma_counters:
+                    mfma_counters[p] = hit
         roofline = dict(bound=d["bound"], achieved=round(d["achieved"], 3), peak=d["peak"],
                         unit=d["unit"], frac=round(d["frac"], 4),
                         traffic=None if traffic is None else round(traffic),
@@ -412,6 +422,7 @@ def main(argv=None):
         "per_chain_ms": per_chain,
         "per_master_ms": per_master,
         "ns_mfma_frac": None if ns_frac is None else round(ns_frac, 4),
+        "ns_mfma_counters": mfma_counters or None,
         "step_ms_stats": {"mean": round(ms, 4), "median": round(statistics.median(per), 4),
                           "min": round(min(per), 4), "mean_last_20": round(statistics.mean(tail), 4),
                           "wall_s": round(wall, 3)},

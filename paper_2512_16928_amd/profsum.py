@@ -9,9 +9,16 @@
         the calibration copy (a single elementwise kernel, `torch.neg` of
         2^28 fp32 values: 1 GiB read, 1 GiB written)
 
-The traffic summary ends with one `traffic ...` line per phase, tagged with
-a hash of the kernel sources it was taken on; bench.py reports a phase's
-traffic only while those sources are unchanged.
+    python -m paper_2512_16928_amd.profsum mfma PMC_DIR STATS_DIR --workload W --alpha A
+        MFMA utilisation of the Newton-Schulz phases from a `--pmc MfmaUtil
+        MfmaFlopsBF16 MfmaFlopsF16` run (rocprofv3's derived counters: busy
+        cycles of the matrix cores over active cycles of every SIMD, and 512
+        flops per counted matrix op), with the kernels' average durations
+        from a `--kernel-trace --stats` run of the same command
+
+The traffic and MFMA summaries end with one line per phase, tagged with a
+hash of the kernel sources it was taken on; bench.py reports a phase's
+figures only while those sources are unchanged.
 """
 from __future__ import annotations
 
@@ -193,6 +200,88 @@ def cmd_traffic(args):
         print(ln)
 
 
+MFMA_PEAK_FLOPS = {"bf16": 2.5e15, "f16": 2.5e15}   # dense matrix-core peaks of MI355X
+NS_PHASES = ("ns_gram", "ns_poly", "ns_update")
+
+
+def read_values(d: str, counters):
+    """{dispatch id: (kernel name, {counter: [values]})} for the given counters."""
+    path = find_csv(d, "counter_collection.csv")
+    out = {}
+    for r in csv.DictReader(open(path)):
+        c = r["Counter_Name"]
+        if c not in counters:
+            continue
+        ent = out.setdefault(int(r["Dispatch_Id"]), (r["Kernel_Name"], {}))
+        ent[1].setdefault(c, []).append(float(r["Counter_Value"]))
+    return out
+
+
+def kernel_durations(d: str):
+    """{short kernel name: average duration in ns} from a kernel-stats run."""
+    rows = csv.DictReader(open(find_csv(d, "kernel_stats.csv")))
+    return {short_name(r["Name"]): float(r["AverageNs"]) for r in rows if phase_of(r["Name"])}
+
+
+def cmd_mfma(args):
+    data = read_values(args.pmc_dir, ("MfmaUtil", "MfmaFlopsBF16", "MfmaFlopsF16"))
+    dur = kernel_durations(args.stats_dir)
+    acc = {}
+    for name, vals in data.values():
+        ph = phase_of(name)
+        if ph not in NS_PHASES:
+            continue
+        k = short_name(name)
+        a = acc.setdefault(ph, {}).setdefault(k, [0, 0.0, 0.0])
+        a[0] += 1
+        a[1] += statistics.mean(vals.get("MfmaUtil", [0.0]))
+        a[2] += sum(vals.get("MfmaFlopsBF16", [0.0])) + sum(vals.get("MfmaFlopsF16", [0.0]))
+    peak = MFMA_PEAK_FLOPS["bf16"]
+    print(f"{'kernel':72s} {'n':>5s} {'MfmaUtil %':>10s} {'GFLOP/disp':>11s} {'avg us':>8s} {'TFLOP/s':>8s} {'of peak':>8s}")
+    lines = []
+    for ph in NS_PHASES:
+        if ph not in acc:
+            continue
+        n_tot = t_tot = f_tot = u_w = 0.0
+        for k, (n, u, f) in acc[ph].items():
+            us = dur.get(k, float("nan")) / 1e3
+            print(f"{k:72s} {n:5d} {u / n:10.1f} {f / n / 1e9:11.2f} {us:8.2f} "
+                  f"{f / n / us / 1e6:8.1f} {f / n / us / 1e6 / (peak / 1e12):8.3f}")
+            n_tot += n
+            t_tot += n * us
+            f_tot += f
+            u_w += u * us          # utilisation weighted by each dispatch's duration
+        util = u_w / t_tot
+        tflops = f_tot / t_tot / 1e6
+        lines.append(f"mfma phase={ph} workload={args.workload} alpha={args.alpha} "
+                     f"sources={source_hash(ph)} mfma_util_pct={util:.2f} "
+                     f"counted_flops_per_launch={f_tot / n_tot:.0f} avg_launch_us={t_tot / n_tot:.2f} "
+                     f"counted_tflops={tflops:.1f} frac_of_peak={tflops * 1e12 / peak:.4f} "
+                     f"launches={n_tot:.0f}")
+    print()
+    for ln in lines:
+        print(ln)
+
+
+def lookup_mfma(path: str, phase: str, workload: str, alpha: float):
+    """The counter-based MFMA figures of `phase` from a committed summary, or
+    None when absent or taken on other kernel sources."""
+    if not os.path.exists(path):
+        return None
+    want = source_hash(phase)
+    for ln in open(path):
+        if not ln.startswith("mfma "):
+            continue
+        kv = dict(x.split("=", 1) for x in ln.split()[1:])
+        if (kv.get("phase") == phase and kv.get("workload") == workload
+                and float(kv.get("alpha", "nan")) == alpha and kv.get("sources") == want):
+            return {"mfma_util_pct": float(kv["mfma_util_pct"]),
+                    "counted_flops_per_launch": float(kv["counted_flops_per_launch"]),
+                    "counted_tflops": float(kv["counted_tflops"]),
+                    "frac_of_peak": float(kv["frac_of_peak"])}
+    return None
+
+
 def lookup_traffic(path: str, phase: str, workload: str, alpha: float):
     """Scaled HBM bytes per launch of `phase` from a committed traffic summary,
     or None when absent or taken on other kernel sources."""
@@ -220,8 +309,13 @@ def main(argv=None):
     t.add_argument("write_dir")
     t.add_argument("--workload", required=True)
     t.add_argument("--alpha", type=float, required=True)
+    m = sub.add_parser("mfma")
+    m.add_argument("pmc_dir")
+    m.add_argument("stats_dir")
+    m.add_argument("--workload", required=True)
+    m.add_argument("--alpha", type=float, required=True)
     args = ap.parse_args(argv)
-    {"stats": cmd_stats, "traffic": cmd_traffic}[args.cmd](args)
+    {"stats": cmd_stats, "traffic": cmd_traffic, "mfma": cmd_mfma}[args.cmd](args)
 
 
 if __name__ == "__main__":

@@ -42,6 +42,51 @@ def test_traffic_lookup_requires_matching_sources(tmp_path):
     assert profsum.lookup_traffic(str(f), "apply", "1b", 0.25) is None      # stale sources
 
 
+def test_mfma_lookup_requires_matching_sources(tmp_path):
+    f = tmp_path / "m.txt"
+    good = profsum.source_hash("ns_poly")
+    f.write_text("kernel table ...\n"
+                 f"mfma phase=ns_poly workload=1b alpha=0.25 sources={good} mfma_util_pct=16.5 "
+                 "counted_flops_per_launch=2e10 avg_launch_us=35.0 counted_tflops=571.4 "
+                 "frac_of_peak=0.2286 launches=126\n"
+                 "mfma phase=ns_gram workload=1b alpha=0.25 sources=0000000000000000 mfma_util_pct=1 "
+                 "counted_flops_per_launch=1 avg_launch_us=1 counted_tflops=1 frac_of_peak=0.1 launches=1\n")
+    hit = profsum.lookup_mfma(str(f), "ns_poly", "1b", 0.25)
+    assert hit == {"mfma_util_pct": 16.5, "counted_flops_per_launch": 2e10, "counted_tflops": 571.4,
+                   "frac_of_peak": 0.2286}
+    assert profsum.lookup_mfma(str(f), "ns_poly", "7b", 0.25) is None      # other workload
+    assert profsum.lookup_mfma(str(f), "ns_gram", "1b", 0.25) is None      # stale sources
+
+
+def test_mfma_summary_from_counter_csv(tmp_path, capsys):
+    """profsum mfma: per-dispatch counters and the stats run's durations give
+    the phase's counted TFLOP/s and duration-weighted MfmaUtil."""
+    k_poly = "void dion2::(anonymous namespace)::gemm<3, 0, Tile<3, 0, 128, 128, 32, 4, 2, 2, false>, true>(dion2::GemmArgs)"
+    k_mom = "void dion2::(anonymous namespace)::momentum_rows<4, unsigned short>(dion2::MatSet)"
+    pmc = tmp_path / "pmc"
+    st = tmp_path / "st"
+    pmc.mkdir()
+    st.mkdir()
+    rows = ['"Dispatch_Id","Kernel_Name","Counter_Name","Counter_Value"']
+    for d, util, fl in ((1, 10.0, 1e10), (2, 30.0, 3e10)):
+        rows += [f'{d},"{k_poly}","MfmaUtil",{util}', f'{d},"{k_poly}","MfmaFlopsBF16",{fl}',
+                 f'{d},"{k_poly}","MfmaFlopsF16",0']
+    rows.append(f'3,"{k_mom}","MfmaUtil",0')
+    (pmc / "run_counter_collection.csv").write_text("\n".join(rows) + "\n")
+    (st / "run_kernel_stats.csv").write_text(
+        '"Name","Calls","TotalDurationNs","AverageNs"\n'
+        f'"{k_poly}",2,80000,40000\n"{k_mom}",1,1000,1000\n')
+    profsum.main(["mfma", str(pmc), str(st), "--workload", "1b", "--alpha", "0.25"])
+    out = capsys.readouterr().out
+    line = [ln for ln in out.splitlines() if ln.startswith("mfma ")]
+    assert len(line) == 1 and "phase=ns_poly" in line[0]
+    kv = dict(x.split("=", 1) for x in line[0].split()[1:])
+    assert float(kv["mfma_util_pct"]) == 20.0                   # equal durations: the plain mean
+    assert float(kv["counted_flops_per_launch"]) == 2e10
+    assert abs(float(kv["counted_tflops"]) - 500.0) < 1e-9     # 2e10 flops in 40 us
+    assert abs(float(kv["frac_of_peak"]) - 0.2) < 1e-9
+
+
 def test_bench_refuses_more_than_one_gpu():
     r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", "2"],
                        capture_output=True, text=True, timeout=300)
