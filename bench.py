@@ -45,6 +45,7 @@ HBM_PEAK_GBS = 8000.0          # MI355X HBM3E
 MFMA_BF16_PEAK_TFS = 2500.0    # MI355X dense bf16 MFMA
 RIDGE_FLOP_PER_BYTE = MFMA_BF16_PEAK_TFS * 1e12 / (HBM_PEAK_GBS * 1e9)
 NS_PHASES = ("ns_gram", "ns_poly", "ns_update")
+STREAMING_PHASES = ("momentum", "gather", "apply")
 
 
 def log(msg):
@@ -309,6 +310,7 @@ def main(argv=None):
     roofline = None
     ns_frac = None
     mfma_counters = {}
+    hbm_counters = {}
     if not args.no_profile:
         phases = profile_phases(wl, groups, alpha, args.steps)
         dom = max(phases, key=lambda p: phases[p]["total_ms_per_step"])
@@ -320,6 +322,11 @@ def main(argv=None):
         traffic = None
         for path in sorted(glob.glob(os.path.join(ROOT, "profiles", "*traffic*.txt"))):
             traffic = traffic or (profsum.lookup_traffic(path, dom, wl.name, alpha) if profiled else None)
+        for p in STREAMING_PHASES:
+            for path in sorted(glob.glob(os.path.join(ROOT, "profiles", "*traffic*.txt"))):
+                hit = profsum.lookup_hbm_rate(path, p, wl.name, alpha) if profiled else None
+                if hit and p not in hbm_counters:
+                    hbm_counters[p] = hit
         for p in NS_PHASES:
             for path in sorted(glob.glob(os.path.join(ROOT, "profiles", "*mfma*.txt"))):
                 hit = profsum.lookup_mfma(path, p, wl.name, alpha) if profiled else None
@@ -423,6 +430,7 @@ def main(argv=None):
         "per_master_ms": per_master,
         "ns_mfma_frac": None if ns_frac is None else round(ns_frac, 4),
         "ns_mfma_counters": mfma_counters or None,
+        "streaming_hbm_counters": hbm_counters or None,
         "step_ms_stats": {"mean": round(ms, 4), "median": round(statistics.median(per), 4),
                           "min": round(min(per), 4), "mean_last_20": round(statistics.mean(tail), 4),
                           "wall_s": round(wall, 3)},

@@ -3,11 +3,13 @@
     python -m paper_2512_16928_amd.profsum stats DIR
         per-kernel and per-phase launch statistics from a
         `rocprofv3 --kernel-trace --stats -f csv -d DIR` run
-    python -m paper_2512_16928_amd.profsum traffic FETCH_DIR WRITE_DIR --workload W --alpha A
+    python -m paper_2512_16928_amd.profsum traffic FETCH_DIR WRITE_DIR --workload W --alpha A [--stats DIR]
         HBM bytes per launch of every phase from two `--pmc FETCH_SIZE` and
         `--pmc WRITE_SIZE` runs, scaled by what the same counters read for
         the calibration copy (a single elementwise kernel, `torch.neg` of
-        2^28 fp32 values: 1 GiB read, 1 GiB written)
+        2^28 fp32 values: 1 GiB read, 1 GiB written); with the kernels'
+        average durations from a `--kernel-trace --stats` run, also the
+        counted HBM GB/s against the 8 TB/s peak
 
     python -m paper_2512_16928_amd.profsum mfma PMC_DIR STATS_DIR --workload W --alpha A
         MFMA utilisation of the Newton-Schulz phases from a `--pmc MfmaUtil
@@ -178,29 +180,42 @@ def cmd_traffic(args):
         return acc
 
     pf, pw = per_phase(fetch, f_fetch), per_phase(write, f_write)
-    print(f"{'kernel':72s} {'n':>5s} {'read MiB':>10s} {'write MiB':>10s}  (scaled, per dispatch)")
+    dur = kernel_durations(args.stats) if args.stats else {}
+    print(f"{'kernel':72s} {'n':>5s} {'read MiB':>10s} {'write MiB':>10s}  (scaled, per dispatch)"
+          + (f" {'avg us':>8s} {'GB/s':>8s}" if dur else ""))
     lines = []
     for ph in PHASE_SOURCES:
         if ph not in pf or ph not in pw:
             continue
         nf_tot = sum(n for n, _ in pf[ph].values())
         nw_tot = sum(n for n, _ in pw[ph].values())
+        t_tot = 0.0   # ns over the phase's dispatches, from the stats run
         for k in pf[ph]:
             n, b = pf[ph][k]
             wn, wb = pw[ph].get(k, (1, 0.0))
-            print(f"{k:72s} {n:5d} {b / n / 2**20:10.2f} {wb / max(wn, 1) / 2**20:10.2f}")
+            row = f"{k:72s} {n:5d} {b / n / 2**20:10.2f} {wb / max(wn, 1) / 2**20:10.2f}"
+            if dur:
+                ns = dur.get(k, float("nan"))
+                t_tot += n * ns
+                row += f" {ns / 1e3:8.2f} {(b / n + wb / max(wn, 1)) / ns:8.1f}"
+            print(row)
         rd = sum(b for _, b in pf[ph].values()) / nf_tot
         wr = sum(b for _, b in pw[ph].values()) / nw_tot
+        rate = ""
+        if dur:
+            gbs = (rd + wr) / (t_tot / nf_tot)
+            rate = f" avg_launch_us={t_tot / nf_tot / 1e3:.2f} counted_gbs={gbs:.1f} frac_of_peak={gbs / HBM_PEAK_GBS:.4f}"
         lines.append(f"traffic phase={ph} workload={args.workload} alpha={args.alpha} "
                      f"sources={source_hash(ph)} read_bytes_per_launch={rd:.0f} "
                      f"write_bytes_per_launch={wr:.0f} bytes_per_launch={rd + wr:.0f} "
-                     f"launches={nf_tot}")
+                     f"launches={nf_tot}{rate}")
     print()
     for ln in lines:
         print(ln)
 
 
 MFMA_PEAK_FLOPS = {"bf16": 2.5e15, "f16": 2.5e15}   # dense matrix-core peaks of MI355X
+HBM_PEAK_GBS = 8000.0                                 # MI355X HBM3E
 NS_PHASES = ("ns_gram", "ns_poly", "ns_update")
 
 
@@ -266,36 +281,45 @@ def cmd_mfma(args):
 def lookup_mfma(path: str, phase: str, workload: str, alpha: float):
     """The counter-based MFMA figures of `phase` from a committed summary, or
     None when absent or taken on other kernel sources."""
+    kv = lookup_line(path, "mfma", phase, workload, alpha)
+    if kv is None:
+        return None
+    return {"mfma_util_pct": float(kv["mfma_util_pct"]),
+            "counted_flops_per_launch": float(kv["counted_flops_per_launch"]),
+            "counted_tflops": float(kv["counted_tflops"]),
+            "frac_of_peak": float(kv["frac_of_peak"])}
+
+
+def lookup_line(path: str, kind: str, phase: str, workload: str, alpha: float):
+    """The key=value fields of the `kind` line of `phase` in a committed
+    summary, or None when absent or taken on other kernel sources."""
     if not os.path.exists(path):
         return None
     want = source_hash(phase)
     for ln in open(path):
-        if not ln.startswith("mfma "):
+        if not ln.startswith(kind + " "):
             continue
         kv = dict(x.split("=", 1) for x in ln.split()[1:])
         if (kv.get("phase") == phase and kv.get("workload") == workload
                 and float(kv.get("alpha", "nan")) == alpha and kv.get("sources") == want):
-            return {"mfma_util_pct": float(kv["mfma_util_pct"]),
-                    "counted_flops_per_launch": float(kv["counted_flops_per_launch"]),
-                    "counted_tflops": float(kv["counted_tflops"]),
-                    "frac_of_peak": float(kv["frac_of_peak"])}
+            return kv
     return None
 
 
 def lookup_traffic(path: str, phase: str, workload: str, alpha: float):
     """Scaled HBM bytes per launch of `phase` from a committed traffic summary,
     or None when absent or taken on other kernel sources."""
-    if not os.path.exists(path):
+    kv = lookup_line(path, "traffic", phase, workload, alpha)
+    return None if kv is None else float(kv["bytes_per_launch"])
+
+
+def lookup_hbm_rate(path: str, phase: str, workload: str, alpha: float):
+    """Counted HBM GB/s of `phase` (scaled counter bytes over the average
+    launch duration) and its fraction of the peak, or None."""
+    kv = lookup_line(path, "traffic", phase, workload, alpha)
+    if kv is None or "counted_gbs" not in kv:
         return None
-    want = source_hash(phase)
-    for ln in open(path):
-        if not ln.startswith("traffic "):
-            continue
-        kv = dict(x.split("=", 1) for x in ln.split()[1:])
-        if (kv.get("phase") == phase and kv.get("workload") == workload
-                and float(kv.get("alpha", "nan")) == alpha and kv.get("sources") == want):
-            return float(kv["bytes_per_launch"])
-    return None
+    return {"counted_gbs": float(kv["counted_gbs"]), "frac_of_peak": float(kv["frac_of_peak"])}
 
 
 def main(argv=None):
@@ -309,6 +333,7 @@ def main(argv=None):
     t.add_argument("write_dir")
     t.add_argument("--workload", required=True)
     t.add_argument("--alpha", type=float, required=True)
+    t.add_argument("--stats", default=None)
     m = sub.add_parser("mfma")
     m.add_argument("pmc_dir")
     m.add_argument("stats_dir")

@@ -40,6 +40,13 @@ def test_traffic_lookup_requires_matching_sources(tmp_path):
     assert profsum.lookup_traffic(str(f), "ns_poly", "1b", 0.25) == 3.0
     assert profsum.lookup_traffic(str(f), "ns_poly", "1b", 0.5) is None     # other workload point
     assert profsum.lookup_traffic(str(f), "apply", "1b", 0.25) is None      # stale sources
+    assert profsum.lookup_hbm_rate(str(f), "ns_poly", "1b", 0.25) is None   # no durations given
+    good = profsum.source_hash("gather")
+    f.write_text(f"traffic phase=gather workload=1b alpha=0.25 sources={good} read_bytes_per_launch=1 "
+                 "write_bytes_per_launch=2 bytes_per_launch=3 launches=9 avg_launch_us=241.08 "
+                 "counted_gbs=5758.4 frac_of_peak=0.7198\n")
+    assert profsum.lookup_hbm_rate(str(f), "gather", "1b", 0.25) == {"counted_gbs": 5758.4,
+                                                                       "frac_of_peak": 0.7198}
 
 
 def test_mfma_lookup_requires_matching_sources(tmp_path):
