@@ -48,6 +48,24 @@ NS_PHASES = ("ns_gram", "ns_poly", "ns_update")
 STREAMING_PHASES = ("momentum", "gather", "apply")
 
 
+def mfma_per_alpha(workload, per_alpha, profiled):
+    """{alpha: {phase: counter figures}} from the committed MFMA summaries, for
+    the selection fractions this run timed (default Newton-Schulz settings only)."""
+    out = {}
+    if not profiled:
+        return out
+    paths = sorted(glob.glob(os.path.join(ROOT, "profiles", "*mfma*.txt")))
+    for a in per_alpha:
+        for p in NS_PHASES:
+            for path in paths:
+                hit = profsum.lookup_mfma(path, p, workload, float(a))
+                if hit:
+                    out.setdefault(a, {})[p] = {"mfma_util_pct": hit["mfma_util_pct"],
+                                                "frac_of_peak": hit["frac_of_peak"]}
+                    break
+    return out
+
+
 def log(msg):
     print(msg, file=sys.stderr, flush=True)
 
@@ -306,6 +324,10 @@ def main(argv=None):
     ms = statistics.mean(per)
     log(f"[bench] alpha={alpha}: {ms:.3f} ms/step (min {min(per):.3f})")
 
+    # the committed counter summaries were taken with the default
+    # Newton-Schulz settings; other settings run other kernels
+    profiled = (args.ns_chain == "hilo" and args.ns_master == "bf16" and args.ns_form == "auto"
+                and wl.ns_steps == workloads.WORKLOADS[args.workload].ns_steps)
     phases = {}
     roofline = None
     ns_frac = None
@@ -315,10 +337,6 @@ def main(argv=None):
         phases = profile_phases(wl, groups, alpha, args.steps)
         dom = max(phases, key=lambda p: phases[p]["total_ms_per_step"])
         d = phases[dom]
-        # the committed counter summaries were taken with the default
-        # Newton-Schulz settings; other settings run other kernels
-        profiled = (args.ns_chain == "hilo" and args.ns_master == "bf16" and args.ns_form == "auto"
-                    and wl.ns_steps == workloads.WORKLOADS[args.workload].ns_steps)
         traffic = None
         for path in sorted(glob.glob(os.path.join(ROOT, "profiles", "*traffic*.txt"))):
             traffic = traffic or (profsum.lookup_traffic(path, dom, wl.name, alpha) if profiled else None)
@@ -430,6 +448,7 @@ def main(argv=None):
         "per_master_ms": per_master,
         "ns_mfma_frac": None if ns_frac is None else round(ns_frac, 4),
         "ns_mfma_counters": mfma_counters or None,
+        "ns_mfma_counters_per_alpha": mfma_per_alpha(wl.name, per_alpha, profiled) or None,
         "streaming_hbm_counters": hbm_counters or None,
         "step_ms_stats": {"mean": round(ms, 4), "median": round(statistics.median(per), 4),
                           "min": round(min(per), 4), "mean_last_20": round(statistics.mean(tail), 4),
