@@ -228,8 +228,8 @@ __global__ __launch_bounds__(kThreads) void apply_cols_strip(ApplyArgs a) {
     __shared__ __attribute__((aligned(16))) float ot[kStripRows][kOtPitch];
     const int b = blockIdx.z;
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    // blocks run along the strips of one row block, then the next row block
-    // (one grid dimension: a million rows make 65536 row blocks)
+    // one grid dimension: blocks run along the strips of one row block, then
+    // the next row block
     const int64_t nstrips = (a.cols + kStrip - 1) / kStrip;
     const int64_t s0 = ((int64_t)blockIdx.x % nstrips) * kStrip;
     const int64_t s1 = s0 + kStrip < a.cols ? s0 + kStrip : a.cols;
