@@ -4,6 +4,9 @@ Acceptance (per matrix):
   * selected indices K equal the oracle's exactly (ties to the lower index);
   * the l1 line norms equal the oracle's exactly rounded sums bitwise;
   * the momentum M equals the oracle's fp32 result bitwise;
+  * where a test asks for it (debug output dbg_compact), the compact bf16
+    matrix X equals the oracle's normalised lines rounded in the kernel's
+    precision, bitwise;
   * the Newton-Schulz output O (debug output, before the lr scale) is within
     relative Frobenius error 2e-2 of the oracle's fp64 result (bf16 and fp16
     MFMA);
