@@ -107,7 +107,8 @@ typedef enum dion2_select_rule {
 } dion2_select_rule;
 
 typedef enum dion2_ns_form {
-    DION2_NS_AUTO = 0,   /* GRAM when l >= 3 s (padded sides), else DIRECT     */
+    DION2_NS_AUTO = 0,   /* GRAM when l >= 3 s or s <= 128 (padded sides),
+                            else DIRECT                                        */
     DION2_NS_DIRECT = 1, /* iterate on X (s x l)                               */
     DION2_NS_GRAM = 2    /* iterate on s x s matrices, X read twice            */
 } dion2_ns_form;

@@ -100,8 +100,12 @@ int make_plan(int batch, int64_t rows, int64_t cols, float alpha, int axis, int 
     P.s_pad = P.z_is_L ? P.kpad : P.opad;
     P.l_pad = P.z_is_L ? P.opad : P.kpad;
     // The GRAM form trades 2 (s x l) GEMMs and the X traffic of every step
-    // for about four three-pass s x s products; it pays once X is wide.
-    P.gram = ns_form == DION2_NS_GRAM || (ns_form == DION2_NS_AUTO && P.l_pad >= 3 * P.s_pad);
+    // for about four three-pass s x s products; it pays once X is wide. With
+    // a single tile a side (s <= 128) both forms cost a few microseconds of
+    // launches, and GRAM, which keeps the iterate in hi / lo pairs, is the
+    // more accurate one.
+    P.gram = ns_form == DION2_NS_GRAM ||
+             (ns_form == DION2_NS_AUTO && (P.l_pad >= 3 * P.s_pad || P.s_pad <= kTile));
     // the fp32 master runs in the GRAM order (its caller rejects a forced DIRECT)
     P.master = master;
     if (master) P.gram = true;

@@ -128,7 +128,7 @@ def test_ex_options_validation(lib):
     assert ex(ns_master=2) == DION2_ERR_INVALID_ARG and "ns_master" in binding.dion2_last_error()
     assert ex(ns_master=1, ns_chain=binding.CHAIN_F16) == DION2_ERR_INVALID_ARG
     assert ex(ns_master=1, ns_form=binding.NS_DIRECT) == DION2_ERR_UNSUPPORTED
-    # the fp32 master runs in the GRAM order: more workspace than the AUTO plan's DIRECT form here
+    # the fp32 master also keeps X's lo half: more workspace than the AUTO plan
     need_auto = binding.dion2_workspace_size(1, 64, 64, 0.25)
     assert ex(ns_master=1, workspace=FAKE, workspace_bytes=need_auto) == DION2_ERR_WORKSPACE
     # the lo halves of X exist only with the fp32 master and a Newton-Schulz step

@@ -768,11 +768,12 @@ def test_random_selection_full_1b_group(hip_device):
 
 
 # Several shape groups in one grouped call: five in the GRAM form (four of
-# padded s = 128, one of 256: two shared chains) and one in the DIRECT form.
+# padded s = 128, one of 256: two shared chains) and one in the DIRECT form
+# (600 x 640: s = 150, padded 256, and l = 640 < 3 s).
 GROUPED = workloads.Workload(
     "grouped", "test", (workloads.Group("a", 256, 640, 2), workloads.Group("b", 640, 256, 3),
                         workloads.Group("c", 384, 384, 2), workloads.Group("d", 300, 200, 1),
-                        workloads.Group("e", 128, 160, 2), workloads.Group("f", 1024, 2048, 1)),
+                        workloads.Group("e", 600, 640, 2), workloads.Group("f", 1024, 2048, 1)),
     (0.25,))
 
 
