@@ -545,6 +545,54 @@ def test_near_2_31_elements_strip_kernel(hip_device):
     sampled_column_step(hip_device, 524160, 4097, 0.25, "near2p31")
 
 
+CONCURRENT = workloads.Workload(
+    "concurrent", "test", (workloads.Group("a", 256, 640, 3), workloads.Group("b", 640, 256, 2),
+                           workloads.Group("c", 384, 384, 2)), (0.25,))
+
+
+def test_concurrent_streams_and_threads(hip_device):
+    """Calls on three streams at once (one workspace per stream), and calls
+    from three host threads on one stream (serialised by the library), give
+    bitwise the results of the same calls made one after another; two steps
+    each, so a workspace reused across calls is covered too."""
+    import threading
+    stacks = [workloads.make_group(CONCURRENT, gi, hip_device) for gi in range(3)]
+    seq = [tuple(t.clone() for t in st) for st in stacks]
+    thr = [tuple(t.clone() for t in st) for st in stacks]
+    for W, M, G in seq:
+        for _ in range(2):
+            binding.dion2_step_ex(W, M, G, 0.25)
+    torch.cuda.synchronize()
+
+    streams = [torch.cuda.Stream(device=hip_device) for _ in stacks]   # default priority
+    for st, (W, M, G) in zip(streams, stacks):
+        for _ in range(2):
+            binding.dion2_step_ex(W, M, G, 0.25, stream=st)
+    torch.cuda.synchronize()
+
+    errors = []
+
+    def worker(W, M, G):
+        try:
+            for _ in range(2):
+                binding.dion2_step_ex(W, M, G, 0.25)
+        except Exception as e:   # reported below, in the test's thread
+            errors.append(e)
+
+    threads = [threading.Thread(target=worker, args=t) for t in thr]
+    for t in threads:
+        t.start()
+    for t in threads:
+        t.join()
+    torch.cuda.synchronize()
+    assert not errors, errors
+    for gi in range(3):
+        for got, name in ((stacks[gi], "streams"), (thr[gi], "threads")):
+            assert torch.equal(got[1], seq[gi][1]), f"group {gi}, {name}: momentum"
+            assert torch.equal(got[0].view(torch.int16), seq[gi][0].view(torch.int16)), \
+                f"group {gi}, {name}: weights"
+
+
 def test_decay_all_ablation(hip_device):
     wl = one_group_workload(128, 256, name="decayall")
     W, M, G = workloads.make_group(wl, 0, hip_device)
