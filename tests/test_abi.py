@@ -40,6 +40,34 @@ def test_every_declared_symbol_is_exported(lib):
         assert hasattr(lib, name), name
 
 
+def test_struct_layouts_match_the_header(tmp_path):
+    """The ctypes mirrors of dion2_options and dion2_group have the header's
+    field offsets and sizes (a C program built with gcc against
+    include/dion2.h prints them)."""
+    import shutil
+    import subprocess
+    cc = shutil.which("gcc") or shutil.which("cc")
+    if cc is None:
+        pytest.skip("no C compiler")
+    lines = []
+    for struct, mirror in (("dion2_options", Options), ("dion2_group", binding.Group)):
+        lines.append(f'printf("{struct} size %zu\\n", sizeof({struct}));')
+        for name, _ in mirror._fields_:
+            lines.append(f'printf("{struct} {name} %zu\\n", offsetof({struct}, {name}));')
+    src = tmp_path / "layout.c"
+    src.write_text('#include <stdio.h>\n#include <stddef.h>\n#include "dion2.h"\nint main(void) {\n'
+                   + "\n".join(lines) + "\nreturn 0;\n}\n")
+    exe = tmp_path / "layout"
+    subprocess.run([cc, "-std=c99", "-I", os.path.join(ROOT, "include"), str(src), "-o", str(exe)],
+                   check=True, capture_output=True, timeout=120)
+    out = subprocess.run([str(exe)], check=True, capture_output=True, text=True, timeout=60).stdout
+    c_side = {tuple(ln.split()[:2]): int(ln.split()[2]) for ln in out.splitlines()}
+    for struct, mirror in (("dion2_options", Options), ("dion2_group", binding.Group)):
+        assert c_side[(struct, "size")] == ctypes.sizeof(mirror), struct
+        for name, _ in mirror._fields_:
+            assert c_side[(struct, name)] == getattr(mirror, name).offset, (struct, name)
+
+
 def test_version_and_status_strings(lib):
     assert binding.dion2_version() == 1
     for st in (0, -1, -2, -3, -4):
