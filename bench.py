@@ -11,8 +11,17 @@ dion2_step_groups call for the whole stack instead. The default is the paper's t
 (Sec. 4.4): 100 steps, the mean of the final 20 reported (warmup 80,
 steps 20). Prints one JSON line:
   value        mean ms per step at --alpha (lower is better)
-  roofline     the dominant kernel phase against its roofline, measured with
-               HIP events on the library's stream in a second timed pass
+  roofline     K4, the Newton-Schulz GEMMs, against the bf16 MFMA peak: the
+               iteration's dense flop count T (4 s^2 l + 2 s^3) per matrix
+               over the stack, divided by the Newton-Schulz kernels' time per
+               step, measured with HIP events on the library's stream in a
+               second timed pass; beside it rocprofv3's MFMA counters and the
+               counted HBM bytes from the committed profiles
+  step_frac    the step's roofline floor (the larger of the MFMA time of those
+               flops and the HBM time of the step's algorithmic bytes) over
+               the measured step time
+  per_workload the other stacks (single matrix, column selection, 7B, MoE),
+               each at its fractions, timed and measured the same way
   cpu_baseline the CPU oracle timed on a bounded sample of the same stack
   per_alpha_ms the other fractions of the workload, timed the same way
   per_rule_ms  the l1 (Default) and Random selection rules at --alpha
@@ -27,6 +36,7 @@ import argparse
 import dataclasses
 import glob
 import json
+import math
 import os
 import statistics
 import sys
@@ -43,7 +53,6 @@ from paper_2512_16928_amd import binding, profsum, workloads  # noqa: E402
 METRIC = "Dion2 optimizer-step ms per layer stack at α=0.25/0.5/1; NS MFMA util %"
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E
 MFMA_BF16_PEAK_TFS = 2500.0    # MI355X dense bf16 MFMA
-RIDGE_FLOP_PER_BYTE = MFMA_BF16_PEAK_TFS * 1e12 / (HBM_PEAK_GBS * 1e9)
 NS_PHASES = ("ns_gram", "ns_poly", "ns_update")
 STREAMING_PHASES = ("momentum", "gather", "apply")
 
@@ -68,6 +77,44 @@ def mfma_per_alpha(workload, per_alpha, profiled):
 
 def log(msg):
     print(msg, file=sys.stderr, flush=True)
+
+
+def num_selected(alpha, d_sel):
+    """k = ceil(alpha * d_sel) with alpha as the fp32 value the library takes,
+    clamped to [1, d_sel] (the fraction of lines Algorithm 1 selects)."""
+    import numpy as np
+    return int(min(d_sel, max(1, math.ceil(float(np.float32(alpha)) * d_sel))))
+
+
+def floors(wl, alpha, ns_steps=None):
+    """The step's algorithmic work and its roofline floors on one MI355X.
+
+    Per matrix (rows x cols = fan-out x fan-in, N elements, k selected lines
+    of length d_oth, s = min(k, d_oth), l = max(k, d_oth), T steps):
+      Newton-Schulz flops   T (4 s^2 l + 2 s^3), the dense count of the
+                            iteration A = X X^T, B = b A + c A^2, X <- a X + B X
+      algorithmic bytes     N (4 + g + 4) + k d_oth (4 + 4 + 2 w): the momentum
+                            read and written with the gradient read (every
+                            element), then the selected lines of M read and
+                            written and those of W read and written (g, w the
+                            bytes per element of G and W)
+    The compact matrix and the Newton-Schulz intermediates are implementation
+    traffic, not counted here."""
+    T = wl.ns_steps if ns_steps is None else ns_steps
+    eb = 2.0 if wl.w_dtype == "bf16" else 4.0
+    flops = nbytes = 0.0
+    for g in wl.groups:
+        axis = (0 if g.rows <= g.cols else 1) if g.axis == workloads.AXIS_AUTO else g.axis
+        d_sel, d_oth = (g.rows, g.cols) if axis == 0 else (g.cols, g.rows)
+        k = num_selected(alpha, d_sel)
+        s_, l_ = min(k, d_oth), max(k, d_oth)
+        n_el = float(g.rows) * g.cols
+        flops += g.count * T * (4.0 * s_ * s_ * l_ + 2.0 * s_ ** 3)
+        nbytes += g.count * (n_el * (8.0 + eb) + float(k) * d_oth * (8.0 + 2.0 * eb))
+    ns_ms = flops / (MFMA_BF16_PEAK_TFS * 1e12) * 1e3
+    hbm_ms = nbytes / (HBM_PEAK_GBS * 1e9) * 1e3
+    return dict(ns_flops=flops, alg_bytes=nbytes, ns_ms_at_peak=ns_ms, hbm_ms_at_peak=hbm_ms,
+                floor_ms=max(ns_ms, hbm_ms), bound="mfma" if ns_ms >= hbm_ms else "hbm")
 
 
 def allocate(wl, dev, split=1):
@@ -176,11 +223,11 @@ def profile_phases(wl, groups, alpha, steps):
         avg_ms = d["ms"] / d["launches"]       # per kernel launch
         flops, nbytes = d["flops"] / d["launches"], d["bytes"] / d["launches"]
         sec = avg_ms * 1e-3
-        # the bound is the roofline's: MFMA where the phase's arithmetic
-        # intensity reaches the ridge point, HBM below it
+        # the Newton-Schulz GEMMs against the MFMA peak (their executed
+        # flops, hi/lo passes included), the streaming kernels against HBM
         if ph == "select":
             bound, ach, peak, unit = "latency", nbytes / sec / 1e9, HBM_PEAK_GBS, "GB/s"
-        elif flops > 0 and flops / nbytes >= RIDGE_FLOP_PER_BYTE:
+        elif ph in NS_PHASES:
             bound, ach, peak, unit = "mfma", flops / sec / 1e12, MFMA_BF16_PEAK_TFS, "TFLOP/s"
         else:
             bound, ach, peak, unit = "hbm", nbytes / sec / 1e9, HBM_PEAK_GBS, "GB/s"
@@ -192,17 +239,30 @@ def profile_phases(wl, groups, alpha, steps):
     return out
 
 
+def cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for ln in f:
+                if ln.startswith("model name"):
+                    return ln.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return None
+
+
 def cpu_baseline(wl, alpha, seconds):
     """The oracle on a bounded sample: one matrix of each shape group per
     pass, repeated until `seconds` of CPU time have run, then scaled by the
-    group counts to a whole-stack step."""
+    group counts to a whole-stack step. Also the single 256x256 matrix on
+    one thread (its BLAS limited to one thread)."""
     import numpy as np
 
     import oracle
     try:
-        from threadpoolctl import threadpool_info
+        from threadpoolctl import threadpool_info, threadpool_limits
         blas_threads = max((i.get("num_threads", 1) for i in threadpool_info()), default=1)
     except Exception:  # pragma: no cover - threadpoolctl is optional
+        threadpool_limits = None
         blas_threads = None
     dev = torch.device("cuda:0")
     per_group = [[] for _ in wl.groups]
@@ -222,12 +282,122 @@ def cpu_baseline(wl, alpha, seconds):
         passes += 1
     est_s = sum(statistics.mean(t) * grp.count for t, grp in zip(per_group, wl.groups))
     cores = len(os.sched_getaffinity(0))
-    return dict(value=est_s * 1e3, unit="ms", cores=blas_threads or cores, kind="oracle",
-                host_cores=cores,
+    # the single fp32 256x256 matrix (alpha 0.25, rows) on one thread, in full
+    single = workloads.WORKLOADS["single-256"]
+    W, M, G = workloads.make_group(single, 0, dev)
+    Wh, Mh, Gh = (W[0].double().cpu().numpy(), M[0].cpu().numpy(), G[0].cpu().numpy())
+    c1 = []
+    if threadpool_limits is not None:
+        with threadpool_limits(limits=1):
+            for _ in range(5):
+                t0 = time.perf_counter()
+                oracle.dion2_step(Wh, Mh, Gh, 0.25, single.mu, single.lr, single.ns_steps,
+                                  single.groups[0].axis, w_dtype=single.w_dtype)
+                c1.append(time.perf_counter() - t0)
+    return dict(value=est_s * 1e3, unit="ms", cores=blas_threads or 1, kind="oracle",
+                host_cores=cores, blas_threads=blas_threads, cpu_model=cpu_model(),
+                extrapolated=True,
+                single_256_one_thread_ms=round(statistics.median(c1) * 1e3, 3) if c1 else None,
                 sample=(f"{passes} pass(es) over one matrix of each of the {len(wl.groups)} "
                         f"shape groups ({sum(len(t) for t in per_group)} oracle steps, "
                         f"{sum(sum(t) for t in per_group):.1f} s), mean per group scaled by "
-                        f"the group counts to the {wl.matrices()}-matrix stack"))
+                        f"the group counts to the {wl.matrices()}-matrix stack; 'cores' is the "
+                        f"BLAS thread count the oracle's matrix products ran on (its l1 sums "
+                        f"are single-threaded); the single 256x256 fp32 matrix also ran in "
+                        f"full on one thread (median of 5)"))
+
+
+def ns_roofline(wl, alpha, phases, profiled):
+    """K4 against the bf16 MFMA peak: the stack's dense Newton-Schulz flops
+    per step over the Newton-Schulz kernels' event-timed time per step, with
+    the committed counter figures for the same kernels beside it."""
+    fl = floors(wl, alpha)
+    ns_ms = sum(phases[p]["total_ms_per_step"] for p in NS_PHASES if p in phases)
+    if ns_ms <= 0:
+        return None
+    ach = fl["ns_flops"] / (ns_ms * 1e-3) / 1e12
+    executed = sum(phases[p]["flops_per_launch"] * phases[p]["launches_per_step"]
+                   for p in NS_PHASES if p in phases)
+    counters, traffic = {}, None
+    if profiled:
+        for p in NS_PHASES:
+            for path in sorted(glob.glob(os.path.join(ROOT, "profiles", "*mfma*.txt"))):
+                hit = profsum.lookup_mfma(path, p, wl.name, alpha)
+                if hit and p not in counters:
+                    counters[p] = hit
+        tot = 0.0
+        for p in NS_PHASES:
+            if p not in phases:
+                continue
+            hit = None
+            for path in sorted(glob.glob(os.path.join(ROOT, "profiles", "*traffic*.txt"))):
+                hit = hit or profsum.lookup_traffic(path, p, wl.name, alpha)
+            if hit is None:
+                tot = None
+                break
+            tot += hit * phases[p]["launches_per_step"]
+        traffic = None if tot is None else round(tot)
+    util = None
+    if counters and all(p in counters for p in NS_PHASES if p in phases):
+        # duration-weighted over the Newton-Schulz phases
+        w = {p: phases[p]["total_ms_per_step"] for p in NS_PHASES if p in phases}
+        util = round(sum(counters[p]["mfma_util_pct"] * w[p] for p in w) / sum(w.values()), 2)
+    return dict(bound="mfma", achieved=round(ach, 2), peak=MFMA_BF16_PEAK_TFS, unit="TFLOP/s",
+                frac=round(ach / MFMA_BF16_PEAK_TFS, 4), traffic=traffic,
+                traffic_unit="HBM bytes per step of the Newton-Schulz kernels (rocprofv3 "
+                             "FETCH_SIZE + WRITE_SIZE, calibrated)",
+                kernel="K4 Newton-Schulz GEMMs (ns_gram + ns_poly + ns_update)",
+                unit_of_work="one step's Newton-Schulz over the whole stack",
+                algorithmic_flops_per_step=fl["ns_flops"],
+                ns_ms_per_step=round(ns_ms, 4),
+                launches_per_step=round(sum(phases[p]["launches_per_step"] for p in NS_PHASES
+                                            if p in phases), 2),
+                executed_flops_per_step=executed,
+                executed_tflops=round(executed / (ns_ms * 1e-3) / 1e12, 2),
+                mfma_util_pct=util, mfma_counters=counters or None)
+
+
+def measure_workload(name, alphas, warmup, steps, prof_steps, dev):
+    """One other stack: allocated, timed at each fraction (one stream per
+    shape group, as the headline), its Newton-Schulz phases event-timed in a
+    second pass, then released."""
+    wl = workloads.WORKLOADS[name]
+    t0 = time.perf_counter()
+    groups = allocate(wl, dev)
+    log(f"[bench] workload {name}: {wl.matrices()} matrices, {wl.elements() / 1e6:.1f}M elements "
+        f"(allocated in {time.perf_counter() - t0:.1f} s)")
+    saved = STREAMS[:]
+    STREAMS.clear()
+    STREAMS.extend(torch.cuda.Stream() for _ in wl.groups)
+    out = {}
+    try:
+        for a in alphas:
+            w_, s_ = (warmup, steps) if not isinstance(warmup, dict) else (warmup[a], steps[a])
+            per, _ = time_steps(wl, groups, a, w_, s_)
+            ms = statistics.mean(per)
+            phases = profile_phases(wl, groups, a, prof_steps if not isinstance(prof_steps, dict)
+                                    else prof_steps[a])
+            fl = floors(wl, a)
+            roof = ns_roofline(wl, a, phases, True)
+            out[str(a)] = dict(ms_per_step=round(ms, 4), steps=s_, warmup=w_,
+                               floor_ms=round(fl["floor_ms"], 4), floor_bound=fl["bound"],
+                               step_frac=round(fl["floor_ms"] / ms, 4),
+                               ns_frac=None if roof is None else roof["frac"],
+                               ns_ms_per_step=None if roof is None else roof["ns_ms_per_step"],
+                               streaming_ms_per_step=round(sum(
+                                   phases[p]["total_ms_per_step"] for p in
+                                   ("momentum", "select", "gather", "apply") if p in phases), 4))
+            log(f"[bench]   {name} alpha={a}: {ms:.3f} ms/step, floor {fl['floor_ms']:.3f} ms "
+                f"({fl['bound']}), NS {out[str(a)]['ns_frac']} of MFMA peak")
+    finally:
+        STREAMS.clear()
+        STREAMS.extend(saved)
+        del groups
+        torch.cuda.synchronize()
+        binding.dion2_release_workspaces()
+        torch.cuda.empty_cache()
+    return {"description": wl.description, "matrices": wl.matrices(), "elements": wl.elements(),
+            "per_alpha": out}
 
 
 def main(argv=None):
@@ -270,6 +440,10 @@ def main(argv=None):
                     help="skip timing the other GRAM chain storage (--ns-chain) at each fraction")
     ap.add_argument("--no-random-rule", action="store_true",
                     help="skip timing the Random selection rule at --alpha")
+    ap.add_argument("--no-workloads", action="store_true",
+                    help="skip the other stacks (single matrix, column selection, MoE, 7B)")
+    ap.add_argument("--workload-steps", type=int, default=10,
+                    help="timed steps per fraction of each other stack (3 for 7B at alpha 1)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run plain 1 GiB device copies, the reference dispatches that "
                          "scale HBM byte counters (FETCH_SIZE / WRITE_SIZE) in a profiler run")
@@ -331,35 +505,15 @@ def main(argv=None):
     phases = {}
     roofline = None
     ns_frac = None
-    mfma_counters = {}
     hbm_counters = {}
     if not args.no_profile:
         phases = profile_phases(wl, groups, alpha, args.steps)
-        dom = max(phases, key=lambda p: phases[p]["total_ms_per_step"])
-        d = phases[dom]
-        traffic = None
-        for path in sorted(glob.glob(os.path.join(ROOT, "profiles", "*traffic*.txt"))):
-            traffic = traffic or (profsum.lookup_traffic(path, dom, wl.name, alpha) if profiled else None)
         for p in STREAMING_PHASES:
             for path in sorted(glob.glob(os.path.join(ROOT, "profiles", "*traffic*.txt"))):
                 hit = profsum.lookup_hbm_rate(path, p, wl.name, alpha) if profiled else None
                 if hit and p not in hbm_counters:
                     hbm_counters[p] = hit
-        for p in NS_PHASES:
-            for path in sorted(glob.glob(os.path.join(ROOT, "profiles", "*mfma*.txt"))):
-                hit = profsum.lookup_mfma(path, p, wl.name, alpha) if profiled else None
-                if hit and p not in mfma_counters:
-                    mfma_counters[p] = hit
-        roofline = dict(bound=d["bound"], achieved=round(d["achieved"], 3), peak=d["peak"],
-                        unit=d["unit"], frac=round(d["frac"], 4),
-                        traffic=None if traffic is None else round(traffic),
-                        traffic_unit="bytes per launch", kernel=dom,
-                        avg_launch_ms=round(d["avg_launch_ms"], 5),
-                        algorithmic_per_launch=round(d["bytes_per_launch"] if d["unit"] == "GB/s"
-                                                     else d["flops_per_launch"]),
-                        algorithmic_unit="bytes" if d["unit"] == "GB/s" else "flops",
-                        flops_per_launch=round(d["flops_per_launch"]),
-                        bytes_per_launch=round(d["bytes_per_launch"]))
+        roofline = ns_roofline(wl, alpha, phases, profiled)
         ns_ms = sum(phases[p]["total_ms_per_step"] for p in NS_PHASES if p in phases)
         ns_work = sum(phases[p]["flops_per_launch"] * phases[p]["launches_per_step"]
                       for p in NS_PHASES if p in phases)
@@ -369,6 +523,12 @@ def main(argv=None):
             log(f"[bench]   {p:10s} {d['total_ms_per_step']:8.3f} ms/step  {d['bound']:7s} "
                 f"{d['achieved']:9.1f} {d['unit']} ({100 * d['frac']:.1f}% of peak)"
                 f"   [{d['hbm_gbs']:7.0f} GB/s, {d['mfma_tflops']:6.1f} TFLOP/s]")
+        if roofline:
+            log(f"[bench] K4 roofline: {roofline['achieved']:.1f} TFLOP/s of dense Newton-Schulz "
+                f"work = {100 * roofline['frac']:.1f}% of the bf16 MFMA peak "
+                f"({roofline['ns_ms_per_step']:.3f} ms/step)")
+    fl = floors(wl, alpha)
+    step_frac = fl["floor_ms"] / ms
 
     per_alpha = {str(alpha): round(ms, 4)}
     if not args.no_extra_alphas:
@@ -413,6 +573,30 @@ def main(argv=None):
         per_rule["random"] = round(statistics.mean(p3), 4)
         log(f"[bench] alpha={alpha}, Random rule: {per_rule['random']:.3f} ms/step")
 
+    per_workload = {}
+    if not args.no_workloads and args.workload == "1b" and not GROUPED[0] and args.split == 1 \
+            and NS_FORM == binding.NS_AUTO and NS_CHAIN == binding.CHAIN_HILO \
+            and NS_MASTER == binding.MASTER_BF16 and wl.ns_steps == 5:
+        # The other stacks of the measurement plan, one at a time (each
+        # allocated, timed and released), with fewer steps: the 7B stack at
+        # alpha = 1 takes about a second per step.
+        n = args.workload_steps
+        del groups
+        torch.cuda.synchronize()
+        binding.dion2_release_workspaces()
+        torch.cuda.empty_cache()
+        plan = [("single-256", (0.25,)), ("1b-colsel", (0.25,)), ("moe", (0.25,)),
+                ("7b", (0.125, 0.25, 1.0))]
+        for name, alist in plan:
+            if name == "7b":
+                warm = {0.125: 3, 0.25: 3, 1.0: 1}
+                stp = {0.125: n, 0.25: n, 1.0: 3}
+                prof = {0.125: 2, 0.25: 2, 1.0: 1}
+            else:
+                warm, stp, prof = 3, n, 2
+            per_workload[name] = measure_workload(name, alist, warm, stp, prof, dev)
+        groups = None
+
     cpu = None
     if not args.no_cpu_baseline:
         log(f"[bench] timing the CPU oracle for ~{args.cpu_seconds:.0f} s")
@@ -441,13 +625,19 @@ def main(argv=None):
                    "calls": args.calls, "group_streams": args.group_streams,
                    "streams": args.streams, "split": args.split},
         "roofline": roofline,
+        "step_frac": round(step_frac, 4),
+        "floors": {"floor_ms": round(fl["floor_ms"], 4), "bound": fl["bound"],
+                   "ns_ms_at_mfma_peak": round(fl["ns_ms_at_peak"], 4),
+                   "hbm_ms_at_peak": round(fl["hbm_ms_at_peak"], 4),
+                   "ns_flops": fl["ns_flops"], "alg_bytes": fl["alg_bytes"],
+                   "per_alpha_step_frac": {a: round(floors(wl, float(a))["floor_ms"] / v, 4)
+                                           for a, v in per_alpha.items()}},
         "cpu_baseline": cpu,
         "per_alpha_ms": per_alpha,
         "per_rule_ms": per_rule,
         "per_chain_ms": per_chain,
         "per_master_ms": per_master,
-        "ns_mfma_frac": None if ns_frac is None else round(ns_frac, 4),
-        "ns_mfma_counters": mfma_counters or None,
+        "ns_mfma_frac_executed": None if ns_frac is None else round(ns_frac, 4),
         "ns_mfma_counters_per_alpha": mfma_per_alpha(wl.name, per_alpha, profiled) or None,
         "streaming_hbm_counters": hbm_counters or None,
         "step_ms_stats": {"mean": round(ms, 4), "median": round(statistics.median(per), 4),
@@ -455,6 +645,7 @@ def main(argv=None):
                           "wall_s": round(wall, 3)},
         "phases": {p: {k: (round(v, 5) if isinstance(v, float) else v) for k, v in d.items()}
                    for p, d in phases.items()},
+        "per_workload": per_workload or None,
     }
     print(json.dumps(line), flush=True)
     return 0

@@ -17,10 +17,15 @@
  * Numerical contract:
  *   - M is fp32; the accumulate and the decay are single IEEE fp32 RNE
  *     operations (bitwise reproducible).
- *   - The l1 norm of each line is the exact sum of |M_ij| rounded once to
- *     fp64 (double-double accumulation), so selection does not depend on a
- *     summation order. Ties go to the lower index; NaN ranks as +inf.
- *     K is ascending. (dion2_options.select_rule selects the Random rule.)
+ *   - The l1 norm of each line is accumulated in double-double from the fp32
+ *     values of M and rounded once to fp64, in an order fixed by the shape,
+ *     so selection does not depend on scheduling. It equals the exact sum of
+ *     |M_ij| rounded once to fp64, except when that exact sum S lies within
+ *     about n^2 2^-106 S (n the line's length) of a point halfway between
+ *     two adjacent fp64 values: there the low word's own rounding can move
+ *     the result by one unit. Ties go to the lower index; NaN ranks as
+ *     +inf. K is ascending. (dion2_options.select_rule selects the Random
+ *     rule.)
  *   - Newton-Schulz: X = M[K,:] / (||M[K,:]||_F + eps), then per step
  *     A = X X^T, B = b A + c A^2, X <- a X + B X on the orientation with the
  *     smaller Gram matrix (s x s, X is s x l, s <= l); X is rounded once to
@@ -107,11 +112,21 @@ typedef enum dion2_select_rule {
 } dion2_select_rule;
 
 typedef enum dion2_ns_form {
-    DION2_NS_AUTO = 0,   /* GRAM when l >= 3 s or s <= 128 (padded sides),
-                            else DIRECT                                        */
-    DION2_NS_DIRECT = 1, /* iterate on X (s x l)                               */
+    DION2_NS_AUTO = 0,   /* GRAM when l >= 3 s or s <= 128 (padded sides) or
+                            ns_steps > DION2_DIRECT_MAX_STEPS, else DIRECT     */
+    DION2_NS_DIRECT = 1, /* iterate on X (s x l). X is rounded to bf16 after
+                            every step, so the error grows with the step
+                            count: at most DION2_DIRECT_MAX_STEPS steps, more
+                            return DION2_ERR_UNSUPPORTED                      */
     DION2_NS_GRAM = 2    /* iterate on s x s matrices, X read twice            */
 } dion2_ns_form;
+
+/* The most Newton-Schulz steps the DIRECT form runs. An emulation of its
+   bf16 arithmetic on near-square compact matrices puts the relative
+   Frobenius error of O at about 1.6e-2 after 6 steps and 2.1e-2 after 8,
+   against 1.2e-2 after the default 5; the GRAM form stays at its 5-step
+   error. */
+#define DION2_DIRECT_MAX_STEPS 6
 
 typedef enum dion2_ns_chain {
     DION2_CHAIN_HILO = 0, /* GRAM s x s matrices as bf16 hi/lo pairs (default)  */
@@ -206,16 +221,33 @@ int dion2_step_strided(void* W, float* M, const void* G, int batch,
                        float lr, int ns_steps, int axis, void* stream);
 
 /* A batch of same-shape matrices given by HOST arrays of DEVICE pointers
-   (W[i], G[i] bf16, M[i] fp32, each [rows][cols]). The pointer tables are
-   copied to the device before the call returns; the caller may reuse them. */
+   (W[i], G[i] bf16, M[i] fp32, each [rows][cols]): the step of Algorithm 1
+   for every matrix, each with its own selection and Newton-Schulz, as in
+   dion2_step_strided. The tables are read into pinned staging before the
+   call returns, so the caller may reuse them at once; the copy to the device
+   is queued on `stream`. The host does not wait for the device, except when
+   more than 8 calls with pointer tables are still queued on one stream (it
+   then waits for the oldest one's table copy). The batch must not exceed 64
+   matrices when the tables cannot be staged (no library workspace). */
 int dion2_step_batched(void* const* W, float* const* M, const void* const* G,
                        int batch, int64_t rows, int64_t cols, float alpha,
                        float mu, float lr, int ns_steps, int axis,
                        void* stream);
 
-/* Strided stacks with full control (dtypes, coefficients, eps, ablation,
-   Newton-Schulz form and precision, selection rule, caller workspace, debug
-   outputs). opt == NULL means defaults. */
+/* Strided stacks with full control; opt == NULL means defaults. Per matrix
+   this is Algorithm 1 with the choices the options expose:
+     - selection by the Default (l1) rule or the Random rule (Algorithm 1,
+       selection step; Sec. 3.1), select_rule;
+     - the selective decay of eq. (2) (Algorithm 1, decay step), or the
+       decay of all of M, the ablation of Sec. 4.2 (decay_all);
+     - the Newton-Schulz iteration of Algorithm 1's orthonormalisation step
+       (Sec. 1) with a per-step coefficient table, eps, evaluation order and
+       precision (ns_coeffs, ns_eps, ns_form, ns_chain, ns_master);
+     - the storage types of W and G, a caller workspace and debug outputs.
+   Errors as for every entry point; in addition DION2_ERR_UNSUPPORTED for
+   ns_form DIRECT with more than DION2_DIRECT_MAX_STEPS steps, and
+   DION2_ERR_WORKSPACE for a caller workspace smaller than
+   dion2_workspace_size_ex gives for the same arguments. */
 int dion2_step_ex(void* W, float* M, const void* G, int batch, int64_t rows,
                   int64_t cols, float alpha, float mu, float lr, int ns_steps,
                   int axis, const dion2_options* opt, void* stream);
@@ -235,7 +267,8 @@ typedef struct dion2_group {
 
 /* The step of Algorithm 1 for several same-shape groups in one call on one
    stream, with shared hyper-parameters and options (a model's whole layer
-   stack, say). The result is bitwise that of dion2_step_ex called for each
+   stack, say; every matrix is stepped independently, as Algorithm 1 is per
+   matrix, with the options' meaning as in dion2_step_ex). The result is bitwise that of dion2_step_ex called for each
    group in order; for the RANDOM rule group g's matrix indices start at
    rand_matrix0 plus the batches of groups 0 .. g-1. Groups whose
    Newton-Schulz runs in the GRAM form with the same padded s x s size share
@@ -257,13 +290,20 @@ int dion2_step_groups(const dion2_group* groups, int ngroups, float alpha,
                       float mu, float lr, int ns_steps,
                       const dion2_options* opt, void* stream);
 
-/* Bytes of device workspace one call with these arguments needs (for
-   dion2_options.workspace) with ns_form = DION2_NS_AUTO and ns_master =
-   DION2_MASTER_BF16; a forced form or the fp32 master may need more
-   (dion2_step_ex then fails with DION2_ERR_WORKSPACE). Returns 0
-   for invalid arguments. */
+/* Bytes of device workspace (for dion2_options.workspace) that suffice for
+   a call with these arguments under any options and step count: the
+   largest plan, the GRAM order with DION2_MASTER_FP32. Returns 0 for
+   invalid arguments. */
 size_t dion2_workspace_size(int batch, int64_t rows, int64_t cols,
                             float alpha, int axis);
+
+/* Bytes of device workspace a dion2_step_ex call with exactly these
+   arguments and options needs (opt == NULL: defaults; the options'
+   workspace and debug pointers are ignored). Returns 0 where dion2_step_ex
+   would reject the arguments or options. */
+size_t dion2_workspace_size_ex(int batch, int64_t rows, int64_t cols,
+                               float alpha, int axis, int ns_steps,
+                               const dion2_options* opt);
 
 /* Number of selected lines k = ceil(alpha * d_sel) clamped to [1, d_sel]
    and the resolved axis (DION2_AXIS_ROWS / _COLS), for sizing debug

@@ -125,12 +125,6 @@ def l1_norms(M, axis):
     return np.array([math.fsum(line.tolist()) for line in lines], dtype=np.float64)
 
 
-def sum_squares(M, axis):
-    """Squared l2 norm of every line along the selection axis, fp64."""
-    A = np.asarray(M, dtype=np.float64)
-    return np.sum(A * A, axis=1 if axis == AXIS_ROWS else 0)
-
-
 def select_top(norms, k):
     """Select_alpha, Default rule: indices of the k largest norms, ties to the
     lower index, NaN ranked as +inf; returned in ascending index order."""

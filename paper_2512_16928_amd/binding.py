@@ -38,7 +38,8 @@ MAX_NS_STEPS = 16
 
 # Every function include/dion2.h declares (checked by the ABI tests).
 EXPORTED = ("dion2_options_init", "dion2_step", "dion2_step_strided", "dion2_step_batched",
-            "dion2_step_ex", "dion2_step_groups", "dion2_workspace_size", "dion2_plan_info",
+            "dion2_step_ex", "dion2_step_groups", "dion2_workspace_size",
+            "dion2_workspace_size_ex", "dion2_plan_info",
             "dion2_release_workspaces", "dion2_status_string", "dion2_last_error",
             "dion2_version", "dion2_profile_enable", "dion2_profile_read", "dion2_profile_reset")
 
@@ -121,6 +122,8 @@ def load(path: str = LIB_PATH):
     lib.dion2_step_groups.restype = c_int
     lib.dion2_workspace_size.argtypes = [c_int, i64, i64, c_float, c_int]
     lib.dion2_workspace_size.restype = c_size_t
+    lib.dion2_workspace_size_ex.argtypes = [c_int, i64, i64, c_float, c_int, c_int, POINTER(Options)]
+    lib.dion2_workspace_size_ex.restype = c_size_t
     lib.dion2_plan_info.argtypes = [i64, i64, c_float, c_int, POINTER(c_int64), POINTER(c_int)]
     lib.dion2_plan_info.restype = c_int
     lib.dion2_release_workspaces.argtypes = []
@@ -332,7 +335,33 @@ def dion2_step_groups_raw(group_array, ngroups, alpha, mu, lr, ns_steps, opt, st
 
 
 def dion2_workspace_size(batch, rows, cols, alpha, axis=AXIS_AUTO) -> int:
+    """Workspace bytes that suffice for these arguments under any options."""
     return int(load().dion2_workspace_size(batch, rows, cols, alpha, axis))
+
+
+def dion2_workspace_size_ex(batch, rows, cols, alpha, axis=AXIS_AUTO, ns_steps=5, *,
+                            w_dtype=torch.bfloat16, g_dtype=torch.bfloat16, ns_form=NS_AUTO,
+                            ns_chain=CHAIN_HILO, ns_master=MASTER_BF16, select_rule=SELECT_L1,
+                            ns_coeffs=None) -> int:
+    """Workspace bytes a dion2_step_ex call with exactly these options needs
+    (0 where the call would be rejected)."""
+    lib = load()
+    opt = Options()
+    lib.dion2_options_init(ctypes.byref(opt))
+    opt.w_dtype = _DT[w_dtype]
+    opt.g_dtype = _DT[g_dtype]
+    keep = None
+    if ns_coeffs is not None:
+        flat = [float(v) for abc in ns_coeffs for v in abc]
+        keep = (c_float * len(flat))(*flat)
+        opt.ns_coeffs = ctypes.cast(keep, POINTER(c_float))
+    opt.ns_form = ns_form
+    opt.ns_chain = ns_chain
+    opt.ns_master = ns_master
+    opt.select_rule = select_rule
+    n = int(lib.dion2_workspace_size_ex(batch, rows, cols, alpha, axis, ns_steps, ctypes.byref(opt)))
+    del keep
+    return n
 
 
 def dion2_plan_info(rows, cols, alpha, axis=AXIS_AUTO):

@@ -69,10 +69,19 @@ struct Plan {
 enum { SQ_AHI, SQ_ALO, SQ_B, SQ_DIRECT_COUNT = 3 };
 enum { SQ_QHI = 2, SQ_QLO, SQ_THI, SQ_TLO, SQ_P0HI, SQ_P0LO, SQ_P1HI, SQ_P1LO, SQ_GRAM_COUNT };
 
+// The DIRECT form rounds X to bf16 after every step, so its distance from
+// the exact iteration grows with the step count. An emulation of its bf16
+// arithmetic on the compact shapes it is chosen for (near-square, from
+// 80 x 640 to 1024 x 2048) put the relative Frobenius error of O at up to
+// 1.2e-2 after 5 steps, 1.6e-2 after 6, 1.8e-2 after 7 and 2.1e-2 after 8.
+// Beyond DION2_DIRECT_MAX_STEPS AUTO takes the GRAM form, which carries the
+// iteration in hi / lo pairs, and a forced DIRECT is refused.
+constexpr int kDirectMaxSteps = DION2_DIRECT_MAX_STEPS;
+
 // own_sq = false leaves out the s x s buffers (a grouped call carves them
 // once for every group of a shared Newton-Schulz chain).
-int make_plan(int batch, int64_t rows, int64_t cols, float alpha, int axis, int ns_form, Plan* p,
-              bool own_sq = true, bool master = false) {
+int make_plan(int batch, int64_t rows, int64_t cols, float alpha, int axis, int ns_form, int ns_steps,
+              Plan* p, bool own_sq = true, bool master = false) {
     if (batch < 1 || batch > 65535) return fail(DION2_ERR_INVALID_ARG, "batch %d not in [1, 65535]", batch);
     if (rows < 1 || cols < 1)
         return fail(DION2_ERR_INVALID_ARG, "rows (%lld) and cols (%lld) must be >= 1",
@@ -86,6 +95,11 @@ int make_plan(int batch, int64_t rows, int64_t cols, float alpha, int axis, int 
         return fail(DION2_ERR_INVALID_ARG, "axis %d is not AUTO, ROWS or COLS", axis);
     if (ns_form != DION2_NS_AUTO && ns_form != DION2_NS_DIRECT && ns_form != DION2_NS_GRAM)
         return fail(DION2_ERR_INVALID_ARG, "ns_form %d is not AUTO, DIRECT or GRAM", ns_form);
+    if (ns_form == DION2_NS_DIRECT && ns_steps > kDirectMaxSteps)
+        return fail(DION2_ERR_UNSUPPORTED,
+                    "ns_form DIRECT takes at most %d Newton-Schulz steps (%d given): its bf16 "
+                    "rounding of X after every step grows past the 2e-2 accuracy bound",
+                    kDirectMaxSteps, ns_steps);
     Plan& P = *p;
     P.axis = axis == DION2_AXIS_AUTO ? (rows <= cols ? 0 : 1) : axis;
     P.rows = rows;
@@ -105,7 +119,8 @@ int make_plan(int batch, int64_t rows, int64_t cols, float alpha, int axis, int 
     // launches, and GRAM, which keeps the iterate in hi / lo pairs, is the
     // more accurate one.
     P.gram = ns_form == DION2_NS_GRAM ||
-             (ns_form == DION2_NS_AUTO && (P.l_pad >= 3 * P.s_pad || P.s_pad <= kTile));
+             (ns_form == DION2_NS_AUTO &&
+              (P.l_pad >= 3 * P.s_pad || P.s_pad <= kTile || ns_steps > kDirectMaxSteps));
     // the fp32 master runs in the GRAM order (its caller rejects a forced DIRECT)
     P.master = master;
     if (master) P.gram = true;
@@ -139,13 +154,22 @@ int make_plan(int batch, int64_t rows, int64_t cols, float alpha, int axis, int 
 
 // ------------------------------------------------------------- workspaces
 
+// Pinned host staging for one call's pointer tables. The copy to the device
+// reads it after the call has returned, so a slot is reused only once the
+// event recorded behind that copy has completed.
+struct TableSlot {
+    void** host = nullptr;
+    size_t count = 0;
+    hipEvent_t done = nullptr;
+    bool pending = false;
+};
+constexpr int kTableSlots = 8;
+
 struct Workspace {
     void* dev = nullptr;
     size_t bytes = 0;
-    void** pinned = nullptr;       // staging for pointer tables
-    size_t pinned_count = 0;
-    hipEvent_t tables_done = nullptr;
-    bool tables_pending = false;
+    TableSlot slots[kTableSlots];  // pointer-table staging, used round-robin
+    int next_slot = 0;
     std::vector<hipStream_t> aux;  // grouped calls: streams the groups run on
     std::vector<hipEvent_t> ev;    // grouped calls: fork / dependency / join events
     std::mutex use;                // serialises host threads sharing a stream
@@ -900,25 +924,42 @@ int run_step(const Plan& P, void* W, float* M, const void* G, const Tables* tabs
         void** dst = reinterpret_cast<void**>(ws + P.o_tables);
         const size_t n = 3 * (size_t)P.batch;
         void** staging = nullptr;
+        TableSlot* slot = nullptr;
         if (w) {
-            if (w->tables_pending) {
-                e = hipEventSynchronize(w->tables_done);
+            // The first slot whose earlier copy has completed (checked with
+            // hipEventQuery, which does not block). Only with all slots'
+            // copies still queued -- more than kTableSlots table calls in
+            // flight on this stream -- does the host wait, for the oldest.
+            for (int i = 0; i < kTableSlots && !slot; ++i) {
+                TableSlot& c = w->slots[(w->next_slot + i) % kTableSlots];
+                if (c.pending) {
+                    e = hipEventQuery(c.done);
+                    if (e == hipErrorNotReady) continue;
+                    if (e != hipSuccess) return hip_fail(e, "hipEventQuery(tables)");
+                    c.pending = false;
+                }
+                slot = &c;
+            }
+            if (!slot) {
+                slot = &w->slots[w->next_slot];
+                e = hipEventSynchronize(slot->done);
                 if (e != hipSuccess) return hip_fail(e, "hipEventSynchronize(tables)");
-                w->tables_pending = false;
+                slot->pending = false;
             }
-            if (w->pinned_count < n) {
-                if (w->pinned) (void)hipHostFree(w->pinned);   // a failed free only leaks
-                w->pinned = nullptr;
-                w->pinned_count = 0;
-                e = hipHostMalloc(reinterpret_cast<void**>(&w->pinned), n * sizeof(void*));
+            w->next_slot = (int)(slot - w->slots + 1) % kTableSlots;
+            if (slot->count < n) {
+                if (slot->host) (void)hipHostFree(slot->host);   // a failed free only leaks
+                slot->host = nullptr;
+                slot->count = 0;
+                e = hipHostMalloc(reinterpret_cast<void**>(&slot->host), n * sizeof(void*));
                 if (e != hipSuccess) return hip_fail(e, "hipHostMalloc(pointer tables)");
-                w->pinned_count = n;
+                slot->count = n;
             }
-            if (!w->tables_done) {
-                e = hipEventCreateWithFlags(&w->tables_done, hipEventDisableTiming);
+            if (!slot->done) {
+                e = hipEventCreateWithFlags(&slot->done, hipEventDisableTiming);
                 if (e != hipSuccess) return hip_fail(e, "hipEventCreate");
             }
-            staging = w->pinned;
+            staging = slot->host;
         }
         void* tmp_local[3 * 64];
         if (!staging) staging = n <= 3 * 64 ? tmp_local : nullptr;
@@ -933,10 +974,10 @@ int run_step(const Plan& P, void* W, float* M, const void* G, const Tables* tabs
         }
         e = hipMemcpyAsync(dst, staging, n * sizeof(void*), hipMemcpyHostToDevice, stream);
         if (e != hipSuccess) return hip_fail(e, "hipMemcpyAsync(pointer tables)");
-        if (w) {
-            e = hipEventRecord(w->tables_done, stream);
+        if (slot) {
+            e = hipEventRecord(slot->done, stream);
             if (e != hipSuccess) return hip_fail(e, "hipEventRecord(tables)");
-            w->tables_pending = true;
+            slot->pending = true;
         } else {
             e = hipStreamSynchronize(stream);   // tmp_local goes out of scope
             if (e != hipSuccess) return hip_fail(e, "hipStreamSynchronize(tables)");
@@ -1001,11 +1042,11 @@ int step_impl(void* W, float* M, const void* G, const Tables* tabs, int batch, i
     dion2_options opt;
     if (opt_in) opt = *opt_in;
     else dion2_options_init(&opt);
-    Plan P;
-    int st = make_plan(batch, rows, cols, alpha, axis, opt.ns_form, &P, true,
-                       opt.ns_master == DION2_MASTER_FP32);
+    int st = validate_common(mu, lr, ns_steps, opt);
     if (st != DION2_OK) return st;
-    st = validate_common(mu, lr, ns_steps, opt);
+    Plan P;
+    st = make_plan(batch, rows, cols, alpha, axis, opt.ns_form, ns_steps, &P, true,
+                   opt.ns_master == DION2_MASTER_FP32);
     if (st != DION2_OK) return st;
     ChainFmt fmt;
     st = chain_format(opt, ns_steps, &fmt);
@@ -1091,7 +1132,7 @@ int groups_impl(const dion2_group* groups, int ngroups, float alpha, float mu, f
         const dion2_group& G = groups[g];
         Plan P;
         const bool master = opt.ns_master == DION2_MASTER_FP32;
-        st = make_plan(G.batch, G.rows, G.cols, alpha, G.axis, opt.ns_form, &P, true, master);
+        st = make_plan(G.batch, G.rows, G.cols, alpha, G.axis, opt.ns_form, ns_steps, &P, true, master);
         if (st != DION2_OK) return fail(st, "group %d: %s", g, g_last_error.c_str());
         if (!G.W || !G.M || !G.G) return fail(DION2_ERR_INVALID_ARG, "group %d: W, M and G must not be NULL", g);
         if (!aligned16(G.W) || !aligned16(G.M) || !aligned16(G.G))
@@ -1110,7 +1151,7 @@ int groups_impl(const dion2_group* groups, int ngroups, float alpha, float mu, f
             chain_of[g] = c;
             chain_pos[g] = chains[c].batch;
             chains[c].batch += P.batch;
-            make_plan(G.batch, G.rows, G.cols, alpha, G.axis, opt.ns_form, &P, false, master);
+            make_plan(G.batch, G.rows, G.cols, alpha, G.axis, opt.ns_form, ns_steps, &P, false, master);
         }
         plans[g] = P;
         total_batch += G.batch;
@@ -1345,15 +1386,31 @@ int dion2_step_groups(const dion2_group* groups, int ngroups, float alpha, float
 }
 
 size_t dion2_workspace_size(int batch, int64_t rows, int64_t cols, float alpha, int axis) {
+    // the largest plan any options take: the GRAM order with the fp32 master
+    // (X's lo half beside it and every s x s buffer); DIRECT needs less
     Plan P;
-    if (make_plan(batch, rows, cols, alpha, axis, DION2_NS_AUTO, &P) != DION2_OK) return 0;
+    if (make_plan(batch, rows, cols, alpha, axis, DION2_NS_GRAM, 0, &P, true, true) != DION2_OK) return 0;
     return P.total;
+}
+
+size_t dion2_workspace_size_ex(int batch, int64_t rows, int64_t cols, float alpha, int axis,
+                               int ns_steps, const dion2_options* opt_in) {
+    dion2_options opt;
+    if (opt_in) opt = *opt_in;
+    else dion2_options_init(&opt);
+    const std::string saved = g_last_error;   // a size query leaves the last error alone
+    Plan P;
+    const bool ok = validate_common(0.f, 0.f, ns_steps, opt) == DION2_OK &&
+                    make_plan(batch, rows, cols, alpha, axis, opt.ns_form, ns_steps, &P, true,
+                              opt.ns_master == DION2_MASTER_FP32) == DION2_OK;
+    g_last_error = saved;
+    return ok ? P.total : 0;
 }
 
 int dion2_plan_info(int64_t rows, int64_t cols, float alpha, int axis, int64_t* k_out,
                     int* axis_out) {
     Plan P;
-    int st = make_plan(1, rows, cols, alpha, axis, DION2_NS_AUTO, &P);
+    int st = make_plan(1, rows, cols, alpha, axis, DION2_NS_AUTO, 0, &P);
     if (st != DION2_OK) return st;
     if (k_out) *k_out = P.k;
     if (axis_out) *axis_out = P.axis;
@@ -1370,18 +1427,18 @@ void dion2_release_workspaces(void) {
         // best effort: a failure here leaves memory to the process's end
         if (hipSetDevice(kv.first.first) == hipSuccess) (void)hipDeviceSynchronize();
         if (w->dev) (void)hipFree(w->dev);
-        if (w->pinned) (void)hipHostFree(w->pinned);
-        if (w->tables_done) (void)hipEventDestroy(w->tables_done);
+        for (TableSlot& c : w->slots) {
+            if (c.host) (void)hipHostFree(c.host);
+            if (c.done) (void)hipEventDestroy(c.done);
+            c = TableSlot{};
+        }
+        w->next_slot = 0;
         for (hipStream_t a : w->aux) (void)hipStreamDestroy(a);
         for (hipEvent_t ev : w->ev) (void)hipEventDestroy(ev);
         w->aux.clear();
         w->ev.clear();
         w->dev = nullptr;
         w->bytes = 0;
-        w->pinned = nullptr;
-        w->pinned_count = 0;
-        w->tables_done = nullptr;
-        w->tables_pending = false;
     }
     if (prev >= 0) (void)hipSetDevice(prev);
 }

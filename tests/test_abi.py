@@ -157,7 +157,7 @@ def test_ex_options_validation(lib):
     assert ex(ns_master=1, ns_chain=binding.CHAIN_F16) == DION2_ERR_INVALID_ARG
     assert ex(ns_master=1, ns_form=binding.NS_DIRECT) == DION2_ERR_UNSUPPORTED
     # the fp32 master also keeps X's lo half: more workspace than the AUTO plan
-    need_auto = binding.dion2_workspace_size(1, 64, 64, 0.25)
+    need_auto = binding.dion2_workspace_size_ex(1, 64, 64, 0.25, AXIS_AUTO, 2)
     assert ex(ns_master=1, workspace=FAKE, workspace_bytes=need_auto) == DION2_ERR_WORKSPACE
     # the lo halves of X exist only with the fp32 master and a Newton-Schulz step
     assert ex(dbg_compact_lo=FAKE) == DION2_ERR_INVALID_ARG
@@ -169,9 +169,32 @@ def test_ex_options_validation(lib):
     assert st == DION2_ERR_INVALID_ARG and "ns_steps" in binding.dion2_last_error()
     coeffs = (ctypes.c_float * 6)(1.0, 2.0, 3.0, 1.0, float("inf"), 0.0)
     assert ex(ns_coeffs=ctypes.cast(coeffs, ctypes.POINTER(ctypes.c_float))) == DION2_ERR_INVALID_ARG
-    need = binding.dion2_workspace_size(1, 64, 64, 0.25)
+    need = binding.dion2_workspace_size_ex(1, 64, 64, 0.25, AXIS_AUTO, 2)
     assert ex(workspace=FAKE, workspace_bytes=need - 1) == DION2_ERR_WORKSPACE
     assert ex(workspace=FAKE + 16, workspace_bytes=need) == DION2_ERR_INVALID_ARG
+
+
+def test_direct_form_step_limit(lib):
+    """DIRECT rounds X to bf16 after every step; past DION2_DIRECT_MAX_STEPS
+    a forced DIRECT is refused (nothing launched), and the header and the
+    binding agree on the limit."""
+    text = open(HEADER).read()
+    limit = int(re.search(r"#define DION2_DIRECT_MAX_STEPS (\d+)", text).group(1))
+    assert limit == 6
+
+    def ex(ns, **o):
+        opt = Options()
+        lib.dion2_options_init(ctypes.byref(opt))
+        for k, v in o.items():
+            setattr(opt, k, v)
+        return lib.dion2_step_ex(FAKE, FAKE, FAKE, 1, 384, 384, 0.5, 0.95, 0.02, ns, -1,
+                                 ctypes.byref(opt), None)
+    for ns in (limit + 1, 16):
+        assert ex(ns, ns_form=binding.NS_DIRECT) == DION2_ERR_UNSUPPORTED
+        assert "DIRECT" in binding.dion2_last_error()
+        assert binding.dion2_workspace_size_ex(1, 384, 384, 0.5, AXIS_AUTO, ns, ns_form=binding.NS_DIRECT) == 0
+    # a step count beyond the maximum is an invalid argument under any form
+    assert ex(17, ns_form=binding.NS_DIRECT) == DION2_ERR_INVALID_ARG
 
 
 @pytest.mark.parametrize("rows,cols,alpha,axis", [
@@ -188,11 +211,15 @@ def test_plan_matches_oracle_reading(lib, rows, cols, alpha, axis):
 
 
 def test_workspace_size(lib):
+    ws_ex = binding.dion2_workspace_size_ex
     assert binding.dion2_workspace_size(0, 64, 64, 0.25) == 0
     assert binding.dion2_workspace_size(1, 64, 64, 2.0) == 0
-    a = binding.dion2_workspace_size(1, 2048, 2048, 0.25)
-    b = binding.dion2_workspace_size(2, 2048, 2048, 0.25)
-    c = binding.dion2_workspace_size(1, 2048, 2048, 1.0)
+    assert ws_ex(0, 64, 64, 0.25) == 0 and ws_ex(1, 64, 64, 2.0) == 0
+    assert ws_ex(1, 64, 64, 0.25, AXIS_AUTO, 17) == 0
+    assert ws_ex(1, 64, 64, 0.25, ns_master=binding.MASTER_FP32, ns_chain=binding.CHAIN_F16) == 0
+    a = ws_ex(1, 2048, 2048, 0.25)
+    b = ws_ex(2, 2048, 2048, 0.25)
+    c = ws_ex(1, 2048, 2048, 1.0)
     assert 0 < a < b and a < c
     assert a % 256 == 0
     # k = 512 of 2048 with l = 4 s: the GRAM form, one bf16 compact matrix,
@@ -200,6 +227,25 @@ def test_workspace_size(lib):
     assert a >= 512 * 2048 * (2 + 4) + 10 * 512 * 512 * 2
     # alpha = 1 (s = l): the DIRECT form, two bf16 compact buffers, three s x s
     assert c >= 2048 * 2048 * (2 * 2 + 4) + 3 * 2048 * 2048 * 2
+    # past the DIRECT form's step limit AUTO takes GRAM: ten s x s buffers
+    c7 = ws_ex(1, 2048, 2048, 1.0, AXIS_AUTO, 7)
+    assert c7 == ws_ex(1, 2048, 2048, 1.0, AXIS_AUTO, 5, ns_form=binding.NS_GRAM) and c7 > c
+    assert c7 >= 2048 * 2048 * (2 + 4) + 10 * 2048 * 2048 * 2
+    # the size without options covers every option and step count
+    for shape in ((1, 2048, 2048, 0.25), (2, 2048, 2048, 1.0), (3, 640, 256, 0.5), (1, 300, 200, 0.75)):
+        top = binding.dion2_workspace_size(*shape)
+        for kw in (dict(), dict(ns_form=binding.NS_DIRECT), dict(ns_form=binding.NS_GRAM),
+                   dict(ns_master=binding.MASTER_FP32), dict(ns_chain=binding.CHAIN_F16),
+                   dict(w_dtype=torch_f32(), g_dtype=torch_f32())):
+            for ns in (0, 1, 5, 6, 16):
+                need = ws_ex(*shape, AXIS_AUTO, ns, **kw)
+                assert need <= top, (shape, kw, ns)
+                assert need > 0 or (kw.get("ns_form") == binding.NS_DIRECT and ns > 6), (shape, kw, ns)
+
+
+def torch_f32():
+    import torch
+    return torch.float32
 
 
 def test_status_codes_match_header():

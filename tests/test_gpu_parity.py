@@ -314,13 +314,14 @@ def test_batch_beyond_grid_z(hip_device, chain):
 @pytest.mark.parametrize("rows,cols,alpha", [(256, 1024, 0.25), (1024, 256, 0.5), (384, 384, 0.5)],
                          ids=["rows-gram", "cols-gram", "square-direct"])
 def test_caller_workspace(hip_device, rows, cols, alpha):
-    """A caller-provided workspace of dion2_workspace_size bytes gives bitwise
-    the result of the library's own; one byte short, or a plan that needs more
-    (the fp32 master on a DIRECT shape), is refused before anything runs."""
+    """A caller-provided workspace of dion2_workspace_size_ex bytes gives
+    bitwise the result of the library's own; one block short, or a plan that
+    needs more (the fp32 master on a DIRECT shape), is refused before
+    anything runs."""
     wl = one_group_workload(rows, cols, count=2, name=f"ws{rows}x{cols}")
     W, M, G = workloads.make_group(wl, 0, hip_device)
     W2, M2 = W.clone(), M.clone()
-    need = binding.dion2_workspace_size(2, rows, cols, alpha)
+    need = binding.dion2_workspace_size_ex(2, rows, cols, alpha)
     assert need > 0
     ws = torch.empty(need, dtype=torch.uint8, device=hip_device)
     binding.dion2_step_ex(W, M, G, alpha, workspace=ws)
@@ -338,6 +339,33 @@ def test_caller_workspace(hip_device, rows, cols, alpha):
         assert ei.value.status == binding.DION2_ERR_WORKSPACE
     torch.cuda.synchronize()
     assert torch.equal(W3.view(torch.int16), W.view(torch.int16)) and torch.equal(M3, M), "refused calls modified state"
+
+
+@pytest.mark.parametrize("kw", [dict(ns_form=NS_GRAM), dict(ns_master=binding.MASTER_FP32),
+                                dict(ns_form=NS_DIRECT), dict(ns_form=NS_GRAM, ns_chain=binding.CHAIN_F16)],
+                         ids=["gram", "fp32-master", "direct", "f16-chain"])
+@pytest.mark.parametrize("rows,cols,alpha", [(384, 384, 0.5), (256, 1024, 0.25), (640, 256, 0.5)])
+def test_caller_workspace_sized_for_options(hip_device, kw, rows, cols, alpha):
+    """A caller workspace of exactly dion2_workspace_size_ex bytes for forced
+    options gives bitwise the library workspace's result, one block less is
+    refused (state untouched), and dion2_workspace_size (no options) covers
+    it."""
+    wl = one_group_workload(rows, cols, count=2, name=f"wsx{rows}x{cols}")
+    W, M, G = workloads.make_group(wl, 0, hip_device)
+    W2, M2, W3, M3 = W.clone(), M.clone(), W.clone(), M.clone()
+    need = binding.dion2_workspace_size_ex(2, rows, cols, alpha, AXIS_AUTO, 5, **kw)
+    assert 0 < need <= binding.dion2_workspace_size(2, rows, cols, alpha)
+    ws = torch.empty(need, dtype=torch.uint8, device=hip_device)
+    binding.dion2_step_ex(W, M, G, alpha, workspace=ws, **kw)
+    binding.dion2_step_ex(W2, M2, G, alpha, **kw)
+    with pytest.raises(binding.Dion2Error) as ei:
+        binding.dion2_step_ex(W3, M3, G, alpha, workspace=ws[:need - 256], **kw)
+    assert ei.value.status == binding.DION2_ERR_WORKSPACE
+    torch.cuda.synchronize()
+    assert torch.equal(W.view(torch.int16), W2.view(torch.int16)) and torch.equal(M, M2)
+    W0, M0, _ = workloads.make_group(wl, 0, hip_device)
+    assert torch.equal(W3.view(torch.int16), W0.view(torch.int16)) and torch.equal(M3, M0), \
+        "a refused call modified state"
 
 
 @pytest.mark.parametrize("eps", [0.0, 1.0], ids=["eps0", "eps-large"])
@@ -677,10 +705,15 @@ def test_gram_form_tracks_duplicate_lines(hip_device):
 
 
 @pytest.mark.parametrize("gi,alpha,samples", [(0, 0.25, (0, 63)), (1, 0.25, (7,)), (2, 0.25, (15,)),
-                                              (0, 0.5, (31,)), (0, 1.0, (5,))])
+                                              (0, 0.5, (31,)), (1, 0.5, (3,)), (2, 0.5, (10,)),
+                                              (0, 1.0, (5,)), (1, 1.0, (12,)), (2, 1.0, (0,))])
 def test_1b_stack_full_size_sampled(hip_device, gi, alpha, samples):
     """The whole group of the 1B-style stack in one batched call (the launch
-    configuration the benchmark times); sampled matrices checked in full."""
+    configuration the benchmark times) at every selection fraction the
+    benchmark reports (the sweep of Sec. 4.1 and Muon's alpha = 1); sampled
+    matrices checked in full. At alpha = 0.5 and 1 the 8192x2048 (columns)
+    and 2048x8192 (rows) groups run the GRAM chain at s = 1024 and 2048, and
+    the 2048x2048 group the DIRECT form."""
     wl = workloads.WORKLOADS["1b"]
     W, M, G = workloads.make_group(wl, gi, hip_device)
     grp = wl.groups[gi]
@@ -892,20 +925,50 @@ def test_groups_at_the_group_limit(hip_device):
         assert torch.equal(W.view(torch.int16), Ws.view(torch.int16)), f"group {gi}: weights"
 
 
-def test_sixteen_newton_schulz_steps(hip_device):
-    """The most steps a call takes. DIRECT rounds X to bf16 after every step,
-    so its distance from the fp64 iteration grows with the step count
-    (about 1e-2 at 5 steps); the GRAM form and the fp32 master carry the
-    iteration in hi/lo pairs and stay at their 5-step error."""
-    wl = one_group_workload(160, 640, name="ns16")
+@pytest.mark.parametrize("rows,cols,alpha", [(160, 640, 0.5), (384, 384, 0.5), (300, 200, 0.75),
+                                              (257, 129, 1.0)])
+def test_sixteen_newton_schulz_steps(hip_device, rows, cols, alpha):
+    """The most steps a call takes, on near-square compact matrices (where AUTO
+    would take DIRECT at 5 steps). DIRECT rounds X to bf16 after every step,
+    so its error grows with the step count and it is refused past
+    DION2_DIRECT_MAX_STEPS; every path the library accepts at 16 steps meets
+    the 2e-2 bar: AUTO (which takes GRAM), GRAM, and the fp32 master at a
+    tenth of it."""
+    wl = one_group_workload(rows, cols, name=f"ns16-{rows}x{cols}")
     W, M, G = workloads.make_group(wl, 0, hip_device)
+    W1, M1 = W.clone(), M.clone()
+    with pytest.raises(binding.Dion2Error) as ei:
+        binding.dion2_step_ex(W1, M1, G, alpha, 0.95, 0.02, 16, ns_form=NS_DIRECT)
+    assert ei.value.status == binding.DION2_ERR_UNSUPPORTED
+    torch.cuda.synchronize()
+    assert torch.equal(W1.view(torch.int16), W.view(torch.int16)) and torch.equal(M1, M), \
+        "a refused call modified state"
     errs = {}
-    for name, kw, tol in (("direct", dict(form=NS_DIRECT), 8e-2), ("gram", dict(form=NS_GRAM), NS_TOL),
+    for name, kw, tol in (("auto", dict(), NS_TOL), ("gram", dict(form=NS_GRAM), NS_TOL),
                           ("master", dict(master=binding.MASTER_FP32), MASTER_TOL)):
-        res = run_gpu(W.clone(), M.clone(), G, 0.5, ns_steps=16, **kw)
-        errs[name] = check_matrix(res, 0, 0.5, ns_steps=16, ns_tol=tol)
-    assert errs["gram"] < errs["direct"] and errs["master"] < errs["gram"], errs
+        res = run_gpu(W.clone(), M.clone(), G, alpha, ns_steps=16, **kw)
+        errs[name] = check_matrix(res, 0, alpha, ns_steps=16, ns_tol=tol)
+        if name == "auto":
+            O_auto = res["O"]
+        if name == "gram":
+            assert torch.equal(res["O"], O_auto), "AUTO at 16 steps is not the GRAM form"
+    assert errs["master"] < errs["gram"], errs
     print("16-step errors", errs)
+
+
+@pytest.mark.parametrize("rows,cols,alpha", [(160, 640, 0.5), (384, 384, 0.5), (300, 200, 0.75),
+                                              (257, 129, 1.0), (2048, 2048, 0.5)])
+def test_direct_form_at_its_step_limit(hip_device, rows, cols, alpha):
+    """DIRECT at DION2_DIRECT_MAX_STEPS (6) steps, the most it takes, stays
+    within 2e-2 on the near-square compact matrices it is chosen for; with 6
+    steps AUTO still takes it there (bitwise the forced DIRECT)."""
+    wl = one_group_workload(rows, cols, name=f"direct6-{rows}x{cols}")
+    W, M, G = workloads.make_group(wl, 0, hip_device)
+    res = run_gpu(W.clone(), M.clone(), G, alpha, ns_steps=6, form=NS_DIRECT)
+    err = check_matrix(res, 0, alpha, ns_steps=6)
+    res_auto = run_gpu(W.clone(), M.clone(), G, alpha, ns_steps=6)
+    assert torch.equal(res_auto["O"], res["O"]), "AUTO at 6 steps is not the DIRECT form here"
+    print(f"DIRECT, 6 steps, {rows}x{cols} alpha {alpha}: {err:.3e}")
 
 
 @pytest.mark.parametrize("case", ["f32-decay-all-schedule", "forced-direct", "forced-gram", "no-steps",

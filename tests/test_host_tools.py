@@ -110,3 +110,30 @@ def test_source_hash_ignores_comments_only():
     assert profsum.code_text(base) == profsum.code_text(same)
     assert profsum.code_text(base) != profsum.code_text(other)
     assert profsum.code_text(base) != profsum.code_text(strings)
+
+
+def test_bench_floors_match_the_measurement_plan():
+    """bench.floors: the Newton-Schulz flops T (4 s^2 l + 2 s^3) and the
+    algorithmic bytes N (8 + g) + k d_oth (8 + 2 w) of each stack, against
+    the figures derived for the measurement plan from the Table 1 shapes
+    (three significant digits), and the floors at 2.5 PFLOP/s and 8 TB/s."""
+    sys.path.insert(0, ROOT)
+    import bench
+    from paper_2512_16928_amd import workloads as wls
+    want = {("1b", 0.25): (2.19e12, 10.47e9), ("1b", 0.5): (9.28e12, 12.88e9),
+            ("1b", 1.0): (4.12e13, 17.72e9), ("1b-colsel", 0.25): (9.02e12, 10.47e9),
+            ("7b", 0.125): (8.59e12, 74.5e9), ("7b", 0.25): (3.56e13, 84.2e9),
+            ("7b", 1.0): (6.84e14, 142.5e9), ("moe", 0.25): (1.21e13, 80.3e9),
+            ("single-256", 0.25): (2.36e7, 1.05e6)}
+    for (name, alpha), (flops, nbytes) in want.items():
+        f = bench.floors(wls.WORKLOADS[name], alpha)
+        assert abs(f["ns_flops"] / flops - 1) < 5e-3, (name, alpha, f["ns_flops"])
+        assert abs(f["alg_bytes"] / nbytes - 1) < 5e-3, (name, alpha, f["alg_bytes"])
+        assert abs(f["ns_ms_at_peak"] - f["ns_flops"] / 2.5e12) < 1e-9
+        assert abs(f["hbm_ms_at_peak"] - f["alg_bytes"] / 8e9) < 1e-9
+        assert f["floor_ms"] == max(f["ns_ms_at_peak"], f["hbm_ms_at_peak"])
+    # one 2048x2048 matrix at alpha 0.25 by hand: k = 512 rows of 2048, s = 512, l = 2048
+    one = wls.Workload("one", "t", (wls.Group("g", 2048, 2048, 1),), (0.25,))
+    f = bench.floors(one, 0.25)
+    assert f["ns_flops"] == 5 * (4 * 512 ** 2 * 2048 + 2 * 512 ** 3)
+    assert f["alg_bytes"] == 2048 * 2048 * 10 + 512 * 2048 * 12
