@@ -167,7 +167,8 @@ def one_step(wl, groups, alpha, rule=binding.SELECT_L1):
             s.wait_event(fork)
         with torch.cuda.stream(s):
             if (NS_FORM == binding.NS_AUTO and NS_CHAIN == binding.CHAIN_HILO
-                    and NS_MASTER == binding.MASTER_BF16 and rule == binding.SELECT_L1):
+                    and NS_MASTER == binding.MASTER_BF16 and rule == binding.SELECT_L1
+                    and wl.w_dtype == "bf16"):
                 binding.dion2_step_strided(W, M, G, alpha, wl.mu, wl.lr, wl.ns_steps, grp.axis)
             else:
                 binding.dion2_step_ex(W, M, G, alpha, wl.mu, wl.lr, wl.ns_steps, grp.axis,
