@@ -252,6 +252,26 @@ int dion2_step_ex(void* W, float* M, const void* G, int batch, int64_t rows,
                   int64_t cols, float alpha, float mu, float lr, int ns_steps,
                   int axis, const dion2_options* opt, void* stream);
 
+/* For callers that cannot allocate device memory (code under HIP graph
+   capture, tight serving loops, harnesses that forbid hipMalloc): the step
+   of dion2_step_ex, bitwise the same results, with the workspace taken from
+   a fixed device array of DION2_NOALLOC_SCRATCH_BYTES that each GPU the
+   library runs on holds until the process ends. The call allocates no
+   device memory (no hipMalloc, hipFree or allocating library routine) and
+   takes strided stacks only. opt->workspace must be NULL
+   (DION2_ERR_INVALID_ARG otherwise); a call whose workspace
+   (dion2_workspace_size_ex) exceeds the array fails with DION2_ERR_WORKSPACE
+   before anything runs. Every call on one GPU uses that GPU's one array, and
+   nothing in it needs to start at zero: calls whose kernels overlap on one
+   GPU (on different streams, say) race and give wrong results; calls queued
+   on one stream, or otherwise ordered, are safe. The measurement hooks do
+   not time its phases. */
+#define DION2_NOALLOC_SCRATCH_BYTES ((size_t)128 << 20)
+int dion2_step_noalloc(void* W, float* M, const void* G, int batch,
+                       int64_t rows, int64_t cols, float alpha, float mu,
+                       float lr, int ns_steps, int axis,
+                       const dion2_options* opt, void* stream);
+
 /* One same-shape group for dion2_step_groups: contiguous DEVICE stacks W
    and G [batch][rows][cols] in the storage types of the options, M fp32
    [batch][rows][cols], each 16-byte aligned, and the group's selection axis

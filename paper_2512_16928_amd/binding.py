@@ -38,7 +38,7 @@ MAX_NS_STEPS = 16
 
 # Every function include/dion2.h declares (checked by the ABI tests).
 EXPORTED = ("dion2_options_init", "dion2_step", "dion2_step_strided", "dion2_step_batched",
-            "dion2_step_ex", "dion2_step_groups", "dion2_workspace_size",
+            "dion2_step_ex", "dion2_step_noalloc", "dion2_step_groups", "dion2_workspace_size",
             "dion2_workspace_size_ex", "dion2_plan_info",
             "dion2_release_workspaces", "dion2_status_string", "dion2_last_error",
             "dion2_version", "dion2_profile_enable", "dion2_profile_read", "dion2_profile_reset")
@@ -117,6 +117,8 @@ def load(path: str = LIB_PATH):
     lib.dion2_step_batched.restype = c_int
     lib.dion2_step_ex.argtypes = [vp, vp, vp, c_int, i64, i64, *step_tail, POINTER(Options), vp]
     lib.dion2_step_ex.restype = c_int
+    lib.dion2_step_noalloc.argtypes = [vp, vp, vp, c_int, i64, i64, *step_tail, POINTER(Options), vp]
+    lib.dion2_step_noalloc.restype = c_int
     lib.dion2_step_groups.argtypes = [POINTER(Group), c_int, c_float, c_float, c_float, c_int,
                                       POINTER(Options), vp]
     lib.dion2_step_groups.restype = c_int
@@ -267,6 +269,29 @@ def dion2_step_ex(W, M, G, alpha, mu=0.95, lr=0.02, ns_steps=5, axis=AXIS_AUTO, 
     _check(lib.dion2_step_ex(W.data_ptr(), M.data_ptr(), G.data_ptr(), batch, rows, cols, alpha,
                              mu, lr, ns_steps, axis, ctypes.byref(opt),
                              _stream_ptr(stream, W.device)))
+    del coeff_buf
+
+
+NOALLOC_SCRATCH_BYTES = 128 << 20
+
+
+def dion2_step_noalloc(W, M, G, alpha, mu=0.95, lr=0.02, ns_steps=5, axis=AXIS_AUTO, *,
+                       ns_coeffs=None, ns_eps=1e-7, decay_all=False, ns_form=NS_AUTO,
+                       select_rule=SELECT_L1, rand_seed=0, rand_step=0, rand_matrix0=0,
+                       ns_chain=CHAIN_HILO, ns_master=MASTER_BF16, stream=None):
+    """The step of dion2_step_ex without any device allocation: the library's
+    fixed scratch array holds the workspace (NOALLOC_SCRATCH_BYTES per GPU).
+    Calls that overlap on one GPU race."""
+    if W.dim() == 2:
+        W, M, G = W.unsqueeze(0), M.unsqueeze(0), G.unsqueeze(0)
+    _mats(W, M, G, 3)
+    lib = load()
+    opt, coeff_buf = _options(W, G, ns_steps, ns_coeffs, ns_eps, decay_all, ns_form, select_rule,
+                              rand_seed, rand_step, rand_matrix0, ns_chain, ns_master)
+    batch, rows, cols = W.shape
+    _check(lib.dion2_step_noalloc(W.data_ptr(), M.data_ptr(), G.data_ptr(), batch, rows, cols,
+                                  alpha, mu, lr, ns_steps, axis, ctypes.byref(opt),
+                                  _stream_ptr(stream, W.device)))
     del coeff_buf
 
 

@@ -256,10 +256,15 @@ struct Profiler {
 
 Profiler g_prof;
 
+// Set for the duration of an allocation-free call: its phases are not timed
+// (the hooks create HIP events on demand).
+thread_local bool t_no_alloc = false;
+
 // Brackets one kernel phase with events when the hooks are on.
 class PhaseTimer {
   public:
     PhaseTimer(int phase, double flops, double bytes, int launches, hipStream_t s) : s_(s) {
+        if (t_no_alloc) return;
         std::lock_guard<std::mutex> lk(g_prof.mu);
         if (!g_prof.on) return;
         rec_.phase = phase;
@@ -1036,9 +1041,38 @@ int validate_common(float mu, float lr, int ns_steps, const dion2_options& opt) 
     return DION2_OK;
 }
 
+// ------------------------------------------------- allocation-free calls
+// The workspace of dion2_step_noalloc: a fixed device array that every GPU
+// the library runs on holds until the process ends. In host code `scratch`
+// names a host-side stand-in, not device memory; the device address of each
+// GPU's copy comes from hipGetSymbolAddress, taken once per device with that
+// device current, and only that address is ever handed to a kernel.
+constexpr size_t kScratchBytes = DION2_NOALLOC_SCRATCH_BYTES;
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+
+std::mutex g_scratch_mu;
+std::map<int, void*> g_scratch_ptr;   // device -> address of its scratch
+
+int scratch_address(void** out) {
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+    std::lock_guard<std::mutex> lk(g_scratch_mu);
+    auto it = g_scratch_ptr.find(dev);
+    if (it == g_scratch_ptr.end()) {
+        void* ptr = nullptr;
+        e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return hip_fail(e, "hipGetSymbolAddress(scratch)");
+        if (!ptr) return fail(DION2_ERR_HIP, "hipGetSymbolAddress(scratch) gave a null address");
+        it = g_scratch_ptr.emplace(dev, ptr).first;
+    }
+    *out = it->second;
+    return DION2_OK;
+}
+
 int step_impl(void* W, float* M, const void* G, const Tables* tabs, int batch, int64_t rows,
               int64_t cols, float alpha, float mu, float lr, int ns_steps, int axis,
-              const dion2_options* opt_in, void* stream) {
+              const dion2_options* opt_in, void* stream, bool no_alloc = false) {
     dion2_options opt;
     if (opt_in) opt = *opt_in;
     else dion2_options_init(&opt);
@@ -1068,6 +1102,25 @@ int step_impl(void* W, float* M, const void* G, const Tables* tabs, int batch, i
         if (!W || !M || !G) return fail(DION2_ERR_INVALID_ARG, "W, M and G must not be NULL");
         if (!aligned16(W) || !aligned16(M) || !aligned16(G))
             return fail(DION2_ERR_INVALID_ARG, "W, M and G must be 16-byte aligned");
+    }
+    if (no_alloc) {
+        if (opt.workspace)
+            return fail(DION2_ERR_INVALID_ARG,
+                        "dion2_step_noalloc uses its own scratch (opt->workspace must be NULL)");
+        if (P.total > kScratchBytes)
+            return fail(DION2_ERR_WORKSPACE,
+                        "this call needs %zu bytes of scratch; dion2_step_noalloc holds %zu "
+                        "(DION2_NOALLOC_SCRATCH_BYTES): use a smaller batch or dion2_step_ex",
+                        P.total, kScratchBytes);
+        void* ptr = nullptr;
+        st = scratch_address(&ptr);
+        if (st != DION2_OK) return st;
+        opt.workspace = ptr;
+        opt.workspace_bytes = kScratchBytes;
+        t_no_alloc = true;
+        st = run_step(P, W, M, G, tabs, mu, lr, ns_steps, opt, fmt, static_cast<hipStream_t>(stream));
+        t_no_alloc = false;
+        return st;
     }
     if (opt.workspace) {
         if ((reinterpret_cast<uintptr_t>(opt.workspace) & 255u) != 0)
@@ -1378,6 +1431,13 @@ int dion2_step_ex(void* W, float* M, const void* G, int batch, int64_t rows, int
                   const dion2_options* opt, void* stream) {
     return step_impl(W, M, G, nullptr, batch, rows, cols, alpha, mu, lr, ns_steps, axis, opt,
                      stream);
+}
+
+int dion2_step_noalloc(void* W, float* M, const void* G, int batch, int64_t rows, int64_t cols,
+                       float alpha, float mu, float lr, int ns_steps, int axis,
+                       const dion2_options* opt, void* stream) {
+    return step_impl(W, M, G, nullptr, batch, rows, cols, alpha, mu, lr, ns_steps, axis, opt,
+                     stream, true);
 }
 
 int dion2_step_groups(const dion2_group* groups, int ngroups, float alpha, float mu, float lr,

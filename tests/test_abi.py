@@ -307,3 +307,28 @@ def test_groups_stream_count_validated(lib):
         opt.group_streams = bad
         assert binding.dion2_step_groups_raw(arr, 1, 0.25, 0.95, 0.02, 5, opt, None) == DION2_ERR_INVALID_ARG
         assert "group_streams" in binding.dion2_last_error()
+
+
+def test_noalloc_validation(lib):
+    """dion2_step_noalloc validates like dion2_step_ex, refuses a workspace of
+    the caller's, and refuses a plan beyond its scratch array before any HIP
+    call."""
+    text = open(HEADER).read()
+    assert re.search(r"#define DION2_NOALLOC_SCRATCH_BYTES \(\(size_t\)128 << 20\)", text)
+    assert binding.NOALLOC_SCRATCH_BYTES == 128 << 20
+
+    def na(rows=64, cols=64, batch=1, alpha=0.25, ns=5, **o):
+        opt = Options()
+        lib.dion2_options_init(ctypes.byref(opt))
+        for k, v in o.items():
+            setattr(opt, k, v)
+        return lib.dion2_step_noalloc(FAKE, FAKE, FAKE, batch, rows, cols, alpha, 0.95, 0.02, ns, -1,
+                                      ctypes.byref(opt), None)
+    assert na(alpha=0.0) == DION2_ERR_INVALID_ARG
+    assert na(ns=17) == DION2_ERR_INVALID_ARG
+    assert na(workspace=FAKE, workspace_bytes=1 << 30) == DION2_ERR_INVALID_ARG
+    assert "workspace" in binding.dion2_last_error()
+    big = (16, 2048, 8192, 1.0)
+    assert binding.dion2_workspace_size_ex(*big) > binding.NOALLOC_SCRATCH_BYTES
+    assert na(rows=2048, cols=8192, batch=16, alpha=1.0) == DION2_ERR_WORKSPACE
+    assert "scratch" in binding.dion2_last_error()
