@@ -134,40 +134,47 @@ __device__ __forceinline__ int nmajor_off(int r, int c) {
     return r * 256 + 16 * (c ^ ((r & 3) << 2));
 }
 
-// Issue the direct-to-LDS loads of K-slice `kt` into the stage at `dst`.
-// Wave w owns the stage's 1 KB blocks w, w + WAVES, ...; lane i of a block
-// fills the block's 16-byte slot i with the global chunk that belongs there.
+// Issue the direct-to-LDS load `q` (0 <= q < IPW) of this wave's part of
+// K-slice `kt` into the stage at `dst`. Wave w owns the stage's 1 KB blocks
+// w, w + WAVES, ...; lane i of a block fills the block's 16-byte slot i with
+// the global chunk that belongs there.
+template <int NPASS, typename T>
+__device__ __forceinline__ void load_one(const GemmArgs& a, unsigned char* dst, int kt,
+                                         const uint16_t* const (&abase)[2],
+                                         const uint16_t* const (&bbase)[2], int wave, int lane, int q) {
+    const int blk = wave + q * T::WAVES;   // 1 KB block of the stage (wave-uniform)
+    const uint16_t* src;
+    if (blk * 1024 < T::NA * T::A_BYTES) {
+        // K-major A tile: the block holds 1024 / PK whole rows
+        const int t = (blk * 1024) / T::A_BYTES;
+        const int lb = (blk * 1024) % T::A_BYTES + lane * 16;
+        const int r = lb / T::PK, slot = (lb % T::PK) / 16;
+        const int c = slot ^ ((r / T::GK) % T::CPR);
+        src = (t ? abase[1] : abase[0]) + (int64_t)r * a.lda + (int64_t)kt * T::BK + c * 8;
+    } else {
+        const int bb = blk * 1024 - T::NA * T::A_BYTES;
+        const int t = bb / T::B_BYTES;
+        const int lb = bb % T::B_BYTES + lane * 16;
+        if constexpr (T::BT) {
+            const int r = lb / 256, slot = (lb % 256) / 16;
+            const int c = slot ^ ((r & 3) << 2);
+            src = (t ? bbase[1] : bbase[0]) + ((int64_t)kt * T::BK + r) * a.ldb + c * 8;
+        } else {
+            const int r = lb / T::PK, slot = (lb % T::PK) / 16;
+            const int c = slot ^ ((r / T::GK) % T::CPR);
+            src = (t ? bbase[1] : bbase[0]) + (int64_t)r * a.ldb + (int64_t)kt * T::BK + c * 8;
+        }
+    }
+    __builtin_amdgcn_global_load_lds(src, (lds_void*)(dst + blk * 1024), 16, 0, 0);
+}
+
+// All of this wave's loads of K-slice `kt` (the ring's prologue).
 template <int NPASS, typename T>
 __device__ __forceinline__ void load_slice(const GemmArgs& a, unsigned char* dst, int kt,
                                            const uint16_t* const (&abase)[2],
                                            const uint16_t* const (&bbase)[2], int wave, int lane) {
 #pragma unroll
-    for (int q = 0; q < T::IPW; ++q) {
-        const int blk = wave + q * T::WAVES;   // 1 KB block of the stage (wave-uniform)
-        const uint16_t* src;
-        if (blk * 1024 < T::NA * T::A_BYTES) {
-            // K-major A tile: the block holds 1024 / PK whole rows
-            const int t = (blk * 1024) / T::A_BYTES;
-            const int lb = (blk * 1024) % T::A_BYTES + lane * 16;
-            const int r = lb / T::PK, slot = (lb % T::PK) / 16;
-            const int c = slot ^ ((r / T::GK) % T::CPR);
-            src = (t ? abase[1] : abase[0]) + (int64_t)r * a.lda + (int64_t)kt * T::BK + c * 8;
-        } else {
-            const int bb = blk * 1024 - T::NA * T::A_BYTES;
-            const int t = bb / T::B_BYTES;
-            const int lb = bb % T::B_BYTES + lane * 16;
-            if constexpr (T::BT) {
-                const int r = lb / 256, slot = (lb % 256) / 16;
-                const int c = slot ^ ((r & 3) << 2);
-                src = (t ? bbase[1] : bbase[0]) + ((int64_t)kt * T::BK + r) * a.ldb + c * 8;
-            } else {
-                const int r = lb / T::PK, slot = (lb % T::PK) / 16;
-                const int c = slot ^ ((r / T::GK) % T::CPR);
-                src = (t ? bbase[1] : bbase[0]) + (int64_t)r * a.ldb + (int64_t)kt * T::BK + c * 8;
-            }
-        }
-        __builtin_amdgcn_global_load_lds(src, (lds_void*)(dst + blk * 1024), 16, 0, 0);
-    }
+    for (int q = 0; q < T::IPW; ++q) load_one<NPASS, T>(a, dst, kt, abase, bbase, wave, lane, q);
 }
 
 // Wait until at most N vector-memory loads of this wave are outstanding
@@ -196,10 +203,15 @@ __device__ __forceinline__ bf16x8 b_frag_tr(const unsigned char* sb, int krow, i
 }
 
 // MFMAs of one BK-deep K-slice staged at `st`, fragments software-pipelined
-// (k-step kk+1 is read from LDS while the MFMAs of kk run).
+// (k-step kk+1 is read from LDS while the MFMAs of kk run). The loads of
+// slice `kn` into the stage at `ldst` are spread between the MFMAs, each
+// fenced in place: issued in one burst ahead of the MFMAs they hold the
+// wave in the vector-memory issue queue while its matrix pipe idles.
 template <int NPASS, typename T>
 __device__ __forceinline__ void mma_slice(f32x16 (&acc)[T::FM][T::FN], const unsigned char* st,
-                                          int wm, int wn, int lane) {
+                                          int wm, int wn, int lane, const GemmArgs& a, unsigned char* ldst,
+                                          int kn, const uint16_t* const (&abase)[2],
+                                          const uint16_t* const (&bbase)[2], int wave) {
     const unsigned char* sa0 = st;
     const unsigned char* sa1 = st + T::A_BYTES;
     const unsigned char* sb0 = st + T::NA * T::A_BYTES;
@@ -208,8 +220,12 @@ __device__ __forceinline__ void mma_slice(f32x16 (&acc)[T::FM][T::FN], const uns
     const int brow = wn * T::TN + (lane & 31);
     const int half = lane >> 5;
     constexpr int KK = T::BK / 16;
+    constexpr int NM = T::FM * T::FN * NPASS;            // MFMAs per k-step
+    constexpr int NL = (T::IPW + KK - 1) / KK;           // loads per k-step
+    constexpr int EVERY = NM / NL > 0 ? NM / NL : 1;     // MFMAs between two loads
     using Frag = typename T::Frag;
     Frag fa0[2][T::FM], fb0[2][T::FN], fa1[2][T::FM], fb1[2][T::FN];
+    int q = 0;   // next load of slice kn (compile-time after unrolling)
 #pragma unroll
     for (int kk = 0; kk <= KK; ++kk) {
         if (kk < KK) {
@@ -244,16 +260,28 @@ __device__ __forceinline__ void mma_slice(f32x16 (&acc)[T::FM][T::FN], const uns
         }
         if (kk > 0) {
             const int slot = (kk - 1) & 1;
+            int m = 0;
 #pragma unroll
             for (int i = 0; i < T::FM; ++i)
 #pragma unroll
-                for (int j = 0; j < T::FN; ++j) {
-                    if constexpr (NPASS == 3) acc[i][j] = mfma32(fa0[slot][i], fb1[slot][j], acc[i][j]);
-                    if constexpr (NPASS >= 2) acc[i][j] = mfma32(fa1[slot][i], fb0[slot][j], acc[i][j]);
-                    acc[i][j] = mfma32(fa0[slot][i], fb0[slot][j], acc[i][j]);
-                }
+                for (int j = 0; j < T::FN; ++j)
+#pragma unroll
+                    for (int p = 0; p < NPASS; ++p) {
+                        // per block: hi*lo, lo*hi, then hi*hi (the order of the sums)
+                        if (NPASS == 3 && p == 0) acc[i][j] = mfma32(fa0[slot][i], fb1[slot][j], acc[i][j]);
+                        else if (NPASS >= 2 && p == NPASS - 2) acc[i][j] = mfma32(fa1[slot][i], fb0[slot][j], acc[i][j]);
+                        else acc[i][j] = mfma32(fa0[slot][i], fb0[slot][j], acc[i][j]);
+                        if (++m % EVERY == 0 && q < T::IPW && q < kk * NL) {
+                            __builtin_amdgcn_sched_barrier(0);
+                            load_one<NPASS, T>(a, ldst, kn, abase, bbase, wave, lane, q);
+                            __builtin_amdgcn_sched_barrier(0);
+                            ++q;
+                        }
+                    }
         }
     }
+#pragma unroll
+    for (; q < T::IPW; ++q) load_one<NPASS, T>(a, ldst, kn, abase, bbase, wave, lane, q);
 }
 
 // Store a wave's finished 32 x 32 block from its LDS tile (fp32, row pitch
@@ -445,9 +473,8 @@ __global__ __launch_bounds__(T::THREADS) void gemm(GemmArgs a) {
         wait_vmcnt<(T::S - 2) * T::IPW>();
         __builtin_amdgcn_s_barrier();
         const int kn = kt + T::S - 1;
-        load_slice<NPASS, T>(a, smem_raw + (kn % T::S) * T::STAGE_BYTES, kn < nk ? kn : nk - 1,
-                             abase, bbase, wave, lane);
-        mma_slice<NPASS, T>(acc, smem_raw + (kt % T::S) * T::STAGE_BYTES, wm, wn, lane);
+        mma_slice<NPASS, T>(acc, smem_raw + (kt % T::S) * T::STAGE_BYTES, wm, wn, lane, a,
+                            smem_raw + (kn % T::S) * T::STAGE_BYTES, kn < nk ? kn : nk - 1, abase, bbase, wave);
     }
     wait_vmcnt<0>();   // no load may land in the ring once the epilogue reuses it
     __syncthreads();
@@ -661,17 +688,32 @@ hipError_t launch_tile(const GemmArgs& a, hipStream_t s) {
 
 }  // namespace
 
+// A three-pass symmetric s x s product without a polynomial epilogue goes
+// on 256 x 256 tiles (one block of eight waves per compute unit) when s is
+// a multiple of 256 and the launch has enough of those tiles to fill the
+// chip twice; otherwise on 128 x 128.
+bool big_sym(const GemmArgs& a) {
+    if (a.M < 1024 || a.M % 256) return false;
+    const int64_t t = a.M / 256;
+    return (int64_t)a.batch * (a.dual ? 2 : 1) * (t * (t + 1) / 2) >= 512;
+}
+
 hipError_t launch_gemm(const GemmArgs& a, GemmEpi epi, int npass, hipStream_t s) {
-    // Tile choices measured on MI355X at the Newton-Schulz shapes. At s = 512
-    // the kernels are bound by load latency, so blocks resident per CU count
-    // for more than ring depth: 128 x 128 tiles keep enough blocks in flight;
-    // from s = 1024 the Gram matrix runs faster on
-    // 256 x 256 tiles of 8 waves; the X-side products use a two-stage ring,
-    // which leaves room for three blocks per CU; with the update applied in
-    // the epilogue eight waves per block hide more of the W traffic.
-    using TG = Tile<1, 0, 128, 128, 32, 2, 2, 4>;    // Gram
+    // Tile choices measured on MI355X at the Newton-Schulz shapes. The Gram
+    // matrix reads Z with BK = 64, so each row of a K-slice is one whole
+    // 128-byte line (64-byte rows halve what the L2 delivers per request),
+    // two blocks of eight waves per CU (a third stage, one block per CU, is
+    // faster alone but slows the step, whose groups run side by side); from
+    // s = 1024 it runs on 256 x 256 tiles.
+    // The three-pass s x s products keep 128 x 128 tiles, two blocks per CU,
+    // except large launches of the plain (hi / lo) products, which run on
+    // 256 x 256. The X-side products use a two-stage ring, which leaves
+    // room for three blocks per CU; with the update applied in the
+    // epilogue eight waves per block hide more of the W traffic.
+    using TG = Tile<1, 0, 128, 128, 64, 4, 2, 2>;    // Gram
     using TGL = Tile<1, 0, 256, 256, 32, 4, 2, 3>;   // Gram, large s
     using TP = Tile<3, 0, 128, 128, 32, 4, 2, 2>;    // three-pass symmetric products
+    using TPL = Tile<3, 0, 256, 256, 32, 2, 4, 2>;   // three-pass symmetric products, large s
     using TU = Tile<1, 1, 128, 128, 32, 2, 2, 2>;    // update (B operand [K][N])
     using TU2 = Tile<2, 1, 128, 128, 32, 2, 2, 2>;   // two-pass final product
     using TU2A = Tile<2, 1, 128, 128, 32, 4, 2, 2>;  // two-pass final product applying the update
@@ -694,7 +736,10 @@ hipError_t launch_gemm(const GemmArgs& a, GemmEpi epi, int npass, hipStream_t s)
     if (a.dual && !(epi == EPI_SPLIT && npass == 3)) return hipErrorInvalidValue;
     switch (epi) {
         case EPI_SPLIT:
-            if (npass == 3) return launch_tile<3, EPI_SPLIT, TP, true>(a, s);
+            if (npass == 3) {
+                if (big_sym(a)) return launch_tile<3, EPI_SPLIT, TPL, true>(a, s);
+                return launch_tile<3, EPI_SPLIT, TP, true>(a, s);
+            }
             if (npass != 1) break;
             if (a.M >= 1024 && a.M % 256 == 0) return launch_tile<1, EPI_SPLIT, TGL, true>(a, s);
             return launch_tile<1, EPI_SPLIT, TG, true>(a, s);
@@ -702,7 +747,7 @@ hipError_t launch_gemm(const GemmArgs& a, GemmEpi epi, int npass, hipStream_t s)
             if (npass != 1) break;
             if (a.M >= 1024 && a.M % 256 == 0) return launch_tile<1, EPI_H16, TGL, true>(a, s);
             return launch_tile<1, EPI_H16, TG, true>(a, s);
-        case EPI_POLY:
+        case EPI_POLY:   // (the polynomial epilogues keep 128 x 128: on 256 x 256 they spill)
             if (npass == 3) return launch_tile<3, EPI_POLY, TP, true>(a, s);
             break;
         case EPI_QPOLY:
