@@ -17,6 +17,10 @@
         cycles of the matrix cores over active cycles of every SIMD, and 512
         flops per counted matrix op), with the kernels' average durations
         from a `--kernel-trace --stats` run of the same command
+    python -m paper_2512_16928_amd.profsum gaps DIR [--split-us US]
+        idle time between consecutive library kernels on each stream of a
+        `--kernel-trace` run, and the share of the traced span during which
+        some library kernel ran
 
 The traffic and MFMA summaries end with one line per phase, tagged with a
 hash of the kernel sources it was taken on; bench.py reports a phase's
@@ -322,6 +326,41 @@ def lookup_hbm_rate(path: str, phase: str, workload: str, alpha: float):
     return {"counted_gbs": float(kv["counted_gbs"]), "frac_of_peak": float(kv["frac_of_peak"])}
 
 
+def cmd_gaps(args):
+    """Idle time between consecutive library kernels on each stream of a
+    kernel-trace run (the launch overhead that graph capture would remove),
+    and how much of the traced span some library kernel was running."""
+    path = find_csv(args.dir, "kernel_trace.csv")
+    rows = [r for r in csv.DictReader(open(path)) if phase_of(r["Kernel_Name"])]
+    if not rows:
+        sys.exit(f"no library kernels in {path}")
+    by_stream = {}
+    for r in rows:
+        by_stream.setdefault(r["Stream_Id"], []).append((int(r["Start_Timestamp"]), int(r["End_Timestamp"])))
+    print(f"{'stream':>6s} {'kernels':>8s} {'gaps':>6s} {'median us':>10s} {'mean us':>8s} {'p95 us':>7s} "
+          f"{'total ms':>9s}")
+    for sid in sorted(by_stream, key=lambda x: int(x)):
+        ks = sorted(by_stream[sid])
+        # a gap longer than args.split_us separates two steps (host-side work, events)
+        gaps = [b[0] - a[1] for a, b in zip(ks, ks[1:])]
+        gaps = sorted(max(0, g) for g in gaps if g < args.split_us * 1e3)
+        if not gaps:
+            continue
+        med, p95 = gaps[len(gaps) // 2], gaps[min(len(gaps) - 1, int(0.95 * len(gaps)))]
+        print(f"{sid:>6s} {len(ks):8d} {len(gaps):6d} {med / 1e3:10.2f} {sum(gaps) / len(gaps) / 1e3:8.2f} "
+              f"{p95 / 1e3:7.2f} {sum(gaps) / 1e6:9.3f}")
+    ev = sorted([(int(r["Start_Timestamp"]), 1) for r in rows] + [(int(r["End_Timestamp"]), -1) for r in rows])
+    busy, depth, last = 0, 0, ev[0][0]
+    for t, d in ev:
+        if depth > 0:
+            busy += t - last
+        depth += d
+        last = t
+    span = ev[-1][0] - ev[0][0]
+    print(f"\nlibrary kernels running during {busy / 1e6:.3f} ms of the {span / 1e6:.3f} ms traced "
+          f"({100 * busy / span:.1f}%)")
+
+
 def main(argv=None):
     ap = argparse.ArgumentParser(description=__doc__,
                                  formatter_class=argparse.RawDescriptionHelpFormatter)
@@ -339,8 +378,12 @@ def main(argv=None):
     m.add_argument("stats_dir")
     m.add_argument("--workload", required=True)
     m.add_argument("--alpha", type=float, required=True)
+    g = sub.add_parser("gaps")
+    g.add_argument("dir")
+    g.add_argument("--split-us", type=float, default=200.0,
+                   help="gaps longer than this separate steps and are not counted")
     args = ap.parse_args(argv)
-    {"stats": cmd_stats, "traffic": cmd_traffic, "mfma": cmd_mfma}[args.cmd](args)
+    {"stats": cmd_stats, "traffic": cmd_traffic, "mfma": cmd_mfma, "gaps": cmd_gaps}[args.cmd](args)
 
 
 if __name__ == "__main__":

@@ -94,6 +94,29 @@ def test_mfma_summary_from_counter_csv(tmp_path, capsys):
     assert abs(float(kv["frac_of_peak"]) - 0.2) < 1e-9
 
 
+
+def test_launch_gaps_from_kernel_trace(tmp_path, capsys):
+    """profsum gaps: per-stream idle time between consecutive library kernels
+    (other kernels ignored, gaps past the step split left out) and the share
+    of the span some library kernel ran."""
+    k = "void dion2::(anonymous namespace)::gemm<3, 0, Tile<3, 0, 128, 128, 32, 4, 2, 2, false>, true>(dion2::GemmArgs)"
+    other = "void at::native::vectorized_elementwise_kernel<4>(int)"
+    rows = ['"Stream_Id","Kernel_Name","Start_Timestamp","End_Timestamp"']
+    # stream 1: kernels at [0,10) [12,20) [20,30) (us) then one after a 1 ms step break
+    for a, b in ((0, 10), (12, 20), (20, 30), (1030, 1040)):
+        rows.append(f'1,"{k}",{a * 1000},{b * 1000}')
+    rows.append(f'2,"{k}",{5 * 1000},{15 * 1000}')
+    rows.append(f'1,"{other}",{10 * 1000},{12 * 1000}')
+    (tmp_path / "run_kernel_trace.csv").write_text("\n".join(rows) + "\n")
+    profsum.main(["gaps", str(tmp_path)])
+    out = capsys.readouterr().out.splitlines()
+    s1 = [ln.split() for ln in out if ln.split()[:1] == ["1"]][0]
+    assert s1[1:3] == ["4", "2"]                   # 4 kernels, 2 gaps under the split
+    assert float(s1[4]) == 1.0                     # mean of 2 us and 0 us
+    assert float(s1[6]) == 0.002                   # 2 us in total
+    # busy: [0,30) and [1030,1040) -> 40 us of a 1040 us span
+    assert "0.040 ms of the 1.040 ms traced" in out[-1]
+
 def test_bench_refuses_more_than_one_gpu():
     r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", "2"],
                        capture_output=True, text=True, timeout=300)
