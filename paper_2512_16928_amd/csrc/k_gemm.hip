@@ -700,17 +700,17 @@ bool big_sym(const GemmArgs& a) {
 
 hipError_t launch_gemm(const GemmArgs& a, GemmEpi epi, int npass, hipStream_t s) {
     // Tile choices measured on MI355X at the Newton-Schulz shapes. The Gram
-    // matrix reads Z with BK = 64, so each row of a K-slice is one whole
-    // 128-byte line (64-byte rows halve what the L2 delivers per request),
-    // two blocks of eight waves per CU (a third stage, one block per CU, is
-    // faster alone but slows the step, whose groups run side by side); from
-    // s = 1024 it runs on 256 x 256 tiles.
+    // matrix keeps four stages of 32-deep slices on 128 x 128 tiles, two
+    // blocks of four waves per CU (64-deep slices fetch whole 128-byte lines
+    // per row, but either cost blocks per CU, which slows the step whose
+    // groups run side by side, or a stage in flight); from s = 1024 it runs
+    // on 256 x 256 tiles.
     // The three-pass s x s products keep 128 x 128 tiles, two blocks per CU,
     // except large launches of the plain (hi / lo) products, which run on
     // 256 x 256. The X-side products use a two-stage ring, which leaves
     // room for three blocks per CU; with the update applied in the
     // epilogue eight waves per block hide more of the W traffic.
-    using TG = Tile<1, 0, 128, 128, 64, 4, 2, 2>;    // Gram
+    using TG = Tile<1, 0, 128, 128, 32, 2, 2, 4>;    // Gram
     using TGL = Tile<1, 0, 256, 256, 32, 4, 2, 3>;   // Gram, large s
     using TP = Tile<3, 0, 128, 128, 32, 4, 2, 2>;    // three-pass symmetric products
     using TPL = Tile<3, 0, 256, 256, 32, 2, 4, 2>;   // three-pass symmetric products, large s
