@@ -793,6 +793,19 @@ def test_7b_square_muon(hip_device):
     check_matrix(res, 0, 1.0)
 
 
+@pytest.mark.parametrize("gi", [1, 2], ids=["11008x4096", "4096x11008"])
+def test_7b_tall_wide_muon(hip_device, gi):
+    """alpha = 1 on one matrix of each non-square 7B group: every one of the
+    4096 short-side lines is selected, so the orthogonalised block is the whole
+    4096 x 11008 (or 11008 x 4096) momentum, the largest Newton-Schulz product
+    the 7B stack runs."""
+    wl = workloads.WORKLOADS["7b"]
+    W, M, G = workloads.make_group(wl, gi, hip_device, first=9, count=1)
+    res = run_gpu(W, M, G, 1.0)
+    assert res["k"] == 4096
+    check_matrix(res, 0, 1.0)
+
+
 @pytest.mark.parametrize("gi", [0, 1], ids=["2048x1408", "1408x2048"])
 @pytest.mark.parametrize("m0_zero", [True, False], ids=["m0-zero", "m0-drawn"])
 def test_moe_experts_with_zero_gradients(hip_device, gi, m0_zero):
