@@ -32,8 +32,11 @@
  *     bf16 and every product runs on bf16 MFMA operands with fp32
  *     accumulation. Two evaluation orders give the same result in exact
  *     arithmetic (dion2_options.ns_form):
- *       DIRECT  the steps as written, X kept in bf16 between steps, A^2 from
- *               a three-pass bf16 hi/lo split of A;
+ *       DIRECT  the steps as written, X kept in bf16 between steps, A kept
+ *               in fp16 with a power-of-two scale bounded from the
+ *               coefficients (fp16 MFMA, one pass for A^2), or, for
+ *               coefficients that take A beyond fp16's range, as a bf16
+ *               hi/lo pair with three passes for A^2;
  *       GRAM    the iteration carried on s x s matrices: with
  *               Q_t = a I + b A_t + c A_t^2 one has X_{t+1} = Q_t X_t and
  *               A_{t+1} = Q_t A_t Q_t, so X_T = (Q_{T-1} ... Q_0) X_0, and X
@@ -343,8 +346,9 @@ int dion2_plan_info(int64_t rows, int64_t cols, float alpha, int axis,
  *     read and the selected lines of W read and written (rows), or W read
  *     and written whole (columns). Newton-Schulz: each product's distinct
  *     operands read and its result written (the Gram matrix: X in, A hi/lo
- *     out; an s x s product: two hi/lo operands in, one out; the final
- *     product: X in, O (or W's selected lines, read and written) out).
+ *     or fp16 out; an s x s product: two hi/lo or fp16 operands in, one
+ *     out; the final product: X in, O (or W's selected lines, read and
+ *     written) out).
  *   flops: MFMA flops of the Newton-Schulz GEMMs, every bf16 hi/lo pass
  *     included, a product with a symmetric result counted at s (s + 1) per
  *     inner index (the half it computes) instead of 2 s^2: the Gram matrix
@@ -357,7 +361,7 @@ typedef enum dion2_phase {
     DION2_PHASE_MOMENTUM = 0,  /* K1: M += G and line norms         */
     DION2_PHASE_SELECT = 1,    /* K2: top-k selection               */
     DION2_PHASE_GATHER = 2,    /* K3: compact gather + decay        */
-    DION2_PHASE_NS_GRAM = 3,   /* K4: A = X X^T (hi/lo split)       */
+    DION2_PHASE_NS_GRAM = 3,   /* K4: A = X X^T (hi/lo or fp16)     */
     DION2_PHASE_NS_POLY = 4,   /* K4: the s x s products            */
     DION2_PHASE_NS_UPDATE = 5, /* K4: X <- a X + B X, or O = P X_0  */
     DION2_PHASE_APPLY = 6,     /* K5: scatter-apply into W          */

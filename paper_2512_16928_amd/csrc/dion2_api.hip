@@ -344,6 +344,43 @@ bool chain_bounds(const float* coeffs, int ns_steps, ChainFmt* f) {
     return expo(mA, &f->eA) && expo(mQ, &f->eQ) && expo(mT, &f->eT) && expo(mP, &f->eP);
 }
 
+// The DIRECT form keeps A_t = X_t X_t^T in fp16, as fp16(2^e A_t). A_t is
+// positive semidefinite, so its entries are bounded by its largest
+// eigenvalue x_t, the squared largest singular value of X_t; that follows
+// x_{t+1} = x_t q_t(x_t)^2 from x_0 in [0, 1.0625] (X_0 is the bf16 rounding
+// of a matrix of unit Frobenius norm). e puts the bound of every A_t at or
+// below 2^14, a quarter of fp16's largest value, which leaves room for
+// rounding; A_t^2 then accumulates in fp32 at scale 2^(2e). false when the
+// coefficients take the bound beyond 2^40: the form then keeps A as a bf16
+// hi / lo pair with three passes for A^2.
+bool direct_a_exp_scan(const float* coeffs, int ns_steps, int* e) {
+    double mA = 1.0625;
+    constexpr int kGrid = 2048;
+    for (int i = 0; i <= kGrid; ++i) {
+        double x = 1.0625 * i / kGrid;
+        for (int t = 0; t + 1 < ns_steps; ++t) {
+            const float* cf = coeffs ? coeffs + 3 * t : kMuonQuintic;
+            const double q = (double)cf[0] + (double)cf[1] * x + (double)cf[2] * x * x;
+            x *= q * q;
+            mA = std::fmax(mA, std::fabs(x));
+        }
+    }
+    if (!std::isfinite(mA) || mA > 0x1p40) return false;
+    *e = (int)std::floor(std::log2(16384.0 / mA));
+    return true;
+}
+
+bool direct_a_exp(const float* coeffs, int ns_steps, int* e) {
+    if (coeffs) return direct_a_exp_scan(coeffs, ns_steps, e);
+    static const std::vector<int> tab = [] {
+        std::vector<int> v(DION2_MAX_NS_STEPS + 1, 0);
+        for (int n = 0; n <= DION2_MAX_NS_STEPS; ++n) direct_a_exp_scan(nullptr, n, &v[n]);
+        return v;
+    }();
+    *e = tab[ns_steps];
+    return true;
+}
+
 // dion2_options.ns_chain resolved for a call: fp16 for chains of two or more
 // steps when asked for.
 int chain_format(const dion2_options& opt, int ns_steps, ChainFmt* f) {
@@ -458,21 +495,26 @@ GemmEpi final_output(const Plan& P, GemmArgs& x, float* O, const FinalSpec& f) {
     return EPI_FINAL;
 }
 
-// DIRECT: per step A = Z Z^T (hi / lo), B = b A + c A^2, Z <- a Z + B Z.
+// DIRECT: per step A = Z Z^T (fp16, scaled by 2^eA; or a bf16 hi / lo pair
+// when the coefficients leave fp16's range), B = b A + c A^2, Z <- a Z + B Z.
 hipError_t ns_direct(const Plan& P, uint16_t* Z0, uint16_t* Z1, uint16_t* const* sq, float* O,
                      int ns_steps, const dion2_options& opt, const FinalSpec& fin, hipStream_t stream) {
     const double s_r = (double)(P.k < P.d_oth ? P.k : P.d_oth);   // unpadded sides
     const double l_r = (double)(P.k < P.d_oth ? P.d_oth : P.k);
     const double nb = (double)P.batch;
-    const double gram_bytes = (2.0 * s_r * l_r + 4.0 * s_r * s_r) * nb;   // Z in, A hi + lo out
+    int eA = 0;
+    const bool a16 = direct_a_exp(opt.ns_coeffs, ns_steps, &eA);
+    // Z in, A out (fp16, or hi + lo)
+    const double gram_bytes = (2.0 * s_r * l_r + (a16 ? 2.0 : 4.0) * s_r * s_r) * nb;
     uint16_t* zbuf[2] = {Z0, Z1};
     int cur = 0;
     for (int t = 0; t < ns_steps; ++t) {
         const float* cf = opt.ns_coeffs ? opt.ns_coeffs + 3 * t : kMuonQuintic;
         uint16_t* Z = zbuf[cur];
-        GemmArgs g = gram_args(P, Z, sq[SQ_AHI], sq[SQ_ALO]);
+        GemmArgs g = gram_args(P, Z, sq[SQ_AHI], a16 ? nullptr : sq[SQ_ALO]);
+        if (a16) g.oexp = eA;
         hipError_t e = timed(DION2_PHASE_NS_GRAM, sym_flops(s_r, l_r) * nb, gram_bytes, 1, stream,
-                             [&] { return launch_gemm(g, EPI_SPLIT, 1, stream); });
+                             [&] { return launch_gemm(g, a16 ? EPI_H16 : EPI_SPLIT, 1, stream); });
         if (e != hipSuccess) return e;
 
         GemmArgs q = sym3_args(P, sq[SQ_AHI], sq[SQ_ALO], sq[SQ_AHI], sq[SQ_ALO], sq[SQ_B], nullptr);
@@ -482,8 +524,18 @@ hipError_t ns_direct(const Plan& P, uint16_t* Z0, uint16_t* Z1, uint16_t* const*
         q.E1 = sq[SQ_ALO];
         q.sE = P.s_pad * P.s_pad;
         q.lde = (int)P.s_pad;
-        e = timed(DION2_PHASE_NS_POLY, 3.0 * sym_flops(s_r, s_r) * nb, 6.0 * s_r * s_r * nb, 1, stream,
-                  [&] { return launch_gemm(q, EPI_POLY, 3, stream); });
+        if (a16) {
+            // one fp16 pass: C = 2^(2 eA) A^2, E0 = 2^eA A
+            q.A1 = q.B1 = q.E1 = nullptr;
+            q.f16 = 1;
+            q.oexp = -2 * eA;
+            q.eexp = -eA;
+            e = timed(DION2_PHASE_NS_POLY, sym_flops(s_r, s_r) * nb, 4.0 * s_r * s_r * nb, 1, stream,
+                      [&] { return launch_gemm(q, EPI_POLY_H16, 1, stream); });
+        } else {
+            e = timed(DION2_PHASE_NS_POLY, 3.0 * sym_flops(s_r, s_r) * nb, 6.0 * s_r * s_r * nb, 1, stream,
+                      [&] { return launch_gemm(q, EPI_POLY, 3, stream); });
+        }
         if (e != hipSuccess) return e;
 
         // Z' = a Z + B Z (a Z added in the epilogue)

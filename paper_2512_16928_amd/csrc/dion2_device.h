@@ -252,13 +252,16 @@ hipError_t launch_copy_compact(const CompactCopyArgs& a, hipStream_t s);
 //   EPI_H16    (B as rows [N][K], symmetric C; npass 1): out0 = fp16(2^oexp C)
 //   EPI_QPOLY_H16 (B as rows [N][K], npass 1, fp16 operands and E0):
 //              Q = ca I + cb 2^eexp E0 + cc 2^oexp C, out0 = fp16(2^sexp Q)
+//   EPI_POLY_H16 (B as rows [N][K], npass 1, fp16 operands and E0):
+//              out0 = bf16(cb 2^eexp E0 + cc 2^oexp C)
 // With f16 set the operands are fp16 (one pass); EPI_SPLIT then stores
 // 2^oexp C as the hi / lo pair. The power-of-two exponents keep the fp16
 // values of the Gram-form chain clear of fp16's overflow and subnormal range.
 // The symmetric products (EPI_SPLIT, EPI_POLY, EPI_QPOLY, EPI_H16,
-// EPI_QPOLY_H16) compute the tiles on and above the diagonal and mirror them.
+// EPI_QPOLY_H16, EPI_POLY_H16) compute the tiles on and above the diagonal
+// and mirror them.
 enum GemmEpi { EPI_SPLIT = 0, EPI_POLY = 1, EPI_UPDATE = 2, EPI_FINAL = 3, EPI_QPOLY = 4,
-               EPI_APPLY = 5, EPI_H16 = 6, EPI_QPOLY_H16 = 7 };
+               EPI_APPLY = 5, EPI_H16 = 6, EPI_QPOLY_H16 = 7, EPI_POLY_H16 = 8 };
 struct GemmArgs {
     const uint16_t* A0; const uint16_t* A1;   // A operand(s), [M][K] ld lda
     const uint16_t* B0; const uint16_t* B1;   // B operand(s), [N][K] or [K][N], ld ldb

@@ -1,9 +1,8 @@
 // K4: the Newton-Schulz GEMMs on MFMA (bf16 operands, fp32 accumulation).
 //
 // One Newton-Schulz step on the wide compact matrix Z (s x l, s <= l) is
-//   A  = Z Z^T                     gemm<1, EPI_SPLIT>, B as rows  A kept as bf16 hi + lo
-//   B  = b A + c A^2               gemm<3, EPI_POLY>, B as rows   A^2 = A A^T from three
-//                                                                 passes hi*hi+hi*lo+lo*hi
+//   A  = Z Z^T                     gemm<1, EPI_H16>, B as rows    A kept as fp16 (scaled)
+//   B  = b A + c A^2               gemm<1, EPI_POLY_H16>, B as rows  A^2 = A A^T, one fp16 pass
 //   Z' = a Z + B Z                 gemm<1, EPI_UPDATE | EPI_FINAL>, B operand = Z as [K][N]
 // The a Z term is added in fp32 in the epilogue rather than folded into the
 // diagonal of B: with it separate, lines of Z that are exactly equal stay
@@ -406,7 +405,7 @@ __global__ __launch_bounds__(T::THREADS) void gemm(GemmArgs a) {
     const int er = lane >> 1;          // epilogue: row (or transposed row) of this lane
     const int ec = (lane & 1) * 16;    // epilogue: 16 consecutive columns
     constexpr bool kPreE0 = EPI == EPI_POLY || EPI == EPI_QPOLY || EPI == EPI_UPDATE || EPI == EPI_FINAL ||
-                            EPI == EPI_APPLY || EPI == EPI_QPOLY_H16;
+                            EPI == EPI_APPLY || EPI == EPI_QPOLY_H16 || EPI == EPI_POLY_H16;
     constexpr bool kPreE1 = EPI == EPI_POLY || EPI == EPI_QPOLY;
     const bool pre = kPreE0 && a.E0 != nullptr && !(EPI == EPI_FINAL && a.out_transposed);
     uint4 e0[T::FM][T::FN][2], e1[T::FM][T::FN][2];
@@ -568,11 +567,10 @@ __global__ __launch_bounds__(T::THREADS) void gemm(GemmArgs a) {
                             if (er == ec + q) v[q] += a.ca;
                     }
                 }
-            } else if constexpr (EPI == EPI_QPOLY_H16) {
-                // Q = a I + b A + c A^2 from the fp16 A (scale 2^-eexp back
-                // to A), stored as fp16(2^sexp Q)
+            } else if constexpr (EPI == EPI_QPOLY_H16 || EPI == EPI_POLY_H16) {
+                // b A + c A^2 from the fp16 A (scale 2^eexp back to A); the
+                // chain's Q adds a I and is stored as fp16(2^sexp Q)
                 const float esc = __builtin_amdgcn_ldexpf(1.0f, a.eexp);
-                const float ssc = __builtin_amdgcn_ldexpf(1.0f, a.sexp);
                 const uint4 h0 = e0[i][j][0];
                 const uint4 h1 = e0[i][j][1];
                 const uint32_t hw[8] = {h0.x, h0.y, h0.z, h0.w, h1.x, h1.y, h1.z, h1.w};
@@ -581,13 +579,16 @@ __global__ __launch_bounds__(T::THREADS) void gemm(GemmArgs a) {
                     v[2 * q] = a.cb * (esc * f16_bits_to_f32(hw[q] & 0xffffu)) + a.cc * v[2 * q];
                     v[2 * q + 1] = a.cb * (esc * f16_bits_to_f32(hw[q] >> 16)) + a.cc * v[2 * q + 1];
                 }
-                if (R == Cc) {
+                if constexpr (EPI == EPI_QPOLY_H16) {
+                    const float ssc = __builtin_amdgcn_ldexpf(1.0f, a.sexp);
+                    if (R == Cc) {
 #pragma unroll
-                    for (int q = 0; q < 16; ++q)
-                        if (er == ec + q) v[q] += a.ca;
+                        for (int q = 0; q < 16; ++q)
+                            if (er == ec + q) v[q] += a.ca;
+                    }
+#pragma unroll
+                    for (int q = 0; q < 16; ++q) v[q] *= ssc;
                 }
-#pragma unroll
-                for (int q = 0; q < 16; ++q) v[q] *= ssc;
             }
             if constexpr (EPI == EPI_APPLY) {
                 // W[K[p]][j] <- bf16(W[K[p]][j] - lr_eff O[p][j]) (update step, eq. (1))
@@ -729,6 +730,9 @@ hipError_t launch_gemm(const GemmArgs& a, GemmEpi epi, int npass, hipStream_t s)
             case EPI_QPOLY_H16:
                 if (a.dual) break;
                 return launch_tile<1, EPI_QPOLY_H16, TH, true>(a, s);
+            case EPI_POLY_H16:   // the Direct form's B = b A + c A^2
+                if (a.dual) break;
+                return launch_tile<1, EPI_POLY_H16, TH, true>(a, s);
             default: break;
         }
         return hipErrorInvalidValue;

@@ -97,7 +97,10 @@ def phase_of(kernel: str):
         npass, epi = int(m.group(1)), int(m.group(2))
         if epi in (2, 3, 5):         # update / final product with X (5: with the update step)
             return "ns_update"
-        if epi == 0 and npass == 1:  # X X^T
+        # X X^T: one pass on bf16 operands, stored as a hi / lo pair (0) or in
+        # fp16 (6); the same epilogues on fp16 operands are s x s products
+        f16_tile = re.search(r"Tile<[^>]*\btrue>", k) is not None
+        if epi in (0, 6) and npass == 1 and not f16_tile:
             return "ns_gram"
         return "ns_poly"             # the s x s products
     return None

@@ -21,6 +21,10 @@ def test_phase_of_kernel_names():
         "void dion2::(anonymous namespace)::gemm<3, 0, dion2::(anonymous namespace)::Tile<3, 0, 128, 128, 32, 4, 2, 2>, true>(dion2::GemmArgs)": "ns_poly",
         "void dion2::(anonymous namespace)::gemm<3, 4, dion2::(anonymous namespace)::Tile<3, 0, 128, 128, 32, 4, 2, 2>, true>(dion2::GemmArgs)": "ns_poly",
         "void dion2::(anonymous namespace)::gemm<3, 1, dion2::(anonymous namespace)::Tile<3, 0, 128, 128, 32, 4, 2, 2>, true>(dion2::GemmArgs)": "ns_poly",
+        "void dion2::(anonymous namespace)::gemm<1, 6, dion2::(anonymous namespace)::Tile<1, 0, 256, 256, 32, 4, 2, 3, false>, true>(dion2::GemmArgs)": "ns_gram",
+        "void dion2::(anonymous namespace)::gemm<1, 6, dion2::(anonymous namespace)::Tile<1, 0, 128, 128, 32, 2, 2, 4, true>, true>(dion2::GemmArgs)": "ns_poly",
+        "void dion2::(anonymous namespace)::gemm<1, 0, dion2::(anonymous namespace)::Tile<1, 0, 128, 128, 32, 2, 2, 4, true>, true>(dion2::GemmArgs)": "ns_poly",
+        "void dion2::(anonymous namespace)::gemm<1, 8, dion2::(anonymous namespace)::Tile<1, 0, 128, 128, 32, 2, 2, 4, true>, true>(dion2::GemmArgs)": "ns_poly",
         "void dion2::(anonymous namespace)::gemm<1, 2, dion2::(anonymous namespace)::Tile<1, 1, 128, 128, 32, 2, 2, 2>, false>(dion2::GemmArgs)": "ns_update",
         "void dion2::(anonymous namespace)::gemm<2, 3, dion2::(anonymous namespace)::Tile<2, 1, 128, 128, 32, 2, 2, 2>, false>(dion2::GemmArgs)": "ns_update",
         "void dion2::(anonymous namespace)::gemm<2, 5, dion2::(anonymous namespace)::Tile<2, 1, 128, 128, 32, 2, 2, 2>, false>(dion2::GemmArgs)": "ns_update",
