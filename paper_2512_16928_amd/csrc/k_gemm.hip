@@ -706,6 +706,9 @@ hipError_t launch_gemm(const GemmArgs& a, GemmEpi epi, int npass, hipStream_t s)
     // per row, but either cost blocks per CU, which slows the step whose
     // groups run side by side, or a stage in flight); from s = 1024 it runs
     // on 256 x 256 tiles.
+    // The fp16 s x s products (one pass) run on 128 x 128 tiles of four
+    // waves, and from s = 2048 on 256 x 256 tiles of eight (12% faster at
+    // s = 2048, 24% at 4096; 13% slower at 1024).
     // The three-pass s x s products keep 128 x 128 tiles, two blocks per CU,
     // except large launches of the plain (hi / lo) products, which run on
     // 256 x 256. The X-side products use a two-stage ring, which leaves
@@ -720,19 +723,22 @@ hipError_t launch_gemm(const GemmArgs& a, GemmEpi epi, int npass, hipStream_t s)
     using TU2A = Tile<2, 1, 128, 128, 32, 4, 2, 2>;  // two-pass final product applying the update
     using TU3 = Tile<3, 1, 128, 128, 32, 2, 2, 2>;   // three-pass final product (fp32 master)
     using TH = Tile<1, 0, 128, 128, 32, 2, 2, 4, true>;   // fp16 s x s products
+    using THL = Tile<1, 0, 256, 256, 32, 4, 2, 3, true>;  // fp16 s x s products from s = 2048
     if (a.f16) {
         if (npass != 1) return hipErrorInvalidValue;
+        const bool big = a.M >= 2048 && a.M % 256 == 0;
+        if (a.dual && epi != EPI_H16) return hipErrorInvalidValue;   // the chain's P and T
         switch (epi) {
             case EPI_SPLIT:
-                if (a.dual) break;
-                return launch_tile<1, EPI_SPLIT, TH, true>(a, s);
-            case EPI_H16: return launch_tile<1, EPI_H16, TH, true>(a, s);
+                return big ? launch_tile<1, EPI_SPLIT, THL, true>(a, s) : launch_tile<1, EPI_SPLIT, TH, true>(a, s);
+            case EPI_H16:
+                return big ? launch_tile<1, EPI_H16, THL, true>(a, s) : launch_tile<1, EPI_H16, TH, true>(a, s);
             case EPI_QPOLY_H16:
-                if (a.dual) break;
-                return launch_tile<1, EPI_QPOLY_H16, TH, true>(a, s);
+                return big ? launch_tile<1, EPI_QPOLY_H16, THL, true>(a, s)
+                           : launch_tile<1, EPI_QPOLY_H16, TH, true>(a, s);
             case EPI_POLY_H16:   // the Direct form's B = b A + c A^2
-                if (a.dual) break;
-                return launch_tile<1, EPI_POLY_H16, TH, true>(a, s);
+                return big ? launch_tile<1, EPI_POLY_H16, THL, true>(a, s)
+                           : launch_tile<1, EPI_POLY_H16, TH, true>(a, s);
             default: break;
         }
         return hipErrorInvalidValue;
