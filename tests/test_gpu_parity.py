@@ -174,6 +174,22 @@ def test_ns_schedules(hip_device, ns_steps, coeffs, form, rows, cols):
     check_matrix(res, 0, 0.5, ns_steps=ns_steps, coeffs=coeffs)
 
 
+@pytest.mark.parametrize("grow", [10, 21], ids=["fp16-scaled-down", "hilo-fallback"])
+def test_direct_a_range(hip_device, grow):
+    """The DIRECT form keeps A = X X^T in fp16 with a power-of-two scale bounded
+    from the coefficients. A first step X <- 2^g X followed by a quintic step
+    with b and c rescaled by 2^-2g and 2^-4g gives 2^g times one ordinary
+    step. g = 10 puts A near 2^20 (stored scaled down by 2^-7); g = 21 takes A
+    past the 2^40 that the fp16 path accepts, so A stays a bf16 hi/lo pair and
+    A^2 takes three passes. Both match the oracle."""
+    g = float(2 ** grow)
+    coeffs = [(g, 0.0, 0.0), (3.4445, -4.7750 / g ** 2, 2.0315 / g ** 4)]
+    wl = one_group_workload(160, 384, name=f"arange{grow}")
+    W, M, G = workloads.make_group(wl, 0, hip_device)
+    res = run_gpu(W, M, G, 1.0, ns_steps=2, coeffs=coeffs, form=NS_DIRECT)
+    check_matrix(res, 0, 1.0, ns_steps=2, coeffs=coeffs)
+
+
 @pytest.mark.parametrize("ns_steps,coeffs", [
     (2, None), (3, [(1.5, -0.5, 0.0)] * 3),
     (4, [(3.0, -3.2, 1.2), (2.0, -1.5, 0.5), (1.5, -0.5, 0.0), (1.5, -0.5, 0.0)]),
