@@ -216,17 +216,22 @@ def test_f16_chain_of_one_step_is_hilo(hip_device):
     assert torch.equal(W.view(torch.int16), W2.view(torch.int16)) and torch.equal(M, M2)
 
 
-@pytest.mark.parametrize("wl_name,gi,first,alpha", [
-    ("1b", 0, 9, 0.25),          # 2048x2048: s = 512, l = 2048
-    ("1b", 1, 4, 0.25),          # 8192x2048, columns: s = 512, l = 8192
-    ("1b-colsel", 2, 3, 0.25),   # 5% of the columns with x20 gradients
-    ("moe", 0, 70, 0.25),        # 2048x1408 expert: s = 352 padded to 384
+@pytest.mark.parametrize("wl_name,gi,first,alpha,ratio", [
+    ("1b", 0, 9, 0.25, 2.0),          # 2048x2048: s = 512, l = 2048
+    ("1b", 1, 4, 0.25, 2.0),          # 8192x2048, columns: s = 512, l = 8192
+    ("1b-colsel", 2, 3, 0.25, 2.0),   # 5% of the columns with x20 gradients
+    ("moe", 0, 70, 0.25, 2.0),        # 2048x1408 expert: s = 352 padded to 384
+    ("1b", 2, 4, 0.5, 2.0),           # 2048x8192, rows: s = 1024, l = 8192
+    ("1b", 1, 6, 1.0, 4.0),           # 8192x2048, columns: s = 2048 (256 x 256 fp16 tiles)
 ])
-def test_gram_chain_storage(hip_device, wl_name, gi, first, alpha):
+def test_gram_chain_storage(hip_device, wl_name, gi, first, alpha, ratio):
     """Both storages of the GRAM chain against the oracle on one matrix of a
     benchmark shape. The fp16 chain keeps 11 significant bits where the hi/lo
     pairs keep about 16; on these wide, balanced matrices Z's own bf16
-    rounding dominates both, and fp16 stays within twice the hi/lo error."""
+    rounding dominates both, and fp16 stays within twice the hi/lo error. At
+    alpha = 1 the compact matrix is the whole momentum (smallest singular
+    value 4.6e-3 of X / ||X||_F): fp16 measures 7.5e-3 against 2.3e-3 for
+    hi/lo, still inside the 2e-2 bound that check_matrix applies."""
     wl = workloads.WORKLOADS[wl_name]
     grp = wl.groups[gi]
     W, M, G = workloads.make_group(wl, gi, hip_device, first=first, count=1)
@@ -234,7 +239,7 @@ def test_gram_chain_storage(hip_device, wl_name, gi, first, alpha):
     for chain in (binding.CHAIN_HILO, binding.CHAIN_F16):
         res = run_gpu(W.clone(), M.clone(), G, alpha, axis=grp.axis, form=NS_GRAM, chain=chain)
         errs[chain] = check_matrix(res, 0, alpha, axis=grp.axis)
-    assert errs[binding.CHAIN_F16] <= 2.0 * errs[binding.CHAIN_HILO] + 1e-3, errs
+    assert errs[binding.CHAIN_F16] <= ratio * errs[binding.CHAIN_HILO] + 1e-3, errs
 
 
 @pytest.mark.parametrize("rows,cols,alpha,axis", [
