@@ -61,8 +61,9 @@ struct Plan {
     int nrb, rb_rows;         // column-mode reduction blocking
     bool gram;                // Newton-Schulz on s x s matrices (DION2_NS_GRAM)
     bool master;              // X kept as a hi / lo pair (DION2_MASTER_FP32; implies gram)
+    bool xrows;               // DIRECT from s = 2048: X also kept as X^T for the update's B operand
     // workspace offsets
-    size_t o_l1, o_sq, o_part, o_sel, o_rank, o_scale, o_Z, o_Z1, o_S, S_bytes, o_O, o_tables, total;
+    size_t o_l1, o_sq, o_part, o_sel, o_rank, o_scale, o_Z, o_Z1, o_ZT, o_S, S_bytes, o_O, o_tables, total;
 };
 
 // s x s buffers of the two Newton-Schulz forms (bf16 [batch][s_pad][s_pad])
@@ -124,6 +125,9 @@ int make_plan(int batch, int64_t rows, int64_t cols, float alpha, int axis, int 
     // the fp32 master runs in the GRAM order (its caller rejects a forced DIRECT)
     P.master = master;
     if (master) P.gram = true;
+    // DIRECT's update B X on the plain-read 256-row tiles needs X^T as rows;
+    // it pays from s = 2048 (below, the transposes cost more than they save)
+    P.xrows = !P.gram && P.s_pad >= 2048 && P.s_pad % 256 == 0;
     P.batch = batch;
     P.nrb = P.axis == 1 ? (int)momentum_col_blocks(rows, &P.rb_rows) : 0;
     if (P.axis == 0) P.rb_rows = 0;
@@ -144,6 +148,7 @@ int make_plan(int batch, int64_t rows, int64_t cols, float alpha, int axis, int 
     const size_t comp = B * (size_t)P.kpad * (size_t)P.opad * 2;
     P.o_Z = take(comp);
     P.o_Z1 = take(P.gram && !P.master ? 0 : comp);   // DIRECT's ping-pong copy, or the lo half of X
+    P.o_ZT = take(P.xrows ? 2 * comp : 0);            // DIRECT's X^T, ping-pong
     P.S_bytes = align256(B * (size_t)P.s_pad * (size_t)P.s_pad * 2);
     P.o_S = take(own_sq ? P.S_bytes * (P.gram ? SQ_GRAM_COUNT : SQ_DIRECT_COUNT) : 0);
     P.o_O = take(B * (size_t)P.kpad * (size_t)P.opad * 4);
@@ -497,8 +502,11 @@ GemmEpi final_output(const Plan& P, GemmArgs& x, float* O, const FinalSpec& f) {
 
 // DIRECT: per step A = Z Z^T (fp16, scaled by 2^eA; or a bf16 hi / lo pair
 // when the coefficients leave fp16's range), B = b A + c A^2, Z <- a Z + B Z.
-hipError_t ns_direct(const Plan& P, uint16_t* Z0, uint16_t* Z1, uint16_t* const* sq, float* O,
-                     int ns_steps, const dion2_options& opt, const FinalSpec& fin, hipStream_t stream) {
+// With P.xrows the update reads Z^T (ZT[cur]) as rows and writes Z'^T beside
+// Z'; Z_0^T comes from one transpose.
+hipError_t ns_direct(const Plan& P, uint16_t* Z0, uint16_t* Z1, uint16_t* const* ZT, uint16_t* const* sq,
+                     float* O, int ns_steps, const dion2_options& opt, const FinalSpec& fin,
+                     hipStream_t stream) {
     const double s_r = (double)(P.k < P.d_oth ? P.k : P.d_oth);   // unpadded sides
     const double l_r = (double)(P.k < P.d_oth ? P.d_oth : P.k);
     const double nb = (double)P.batch;
@@ -507,6 +515,13 @@ hipError_t ns_direct(const Plan& P, uint16_t* Z0, uint16_t* Z1, uint16_t* const*
     // Z in, A out (fp16, or hi + lo)
     const double gram_bytes = (2.0 * s_r * l_r + (a16 ? 2.0 : 4.0) * s_r * s_r) * nb;
     uint16_t* zbuf[2] = {Z0, Z1};
+    const bool xrows = P.xrows && ns_steps > 0;
+    if (xrows) {
+        hipError_t e = timed(DION2_PHASE_NS_UPDATE, 0.0, 4.0 * s_r * l_r * nb, 1, stream, [&] {
+            return launch_transpose_bf16(Z0, ZT[0], P.s_pad, P.l_pad, P.batch, P.s_pad * P.l_pad, stream);
+        });
+        if (e != hipSuccess) return e;
+    }
     int cur = 0;
     for (int t = 0; t < ns_steps; ++t) {
         const float* cf = opt.ns_coeffs ? opt.ns_coeffs + 3 * t : kMuonQuintic;
@@ -544,16 +559,26 @@ hipError_t ns_direct(const Plan& P, uint16_t* Z0, uint16_t* Z1, uint16_t* const*
         x.E0 = Z;
         x.sE = P.s_pad * P.l_pad;
         x.lde = (int)P.l_pad;
+        if (xrows) {   // Z^T [l_pad][s_pad] as the B operand's rows
+            x.B0 = ZT[cur];
+            x.ldb = (int)P.s_pad;
+            x.b_rows = 1;
+        }
         const bool last = t + 1 == ns_steps;
         GemmEpi epi = EPI_UPDATE;
         if (!last) {
             x.out0 = zbuf[1 - cur];
             x.sOut0 = P.s_pad * P.l_pad;
             x.ldo0 = (int)P.l_pad;
+            if (xrows) {
+                x.out1 = ZT[1 - cur];
+                x.sOut1 = P.s_pad * P.l_pad;
+                x.ldo1 = (int)P.s_pad;
+            }
         } else {
             epi = final_output(P, x, O, fin);
         }
-        const double ubytes = (2.0 * s_r * s_r + (last ? 6.0 : 4.0) * s_r * l_r) * nb;
+        const double ubytes = (2.0 * s_r * s_r + (last ? 6.0 : (xrows ? 6.0 : 4.0)) * s_r * l_r) * nb;
         e = timed(DION2_PHASE_NS_UPDATE, 2.0 * s_r * s_r * l_r * nb, ubytes, 1, stream,
                   [&] { return launch_gemm(x, epi, 1, stream); });
         if (e != hipSuccess) return e;
@@ -777,6 +802,7 @@ struct Bufs {
     double* scale;
     uint16_t* Z0;   // compact matrix in its wide orientation: L [kpad][opad] or L^T [opad][kpad]
     uint16_t* Z1;
+    uint16_t* ZT[2];   // DIRECT with xrows: X^T [l_pad][s_pad], ping-pong
     uint16_t* sbuf[SQ_GRAM_COUNT];   // s x s buffers (null when a shared chain owns them)
     float* O;
     double* part;
@@ -791,6 +817,8 @@ Bufs carve(const Plan& P, char* ws) {
     b.scale = reinterpret_cast<double*>(ws + P.o_scale);
     b.Z0 = reinterpret_cast<uint16_t*>(ws + P.o_Z);
     b.Z1 = reinterpret_cast<uint16_t*>(ws + P.o_Z1);
+    b.ZT[0] = P.xrows ? reinterpret_cast<uint16_t*>(ws + P.o_ZT) : nullptr;
+    b.ZT[1] = P.xrows ? b.ZT[0] + (size_t)P.batch * (size_t)P.s_pad * (size_t)P.l_pad : nullptr;
     for (int i = 0; i < SQ_GRAM_COUNT; ++i)
         b.sbuf[i] = reinterpret_cast<uint16_t*>(ws + P.o_S + (size_t)i * P.S_bytes);
     b.O = reinterpret_cast<float*>(ws + P.o_O);
@@ -1054,7 +1082,7 @@ int run_step(const Plan& P, void* W, float* M, const void* G, const Tables* tabs
     const FinalSpec fin = make_final(P, ms, b, lr, ns_steps, opt);
     if (ns_steps > 0) {   // with no step the gather has written O
         e = P.gram ? ns_gram(P, b.Z0, P.master ? b.Z1 : nullptr, b.sbuf, b.O, ns_steps, opt, fmt, fin, stream)
-                   : ns_direct(P, b.Z0, b.Z1, b.sbuf, b.O, ns_steps, opt, fin, stream);
+                   : ns_direct(P, b.Z0, b.Z1, b.ZT, b.sbuf, b.O, ns_steps, opt, fin, stream);
         if (e != hipSuccess) return hip_fail(e, "launch K4 Newton-Schulz");
     }
     return back(P, ms, b, fin, opt, stream);
@@ -1381,7 +1409,7 @@ int groups_impl(const dion2_group* groups, int ngroups, float alpha, float mu, f
         }
         if (ns_steps > 0) {
             e = P.gram ? ns_gram(P, b.Z0, P.master ? b.Z1 : nullptr, b.sbuf, b.O, ns_steps, gopt[g], fmt, fins[g], s)
-                       : ns_direct(P, b.Z0, b.Z1, b.sbuf, b.O, ns_steps, gopt[g], fins[g], s);
+                       : ns_direct(P, b.Z0, b.Z1, b.ZT, b.sbuf, b.O, ns_steps, gopt[g], fins[g], s);
             if (e != hipSuccess) return hip_fail(e, "launch K4 Newton-Schulz");
         }
         st = back(P, ms, b, fins[g], gopt[g], s);

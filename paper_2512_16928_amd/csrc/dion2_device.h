@@ -242,13 +242,16 @@ hipError_t launch_copy_compact(const CompactCopyArgs& a, hipStream_t s);
 //   EPI_POLY   (B as rows [N][K], npass 3): out0 = bf16(cb (E0 + E1) + cc C)
 //   EPI_QPOLY  (B as rows [N][K], npass 3): Q = ca I + cb (E0 + E1) + cc C,
 //              out0 = bf16(Q), out1 = bf16(Q - out0)
-//   EPI_UPDATE (B as [K][N], npass 1): out0 = bf16(ca E0 + C)
-//   EPI_FINAL  (B as [K][N], npass 1 to 3): out0 = ca E0 + C in fp32 (no
-//              E0 term when E0 is null), or its transpose when out_transposed
-//   EPI_APPLY  (B as [K][N], npass 1 to 3): O = ca E0 + C (row selection, O in
-//              the L layout) is not stored; the update step is applied
-//              directly: W[K[p]][j] <- bf16(W[K[p]][j] - lr_eff O[p][j]) for
-//              p < k, j < d_oth (bf16 W, cols % 8 == 0); dbg gets O if set
+//   EPI_UPDATE (B as [K][N], or as rows with b_rows; npass 1):
+//              out0 = bf16(ca E0 + C), and out1 = its transpose when set
+//   EPI_FINAL  (B as [K][N], npass 1 to 3; as rows with b_rows, npass 1):
+//              out0 = ca E0 + C in fp32 (no E0 term when E0 is null), or its
+//              transpose when out_transposed
+//   EPI_APPLY  (B as [K][N], npass 1 to 3; as rows with b_rows, npass 1):
+//              O = ca E0 + C (row selection, O in the L layout) is not
+//              stored; the update step is applied directly:
+//              W[K[p]][j] <- bf16(W[K[p]][j] - lr_eff O[p][j]) for p < k,
+//              j < d_oth (bf16 W, cols % 8 == 0); dbg gets O if set
 //   EPI_H16    (B as rows [N][K], symmetric C; npass 1): out0 = fp16(2^oexp C)
 //   EPI_QPOLY_H16 (B as rows [N][K], npass 1, fp16 operands and E0):
 //              Q = ca I + cb 2^eexp E0 + cc 2^oexp C, out0 = fp16(2^sexp Q)
@@ -274,6 +277,10 @@ struct GemmArgs {
     void* out0; int64_t sOut0; int ldo0;
     void* out1; int64_t sOut1; int ldo1;
     int out_transposed;                        // EPI_FINAL: write out0[j][i]
+    // X-side products (EPI_UPDATE, EPI_FINAL, EPI_APPLY): the B operand given
+    // as rows [N][K] (X^T) instead of [K][N]; EPI_UPDATE then also writes the
+    // transpose of its output to out1 (ld ldo1) when out1 is set
+    int b_rows;
     // dual launch (EPI_SPLIT npass 3, or EPI_H16): a second product with the
     // same A operand, B = B0x/B1x into out0x/out1x (scale 2^oexpx), computed
     // in the same grid
@@ -292,6 +299,11 @@ struct GemmArgs {
     float* dbg;                                // nullable [batch][k][d_oth]
 };
 hipError_t launch_gemm(const GemmArgs& a, GemmEpi epi, int npass, hipStream_t s);
+
+// out[b][j][i] = in[b][i][j] for bf16 [batch][rows][cols] stacks (both sides
+// multiples of 64; `stride` elements between matrices on both sides).
+hipError_t launch_transpose_bf16(const uint16_t* in, uint16_t* out, int64_t rows, int64_t cols, int batch,
+                                 int64_t stride, hipStream_t s);
 
 struct ApplyArgs {
     MatSet ms;

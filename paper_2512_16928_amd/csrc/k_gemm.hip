@@ -291,8 +291,9 @@ __device__ __forceinline__ void mma_slice(f32x16 (&acc)[T::FM][T::FN], const uns
 // contiguous segments of few cache lines. With TR the tile is read
 // transposed (output row q = tile column q), for the mirrored block; with
 // DIAG (a block on the diagonal of a symmetric product) the entries below
-// the diagonal are taken from their mirror images above it.
-template <int EPI, typename T, bool TR, bool DIAG = false>
+// the diagonal are taken from their mirror images above it. O1 sends a bf16
+// block to out1 instead of out0 (EPI_UPDATE's transposed copy).
+template <int EPI, typename T, bool TR, bool DIAG = false, bool O1 = false>
 __device__ __forceinline__ void store_block(const GemmArgs& a, int b, const float* stage, int64_t orow0,
                                             int64_t ocol0, int lane) {
     auto at = [&](int r, int c) {
@@ -331,6 +332,10 @@ __device__ __forceinline__ void store_block(const GemmArgs& a, int b, const floa
                 uint16_t* op = static_cast<uint16_t*>(a.out0) + (int64_t)b * a.sOut0 + (orow0 + r) * a.ldo0 + ocol0 + c8;
                 *reinterpret_cast<uint4*>(op) = make_uint4(pack2h(v[0], v[1]), pack2h(v[2], v[3]),
                                                            pack2h(v[4], v[5]), pack2h(v[6], v[7]));
+            } else if constexpr (O1) {   // EPI_UPDATE's transposed copy: bf16
+                uint16_t* op = static_cast<uint16_t*>(a.out1) + (int64_t)b * a.sOut1 + (orow0 + r) * a.ldo1 + ocol0 + c8;
+                *reinterpret_cast<uint4*>(op) = make_uint4(pack2(v[0], v[1]), pack2(v[2], v[3]),
+                                                           pack2(v[4], v[5]), pack2(v[6], v[7]));
             } else {   // EPI_POLY, EPI_UPDATE: bf16
                 uint16_t* op = static_cast<uint16_t*>(a.out0) + (int64_t)b * a.sOut0 + (orow0 + r) * a.ldo0 + ocol0 + c8;
                 *reinterpret_cast<uint4*>(op) = make_uint4(pack2(v[0], v[1]), pack2(v[2], v[3]),
@@ -635,6 +640,10 @@ __global__ __launch_bounds__(T::THREADS) void gemm(GemmArgs a) {
                     store_block<EPI, T, false>(a, b, stage, orow - er, ocol - ec, lane);
                     if (SYM) store_block<EPI, T, true>(a, b, stage, (int64_t)Cc, (int64_t)R, lane);
                 }
+                if constexpr (EPI == EPI_UPDATE) {
+                    // X' also as X'^T, the next step's B operand given as rows
+                    if (a.out1) store_block<EPI, T, true, false, true>(a, b, stage, (int64_t)Cc, (int64_t)R, lane);
+                }
             }
             __builtin_amdgcn_wave_barrier();   // the stage tile is rewritten next
         }
@@ -699,6 +708,35 @@ bool big_sym(const GemmArgs& a) {
     return (int64_t)a.batch * (a.dual ? 2 : 1) * (t * (t + 1) / 2) >= 512;
 }
 
+// bf16 transpose through a 64 x 64 LDS tile (row pitch 66 elements, so the
+// column reads spread over the banks): 16-byte row segments in and out.
+__global__ __launch_bounds__(256) void transpose_bf16(const uint16_t* __restrict__ in, uint16_t* __restrict__ out,
+                                                      int64_t rows, int64_t cols, int64_t stride) {
+    __shared__ uint16_t t[64][66];
+    const int64_t b = blockIdx.z;
+    const int64_t r0 = (int64_t)blockIdx.y * 64, c0 = (int64_t)blockIdx.x * 64;
+    const uint16_t* src = in + b * stride + r0 * cols + c0;
+    uint16_t* dst = out + b * stride + c0 * rows + r0;
+    for (int i = threadIdx.x; i < 64 * 8; i += 256) {
+        const int r = i >> 3, c = (i & 7) * 8;
+        const uint4 v = ldg<uint4>(src + (int64_t)r * cols + c);
+        const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            t[r][c + 2 * q] = (uint16_t)(w[q] & 0xffffu);
+            t[r][c + 2 * q + 1] = (uint16_t)(w[q] >> 16);
+        }
+    }
+    __syncthreads();
+    for (int i = threadIdx.x; i < 64 * 8; i += 256) {
+        const int r = i >> 3, c = (i & 7) * 8;   // output row r (input column), input rows c .. c + 7
+        uint32_t w[4];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) w[q] = (uint32_t)t[c + 2 * q][r] | ((uint32_t)t[c + 2 * q + 1][r] << 16);
+        stg(dst + (int64_t)r * rows + c, make_uint4(w[0], w[1], w[2], w[3]));
+    }
+}
+
 hipError_t launch_gemm(const GemmArgs& a, GemmEpi epi, int npass, hipStream_t s) {
     // Tile choices measured on MI355X at the Newton-Schulz shapes. The Gram
     // matrix keeps four stages of 32-deep slices on 128 x 128 tiles, two
@@ -722,6 +760,8 @@ hipError_t launch_gemm(const GemmArgs& a, GemmEpi epi, int npass, hipStream_t s)
     using TU2 = Tile<2, 1, 128, 128, 32, 2, 2, 2>;   // two-pass final product
     using TU2A = Tile<2, 1, 128, 128, 32, 4, 2, 2>;  // two-pass final product applying the update
     using TU3 = Tile<3, 1, 128, 128, 32, 2, 2, 2>;   // three-pass final product (fp32 master)
+    using TR = Tile<1, 0, 256, 256, 32, 2, 4, 3>;    // X-side products, B operand as rows (X^T)
+    using TRN = Tile<1, 0, 256, 128, 32, 4, 2, 4>;   // the same when l is not a multiple of 256
     using TH = Tile<1, 0, 128, 128, 32, 2, 2, 4, true>;   // fp16 s x s products
     using THL = Tile<1, 0, 256, 256, 32, 4, 2, 3, true>;  // fp16 s x s products from s = 2048
     if (a.f16) {
@@ -744,6 +784,24 @@ hipError_t launch_gemm(const GemmArgs& a, GemmEpi epi, int npass, hipStream_t s)
         return hipErrorInvalidValue;
     }
     if (a.dual && !(epi == EPI_SPLIT && npass == 3)) return hipErrorInvalidValue;
+    if (a.b_rows) {
+        // the Direct form's X-side products from s = 2048: X^T as rows lets
+        // them run on the wide plain-read tiles (28% faster at s = 2048, 35%
+        // at 4096 than the transposing reads of the [K][N] operand)
+        if (npass != 1 || a.M % 256) return hipErrorInvalidValue;
+        const bool wide = a.N % 256 == 0;
+        switch (epi) {
+            case EPI_UPDATE:
+                return wide ? launch_tile<1, EPI_UPDATE, TR>(a, s) : launch_tile<1, EPI_UPDATE, TRN>(a, s);
+            case EPI_FINAL:
+                return wide ? launch_tile<1, EPI_FINAL, TR>(a, s) : launch_tile<1, EPI_FINAL, TRN>(a, s);
+            case EPI_APPLY:   // (its W rows spill on 256 x 256)
+                if (a.cols % 8 || a.cols < 16 || a.out_transposed) break;
+                return launch_tile<1, EPI_APPLY, TRN>(a, s);
+            default: break;
+        }
+        return hipErrorInvalidValue;
+    }
     switch (epi) {
         case EPI_SPLIT:
             if (npass == 3) {
@@ -781,6 +839,15 @@ hipError_t launch_gemm(const GemmArgs& a, GemmEpi epi, int npass, hipStream_t s)
             break;
     }
     return hipErrorInvalidValue;
+}
+
+hipError_t launch_transpose_bf16(const uint16_t* in, uint16_t* out, int64_t rows, int64_t cols, int batch,
+                                 int64_t stride, hipStream_t s) {
+    if (rows < 64 || cols < 64 || rows % 64 || cols % 64 || rows / 64 > 65535 || batch < 1 || batch > 65535)
+        return hipErrorInvalidValue;
+    const dim3 grid((unsigned)(cols / 64), (unsigned)(rows / 64), (unsigned)batch);
+    hipLaunchKernelGGL(transpose_bf16, grid, dim3(256), 0, s, in, out, rows, cols, stride);
+    return hipGetLastError();
 }
 
 }  // namespace dion2

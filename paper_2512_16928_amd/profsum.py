@@ -92,6 +92,8 @@ def phase_of(kernel: str):
         return "gather"
     if k.startswith("apply"):
         return "apply"
+    if k.startswith("transpose"):    # X^T for the Direct form's update
+        return "ns_update"
     m = re.match(r"gemm<(\d+), (?:\(dion2::GemmEpi\))?(\d)", k)
     if m:
         npass, epi = int(m.group(1)), int(m.group(2))
