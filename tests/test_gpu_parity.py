@@ -174,6 +174,22 @@ def test_ns_schedules(hip_device, ns_steps, coeffs, form, rows, cols):
     check_matrix(res, 0, 0.5, ns_steps=ns_steps, coeffs=coeffs)
 
 
+@pytest.mark.parametrize("rows,cols,ns_steps", [
+    (2048, 2176, 5),   # rows: l = 2176 (not a multiple of 256), update and fused apply on 256 x 128 tiles
+    (2176, 2048, 5),   # columns: the final product writes O transposed, 256 x 128 tiles
+    (2048, 2048, 1),   # one step: X_0^T straight into the final product
+])
+def test_direct_transposed_operand(hip_device, rows, cols, ns_steps):
+    """From s = 2048 the DIRECT form keeps X^T beside X and runs the update
+    B X with X^T as the B operand's rows (X_0^T from a transpose, later ones
+    written by the update's epilogue)."""
+    wl = one_group_workload(rows, cols, name=f"xrows{rows}c{cols}")
+    W, M, G = workloads.make_group(wl, 0, hip_device)
+    res = run_gpu(W, M, G, 1.0, ns_steps=ns_steps, form=NS_DIRECT)
+    assert res["k"] == 2048
+    check_matrix(res, 0, 1.0, ns_steps=ns_steps)
+
+
 @pytest.mark.parametrize("grow", [10, 21], ids=["fp16-scaled-down", "hilo-fallback"])
 def test_direct_a_range(hip_device, grow):
     """The DIRECT form keeps A = X X^T in fp16 with a power-of-two scale bounded
