@@ -751,7 +751,9 @@ hipError_t launch_gemm(const GemmArgs& a, GemmEpi epi, int npass, hipStream_t s)
     // except large launches of the plain (hi / lo) products, which run on
     // 256 x 256. The X-side products use a two-stage ring, which leaves
     // room for three blocks per CU; with the update applied in the
-    // epilogue eight waves per block hide more of the W traffic.
+    // epilogue eight waves per block hide more of the W traffic. Given X^T
+    // as rows (b_rows) they run on 256 x 256 plain-read tiles, or 256 x 128
+    // where l is not a multiple of 256 and for the fused update step.
     using TG = Tile<1, 0, 128, 128, 32, 2, 2, 4>;    // Gram
     using TGL = Tile<1, 0, 256, 256, 32, 4, 2, 3>;   // Gram, large s
     using TP = Tile<3, 0, 128, 128, 32, 4, 2, 2>;    // three-pass symmetric products
@@ -761,7 +763,7 @@ hipError_t launch_gemm(const GemmArgs& a, GemmEpi epi, int npass, hipStream_t s)
     using TU2A = Tile<2, 1, 128, 128, 32, 4, 2, 2>;  // two-pass final product applying the update
     using TU3 = Tile<3, 1, 128, 128, 32, 2, 2, 2>;   // three-pass final product (fp32 master)
     using TR = Tile<1, 0, 256, 256, 32, 2, 4, 3>;    // X-side products, B operand as rows (X^T)
-    using TRN = Tile<1, 0, 256, 128, 32, 4, 2, 4>;   // the same when l is not a multiple of 256
+    using TRN = Tile<1, 0, 256, 128, 32, 4, 2, 4>;   // the same, l not a multiple of 256; fused update
     using TH = Tile<1, 0, 128, 128, 32, 2, 2, 4, true>;   // fp16 s x s products
     using THL = Tile<1, 0, 256, 256, 32, 4, 2, 3, true>;  // fp16 s x s products from s = 2048
     if (a.f16) {
