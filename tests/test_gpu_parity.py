@@ -946,6 +946,22 @@ def test_groups_equal_per_group_calls(hip_device, rand, gs):
     check_matrix(res, 1, alpha, rand=rand)
 
 
+def test_groups_with_direct_transposed_operand(hip_device):
+    """A grouped call whose first group takes the DIRECT form with X^T kept
+    beside X (2048 x 2048 at alpha = 1) is bitwise the per-group calls."""
+    wl = workloads.Workload("gxr", "test", (workloads.Group("a", 2048, 2048, 2), workloads.Group("b", 256, 384, 3)),
+                            (1.0,))
+    stacks = [workloads.make_group(wl, gi, hip_device) for gi in range(2)]
+    solo = [tuple(t.clone() for t in st) for st in stacks]
+    for W, M, G in solo:
+        binding.dion2_step_ex(W, M, G, 1.0)
+    binding.dion2_step_groups([(W, M, G, AXIS_AUTO) for W, M, G in stacks], 1.0)
+    torch.cuda.synchronize()
+    for gi, ((W, M, _), (Ws, Ms, _)) in enumerate(zip(stacks, solo)):
+        assert torch.equal(M, Ms), f"group {gi}: momentum"
+        assert torch.equal(W.view(torch.int16), Ws.view(torch.int16)), f"group {gi}: weights"
+
+
 def test_groups_single_group_equals_strided(hip_device):
     """One group through the grouped entry point equals dion2_step_strided."""
     wl = one_group_workload(2048, 2048, count=4, name="g1")
