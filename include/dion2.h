@@ -315,8 +315,9 @@ int dion2_step_groups(const dion2_group* groups, int ngroups, float alpha,
 
 /* Bytes of device workspace (for dion2_options.workspace) that suffice for
    a call with these arguments under any options and step count: the
-   largest plan, the GRAM order with DION2_MASTER_FP32. Returns 0 for
-   invalid arguments. */
+   largest of the GRAM order with DION2_MASTER_FP32, and the GRAM and DIRECT
+   orders under the Random rule (whose column selection keeps per-block
+   partial sums). Returns 0 for invalid arguments. */
 size_t dion2_workspace_size(int batch, int64_t rows, int64_t cols,
                             float alpha, int axis);
 

@@ -62,8 +62,10 @@ struct Plan {
     bool gram;                // Newton-Schulz on s x s matrices (DION2_NS_GRAM)
     bool master;              // X kept as a hi / lo pair (DION2_MASTER_FP32; implies gram)
     bool xrows;               // DIRECT from s = 2048: X also kept as X^T for the update's B operand
+    bool colpass;             // columns under the Random rule: one pass over M and G (see front)
     // workspace offsets
-    size_t o_l1, o_sq, o_part, o_sel, o_rank, o_scale, o_Z, o_Z1, o_ZT, o_S, S_bytes, o_O, o_tables, total;
+    size_t o_l1, o_sq, o_part, o_sel, o_rank, o_scale, o_Z, o_Z1, o_ZT, o_sqp, o_S, S_bytes, o_O, o_tables,
+        total;
 };
 
 // s x s buffers of the two Newton-Schulz forms (bf16 [batch][s_pad][s_pad])
@@ -82,7 +84,7 @@ constexpr int kDirectMaxSteps = DION2_DIRECT_MAX_STEPS;
 // own_sq = false leaves out the s x s buffers (a grouped call carves them
 // once for every group of a shared Newton-Schulz chain).
 int make_plan(int batch, int64_t rows, int64_t cols, float alpha, int axis, int ns_form, int ns_steps,
-              Plan* p, bool own_sq = true, bool master = false) {
+              Plan* p, bool own_sq = true, bool master = false, bool random_rule = false) {
     if (batch < 1 || batch > 65535) return fail(DION2_ERR_INVALID_ARG, "batch %d not in [1, 65535]", batch);
     if (rows < 1 || cols < 1)
         return fail(DION2_ERR_INVALID_ARG, "rows (%lld) and cols (%lld) must be >= 1",
@@ -128,6 +130,10 @@ int make_plan(int batch, int64_t rows, int64_t cols, float alpha, int axis, int 
     // DIRECT's update B X on the plain-read 256-row tiles needs X^T as rows;
     // it pays from s = 2048 (below, the transposes cost more than they save)
     P.xrows = !P.gram && P.s_pad >= 2048 && P.s_pad % 256 == 0;
+    // The Random rule draws K before M is read, so column selection can form
+    // M + G, decay and gather in one pass instead of a norm pass and a second
+    // read; the compact matrix is normalised once every row is in.
+    P.colpass = random_rule && P.axis == 1 && !P.master && ns_steps > 0;
     P.batch = batch;
     P.nrb = P.axis == 1 ? (int)momentum_col_blocks(rows, &P.rb_rows) : 0;
     if (P.axis == 0) P.rb_rows = 0;
@@ -149,6 +155,7 @@ int make_plan(int batch, int64_t rows, int64_t cols, float alpha, int axis, int 
     P.o_Z = take(comp);
     P.o_Z1 = take(P.gram && !P.master ? 0 : comp);   // DIRECT's ping-pong copy, or the lo half of X
     P.o_ZT = take(P.xrows ? 2 * comp : 0);            // DIRECT's X^T, ping-pong
+    P.o_sqp = take(P.colpass ? B * (size_t)(P.opad / 64) * (size_t)P.kpad * 8 : 0);
     P.S_bytes = align256(B * (size_t)P.s_pad * (size_t)P.s_pad * 2);
     P.o_S = take(own_sq ? P.S_bytes * (P.gram ? SQ_GRAM_COUNT : SQ_DIRECT_COUNT) : 0);
     P.o_O = take(B * (size_t)P.kpad * (size_t)P.opad * 4);
@@ -803,6 +810,7 @@ struct Bufs {
     uint16_t* Z0;   // compact matrix in its wide orientation: L [kpad][opad] or L^T [opad][kpad]
     uint16_t* Z1;
     uint16_t* ZT[2];   // DIRECT with xrows: X^T [l_pad][s_pad], ping-pong
+    double* sqp;       // colpass: per-block sums of squares of the selected columns
     uint16_t* sbuf[SQ_GRAM_COUNT];   // s x s buffers (null when a shared chain owns them)
     float* O;
     double* part;
@@ -819,6 +827,7 @@ Bufs carve(const Plan& P, char* ws) {
     b.Z1 = reinterpret_cast<uint16_t*>(ws + P.o_Z1);
     b.ZT[0] = P.xrows ? reinterpret_cast<uint16_t*>(ws + P.o_ZT) : nullptr;
     b.ZT[1] = P.xrows ? b.ZT[0] + (size_t)P.batch * (size_t)P.s_pad * (size_t)P.l_pad : nullptr;
+    b.sqp = P.colpass ? reinterpret_cast<double*>(ws + P.o_sqp) : nullptr;
     for (int i = 0; i < SQ_GRAM_COUNT; ++i)
         b.sbuf[i] = reinterpret_cast<uint16_t*>(ws + P.o_S + (size_t)i * P.S_bytes);
     b.O = reinterpret_cast<float*>(ws + P.o_O);
@@ -844,6 +853,10 @@ PhaseBytes phase_bytes(const Plan& P, const dion2_options& opt) {
     PhaseBytes pb;
     pb.k1 = n_el * ((cm ? 4.0 : 8.0) + g_bytes);
     pb.k3 = (cm ? n_el * (8.0 + g_bytes) : sel_el * 8.0) + sel_el * 2.0;
+    if (cm && P.colpass && !opt.dbg_norms) {
+        pb.k1 = 0.0;                   // no norm pass
+        pb.k3 += sel_el * 8.0;         // the unscaled fp32 copy written and read back
+    }
     pb.k5 = (cm ? n_el : sel_el) * 2.0 * w_bytes + sel_el * 4.0;
     return pb;
 }
@@ -853,6 +866,8 @@ int front(const Plan& P, const MatSet& ms, const Bufs& b, float mu, int ns_steps
           const dion2_options& opt, hipStream_t stream) {
     const PhaseBytes pb = phase_bytes(P, opt);
     const bool cm = P.axis == 1;
+    // columns under the Random rule: no norm pass (the debug l1 norms need it)
+    const bool colpass = P.colpass && !opt.dbg_norms;
     MomentumArgs ma{};
     ma.ms = ms;
     ma.rows = P.rows;
@@ -864,13 +879,16 @@ int front(const Plan& P, const MatSet& ms, const Bufs& b, float mu, int ns_steps
     ma.rb_rows = P.rb_rows;
     ma.nrb = P.nrb;
     ma.mu = mu;
-    hipError_t e = timed(DION2_PHASE_MOMENTUM, 0.0, pb.k1, P.axis == 0 ? 1 : 2, stream,
-                         [&] { return launch_momentum(ma, P.axis, opt.g_dtype == DION2_DTYPE_BF16, stream); });
-    if (e != hipSuccess) return hip_fail(e, "launch K1 momentum");
+    hipError_t e = hipSuccess;
+    if (!colpass) {
+        e = timed(DION2_PHASE_MOMENTUM, 0.0, pb.k1, P.axis == 0 ? 1 : 2, stream,
+                  [&] { return launch_momentum(ma, P.axis, opt.g_dtype == DION2_DTYPE_BF16, stream); });
+        if (e != hipSuccess) return hip_fail(e, "launch K1 momentum");
+    }
 
     SelectArgs sa{};
     sa.l1 = b.l1;
-    sa.sq = b.sq;
+    sa.sq = colpass ? nullptr : b.sq;   // the single pass computes the scale itself
     sa.d_sel = (int)P.d_sel;
     sa.k = (int)P.k;
     sa.batch = P.batch;
@@ -908,8 +926,27 @@ int front(const Plan& P, const MatSet& ms, const Bufs& b, float mu, int ns_steps
         ga.LTlo = P.z_is_L ? nullptr : b.Z1;
     }
     ga.O = ns_steps == 0 ? b.O : nullptr;
-    e = timed(DION2_PHASE_GATHER, 0.0, pb.k3, 1, stream,
-              [&] { return launch_gather(ga, P.axis, opt.g_dtype == DION2_DTYPE_BF16, stream); });
+    if (colpass) {   // unscaled columns into O (free until the final product), then normalised
+        ga.L = ga.LT = nullptr;
+        ga.O = b.O;
+        ga.sq_part = b.sqp;
+    }
+    e = timed(DION2_PHASE_GATHER, 0.0, pb.k3, colpass ? 3 : 1, stream, [&] {
+        hipError_t r = launch_gather(ga, P.axis, opt.g_dtype == DION2_DTYPE_BF16, stream);
+        if (r != hipSuccess || !colpass) return r;
+        ColpassArgs ca{};
+        ca.Ot = b.O;
+        ca.sq_part = b.sqp;
+        ca.scale = b.scale;
+        ca.L = P.z_is_L ? b.Z0 : nullptr;
+        ca.LT = P.z_is_L ? nullptr : b.Z0;
+        ca.batch = P.batch;
+        ca.k = (int)P.k;
+        ca.kpad = (int)P.kpad;
+        ca.opad = (int)P.opad;
+        ca.eps = (double)opt.ns_eps;
+        return launch_colpass_finish(ca, stream);
+    });
     if (e != hipSuccess) return hip_fail(e, "launch K3 gather");
     // the debug copies of X, before Newton-Schulz overwrites the DIRECT form's buffer
     for (int h = 0; h < 2; ++h) {
@@ -1160,7 +1197,7 @@ int step_impl(void* W, float* M, const void* G, const Tables* tabs, int batch, i
     if (st != DION2_OK) return st;
     Plan P;
     st = make_plan(batch, rows, cols, alpha, axis, opt.ns_form, ns_steps, &P, true,
-                   opt.ns_master == DION2_MASTER_FP32);
+                   opt.ns_master == DION2_MASTER_FP32, opt.select_rule == DION2_SELECT_RANDOM);
     if (st != DION2_OK) return st;
     ChainFmt fmt;
     st = chain_format(opt, ns_steps, &fmt);
@@ -1265,7 +1302,8 @@ int groups_impl(const dion2_group* groups, int ngroups, float alpha, float mu, f
         const dion2_group& G = groups[g];
         Plan P;
         const bool master = opt.ns_master == DION2_MASTER_FP32;
-        st = make_plan(G.batch, G.rows, G.cols, alpha, G.axis, opt.ns_form, ns_steps, &P, true, master);
+        st = make_plan(G.batch, G.rows, G.cols, alpha, G.axis, opt.ns_form, ns_steps, &P, true, master,
+                       opt.select_rule == DION2_SELECT_RANDOM);
         if (st != DION2_OK) return fail(st, "group %d: %s", g, g_last_error.c_str());
         if (!G.W || !G.M || !G.G) return fail(DION2_ERR_INVALID_ARG, "group %d: W, M and G must not be NULL", g);
         if (!aligned16(G.W) || !aligned16(G.M) || !aligned16(G.G))
@@ -1284,7 +1322,8 @@ int groups_impl(const dion2_group* groups, int ngroups, float alpha, float mu, f
             chain_of[g] = c;
             chain_pos[g] = chains[c].batch;
             chains[c].batch += P.batch;
-            make_plan(G.batch, G.rows, G.cols, alpha, G.axis, opt.ns_form, ns_steps, &P, false, master);
+            make_plan(G.batch, G.rows, G.cols, alpha, G.axis, opt.ns_form, ns_steps, &P, false, master,
+                      opt.select_rule == DION2_SELECT_RANDOM);
         }
         plans[g] = P;
         total_batch += G.batch;
@@ -1527,10 +1566,22 @@ int dion2_step_groups(const dion2_group* groups, int ngroups, float alpha, float
 
 size_t dion2_workspace_size(int batch, int64_t rows, int64_t cols, float alpha, int axis) {
     // the largest plan any options take: the GRAM order with the fp32 master
-    // (X's lo half beside it and every s x s buffer); DIRECT needs less
-    Plan P;
-    if (make_plan(batch, rows, cols, alpha, axis, DION2_NS_GRAM, 0, &P, true, true) != DION2_OK) return 0;
-    return P.total;
+    // (X's lo half beside it and every s x s buffer), or DIRECT (X's
+    // ping-pong copy and, from s = 2048, X^T twice) or GRAM with the Random
+    // rule's column partials
+    struct Case {
+        int form;
+        bool master, random;
+    };
+    const Case cases[] = {{DION2_NS_GRAM, true, false}, {DION2_NS_GRAM, false, true}, {DION2_NS_DIRECT, false, true}};
+    size_t best = 0;
+    for (const Case& c : cases) {
+        Plan P;
+        if (make_plan(batch, rows, cols, alpha, axis, c.form, 1, &P, true, c.master, c.random) != DION2_OK)
+            return 0;
+        best = P.total > best ? P.total : best;
+    }
+    return best;
 }
 
 size_t dion2_workspace_size_ex(int batch, int64_t rows, int64_t cols, float alpha, int axis,
@@ -1542,7 +1593,8 @@ size_t dion2_workspace_size_ex(int batch, int64_t rows, int64_t cols, float alph
     Plan P;
     const bool ok = validate_common(0.f, 0.f, ns_steps, opt) == DION2_OK &&
                     make_plan(batch, rows, cols, alpha, axis, opt.ns_form, ns_steps, &P, true,
-                              opt.ns_master == DION2_MASTER_FP32) == DION2_OK;
+                              opt.ns_master == DION2_MASTER_FP32,
+                              opt.select_rule == DION2_SELECT_RANDOM) == DION2_OK;
     g_last_error = saved;
     return ok ? P.total : 0;
 }

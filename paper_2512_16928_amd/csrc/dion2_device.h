@@ -190,7 +190,7 @@ struct SelectArgs {
     int d_sel, k, batch;
     double eps;
     int32_t* sel;      // [batch][k] ascending
-    double* scale;     // [batch] 1 / (sqrt(sum sq over K) + eps)
+    double* scale;     // [batch] 1 / (sqrt(sum sq over K) + eps); not written when sq is null
     int32_t* rank;     // nullable [batch][d_sel + 1]: selected lines below i
     int rule;          // 0: largest l1 norms, 1: smallest Philox keys (Random rule)
     uint64_t seed, step;
@@ -213,8 +213,27 @@ struct GatherArgs {
     uint16_t* LTlo;    // same entries, for the fp32-master Newton-Schulz
     float* O;          // nullable: fp32 copy (no Newton-Schulz step), L layout for
                        // rows, L^T layout [opad][kpad] for columns
+    double* sq_part;   // columns, single pass (the Random rule: K known before M is
+                       // read): scale is not read; O gets the unscaled selected
+                       // columns and sq_part[batch][opad / 64][kpad] the sums of
+                       // squares of each 64-row block of each selected column
 };
 hipError_t launch_gather(const GatherArgs& a, int axis, int g_bf16, hipStream_t s);
+
+// The end of the single column pass: scale[b] = 1 / (sqrt(sum of sq_part over
+// K's lines and the row blocks, in a fixed order) + eps), then the compact
+// matrix bf16(fl32(x * fl32(scale))) from the unscaled copy Ot [opad][kpad],
+// into L [kpad][opad] or LT [opad][kpad] (padded lines zero).
+struct ColpassArgs {
+    const float* Ot;
+    double* sq_part;   // folded in place
+    double* scale;
+    uint16_t* L;
+    uint16_t* LT;
+    int batch, k, kpad, opad;
+    double eps;
+};
+hipError_t launch_colpass_finish(const ColpassArgs& a, hipStream_t s);
 
 struct DecayAllArgs {
     MatSet ms;

@@ -139,7 +139,9 @@ __global__ __launch_bounds__(kThreads) void update_cols(GatherArgs a) {
     const int p0 = rank[c0], p1 = rank[cend];
     float* __restrict__ M = a.ms.m(b);
     const GT* __restrict__ G = a.ms.g<GT>(b);
-    const float sc = (float)a.scale[b];
+    // the single pass (sq_part) copies the columns unscaled: their norm is
+    // known only once every row has been read
+    const float sc = a.sq_part ? 1.0f : (float)a.scale[b];
     const int cq = threadIdx.x & 63, rg = threadIdx.x >> 6;
     const int64_t c = c0 + 4 * cq;
     int pl[4];        // tile row of each of the four columns, -1 if unselected
@@ -213,6 +215,18 @@ __global__ __launch_bounds__(kThreads) void update_cols(GatherArgs a) {
     __syncthreads();
     const int np = p1 - p0;
     const bool last = cend == a.cols;   // this chunk also zeroes the padded lines k..kpad
+    if (a.sq_part) {
+        // sum of squares of this block's 64 rows of each selected column, in row order
+        double* sp = a.sq_part + ((int64_t)b * (a.opad / kRB) + blockIdx.y) * a.kpad + p0;
+        for (int pi = threadIdx.x; pi < np; pi += kThreads) {
+            double q = 0.0;
+            for (int rl = 0; rl < kRB; ++rl) {
+                const double x = (double)tile[pi][rl];
+                q += x * x;
+            }
+            sp[pi] = q;
+        }
+    }
     if (a.L) {
         // L[p][r0 .. r0 + 64), four rows per thread
         const int q = threadIdx.x & 15;
@@ -293,6 +307,123 @@ hipError_t launch_copy_compact(const CompactCopyArgs& a, hipStream_t s) {
     int64_t blocks = (n + kThreads - 1) / kThreads;
     if (blocks > 1024) blocks = 1024;
     hipLaunchKernelGGL(copy_compact, dim3((unsigned)blocks, (unsigned)a.batch), dim3(kThreads), 0, s, a);
+    return hipGetLastError();
+}
+
+// ---- the end of the single column pass (see ColpassArgs)
+
+namespace {
+
+// Sums of squares of the selected columns from update_cols' partials
+// sq_part[b][rb][p] (rb = 64-row block), in a fixed order. Level 1: a block
+// takes 64 lines and up to 256 row blocks (four quarters, one per group of 64
+// threads, each summed in row order with its loads issued ahead), folds the
+// quarters in order and writes the result in place of the chunk's first row
+// block.
+constexpr int kChunk = 256;   // row blocks folded by one level-1 block
+
+__global__ __launch_bounds__(kThreads) void colpass_fold(ColpassArgs a) {
+    __shared__ double part[4][64];
+    const int b = blockIdx.z;
+    const int nrb = a.opad / kRB;
+    const int p = blockIdx.x * 64 + (threadIdx.x & 63);
+    const int quarter = threadIdx.x >> 6;
+    const int rb0 = blockIdx.y * kChunk;
+    const int rb1 = rb0 + kChunk < nrb ? rb0 + kChunk : nrb;
+    const int per = (rb1 - rb0 + 3) / 4;
+    const int q0 = rb0 + quarter * per;
+    const int q1 = q0 + per < rb1 ? q0 + per : rb1;
+    double* sp = a.sq_part + (int64_t)b * nrb * a.kpad;
+    double q = 0.0;
+    if (p < a.k) {
+        int rb = q0;
+        for (; rb + 8 <= q1; rb += 8) {
+            double v[8];
+#pragma unroll
+            for (int u = 0; u < 8; ++u) v[u] = sp[(int64_t)(rb + u) * a.kpad + p];
+#pragma unroll
+            for (int u = 0; u < 8; ++u) q += v[u];
+        }
+        for (; rb < q1; ++rb) q += sp[(int64_t)rb * a.kpad + p];
+    }
+    part[quarter][threadIdx.x & 63] = q;
+    __syncthreads();
+    if (quarter == 0 && p < a.k) {
+        const int l = threadIdx.x;
+        sp[(int64_t)rb0 * a.kpad + p] = ((part[0][l] + part[1][l]) + part[2][l]) + part[3][l];
+    }
+}
+
+// Level 2, one block per matrix: each line's chunks in order, the lines in a
+// fixed order, then scale = 1 / (sqrt(sum) + eps).
+__global__ __launch_bounds__(kThreads) void colpass_scale(ColpassArgs a) {
+    const int b = blockIdx.x;
+    const int nrb = a.opad / kRB;
+    const double* sp = a.sq_part + (int64_t)b * nrb * a.kpad;
+    double f = 0.0;
+    for (int p = threadIdx.x; p < a.k; p += kThreads) {
+        double q = 0.0;
+        for (int rb0 = 0; rb0 < nrb; rb0 += kChunk) q += sp[(int64_t)rb0 * a.kpad + p];
+        f += q;
+    }
+    __shared__ double red[kThreads / 64];
+    for (int off = 32; off > 0; off >>= 1) f += __shfl_xor(f, off);
+    if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = f;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        double t = 0.0;
+        for (int w = 0; w < kThreads / 64; ++w) t += red[w];
+        a.scale[b] = 1.0 / (sqrt(t) + a.eps);
+    }
+}
+
+// 64 rows x 64 lines per block through an LDS tile; every store writes eight
+// consecutive bf16 (16 bytes).
+__global__ __launch_bounds__(kThreads) void colpass_compact(ColpassArgs a) {
+    __shared__ float t[64][65];
+    const int b = blockIdx.z;
+    const int r0 = blockIdx.y * 64, p0 = blockIdx.x * 64;
+    const float sc = (float)a.scale[b];
+    const float* Ot = a.Ot + (int64_t)b * a.opad * a.kpad;
+    for (int idx = threadIdx.x; idx < 64 * 16; idx += kThreads) {
+        const int r = idx >> 4, pq = (idx & 15) * 4;
+        float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+        if (p0 + pq < a.k) v = ldg<float4>(Ot + (int64_t)(r0 + r) * a.kpad + p0 + pq);
+        const float x[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+        for (int u = 0; u < 4; ++u) t[r][pq + u] = p0 + pq + u < a.k ? x[u] * sc : 0.f;
+    }
+    __syncthreads();
+    for (int idx = threadIdx.x; idx < 64 * 8; idx += kThreads) {
+        const int row = idx >> 3, c8 = (idx & 7) * 8;   // output row, first of eight entries
+        uint32_t w[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            const float x0 = a.LT ? t[row][c8 + 2 * u] : t[c8 + 2 * u][row];
+            const float x1 = a.LT ? t[row][c8 + 2 * u + 1] : t[c8 + 2 * u + 1][row];
+            w[u] = (uint32_t)f32_to_bf16(x0) | ((uint32_t)f32_to_bf16(x1) << 16);
+        }
+        uint16_t* dst = a.LT ? a.LT + (int64_t)b * a.opad * a.kpad + (int64_t)(r0 + row) * a.kpad + p0 + c8
+                             : a.L + (int64_t)b * a.kpad * a.opad + (int64_t)(p0 + row) * a.opad + r0 + c8;
+        stg(dst, make_uint4(w[0], w[1], w[2], w[3]));
+    }
+}
+
+}  // namespace
+
+hipError_t launch_colpass_finish(const ColpassArgs& a, hipStream_t s) {
+    if (a.kpad % 64 || a.opad % 64 || a.batch < 1 || a.batch > 65535 || (!a.L) == (!a.LT))
+        return hipErrorInvalidValue;
+    const int nrb = a.opad / kRB;
+    const dim3 fold((unsigned)((a.k + 63) / 64), (unsigned)((nrb + kChunk - 1) / kChunk), (unsigned)a.batch);
+    hipLaunchKernelGGL(colpass_fold, fold, dim3(kThreads), 0, s, a);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(colpass_scale, dim3((unsigned)a.batch), dim3(kThreads), 0, s, a);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    const dim3 grid((unsigned)(a.kpad / 64), (unsigned)(a.opad / 64), (unsigned)a.batch);
+    hipLaunchKernelGGL(colpass_compact, grid, dim3(kThreads), 0, s, a);
     return hipGetLastError();
 }
 

@@ -80,7 +80,7 @@ __device__ __forceinline__ int block_excl_prefix(bool flag, int* wave_tot, int& 
 __global__ __launch_bounds__(kThreads) void select_topk(SelectArgs a) {
     const int b = blockIdx.x;
     const double* __restrict__ nrm = a.l1 + (int64_t)b * a.d_sel;
-    const double* __restrict__ sq = a.sq + (int64_t)b * a.d_sel;
+    const double* __restrict__ sq = a.sq ? a.sq + (int64_t)b * a.d_sel : nullptr;
     int32_t* __restrict__ out = a.sel + (int64_t)b * a.k;
     int32_t* __restrict__ rank = a.rank ? a.rank + (int64_t)b * (a.d_sel + 1) : nullptr;
 
@@ -170,7 +170,7 @@ __global__ __launch_bounds__(kThreads) void select_topk(SelectArgs a) {
         const int pos = taken + block_excl_prefix(pick, wave_tot, pick_total);
         if (pick) {
             out[pos] = i;
-            fro += sq[i];
+            if (sq) fro += sq[i];
         }
         if (rank && valid) rank[i] = pos;   // selected lines before i
         taken += pick_total;
@@ -183,7 +183,7 @@ __global__ __launch_bounds__(kThreads) void select_topk(SelectArgs a) {
     if (threadIdx.x == 0) {
         double f = 0.0;
         for (int w = 0; w < kWaves; ++w) f += red[w];
-        a.scale[b] = 1.0 / (sqrt(f) + a.eps);
+        if (sq) a.scale[b] = 1.0 / (sqrt(f) + a.eps);
         if (rank) rank[a.d_sel] = a.k;
     }
 }

@@ -88,7 +88,8 @@ def phase_of(kernel: str):
         return "momentum"
     if k.startswith("select"):
         return "select"
-    if k.startswith("gather") or k.startswith("update_cols") or k.startswith("decay_all"):
+    if (k.startswith("gather") or k.startswith("update_cols") or k.startswith("decay_all")
+            or k.startswith("colpass")):   # colpass_*: the end of the Random rule's single column pass
         return "gather"
     if k.startswith("apply"):
         return "apply"

@@ -225,18 +225,25 @@ def test_workspace_size(lib):
     # k = 512 of 2048 with l = 4 s: the GRAM form, one bf16 compact matrix,
     # the fp32 result and ten bf16 s x s buffers
     assert a >= 512 * 2048 * (2 + 4) + 10 * 512 * 512 * 2
-    # alpha = 1 (s = l): the DIRECT form, two bf16 compact buffers, three s x s
-    assert c >= 2048 * 2048 * (2 * 2 + 4) + 3 * 2048 * 2048 * 2
+    # alpha = 1 (s = l = 2048): the DIRECT form, two bf16 compact buffers and
+    # two of X^T (the update's B operand as rows), three s x s
+    assert c >= 2048 * 2048 * (4 * 2 + 4) + 3 * 2048 * 2048 * 2
+    # the Random rule with column selection adds per-block partial sums
+    r = ws_ex(1, 8192, 2048, 0.25, select_rule=binding.SELECT_RANDOM)
+    assert r >= ws_ex(1, 8192, 2048, 0.25) + (8192 // 64) * 512 * 8
     # past the DIRECT form's step limit AUTO takes GRAM: ten s x s buffers
     c7 = ws_ex(1, 2048, 2048, 1.0, AXIS_AUTO, 7)
     assert c7 == ws_ex(1, 2048, 2048, 1.0, AXIS_AUTO, 5, ns_form=binding.NS_GRAM) and c7 > c
     assert c7 >= 2048 * 2048 * (2 + 4) + 10 * 2048 * 2048 * 2
     # the size without options covers every option and step count
-    for shape in ((1, 2048, 2048, 0.25), (2, 2048, 2048, 1.0), (3, 640, 256, 0.5), (1, 300, 200, 0.75)):
+    rnd = binding.SELECT_RANDOM
+    for shape in ((1, 2048, 2048, 0.25), (2, 2048, 2048, 1.0), (3, 640, 256, 0.5), (1, 300, 200, 0.75),
+                  (1, 2048, 8192, 1.0), (2, 8192, 2048, 1.0), (2, 8192, 2048, 0.25)):
         top = binding.dion2_workspace_size(*shape)
         for kw in (dict(), dict(ns_form=binding.NS_DIRECT), dict(ns_form=binding.NS_GRAM),
                    dict(ns_master=binding.MASTER_FP32), dict(ns_chain=binding.CHAIN_F16),
-                   dict(w_dtype=torch_f32(), g_dtype=torch_f32())):
+                   dict(w_dtype=torch_f32(), g_dtype=torch_f32()), dict(select_rule=rnd),
+                   dict(select_rule=rnd, ns_form=binding.NS_DIRECT), dict(select_rule=rnd, ns_form=binding.NS_GRAM)):
             for ns in (0, 1, 5, 6, 16):
                 need = ws_ex(*shape, AXIS_AUTO, ns, **kw)
                 assert need <= top, (shape, kw, ns)

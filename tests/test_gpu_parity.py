@@ -38,9 +38,10 @@ CHAINS = pytest.mark.parametrize("chain", [binding.CHAIN_HILO, binding.CHAIN_F16
 
 def run_gpu(W, M, G, alpha, ns_steps=5, axis=AXIS_AUTO, mu=0.95, lr=0.02, coeffs=None,
             decay_all=False, form=binding.NS_AUTO, rand=None, chain=binding.CHAIN_HILO,
-            master=binding.MASTER_BF16, eps=1e-7, dbg_compact=None, dbg_compact_lo=None):
+            master=binding.MASTER_BF16, eps=1e-7, dbg_compact=None, dbg_compact_lo=None, norms=True):
     """One library call on stacks [B, rows, cols]; returns host copies and the
-    debug outputs."""
+    debug outputs (norms=False leaves out the l1 norms, which the Random
+    rule's single column pass does not compute)."""
     B, rows, cols = W.shape
     k, ax = binding.dion2_plan_info(rows, cols, alpha, axis)
     d_sel, d_oth = (rows, cols) if ax == AXIS_ROWS else (cols, rows)
@@ -54,11 +55,11 @@ def run_gpu(W, M, G, alpha, ns_steps=5, axis=AXIS_AUTO, mu=0.95, lr=0.02, coeffs
         extra = dict(select_rule=binding.SELECT_RANDOM, rand_seed=rand[0], rand_step=rand[1],
                      rand_matrix0=rand[2])
     binding.dion2_step_ex(W, M, G, alpha, mu, lr, ns_steps, axis, ns_coeffs=coeffs, ns_eps=eps,
-                          decay_all=decay_all, dbg_sel_idx=sel, dbg_norms=nrm, dbg_update=upd,
+                          decay_all=decay_all, dbg_sel_idx=sel, dbg_norms=nrm if norms else None, dbg_update=upd,
                           ns_form=form, ns_chain=chain, ns_master=master, dbg_compact=dbg_compact,
                           dbg_compact_lo=dbg_compact_lo, **extra)
     torch.cuda.synchronize()
-    return dict(W=W.cpu(), M=M.cpu(), K=sel.cpu(), norms=nrm.cpu(), O=upd.cpu(), W0=W0, M0=M0,
+    return dict(W=W.cpu(), M=M.cpu(), K=sel.cpu(), norms=nrm.cpu() if norms else None, O=upd.cpu(), W0=W0, M0=M0,
                 G=G.cpu(), axis=ax, k=k)
 
 
@@ -76,7 +77,8 @@ def check_matrix(res, b, alpha, ns_steps=5, axis=AXIS_AUTO, mu=0.95, lr=0.02, co
     assert out["axis"] == res["axis"] and out["k"] == res["k"]
     K = res["K"][b].numpy().astype(np.int64)
     np.testing.assert_array_equal(K, out["K"], err_msg="selected indices")
-    np.testing.assert_array_equal(res["norms"][b].numpy(), out["norms"], err_msg="l1 norms")
+    if res["norms"] is not None:
+        np.testing.assert_array_equal(res["norms"][b].numpy(), out["norms"], err_msg="l1 norms")
     np.testing.assert_array_equal(res["M"][b].numpy(), out["M"], err_msg="momentum")
     O_gpu = res["O"][b].numpy().astype(np.float64)          # [k, d_oth]
     O_ref = out["O"] if out["axis"] == AXIS_ROWS else out["O"].T
@@ -478,6 +480,42 @@ def test_compact_x_bitwise(hip_device, rows, cols, alpha, axis, gdt, form, steps
         off = got[b] != oracle.round_bf16(q)
         assert off.mean() < 1e-3
         assert np.all(np.abs(got[b][off] - q[off]) <= 2.0 ** -7 * np.abs(q[off]))
+
+
+@pytest.mark.parametrize("rows,cols,alpha,gdt,decay_all", [
+    (600, 330, 0.25, "bf16", False),    # k = 83 <= d_oth: L layout, ragged tiles
+    (300, 800, 1.0, "f32", False),      # k = 800 > d_oth = 300: L^T layout
+    (1000, 512, 0.5, "bf16", True),     # decay-all
+])
+def test_random_rule_single_column_pass(hip_device, rows, cols, alpha, gdt, decay_all):
+    """Column selection under the Random rule reads M and G once: K is drawn
+    first, update_cols forms M + G, decays and copies the selected columns
+    unscaled with per-block sums of squares, and ||X||_F and the compact
+    matrix follow. Against the oracle (K, M, X bitwise; O; W given O), and
+    bitwise the two-pass path the debug l1 norms select."""
+    wl = one_group_workload(rows, cols, count=2, axis=AXIS_COLS, w_dtype="f32", name=f"cp{rows}")
+    W, M, G = workloads.make_group(wl, 0, hip_device)
+    W = W.to(torch.bfloat16).contiguous()
+    G = G.to(torch.bfloat16 if gdt == "bf16" else torch.float32).contiguous()
+    B = W.shape[0]
+    k, ax = binding.dion2_plan_info(rows, cols, alpha, AXIS_COLS)
+    assert ax == AXIS_COLS
+    rand = (21, 4, 7)
+    M0, G0 = M.cpu().numpy(), G.float().cpu().numpy()
+    W2, M2 = W.clone(), M.clone()
+    cx = torch.zeros((B, k, rows), dtype=torch.bfloat16, device=hip_device)
+    res = run_gpu(W, M, G, alpha, axis=AXIS_COLS, rand=rand, decay_all=decay_all, dbg_compact=cx,
+                  norms=False)
+    got = cx.float().cpu().numpy().astype(np.float64)
+    eps = float(np.float32(1e-7))
+    for b in range(B):
+        check_matrix(res, b, alpha, axis=AXIS_COLS, rand=rand, decay_all=decay_all)
+        if not decay_all:
+            hi, _, _ = compact_x_want(M0[b], G0[b], res["K"][b].numpy().astype(np.int64), ax, eps)
+            np.testing.assert_array_equal(got[b], hi, err_msg=f"compact X, matrix {b}")
+    two = run_gpu(W2, M2, G, alpha, axis=AXIS_COLS, rand=rand, decay_all=decay_all)
+    assert torch.equal(two["K"], res["K"]) and torch.equal(two["M"], res["M"])
+    assert torch.equal(two["W"].view(torch.int16), res["W"].view(torch.int16))
 
 
 @pytest.mark.parametrize("rows,cols,alpha,axis", [

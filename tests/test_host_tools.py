@@ -29,6 +29,8 @@ def test_phase_of_kernel_names():
         "void dion2::(anonymous namespace)::gemm<2, 3, dion2::(anonymous namespace)::Tile<2, 1, 128, 128, 32, 2, 2, 2>, false>(dion2::GemmArgs)": "ns_update",
         "void dion2::(anonymous namespace)::gemm<2, 5, dion2::(anonymous namespace)::Tile<2, 1, 128, 128, 32, 2, 2, 2>, false>(dion2::GemmArgs)": "ns_update",
         "dion2::transpose_bf16(unsigned short const*, unsigned short*, long, long, long)": "ns_update",
+        "dion2::(anonymous namespace)::colpass_compact(dion2::ColpassArgs)": "gather",
+        "dion2::(anonymous namespace)::colpass_fold(dion2::ColpassArgs)": "gather",
         "void at::native::vectorized_elementwise_kernel<4, at::native::neg_kernel_cuda>": None,
     }
     for name, phase in cases.items():
