@@ -407,6 +407,34 @@ def test_caller_workspace_sized_for_options(hip_device, kw, rows, cols, alpha):
         "a refused call modified state"
 
 
+@pytest.mark.parametrize("rows,cols,alpha,kw", [
+    (2048, 8192, 1.0, dict(ns_form=NS_DIRECT)),                    # X^T pair; l = 4 s
+    (8192, 2048, 0.25, dict(select_rule=binding.SELECT_RANDOM)),  # column partials
+], ids=["direct-xt", "random-columns"])
+def test_caller_workspace_new_buffers(hip_device, rows, cols, alpha, kw):
+    """The buffers the plan adds for the Direct form's X^T (from s = 2048) and
+    the Random rule's single column pass: a caller workspace of exactly
+    dion2_workspace_size_ex bytes gives bitwise the library workspace's
+    result, one block less is refused, and dion2_workspace_size covers it."""
+    wl = one_group_workload(rows, cols, count=1, name=f"wsn{rows}x{cols}")
+    W, M, G = workloads.make_group(wl, 0, hip_device)
+    W2, M2, W3, M3 = W.clone(), M.clone(), W.clone(), M.clone()
+    need = binding.dion2_workspace_size_ex(1, rows, cols, alpha, AXIS_AUTO, 5, **kw)
+    base = binding.dion2_workspace_size_ex(1, rows, cols, alpha, AXIS_AUTO, 5)
+    assert base < need <= binding.dion2_workspace_size(1, rows, cols, alpha)
+    ws = torch.empty(need, dtype=torch.uint8, device=hip_device)
+    binding.dion2_step_ex(W, M, G, alpha, workspace=ws, **kw)
+    binding.dion2_step_ex(W2, M2, G, alpha, **kw)
+    with pytest.raises(binding.Dion2Error) as ei:
+        binding.dion2_step_ex(W3, M3, G, alpha, workspace=ws[:need - 256], **kw)
+    assert ei.value.status == binding.DION2_ERR_WORKSPACE
+    torch.cuda.synchronize()
+    assert torch.equal(W.view(torch.int16), W2.view(torch.int16)) and torch.equal(M, M2)
+    W0, M0, _ = workloads.make_group(wl, 0, hip_device)
+    assert torch.equal(W3.view(torch.int16), W0.view(torch.int16)) and torch.equal(M3, M0), \
+        "a refused call modified state"
+
+
 @pytest.mark.parametrize("eps", [0.0, 1.0], ids=["eps0", "eps-large"])
 @FORMS
 def test_normalisation_eps(hip_device, eps, form):
