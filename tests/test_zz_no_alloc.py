@@ -27,6 +27,8 @@ CALLS = [
     (640, 256, 3, 0.5, AXIS_AUTO, {}),                                       # columns, k > d_oth
     (384, 384, 2, 0.5, AXIS_ROWS, dict(ns_master=binding.MASTER_FP32)),     # fp32 master
     (200, 328, 1, 0.25, AXIS_AUTO, dict(ns_form=binding.NS_DIRECT)),        # DIRECT, ragged
+    (2048, 2048, 1, 1.0, AXIS_AUTO, {}),                                     # DIRECT with X^T (s = 2048)
+    (640, 256, 2, 0.25, AXIS_AUTO, dict(select_rule=binding.SELECT_RANDOM)),  # Random rule, one column pass
     (2048, 2048, 4, 0.25, AXIS_AUTO, {}),
 ]
 
@@ -45,8 +47,9 @@ def test_noalloc_equals_ex_calls_in_a_row(hip_device):
         assert torch.equal(M, M2), f"call {i}: momentum"
         assert torch.equal(W.view(torch.int16), W2.view(torch.int16)), f"call {i}: weights"
         # and the first matrix against the oracle's momentum and selection
+        rnd = dict(select="random", seed=0, step=0, matrix=0) if kw.get("select_rule") else {}
         out = oracle.dion2_step(snap[0].float().numpy().astype(np.float64), snap[1].numpy(),
-                                snap[2].float().numpy(), alpha, 0.95, 0.02, 5, axis, w_dtype="bf16")
+                                snap[2].float().numpy(), alpha, 0.95, 0.02, 5, axis, w_dtype="bf16", **rnd)
         np.testing.assert_array_equal(M[0].cpu().numpy(), out["M"], err_msg=f"call {i}: momentum")
         sel = np.zeros(W.shape[1] if out["axis"] == AXIS_ROWS else W.shape[2], dtype=bool)
         sel[out["K"]] = True
