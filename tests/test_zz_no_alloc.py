@@ -77,3 +77,40 @@ def test_noalloc_refusals_leave_state_untouched(hip_device):
     assert "scratch" in str(ei.value)
     torch.cuda.synchronize()
     assert torch.equal(Wb.view(torch.int16), W0.view(torch.int16)) and torch.equal(Mb, M0)
+
+
+
+def _bits(t):
+    return t.view(torch.int16) if t.dtype == torch.bfloat16 else t
+
+
+@pytest.mark.parametrize("name,rows,cols,batch,w_dtype,alpha,kw", [
+    ("single-256", 256, 256, 1, "f32", 0.25, {}),              # one fp32 matrix: launch-bound
+    ("bf16-group", 512, 1024, 4, "bf16", 0.25, {}),            # GRAM with the fused update
+    ("random-cols", 640, 256, 2, "bf16", 0.25, dict(select_rule=binding.SELECT_RANDOM)),
+])
+def test_noalloc_step_in_a_hip_graph(hip_device, name, rows, cols, batch, w_dtype, alpha, kw):
+    """dion2_step_noalloc captured in a HIP graph (it allocates nothing and
+    issues only kernel launches) and replayed: every replay equals one eager
+    dion2_step_ex step, bitwise, with other eager work and synchronisations
+    between the replays."""
+    wl = wl_of(rows, cols, batch, w_dtype=w_dtype, name=f"graph-{name}")
+    W, M, G = workloads.make_group(wl, 0, hip_device)
+    We, Me = W.clone(), M.clone()
+    binding.dion2_step_noalloc(W, M, G, alpha, **kw)    # outside capture: the scratch address is taken
+    binding.dion2_step_ex(We, Me, G, alpha, **kw)
+    torch.cuda.synchronize()
+    assert torch.equal(M, Me) and torch.equal(_bits(W), _bits(We))
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        binding.dion2_step_noalloc(W, M, G, alpha, **kw)
+    torch.cuda.synchronize()
+    assert torch.equal(M, Me) and torch.equal(_bits(W), _bits(We)), "capture ran the step"
+    for i in range(4):
+        graph.replay()
+        binding.dion2_step_ex(We, Me, G, alpha, **kw)
+        junk = torch.randn(1 << 16, device=hip_device).square().sum()   # eager work between replays
+        torch.cuda.synchronize()
+        assert float(junk) > 0.0
+        assert torch.equal(M, Me), f"replay {i}: momentum"
+        assert torch.equal(_bits(W), _bits(We)), f"replay {i}: weights"
