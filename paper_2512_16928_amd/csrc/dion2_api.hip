@@ -13,6 +13,7 @@
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
+#include <algorithm>
 #include <cstring>
 #include <map>
 #include <mutex>
@@ -57,6 +58,7 @@ struct Plan {
     int64_t kpad, opad;
     bool z_is_L;              // Newton-Schulz iterates on L (k <= d_oth) or L^T
     int64_t s_pad, l_pad;
+    int64_t s_k, l_k;         // K extents of the s- and l-deep products (see make_plan)
     int batch;
     int nrb, rb_rows;         // column-mode reduction blocking
     bool gram;                // Newton-Schulz on s x s matrices (DION2_NS_GRAM)
@@ -116,6 +118,14 @@ int make_plan(int batch, int64_t rows, int64_t cols, float alpha, int axis, int 
     P.z_is_L = P.k <= P.d_oth;
     P.s_pad = P.z_is_L ? P.kpad : P.opad;
     P.l_pad = P.z_is_L ? P.opad : P.kpad;
+    // Every s x s matrix of either form is block diagonal, the s x s block
+    // and the padding (Z's padding rows are zero; only Q's a I reaches the
+    // padding's diagonal), so a product whose inner dimension is s or l
+    // sums only to the real side, rounded up to the 32-deep K slice: the
+    // terms left out are exact zeros in every real entry. (MoE experts:
+    // s = 352 padded to 384, one slice in twelve.)
+    P.s_k = round_up(P.z_is_L ? P.k : P.d_oth, kSliceK);
+    P.l_k = round_up(P.z_is_L ? P.d_oth : P.k, kSliceK);
     // The GRAM form trades 2 (s x l) GEMMs and the X traffic of every step
     // for about four three-pass s x s products; it pays once X is wide. With
     // a single tile a side (s <= 128) both forms cost a few microseconds of
@@ -429,7 +439,7 @@ GemmArgs gram_args(const Plan& P, const uint16_t* Z, uint16_t* hi, uint16_t* lo)
     g.A0 = g.B0 = Z;
     g.sA = g.sB = P.s_pad * P.l_pad;
     g.M = g.N = (int)P.s_pad;
-    g.K = (int)P.l_pad;
+    g.K = (int)P.l_k;
     g.lda = g.ldb = (int)P.l_pad;
     g.out0 = hi;
     g.out1 = lo;
@@ -449,7 +459,8 @@ GemmArgs sym3_args(const Plan& P, const uint16_t* xh, const uint16_t* xl, const 
     q.B0 = yh;
     q.B1 = yl;
     q.sA = q.sB = P.s_pad * P.s_pad;
-    q.M = q.N = q.K = (int)P.s_pad;
+    q.M = q.N = (int)P.s_pad;
+    q.K = (int)P.s_k;
     q.lda = q.ldb = (int)P.s_pad;
     q.out0 = oh;
     q.out1 = ol;
@@ -469,7 +480,7 @@ GemmArgs right_args(const Plan& P, const uint16_t* xh, const uint16_t* xl, const
     x.sB = P.s_pad * P.l_pad;
     x.M = (int)P.s_pad;
     x.N = (int)P.l_pad;
-    x.K = (int)P.s_pad;
+    x.K = (int)P.s_k;
     x.lda = (int)P.s_pad;
     x.ldb = (int)P.l_pad;
     return x;
@@ -708,12 +719,13 @@ hipError_t chain_f16(const Plan& C, uint16_t* const* sq, int ns_steps, const dio
     return hipSuccess;
 }
 
-hipError_t gram_chain(int batch, int64_t s_pad, uint16_t* const* sq, int ns_steps,
+hipError_t gram_chain(int batch, int64_t s_pad, int64_t s_k, uint16_t* const* sq, int ns_steps,
                       const dion2_options& opt, const ChainFmt& fmt, const ChainCost& cost,
                       hipStream_t stream, int* cur_out) {
     Plan C{};
     C.batch = batch;
     C.s_pad = s_pad;
+    C.s_k = s_k;
     if (fmt.f16)
         return timed(DION2_PHASE_NS_POLY, cost.flops, cost.bytes, chain_launches(ns_steps), stream,
                      [&] { return chain_f16(C, sq, ns_steps, opt, fmt, stream, cur_out); });
@@ -792,7 +804,8 @@ hipError_t ns_gram(const Plan& P, const uint16_t* Z, const uint16_t* Zlo, uint16
     hipError_t e = gram_a0(P, Z, Zlo, sq[SQ_AHI], sq[SQ_ALO], fmt, stream);
     if (e != hipSuccess) return e;
     int cur = 0;
-    e = gram_chain(P.batch, P.s_pad, sq, ns_steps, opt, fmt, chain_cost(P, ns_steps, fmt), stream, &cur);
+    e = gram_chain(P.batch, P.s_pad, P.s_k, sq, ns_steps, opt, fmt, chain_cost(P, ns_steps, fmt), stream,
+                   &cur);
     if (e != hipSuccess) return e;
     return gram_final(P, cur ? sq[SQ_P1HI] : sq[SQ_P0HI], cur ? sq[SQ_P1LO] : sq[SQ_P0LO], Z, Zlo, O,
                       fin, stream);
@@ -1289,7 +1302,7 @@ int groups_impl(const dion2_group* groups, int ngroups, float alpha, float mu, f
     if (st != DION2_OK) return st;
 
     struct Chain {
-        int64_t s_pad;
+        int64_t s_pad, s_k = 0;
         int batch = 0;
         size_t off = 0, S_bytes = 0;
     };
@@ -1319,6 +1332,8 @@ int groups_impl(const dion2_group* groups, int ngroups, float alpha, float mu, f
                 chains.push_back(Chain{});
                 chains[c].s_pad = P.s_pad;
             }
+            // the shared products sum to the widest member's real side
+            chains[c].s_k = std::max(chains[c].s_k, P.s_k);
             chain_of[g] = c;
             chain_pos[g] = chains[c].batch;
             chains[c].batch += P.batch;
@@ -1473,7 +1488,8 @@ int groups_impl(const dion2_group* groups, int ngroups, float alpha, float mu, f
         }
         uint16_t* sq[SQ_GRAM_COUNT];
         for (int i = 0; i < SQ_GRAM_COUNT; ++i) sq[i] = chain_buf(c, i);
-        e = gram_chain(chains[c].batch, chains[c].s_pad, sq, ns_steps, opt, fmt, cost, s, &chain_cur[c]);
+        e = gram_chain(chains[c].batch, chains[c].s_pad, chains[c].s_k, sq, ns_steps, opt, fmt, cost, s,
+                       &chain_cur[c]);
         if (e != hipSuccess) return hip_fail(e, "launch K4 s x s products");
         if (nS > 1) {
             e = hipEventRecord(ev_chain[c], s);

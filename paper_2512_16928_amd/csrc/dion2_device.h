@@ -18,6 +18,7 @@
 namespace dion2 {
 
 constexpr int kTile = 128;  // padding granule of the compact buffers
+constexpr int kSliceK = 32;  // K depth of one slice in every GEMM tile
 
 // A batch of same-shape matrices: either one strided stack (tables == null)
 // or device-resident tables of per-matrix pointers.

@@ -754,18 +754,18 @@ hipError_t launch_gemm(const GemmArgs& a, GemmEpi epi, int npass, hipStream_t s)
     // epilogue eight waves per block hide more of the W traffic. Given X^T
     // as rows (b_rows) they run on 256 x 256 plain-read tiles, or 256 x 128
     // where l is not a multiple of 256 and for the fused update step.
-    using TG = Tile<1, 0, 128, 128, 32, 2, 2, 4>;    // Gram
-    using TGL = Tile<1, 0, 256, 256, 32, 4, 2, 3>;   // Gram, large s
-    using TP = Tile<3, 0, 128, 128, 32, 4, 2, 2>;    // three-pass symmetric products
-    using TPL = Tile<3, 0, 256, 256, 32, 2, 4, 2>;   // three-pass symmetric products, large s
-    using TU = Tile<1, 1, 128, 128, 32, 2, 2, 2>;    // update (B operand [K][N])
-    using TU2 = Tile<2, 1, 128, 128, 32, 2, 2, 2>;   // two-pass final product
-    using TU2A = Tile<2, 1, 128, 128, 32, 4, 2, 2>;  // two-pass final product applying the update
-    using TU3 = Tile<3, 1, 128, 128, 32, 2, 2, 2>;   // three-pass final product (fp32 master)
-    using TR = Tile<1, 0, 256, 256, 32, 2, 4, 3>;    // X-side products, B operand as rows (X^T)
-    using TRN = Tile<1, 0, 256, 128, 32, 4, 2, 4>;   // the same, l not a multiple of 256; fused update
-    using TH = Tile<1, 0, 128, 128, 32, 2, 2, 4, true>;   // fp16 s x s products
-    using THL = Tile<1, 0, 256, 256, 32, 4, 2, 3, true>;  // fp16 s x s products from s = 2048
+    using TG = Tile<1, 0, 128, 128, kSliceK, 2, 2, 4>;    // Gram
+    using TGL = Tile<1, 0, 256, 256, kSliceK, 4, 2, 3>;   // Gram, large s
+    using TP = Tile<3, 0, 128, 128, kSliceK, 4, 2, 2>;    // three-pass symmetric products
+    using TPL = Tile<3, 0, 256, 256, kSliceK, 2, 4, 2>;   // three-pass symmetric products, large s
+    using TU = Tile<1, 1, 128, 128, kSliceK, 2, 2, 2>;    // update (B operand [K][N])
+    using TU2 = Tile<2, 1, 128, 128, kSliceK, 2, 2, 2>;   // two-pass final product
+    using TU2A = Tile<2, 1, 128, 128, kSliceK, 4, 2, 2>;  // two-pass final product applying the update
+    using TU3 = Tile<3, 1, 128, 128, kSliceK, 2, 2, 2>;   // three-pass final product (fp32 master)
+    using TR = Tile<1, 0, 256, 256, kSliceK, 2, 4, 3>;    // X-side products, B operand as rows (X^T)
+    using TRN = Tile<1, 0, 256, 128, kSliceK, 4, 2, 4>;   // the same, l not a multiple of 256; fused update
+    using TH = Tile<1, 0, 128, 128, kSliceK, 2, 2, 4, true>;   // fp16 s x s products
+    using THL = Tile<1, 0, 256, 256, kSliceK, 4, 2, 3, true>;  // fp16 s x s products from s = 2048
     if (a.f16) {
         if (npass != 1) return hipErrorInvalidValue;
         const bool big = a.M >= 2048 && a.M % 256 == 0;
