@@ -203,6 +203,11 @@ typedef struct dion2_options {
                                 bf16(x - hi) of X's fp32 values; only with
                                 DION2_MASTER_FP32 and ns_steps >= 1, else the
                                 call returns DION2_ERR_INVALID_ARG              */
+    int ns_chain_per_product;/* GRAM form: 0 (default) runs the chain of s x s
+                                products of a compact matrix with s <= 64 in one
+                                launch, its matrices kept in LDS as hi / lo pairs
+                                whatever ns_chain says; nonzero gives every
+                                product its own launch. Bitwise the same result */
 } dion2_options;
 
 /* Defaults: bf16 W and G, Muon quintic, eps 1e-7, selective decay, internal

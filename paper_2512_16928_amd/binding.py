@@ -75,6 +75,7 @@ class Options(ctypes.Structure):
         ("ns_master", c_int),
         ("dbg_compact", c_void_p),
         ("dbg_compact_lo", c_void_p),
+        ("ns_chain_per_product", c_int),
     ]
 
 
@@ -232,7 +233,7 @@ def dion2_step_ex(W, M, G, alpha, mu=0.95, lr=0.02, ns_steps=5, axis=AXIS_AUTO, 
                   dbg_sel_idx=None, dbg_norms=None, dbg_update=None, dbg_compact=None,
                   dbg_compact_lo=None, ns_form=NS_AUTO, select_rule=SELECT_L1, rand_seed=0,
                   rand_step=0, rand_matrix0=0, ns_chain=CHAIN_HILO, ns_master=MASTER_BF16,
-                  stream=None):
+                  ns_chain_per_product=False, stream=None):
     """Full control. W, M, G are [rows, cols] or [batch, rows, cols]; W and G
     may be bf16 or fp32. Debug outputs are preallocated device tensors:
     dbg_sel_idx int32 [batch, k], dbg_norms float64 [batch, d_sel],
@@ -242,7 +243,8 @@ def dion2_step_ex(W, M, G, alpha, mu=0.95, lr=0.02, ns_steps=5, axis=AXIS_AUTO, 
     NS_GRAM (the Newton-Schulz evaluation order); ns_chain CHAIN_HILO or
     CHAIN_F16 (storage of the GRAM form's s x s matrices); ns_master
     MASTER_BF16 or MASTER_FP32 (X rounded once to bf16, or kept as a hi/lo
-    pair through every product).
+    pair through every product). ns_chain_per_product gives every s x s
+    product its own launch even where s <= 64 (bitwise the same result).
     select_rule SELECT_RANDOM draws the lines from Philox keys of
     (rand_seed, rand_step, rand_matrix0 + b)."""
     if W.dim() == 2:
@@ -250,7 +252,8 @@ def dion2_step_ex(W, M, G, alpha, mu=0.95, lr=0.02, ns_steps=5, axis=AXIS_AUTO, 
     _mats(W, M, G, 3)
     lib = load()
     opt, coeff_buf = _options(W, G, ns_steps, ns_coeffs, ns_eps, decay_all, ns_form, select_rule,
-                              rand_seed, rand_step, rand_matrix0, ns_chain, ns_master)
+                              rand_seed, rand_step, rand_matrix0, ns_chain, ns_master,
+                              ns_chain_per_product)
     for name, t, dt in (("dbg_sel_idx", dbg_sel_idx, torch.int32),
                         ("dbg_norms", dbg_norms, torch.float64),
                         ("dbg_update", dbg_update, torch.float32),
@@ -278,7 +281,8 @@ NOALLOC_SCRATCH_BYTES = 128 << 20
 def dion2_step_noalloc(W, M, G, alpha, mu=0.95, lr=0.02, ns_steps=5, axis=AXIS_AUTO, *,
                        ns_coeffs=None, ns_eps=1e-7, decay_all=False, ns_form=NS_AUTO,
                        select_rule=SELECT_L1, rand_seed=0, rand_step=0, rand_matrix0=0,
-                       ns_chain=CHAIN_HILO, ns_master=MASTER_BF16, stream=None):
+                       ns_chain=CHAIN_HILO, ns_master=MASTER_BF16, ns_chain_per_product=False,
+                       stream=None):
     """The step of dion2_step_ex without any device allocation: the library's
     fixed scratch array holds the workspace (NOALLOC_SCRATCH_BYTES per GPU).
     Calls that overlap on one GPU race."""
@@ -287,7 +291,8 @@ def dion2_step_noalloc(W, M, G, alpha, mu=0.95, lr=0.02, ns_steps=5, axis=AXIS_A
     _mats(W, M, G, 3)
     lib = load()
     opt, coeff_buf = _options(W, G, ns_steps, ns_coeffs, ns_eps, decay_all, ns_form, select_rule,
-                              rand_seed, rand_step, rand_matrix0, ns_chain, ns_master)
+                              rand_seed, rand_step, rand_matrix0, ns_chain, ns_master,
+                              ns_chain_per_product)
     batch, rows, cols = W.shape
     _check(lib.dion2_step_noalloc(W.data_ptr(), M.data_ptr(), G.data_ptr(), batch, rows, cols,
                                   alpha, mu, lr, ns_steps, axis, ctypes.byref(opt),
@@ -296,7 +301,8 @@ def dion2_step_noalloc(W, M, G, alpha, mu=0.95, lr=0.02, ns_steps=5, axis=AXIS_A
 
 
 def _options(W, G, ns_steps, ns_coeffs, ns_eps, decay_all, ns_form, select_rule, rand_seed,
-             rand_step, rand_matrix0, ns_chain=CHAIN_HILO, ns_master=MASTER_BF16):
+             rand_step, rand_matrix0, ns_chain=CHAIN_HILO, ns_master=MASTER_BF16,
+             ns_chain_per_product=False):
     """Options struct (and the coefficient buffer it points to, kept alive by the caller)."""
     lib = load()
     opt = Options()
@@ -319,13 +325,15 @@ def _options(W, G, ns_steps, ns_coeffs, ns_eps, decay_all, ns_form, select_rule,
     opt.rand_matrix0 = rand_matrix0
     opt.ns_chain = ns_chain
     opt.ns_master = ns_master
+    opt.ns_chain_per_product = 1 if ns_chain_per_product else 0
     return opt, coeff_buf
 
 
 def dion2_step_groups(groups, alpha, mu=0.95, lr=0.02, ns_steps=5, *, ns_coeffs=None,
                       ns_eps=1e-7, decay_all=False, ns_form=NS_AUTO, select_rule=SELECT_L1,
                       rand_seed=0, rand_step=0, rand_matrix0=0, group_streams=0,
-                      ns_chain=CHAIN_HILO, ns_master=MASTER_BF16, stream=None):
+                      ns_chain=CHAIN_HILO, ns_master=MASTER_BF16, ns_chain_per_product=False,
+                      stream=None):
     """Several same-shape stacks in one call: groups is a list of (W, M, G, axis)
     with W, M, G [batch, rows, cols] on one device, W and G of one dtype pair
     across groups. Bitwise the result of dion2_step_ex per group; groups of one
@@ -343,7 +351,7 @@ def dion2_step_groups(groups, alpha, mu=0.95, lr=0.02, ns_steps=5, *, ns_coeffs=
                        W.shape[2], axis)
     W0, _, G0, _ = groups[0]
     opt, keep = _options(W0, G0, ns_steps, ns_coeffs, ns_eps, decay_all, ns_form, select_rule,
-                         rand_seed, rand_step, rand_matrix0, ns_chain, ns_master)
+                         rand_seed, rand_step, rand_matrix0, ns_chain, ns_master, ns_chain_per_product)
     opt.group_streams = group_streams
     lib = load()
     _check(lib.dion2_step_groups(arr, len(groups), alpha, mu, lr, ns_steps, ctypes.byref(opt),

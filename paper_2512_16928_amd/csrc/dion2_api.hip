@@ -82,6 +82,7 @@ enum { SQ_QHI = 2, SQ_QLO, SQ_THI, SQ_TLO, SQ_P0HI, SQ_P0LO, SQ_P1HI, SQ_P1LO, S
 // Beyond DION2_DIRECT_MAX_STEPS AUTO takes the GRAM form, which carries the
 // iteration in hi / lo pairs, and a forced DIRECT is refused.
 constexpr int kDirectMaxSteps = DION2_DIRECT_MAX_STEPS;
+static_assert(kChainMaxSteps == DION2_MAX_NS_STEPS, "the fused chain's coefficient table");
 
 // own_sq = false leaves out the s x s buffers (a grouped call carves them
 // once for every group of a shared Newton-Schulz chain).
@@ -639,16 +640,29 @@ struct ChainCost {
 };
 int chain_products(int ns_steps) { return ns_steps + 3 * (ns_steps - 1); }
 int chain_launches(int ns_steps) { return ns_steps == 1 ? 1 : 3 * ns_steps - 1; }
-ChainCost chain_cost(const Plan& P, int ns_steps, const ChainFmt& fmt) {
+ChainCost chain_cost(const Plan& P, int ns_steps, const ChainFmt& fmt, bool fused) {
     const double s_r = (double)(P.k < P.d_oth ? P.k : P.d_oth);
     const double nb = (double)P.batch;
     const int nprod = chain_products(ns_steps);
     const int ndual = ns_steps >= 3 ? ns_steps - 2 : 0;
     const double per = (8.0 * ns_steps + 12.0 * (nprod - ns_steps) - 4.0 * ndual);
     ChainCost c;
-    c.flops = (fmt.f16 ? 1.0 : 3.0) * sym_flops(s_r, s_r) * nb * nprod;
-    c.bytes = (fmt.f16 ? per / 2.0 + 2.0 : per) * s_r * s_r * nb;
+    c.flops = (fmt.f16 && !fused ? 1.0 : 3.0) * sym_flops(s_r, s_r) * nb * nprod;
+    // fused (in LDS): only A_0 in and P_T out, hi / lo pairs
+    c.bytes = (fused ? 8.0 : fmt.f16 ? per / 2.0 + 2.0 : per) * s_r * s_r * nb;
     return c;
+}
+
+// A GRAM chain whose compact matrices have s <= 64 runs in one launch with
+// its matrices in LDS (launch_chain_small), unless the caller asks for one
+// launch per product; its Gram matrix then comes as a hi / lo pair.
+bool fused_chain(int64_t s_k, const dion2_options& opt) {
+    return !opt.ns_chain_per_product && s_k <= kSmallChainS;
+}
+ChainFmt chain_fmt_for(const ChainFmt& fmt, bool fused) {
+    ChainFmt f = fmt;
+    if (fused) f.f16 = false;
+    return f;
 }
 
 // The s x s products of `batch` matrices of padded side s_pad (buffers sq,
@@ -721,11 +735,31 @@ hipError_t chain_f16(const Plan& C, uint16_t* const* sq, int ns_steps, const dio
 
 hipError_t gram_chain(int batch, int64_t s_pad, int64_t s_k, uint16_t* const* sq, int ns_steps,
                       const dion2_options& opt, const ChainFmt& fmt, const ChainCost& cost,
-                      hipStream_t stream, int* cur_out) {
+                      hipStream_t stream, int* cur_out, bool fused) {
     Plan C{};
     C.batch = batch;
     C.s_pad = s_pad;
     C.s_k = s_k;
+    if (fused) {
+        // P_T lands where the launch-per-product chain leaves it
+        const int cur = (ns_steps - 1) & 1;
+        SmallChainArgs c{};
+        c.Ah = sq[SQ_AHI];
+        c.Al = sq[SQ_ALO];
+        c.Ph = sq[cur ? SQ_P1HI : SQ_P0HI];
+        c.Pl = sq[cur ? SQ_P1LO : SQ_P0LO];
+        c.s_pad = s_pad;
+        c.s_k = (int)s_k;
+        c.ns_steps = ns_steps;
+        c.batch = batch;
+        for (int t = 0; t < ns_steps; ++t) {
+            const float* cf = opt.ns_coeffs ? opt.ns_coeffs + 3 * t : kMuonQuintic;
+            for (int i = 0; i < 3; ++i) c.cf[t][i] = cf[i];
+        }
+        *cur_out = cur;
+        return timed(DION2_PHASE_NS_POLY, cost.flops, cost.bytes, 1, stream,
+                     [&] { return launch_chain_small(c, stream); });
+    }
     if (fmt.f16)
         return timed(DION2_PHASE_NS_POLY, cost.flops, cost.bytes, chain_launches(ns_steps), stream,
                      [&] { return chain_f16(C, sq, ns_steps, opt, fmt, stream, cur_out); });
@@ -801,11 +835,13 @@ hipError_t gram_final(const Plan& P, const uint16_t* Ph, const uint16_t* Pl, con
 hipError_t ns_gram(const Plan& P, const uint16_t* Z, const uint16_t* Zlo, uint16_t* const* sq, float* O,
                    int ns_steps, const dion2_options& opt, const ChainFmt& fmt, const FinalSpec& fin,
                    hipStream_t stream) {
-    hipError_t e = gram_a0(P, Z, Zlo, sq[SQ_AHI], sq[SQ_ALO], fmt, stream);
+    const bool fused = fused_chain(P.s_k, opt);
+    const ChainFmt cf = chain_fmt_for(fmt, fused);
+    hipError_t e = gram_a0(P, Z, Zlo, sq[SQ_AHI], sq[SQ_ALO], cf, stream);
     if (e != hipSuccess) return e;
     int cur = 0;
-    e = gram_chain(P.batch, P.s_pad, P.s_k, sq, ns_steps, opt, fmt, chain_cost(P, ns_steps, fmt), stream,
-                   &cur);
+    e = gram_chain(P.batch, P.s_pad, P.s_k, sq, ns_steps, opt, cf, chain_cost(P, ns_steps, cf, fused), stream,
+                   &cur, fused);
     if (e != hipSuccess) return e;
     return gram_final(P, cur ? sq[SQ_P1HI] : sq[SQ_P0HI], cur ? sq[SQ_P1LO] : sq[SQ_P0LO], Z, Zlo, O,
                       fin, stream);
@@ -1303,6 +1339,7 @@ int groups_impl(const dion2_group* groups, int ngroups, float alpha, float mu, f
 
     struct Chain {
         int64_t s_pad, s_k = 0;
+        bool fused = false;   // one launch, in LDS (every member has s <= 64)
         int batch = 0;
         size_t off = 0, S_bytes = 0;
     };
@@ -1326,11 +1363,13 @@ int groups_impl(const dion2_group* groups, int ngroups, float alpha, float mu, f
         const int64_t st_tiles = P.s_pad / kTile;
         const bool small = (int64_t)P.batch * st_tiles * (st_tiles + 1) / 2 < kChainShareTiles;
         if (P.gram && ns_steps > 0 && small) {
+            const bool fused = fused_chain(P.s_k, opt);
             int c = 0;
-            while (c < (int)chains.size() && chains[c].s_pad != P.s_pad) ++c;
+            while (c < (int)chains.size() && (chains[c].s_pad != P.s_pad || chains[c].fused != fused)) ++c;
             if (c == (int)chains.size()) {
                 chains.push_back(Chain{});
                 chains[c].s_pad = P.s_pad;
+                chains[c].fused = fused;
             }
             // the shared products sum to the widest member's real side
             chains[c].s_k = std::max(chains[c].s_k, P.s_k);
@@ -1453,7 +1492,8 @@ int groups_impl(const dion2_group* groups, int ngroups, float alpha, float mu, f
         if (st != DION2_OK) return st;
         fins[g] = make_final(P, ms, b, lr, ns_steps, gopt[g]);
         if (c >= 0) {
-            e = gram_a0(P, b.Z0, P.master ? b.Z1 : nullptr, b.sbuf[SQ_AHI], b.sbuf[SQ_ALO], fmt, s);
+            e = gram_a0(P, b.Z0, P.master ? b.Z1 : nullptr, b.sbuf[SQ_AHI], b.sbuf[SQ_ALO],
+                        chain_fmt_for(fmt, chains[c].fused), s);
             if (e != hipSuccess) return hip_fail(e, "launch K4 Gram");
             if (nS > 1) {
                 e = hipEventRecord(ev_a0[g], s);
@@ -1478,7 +1518,7 @@ int groups_impl(const dion2_group* groups, int ngroups, float alpha, float mu, f
         ChainCost cost;
         for (int g = 0; g < ngroups; ++g) {
             if (chain_of[g] != c) continue;
-            const ChainCost cg = chain_cost(plans[g], ns_steps, fmt);
+            const ChainCost cg = chain_cost(plans[g], ns_steps, chain_fmt_for(fmt, chains[c].fused), chains[c].fused);
             cost.flops += cg.flops;
             cost.bytes += cg.bytes;
             if (nS > 1) {
@@ -1488,8 +1528,8 @@ int groups_impl(const dion2_group* groups, int ngroups, float alpha, float mu, f
         }
         uint16_t* sq[SQ_GRAM_COUNT];
         for (int i = 0; i < SQ_GRAM_COUNT; ++i) sq[i] = chain_buf(c, i);
-        e = gram_chain(chains[c].batch, chains[c].s_pad, chains[c].s_k, sq, ns_steps, opt, fmt, cost, s,
-                       &chain_cur[c]);
+        e = gram_chain(chains[c].batch, chains[c].s_pad, chains[c].s_k, sq, ns_steps, opt,
+                       chain_fmt_for(fmt, chains[c].fused), cost, s, &chain_cur[c], chains[c].fused);
         if (e != hipSuccess) return hip_fail(e, "launch K4 s x s products");
         if (nS > 1) {
             e = hipEventRecord(ev_chain[c], s);

@@ -320,6 +320,24 @@ struct GemmArgs {
 };
 hipError_t launch_gemm(const GemmArgs& a, GemmEpi epi, int npass, hipStream_t s);
 
+// The GRAM form's chain of s x s products for s <= 64 (s_k, the K extent,
+// 32 or 64) in one launch, one block per matrix: A_0 in, P_T out, both as
+// bf16 hi / lo pairs [batch][s_pad][s_pad]; P_T is zero outside
+// [0, s_k)^2. Every product is computed as the launch-per-product chain
+// computes it, so P_T is bitwise that chain's on [0, s_k)^2.
+constexpr int kSmallChainS = 64;
+constexpr int kChainMaxSteps = 16;   // DION2_MAX_NS_STEPS
+struct SmallChainArgs {
+    const uint16_t* Ah;
+    const uint16_t* Al;
+    uint16_t* Ph;
+    uint16_t* Pl;
+    int64_t s_pad;
+    int s_k, ns_steps, batch;
+    float cf[kChainMaxSteps][3];   // (a, b, c) per step
+};
+hipError_t launch_chain_small(const SmallChainArgs& a, hipStream_t s);
+
 // out[b][j][i] = in[b][i][j] for bf16 [batch][rows][cols] stacks (both sides
 // multiples of 64; `stride` elements between matrices on both sides).
 hipError_t launch_transpose_bf16(const uint16_t* in, uint16_t* out, int64_t rows, int64_t cols, int batch,

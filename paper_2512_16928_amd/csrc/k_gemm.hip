@@ -650,6 +650,151 @@ __global__ __launch_bounds__(T::THREADS) void gemm(GemmArgs a) {
     }
 }
 
+// ---- the GRAM chain of a compact matrix with s <= 64, in one block
+//
+// The s x s matrices stay in LDS as bf16 hi / lo planes of 64 rows (pitch
+// kSmallPitch entries: 144-byte rows put the 32 rows of a fragment read on
+// distinct banks). Every product is the one the launch-per-product chain
+// makes: per 16-deep k-step hi*lo, lo*hi, then hi*hi into fp32
+// accumulators, the same epilogue arithmetic and hi / lo split, and exactly
+// symmetric storage (entries on and above the diagonal computed, mirrored
+// below it). Waves 0..2 take the upper 32 x 32 blocks (0,0), (0,1), (1,1);
+// with s_k = 32 (KS) only the first. Entries past s_k are never read.
+constexpr int kSmallPitch = 72;
+constexpr int kSmallPlane = kSmallChainS * kSmallPitch;
+enum { SP_A = 0, SP_Q = 2, SP_T = 4, SP_P = 6, SP_PLANES = 10 };   // hi, lo; P twice (6 and 8)
+
+// dst[p] = x y[p] (x, y[p] symmetric, given by rows) on this wave's block
+// (bi, bj), for NP products sharing x; their MFMA chains interleave, each in
+// its own order. With QPOLY (NP = 1, x = y = A_t) dst = c x y + b x + a I:
+// Q_t.
+template <int KS, int NP, bool QPOLY>
+__device__ __forceinline__ void small_products(uint16_t* pl, int x, const int (&y)[NP], const int (&dst)[NP],
+                                               int bi, int bj, int lane, float ca, float cb, float cc) {
+    static_assert(!QPOLY || NP == 1, "the polynomial epilogue takes one product");
+    constexpr int NK = KS / 16;
+    const uint16_t* xh = pl + x * kSmallPlane;
+    const uint16_t* xl = xh + kSmallPlane;
+    const int arow = bi * 32 + (lane & 31), brow = bj * 32 + (lane & 31);
+    const int half = lane >> 5;
+    auto entry = [&](int r, int& m, int& n) {
+        m = bi * 32 + (r >> 2) * 8 + (lane >> 5) * 4 + (r & 3);
+        n = bj * 32 + (lane & 31);
+    };
+    // the epilogue's A entries (QPOLY) and every fragment first, then the MFMAs
+    float a0[16];
+    if constexpr (QPOLY) {
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+            int m, n;
+            entry(r, m, n);
+            a0[r] = bf16_bits_to_f32(xh[m * kSmallPitch + n]) + bf16_bits_to_f32(xl[m * kSmallPitch + n]);
+        }
+    }
+    bf16x8 ah[NK], al[NK], bh[NP][NK], bl[NP][NK];
+#pragma unroll
+    for (int k = 0; k < NK; ++k) {
+        const int kc = 16 * k + 8 * half;
+        ah[k] = *reinterpret_cast<const bf16x8*>(xh + arow * kSmallPitch + kc);
+        al[k] = *reinterpret_cast<const bf16x8*>(xl + arow * kSmallPitch + kc);
+#pragma unroll
+        for (int p = 0; p < NP; ++p) {
+            const uint16_t* yh = pl + y[p] * kSmallPlane;
+            bh[p][k] = *reinterpret_cast<const bf16x8*>(yh + brow * kSmallPitch + kc);
+            bl[p][k] = *reinterpret_cast<const bf16x8*>(yh + kSmallPlane + brow * kSmallPitch + kc);
+        }
+    }
+    f32x16 acc[NP];
+#pragma unroll
+    for (int p = 0; p < NP; ++p)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) acc[p][r] = 0.f;
+#pragma unroll
+    for (int k = 0; k < NK; ++k) {
+#pragma unroll
+        for (int p = 0; p < NP; ++p) acc[p] = mfma32(ah[k], bl[p][k], acc[p]);
+#pragma unroll
+        for (int p = 0; p < NP; ++p) acc[p] = mfma32(al[k], bh[p][k], acc[p]);
+#pragma unroll
+        for (int p = 0; p < NP; ++p) acc[p] = mfma32(ah[k], bh[p][k], acc[p]);
+    }
+#pragma unroll
+    for (int p = 0; p < NP; ++p) {
+        uint16_t* oh = pl + dst[p] * kSmallPlane;
+        uint16_t* ol = oh + kSmallPlane;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+            int m, n;
+            entry(r, m, n);
+            if (bi == bj && m > n) continue;   // below the diagonal: the mirror of (n, m)
+            float v = acc[p][r];
+            if constexpr (QPOLY) {
+                v = cb * a0[r] + cc * v;
+                if (m == n) v += ca;
+            }
+            const uint16_t h = f32_to_bf16(v);
+            const uint16_t l = (uint16_t)(pack2(v - bf16_bits_to_f32(h), 0.f) & 0xffffu);
+            oh[m * kSmallPitch + n] = h;
+            ol[m * kSmallPitch + n] = l;
+            if (m != n) {
+                oh[n * kSmallPitch + m] = h;
+                ol[n * kSmallPitch + m] = l;
+            }
+        }
+    }
+}
+
+template <int KS>
+__global__ __launch_bounds__(256) void chain_small(SmallChainArgs a) {
+    __shared__ __attribute__((aligned(16))) uint16_t pl[SP_PLANES * kSmallPlane];
+    const int b = blockIdx.x;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int64_t s2 = a.s_pad * a.s_pad;
+    // A_0's [0, 64)^2 corner (zero past s_k) into the A planes, 16 bytes a lane
+    constexpr int kChunks = kSmallChainS * (kSmallChainS / 8);   // per plane
+    for (int i = tid; i < 2 * kChunks; i += 256) {
+        const int plane = i / kChunks, r = (i % kChunks) / 8, c = i % 8;
+        const uint16_t* src = (plane ? a.Al : a.Ah) + (int64_t)b * s2 + (int64_t)r * a.s_pad + 8 * c;
+        *reinterpret_cast<uint4*>(pl + (SP_A + plane) * kSmallPlane + r * kSmallPitch + 8 * c) = ldg<uint4>(src);
+    }
+    __syncthreads();
+    const int bi = wave == 2 ? 1 : 0, bj = wave == 0 ? 0 : 1;
+    const bool active = wave == 0 || (KS > 32 && wave < 3);
+    int cur = 0;
+    for (int t = 0; t < a.ns_steps; ++t) {
+        const float ca = a.cf[t][0], cb = a.cf[t][1], cc = a.cf[t][2];
+        const int q = t == 0 ? SP_P : SP_Q;   // the first Q_t is P itself
+        if (active) small_products<KS, 1, true>(pl, SP_A, {SP_A}, {q}, bi, bj, lane, ca, cb, cc);
+        __syncthreads();
+        // P <- Q_t P (t > 0) and T = Q_t A (t < T - 1), then A <- Q_t T
+        const bool do_p = t > 0, do_t = t + 1 < a.ns_steps;
+        const int pin = SP_P + 2 * cur, pout = SP_P + 2 * (1 - cur);
+        if (active) {
+            if (do_p && do_t) small_products<KS, 2, false>(pl, q, {pin, SP_A}, {pout, SP_T}, bi, bj, lane, 0.f, 0.f, 0.f);
+            else if (do_p) small_products<KS, 1, false>(pl, q, {pin}, {pout}, bi, bj, lane, 0.f, 0.f, 0.f);
+            else if (do_t) small_products<KS, 1, false>(pl, q, {SP_A}, {SP_T}, bi, bj, lane, 0.f, 0.f, 0.f);
+        }
+        __syncthreads();
+        if (do_p) cur = 1 - cur;
+        if (do_t) {
+            if (active) small_products<KS, 1, false>(pl, q, {SP_T}, {SP_A}, bi, bj, lane, 0.f, 0.f, 0.f);
+            __syncthreads();
+        }
+    }
+    // P_T out: [0, s_k)^2 from LDS, zero elsewhere
+    const uint16_t* ph = pl + (SP_P + 2 * cur) * kSmallPlane;
+    const int64_t cpr = a.s_pad / 8;   // 16-byte chunks per row
+    for (int64_t i = tid; i < 2 * a.s_pad * cpr; i += 256) {
+        const int plane = (int)(i / (a.s_pad * cpr));
+        const int64_t rem = i % (a.s_pad * cpr);
+        const int64_t r = rem / cpr, c = rem % cpr;
+        uint4 v = make_uint4(0u, 0u, 0u, 0u);
+        if (r < KS && 8 * c < KS) v = *reinterpret_cast<const uint4*>(ph + plane * kSmallPlane + r * kSmallPitch + 8 * c);
+        stg((plane ? a.Pl : a.Ph) + (int64_t)b * s2 + r * a.s_pad + 8 * c, v);
+    }
+}
+
 constexpr unsigned kMaxGridZ = 65535;   // the grid's z extent holds the batch
 
 template <int NPASS, int EPI, typename T, bool SYM = false>
@@ -841,6 +986,15 @@ hipError_t launch_gemm(const GemmArgs& a, GemmEpi epi, int npass, hipStream_t s)
             break;
     }
     return hipErrorInvalidValue;
+}
+
+hipError_t launch_chain_small(const SmallChainArgs& a, hipStream_t s) {
+    if (a.s_k < 32 || a.s_k > kSmallChainS || a.s_k % 32 || a.s_pad < kSmallChainS || a.s_pad % 8 ||
+        a.ns_steps < 1 || a.ns_steps > kChainMaxSteps || a.batch < 1)
+        return hipErrorInvalidValue;
+    if (a.s_k == 32) hipLaunchKernelGGL(chain_small<32>, dim3((unsigned)a.batch), dim3(256), 0, s, a);
+    else hipLaunchKernelGGL(chain_small<64>, dim3((unsigned)a.batch), dim3(256), 0, s, a);
+    return hipGetLastError();
 }
 
 hipError_t launch_transpose_bf16(const uint16_t* in, uint16_t* out, int64_t rows, int64_t cols, int batch,

@@ -95,6 +95,8 @@ def phase_of(kernel: str):
         return "apply"
     if k.startswith("transpose"):    # X^T for the Direct form's update
         return "ns_update"
+    if k.startswith("chain_small"):  # the whole s x s chain of s <= 64 in one launch
+        return "ns_poly"
     m = re.match(r"gemm<(\d+), (?:\(dion2::GemmEpi\))?(\d)", k)
     if m:
         npass, epi = int(m.group(1)), int(m.group(2))

@@ -38,7 +38,8 @@ CHAINS = pytest.mark.parametrize("chain", [binding.CHAIN_HILO, binding.CHAIN_F16
 
 def run_gpu(W, M, G, alpha, ns_steps=5, axis=AXIS_AUTO, mu=0.95, lr=0.02, coeffs=None,
             decay_all=False, form=binding.NS_AUTO, rand=None, chain=binding.CHAIN_HILO,
-            master=binding.MASTER_BF16, eps=1e-7, dbg_compact=None, dbg_compact_lo=None, norms=True):
+            master=binding.MASTER_BF16, eps=1e-7, dbg_compact=None, dbg_compact_lo=None, norms=True,
+            per_product=False):
     """One library call on stacks [B, rows, cols]; returns host copies and the
     debug outputs (norms=False leaves out the l1 norms, which the Random
     rule's single column pass does not compute)."""
@@ -57,7 +58,7 @@ def run_gpu(W, M, G, alpha, ns_steps=5, axis=AXIS_AUTO, mu=0.95, lr=0.02, coeffs
     binding.dion2_step_ex(W, M, G, alpha, mu, lr, ns_steps, axis, ns_coeffs=coeffs, ns_eps=eps,
                           decay_all=decay_all, dbg_sel_idx=sel, dbg_norms=nrm if norms else None, dbg_update=upd,
                           ns_form=form, ns_chain=chain, ns_master=master, dbg_compact=dbg_compact,
-                          dbg_compact_lo=dbg_compact_lo, **extra)
+                          dbg_compact_lo=dbg_compact_lo, ns_chain_per_product=per_product, **extra)
     torch.cuda.synchronize()
     return dict(W=W.cpu(), M=M.cpu(), K=sel.cpu(), norms=nrm.cpu() if norms else None, O=upd.cpu(), W0=W0, M0=M0,
                 G=G.cpu(), axis=ax, k=k)
@@ -277,6 +278,63 @@ def test_f16_chain_ragged(hip_device, rows, cols, alpha, axis):
 
 
 MASTER_TOL = 2e-3   # fp32 master: X as a hi/lo pair, about 16 significant bits throughout
+
+SCHEDULE = [(3.4445, -4.7750, 2.0315)] * 3 + [(1.5, -0.5, 0.0)] * 2
+
+
+@pytest.mark.parametrize("rows,cols,alpha,axis,wdt,steps,coeffs,chain,master", [
+    (200, 328, 0.25, AXIS_AUTO, "bf16", 5, None, binding.CHAIN_HILO, binding.MASTER_BF16),   # rows, s = 50
+    (328, 200, 0.25, AXIS_AUTO, "bf16", 5, None, binding.CHAIN_HILO, binding.MASTER_BF16),   # columns, s = 50
+    (256, 256, 0.25, AXIS_ROWS, "f32", 5, None, binding.CHAIN_HILO, binding.MASTER_BF16),    # fp32 W, s = 64
+    (96, 1000, 0.25, AXIS_AUTO, "bf16", 5, None, binding.CHAIN_HILO, binding.MASTER_BF16),   # s = 24: one block
+    (64, 256, 0.5, AXIS_COLS, "bf16", 5, None, binding.CHAIN_HILO, binding.MASTER_BF16),     # Z = L^T, s = 64
+    (130, 75, 0.5, AXIS_AUTO, "bf16", 1, None, binding.CHAIN_HILO, binding.MASTER_BF16),     # P = Q_0
+    (130, 75, 0.5, AXIS_AUTO, "bf16", 2, None, binding.CHAIN_HILO, binding.MASTER_BF16),
+    (200, 328, 0.25, AXIS_AUTO, "bf16", 16, None, binding.CHAIN_HILO, binding.MASTER_BF16),  # the longest schedule
+    (200, 328, 0.25, AXIS_AUTO, "bf16", 5, SCHEDULE, binding.CHAIN_HILO, binding.MASTER_BF16),
+    (200, 328, 0.25, AXIS_AUTO, "bf16", 5, None, binding.CHAIN_F16, binding.MASTER_BF16),    # runs in hi / lo
+    (200, 328, 0.25, AXIS_AUTO, "bf16", 5, None, binding.CHAIN_HILO, binding.MASTER_FP32),
+])
+def test_fused_small_chain(hip_device, rows, cols, alpha, axis, wdt, steps, coeffs, chain, master):
+    """A GRAM chain with s <= 64 runs in one launch, its matrices in LDS: bitwise
+    the chain with one launch per product (hi / lo, whatever ns_chain asks,
+    since the fp16 storage only saves memory traffic), and within tolerance of
+    the oracle."""
+    wl = one_group_workload(rows, cols, axis=axis, w_dtype=wdt, name=f"fused{rows}x{cols}")
+    W, M, G = workloads.make_group(wl, 0, hip_device)
+    fused = run_gpu(W.clone(), M.clone(), G, alpha, steps, axis, coeffs=coeffs, chain=chain, master=master)
+    split = run_gpu(W.clone(), M.clone(), G, alpha, steps, axis, coeffs=coeffs, master=master, per_product=True)
+    assert torch.equal(fused["O"], split["O"]), "O"
+    assert torch.equal(fused["M"], split["M"]), "M"
+    assert torch.equal(fused["W"].view(torch.int32 if wdt == "f32" else torch.int16),
+                       split["W"].view(torch.int32 if wdt == "f32" else torch.int16)), "W"
+    err = check_matrix(fused, 0, alpha, steps, axis, coeffs=coeffs,
+                       ns_tol=MASTER_TOL if master == binding.MASTER_FP32 else NS_TOL)
+    print(f"fused chain {rows}x{cols} alpha {alpha} steps {steps}: {err:.3e}")
+
+
+def test_fused_small_chain_grouped(hip_device):
+    """A grouped call gathers the groups with s <= 64 into one fused chain and
+    keeps those with 64 < s <= 128 (the same padded size) on a chain of
+    launches: bitwise the per-group calls, and bitwise the grouped call with
+    one launch per product."""
+    wl = workloads.Workload("gfused", "test",
+                            (workloads.Group("a", 200, 328, 2), workloads.Group("b", 328, 200, 3),
+                             workloads.Group("c", 96, 1000, 1), workloads.Group("d", 384, 640, 2),
+                             workloads.Group("e", 256, 1024, 2, AXIS_ROWS)), (0.25,))
+    stacks = [workloads.make_group(wl, gi, hip_device) for gi in range(len(wl.groups))]
+    solo = [tuple(t.clone() for t in st) for st in stacks]
+    split = [tuple(t.clone() for t in st) for st in stacks]
+    for (W, M, G), grp in zip(solo, wl.groups):
+        binding.dion2_step_ex(W, M, G, 0.25, 0.95, 0.02, 5, grp.axis)
+    binding.dion2_step_groups([(W, M, G, grp.axis) for (W, M, G), grp in zip(stacks, wl.groups)], 0.25)
+    binding.dion2_step_groups([(W, M, G, grp.axis) for (W, M, G), grp in zip(split, wl.groups)], 0.25,
+                              ns_chain_per_product=True)
+    torch.cuda.synchronize()
+    for gi, ((W, M, _), (Ws, Ms, _), (Wp, Mp, _)) in enumerate(zip(stacks, solo, split)):
+        assert torch.equal(M, Ms) and torch.equal(M, Mp), f"group {gi}: M"
+        assert torch.equal(W.view(torch.int16), Ws.view(torch.int16)), f"group {gi}: W against its own call"
+        assert torch.equal(W.view(torch.int16), Wp.view(torch.int16)), f"group {gi}: W against per-product"
 
 
 @pytest.mark.parametrize("rows,cols,alpha,axis,wdt", [
@@ -1002,9 +1060,11 @@ def test_groups_equal_per_group_calls(hip_device, rand, gs):
     for gi, ((W, M, _), (Ws, Ms, _)) in enumerate(zip(stacks, solo)):
         assert torch.equal(M, Ms), f"group {gi}: momentum"
         assert torch.equal(W.view(torch.int16), Ws.view(torch.int16)), f"group {gi}: weights"
-    # two chains of 14 launches (5 Newton-Schulz steps) instead of one per
-    # GRAM group, plus the DIRECT group's 5 polynomial products
-    assert prof["ns_poly"]["launches"] == 2 * 14 + 5
+    # one launch for the fused chain of the groups with s <= 64 (a, b, d),
+    # a chain of 14 launches (5 Newton-Schulz steps) for c (s = 96, the same
+    # padded size) and one for f (s = 256), plus the DIRECT group's 5
+    # polynomial products
+    assert prof["ns_poly"]["launches"] == 1 + 2 * 14 + 5
     # the first group against the oracle (its own call, with debug outputs)
     W, M, G = workloads.make_group(GROUPED, 0, hip_device)
     res = run_gpu(W, M, G, alpha, rand=(rand[0], rand[1], rand[2]) if rand else None)

@@ -15,6 +15,7 @@ def test_phase_of_kernel_names():
         "dion2::(anonymous namespace)::momentum_cols_final(double const*, int, long)": "momentum",
         "dion2::(anonymous namespace)::select_topk(dion2::SelectArgs)": "select",
         "void dion2::(anonymous namespace)::gather_rows<4>(dion2::GatherArgs)": "gather",
+        "dion2::(anonymous namespace)::chain_small(dion2::SmallChainArgs)": "ns_poly",
         "void dion2::(anonymous namespace)::update_cols<4, unsigned short>(dion2::GatherArgs)": "gather",
         "void dion2::(anonymous namespace)::apply_cols<4, unsigned short>(dion2::ApplyArgs)": "apply",
         "void dion2::(anonymous namespace)::gemm<1, 0, dion2::(anonymous namespace)::Tile<1, 0, 128, 128, 32, 2, 2, 4>, true>(dion2::GemmArgs)": "ns_gram",
