@@ -23,6 +23,9 @@
 // The GRAM form's chain of s x s products runs the same way on bf16 hi / lo
 // pairs (three passes), or, as an option, on scaled fp16 matrices with
 // v_mfma_f32_32x32x16_f16 (one pass; EPI_H16 and EPI_QPOLY_H16 store fp16).
+// For s <= 64 the whole chain is one launch instead (chain_small): one block
+// per matrix keeps its s x s matrices in LDS and computes every product as
+// the launches would, bitwise.
 // With the fp32 master Z itself is a hi / lo pair: the Gram matrix takes
 // three passes, and so does the final product, whose [K][N] operand then
 // has a lo tile read through the same transposing LDS reads.
