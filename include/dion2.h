@@ -119,8 +119,10 @@ typedef enum dion2_ns_form {
                             ns_steps > DION2_DIRECT_MAX_STEPS, else DIRECT     */
     DION2_NS_DIRECT = 1, /* iterate on X (s x l). X is rounded to bf16 after
                             every step, so the error grows with the step
-                            count: at most DION2_DIRECT_MAX_STEPS steps, more
-                            return DION2_ERR_UNSUPPORTED                      */
+                            count and is largest where few directions carry
+                            it: at most DION2_DIRECT_MAX_STEPS steps, and
+                            only for s > 128 (more than one tile a side);
+                            other calls return DION2_ERR_UNSUPPORTED        */
     DION2_NS_GRAM = 2    /* iterate on s x s matrices, X read twice            */
 } dion2_ns_form;
 
@@ -128,7 +130,9 @@ typedef enum dion2_ns_form {
    bf16 arithmetic on near-square compact matrices puts the relative
    Frobenius error of O at about 1.6e-2 after 6 steps and 2.1e-2 after 8,
    against 1.2e-2 after the default 5; the GRAM form stays at its 5-step
-   error. */
+   error. On compact matrices of one tile a side (s <= 128) the same
+   emulation reached 3.6e-2 after 5 steps (s = 3) and 2.2e-2 after 6
+   (s = 32), so DIRECT is refused there; AUTO takes GRAM on them anyway. */
 #define DION2_DIRECT_MAX_STEPS 6
 
 typedef enum dion2_ns_chain {
@@ -253,7 +257,8 @@ int dion2_step_batched(void* const* W, float* const* M, const void* const* G,
        precision (ns_coeffs, ns_eps, ns_form, ns_chain, ns_master);
      - the storage types of W and G, a caller workspace and debug outputs.
    Errors as for every entry point; in addition DION2_ERR_UNSUPPORTED for
-   ns_form DIRECT with more than DION2_DIRECT_MAX_STEPS steps, and
+   ns_form DIRECT with more than DION2_DIRECT_MAX_STEPS steps or a compact
+   matrix of at most 128 lines a side, and
    DION2_ERR_WORKSPACE for a caller workspace smaller than
    dion2_workspace_size_ex gives for the same arguments. */
 int dion2_step_ex(void* W, float* M, const void* G, int batch, int64_t rows,
@@ -322,7 +327,8 @@ int dion2_step_groups(const dion2_group* groups, int ngroups, float alpha,
    a call with these arguments under any options and step count: the
    largest of the GRAM order with DION2_MASTER_FP32, and the GRAM and DIRECT
    orders under the Random rule (whose column selection keeps per-block
-   partial sums). Returns 0 for invalid arguments. */
+   partial sums; DIRECT only where it is accepted, s > 128). Returns 0 for
+   invalid arguments. */
 size_t dion2_workspace_size(int batch, int64_t rows, int64_t cols,
                             float alpha, int axis);
 

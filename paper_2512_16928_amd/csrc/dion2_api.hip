@@ -127,6 +127,17 @@ int make_plan(int batch, int64_t rows, int64_t cols, float alpha, int axis, int 
     // s = 352 padded to 384, one slice in twelve.)
     P.s_k = round_up(P.z_is_L ? P.k : P.d_oth, kSliceK);
     P.l_k = round_up(P.z_is_L ? P.d_oth : P.k, kSliceK);
+    // With a compact matrix of one tile a side the DIRECT form's bf16
+    // rounding of X after every step lands on a few directions: an emulation
+    // of its arithmetic put O up to 3.6e-2 from the exact iteration after 5
+    // steps (s = 3) and 2.2e-2 after 6 (s = 32), against 1.4e-2 from s = 128
+    // on. AUTO takes GRAM there at the same cost; a forced DIRECT is refused.
+    if (ns_form == DION2_NS_DIRECT && P.s_pad <= kTile)
+        return fail(DION2_ERR_UNSUPPORTED,
+                    "ns_form DIRECT needs a compact matrix of more than %d lines a side (s = %lld): on "
+                    "one tile its bf16 rounding of X after every step can exceed the 2e-2 accuracy "
+                    "bound; the GRAM form, which AUTO takes there, costs the same",
+                    kTile, (long long)(P.z_is_L ? P.k : P.d_oth));
     // The GRAM form trades 2 (s x l) GEMMs and the X traffic of every step
     // for about four three-pass s x s products; it pays once X is wide. With
     // a single tile a side (s <= 128) both forms cost a few microseconds of
@@ -1630,13 +1641,19 @@ size_t dion2_workspace_size(int batch, int64_t rows, int64_t cols, float alpha, 
         bool master, random;
     };
     const Case cases[] = {{DION2_NS_GRAM, true, false}, {DION2_NS_GRAM, false, true}, {DION2_NS_DIRECT, false, true}};
+    const std::string saved = g_last_error;   // a size query leaves the last error alone
     size_t best = 0;
     for (const Case& c : cases) {
         Plan P;
-        if (make_plan(batch, rows, cols, alpha, axis, c.form, 1, &P, true, c.master, c.random) != DION2_OK)
+        const int st = make_plan(batch, rows, cols, alpha, axis, c.form, 1, &P, true, c.master, c.random);
+        if (st == DION2_ERR_UNSUPPORTED && c.form == DION2_NS_DIRECT) continue;   // one tile: no DIRECT
+        if (st != DION2_OK) {
+            g_last_error = saved;
             return 0;
+        }
         best = P.total > best ? P.total : best;
     }
+    g_last_error = saved;
     return best;
 }
 

@@ -247,7 +247,39 @@ def test_workspace_size(lib):
             for ns in (0, 1, 5, 6, 16):
                 need = ws_ex(*shape, AXIS_AUTO, ns, **kw)
                 assert need <= top, (shape, kw, ns)
-                assert need > 0 or (kw.get("ns_form") == binding.NS_DIRECT and ns > 6), (shape, kw, ns)
+                refused = kw.get("ns_form") == binding.NS_DIRECT and (ns > 6 or one_tile(*shape))
+                assert need > 0 or refused, (shape, kw, ns)
+
+
+def one_tile(batch, rows, cols, alpha, axis=AXIS_AUTO):
+    """The compact matrix fits one 128-line tile a side."""
+    k, ax = binding.dion2_plan_info(rows, cols, alpha, axis)
+    d_oth = cols if ax == binding.AXIS_ROWS else rows
+    return min(k, d_oth) <= 128
+
+
+def test_direct_form_needs_more_than_one_tile(lib):
+    """On a compact matrix of one tile a side the DIRECT form's bf16 rounding
+    of X after every step can exceed the 2e-2 bound, so a forced DIRECT is
+    refused there (nothing launched) while AUTO and GRAM run; from 129 lines
+    it is accepted, and the size without options still covers every plan."""
+    def ex(rows, cols, alpha, form):
+        opt = Options()
+        lib.dion2_options_init(ctypes.byref(opt))
+        opt.ns_form = form
+        return lib.dion2_step_ex(FAKE, FAKE, FAKE, 1, rows, cols, alpha, 0.95, 0.02, 5, -1,
+                                 ctypes.byref(opt), None)
+    for rows, cols, alpha in ((256, 256, 0.25), (640, 256, 0.5), (12, 68, 0.3), (1, 40, 1.0)):
+        assert one_tile(1, rows, cols, alpha)
+        assert ex(rows, cols, alpha, binding.NS_DIRECT) == DION2_ERR_UNSUPPORTED
+        assert "DIRECT" in binding.dion2_last_error() and "128" in binding.dion2_last_error()
+        assert binding.dion2_workspace_size_ex(1, rows, cols, alpha, AXIS_AUTO, 5, ns_form=binding.NS_DIRECT) == 0
+        for form in (binding.NS_AUTO, binding.NS_GRAM):
+            assert binding.dion2_workspace_size_ex(1, rows, cols, alpha, AXIS_AUTO, 5, ns_form=form) > 0
+        assert binding.dion2_workspace_size(1, rows, cols, alpha) > 0
+    for rows, cols, alpha in ((200, 328, 0.75), (257, 129, 1.0), (384, 384, 0.5)):
+        assert not one_tile(1, rows, cols, alpha)
+        assert binding.dion2_workspace_size_ex(1, rows, cols, alpha, AXIS_AUTO, 5, ns_form=binding.NS_DIRECT) > 0
 
 
 def torch_f32():

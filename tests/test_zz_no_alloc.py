@@ -26,7 +26,7 @@ CALLS = [
     (2048, 2048, 4, 0.25, AXIS_AUTO, {}),                                    # rows, GRAM, fused update
     (640, 256, 3, 0.5, AXIS_AUTO, {}),                                       # columns, k > d_oth
     (384, 384, 2, 0.5, AXIS_ROWS, dict(ns_master=binding.MASTER_FP32)),     # fp32 master
-    (200, 328, 1, 0.25, AXIS_AUTO, dict(ns_form=binding.NS_DIRECT)),        # DIRECT, ragged
+    (200, 328, 1, 0.75, AXIS_AUTO, dict(ns_form=binding.NS_DIRECT)),        # DIRECT, ragged (s = 150)
     (2048, 2048, 1, 1.0, AXIS_AUTO, {}),                                     # DIRECT with X^T (s = 2048)
     (640, 256, 2, 0.25, AXIS_AUTO, dict(select_rule=binding.SELECT_RANDOM)),  # Random rule, one column pass
     (2048, 2048, 4, 0.25, AXIS_AUTO, {}),
