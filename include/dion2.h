@@ -143,10 +143,15 @@ typedef enum dion2_ns_chain {
                              significant bits, so accuracy drops for inputs
                              whose spectrum is dominated by a few directions
                              (kappa(Z)^2 beyond about 2^11); balanced wide
-                             inputs stay within 2x of HILO. With ns_coeffs
-                             that take the chain's values beyond 2^40 the call
-                             fails with DION2_ERR_UNSUPPORTED; a chain of one
-                             step (ns_steps = 1) uses HILO.                   */
+                             inputs stay within 2x of HILO. Taken only on
+                             wide compact matrices (l_pad >= 3 s_pad) with
+                             s > 64; elsewhere (near-square ones, where it
+                             measured up to 0.4 from the exact iteration,
+                             and the one-launch chains of s <= 64) the chain
+                             stays in HILO. With ns_coeffs that take the
+                             chain's values beyond 2^40 the call fails with
+                             DION2_ERR_UNSUPPORTED; a chain of one step
+                             (ns_steps = 1) uses HILO.                        */
 } dion2_ns_chain;
 
 typedef enum dion2_ns_master {
@@ -157,8 +162,12 @@ typedef enum dion2_ns_master {
                               GRAM (DIRECT: DION2_ERR_UNSUPPORTED) and ns_chain
                               HILO (F16: DION2_ERR_INVALID_ARG). Costs three
                               times the Gram products and 1.5 times the final
-                              one; the result is 10 to 70 times closer to the
-                              exact iteration                                */
+                              one; on wide compact matrices the result is 10
+                              to 70 times closer to the exact iteration. On
+                              near-square ones the GRAM order squares their
+                              condition number and the hi/lo chain limits it
+                              (1.2e-2 measured at 78 x 90), still within the
+                              2e-2 bound                                      */
 } dion2_ns_master;
 
 /* Full-control options for dion2_step_ex. Fill with dion2_options_init. */

@@ -670,9 +670,18 @@ ChainCost chain_cost(const Plan& P, int ns_steps, const ChainFmt& fmt, bool fuse
 bool fused_chain(int64_t s_k, const dion2_options& opt) {
     return !opt.ns_chain_per_product && s_k <= kSmallChainS;
 }
-ChainFmt chain_fmt_for(const ChainFmt& fmt, bool fused) {
+// The fp16 chain (ns_chain F16) is taken only where it pays and holds: a
+// chain of launches on a wide compact matrix (l_pad >= 3 s_pad, the shapes
+// AUTO sends to GRAM for their width). On near-square ones the Gram matrix
+// squares a condition number that fp16's 11 bits cannot carry (randomly
+// drawn calls measured O 0.13-0.41 from the exact iteration), so the chain
+// stays in hi / lo there, as it does in LDS.
+bool f16_chain(const ChainFmt& fmt, bool fused, int64_t s_pad, int64_t l_pad) {
+    return fmt.f16 && !fused && l_pad >= 3 * s_pad;
+}
+ChainFmt chain_fmt_for(const ChainFmt& fmt, bool f16) {
     ChainFmt f = fmt;
-    if (fused) f.f16 = false;
+    f.f16 = f16;
     return f;
 }
 
@@ -847,7 +856,7 @@ hipError_t ns_gram(const Plan& P, const uint16_t* Z, const uint16_t* Zlo, uint16
                    int ns_steps, const dion2_options& opt, const ChainFmt& fmt, const FinalSpec& fin,
                    hipStream_t stream) {
     const bool fused = fused_chain(P.s_k, opt);
-    const ChainFmt cf = chain_fmt_for(fmt, fused);
+    const ChainFmt cf = chain_fmt_for(fmt, f16_chain(fmt, fused, P.s_pad, P.l_pad));
     hipError_t e = gram_a0(P, Z, Zlo, sq[SQ_AHI], sq[SQ_ALO], cf, stream);
     if (e != hipSuccess) return e;
     int cur = 0;
@@ -1351,6 +1360,7 @@ int groups_impl(const dion2_group* groups, int ngroups, float alpha, float mu, f
     struct Chain {
         int64_t s_pad, s_k = 0;
         bool fused = false;   // one launch, in LDS (every member has s <= 64)
+        bool f16 = false;     // the fp16 chain (every member wide)
         int batch = 0;
         size_t off = 0, S_bytes = 0;
     };
@@ -1375,12 +1385,16 @@ int groups_impl(const dion2_group* groups, int ngroups, float alpha, float mu, f
         const bool small = (int64_t)P.batch * st_tiles * (st_tiles + 1) / 2 < kChainShareTiles;
         if (P.gram && ns_steps > 0 && small) {
             const bool fused = fused_chain(P.s_k, opt);
+            const bool f16 = f16_chain(fmt, fused, P.s_pad, P.l_pad);
             int c = 0;
-            while (c < (int)chains.size() && (chains[c].s_pad != P.s_pad || chains[c].fused != fused)) ++c;
+            while (c < (int)chains.size() &&
+                   (chains[c].s_pad != P.s_pad || chains[c].fused != fused || chains[c].f16 != f16))
+                ++c;
             if (c == (int)chains.size()) {
                 chains.push_back(Chain{});
                 chains[c].s_pad = P.s_pad;
                 chains[c].fused = fused;
+                chains[c].f16 = f16;
             }
             // the shared products sum to the widest member's real side
             chains[c].s_k = std::max(chains[c].s_k, P.s_k);
@@ -1504,7 +1518,7 @@ int groups_impl(const dion2_group* groups, int ngroups, float alpha, float mu, f
         fins[g] = make_final(P, ms, b, lr, ns_steps, gopt[g]);
         if (c >= 0) {
             e = gram_a0(P, b.Z0, P.master ? b.Z1 : nullptr, b.sbuf[SQ_AHI], b.sbuf[SQ_ALO],
-                        chain_fmt_for(fmt, chains[c].fused), s);
+                        chain_fmt_for(fmt, chains[c].f16), s);
             if (e != hipSuccess) return hip_fail(e, "launch K4 Gram");
             if (nS > 1) {
                 e = hipEventRecord(ev_a0[g], s);
@@ -1529,7 +1543,7 @@ int groups_impl(const dion2_group* groups, int ngroups, float alpha, float mu, f
         ChainCost cost;
         for (int g = 0; g < ngroups; ++g) {
             if (chain_of[g] != c) continue;
-            const ChainCost cg = chain_cost(plans[g], ns_steps, chain_fmt_for(fmt, chains[c].fused), chains[c].fused);
+            const ChainCost cg = chain_cost(plans[g], ns_steps, chain_fmt_for(fmt, chains[c].f16), chains[c].fused);
             cost.flops += cg.flops;
             cost.bytes += cg.bytes;
             if (nS > 1) {
@@ -1540,7 +1554,7 @@ int groups_impl(const dion2_group* groups, int ngroups, float alpha, float mu, f
         uint16_t* sq[SQ_GRAM_COUNT];
         for (int i = 0; i < SQ_GRAM_COUNT; ++i) sq[i] = chain_buf(c, i);
         e = gram_chain(chains[c].batch, chains[c].s_pad, chains[c].s_k, sq, ns_steps, opt,
-                       chain_fmt_for(fmt, chains[c].fused), cost, s, &chain_cur[c], chains[c].fused);
+                       chain_fmt_for(fmt, chains[c].f16), cost, s, &chain_cur[c], chains[c].fused);
         if (e != hipSuccess) return hip_fail(e, "launch K4 s x s products");
         if (nS > 1) {
             e = hipEventRecord(ev_chain[c], s);

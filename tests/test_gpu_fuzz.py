@@ -1,58 +1,117 @@
 """Opt-in (DION2_FUZZ=<cases>): randomly drawn calls against the oracle --
-shapes from 1 to 700 lines a side, selection fractions, axes, Newton-Schulz
-forms and step counts, the fp32 master, fp32 W and G, the Random rule and
-batches of one to three matrices -- each held to the same bar as the fixed
-parity cases: K exact, M and the l1 norms bitwise, O within the tolerance of
-its path, and W bitwise given O (or, for a forced DIRECT on a compact matrix
-of one tile, the call refused). The draw is seeded, so case n is the same
-call on every run."""
+shapes from 1 to 700 lines a side (now and then up to 2500), selection
+fractions, axes, Newton-Schulz forms, step counts and coefficient schedules,
+the fp16 chain, the fp32 master, W and G in either storage type, eps, the
+decay-all ablation, the Random rule and batches of one to three matrices --
+each held to the same bar as the fixed parity cases: K exact, M and the l1
+norms bitwise, O within 2e-2 of the exact iteration whatever the options
+(the fp32 master's tighter 2e-3 holds on wide compact matrices, not on
+near-square ones, where the Gram order squares the condition number), and W
+bitwise given O (or, for a forced DIRECT on a compact matrix of one tile,
+the call refused). And randomly drawn grouped calls, bitwise the per-group
+calls. The draws are seeded, so case n is the same call on every run."""
 import os
 
 import numpy as np
 import pytest
+import torch
 
 from paper_2512_16928_amd import binding, workloads
 from paper_2512_16928_amd.binding import AXIS_AUTO, AXIS_COLS, AXIS_ROWS, NS_AUTO, NS_DIRECT, NS_GRAM
-from test_gpu_parity import MASTER_TOL, NS_TOL, check_matrix, direct_refused, one_group_workload, run_gpu
+from test_gpu_parity import NS_TOL, check_matrix, direct_refused, one_group_workload, run_gpu
 
 CASES = int(os.environ.get("DION2_FUZZ", "0") or 0)
 pytestmark = [pytest.mark.gpu,
               pytest.mark.skipif(CASES <= 0, reason="opt-in randomized sweep (set DION2_FUZZ=<cases>)")]
 
-F16_TOL = 1e-1   # the fp16 chain loses the small directions of ill-conditioned Gram matrices
+STEP_COEFFS = [(3.4445, -4.7750, 2.0315), (1.5, -0.5, 0.0), (3.0, -3.2, 1.2), (2.0, -1.5, 0.5),
+               (1.875, -1.25, 0.375)]
+TO = {"bf16": torch.bfloat16, "f32": torch.float32}
 
 
 def draw(n):
     rng = np.random.default_rng([2512, 16928, n])
-    small = rng.random() < 0.5
-    hi = 130 if small else 700
+    u = rng.random()
+    hi = 130 if u < 0.5 else (700 if u < 0.97 else 2500)
     rows, cols = int(rng.integers(1, hi)), int(rng.integers(1, hi))
     alpha = float(rng.choice([0.01, 0.1, 0.25, 0.3, 0.5, 0.75, 1.0]))
     axis = int(rng.choice([AXIS_AUTO, AXIS_AUTO, AXIS_ROWS, AXIS_COLS]))
     master = binding.MASTER_FP32 if rng.random() < 0.15 else binding.MASTER_BF16
     form = NS_AUTO if master == binding.MASTER_FP32 else int(rng.choice([NS_AUTO, NS_AUTO, NS_DIRECT, NS_GRAM]))
     steps = int(rng.choice([0, 1, 2, 5, 5, 5, 6]))
-    chain = binding.CHAIN_F16 if (form == NS_GRAM and steps >= 2 and rng.random() < 0.3) else binding.CHAIN_HILO
+    coeffs = [STEP_COEFFS[int(i)] for i in rng.integers(0, len(STEP_COEFFS), steps)] \
+        if (steps and rng.random() < 0.2) else None
+    chain = binding.CHAIN_F16 if (form == NS_GRAM and steps >= 2 and coeffs is None and rng.random() < 0.3) \
+        else binding.CHAIN_HILO
     wdt = "f32" if rng.random() < 0.25 else "bf16"
+    gdt = wdt if rng.random() < 0.85 else ("bf16" if wdt == "f32" else "f32")
+    eps = float(rng.choice([1e-7, 1e-7, 1e-7, 0.0, 1e-3]))
+    decay_all = bool(rng.random() < 0.1)
     rand = (int(rng.integers(0, 2**63)), int(rng.integers(0, 2**40)), int(rng.integers(0, 1000))) \
         if rng.random() < 0.2 else None
-    batch = int(rng.integers(1, 4))
-    return dict(rows=rows, cols=cols, alpha=alpha, axis=axis, form=form, steps=steps, chain=chain,
-                master=master, wdt=wdt, rand=rand, batch=batch)
+    batch = int(rng.integers(1, 4)) if hi < 2500 else 1
+    return dict(rows=rows, cols=cols, alpha=alpha, axis=axis, form=form, steps=steps, coeffs=coeffs,
+                chain=chain, master=master, wdt=wdt, gdt=gdt, eps=eps, decay_all=decay_all, rand=rand,
+                batch=batch)
 
 
 @pytest.mark.parametrize("n", range(max(CASES, 0)))
 def test_random_call(hip_device, n):
     c = draw(n)
     print(f"case {n}: {c}", flush=True)
-    wl = one_group_workload(c["rows"], c["cols"], count=c["batch"], axis=c["axis"], w_dtype=c["wdt"],
+    wl = one_group_workload(c["rows"], c["cols"], count=c["batch"], axis=c["axis"], w_dtype="f32",
                             name=f"fuzz{n}")
-    W, M, G = workloads.make_group(wl, 0, hip_device)
+    W, M, G = workloads.make_group(wl, 0, hip_device)   # fp32 W and G, then each to its type
+    W, G = W.to(TO[c["wdt"]]).contiguous(), G.to(TO[c["gdt"]]).contiguous()
     if direct_refused(W, M, G, c["alpha"], c["axis"], c["form"]):
         return   # DIRECT on one tile: refused, nothing run
-    res = run_gpu(W, M, G, c["alpha"], c["steps"], c["axis"], form=c["form"], rand=c["rand"],
-                  chain=c["chain"], master=c["master"], norms=c["rand"] is None)
-    tol = F16_TOL if c["chain"] == binding.CHAIN_F16 else (
-        MASTER_TOL if c["master"] == binding.MASTER_FP32 else NS_TOL)
+    res = run_gpu(W, M, G, c["alpha"], c["steps"], c["axis"], coeffs=c["coeffs"], decay_all=c["decay_all"],
+                  form=c["form"], rand=c["rand"], chain=c["chain"], master=c["master"], eps=c["eps"],
+                  norms=c["rand"] is None)
     for b in range(c["batch"]):
-        check_matrix(res, b, c["alpha"], c["steps"], c["axis"], ns_tol=tol, rand=c["rand"])
+        check_matrix(res, b, c["alpha"], c["steps"], c["axis"], coeffs=c["coeffs"], decay_all=c["decay_all"],
+                     ns_tol=NS_TOL, rand=c["rand"], eps=c["eps"])
+
+
+@pytest.mark.parametrize("n", range(max(CASES // 10, 0)))
+def test_random_grouped_call(hip_device, n):
+    """Two to six groups of random shapes, batches and axes in one grouped
+    call (groups of one padded size sharing a chain, fused or not): bitwise
+    the per-group calls, each of which is checked against the oracle on its
+    first matrix."""
+    rng = np.random.default_rng([2512, 16928, 7, n])
+    ngroups = int(rng.integers(2, 7))
+    shapes = [(int(rng.integers(1, 400)), int(rng.integers(1, 400)), int(rng.integers(1, 4)),
+               int(rng.choice([AXIS_AUTO, AXIS_ROWS, AXIS_COLS]))) for _ in range(ngroups)]
+    alpha = float(rng.choice([0.1, 0.25, 0.5, 1.0]))
+    steps = int(rng.choice([0, 1, 5, 5, 6]))
+    kw = dict(ns_form=int(rng.choice([NS_AUTO, NS_GRAM])))
+    if rng.random() < 0.3:
+        kw.update(select_rule=binding.SELECT_RANDOM, rand_seed=int(rng.integers(0, 2**63)),
+                  rand_step=int(rng.integers(0, 2**40)))
+    if rng.random() < 0.2:
+        kw.update(ns_master=binding.MASTER_FP32, ns_form=NS_AUTO)
+    print(f"grouped case {n}: alpha {alpha} steps {steps} {kw} groups {shapes}", flush=True)
+    wl = workloads.Workload(f"gfuzz{n}", "test", tuple(workloads.Group(f"g{i}", r, c, b, ax)
+                                                       for i, (r, c, b, ax) in enumerate(shapes)), (alpha,))
+    stacks = [workloads.make_group(wl, gi, hip_device) for gi in range(ngroups)]
+    solo = [tuple(t.clone() for t in st) for st in stacks]
+    m0 = 0
+    for (W, M, G), (_, _, b, ax) in zip(solo, shapes):
+        binding.dion2_step_ex(W, M, G, alpha, 0.95, 0.02, steps, ax, rand_matrix0=m0, **kw)
+        m0 += b
+    binding.dion2_step_groups([(W, M, G, ax) for (W, M, G), (_, _, _, ax) in zip(stacks, shapes)], alpha,
+                              0.95, 0.02, steps, **kw)
+    torch.cuda.synchronize()
+    for gi, ((W, M, _), (Ws, Ms, _)) in enumerate(zip(stacks, solo)):
+        assert torch.equal(M, Ms), f"group {gi}: momentum"
+        assert torch.equal(W.view(torch.int16), Ws.view(torch.int16)), f"group {gi}: weights"
+    m0 = 0
+    for gi, (r, c, b, ax) in enumerate(shapes):
+        W, M, G = workloads.make_group(wl, gi, hip_device, count=1)
+        rand = (kw["rand_seed"], kw["rand_step"], m0) if "rand_seed" in kw else None
+        res = run_gpu(W, M, G, alpha, steps, ax, form=kw["ns_form"], rand=rand,
+                      master=kw.get("ns_master", binding.MASTER_BF16), norms=rand is None)
+        assert torch.equal(res["W"][0].view(torch.int16), solo[gi][0][0].cpu().view(torch.int16))
+        check_matrix(res, 0, alpha, steps, ax, rand=rand, ns_tol=NS_TOL)
+        m0 += b
