@@ -50,9 +50,10 @@ def draw(n):
     rand = (int(rng.integers(0, 2**63)), int(rng.integers(0, 2**40)), int(rng.integers(0, 1000))) \
         if rng.random() < 0.2 else None
     batch = int(rng.integers(1, 4)) if hi < 2500 else 1
+    scale = float(10.0 ** rng.integers(-20, 21)) if rng.random() < 0.15 else 1.0
     return dict(rows=rows, cols=cols, alpha=alpha, axis=axis, form=form, steps=steps, coeffs=coeffs,
                 chain=chain, master=master, wdt=wdt, gdt=gdt, eps=eps, decay_all=decay_all, rand=rand,
-                batch=batch)
+                batch=batch, scale=scale)
 
 
 @pytest.mark.parametrize("n", range(max(CASES, 0)))
@@ -62,6 +63,7 @@ def test_random_call(hip_device, n):
     wl = one_group_workload(c["rows"], c["cols"], count=c["batch"], axis=c["axis"], w_dtype="f32",
                             name=f"fuzz{n}")
     W, M, G = workloads.make_group(wl, 0, hip_device)   # fp32 W and G, then each to its type
+    M, G = M * c["scale"], G * c["scale"]               # the state's magnitude, 1e-20 to 1e20
     W, G = W.to(TO[c["wdt"]]).contiguous(), G.to(TO[c["gdt"]]).contiguous()
     if direct_refused(W, M, G, c["alpha"], c["axis"], c["form"]):
         return   # DIRECT on one tile: refused, nothing run
@@ -115,3 +117,44 @@ def test_random_grouped_call(hip_device, n):
         assert torch.equal(res["W"][0].view(torch.int16), solo[gi][0][0].cpu().view(torch.int16))
         check_matrix(res, 0, alpha, steps, ax, rand=rand, ns_tol=NS_TOL)
         m0 += b
+
+
+@pytest.mark.parametrize("n", range(max(CASES // 10, 0)))
+def test_random_call_entry_points(hip_device, n):
+    """One randomly drawn bf16 call through every same-shape entry point:
+    dion2_step_ex with the library workspace, with a caller workspace of
+    exactly dion2_workspace_size_ex bytes, dion2_step_noalloc (when the
+    scratch holds the plan), dion2_step_batched (pointer tables) and
+    dion2_step_strided -- bitwise the same W and M."""
+    rng = np.random.default_rng([2512, 16928, 11, n])
+    rows, cols = int(rng.integers(1, 600)), int(rng.integers(1, 600))
+    batch = int(rng.integers(1, 5))
+    alpha = float(rng.choice([0.05, 0.25, 0.5, 1.0]))
+    axis = int(rng.choice([AXIS_AUTO, AXIS_ROWS, AXIS_COLS]))
+    print(f"entry points case {n}: {batch} x {rows} x {cols}, alpha {alpha}, axis {axis}", flush=True)
+    wl = one_group_workload(rows, cols, count=batch, axis=axis, name=f"ep{n}")
+    W, M, G = workloads.make_group(wl, 0, hip_device)
+    outs = {}
+    for name in ("ex", "workspace", "noalloc", "batched", "strided"):
+        Wc, Mc = W.clone(), M.clone()
+        if name == "ex":
+            binding.dion2_step_ex(Wc, Mc, G, alpha, 0.95, 0.02, 5, axis)
+        elif name == "workspace":
+            need = binding.dion2_workspace_size_ex(batch, rows, cols, alpha, axis, 5)
+            ws = torch.empty(need, dtype=torch.uint8, device=hip_device)
+            binding.dion2_step_ex(Wc, Mc, G, alpha, 0.95, 0.02, 5, axis, workspace=ws)
+        elif name == "noalloc":
+            if binding.dion2_workspace_size_ex(batch, rows, cols, alpha, axis, 5) > binding.NOALLOC_SCRATCH_BYTES:
+                continue
+            binding.dion2_step_noalloc(Wc, Mc, G, alpha, 0.95, 0.02, 5, axis)
+        elif name == "batched":   # one allocation per matrix (the tables take 16-byte aligned pointers)
+            Ws, Ms, Gs = ([t[i].clone() for i in range(batch)] for t in (Wc, Mc, G))
+            binding.dion2_step_batched(Ws, Ms, Gs, alpha, 0.95, 0.02, 5, axis)
+            torch.cuda.synchronize()
+            Wc, Mc = torch.stack(Ws), torch.stack(Ms)
+        else:
+            binding.dion2_step_strided(Wc, Mc, G, alpha, 0.95, 0.02, 5, axis)
+        torch.cuda.synchronize()
+        outs[name] = (Wc.view(torch.int16).cpu(), Mc.cpu())
+    for name, (Wn, Mn) in outs.items():
+        assert torch.equal(Wn, outs["ex"][0]) and torch.equal(Mn, outs["ex"][1]), name
