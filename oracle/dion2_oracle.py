@@ -208,7 +208,10 @@ def newton_schulz(X, steps, coeffs=None, eps=DEFAULT_EPS):
     tall = X.shape[0] > X.shape[1]
     if tall:
         X = X.T
-    X = X / (np.linalg.norm(X) + eps)
+    # a zero X with eps = 0 leaves the normalisation 0 / 0; it is taken at its
+    # limit as eps -> 0+, where X / (||X||_F + eps) = 0, so O = 0
+    d = np.linalg.norm(X) + eps
+    X = X / d if d > 0 else X
     for t in range(steps):
         a, b, c = coeffs[t]
         A = X @ X.T

@@ -373,7 +373,8 @@ __global__ __launch_bounds__(kThreads) void colpass_scale(ColpassArgs a) {
     if (threadIdx.x == 0) {
         double t = 0.0;
         for (int w = 0; w < kThreads / 64; ++w) t += red[w];
-        a.scale[b] = 1.0 / (sqrt(t) + a.eps);
+        const double d = sqrt(t) + a.eps;   // zero X with eps = 0: scale 0, X stays 0
+        a.scale[b] = d > 0.0 ? 1.0 / d : 0.0;
     }
 }
 

@@ -183,7 +183,10 @@ __global__ __launch_bounds__(kThreads) void select_topk(SelectArgs a) {
     if (threadIdx.x == 0) {
         double f = 0.0;
         for (int w = 0; w < kWaves; ++w) f += red[w];
-        if (sq) a.scale[b] = 1.0 / (sqrt(f) + a.eps);
+        if (sq) {   // a zero X with eps = 0: scale 0 (X / (||X||_F + eps) -> 0 as eps -> 0+)
+            const double d = sqrt(f) + a.eps;
+            a.scale[b] = d > 0.0 ? 1.0 / d : 0.0;
+        }
         if (rank) rank[a.d_sel] = a.k;
     }
 }

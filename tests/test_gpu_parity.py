@@ -850,6 +850,29 @@ def test_zero_state_selects_first_lines(hip_device):
         assert not torch.any(res["O"][b])
 
 
+@pytest.mark.parametrize("rows,cols,alpha,kw", [
+    (200, 328, 0.25, {}),                                     # GRAM, one tile
+    (200, 328, 0.75, dict(form=NS_DIRECT)),                   # DIRECT, s = 150
+    (328, 200, 0.25, dict(rand=(5, 7, 0))),                   # Random rule, columns: the single column pass
+    (200, 328, 0.25, dict(master=binding.MASTER_FP32)),       # X's lo halves too
+], ids=["gram", "direct", "random-columns", "fp32-master"])
+def test_zero_matrix_with_eps_zero(hip_device, rows, cols, alpha, kw):
+    """With ns_eps = 0 a zero compact matrix leaves X / (||X||_F + eps) at
+    0 / 0; it is taken at its limit as eps -> 0+, which is 0: O = 0 and W
+    unchanged, no NaN, while the other matrix of the batch steps as usual."""
+    wl = one_group_workload(rows, cols, count=2, name=f"zeps{rows}")
+    W, M, G = workloads.make_group(wl, 0, hip_device)
+    M[0] = 0.0
+    G[0] = 0.0
+    rand = kw.get("rand")
+    res = run_gpu(W, M, G, alpha, eps=0.0, norms=rand is None, **kw)
+    assert torch.all(torch.isfinite(res["O"])) and not torch.any(res["O"][0])
+    assert torch.equal(res["W"][0].view(torch.int16), res["W0"][0].view(torch.int16))
+    for b in range(2):
+        check_matrix(res, b, alpha, eps=0.0, rand=rand,
+                     ns_tol=MASTER_TOL if kw.get("master") == binding.MASTER_FP32 else NS_TOL)
+
+
 @FORMS
 def test_exact_ties_go_to_lower_index(hip_device, form):
     wl = one_group_workload(640, 768, name="ties")

@@ -217,6 +217,13 @@ def test_ns_equivariance():
 
 def test_ns_zero_matrix_gives_zero():
     assert not np.any(oracle.newton_schulz(np.zeros((4, 9)), 5))
+    # with eps = 0 too: X / (||X||_F + eps) -> 0 as eps -> 0+ for X = 0, so no NaN
+    out = oracle.newton_schulz(np.zeros((4, 9)), 5, eps=0.0)
+    assert np.all(np.isfinite(out)) and not np.any(out)
+    # and the step: W unchanged, M decayed on the first k lines (all tied)
+    M = np.zeros((6, 8))
+    res = oracle.dion2_step(np.ones((6, 8)), M, np.zeros_like(M), alpha=0.5, eps=0.0)
+    assert np.array_equal(res["W"], np.ones((6, 8))) and not np.any(res["O"])
 
 
 # --------------------------------------- paper identities: eq. (3), eq. (4)
