@@ -1,9 +1,18 @@
 """Builds libdion2.so (the HIP kernels and the C ABI) for gfx950, in-tree.
 
-    python -m paper_2512_16928_amd.build [--jobs N] [--verbose]
+    python -m paper_2512_16928_amd.build [--jobs N] [--verbose] [--sanitize-host]
 
 Every source is compiled with hipcc for gfx950 only; the shared library is
 written next to this file, where the Python binding loads it from.
+
+--sanitize-host builds a copy whose host code (validation, planning,
+workspace layout, launch set-up) carries AddressSanitizer and
+UndefinedBehaviorSanitizer checks, the device code unchanged, into
+_build/san/libdion2.so. The CPU tests run against it with
+
+    ASAN_OPTIONS=detect_leaks=0 \
+    LD_PRELOAD=$(clang -print-file-name=libclang_rt.asan-x86_64.so) \
+    python -m pytest tests -m "not gpu" --dion2-lib _build/san/libdion2.so
 """
 from __future__ import annotations
 
@@ -49,29 +58,42 @@ def _run(cmd, verbose):
     return r
 
 
-def build(jobs: int = 8, verbose: bool = False) -> str:
-    os.makedirs(BUILD, exist_ok=True)
+# host code only: each -fsanitize= goes to the host compilation
+SAN_FLAGS = ["-Xarch_host", "-fsanitize=address", "-Xarch_host", "-fsanitize=undefined",
+             "-Xarch_host", "-fno-sanitize-recover=undefined", "-Xarch_host", "-fno-omit-frame-pointer"]
+SAN_LIB = os.path.join(BUILD, "san", "libdion2.so")
+
+
+def build(jobs: int = 8, verbose: bool = False, sanitize_host: bool = False) -> str:
+    out_dir = os.path.dirname(SAN_LIB) if sanitize_host else BUILD
+    lib = SAN_LIB if sanitize_host else LIB
+    extra = SAN_FLAGS if sanitize_host else []
+    os.makedirs(out_dir, exist_ok=True)
     cc = hipcc()
     objs = []
     cmds = []
     for src in SOURCES:
-        obj = os.path.join(BUILD, os.path.splitext(src)[0] + ".o")
+        obj = os.path.join(out_dir, os.path.splitext(src)[0] + ".o")
         objs.append(obj)
-        cmds.append([cc, *FLAGS, "-c", os.path.join(CSRC, src), "-o", obj])
+        cmds.append([cc, *FLAGS, *extra, "-c", os.path.join(CSRC, src), "-o", obj])
     with ThreadPoolExecutor(max_workers=max(1, min(jobs, len(cmds)))) as ex:
         list(ex.map(lambda c: _run(c, verbose), cmds))
-    tmp = LIB + ".tmp"
-    _run([cc, f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", tmp, *objs], verbose)
-    os.replace(tmp, LIB)
-    return LIB
+    tmp = lib + ".tmp"
+    link_extra = ["-shared-libsan", "-Xarch_host", "-fsanitize=address", "-Xarch_host",
+                  "-fsanitize=undefined"] if sanitize_host else []
+    _run([cc, f"--offload-arch={ARCH}", "-shared", "-fPIC", *link_extra, "-o", tmp, *objs], verbose)
+    os.replace(tmp, lib)
+    return lib
 
 
 def main(argv=None):
     ap = argparse.ArgumentParser(description=__doc__)
     ap.add_argument("--jobs", type=int, default=8)
     ap.add_argument("--verbose", action="store_true")
+    ap.add_argument("--sanitize-host", action="store_true",
+                    help="host code with AddressSanitizer and UBSan, into _build/san/libdion2.so")
     args = ap.parse_args(argv)
-    print(build(args.jobs, args.verbose))
+    print(build(args.jobs, args.verbose, args.sanitize_host))
 
 
 if __name__ == "__main__":

@@ -8,9 +8,18 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 
+def pytest_addoption(parser):
+    parser.addoption("--dion2-lib", default=None,
+                     help="load this build of libdion2.so (e.g. the host-sanitized one) instead of the package's")
+
+
 def pytest_configure(config):
     config.addinivalue_line(
         "markers", "gpu: needs an MI355X (gfx950) HIP device; parity tests proper")
+    path = config.getoption("--dion2-lib")
+    if path:
+        from paper_2512_16928_amd import binding
+        binding.load(os.path.abspath(path))
 
 
 @pytest.fixture(scope="session")
