@@ -122,7 +122,8 @@ def test_random_grouped_call(hip_device, n):
         kw.update(ns_coeffs=[STEP_COEFFS[int(i)] for i in rng.integers(0, len(STEP_COEFFS), steps)])
     if rng.random() < 0.15:
         kw.update(ns_eps=float(rng.choice([0.0, 1e-3])))
-    print(f"grouped case {n}: alpha {alpha} steps {steps} {kw} groups {shapes}", flush=True)
+    gs = int(rng.choice([0, 0, 1, 2, 3, 4, 8]))   # internal streams the groups may spread over
+    print(f"grouped case {n} (group_streams {gs}): alpha {alpha} steps {steps} {kw} groups {shapes}", flush=True)
     wl = workloads.Workload(f"gfuzz{n}", "test", tuple(workloads.Group(f"g{i}", r, c, b, ax)
                                                        for i, (r, c, b, ax) in enumerate(shapes)), (alpha,))
     stacks = [workloads.make_group(wl, gi, hip_device) for gi in range(ngroups)]
@@ -132,7 +133,7 @@ def test_random_grouped_call(hip_device, n):
         binding.dion2_step_ex(W, M, G, alpha, 0.95, 0.02, steps, ax, rand_matrix0=m0, **kw)
         m0 += b
     binding.dion2_step_groups([(W, M, G, ax) for (W, M, G), (_, _, _, ax) in zip(stacks, shapes)], alpha,
-                              0.95, 0.02, steps, **kw)
+                              0.95, 0.02, steps, group_streams=gs, **kw)
     torch.cuda.synchronize()
     for gi, ((W, M, _), (Ws, Ms, _)) in enumerate(zip(stacks, solo)):
         assert torch.equal(M, Ms), f"group {gi}: momentum"
