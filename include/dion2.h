@@ -95,7 +95,11 @@ extern "C" {
    steps on compact matrices of a few lines, and near-square ones drift past
    it after about 12. Longer schedules keep the bound when their steps after
    the fifth contract toward 1, e.g. cubic Newton-Schulz (1.5, -0.5, 0)
-   through ns_coeffs. */
+   through ns_coeffs, on compact matrices at least three times as long as
+   high (l >= 3 s). Past DION2_DIRECT_MAX_STEPS every call runs the GRAM
+   form, whose s x s matrices resolve singular values down to about 2^-8 of
+   the largest; near-square compact matrices have many below that, and a
+   schedule that lifts them toward 1 moves O by up to 7e-2 there. */
 #define DION2_MAX_NS_STEPS 16
 
 typedef enum dion2_status {
@@ -153,9 +157,10 @@ typedef enum dion2_ns_chain {
                              whose spectrum is dominated by a few directions
                              (kappa(Z)^2 beyond about 2^11); balanced wide
                              inputs stay within 2x of HILO. Taken only on
-                             wide compact matrices (l_pad >= 3 s_pad) with
-                             s > 64; elsewhere (near-square ones, where it
-                             measured up to 0.4 from the exact iteration,
+                             compact matrices at least four times as long
+                             as high (l >= 4 s) with s > 64; elsewhere
+                             (near-square ones, where it measured up to 0.4
+                             from the exact iteration, 2.3e-2 at l = 2.8 s,
                              and the one-launch chains of s <= 64) the chain
                              stays in HILO. With ns_coeffs that take the
                              chain's values beyond 2^40 the call fails with

@@ -671,13 +671,15 @@ bool fused_chain(int64_t s_k, const dion2_options& opt) {
     return !opt.ns_chain_per_product && s_k <= kSmallChainS;
 }
 // The fp16 chain (ns_chain F16) is taken only where it pays and holds: a
-// chain of launches on a wide compact matrix (l_pad >= 3 s_pad, the shapes
-// AUTO sends to GRAM for their width). On near-square ones the Gram matrix
+// chain of launches on a compact matrix at least four times as long as it
+// is high (l >= 4 s, real sides). On near-square ones the Gram matrix
 // squares a condition number that fp16's 11 bits cannot carry (randomly
-// drawn calls measured O 0.13-0.41 from the exact iteration), so the chain
-// stays in hi / lo there, as it does in LDS.
-bool f16_chain(const ChainFmt& fmt, bool fused, int64_t s_pad, int64_t l_pad) {
-    return fmt.f16 && !fused && l_pad >= 3 * s_pad;
+// drawn calls measured O 0.13-0.41 from the exact iteration), and with
+// l / s just under 3 (235 x 664, log-normal row scales) one reached 2.3e-2,
+// so the chain stays in hi / lo there, as it does in LDS.
+bool f16_chain(const ChainFmt& fmt, bool fused, const Plan& P) {
+    const int64_t s = P.z_is_L ? P.k : P.d_oth, l = P.z_is_L ? P.d_oth : P.k;
+    return fmt.f16 && !fused && l >= 4 * s;
 }
 ChainFmt chain_fmt_for(const ChainFmt& fmt, bool f16) {
     ChainFmt f = fmt;
@@ -856,7 +858,7 @@ hipError_t ns_gram(const Plan& P, const uint16_t* Z, const uint16_t* Zlo, uint16
                    int ns_steps, const dion2_options& opt, const ChainFmt& fmt, const FinalSpec& fin,
                    hipStream_t stream) {
     const bool fused = fused_chain(P.s_k, opt);
-    const ChainFmt cf = chain_fmt_for(fmt, f16_chain(fmt, fused, P.s_pad, P.l_pad));
+    const ChainFmt cf = chain_fmt_for(fmt, f16_chain(fmt, fused, P));
     hipError_t e = gram_a0(P, Z, Zlo, sq[SQ_AHI], sq[SQ_ALO], cf, stream);
     if (e != hipSuccess) return e;
     int cur = 0;
@@ -1385,7 +1387,7 @@ int groups_impl(const dion2_group* groups, int ngroups, float alpha, float mu, f
         const bool small = (int64_t)P.batch * st_tiles * (st_tiles + 1) / 2 < kChainShareTiles;
         if (P.gram && ns_steps > 0 && small) {
             const bool fused = fused_chain(P.s_k, opt);
-            const bool f16 = f16_chain(fmt, fused, P.s_pad, P.l_pad);
+            const bool f16 = f16_chain(fmt, fused, P);
             int c = 0;
             while (c < (int)chains.size() &&
                    (chains[c].s_pad != P.s_pad || chains[c].fused != fused || chains[c].f16 != f16))
