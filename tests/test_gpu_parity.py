@@ -277,6 +277,31 @@ def test_f16_chain_of_one_step_is_hilo(hip_device):
     assert torch.equal(W.view(torch.int16), W2.view(torch.int16)) and torch.equal(M, M2)
 
 
+@pytest.mark.parametrize("rows,cols,taken", [
+    (664, 235, False),   # s = 235, l = 664 = 2.8 s (padded 256 and 768: three times)
+    (1024, 256, True),   # s = 256, l = 1024 = 4 s
+    (256, 1100, True),   # columns of the transpose: s = 256, l = 1100
+])
+def test_f16_chain_needs_four_times_as_long(hip_device, rows, cols, taken):
+    """The fp16 chain is taken only where the compact matrix is at least four
+    times as long as it is high (real sides); elsewhere an fp16 request runs
+    the hi/lo chain, bitwise."""
+    wl = one_group_workload(rows, cols, name=f"f16w{rows}c{cols}")
+    W, M, G = workloads.make_group(wl, 0, hip_device)
+    k, ax = binding.dion2_plan_info(rows, cols, 1.0, AXIS_AUTO)
+    d_oth = cols if ax == AXIS_ROWS else rows
+    assert (max(k, d_oth) >= 4 * min(k, d_oth)) == taken
+    out = {}
+    for chain in (binding.CHAIN_HILO, binding.CHAIN_F16):
+        W1, M1 = W.clone(), M.clone()
+        binding.dion2_step_ex(W1, M1, G, 1.0, 0.95, 0.02, 5, ns_form=NS_GRAM, ns_chain=chain)
+        torch.cuda.synchronize()
+        out[chain] = W1.view(torch.int16).cpu()
+    assert torch.equal(out[binding.CHAIN_HILO], out[binding.CHAIN_F16]) != taken
+    res = run_gpu(W, M, G, 1.0, axis=AXIS_AUTO, form=NS_GRAM, chain=binding.CHAIN_F16)
+    check_matrix(res, 0, 1.0, axis=AXIS_AUTO)
+
+
 @pytest.mark.parametrize("wl_name,gi,first,alpha,ratio", [
     ("1b", 0, 9, 0.25, 2.0),          # 2048x2048: s = 512, l = 2048
     ("1b", 1, 4, 0.25, 2.0),          # 8192x2048, columns: s = 512, l = 8192
