@@ -17,10 +17,9 @@ import numpy as np
 import pytest
 import torch
 
-import oracle
 from paper_2512_16928_amd import binding, workloads
 from paper_2512_16928_amd.binding import AXIS_AUTO, AXIS_COLS, AXIS_ROWS, NS_AUTO, NS_DIRECT, NS_GRAM
-from test_gpu_parity import NS_TOL, check_matrix, direct_refused, one_group_workload, run_gpu
+from test_gpu_parity import NS_TOL, check_matrix, direct_refused, one_group_workload, rounding_floor, run_gpu
 
 CASES = int(os.environ.get("DION2_FUZZ", "0") or 0)
 FIRST = int(os.environ.get("DION2_FUZZ_FROM", "0") or 0)   # resume a sweep at case FIRST
@@ -89,26 +88,6 @@ def draw(n):
     return dict(rows=rows, cols=cols, alpha=alpha, axis=axis, form=form, steps=steps, coeffs=coeffs,
                 chain=chain, master=master, wdt=wdt, gdt=gdt, eps=eps, decay_all=decay_all, rand=rand,
                 batch=batch, scale=scale, zero=zero, dup=dup)
-
-
-def rounding_floor(M, G, b, alpha, steps, axis, coeffs=None, eps=1e-7, rand=None):
-    """The relative Frobenius distance between the exact iteration on matrix
-    b's compact X and the exact iteration on X / (||X||_F + eps) rounded once
-    to bf16: the least error a path that rounds its input to bf16 can show.
-    Compact matrices of a few lines with a small singular value, and long
-    quintic schedules, can put it near the 2e-2 bound by itself."""
-    M0, Gb = M[b].cpu().numpy(), G[b].float().cpu().numpy()
-    sel = dict(select="random", seed=rand[0], step=rand[1], matrix=rand[2] + b) if rand is not None else {}
-    eps = float(np.float32(eps))
-    out = oracle.dion2_step(np.zeros(M0.shape), M0, Gb, alpha, 0.95, 0.02, steps, axis, coeffs, eps=eps, **sel)
-    X = oracle.gather(oracle.momentum_accumulate(M0, Gb), out["K"], out["axis"])
-    nx = np.linalg.norm(X)
-    if steps == 0 or not np.isfinite(nx) or nx == 0.0:
-        return 0.0
-    Z = oracle.round_bf16(X / (nx + eps))
-    # eps chosen so that the oracle divides Z by exactly one, not by its norm
-    O = oracle.newton_schulz(Z, steps, coeffs, eps=1.0 - np.linalg.norm(Z))
-    return float(np.linalg.norm(O - out["O"]) / np.linalg.norm(out["O"]))
 
 
 def floor_too_high(floors):

@@ -32,6 +32,27 @@ def rel_fro(a, b):
     return float(np.linalg.norm(a - b) / max(np.linalg.norm(b), 1e-300))
 
 
+def rounding_floor(M, G, b, alpha, steps, axis, coeffs=None, eps=1e-7, rand=None):
+    """The relative Frobenius distance between the exact iteration on matrix
+    b's compact X and the exact iteration on X / (||X||_F + eps) rounded once
+    to bf16: the least error a path that rounds its input to bf16 can show.
+    Compact matrices of a few lines with a small singular value, long
+    quintic schedules and momentum of low rank plus a little noise can put
+    it near or past the 2e-2 bound by itself."""
+    M0, Gb = M[b].cpu().numpy(), G[b].float().cpu().numpy()
+    sel = dict(select="random", seed=rand[0], step=rand[1], matrix=rand[2] + b) if rand is not None else {}
+    eps = float(np.float32(eps))
+    out = oracle.dion2_step(np.zeros(M0.shape), M0, Gb, alpha, 0.95, 0.02, steps, axis, coeffs, eps=eps, **sel)
+    X = oracle.gather(oracle.momentum_accumulate(M0, Gb), out["K"], out["axis"])
+    nx = np.linalg.norm(X)
+    if steps == 0 or not np.isfinite(nx) or nx == 0.0:
+        return 0.0
+    Z = oracle.round_bf16(X / (nx + eps))
+    # eps chosen so that the oracle divides Z by exactly one, not by its norm
+    O = oracle.newton_schulz(Z, steps, coeffs, eps=1.0 - np.linalg.norm(Z))
+    return float(np.linalg.norm(O - out["O"]) / np.linalg.norm(out["O"]))
+
+
 FORMS = pytest.mark.parametrize("form", [NS_DIRECT, NS_GRAM], ids=["direct", "gram"])
 CHAINS = pytest.mark.parametrize("chain", [binding.CHAIN_HILO, binding.CHAIN_F16], ids=["hilo", "f16"])
 
@@ -421,6 +442,33 @@ def test_fp32_master_ragged(hip_device, rows, cols, alpha, axis, wdt):
     W, M, G = workloads.make_group(wl, 0, hip_device)
     res = run_gpu(W, M, G, alpha, axis=axis, master=binding.MASTER_FP32)
     check_matrix(res, 0, alpha, axis=axis, ns_tol=MASTER_TOL)
+
+
+@pytest.mark.parametrize("noise", [1e-2, 1e-3])
+def test_low_rank_plus_noise_takes_the_master(hip_device, noise):
+    """Momentum of rank 32 plus a little noise (512 x 2048, row selection at
+    alpha = 0.25, so X is 128 x 2048). The noise directions' singular values
+    are so far below the signal's that rounding X once to bf16 moves them:
+    the exact iteration on the rounded X already lies about 0.1 from the
+    exact result. The default path lands on that floor; the fp32 master,
+    which carries X as a hi/lo pair, holds the 2e-2 bound, at least ten
+    times closer."""
+    rng = np.random.default_rng(2512 + int(-math.log10(noise)))
+    rows, cols, r = 512, 2048, 32
+    base = rng.standard_normal((rows, r)) @ rng.standard_normal((r, cols))
+    Mh = 1e-3 * (base + noise * math.sqrt(r) * rng.standard_normal((rows, cols)))
+    M = torch.from_numpy(Mh.astype(np.float32))[None].to(hip_device)
+    G = torch.zeros((1, rows, cols), dtype=torch.bfloat16, device=hip_device)
+    W = (0.02 * torch.from_numpy(rng.standard_normal((1, rows, cols)).astype(np.float32))).to(torch.bfloat16)
+    W = W.to(hip_device)
+    floor = rounding_floor(M, G, 0, 0.25, 5, AXIS_ROWS)
+    assert floor > NS_TOL, floor
+    res = run_gpu(W.clone(), M.clone(), G, 0.25, axis=AXIS_ROWS)
+    err_bf16 = check_matrix(res, 0, 0.25, axis=AXIS_ROWS, ns_tol=1.5 * floor)
+    assert err_bf16 > 0.5 * floor, (err_bf16, floor)
+    res = run_gpu(W.clone(), M.clone(), G, 0.25, axis=AXIS_ROWS, master=binding.MASTER_FP32)
+    err_master = check_matrix(res, 0, 0.25, axis=AXIS_ROWS, ns_tol=NS_TOL)
+    assert err_master < 0.1 * err_bf16, (err_master, err_bf16)
 
 
 @pytest.mark.parametrize("gi,sample", [(0, 21), (1, 5), (2, 12)])
