@@ -99,7 +99,12 @@ extern "C" {
    high (l >= 3 s). Past DION2_DIRECT_MAX_STEPS every call runs the GRAM
    form, whose s x s matrices resolve singular values down to about 2^-8 of
    the largest; near-square compact matrices have many below that, and a
-   schedule that lifts them toward 1 moves O by up to 7e-2 there. */
+   schedule that lifts them toward 1 moves O by up to 7e-2 there. On compact
+   matrices of deficient or nearly deficient rank (low rank plus a little
+   noise, repeated lines) the GRAM form's rounding can leave A's eigenvalues
+   in the null space slightly negative, and every step multiplies those by
+   more than a^2 (a = 3.4445 for the quintic): from about 8 steps the chain
+   can diverge and O overflow. Such momentum stays at the paper's 5 steps. */
 #define DION2_MAX_NS_STEPS 16
 
 typedef enum dion2_status {

@@ -3,7 +3,8 @@ shapes from 1 to 700 lines a side (now and then up to 2500), selection
 fractions, axes, Newton-Schulz forms, step counts and coefficient schedules
 (past 5 steps, quintic steps then cubic ones: a convergent iteration),
 the fp16 chain, the fp32 master, W and G in either storage type, eps, the
-decay-all ablation, the Random rule and batches of one to three matrices --
+decay-all ablation, the Random rule, batches of one to three matrices and,
+now and then, momentum of low rank plus noise --
 each held to the same bar as the fixed parity cases: K exact, M and the l1
 norms bitwise, O within 2e-2 of the exact iteration whatever the options
 (the fp32 master's tighter 2e-3 holds on wide compact matrices, not on
@@ -11,6 +12,7 @@ near-square ones, where the Gram order squares the condition number), and W
 bitwise given O (or, for a forced DIRECT on a compact matrix of one tile,
 the call refused). And randomly drawn grouped calls, bitwise the per-group
 calls. The draws are seeded, so case n is the same call on every run."""
+import math
 import os
 
 import numpy as np
@@ -113,6 +115,20 @@ def test_random_call(hip_device, n):
                             name=f"fuzz{n}")
     W, M, G = workloads.make_group(wl, 0, hip_device)   # fp32 W and G, then each to its type
     M, G = M * c["scale"], G * c["scale"]               # the state's magnitude, 1e-20 to 1e20
+    lr = np.random.default_rng([2512, 16928, 13, n])     # its own stream: the other draws stay as they were
+    if lr.random() < 0.1:   # momentum of low rank plus noise (and a gradient at the noise's level)
+        # at most 5 steps: past them the GRAM chain's slightly negative
+        # eigenvalues in the near-null space grow by more than a^2 per step
+        # and the chain diverges (O overflowed at 8 to 16 steps)
+        if c["steps"] > 5:
+            c.update(steps=5)
+        rank, noise = int(lr.integers(1, 33)), float(10.0 ** lr.uniform(-4, -1))
+        print(f"case {n}: rank {rank} plus noise {noise:.1e}", flush=True)
+        for b in range(c["batch"]):
+            base = lr.standard_normal((c["rows"], rank)) @ lr.standard_normal((rank, c["cols"]))
+            Mb = 1e-3 * c["scale"] * (base + noise * math.sqrt(rank) * lr.standard_normal(base.shape))
+            M[b] = torch.from_numpy(Mb.astype(np.float32)).to(M.device)
+        G = G * noise
     if c["zero"]:
         M[0], G[0] = 0.0, 0.0
     if c["dup"]:
