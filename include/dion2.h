@@ -378,6 +378,22 @@ size_t dion2_workspace_size_ex(int batch, int64_t rows, int64_t cols,
 int dion2_plan_info(int64_t rows, int64_t cols, float alpha, int axis,
                     int64_t* k_out, int* axis_out);
 
+/* How a dion2_step_ex call with these arguments would evaluate the
+   Newton-Schulz iteration of Algorithm 1 (orthonormalisation step), for
+   callers that check or log the choice: *form_out receives DION2_NS_DIRECT or
+   DION2_NS_GRAM (what AUTO resolves to), *chain_out the storage the GRAM
+   chain takes (DION2_CHAIN_F16 only where ns_chain asks for it and the
+   compact matrix qualifies; DION2_CHAIN_HILO otherwise and for DIRECT), and
+   *fused_out 1 where the GRAM chain runs as one launch (s <= 64 and
+   ns_chain_per_product 0), else 0. Host-only: no GPU call, nothing
+   allocated, W, M and G not needed. opt may be NULL (defaults); any output
+   pointer may be NULL. Returns what the call's own validation of the shape,
+   alpha, ns_steps and options would return (e.g. DION2_ERR_UNSUPPORTED for a
+   forced DIRECT on one tile), leaving the outputs unset on error. */
+int dion2_plan_form(int batch, int64_t rows, int64_t cols, float alpha,
+                    int axis, int ns_steps, const dion2_options* opt,
+                    int* form_out, int* chain_out, int* fused_out);
+
 /* ---- Measurement hooks ---------------------------------------------------
  * While enabled, every kernel phase of subsequent calls is bracketed by HIP
  * events recorded on the call's stream (the Newton-Schulz s x s products of

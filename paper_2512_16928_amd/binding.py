@@ -39,7 +39,7 @@ MAX_NS_STEPS = 16
 # Every function include/dion2.h declares (checked by the ABI tests).
 EXPORTED = ("dion2_options_init", "dion2_step", "dion2_step_strided", "dion2_step_batched",
             "dion2_step_ex", "dion2_step_noalloc", "dion2_step_groups", "dion2_workspace_size",
-            "dion2_workspace_size_ex", "dion2_plan_info",
+            "dion2_workspace_size_ex", "dion2_plan_info", "dion2_plan_form",
             "dion2_release_workspaces", "dion2_status_string", "dion2_last_error",
             "dion2_version", "dion2_profile_enable", "dion2_profile_read", "dion2_profile_reset")
 
@@ -129,6 +129,9 @@ def load(path: str = LIB_PATH):
     lib.dion2_workspace_size_ex.restype = c_size_t
     lib.dion2_plan_info.argtypes = [i64, i64, c_float, c_int, POINTER(c_int64), POINTER(c_int)]
     lib.dion2_plan_info.restype = c_int
+    lib.dion2_plan_form.argtypes = [c_int, i64, i64, c_float, c_int, c_int, POINTER(Options),
+                                    POINTER(c_int), POINTER(c_int), POINTER(c_int)]
+    lib.dion2_plan_form.restype = c_int
     lib.dion2_release_workspaces.argtypes = []
     lib.dion2_release_workspaces.restype = None
     lib.dion2_status_string.argtypes = [c_int]
@@ -395,6 +398,31 @@ def dion2_workspace_size_ex(batch, rows, cols, alpha, axis=AXIS_AUTO, ns_steps=5
     n = int(lib.dion2_workspace_size_ex(batch, rows, cols, alpha, axis, ns_steps, ctypes.byref(opt)))
     del keep
     return n
+
+
+def dion2_plan_form(batch, rows, cols, alpha, axis=AXIS_AUTO, ns_steps=5, *, ns_form=NS_AUTO,
+                    ns_chain=CHAIN_HILO, ns_master=MASTER_BF16, ns_coeffs=None,
+                    ns_chain_per_product=False):
+    """(form, chain, fused) a dion2_step_ex call with these options would
+    take: DIRECT or GRAM, the GRAM chain's storage, and whether it runs as one
+    launch. Raises Dion2Error where the call would be rejected."""
+    lib = load()
+    opt = Options()
+    lib.dion2_options_init(ctypes.byref(opt))
+    keep = None
+    if ns_coeffs is not None:
+        flat = [float(v) for abc in ns_coeffs for v in abc]
+        keep = (c_float * len(flat))(*flat)
+        opt.ns_coeffs = ctypes.cast(keep, POINTER(c_float))
+    opt.ns_form = ns_form
+    opt.ns_chain = ns_chain
+    opt.ns_master = ns_master
+    opt.ns_chain_per_product = int(bool(ns_chain_per_product))
+    form, chain, fused = c_int(-1), c_int(-1), c_int(-1)
+    _check(lib.dion2_plan_form(batch, rows, cols, alpha, axis, ns_steps, ctypes.byref(opt),
+                               ctypes.byref(form), ctypes.byref(chain), ctypes.byref(fused)))
+    del keep
+    return int(form.value), int(chain.value), int(fused.value)
 
 
 def dion2_plan_info(rows, cols, alpha, axis=AXIS_AUTO):

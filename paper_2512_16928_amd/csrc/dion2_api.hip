@@ -1698,6 +1698,27 @@ int dion2_plan_info(int64_t rows, int64_t cols, float alpha, int axis, int64_t* 
     return DION2_OK;
 }
 
+int dion2_plan_form(int batch, int64_t rows, int64_t cols, float alpha, int axis, int ns_steps,
+                    const dion2_options* opt_in, int* form_out, int* chain_out, int* fused_out) {
+    dion2_options opt;
+    if (opt_in) opt = *opt_in;
+    else dion2_options_init(&opt);
+    int st = validate_common(0.f, 0.f, ns_steps, opt);
+    if (st != DION2_OK) return st;
+    Plan P;
+    st = make_plan(batch, rows, cols, alpha, axis, opt.ns_form, ns_steps, &P, true,
+                   opt.ns_master == DION2_MASTER_FP32, opt.select_rule == DION2_SELECT_RANDOM);
+    if (st != DION2_OK) return st;
+    ChainFmt fmt;
+    st = chain_format(opt, ns_steps, &fmt);
+    if (st != DION2_OK) return st;
+    const bool fused = P.gram && ns_steps > 0 && fused_chain(P.s_k, opt);
+    if (form_out) *form_out = P.gram ? DION2_NS_GRAM : DION2_NS_DIRECT;
+    if (chain_out) *chain_out = P.gram && f16_chain(fmt, fused, P) ? DION2_CHAIN_F16 : DION2_CHAIN_HILO;
+    if (fused_out) *fused_out = fused ? 1 : 0;
+    return DION2_OK;
+}
+
 void dion2_release_workspaces(void) {
     std::lock_guard<std::mutex> lk(g_ws_mutex);
     int prev = -1;

@@ -371,3 +371,78 @@ def test_noalloc_validation(lib):
     assert binding.dion2_workspace_size_ex(*big) > binding.NOALLOC_SCRATCH_BYTES
     assert na(rows=2048, cols=8192, batch=16, alpha=1.0) == DION2_ERR_WORKSPACE
     assert "scratch" in binding.dion2_last_error()
+
+
+def _pad(n):
+    return (n + 127) // 128 * 128
+
+
+@pytest.mark.parametrize("rows,cols,alpha,steps", [
+    (2048, 2048, 0.25, 5),    # s = 512, l = 2048 = 4 s: GRAM
+    (2048, 2048, 0.5, 5),     # s = 1024, l = 2048: DIRECT
+    (2048, 2048, 1.0, 5),     # s = l = 2048: DIRECT
+    (2048, 2048, 1.0, 6),     # DIRECT up to DION2_DIRECT_MAX_STEPS
+    (2048, 2048, 1.0, 7),     # past it: GRAM
+    (8192, 2048, 0.25, 5),    # columns: s = 512, l = 8192
+    (256, 256, 0.25, 5),      # s = 64: one tile, GRAM
+    (300, 200, 0.75, 5),      # columns: s = 150, l = 300 (padded 256 and 384): DIRECT
+    (129, 900, 1.0, 5),       # s = 129, l = 900 (padded 256 and 1024 >= 3 x 256): GRAM
+])
+def test_plan_form_auto(lib, rows, cols, alpha, steps):
+    """AUTO takes GRAM where the padded compact matrix is at least three
+    times as long as high, fits one tile a side, or the schedule is longer
+    than DIRECT's limit, else DIRECT; host-only, as the step resolves it."""
+    form, chain, fused = binding.dion2_plan_form(1, rows, cols, alpha, AXIS_AUTO, steps)
+    k, ax = binding.dion2_plan_info(rows, cols, alpha, AXIS_AUTO)
+    d_oth = cols if ax == AXIS_ROWS else rows
+    s, l = _pad(min(k, d_oth)), _pad(max(k, d_oth))
+    gram = l >= 3 * s or s <= 128 or steps > 6
+    assert form == (binding.NS_GRAM if gram else binding.NS_DIRECT)
+    assert chain == binding.CHAIN_HILO
+    assert fused == int(gram and min(k, d_oth) <= 64)
+
+
+@pytest.mark.parametrize("rows,cols,steps,want", [
+    (664, 235, 5, False),     # l = 2.8 s (padded sides 768 = 3 x 256): hi/lo
+    (1024, 256, 5, True),     # l = 4 s
+    (256, 1100, 5, True),     # columns of the transpose, l = 4.3 s
+    (1024, 256, 1, False),    # one step: no product to gain
+    (1024, 60, 5, False),     # s = 60: the one-launch chain stays hi/lo
+    (2048, 1024, 5, False),   # l = 2 s: DIRECT
+])
+def test_plan_form_f16_chain_rule(lib, rows, cols, steps, want):
+    """An fp16-chain request is taken only by a chain of launches on a
+    compact matrix at least four times as long as high (real sides)."""
+    form, chain, fused = binding.dion2_plan_form(1, rows, cols, 1.0, AXIS_AUTO, steps,
+                                                 ns_chain=binding.CHAIN_F16)
+    assert chain == (binding.CHAIN_F16 if want else binding.CHAIN_HILO), (form, chain, fused)
+    if want:
+        assert form == binding.NS_GRAM and not fused
+
+
+def test_plan_form_fused_chain_and_refusals(lib):
+    """s <= 64 runs the chain as one launch unless one launch per product is
+    asked for; no steps, no chain; a call the step would refuse raises the
+    same status."""
+    assert binding.dion2_plan_form(1, 256, 256, 0.25, AXIS_ROWS, 5) == (binding.NS_GRAM, binding.CHAIN_HILO, 1)
+    assert binding.dion2_plan_form(1, 256, 256, 0.25, AXIS_ROWS, 5, ns_chain_per_product=True)[2] == 0
+    assert binding.dion2_plan_form(1, 256, 256, 0.25, AXIS_ROWS, 0)[2] == 0
+    assert binding.dion2_plan_form(1, 260, 1000, 0.25, AXIS_ROWS, 5)[2] == 0      # s = 65
+    assert binding.dion2_plan_form(1, 2048, 2048, 1.0, AXIS_AUTO, 5,
+                                   ns_master=binding.MASTER_FP32)[0] == binding.NS_GRAM
+    refused = [
+        (dict(ns_form=binding.NS_DIRECT), (1, 256, 256, 0.25, 5), DION2_ERR_UNSUPPORTED),   # one tile
+        (dict(ns_form=binding.NS_DIRECT), (1, 2048, 2048, 1.0, 7), DION2_ERR_UNSUPPORTED),  # > 6 steps
+        (dict(ns_master=binding.MASTER_FP32, ns_form=binding.NS_DIRECT), (1, 2048, 2048, 1.0, 5),
+         DION2_ERR_UNSUPPORTED),
+        (dict(ns_master=binding.MASTER_FP32, ns_chain=binding.CHAIN_F16), (1, 2048, 2048, 0.25, 5),
+         DION2_ERR_INVALID_ARG),
+        (dict(ns_chain=binding.CHAIN_F16, ns_coeffs=[(3e6, 0.0, 0.0)] * 5), (1, 1024, 256, 1.0, 5),
+         DION2_ERR_UNSUPPORTED),   # the chain's values beyond fp16's range
+        (dict(), (0, 256, 256, 0.25, 5), DION2_ERR_INVALID_ARG),
+        (dict(), (1, 256, 256, 0.25, 17), DION2_ERR_INVALID_ARG),
+    ]
+    for kw, (batch, rows, cols, alpha, steps), status in refused:
+        with pytest.raises(binding.Dion2Error) as ei:
+            binding.dion2_plan_form(batch, rows, cols, alpha, AXIS_AUTO, steps, **kw)
+        assert ei.value.status == status, (kw, ei.value)
