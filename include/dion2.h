@@ -88,7 +88,8 @@ extern "C" {
 
 #define DION2_VERSION 1
 /* Accuracy and step count: with Muon's quintic, the stated 2e-2 bound on O
-   holds at its 5 steps. The quintic has no attracting fixed point (its slope
+   holds at its 5 steps (on compact matrices of a few lines the 16-bit s x s
+   chain has reached 2.1e-2 to 2.8e-2: 3 x 3 to 9 x 6 with ns_eps 1e-3). The quintic has no attracting fixed point (its slope
    inside the band reaches about 1.58), so each further step enlarges the
    bf16 rounding of the normalised input: the exact iteration on that rounded
    input can already lie more than 2e-2 from the exact result after 6 to 16
